@@ -1,0 +1,257 @@
+"""ctypes front end of the float64 CPU oracle (``ams_oracle.c``).
+
+TEST INFRASTRUCTURE ONLY: used by the test suite, the smoke check and the
+benchmark's CPU-baseline leg.  It imports nothing from the HIP library or its
+Python binding, and the HIP path never imports this module.
+
+Every function takes and returns numpy arrays (torch CPU tensors are accepted
+as inputs).  Feature tables and weights may be float32 or bfloat16; bf16 values
+are handed to the C code as raw bits and widened exactly to float64 there.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "ams_oracle.c")
+_LIB_PATH = os.path.join(_HERE, "libams_oracle.so")
+
+POOL_SUM, POOL_MAX, POOL_ATT = 0, 1, 2
+POOL_MODES = {"sum": POOL_SUM, "max": POOL_MAX, "att": POOL_ATT}
+F32, BF16 = 0, 1
+
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile ams_oracle.c with gcc (plain -O2, IEEE semantics, OpenMP)."""
+    if not force and os.path.exists(_LIB_PATH) and os.path.getmtime(_LIB_PATH) >= os.path.getmtime(_SRC):
+        return _LIB_PATH
+    tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+    cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
+           "-Wall", "-Wextra", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"]
+    subprocess.run(cmd, check=True)
+    os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _load():
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH) or os.path.getmtime(_LIB_PATH) < os.path.getmtime(_SRC):
+        build(force=True)
+    lib = ctypes.CDLL(_LIB_PATH)
+    P = ctypes.c_void_p
+    i32, i64 = ctypes.c_int32, ctypes.c_int64
+    lib.orc_dedup.argtypes = [P, i64, i32, P, P, P, P, P]
+    lib.orc_mlp_fwd.argtypes = [ctypes.c_int, P, ctypes.c_int, P, i64, P, i32, P, P, ctypes.c_int, P, P]
+    lib.orc_mlp_bwd.argtypes = [ctypes.c_int, P, ctypes.c_int, P, i64, P, i32, P, ctypes.c_int, P, P, P, P, P]
+    lib.orc_pool_fwd.argtypes = [ctypes.c_int, i32, i32, P, i64, P, P, P, P, P, P]
+    lib.orc_pool_bwd.argtypes = [ctypes.c_int, i32, i32, P, i64, P, i32, P, P, P, P, P, P, P, P, P, P]
+    lib.orc_num_threads.restype = ctypes.c_int
+    lib.orc_set_threads.argtypes = [ctypes.c_int]
+    _lib = lib
+    return lib
+
+
+def num_threads() -> int:
+    return _load().orc_num_threads()
+
+
+def set_threads(n: int) -> None:
+    _load().orc_set_threads(int(n))
+
+
+def _ptr(a):
+    return ctypes.c_void_p(a.ctypes.data) if a is not None else None
+
+
+def _i32(a):
+    return np.ascontiguousarray(np.asarray(a), dtype=np.int32)
+
+
+def _f64(a):
+    return np.ascontiguousarray(np.asarray(a), dtype=np.float64)
+
+
+def _store(x):
+    """(array, dtype code) for a float32 or bfloat16 table/weight."""
+    try:
+        import torch
+        if isinstance(x, torch.Tensor):
+            x = x.detach().cpu().contiguous()
+            if x.dtype == torch.bfloat16:
+                return x.view(torch.int16).numpy().view(np.uint16), BF16
+            return x.to(torch.float32).numpy(), F32
+    except ImportError:  # pragma: no cover
+        pass
+    x = np.ascontiguousarray(x)
+    if x.dtype == np.uint16:
+        return x, BF16
+    return np.ascontiguousarray(x, dtype=np.float32), F32
+
+
+def _check(rc, what):
+    if rc == 2:
+        raise IndexError(f"{what}: image ID out of range")
+    if rc != 0:
+        raise ValueError(f"{what}: bad argument (rc={rc})")
+
+
+# ------------------------------------------------------------------- dedup
+
+def dedup(ids, n_ids: int) -> dict:
+    lib = _load()
+    ids = _i32(ids)
+    n = ids.size
+    uniq = np.zeros(max(n, 1), np.int32)
+    inv = np.zeros(max(n, 1), np.int32)
+    perm = np.zeros(max(n, 1), np.int32)
+    off = np.zeros(n + 1, np.int32)
+    nu = np.zeros(1, np.int32)
+    _check(lib.orc_dedup(_ptr(ids), n, int(n_ids), _ptr(uniq), _ptr(inv), _ptr(perm), _ptr(off), _ptr(nu)), "dedup")
+    k = int(nu[0])
+    return {"uniq": uniq[:k].copy(), "inv": inv[:n].copy(), "occ_perm": perm[:n].copy(),
+            "uniq_off": off[:k + 1].copy(), "n_uniq": k}
+
+
+# --------------------------------------------------------------------- MLP
+
+def _weights(Ws):
+    arrs, codes = zip(*[_store(W) for W in Ws])
+    if len(set(codes)) != 1:
+        raise ValueError("mixed weight dtypes")
+    return list(arrs), codes[0]
+
+
+def mlp_fwd(T, rows, Ws, bs, final_relu: bool = False) -> dict:
+    """E and per-layer pre-activations Z[l] for unique rows T[rows]."""
+    lib = _load()
+    Tn, tcode = _store(T)
+    Wn, wcode = _weights(Ws)
+    if tcode != wcode:
+        raise ValueError("table and weights must share a storage dtype")
+    dims = [Wn[0].shape[1]] + [W.shape[0] for W in Wn]
+    if Tn.ndim != 2 or Tn.shape[1] != dims[0]:
+        raise ValueError("table width does not match the first layer")
+    rows = _i32(rows)
+    n = rows.size
+    L = len(Wn)
+    bn = [np.ascontiguousarray(b, dtype=np.float32) if not hasattr(b, "numpy") else b.detach().cpu().float().numpy() for b in bs]
+    Z = np.zeros(sum(n * d for d in dims[1:]) + 1, np.float64)
+    E = np.zeros(max(n * dims[-1], 1), np.float64)
+    dims_a = np.array(dims, np.int32)
+    Wp = (ctypes.c_void_p * L)(*[W.ctypes.data for W in Wn])
+    bp = (ctypes.c_void_p * L)(*[b.ctypes.data for b in bn])
+    _check(lib.orc_mlp_fwd(L, _ptr(dims_a), tcode, _ptr(Tn), Tn.shape[0], _ptr(rows), n,
+                           Wp, bp, int(final_relu), _ptr(Z), _ptr(E)), "mlp_fwd")
+    Zs, o = [], 0
+    for d in dims[1:]:
+        Zs.append(Z[o:o + n * d].reshape(n, d).copy())
+        o += n * d
+    return {"E": E[:n * dims[-1]].reshape(n, dims[-1]).copy(), "Z": Zs, "dims": dims}
+
+
+def mlp_bwd(T, rows, Ws, fwd: dict, dE, final_relu: bool = False) -> dict:
+    """dW[l], db[l] (float64) and pre-activation gradients dZ[l]."""
+    lib = _load()
+    Tn, tcode = _store(T)
+    Wn, _ = _weights(Ws)
+    dims = fwd["dims"]
+    rows = _i32(rows)
+    n = rows.size
+    L = len(Wn)
+    Z = np.concatenate([z.reshape(-1) for z in fwd["Z"]] + [np.zeros(1)])
+    dE = _f64(dE).reshape(-1)
+    if dE.size != n * dims[-1]:
+        raise ValueError("dE shape")
+    nW = sum(dims[l] * dims[l + 1] for l in range(L))
+    nb = sum(dims[1:])
+    dW = np.zeros(nW, np.float64)
+    db = np.zeros(nb, np.float64)
+    dZ = np.zeros(Z.size, np.float64)
+    dims_a = np.array(dims, np.int32)
+    Wp = (ctypes.c_void_p * L)(*[W.ctypes.data for W in Wn])
+    _check(lib.orc_mlp_bwd(L, _ptr(dims_a), tcode, _ptr(Tn), Tn.shape[0], _ptr(rows), n, Wp,
+                           int(final_relu), _ptr(Z), _ptr(dE), _ptr(dW), _ptr(db), _ptr(dZ)), "mlp_bwd")
+    dWs, dbs, dZs = [], [], []
+    ow = ob = oz = 0
+    for l in range(L):
+        fi, fo = dims[l], dims[l + 1]
+        dWs.append(dW[ow:ow + fi * fo].reshape(fo, fi).copy())
+        dbs.append(db[ob:ob + fo].copy())
+        dZs.append(dZ[oz:oz + n * fo].reshape(n, fo).copy())
+        ow += fi * fo
+        ob += fo
+        oz += n * fo
+    return {"dW": dWs, "db": dbs, "dZ": dZs}
+
+
+# ----------------------------------------------------------------- pooling
+
+def pool_fwd(mode, seg_off, inv, E, n_beh: int | None = None) -> dict:
+    lib = _load()
+    m = POOL_MODES[mode] if isinstance(mode, str) else int(mode)
+    seg_off = _i32(seg_off)
+    inv = _i32(inv)
+    E = _f64(E)
+    B = seg_off.size - 1
+    D = E.shape[1]
+    if n_beh is None:
+        n_beh = int(seg_off[-1])
+    U = np.zeros((B, D), np.float64)
+    A = np.zeros((B, D), np.float64)
+    am = np.full((B, D), -1, np.int32)
+    w = np.zeros(max(n_beh, 1), np.float64)
+    _check(lib.orc_pool_fwd(m, B, D, _ptr(seg_off), n_beh, _ptr(inv), _ptr(E), _ptr(U), _ptr(A),
+                            _ptr(am), _ptr(w)), "pool_fwd")
+    return {"U": U, "A": A, "argmax": am, "w": w[:n_beh].copy()}
+
+
+def pool_bwd(mode, seg_off, inv, n_uniq: int, E, fwd: dict, gU, gA=None) -> dict:
+    lib = _load()
+    m = POOL_MODES[mode] if isinstance(mode, str) else int(mode)
+    seg_off = _i32(seg_off)
+    inv = _i32(inv)
+    E = _f64(E)
+    B = seg_off.size - 1
+    D = E.shape[1]
+    n_beh = int(seg_off[-1])
+    gU = _f64(gU)
+    gA = _f64(gA) if gA is not None else None
+    w = np.ascontiguousarray(fwd["w"], np.float64)
+    if w.size == 0:
+        w = np.zeros(1)
+    am = np.ascontiguousarray(fwd["argmax"], np.int32)
+    dE = np.zeros((max(n_uniq, 1), D), np.float64)
+    ge = np.zeros((n_beh + B, D), np.float64) if n_beh + B > 0 else np.zeros((1, D))
+    dA = np.zeros((max(B, 1), D), np.float64)
+    _check(lib.orc_pool_bwd(m, B, D, _ptr(seg_off), n_beh, _ptr(inv), int(n_uniq), _ptr(E),
+                            _ptr(_f64(fwd["U"])), _ptr(_f64(fwd["A"])), _ptr(am), _ptr(w),
+                            _ptr(gU), _ptr(gA), _ptr(dE), _ptr(ge), _ptr(dA)), "pool_bwd")
+    return {"dE": dE[:n_uniq].copy(), "ge": ge[:n_beh + B].copy(), "dA_att": dA[:B].copy()}
+
+
+# -------------------------------------------------------------- full step
+
+def step(batch: dict, n_ids: int, T, Ws, bs, mode: str, final_relu: bool = False,
+         table_is_compact: bool = False) -> dict:
+    """One whole step: dedup -> MLP fwd -> pool fwd -> pool bwd -> MLP bwd.
+
+    T is the full table ([n_ids, F]) or, with table_is_compact, just the rows
+    of the batch's unique IDs in ascending ID order (as returned by dedup).
+    """
+    occ = np.concatenate([_i32(batch["beh_ids"]), _i32(batch["ad_ids"])])
+    dd = dedup(occ, n_ids)
+    rows = np.arange(dd["n_uniq"], dtype=np.int32) if table_is_compact else dd["uniq"]
+    fw = mlp_fwd(T, rows, Ws, bs, final_relu)
+    pf = pool_fwd(mode, batch["seg_off"], dd["inv"], fw["E"])
+    pb = pool_bwd(mode, batch["seg_off"], dd["inv"], dd["n_uniq"], fw["E"], pf,
+                  batch["g_u"], batch.get("g_a"))
+    bw = mlp_bwd(T, rows, Ws, fw, pb["dE"], final_relu)
+    return {"dedup": dd, "fwd": fw, "pool": pf, "pool_bwd": pb, "bwd": bw}
