@@ -1,0 +1,233 @@
+"""Benchmark of one AMS image-embedding training step on one MI355X.
+
+A step is the whole hot path on one batch already resident in HBM:
+ams_dedup -> ams_embed_fwd -> ams_pool_fwd -> ams_pool_bwd -> ams_embed_bwd,
+enqueued back to back on one stream.  Distinct seeded batches rotate so a batch
+is never replayed against its own warm cache.  Prints ONE JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--workload c1_f32] [--mode att]
+
+Throughput = behavior images embedded and pooled per second (fwd + bwd).
+The roofline entry covers the dominant call, the gather-fused embedding
+forward (4096-wide MFMA GEMM plus the small tail layers), timed with events on
+the stream it runs on.  The CPU baseline is the float64 oracle, timed on this
+host on one whole batch of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "behavior images embedded+pooled/sec (fwd+bwd), % HBM peak and % MFMA peak"
+PEAK_HBM = 8.0e12
+PEAK_MFMA = {"f32": 157.3e12, "bf16": 2.5e15}
+
+
+def flops_per_unique(dims):
+    F, H = dims[0], dims[1]
+    fwd = 2 * sum(a * b for a, b in zip(dims[:-1], dims[1:]))
+    # backward: every weight gradient, plus dH of every layer but the first
+    bwd = 2 * sum(a * b for a, b in zip(dims[:-1], dims[1:])) + 2 * sum(
+        a * b for a, b in zip(dims[1:-1], dims[2:]))
+    return fwd, bwd, 2 * F * H
+
+
+def traffic_from_profile(kernel_src_hash: str, unique_count: float):
+    """HBM bytes per launch from committed PMC summaries, if they were taken
+    on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", "embed_fwd_c1_f32_traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        d = json.load(open(path))
+    except Exception:
+        return None
+    if d.get("source_sha256") != kernel_src_hash:
+        return None
+    return d.get("hbm_bytes_per_launch")
+
+
+def src_hash():
+    h = hashlib.sha256()
+    for f in ("embed.hip", "ams_device.h"):
+        h.update(open(os.path.join(ROOT, "paper_1711_06505_amd", "csrc", f), "rb").read())
+    return h.hexdigest()
+
+
+def cpu_baseline(w, batch, mode):
+    import numpy as np
+
+    from oracle import oracle
+    from paper_1711_06505_amd import synth
+    Ws, bs = synth.make_weights(w)
+    occ = synth.occurrences(batch)
+    uniq = np.unique(occ)
+    T_u = synth.table_rows(w, uniq)
+    t0 = time.perf_counter()
+    oracle.step(batch, w.n_images, T_u, Ws, bs, mode, table_is_compact=True)
+    dt = time.perf_counter() - t0
+    n_beh = int(batch["seg_off"][-1])
+    return {"value": n_beh / dt, "unit": "behavior images/s", "cores": oracle.num_threads(),
+            "kind": "oracle",
+            "sample": f"one whole batch of the same workload ({w.batch} samples, {n_beh} behaviors), "
+                      f"float64 C oracle, {dt:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="c1_f32")
+    ap.add_argument("--mode", default=None)
+    ap.add_argument("--batches", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="instead of the step, run a plain device copy of this many MiB "
+                         "(calibrates the FETCH_SIZE / WRITE_SIZE counters)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    from paper_1711_06505_amd import ams, synth
+
+    if args.copy_probe_mib:
+        n = args.copy_probe_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes_read_per_launch": n * 4, "copy_probe_bytes_written_per_launch": n * 4,
+                          "launches": 3}))
+        return
+
+    w = synth.get(args.workload)
+    mode = args.mode or w.pools[-1]
+    torch.cuda.set_device(0)
+    ams.load()
+
+    # inputs, resident in HBM before timing starts
+    T = synth.table_full(w, device="cuda")
+    Ws, bs = synth.make_weights(w)
+    Wd = [x.cuda() for x in Ws]
+    bd = [x.cuda() for x in bs]
+    host_batches = [synth.make_batch(w, k=k) for k in range(args.batches)]
+    dev_batches = []
+    for hb in host_batches:
+        dev_batches.append({
+            "ids": torch.from_numpy(synth.occurrences(hb)).cuda(),
+            "seg_off": torch.from_numpy(hb["seg_off"]).cuda(),
+            "dU": torch.from_numpy(hb["g_u"]).cuda(),
+            "dA": torch.from_numpy(hb["g_a"]).cuda(),
+            "n_beh": int(hb["seg_off"][-1]),
+        })
+    n_beh_max = max(b["n_beh"] for b in dev_batches)
+    step = ams.Step(w.dims, w.dtype, mode, w.batch, n_beh_max)
+    step.alloc_workspace(w.n_images)
+    stream = torch.cuda.current_stream()
+
+    def one(b, ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        step.dedup(b["ids"], w.n_images)
+        if ev is not None:
+            ev[1].record(stream)
+        step.embed_fwd(T, Wd, bd)
+        if ev is not None:
+            ev[2].record(stream)
+        step.pool_fwd(b["seg_off"], b["n_beh"])
+        step.pool_bwd(b["seg_off"], b["n_beh"], b["dU"], b["dA"])
+        if ev is not None:
+            ev[3].record(stream)
+        step.embed_bwd(T, Wd)
+        if ev is not None:
+            ev[4].record(stream)
+
+    # unique counts per batch (read once, outside the timed region)
+    n_uniq = []
+    for b in dev_batches:
+        one(b)
+        torch.cuda.synchronize()
+        assert int(step.dev_status.item()) == 0
+        n_uniq.append(int(step.n_uniq.item()))
+    for s in range(args.warmup):
+        one(dev_batches[s % len(dev_batches)])
+    torch.cuda.synchronize()
+
+    # timed region: K whole steps back to back
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record(stream)
+    for s in range(args.steps):
+        one(dev_batches[s % len(dev_batches)])
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_total = t_start.elapsed_time(t_end)
+    ms_step = ms_total / args.steps
+    order = [s % len(dev_batches) for s in range(args.steps)]
+    beh_total = sum(dev_batches[i]["n_beh"] for i in order)
+    uniq_total = sum(n_uniq[i] for i in order)
+    value = beh_total / (ms_total * 1e-3)
+
+    # per-call durations: a second pass with events between the calls
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+    for s in range(args.steps):
+        one(dev_batches[s % len(dev_batches)], evs[s])
+    torch.cuda.synchronize()
+    per = {"dedup": 0.0, "embed_fwd": 0.0, "pool_fwd_bwd": 0.0, "embed_bwd": 0.0}
+    for e in evs:
+        per["dedup"] += e[0].elapsed_time(e[1])
+        per["embed_fwd"] += e[1].elapsed_time(e[2])
+        per["pool_fwd_bwd"] += e[2].elapsed_time(e[3])
+        per["embed_bwd"] += e[3].elapsed_time(e[4])
+    per = {k: v / args.steps for k, v in per.items()}
+
+    fwd_f, bwd_f, l1_f = flops_per_unique(w.dims)
+    u_mean = uniq_total / args.steps
+    esz = 2 if w.dtype == "bf16" else 4
+    step_flops = u_mean * (fwd_f + bwd_f)
+    step_bytes = u_mean * 2 * w.in_dim * esz           # the two reads of every unique feature row
+    peak = PEAK_MFMA[w.dtype]
+    ach = u_mean * fwd_f / (per["embed_fwd"] * 1e-3)
+    traffic = traffic_from_profile(src_hash(), u_mean)
+    roof = {"kernel": "ams_embed_fwd (l1_fwd gather+MFMA GEMM, tail layers)",
+            "bound": "mfma", "achieved": ach / 1e12, "peak": peak / 1e12, "unit": "TFLOP/s",
+            "frac": ach / peak, "traffic": traffic,
+            "algorithmic_flops_per_launch": u_mean * fwd_f, "avg_launch_ms": per["embed_fwd"]}
+
+    out = {
+        "metric": METRIC, "value": value, "unit": "behavior images/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": f"{w.name}: B={w.batch}, lengths {w.lengths}, ids {w.ids} over "
+                               f"{w.n_images} images, table {w.n_images}x{w.in_dim} {w.dtype}, "
+                               f"MLP {'-'.join(map(str, w.dims))}, pooling {mode}, fwd+bwd",
+                   "batch": w.batch, "behaviors_per_step": beh_total / args.steps,
+                   "unique_per_step": u_mean, "dedup_ratio": (beh_total + w.batch * args.steps) / uniq_total,
+                   "rotating_batches": len(dev_batches)},
+        "step_mfma_frac": step_flops / (ms_step * 1e-3) / peak,
+        "step_hbm_frac": step_bytes / (ms_step * 1e-3) / PEAK_HBM,
+        "per_call_ms": per,
+        "roofline": roof,
+        "cpu_baseline": None,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(w, host_batches[0], mode)
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

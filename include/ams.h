@@ -1,0 +1,215 @@
+/*
+ * ams.h -- C ABI of libams, the MI355X (gfx950) hot path of one Advanced Model
+ * Server training step for the shared image-embedding model.
+ *
+ * One step (section 4.2; Algorithm 1, SERVEREMBED and SERVERUPDATE) is:
+ *   ams_dedup      the batch's image IDs (behavior images, then ad images) are
+ *                  reduced to one sorted set, so each image is fetched and
+ *                  embedded once and its gradients are merged at one place;
+ *   ams_embed_fwd  each unique image's feature row is gathered from the table
+ *                  and run through the trainable embedding model, a fully
+ *                  connected net 4096-256-64-12 (section 5.1), ReLU between
+ *                  layers;
+ *   ams_pool_fwd   each sample's behavior embeddings are aggregated into one
+ *                  user vector by sum, max, or attentive pooling with the ad
+ *                  image embedding as query (section 5.2);
+ *   ams_pool_bwd   the upstream gradients are taken back through the pooling
+ *                  and summed per unique image (Algorithm 1: gradients for the
+ *                  same image are collected by the same server);
+ *   ams_embed_bwd  the merged embedding gradients are back-propagated through
+ *                  the embedding model into its weight and bias gradients
+ *                  (Algorithm 1, SERVERUPDATE).  The feature table is fixed
+ *                  (the frozen VGG16 part, section 5.1): no gradient flows to it.
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * Pointers:   every array argument is a DEVICE pointer unless marked "host".
+ *             The caller allocates and frees all memory, including workspaces;
+ *             the library allocates no device memory and keeps no mutable
+ *             global state, so calls on different streams with different
+ *             workspaces may run concurrently.
+ * Streams:    `stream` is a hipStream_t passed as void* (NULL = the null
+ *             stream).  Calls only enqueue work and never synchronize.
+ * Counts:     the number of unique images n_u is produced on the device by
+ *             ams_dedup (*n_uniq) and read there by later calls; they take a
+ *             host upper bound `n_uniq_cap` (n_u <= n_uniq_cap <= n_occ) that
+ *             sizes grids and buffers.  Work past n_u is skipped and outputs
+ *             past n_u are left unspecified.
+ * Layouts:    row-major.  Feature table T is [n_rows x dims[0]].  Weights
+ *             W_l are [dims[l+1] x dims[l]] (out x in), biases float32
+ *             [dims[l+1]].  E, U, A, dE, dU, dA have row stride D = dims[last]
+ *             floats.  IDs are int32.
+ * Precision:  AMS_F32: T and W float32, float32 MFMA with float32 accumulation.
+ *             AMS_BF16: T and W bfloat16; bf16 MFMA with float32 accumulation
+ *             for the 4096-wide layer and its weight gradient (whose
+ *             activation-gradient operand is rounded to bf16); all other
+ *             arithmetic, E, U, A, the attention weights and every gradient
+ *             are float32.  H1_save is bf16 in this mode, float32 otherwise.
+ * Determinism: every output is bitwise reproducible for identical inputs on
+ *             the same device (fixed reduction orders, no float atomics).
+ * Errors:     calls return an ams_status.  Problems visible on the host are
+ *             reported before anything is enqueued.  An image ID outside its
+ *             range can only be seen on the device: ams_dedup then writes
+ *             AMS_ERR_ID_RANGE into *dev_status (read it after a sync) and
+ *             its outputs are unspecified; later calls never read outside T.
+ *             Nothing is printed and no call aborts.
+ */
+#ifndef AMS_H
+#define AMS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    AMS_OK = 0,
+    AMS_ERR_NULL = 1,       /* a required pointer is NULL */
+    AMS_ERR_SIZE = 2,       /* a size is negative, too large, or inconsistent */
+    AMS_ERR_DTYPE = 3,      /* unknown storage dtype */
+    AMS_ERR_DIMS = 4,       /* layer widths this build does not support */
+    AMS_ERR_WORKSPACE = 5,  /* ws_bytes below the matching *_workspace() size */
+    AMS_ERR_HIP = 6,        /* a HIP launch or runtime call failed */
+    AMS_ERR_ID_RANGE = 7,   /* (device) an image ID is outside [0, n_ids) */
+    AMS_ERR_MODE = 8        /* unknown pooling mode */
+} ams_status;
+
+typedef enum { AMS_F32 = 0, AMS_BF16 = 1 } ams_dtype;
+
+/* Aggregators of section 5.2.  ATT: w_j = softmax_j(e_j . a_i) over the
+ * sample's behaviors, u_i = sum_j w_j e_j, with a_i the ad image embedding. */
+typedef enum { AMS_POOL_SUM = 0, AMS_POOL_MAX = 1, AMS_POOL_ATT = 2 } ams_pool;
+
+/* Shape of the trainable embedding model (section 5.1: 4096-256-64-12).
+ * Supported: n_layers 2 or 3; dims[0] a multiple of 64 in [64, 65536];
+ * dims[1] a multiple of 64 in [64, 256]; hidden dims[2] (3 layers) in [1, 64];
+ * output D = dims[n_layers] in [1, 32].  final_relu = 1 puts a ReLU after the
+ * last layer as well (default 0: the embedding is the last layer's affine
+ * output). */
+typedef struct {
+    int32_t n_layers;
+    int32_t dims[4];
+    int32_t dtype;       /* ams_dtype of T and the weights */
+    int32_t final_relu;
+} ams_mlp;
+
+/* Text of a status code (host, static storage, never NULL). */
+const char *ams_status_str(ams_status s);
+
+/* Library version and the GPU architecture it was built for (host). */
+const char *ams_build_info(void);
+
+/* ------------------------------------------------------------- dedup ----
+ * Requests for the same image are processed once (section 4.2).
+ *
+ * ids[n_occ]        the batch's image IDs: all behavior IDs (sample by sample)
+ *                   followed by the B ad IDs.  0 <= ids[k] < n_ids.
+ * uniq[n_occ]       out: the n_u distinct IDs in ascending order.
+ * inv[n_occ]        out: uniq[inv[k]] == ids[k].
+ * occ_perm[n_occ]   out: occurrence indices sorted by (ID, k): a stable sort.
+ * uniq_off[n_occ+1] out: occurrences of uniq[u] are
+ *                   occ_perm[uniq_off[u] .. uniq_off[u+1]); uniq_off[n_u] = n_occ.
+ * n_uniq[1]         out: n_u.
+ * dev_status[1]     out: AMS_OK, or AMS_ERR_ID_RANGE if some ID is out of range.
+ * ws, ws_bytes      workspace of at least ams_dedup_workspace(n_occ, n_ids) bytes.
+ * n_occ == 0 is valid (n_u = 0).  Host errors: NULL, SIZE (n_occ < 0,
+ * n_occ > 2^31 - 2, n_ids < 1), WORKSPACE.  Outputs are bit-exact: they are
+ * the unique canonical answer. */
+size_t ams_dedup_workspace(int64_t n_occ, int32_t n_ids);
+ams_status ams_dedup(const int32_t *ids, int64_t n_occ, int32_t n_ids,
+                     int32_t *uniq, int32_t *inv, int32_t *occ_perm,
+                     int32_t *uniq_off, int32_t *n_uniq, int32_t *dev_status,
+                     void *ws, size_t ws_bytes, void *stream);
+
+/* --------------------------------------------------------- embed fwd ----
+ * SERVEREMBED (Algorithm 1): e = E(I) for every unique image.
+ *
+ * mlp (host)        model shape and dtype (see ams_mlp).
+ * T                 feature table [n_rows x dims[0]], dtype mlp->dtype.
+ * uniq, n_uniq      from ams_dedup; rows uniq[0..n_u) of T are embedded.
+ *                   A row index outside [0, n_rows) reads as a zero row.
+ * W1,b1,W2,b2,W3,b3 weights (dtype) and float32 biases; W3/b3 ignored when
+ *                   n_layers == 2.
+ * H1_save           out, optional: post-ReLU first hidden layer [cap x dims[1]]
+ *                   (bf16 in AMS_BF16 mode, float32 otherwise).  Needed by
+ *                   ams_embed_bwd; pass NULL for inference only.
+ * H2_save           out, optional (3 layers): post-ReLU second hidden layer
+ *                   [cap x dims[2]] float32.
+ * E                 out: embeddings [cap x D] float32 (row u for uniq[u]).
+ * ws                at least ams_embed_workspace(mlp, cap) bytes. */
+size_t ams_embed_workspace(const ams_mlp *mlp, int32_t n_uniq_cap);
+ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n_rows,
+                         const int32_t *uniq, const int32_t *n_uniq,
+                         int32_t n_uniq_cap,
+                         const void *W1, const float *b1,
+                         const void *W2, const float *b2,
+                         const void *W3, const float *b3,
+                         void *H1_save, float *H2_save, float *E,
+                         void *ws, size_t ws_bytes, void *stream);
+
+/* --------------------------------------------------------- embed bwd ----
+ * SERVERUPDATE (Algorithm 1): delta_E = grad E(I) . delta_e.
+ *
+ * Inputs as in ams_embed_fwd plus the forward's H1_save/H2_save, its E
+ * (read only when final_relu = 1, for the last layer's ReLU mask; may be NULL
+ * otherwise) and dE [cap x D] float32 (from ams_pool_bwd).  Outputs, all float32 and fully
+ * overwritten (not accumulated): dW1 [dims[1] x dims[0]], db1, dW2, db2,
+ * dW3, db3 (dW3/db3 ignored when n_layers == 2).  Every gradient is a sum over
+ * the n_u unique images in a fixed order.  ReLU'(0) = 0. */
+ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n_rows,
+                         const int32_t *uniq, const int32_t *n_uniq,
+                         int32_t n_uniq_cap,
+                         const void *W1, const void *W2, const void *W3,
+                         const void *H1_save, const float *H2_save,
+                         const float *E_fwd, const float *dE,
+                         float *dW1, float *db1, float *dW2, float *db2,
+                         float *dW3, float *db3,
+                         void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------- pool fwd ----
+ * User behavior image aggregator (section 5.2).
+ *
+ * mode              ams_pool.
+ * B, D              samples and embedding width (1 <= D <= 32).
+ * seg_off[B+1]      CSR offsets of the behavior lists: sample i owns
+ *                   occurrences j in [seg_off[i], seg_off[i+1]);
+ *                   seg_off[0] = 0, seg_off[B] = n_beh, non-decreasing.
+ * inv[n_beh+B]      from ams_dedup (behaviors then ads).
+ * E [n_u x D]       embeddings from ams_embed_fwd.
+ * U [B x D]         out: pooled user vectors (empty segment -> 0).
+ * A [B x D]         out: the ad image embedding of each sample, E[inv[n_beh+i]].
+ * saved             out: MAX: int32 [B x D] index j of the first maximum
+ *                   (-1 for an empty segment); ATT: float32 [n_beh] attention
+ *                   weights; SUM: unused (may be NULL). */
+ams_status ams_pool_fwd(int32_t mode, int32_t B, int32_t D,
+                        const int32_t *seg_off, int64_t n_beh,
+                        const int32_t *inv, const float *E,
+                        float *U, float *A, void *saved, void *stream);
+
+/* ---------------------------------------------------------- pool bwd ----
+ * Loss gradient through the aggregator, merged per unique image.
+ *
+ * dU [B x D]        upstream gradient of U; dA [B x D] of A (NULL = zero).
+ * occ_perm, uniq_off, n_uniq from ams_dedup; E, U, A, saved from the forward.
+ * dE [cap x D]      out: for each unique image, the sum over its occurrences
+ *                   (in ascending occurrence order) of the gradient w.r.t.
+ *                   that occurrence's embedding; fully overwritten for u < n_u.
+ * ws                at least ams_pool_workspace(mode, B, n_beh, D, cap) bytes. */
+size_t ams_pool_workspace(int32_t mode, int32_t B, int64_t n_beh, int32_t D,
+                          int32_t n_uniq_cap);
+ams_status ams_pool_bwd(int32_t mode, int32_t B, int32_t D,
+                        const int32_t *seg_off, int64_t n_beh,
+                        const int32_t *inv, const int32_t *occ_perm,
+                        const int32_t *uniq_off, const int32_t *n_uniq,
+                        int32_t n_uniq_cap,
+                        const float *E, const float *U, const float *A,
+                        const void *saved, const float *dU, const float *dA,
+                        float *dE, void *ws, size_t ws_bytes, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* AMS_H */

@@ -1,0 +1,261 @@
+"""Thin Python binding of libams (C ABI in include/ams.h).
+
+Each ``ams_*`` function here marshals torch tensors (device memory) and the
+current HIP stream into the C call of the same name and raises AmsError on a
+non-OK status.  No step of the method runs in Python: there is no fallback,
+and loading fails loudly when libams.so has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libams.so")
+
+AMS_F32, AMS_BF16 = 0, 1
+AMS_POOL_SUM, AMS_POOL_MAX, AMS_POOL_ATT = 0, 1, 2
+POOL = {"sum": AMS_POOL_SUM, "max": AMS_POOL_MAX, "att": AMS_POOL_ATT}
+STATUS = {0: "AMS_OK", 1: "AMS_ERR_NULL", 2: "AMS_ERR_SIZE", 3: "AMS_ERR_DTYPE", 4: "AMS_ERR_DIMS",
+          5: "AMS_ERR_WORKSPACE", 6: "AMS_ERR_HIP", 7: "AMS_ERR_ID_RANGE", 8: "AMS_ERR_MODE"}
+EXPORTS = ["ams_status_str", "ams_build_info", "ams_dedup_workspace", "ams_dedup",
+           "ams_embed_workspace", "ams_embed_fwd", "ams_embed_bwd", "ams_pool_fwd",
+           "ams_pool_workspace", "ams_pool_bwd"]
+
+
+class AmsError(RuntimeError):
+    def __init__(self, status: int, where: str):
+        self.status = status
+        super().__init__(f"{where}: {STATUS.get(status, status)} ({_text(status)})")
+
+
+class ams_mlp(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("dims", ctypes.c_int32 * 4),
+                ("dtype", ctypes.c_int32), ("final_relu", ctypes.c_int32)]
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libams.so (raises if it has not been built: there is no fallback)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing; build it with `python -m paper_1711_06505_amd.build`")
+    lib = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
+    M = ctypes.POINTER(ams_mlp)
+    lib.ams_status_str.restype = ctypes.c_char_p
+    lib.ams_status_str.argtypes = [ctypes.c_int]
+    lib.ams_build_info.restype = ctypes.c_char_p
+    lib.ams_dedup_workspace.restype = sz
+    lib.ams_dedup_workspace.argtypes = [i64, i32]
+    lib.ams_dedup.restype = ctypes.c_int
+    lib.ams_dedup.argtypes = [P, i64, i32, P, P, P, P, P, P, P, sz, P]
+    lib.ams_embed_workspace.restype = sz
+    lib.ams_embed_workspace.argtypes = [M, i32]
+    lib.ams_embed_fwd.restype = ctypes.c_int
+    lib.ams_embed_fwd.argtypes = [M, P, i64, P, P, i32, P, P, P, P, P, P, P, P, P, P, sz, P]
+    lib.ams_embed_bwd.restype = ctypes.c_int
+    lib.ams_embed_bwd.argtypes = [M, P, i64, P, P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]
+    lib.ams_pool_fwd.restype = ctypes.c_int
+    lib.ams_pool_fwd.argtypes = [i32, i32, i32, P, i64, P, P, P, P, P, P]
+    lib.ams_pool_workspace.restype = sz
+    lib.ams_pool_workspace.argtypes = [i32, i32, i64, i32, i32]
+    lib.ams_pool_bwd.restype = ctypes.c_int
+    lib.ams_pool_bwd.argtypes = [i32, i32, i32, P, i64, P, P, P, P, i32, P, P, P, P, P, P, P, P, sz, P]
+    _lib = lib
+    return lib
+
+
+def _text(status: int) -> str:
+    try:
+        return load().ams_status_str(status).decode()
+    except Exception:  # pragma: no cover
+        return "?"
+
+
+def _check(rc: int, where: str):
+    if rc != 0:
+        raise AmsError(rc, where)
+
+
+def _p(t):
+    """Raw pointer of a tensor (None -> NULL)."""
+    if t is None:
+        return None
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def make_mlp(dims, dtype: str = "f32", final_relu: bool = False) -> ams_mlp:
+    m = ams_mlp()
+    m.n_layers = len(dims) - 1
+    for i, d in enumerate(dims):
+        m.dims[i] = int(d)
+    m.dtype = AMS_BF16 if dtype == "bf16" else AMS_F32
+    m.final_relu = int(final_relu)
+    return m
+
+
+# ------------------------------------------------------------- C calls
+
+def ams_dedup_workspace(n_occ: int, n_ids: int) -> int:
+    return load().ams_dedup_workspace(int(n_occ), int(n_ids))
+
+
+def ams_dedup(ids, n_ids, uniq, inv, occ_perm, uniq_off, n_uniq, dev_status, ws, stream=None):
+    _check(load().ams_dedup(_p(ids), ids.numel(), int(n_ids), _p(uniq), _p(inv), _p(occ_perm),
+                            _p(uniq_off), _p(n_uniq), _p(dev_status), _p(ws),
+                            ws.numel() * ws.element_size() if ws is not None else 0,
+                            _stream(stream)), "ams_dedup")
+
+
+def ams_embed_workspace(mlp: ams_mlp, n_uniq_cap: int) -> int:
+    return load().ams_embed_workspace(ctypes.byref(mlp), int(n_uniq_cap))
+
+
+def ams_embed_fwd(mlp, T, uniq, n_uniq, n_uniq_cap, W, b, H1_save, H2_save, E, ws, stream=None):
+    W3 = W[2] if len(W) > 2 else None
+    b3 = b[2] if len(b) > 2 else None
+    _check(load().ams_embed_fwd(ctypes.byref(mlp), _p(T), T.shape[0], _p(uniq), _p(n_uniq),
+                                int(n_uniq_cap), _p(W[0]), _p(b[0]), _p(W[1]), _p(b[1]), _p(W3), _p(b3),
+                                _p(H1_save), _p(H2_save), _p(E), _p(ws),
+                                ws.numel() * ws.element_size() if ws is not None else 0,
+                                _stream(stream)), "ams_embed_fwd")
+
+
+def ams_embed_bwd(mlp, T, uniq, n_uniq, n_uniq_cap, W, H1_save, H2_save, E_fwd, dE, dW, db, ws,
+                  stream=None):
+    W3 = W[2] if len(W) > 2 else None
+    dW3 = dW[2] if len(dW) > 2 else None
+    db3 = db[2] if len(db) > 2 else None
+    _check(load().ams_embed_bwd(ctypes.byref(mlp), _p(T), T.shape[0], _p(uniq), _p(n_uniq),
+                                int(n_uniq_cap), _p(W[0]), _p(W[1]), _p(W3), _p(H1_save), _p(H2_save),
+                                _p(E_fwd), _p(dE), _p(dW[0]), _p(db[0]), _p(dW[1]), _p(db[1]), _p(dW3),
+                                _p(db3), _p(ws), ws.numel() * ws.element_size(), _stream(stream)),
+           "ams_embed_bwd")
+
+
+def ams_pool_fwd(mode, seg_off, n_beh, inv, E, U, A, saved, stream=None):
+    m = POOL[mode] if isinstance(mode, str) else int(mode)
+    B = seg_off.numel() - 1
+    _check(load().ams_pool_fwd(m, B, U.shape[1], _p(seg_off), int(n_beh), _p(inv), _p(E), _p(U), _p(A),
+                               _p(saved), _stream(stream)), "ams_pool_fwd")
+
+
+def ams_pool_workspace(mode, B: int, n_beh: int, D: int, n_uniq_cap: int) -> int:
+    m = POOL[mode] if isinstance(mode, str) else int(mode)
+    return load().ams_pool_workspace(m, int(B), int(n_beh), int(D), int(n_uniq_cap))
+
+
+def ams_pool_bwd(mode, seg_off, n_beh, inv, occ_perm, uniq_off, n_uniq, n_uniq_cap, E, U, A, saved,
+                 dU, dA, dE, ws, stream=None):
+    m = POOL[mode] if isinstance(mode, str) else int(mode)
+    B = seg_off.numel() - 1
+    _check(load().ams_pool_bwd(m, B, U.shape[1], _p(seg_off), int(n_beh), _p(inv), _p(occ_perm),
+                               _p(uniq_off), _p(n_uniq), int(n_uniq_cap), _p(E), _p(U), _p(A), _p(saved),
+                               _p(dU), _p(dA), _p(dE), _p(ws),
+                               ws.numel() * ws.element_size() if ws is not None else 0,
+                               _stream(stream)), "ams_pool_bwd")
+
+
+# ------------------------------------------------------- one whole step
+
+class Step:
+    """Buffers for one training step of the embedding hot path, and the five
+    calls in order on one stream: dedup -> embed fwd -> pool fwd -> pool bwd
+    -> embed bwd.  Inputs (table, weights, batch) stay caller-owned tensors.
+
+    Buffers are sized for up to B samples and n_beh_max behaviors; `cap`
+    (default B + n_beh_max) bounds the unique count used for grids, since n_u
+    is only known on the device.
+    """
+
+    def __init__(self, dims, dtype: str, mode: str, B: int, n_beh_max: int, final_relu: bool = False,
+                 device="cuda", cap: int | None = None):
+        self.mlp = make_mlp(dims, dtype, final_relu)
+        self.dims = tuple(dims)
+        self.dtype = dtype
+        self.mode = mode
+        self.B, self.n_beh = int(B), int(n_beh_max)
+        self.n_occ = self.n_beh + self.B
+        self.cap = self.n_occ if cap is None else int(cap)
+        D, H = dims[-1], dims[1]
+        dev = torch.device(device)
+        i32, f32 = torch.int32, torch.float32
+        n = max(self.n_occ, 1)
+        self.uniq = torch.empty(n, dtype=i32, device=dev)
+        self.inv = torch.empty(n, dtype=i32, device=dev)
+        self.occ_perm = torch.empty(n, dtype=i32, device=dev)
+        self.uniq_off = torch.empty(n + 1, dtype=i32, device=dev)
+        self.n_uniq = torch.zeros(1, dtype=i32, device=dev)
+        self.dev_status = torch.zeros(1, dtype=i32, device=dev)
+        cap1 = max(self.cap, 1)
+        h1_dtype = torch.bfloat16 if dtype == "bf16" else f32
+        self.H1 = torch.empty((cap1, H), dtype=h1_dtype, device=dev)
+        self.H2 = torch.empty((cap1, dims[2]), dtype=f32, device=dev) if len(dims) == 4 else None
+        self.E = torch.empty((cap1, D), dtype=f32, device=dev)
+        self.U = torch.empty((max(self.B, 1), D), dtype=f32, device=dev)
+        self.A = torch.empty((max(self.B, 1), D), dtype=f32, device=dev)
+        if mode == "max":
+            self.saved = torch.empty((max(self.B, 1), D), dtype=i32, device=dev)
+        elif mode == "att":
+            self.saved = torch.empty(max(self.n_beh, 1), dtype=f32, device=dev)
+        else:
+            self.saved = None
+        self.dE = torch.empty((cap1, D), dtype=f32, device=dev)
+        self.dW = [torch.empty((o, i), dtype=f32, device=dev) for i, o in zip(dims[:-1], dims[1:])]
+        self.db = [torch.empty((o,), dtype=f32, device=dev) for o in dims[1:]]
+        self.ws = None
+        self.n_ids = None
+
+    def alloc_workspace(self, n_ids: int):
+        """One workspace shared by the five calls (they run in order on one stream)."""
+        need = max(ams_dedup_workspace(self.n_occ, n_ids),
+                   ams_embed_workspace(self.mlp, self.cap),
+                   ams_pool_workspace(self.mode, self.B, self.n_beh, self.dims[-1], self.cap), 256)
+        if self.ws is None or self.ws.numel() < need:
+            self.ws = torch.empty(need, dtype=torch.uint8, device=self.uniq.device)
+        self.n_ids = int(n_ids)
+
+    def dedup(self, ids, n_ids, stream=None):
+        if self.ws is None or self.n_ids != int(n_ids):
+            self.alloc_workspace(n_ids)
+        ams_dedup(ids, n_ids, self.uniq, self.inv, self.occ_perm, self.uniq_off, self.n_uniq,
+                  self.dev_status, self.ws, stream)
+
+    def embed_fwd(self, T, W, b, stream=None):
+        ams_embed_fwd(self.mlp, T, self.uniq, self.n_uniq, self.cap, W, b, self.H1, self.H2, self.E,
+                      self.ws, stream)
+
+    def pool_fwd(self, seg_off, n_beh, stream=None):
+        ams_pool_fwd(self.mode, seg_off, n_beh, self.inv, self.E, self.U, self.A, self.saved, stream)
+
+    def pool_bwd(self, seg_off, n_beh, dU, dA, stream=None):
+        ams_pool_bwd(self.mode, seg_off, n_beh, self.inv, self.occ_perm, self.uniq_off, self.n_uniq,
+                     self.cap, self.E, self.U, self.A, self.saved, dU, dA, self.dE, self.ws, stream)
+
+    def embed_bwd(self, T, W, stream=None):
+        ams_embed_bwd(self.mlp, T, self.uniq, self.n_uniq, self.cap, W, self.H1, self.H2, self.E,
+                      self.dE, self.dW, self.db, self.ws, stream)
+
+    def run(self, ids, n_ids, T, W, b, seg_off, dU, dA, stream=None):
+        """The whole step, enqueued on one stream with no host synchronisation."""
+        n_beh = ids.numel() - (seg_off.numel() - 1)
+        if n_beh > self.n_beh or seg_off.numel() - 1 > self.B:
+            raise ValueError("batch larger than the buffers of this Step")
+        self.dedup(ids, n_ids, stream)
+        self.embed_fwd(T, W, b, stream)
+        self.pool_fwd(seg_off, n_beh, stream)
+        self.pool_bwd(seg_off, n_beh, dU, dA, stream)
+        self.embed_bwd(T, W, stream)

@@ -1,0 +1,447 @@
+// pool.hip -- ams_pool_fwd / ams_pool_bwd: the user behavior image aggregator
+// of section 5.2 (sum, max, attentive pooling with the ad image embedding as
+// query) and its backward, merged per unique image as Algorithm 1 merges the
+// embedding gradients of one image at its server.
+//
+// Forward: one wave per sample; lanes stride over the sample's behaviors,
+// fetch E[inv[j]] (12 floats, L2 resident) and reduce across the wave in a
+// fixed butterfly order.  Attentive pooling makes three passes over its
+// segment: logits and their max, exp-weights and weighted sum, normalisation.
+//
+// Backward: (1) one wave per sample computes the per-sample terms of the
+// attention gradient and tags every behavior occurrence with its sample;
+// (2) one wave per chunk of 64 positions of the stable occurrence order
+// evaluates each occurrence's embedding gradient and sums runs of equal
+// unique image with a segmented lane scan -- runs wholly inside the chunk go
+// straight to dE, runs that cross a chunk edge leave a partial; (3) one wave
+// per chunk in which a crossing run starts adds that run's partials in chunk
+// order.  Fixed orders throughout: no float atomics, bitwise reproducible.
+#include "ams_device.h"
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / AMS_WAVE;
+
+template <int DM>
+__device__ __forceinline__ void load_row(const float *__restrict__ E, int row, int D, float (&e)[DM])
+{
+    const float *p = E + (size_t)row * D;
+#pragma unroll
+    for (int d = 0; d < DM; ++d) e[d] = d < D ? p[d] : 0.f;
+}
+
+template <int MODE, int DM>
+__global__ __launch_bounds__(kThreads) void pool_fwd_k(int B, int D, const int32_t *__restrict__ seg_off,
+                                                       int64_t n_beh, const int32_t *__restrict__ inv,
+                                                       const float *__restrict__ E, float *__restrict__ U,
+                                                       float *__restrict__ A, void *__restrict__ saved)
+{
+    const int lane = ams_lane();
+    const int i = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
+    if (i >= B) return;
+    const int j0 = seg_off[i], j1 = seg_off[i + 1];
+    const int ad_row = inv[n_beh + i];
+    if (lane < D) A[(size_t)i * D + lane] = E[(size_t)ad_row * D + lane];
+    float out[DM];
+    if (MODE == AMS_POOL_SUM) {
+        float acc[DM];
+#pragma unroll
+        for (int d = 0; d < DM; ++d) acc[d] = 0.f;
+        for (int j = j0 + lane; j < j1; j += AMS_WAVE) {
+            float e[DM];
+            load_row<DM>(E, inv[j], D, e);
+#pragma unroll
+            for (int d = 0; d < DM; ++d) acc[d] += e[d];
+        }
+#pragma unroll
+        for (int d = 0; d < DM; ++d) out[d] = ams_wave_sum(acc[d]);
+    } else if (MODE == AMS_POOL_MAX) {
+        float best[DM];
+        int bidx[DM];
+#pragma unroll
+        for (int d = 0; d < DM; ++d) {
+            best[d] = 0.f;
+            bidx[d] = -1;
+        }
+        for (int j = j0 + lane; j < j1; j += AMS_WAVE) {
+            float e[DM];
+            load_row<DM>(E, inv[j], D, e);
+#pragma unroll
+            for (int d = 0; d < DM; ++d)
+                if (bidx[d] < 0 || e[d] > best[d]) {
+                    best[d] = e[d];
+                    bidx[d] = j;
+                }
+        }
+        // first maximum over the segment: larger value wins, ties -> lower j
+#pragma unroll
+        for (int d = 0; d < DM; ++d) {
+            float v = best[d];
+            int x = bidx[d];
+#pragma unroll
+            for (int o = AMS_WAVE / 2; o > 0; o >>= 1) {
+                const float ov = __shfl_xor(v, o, AMS_WAVE);
+                const int ox = __shfl_xor(x, o, AMS_WAVE);
+                const bool take = ox >= 0 && (x < 0 || ov > v || (ov == v && ox < x));
+                if (take) {
+                    v = ov;
+                    x = ox;
+                }
+            }
+            out[d] = x < 0 ? 0.f : v;
+            if (lane == d && d < D) ((int32_t *)saved)[(size_t)i * D + d] = x;
+        }
+    } else {
+        float a[DM];
+        load_row<DM>(E, ad_row, D, a);
+        float *w = (float *)saved;
+        float m = -INFINITY;
+        for (int j = j0 + lane; j < j1; j += AMS_WAVE) {
+            float e[DM];
+            load_row<DM>(E, inv[j], D, e);
+            float s = 0.f;
+#pragma unroll
+            for (int d = 0; d < DM; ++d) s += e[d] * a[d];
+            w[j] = s;                                   // logit, rescaled below
+            m = fmaxf(m, s);
+        }
+        m = ams_wave_max(m);
+        float den = 0.f, acc[DM];
+#pragma unroll
+        for (int d = 0; d < DM; ++d) acc[d] = 0.f;
+        for (int j = j0 + lane; j < j1; j += AMS_WAVE) {
+            float e[DM];
+            load_row<DM>(E, inv[j], D, e);
+            const float p = expf(w[j] - m);
+            w[j] = p;
+            den += p;
+#pragma unroll
+            for (int d = 0; d < DM; ++d) acc[d] += p * e[d];
+        }
+        den = ams_wave_sum(den);
+        const float inv_den = j1 > j0 ? 1.f / den : 0.f;
+#pragma unroll
+        for (int d = 0; d < DM; ++d) out[d] = ams_wave_sum(acc[d]) * inv_den;
+        for (int j = j0 + lane; j < j1; j += AMS_WAVE) w[j] = w[j] * inv_den;
+    }
+    float mine = 0.f;
+#pragma unroll
+    for (int d = 0; d < DM; ++d)
+        if (lane == d) mine = out[d];
+    if (lane < D) U[(size_t)i * D + lane] = mine;
+}
+
+// (1) per sample: tag occurrences with their sample; attention terms
+// c_i = g_i . u_i and da_i = sum_j ds_j e_j, ds_j = w_j (g_i . e_j - c_i).
+template <int MODE, int DM>
+__global__ __launch_bounds__(kThreads) void pool_bwd_sample(int B, int D, const int32_t *__restrict__ seg_off,
+                                                            const int32_t *__restrict__ inv,
+                                                            const float *__restrict__ E,
+                                                            const float *__restrict__ U,
+                                                            const float *__restrict__ wsaved,
+                                                            const float *__restrict__ dU,
+                                                            int32_t *__restrict__ samp,
+                                                            float *__restrict__ cvec,
+                                                            float *__restrict__ da)
+{
+    const int lane = ams_lane();
+    const int i = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
+    if (i >= B) return;
+    const int j0 = seg_off[i], j1 = seg_off[i + 1];
+    for (int j = j0 + lane; j < j1; j += AMS_WAVE) samp[j] = i;
+    if (MODE != AMS_POOL_ATT) return;
+    float g[DM], u[DM];
+    load_row<DM>(dU, i, D, g);
+    load_row<DM>(U, i, D, u);
+    float c = 0.f;
+#pragma unroll
+    for (int d = 0; d < DM; ++d) c += g[d] * u[d];
+    float acc[DM];
+#pragma unroll
+    for (int d = 0; d < DM; ++d) acc[d] = 0.f;
+    for (int j = j0 + lane; j < j1; j += AMS_WAVE) {
+        float e[DM];
+        load_row<DM>(E, inv[j], D, e);
+        float dw = 0.f;
+#pragma unroll
+        for (int d = 0; d < DM; ++d) dw += g[d] * e[d];
+        const float ds = wsaved[j] * (dw - c);
+#pragma unroll
+        for (int d = 0; d < DM; ++d) acc[d] += ds * e[d];
+    }
+    float mine = 0.f;
+#pragma unroll
+    for (int d = 0; d < DM; ++d) {
+        const float v = ams_wave_sum(acc[d]);
+        if (lane == d) mine = v;
+    }
+    if (lane < D) da[(size_t)i * D + lane] = mine;
+    if (lane == 0) cvec[i] = c;
+}
+
+// (2) segmented sums over chunks of 64 positions of the stable occurrence order.
+template <int MODE, int DM>
+__global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int64_t n_beh, int n_occ,
+                                                         const int32_t *__restrict__ inv,
+                                                         const int32_t *__restrict__ occ_perm,
+                                                         const int32_t *__restrict__ uniq_off,
+                                                         const float *__restrict__ E,
+                                                         const float *__restrict__ A,
+                                                         const void *__restrict__ saved,
+                                                         const float *__restrict__ dU,
+                                                         const float *__restrict__ dA,
+                                                         const int32_t *__restrict__ samp,
+                                                         const float *__restrict__ cvec,
+                                                         const float *__restrict__ da, int nch,
+                                                         float *__restrict__ dE,
+                                                         float *__restrict__ head_part,
+                                                         float *__restrict__ tail_part,
+                                                         int32_t *__restrict__ cross)
+{
+    const int lane = ams_lane();
+    const int ch = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
+    if (ch >= nch) return;
+    const int c0 = ch * AMS_WAVE, c1 = c0 + AMS_WAVE;
+    const int p = c0 + lane;
+    const bool valid = p < n_occ;
+    int u = -1 - lane;       // distinct per invalid lane: never joins a run
+    float v[DM];
+#pragma unroll
+    for (int d = 0; d < DM; ++d) v[d] = 0.f;
+    if (valid) {
+        const int k = occ_perm[p];
+        u = inv[k];
+        if (k < n_beh) {
+            const int i = samp[k];
+            float g[DM];
+            load_row<DM>(dU, i, D, g);
+            if (MODE == AMS_POOL_SUM) {
+#pragma unroll
+                for (int d = 0; d < DM; ++d) v[d] = g[d];
+            } else if (MODE == AMS_POOL_MAX) {
+                const int32_t *am = (const int32_t *)saved + (size_t)i * D;
+#pragma unroll
+                for (int d = 0; d < DM; ++d) v[d] = (d < D && am[d] == k) ? g[d] : 0.f;
+            } else {
+                const float wk = ((const float *)saved)[k];
+                float e[DM], a[DM];
+                load_row<DM>(E, u, D, e);
+                load_row<DM>(A, i, D, a);
+                float dw = 0.f;
+#pragma unroll
+                for (int d = 0; d < DM; ++d) dw += g[d] * e[d];
+                const float ds = wk * (dw - cvec[i]);
+#pragma unroll
+                for (int d = 0; d < DM; ++d) v[d] = wk * g[d] + ds * a[d];
+            }
+        } else {
+            const int i = (int)(k - n_beh);
+            if (dA) load_row<DM>(dA, i, D, v);
+            if (MODE == AMS_POOL_ATT) {
+                float t[DM];
+                load_row<DM>(da, i, D, t);
+#pragma unroll
+                for (int d = 0; d < DM; ++d) v[d] += t[d];
+            }
+        }
+    }
+    // inclusive segmented scan over lanes (runs of equal u are contiguous)
+#pragma unroll
+    for (int o = 1; o < AMS_WAVE; o <<= 1) {
+        const int ou = __shfl_up(u, o, AMS_WAVE);
+        const bool join = lane >= o && ou == u;
+#pragma unroll
+        for (int d = 0; d < DM; ++d) {
+            const float ov = __shfl_up(v[d], o, AMS_WAVE);
+            if (join) v[d] += ov;
+        }
+    }
+    const int nu_next = __shfl_down(u, 1, AMS_WAVE);
+    const bool run_end = valid && (lane == AMS_WAVE - 1 || nu_next != u);
+    int cross_u = -1;
+    if (run_end) {
+        const int s = uniq_off[u], e = uniq_off[u + 1];
+        float *dst;
+        if (s < c0) {
+            dst = head_part + (size_t)ch * D;          // run began in an earlier chunk
+        } else if (e > c1) {
+            dst = tail_part + (size_t)ch * D;          // run starts here, continues later
+            cross_u = u;
+        } else {
+            dst = dE + (size_t)u * D;                   // whole run inside this chunk
+        }
+#pragma unroll
+        for (int d = 0; d < DM; ++d)
+            if (d < D) dst[d] = v[d];
+    }
+    // only lane 63 can end a run that continues past the chunk
+    const int cu = __shfl(cross_u, AMS_WAVE - 1, AMS_WAVE);
+    if (lane == 0) cross[ch] = cu;
+}
+
+// (3) a run that starts in chunk ch and crosses chunk edges: tail part of ch,
+// then the head parts of the following chunks up to the run's last chunk.
+template <int DM>
+__global__ __launch_bounds__(kThreads) void pool_bwd_fix(int D, int nch, const int32_t *__restrict__ uniq_off,
+                                                         const int32_t *__restrict__ cross,
+                                                         const float *__restrict__ head_part,
+                                                         const float *__restrict__ tail_part,
+                                                         float *__restrict__ dE)
+{
+    const int lane = ams_lane();
+    const int ch = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
+    if (ch >= nch) return;
+    const int u = cross[ch];
+    if (u < 0) return;
+    const int last = (uniq_off[u + 1] - 1) / AMS_WAVE;
+    float acc[DM];
+#pragma unroll
+    for (int d = 0; d < DM; ++d) acc[d] = 0.f;
+    for (int c = ch + 1 + lane; c <= last; c += AMS_WAVE) {
+        float h[DM];
+        load_row<DM>(head_part, c, D, h);
+#pragma unroll
+        for (int d = 0; d < DM; ++d) acc[d] += h[d];
+    }
+    float mine = 0.f;
+#pragma unroll
+    for (int d = 0; d < DM; ++d) {
+        const float s = ams_wave_sum(acc[d]);
+        if (lane == d) mine = s;
+    }
+    if (lane < D) dE[(size_t)u * D + lane] = tail_part[(size_t)ch * D + lane] + mine;
+}
+
+size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+struct PoolPlan {
+    size_t off_samp, off_c, off_da, off_head, off_tail, off_cross, total;
+    int nch;
+};
+
+PoolPlan plan_pool(int32_t B, int64_t n_beh, int32_t D)
+{
+    PoolPlan p{};
+    const int64_t n_occ = n_beh + B;
+    p.nch = (int)((n_occ + AMS_WAVE - 1) / AMS_WAVE);
+    size_t o = 0;
+    p.off_samp = o; o += al256((size_t)n_beh * 4);
+    p.off_c = o; o += al256((size_t)B * 4);
+    p.off_da = o; o += al256((size_t)B * D * 4);
+    p.off_head = o; o += al256((size_t)p.nch * D * 4);
+    p.off_tail = o; o += al256((size_t)p.nch * D * 4);
+    p.off_cross = o; o += al256((size_t)p.nch * 4);
+    p.total = o;
+    return p;
+}
+
+template <int MODE, int DM>
+void launch_fwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32_t *inv, const float *E,
+                float *U, float *A, void *saved, hipStream_t st)
+{
+    pool_fwd_k<MODE, DM><<<(B + kWaves - 1) / kWaves, kThreads, 0, st>>>(B, D, seg_off, n_beh, inv, E, U, A,
+                                                                         saved);
+}
+
+template <int MODE, int DM>
+void launch_bwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32_t *inv,
+                const int32_t *occ_perm, const int32_t *uniq_off, const float *E, const float *U,
+                const float *A, const void *saved, const float *dU, const float *dA, float *dE,
+                char *ws, const PoolPlan &p, hipStream_t st)
+{
+    int32_t *samp = (int32_t *)(ws + p.off_samp);
+    float *cvec = (float *)(ws + p.off_c);
+    float *da = (float *)(ws + p.off_da);
+    float *head = (float *)(ws + p.off_head);
+    float *tail = (float *)(ws + p.off_tail);
+    int32_t *cross = (int32_t *)(ws + p.off_cross);
+    const int n_occ = (int)(n_beh + B);
+    if (B > 0)
+        pool_bwd_sample<MODE, DM><<<(B + kWaves - 1) / kWaves, kThreads, 0, st>>>(
+            B, D, seg_off, inv, E, U, (const float *)saved, dU, samp, cvec, da);
+    const int g = (p.nch + kWaves - 1) / kWaves;
+    pool_bwd_seg<MODE, DM><<<g, kThreads, 0, st>>>(D, n_beh, n_occ, inv, occ_perm, uniq_off, E, A, saved, dU,
+                                                   dA, samp, cvec, da, p.nch, dE, head, tail, cross);
+    pool_bwd_fix<DM><<<g, kThreads, 0, st>>>(D, p.nch, uniq_off, cross, head, tail, dE);
+}
+
+ams_status check_common(int32_t mode, int32_t B, int32_t D, int64_t n_beh)
+{
+    if (mode < AMS_POOL_SUM || mode > AMS_POOL_ATT) return AMS_ERR_MODE;
+    if (B < 0 || n_beh < 0 || D < 1 || D > 32) return AMS_ERR_SIZE;
+    if (n_beh + (int64_t)B > (int64_t)INT32_MAX - 1) return AMS_ERR_SIZE;
+    return AMS_OK;
+}
+
+}  // namespace
+
+extern "C" ams_status ams_pool_fwd(int32_t mode, int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
+                                   const int32_t *inv, const float *E, float *U, float *A, void *saved,
+                                   void *stream)
+{
+    ams_status s = check_common(mode, B, D, n_beh);
+    if (s != AMS_OK) return s;
+    if (B == 0) return AMS_OK;
+    if (!seg_off || !inv || !E || !U || !A) return AMS_ERR_NULL;
+    if (mode != AMS_POOL_SUM && !saved) return AMS_ERR_NULL;
+    hipStream_t st = (hipStream_t)stream;
+    const bool small = D <= 16;
+    switch (mode) {
+    case AMS_POOL_SUM:
+        small ? launch_fwd<AMS_POOL_SUM, 16>(B, D, seg_off, n_beh, inv, E, U, A, saved, st)
+              : launch_fwd<AMS_POOL_SUM, 32>(B, D, seg_off, n_beh, inv, E, U, A, saved, st);
+        break;
+    case AMS_POOL_MAX:
+        small ? launch_fwd<AMS_POOL_MAX, 16>(B, D, seg_off, n_beh, inv, E, U, A, saved, st)
+              : launch_fwd<AMS_POOL_MAX, 32>(B, D, seg_off, n_beh, inv, E, U, A, saved, st);
+        break;
+    default:
+        small ? launch_fwd<AMS_POOL_ATT, 16>(B, D, seg_off, n_beh, inv, E, U, A, saved, st)
+              : launch_fwd<AMS_POOL_ATT, 32>(B, D, seg_off, n_beh, inv, E, U, A, saved, st);
+    }
+    return ams_launch_status();
+}
+
+extern "C" size_t ams_pool_workspace(int32_t mode, int32_t B, int64_t n_beh, int32_t D, int32_t n_uniq_cap)
+{
+    (void)n_uniq_cap;
+    if (check_common(mode, B, D, n_beh) != AMS_OK) return 0;
+    return plan_pool(B, n_beh, D).total;
+}
+
+extern "C" ams_status ams_pool_bwd(int32_t mode, int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
+                                   const int32_t *inv, const int32_t *occ_perm, const int32_t *uniq_off,
+                                   const int32_t *n_uniq, int32_t n_uniq_cap, const float *E, const float *U,
+                                   const float *A, const void *saved, const float *dU, const float *dA,
+                                   float *dE, void *ws, size_t ws_bytes, void *stream)
+{
+    ams_status s = check_common(mode, B, D, n_beh);
+    if (s != AMS_OK) return s;
+    (void)n_uniq;
+    if (n_uniq_cap < 0) return AMS_ERR_SIZE;
+    const int64_t n_occ = n_beh + B;
+    if (n_occ == 0) return AMS_OK;
+    if (!seg_off || !inv || !occ_perm || !uniq_off || !E || !dE) return AMS_ERR_NULL;
+    if (B > 0 && (!U || !A || !dU)) return AMS_ERR_NULL;
+    if (mode != AMS_POOL_SUM && B > 0 && !saved) return AMS_ERR_NULL;
+    const PoolPlan p = plan_pool(B, n_beh, D);
+    if (!ws || ws_bytes < p.total) return AMS_ERR_WORKSPACE;
+    hipStream_t st = (hipStream_t)stream;
+    char *w = (char *)ws;
+    const bool small = D <= 16;
+#define AMS_POOL_BWD(MODE, DM) \
+    launch_bwd<MODE, DM>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, A, saved, dU, dA, dE, w, p, st)
+    switch (mode) {
+    case AMS_POOL_SUM:
+        if (small) AMS_POOL_BWD(AMS_POOL_SUM, 16); else AMS_POOL_BWD(AMS_POOL_SUM, 32);
+        break;
+    case AMS_POOL_MAX:
+        if (small) AMS_POOL_BWD(AMS_POOL_MAX, 16); else AMS_POOL_BWD(AMS_POOL_MAX, 32);
+        break;
+    default:
+        if (small) AMS_POOL_BWD(AMS_POOL_ATT, 16); else AMS_POOL_BWD(AMS_POOL_ATT, 32);
+    }
+#undef AMS_POOL_BWD
+    return ams_launch_status();
+}

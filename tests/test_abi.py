@@ -1,0 +1,134 @@
+"""The C ABI without a GPU: libams.so loads, exports every function that
+include/ams.h declares, sizes workspaces, and reports host-detectable errors
+before touching the device (these calls return before any HIP call)."""
+import ctypes
+import os
+import re
+import subprocess
+
+import pytest
+
+from paper_1711_06505_amd import ams
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "ams.h")
+
+OK, NULL, SIZE, DTYPE, DIMS, WS, HIP, IDR, MODE = range(9)
+FAKE = ctypes.c_void_p(0x1000)      # never dereferenced: validation fails first
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(ams_[a-z_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(ams.LIB_PATH):
+        pytest.skip("libams.so not built")
+    return ams.load()
+
+
+def test_header_declares_the_boundary():
+    assert declared_functions() == sorted(ams.EXPORTS)
+
+
+def test_every_declared_symbol_is_exported(lib):
+    out = subprocess.run(["nm", "-D", "--defined-only", ams.LIB_PATH], capture_output=True, text=True,
+                         check=True).stdout
+    exported = set(re.findall(r"\bT (ams_\w+)", out))
+    for name in declared_functions():
+        assert name in exported, name
+        assert getattr(lib, name) is not None
+
+
+def test_status_strings(lib):
+    for s in range(9):
+        assert lib.ams_status_str(s).decode()
+    assert b"gfx950" in lib.ams_build_info()
+
+
+def test_workspace_sizes(lib):
+    assert lib.ams_dedup_workspace(-1, 10) == 0
+    assert lib.ams_dedup_workspace(57_000, 200_000) >= 4 * 57_000 * 4
+    m = ams.make_mlp((4096, 256, 64, 12), "f32")
+    assert lib.ams_embed_workspace(ctypes.byref(m), 57_000) >= 57_000 * 256 * 4
+    bad = ams.make_mlp((4000, 256, 64, 12), "f32")
+    assert lib.ams_embed_workspace(ctypes.byref(bad), 100) == 0
+    assert lib.ams_pool_workspace(2, 1024, 56_000, 12, 57_000) > 0
+    assert lib.ams_pool_workspace(9, 1024, 56_000, 12, 57_000) == 0
+
+
+def test_dedup_host_errors(lib):
+    args = [FAKE, 100, 10, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 1 << 30, None]
+    a = list(args); a[1] = -1
+    assert lib.ams_dedup(*a) == SIZE
+    a = list(args); a[2] = 0
+    assert lib.ams_dedup(*a) == SIZE
+    a = list(args); a[1] = 2 ** 31
+    assert lib.ams_dedup(*a) == SIZE
+    a = list(args); a[0] = None
+    assert lib.ams_dedup(*a) == NULL
+    a = list(args); a[7] = None               # n_uniq
+    assert lib.ams_dedup(*a) == NULL
+    a = list(args); a[10] = 16
+    assert lib.ams_dedup(*a) == WS
+
+
+def _embed_args(m):
+    return [ctypes.byref(m), FAKE, 1000, FAKE, FAKE, 100, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+            FAKE, FAKE, FAKE, FAKE, 1 << 30, None]
+
+
+def test_embed_host_errors(lib):
+    m = ams.make_mlp((4096, 256, 64, 12), "f32")
+    assert lib.ams_embed_fwd(None, *_embed_args(m)[1:]) == NULL
+    for dims, code in [((4000, 256, 64, 12), DIMS), ((4096, 300, 64, 12), DIMS),
+                       ((4096, 256, 65, 12), DIMS), ((4096, 256, 64, 33), DIMS),
+                       ((4096, 512, 64, 12), DIMS)]:
+        bad = ams.make_mlp(dims, "f32")
+        assert lib.ams_embed_fwd(*_embed_args(bad)) == code, dims
+    bad = ams.make_mlp((4096, 256, 64, 12), "f32")
+    bad.dtype = 5
+    assert lib.ams_embed_fwd(*_embed_args(bad)) == DTYPE
+    a = _embed_args(m); a[5] = -1
+    assert lib.ams_embed_fwd(*a) == SIZE
+    a = _embed_args(m); a[1] = None
+    assert lib.ams_embed_fwd(*a) == NULL
+    a = _embed_args(m); a[5] = 0              # nothing to do: returns before any launch
+    assert lib.ams_embed_fwd(*a) == OK
+    # fp32 without H1_save keeps H1 in the workspace, which is then required
+    a = _embed_args(m); a[12] = None; a[15] = None; a[16] = 0
+    assert lib.ams_embed_fwd(*a) == WS
+    bw = [ctypes.byref(m), FAKE, 1000, FAKE, FAKE, 100, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE,
+          FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16, None]
+    assert lib.ams_embed_bwd(*bw) == WS
+    b2 = list(bw); b2[9] = None               # H1_save
+    assert lib.ams_embed_bwd(*b2) == NULL
+    fr = ams.make_mlp((4096, 256, 64, 12), "f32", final_relu=True)
+    b3 = list(bw); b3[0] = ctypes.byref(fr)   # final_relu needs the forward's E
+    assert lib.ams_embed_bwd(*b3) == NULL
+
+
+def test_pool_host_errors(lib):
+    f = [2, 4, 12, FAKE, 40, FAKE, FAKE, FAKE, FAKE, FAKE, None]
+    a = list(f); a[0] = 3
+    assert lib.ams_pool_fwd(*a) == MODE
+    a = list(f); a[2] = 0
+    assert lib.ams_pool_fwd(*a) == SIZE
+    a = list(f); a[2] = 33
+    assert lib.ams_pool_fwd(*a) == SIZE
+    a = list(f); a[1] = -1
+    assert lib.ams_pool_fwd(*a) == SIZE
+    a = list(f); a[9] = None                  # attention needs its weights buffer
+    assert lib.ams_pool_fwd(*a) == NULL
+    a = list(f); a[1] = 0                     # empty batch: nothing to do
+    assert lib.ams_pool_fwd(*a) == OK
+    b = [2, 4, 12, FAKE, 40, FAKE, FAKE, FAKE, FAKE, 44, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE,
+         FAKE, 16, None]
+    assert lib.ams_pool_bwd(*b) == WS
+    a = list(b); a[6] = None                  # occ_perm
+    assert lib.ams_pool_bwd(*a) == NULL
+    a = list(b); a[9] = -3
+    assert lib.ams_pool_bwd(*a) == SIZE
