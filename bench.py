@@ -51,7 +51,9 @@ def traffic_from_profile(kernel_src_hash: str, unique_count: float):
         return None
     if d.get("source_sha256") != kernel_src_hash:
         return None
-    return d.get("hbm_bytes_per_launch")
+    # bytes scale with the unique rows a launch gathers: per-unique figure of
+    # the profiled batch times this run's mean unique count
+    return d["hbm_bytes_per_unique"] * unique_count
 
 
 def src_hash():
