@@ -63,34 +63,100 @@ __device__ __forceinline__ int acc_row(int j, int lane) { return 8 * (j >> 2) + 
 
 // ----------------------------------------------------------- layer 1 fwd
 
-// fp32: block tile 64 rows x NT columns, K step 32, double-buffered LDS.
-// Waves are 2 x 2; wave (wm, wn) owns 32 rows x NT/2 columns.  Within a K
-// step, lane l supplies k = 16*(l/32) + i to MFMA i (the sum over k does not
-// care which k goes to which MFMA as long as A and B agree), so each lane reads
-// 16 contiguous floats per operand with four 16-byte LDS loads.
+// fp32 forward of the 4096-wide layer.  Block tile 64 rows x NT columns, K
+// step 32 floats, 4 waves in 2 x 2 (wave (wm, wn) owns 32 rows x NT/2 cols).
+//
+// Operands stream straight from HBM into a 3-slot LDS ring with
+// global_load_lds_dwordx4 (no staging registers): stage s+2 is in flight
+// while stage s feeds the MFMAs.  Each slot is its own __shared__ array and
+// the loop is unrolled by 3 so that the compiler can tell the slot being
+// filled from the slot being read, and each wave waits only for its own
+// oldest stage (s_waitcnt vmcnt) before a bare s_barrier.
+//
+// One DMA instruction moves 1 KB = 8 tile rows of 128 B; lane l writes 16 B
+// to slot (l % 8) of row l / 8.  Rows are XOR-swizzled by ring_swz(row) so
+// that the MFMA operand reads (16 B per lane, 32 consecutive rows) hit
+// distinct banks.  Within a K step lane l supplies k = 16*(l/32) + i to MFMA
+// i (A and B agree, so the sum over k is unchanged).
+//
+// Rows past n_u and rows whose ID is outside the table read the zero row.
+__device__ __forceinline__ int ring_swz(int row) { return (row & 7) ^ ((row >> 1) & 4); }
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+
+__device__ __forceinline__ void dma16(const void *src, void *lds_dst)
+{
+    __builtin_amdgcn_global_load_lds(src, (lds_void_t *)lds_dst, 16, 0, 0);
+}
+
+// s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
+#define AMS_WAIT_VM(n) \
+    __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (((n) >> 4) << 14) | (0x7 << 4) | (0xF << 8))
+
+template <int NT>
+struct L1Ring {
+    static constexpr int BM = 64, BK = 32;
+    static constexpr int ROWS = BM + NT;                 // A rows then B rows
+    static constexpr int SLOT = ROWS * BK;               // floats per ring slot
+    static constexpr int PER_WAVE = ROWS / 8 / 4;        // DMA instructions per wave per stage
+};
+
+template <int NT>
+__device__ __forceinline__ void l1_issue(float *slot, const float *const *src, int k0, int wave)
+{
+#pragma unroll
+    for (int q = 0; q < L1Ring<NT>::PER_WAVE; ++q)
+        dma16(src[q] + k0, slot + (wave * L1Ring<NT>::PER_WAVE + q) * 256);
+}
+
+template <int NT>
+__device__ __forceinline__ void l1_compute(const float *slot, v16f *acc, int lane, int wave)
+{
+    constexpr int NB = NT / 64;
+    const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
+    const int ra = wm * 32 + r32;
+    float a[16], b[NB][16];
+#pragma unroll
+    for (int i4 = 0; i4 < 4; ++i4) {
+        const int q = h * 4 + i4;
+        *(float4 *)&a[4 * i4] = *(const float4 *)&slot[ra * 32 + ((q ^ ring_swz(ra)) << 2)];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            const int rb = 64 + wn * (NT / 2) + nb * 32 + r32;
+            *(float4 *)&b[nb][4 * i4] = *(const float4 *)&slot[rb * 32 + ((q ^ ring_swz(rb)) << 2)];
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma_f32(a[i], b[nb][i], acc[nb]);
+}
+
 template <int NT>
 __global__ __launch_bounds__(kThreads) void l1_fwd_f32(const float *__restrict__ T, int64_t n_rows,
                                                         int F, const int32_t *__restrict__ uniq,
                                                         const int32_t *__restrict__ n_uniq_p,
                                                         int cap, int n_mt, const float *__restrict__ W1,
                                                         const float *__restrict__ b1, int H,
+                                                        const float *__restrict__ zero_row,
                                                         float *__restrict__ H1)
 {
-    constexpr int BM = 64, BK = 32, LD = BK + 4;
-    constexpr int NB = NT / 64;              // 32-column MFMA blocks per wave
-    constexpr int BQ = NT / 32;              // float4 loads of B per thread
-    __shared__ float As[2][BM * LD];
-    __shared__ float Bs[2][NT * LD];
-    __shared__ int rid[BM];
+    using R = L1Ring<NT>;
+    constexpr int NB = NT / 64;
+    constexpr int PW = R::PER_WAVE;
+    __shared__ __attribute__((aligned(16))) float ring0[R::SLOT];
+    __shared__ __attribute__((aligned(16))) float ring1[R::SLOT];
+    __shared__ __attribute__((aligned(16))) float ring2[R::SLOT];
+    __shared__ int rid[R::BM];
 
     const int n_u = min(*n_uniq_p, cap);   // never past the caller's buffers
     int mt, nt;
     if (!xcd_tile(blockIdx.x, n_mt, H / NT, mt, nt)) return;
-    const int m0 = mt * BM;
+    const int m0 = mt * R::BM;
     if (m0 >= n_u) return;
     const int n0 = nt * NT;
-    const int t = threadIdx.x;
-    if (t < BM) {
+    const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
+    if (t < R::BM) {
         int id = -1;
         if (m0 + t < n_u) {
             id = uniq[m0 + t];
@@ -100,80 +166,66 @@ __global__ __launch_bounds__(kThreads) void l1_fwd_f32(const float *__restrict__
     }
     __syncthreads();
 
-    const float *ap[2];
-    int aoff[2];
+    // per-lane source of each of this wave's DMA instructions
+    const float *src[PW];
 #pragma unroll
-    for (int q = 0; q < 2; ++q) {
-        const int idx = t + kThreads * q;
-        const int r = idx >> 3, c = (idx & 7) * 4;
-        ap[q] = rid[r] >= 0 ? T + (size_t)rid[r] * F + c : nullptr;
-        aoff[q] = r * LD + c;
+    for (int q = 0; q < PW; ++q) {
+        const int row = (wave * PW + q) * 8 + (lane >> 3);
+        const int chunk = (lane & 7) ^ ring_swz(row);
+        if (row < R::BM) {
+            const int id = rid[row];
+            src[q] = (id >= 0 ? T + (size_t)id * F : zero_row) + chunk * 4;
+        } else {
+            src[q] = W1 + (size_t)(n0 + row - R::BM) * F + chunk * 4;
+        }
     }
-    const float *bp[BQ];
-    int boff[BQ];
-#pragma unroll
-    for (int q = 0; q < BQ; ++q) {
-        const int idx = t + kThreads * q;
-        const int r = idx >> 3, c = (idx & 7) * 4;
-        bp[q] = W1 + (size_t)(n0 + r) * F + c;
-        boff[q] = r * LD + c;
-    }
-    float4 ra[2], rb[BQ];
-    auto gload = [&](int k0) {
-#pragma unroll
-        for (int q = 0; q < 2; ++q)
-            ra[q] = ap[q] ? *(const float4 *)(ap[q] + k0) : make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-        for (int q = 0; q < BQ; ++q) rb[q] = *(const float4 *)(bp[q] + k0);
-    };
-    auto sstore = [&](int buf) {
-#pragma unroll
-        for (int q = 0; q < 2; ++q) *(float4 *)&As[buf][aoff[q]] = ra[q];
-#pragma unroll
-        for (int q = 0; q < BQ; ++q) *(float4 *)&Bs[buf][boff[q]] = rb[q];
-    };
 
-    const int lane = ams_lane(), wave = t / AMS_WAVE;
-    const int wm = wave >> 1, wn = wave & 1, h = lane >> 5, r32 = lane & 31;
     v16f acc[NB];
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) acc[nb] = (v16f){};
 
-    gload(0);
-    sstore(0);
-    __syncthreads();
-    const int S = F / BK;
-    for (int s = 0; s < S; ++s) {
-        const int buf = s & 1;
-        if (s + 1 < S) gload((s + 1) * BK);
-        float a[16], b[NB][16];
-        const float *pa = &As[buf][(wm * 32 + r32) * LD + h * 16];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) *(float4 *)&a[4 * q] = *(const float4 *)(pa + 4 * q);
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-            const float *pb = &Bs[buf][(wn * (NT / 2) + nb * 32 + r32) * LD + h * 16];
-#pragma unroll
-            for (int q = 0; q < 4; ++q) *(float4 *)&b[nb][4 * q] = *(const float4 *)(pb + 4 * q);
-        }
-#pragma unroll
-        for (int i = 0; i < 16; ++i)
-#pragma unroll
-            for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma_f32(a[i], b[nb][i], acc[nb]);
-        if (s + 1 < S) sstore(buf ^ 1);
-        __syncthreads();
+    const int S = F / R::BK;
+    // stage s lives in ring slot s % 3; stage s + 2 is issued while s computes.
+    // Past the end the last stage is reloaded into a slot nobody reads again,
+    // which keeps every wave's count of outstanding DMA uniform.
+#define L1_STAGE(cur, nxt, s)                                                    \
+    do {                                                                         \
+        AMS_WAIT_VM(PW);                                                         \
+        __builtin_amdgcn_s_barrier();                                            \
+        __builtin_amdgcn_sched_barrier(0);                                       \
+        l1_issue<NT>(nxt, src, min((s) + 2, S - 1) * R::BK, wave);               \
+        __builtin_amdgcn_sched_barrier(0);                                       \
+        l1_compute<NT>(cur, acc, lane, wave);                                    \
+    } while (0)
+
+    l1_issue<NT>(ring0, src, 0, wave);
+    l1_issue<NT>(ring1, src, min(1, S - 1) * R::BK, wave);
+    int s = 0;
+    for (; s + 3 <= S; s += 3) {
+        L1_STAGE(ring0, ring2, s);
+        L1_STAGE(ring1, ring0, s + 1);
+        L1_STAGE(ring2, ring1, s + 2);
     }
+    if (s < S) L1_STAGE(ring0, ring2, s);
+    if (s + 1 < S) L1_STAGE(ring1, ring0, s + 1);
+#undef L1_STAGE
+    AMS_WAIT_VM(0);
 
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb) {
-        const int col = n0 + wn * (NT / 2) + nb * 32 + r32;
+        const int col = n0 + (wave & 1) * (NT / 2) + nb * 32 + (lane & 31);
         const float bias = b1[col];
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-            const int row = m0 + wm * 32 + acc_row(j, lane);
+            const int row = m0 + (wave >> 1) * 32 + acc_row(j, lane);
             if (row < n_u) H1[(size_t)row * H + col] = fmaxf(acc[nb][j] + bias, 0.f);
         }
     }
+}
+
+__global__ void fill_zero(float *p, int n)
+{
+    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0.f;
 }
 
 // bf16: same tiling with K step 64; lane l supplies k = 32*(l/32) + 8*i + e to
@@ -292,16 +344,24 @@ __global__ __launch_bounds__(kThreads) void l1_fwd_bf16(const uint16_t *__restri
     }
 }
 
-// ------------------------------------------------------- tail layers fwd
+// ------------------------------------------------------- tail layers
 
 __device__ __forceinline__ float ld_w(const void *W, int bf16, size_t i)
 {
     return bf16 ? ams_bf16_to_f32(((const uint16_t *)W)[i]) : ((const float *)W)[i];
 }
 
-// One wave per unique image.  Layer a: H (<= 256) -> M (<= 64); for a
-// 3-layer model layer b: M -> D (<= 32).  Weights transposed into LDS so that
-// lanes (outputs) read consecutive addresses and the input vector broadcasts.
+// Both tail kernels walk their unique images in chunks of 32 rows and run
+// the small contractions on fp32 MFMA (32x32x2) with operands in LDS.  Layer
+// widths: H = dims[1] (64..256, a multiple of 64), Mo = width of the second
+// layer's output (dims[2] for 3 layers, D for 2), padded to 64 with zeros.
+constexpr int kTailRows = 32;
+constexpr int kTailLD = kMaxH1 + 4;       // row stride of [row][k] operand tiles
+constexpr int kTailLDo = kMaxH2 + 4;      // row stride of [row][o] tiles
+
+// Forward: Z2 = H1 W2^T + b2 for a chunk of 32 rows.  Wave w computes output
+// columns 32 (w & 1) .. +32 over the K half w >> 1; the two halves are added
+// in a fixed order.  Then H2 = ReLU(Z2) and, for 3 layers, E = H2 W3^T + b3.
 template <int L>
 __global__ __launch_bounds__(kThreads) void tail_fwd(const float *__restrict__ H1, int H, int M,
                                                       int D, const void *__restrict__ W2,
@@ -313,55 +373,83 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(const float *__restrict__ H
                                                       float *__restrict__ H2_save,
                                                       float *__restrict__ E)
 {
-    __shared__ float W2t[kMaxH1 * kMaxH2];
-    __shared__ float W3t[kMaxH2 * kMaxD];
-    __shared__ float hrow[kThreads / AMS_WAVE][kMaxH1];
-    __shared__ float h2row[kThreads / AMS_WAVE][kMaxH2];
+    __shared__ __attribute__((aligned(16))) float W2s[kMaxH2 * kTailLD];     // [o][i]
+    __shared__ __attribute__((aligned(16))) float Hs[kTailRows * kTailLD];   // [row][i]
+    __shared__ float Zp[2][kTailRows][kMaxH2 + 1];
+    __shared__ float W3s[kMaxD * kMaxH2];
+    __shared__ float h2s[kTailRows][kMaxH2 + 1];
     const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
-    for (int e = t; e < M * H; e += kThreads) W2t[(e % H) * M + e / H] = ld_w(W2, wbf16, e);
+    const int h = lane >> 5, r32 = lane & 31;
+    // M = width of the second layer's output (D for a 2-layer model)
+    for (int e = t; e < kMaxH2 * H; e += kThreads) {
+        const int o = e / H, i = e % H;
+        W2s[o * kTailLD + i] = o < M ? ld_w(W2, wbf16, (size_t)o * H + i) : 0.f;
+    }
     if (L == 3)
-        for (int e = t; e < D * M; e += kThreads) W3t[(e % M) * D + e / M] = ld_w(W3, wbf16, e);
-    __syncthreads();
-    const int n_u = min(*n_uniq_p, cap);   // never past the caller's buffers
+        for (int e = t; e < D * M; e += kThreads) W3s[e] = ld_w(W3, wbf16, e);
+    const int n_u = min(*n_uniq_p, cap);
     const bool relu_a = (L == 3) || final_relu;
-    for (int u = blockIdx.x * (kThreads / AMS_WAVE) + wave; u < n_u; u += gridDim.x * (kThreads / AMS_WAVE)) {
-        for (int i = lane; i < H; i += AMS_WAVE) hrow[wave][i] = H1[(size_t)u * H + i];
-        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-        __builtin_amdgcn_wave_barrier();
-        float z = 0.f;
-        if (lane < M) {
-            z = b2[lane];
-            for (int i = 0; i < H; ++i) z += W2t[i * M + lane] * hrow[wave][i];
+    const int kh = wave >> 1, nb = wave & 1, khalf = H / 2;
+    for (int c0 = blockIdx.x * kTailRows; c0 < n_u; c0 += gridDim.x * kTailRows) {
+        __syncthreads();
+        for (int e = t; e < kTailRows * (H / 4); e += kThreads) {
+            const int r = e / (H / 4), q = e % (H / 4);
+            const float4 v = c0 + r < n_u ? *(const float4 *)(H1 + (size_t)(c0 + r) * H + 4 * q)
+                                          : make_float4(0.f, 0.f, 0.f, 0.f);
+            *(float4 *)&Hs[r * kTailLD + 4 * q] = v;
+        }
+        __syncthreads();
+        v16f acc = (v16f){};
+        for (int k0 = kh * khalf; k0 < (kh + 1) * khalf; k0 += 32) {
+            float a[16], b[16];
+            const float *pa = &Hs[r32 * kTailLD + k0 + 16 * h];
+            const float *pb = &W2s[(nb * 32 + r32) * kTailLD + k0 + 16 * h];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                *(float4 *)&a[4 * q] = *(const float4 *)(pa + 4 * q);
+                *(float4 *)&b[4 * q] = *(const float4 *)(pb + 4 * q);
+            }
+#pragma unroll
+            for (int i = 0; i < 16; ++i) acc = mfma_f32(a[i], b[i], acc);
+        }
+#pragma unroll
+        for (int j = 0; j < 16; ++j) Zp[kh][acc_row(j, lane)][nb * 32 + r32] = acc[j];
+        __syncthreads();
+        for (int e = t; e < kTailRows * M; e += kThreads) {
+            const int r = e / M, o = e % M;
+            float z = Zp[0][r][o] + Zp[1][r][o] + b2[o];
             if (relu_a) z = fmaxf(z, 0.f);
+            h2s[r][o] = z;
+            if (c0 + r < n_u) {
+                if (L == 3) {
+                    if (H2_save) H2_save[(size_t)(c0 + r) * M + o] = z;
+                } else {
+                    E[(size_t)(c0 + r) * M + o] = z;
+                }
+            }
         }
         if (L == 3) {
-            if (lane < M) {
-                h2row[wave][lane] = z;
-                if (H2_save) H2_save[(size_t)u * M + lane] = z;
+            __syncthreads();
+            for (int e = t; e < kTailRows * D; e += kThreads) {
+                const int r = e / D, d = e % D;
+                if (c0 + r >= n_u) continue;
+                float v = b3[d];
+                for (int o = 0; o < M; ++o) v += W3s[d * M + o] * h2s[r][o];
+                if (final_relu) v = fmaxf(v, 0.f);
+                E[(size_t)(c0 + r) * D + d] = v;
             }
-            __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            if (lane < D) {
-                float e = b3[lane];
-                for (int o = 0; o < M; ++o) e += W3t[o * D + lane] * h2row[wave][o];
-                if (final_relu) e = fmaxf(e, 0.f);
-                E[(size_t)u * D + lane] = e;
-            }
-        } else {
-            if (lane < M) E[(size_t)u * M + lane] = z;
         }
-        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
-        __builtin_amdgcn_wave_barrier();
     }
 }
 
-// ------------------------------------------------------- tail layers bwd
-
-// Block g owns unique images [g n_u / G, (g+1) n_u / G) in ascending order.
-// Thread t owns hidden unit i = t of layer 1 (column i of dW2, dZ1[:, i],
-// db1[i]) and a slice of dW3.  Partial layout per block:
-//   [dW2: Mo x H][db2: Mo][dW3: D x M][db3: D][db1: H]
-// where Mo = M for 3 layers (Mo = D for 2 layers, and dW3/db3 are empty).
+// Backward of the small layers.  Block g owns unique images
+// [g n_u / G, (g+1) n_u / G), walked in chunks of 32 rows.  Per chunk:
+//   dz_last = dE (masked by the last ReLU if any); for 3 layers
+//   dZ2 = (dz_last W3) * [H2 > 0], else dZ2 = dz_last;
+//   dH1 = dZ2 W2 on MFMA, dZ1 = dH1 * [H1 > 0] (written out for dW1);
+//   dW2 += dZ2^T H1 on MFMA (accumulators live across chunks);
+//   dW3, db1, db2, db3 accumulate on the vector units.
+// Partials per block: [dW2: Mo x H][db2: Mo][dW3: D x M][db3: D][db1: H].
 template <int L>
 __global__ __launch_bounds__(kThreads) void tail_bwd(const void *__restrict__ H1s, int h1_bf16,
                                                       const float *__restrict__ H2s,
@@ -374,83 +462,173 @@ __global__ __launch_bounds__(kThreads) void tail_bwd(const void *__restrict__ H1
                                                       void *__restrict__ dZ1, int dz1_bf16,
                                                       float *__restrict__ part, int PS)
 {
-    __shared__ float W2s[kMaxH2 * kMaxH1];
+    __shared__ __attribute__((aligned(16))) float W2t[kMaxH1 * kTailLDo];    // [i][o]
+    __shared__ __attribute__((aligned(16))) float Hc[kTailRows * kTailLD];   // [row][i]
+    __shared__ __attribute__((aligned(16))) float dz2s[kTailRows * kTailLDo];// [row][o]
     __shared__ float W3s[kMaxD * kMaxH2];
-    __shared__ float dzl[kMaxD];
-    __shared__ float h2s[kMaxH2];
-    __shared__ float dz2s[kMaxH2];
-    const int t = threadIdx.x;
-    const int Mo = (L == 3) ? M : D;                  // width of the layer feeding dW2's rows
-    for (int e = t; e < Mo * H; e += kThreads) W2s[e] = ld_w(W2, wbf16, e);
+    __shared__ float h2c[kTailRows][kMaxH2 + 1];
+    __shared__ float dzl[kTailRows][kMaxD + 1];
+    const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
+    const int h = lane >> 5, r32 = lane & 31;
+    const int Mo = (L == 3) ? M : D;
+    for (int e = t; e < kMaxH2 * H; e += kThreads) {
+        const int o = e / H, i = e % H;
+        W2t[i * kTailLDo + o] = o < Mo ? ld_w(W2, wbf16, (size_t)o * H + i) : 0.f;
+    }
     if (L == 3)
         for (int e = t; e < D * M; e += kThreads) W3s[e] = ld_w(W3, wbf16, e);
-    const int n_u = min(*n_uniq_p, cap);   // never past the caller's buffers
+    const int n_u = min(*n_uniq_p, cap);
     const int r0 = (int)((int64_t)blockIdx.x * n_u / gridDim.x);
     const int r1 = (int)((int64_t)(blockIdx.x + 1) * n_u / gridDim.x);
 
-    float dW2a[kMaxH2];
+    // this wave's share of H: columns [64 wave, 64 wave + 64) (H <= 256)
+    const int i0 = 64 * wave;
+    const bool wave_on = i0 < H;
+    v16f dw2[2][2];                          // [o block][i block]
 #pragma unroll
-    for (int o = 0; o < kMaxH2; ++o) dW2a[o] = 0.f;
+    for (int a = 0; a < 2; ++a)
+#pragma unroll
+        for (int b = 0; b < 2; ++b) dw2[a][b] = (v16f){};
+    float db1a[2] = {0.f, 0.f};              // columns i0 + 32 nb + r32 (h == 0 lanes)
     float dW3a[8];
 #pragma unroll
     for (int q = 0; q < 8; ++q) dW3a[q] = 0.f;
-    float db1a = 0.f, db2a = 0.f, db3a = 0.f;
-    __syncthreads();
+    float db2a = 0.f, db3a = 0.f;
 
-    for (int u = r0; u < r1; ++u) {
-        if (t < D) {
-            float g = dE[(size_t)u * D + t];
-            if (final_relu && !(Efwd[(size_t)u * D + t] > 0.f)) g = 0.f;
-            dzl[t] = g;
-        }
-        if (L == 3 && t < M) h2s[t] = H2s[(size_t)u * M + t];
+    for (int c0 = r0; c0 < r1; c0 += kTailRows) {
         __syncthreads();
-        if (L == 3) {
-            if (t < M) {
-                float dh = 0.f;
-                for (int d = 0; d < D; ++d) dh += W3s[d * M + t] * dzl[d];
-                const float dz = h2s[t] > 0.f ? dh : 0.f;
-                dz2s[t] = dz;
-                db2a += dz;
+        for (int e = t; e < kTailRows * H; e += kThreads) {
+            const int r = e / H, i = e % H;
+            float v = 0.f;
+            if (c0 + r < r1) {
+                const size_t x = (size_t)(c0 + r) * H + i;
+                v = h1_bf16 ? ams_bf16_to_f32(((const uint16_t *)H1s)[x]) : ((const float *)H1s)[x];
             }
+            Hc[r * kTailLD + i] = v;
+        }
+        for (int e = t; e < kTailRows * D; e += kThreads) {
+            const int r = e / D, d = e % D;
+            float g = 0.f;
+            if (c0 + r < r1) {
+                g = dE[(size_t)(c0 + r) * D + d];
+                if (final_relu && !(Efwd[(size_t)(c0 + r) * D + d] > 0.f)) g = 0.f;
+            }
+            dzl[r][d] = g;
+        }
+        if (L == 3)
+            for (int e = t; e < kTailRows * M; e += kThreads) {
+                const int r = e / M, o = e % M;
+                h2c[r][o] = c0 + r < r1 ? H2s[(size_t)(c0 + r) * M + o] : 0.f;
+            }
+        __syncthreads();
+        // dZ2, db2 (thread o), dW3 / db3 (vector units)
+        for (int e = t; e < kTailRows * kMaxH2; e += kThreads) {
+            const int r = e / kMaxH2, o = e % kMaxH2;
+            float dz = 0.f;
+            if (o < Mo) {
+                if (L == 3) {
+                    float dh = 0.f;
+                    for (int d = 0; d < D; ++d) dh += W3s[d * M + o] * dzl[r][d];
+                    dz = h2c[r][o] > 0.f ? dh : 0.f;
+                } else {
+                    dz = dzl[r][o];
+                }
+            }
+            dz2s[r * kTailLDo + o] = dz;
+        }
+        if (L == 3) {
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
                 const int e = t + kThreads * q;
-                if (e < D * M) dW3a[q] += dzl[e / M] * h2s[e % M];
+                if (e < D * M) {
+                    const int d = e / M, o = e % M;
+                    float s = 0.f;
+                    for (int r = 0; r < kTailRows; ++r) s += dzl[r][d] * h2c[r][o];
+                    dW3a[q] += s;
+                }
             }
-            if (t < D) db3a += dzl[t];
-        } else {
             if (t < D) {
-                dz2s[t] = dzl[t];
-                db2a += dzl[t];
+                float s = 0.f;
+                for (int r = 0; r < kTailRows; ++r) s += dzl[r][t];
+                db3a += s;
             }
         }
         __syncthreads();
-        if (t < H) {
-            const float h1 = h1_bf16 ? ams_bf16_to_f32(((const uint16_t *)H1s)[(size_t)u * H + t])
-                                     : ((const float *)H1s)[(size_t)u * H + t];
-            float dh = 0.f;
-#pragma unroll
-            for (int o = 0; o < kMaxH2; ++o)
-                if (o < Mo) dh += W2s[o * H + t] * dz2s[o];
-            const float dz = h1 > 0.f ? dh : 0.f;
-            if (dz1_bf16)
-                ((uint16_t *)dZ1)[(size_t)u * H + t] = ams_f32_to_bf16(dz);
-            else
-                ((float *)dZ1)[(size_t)u * H + t] = dz;
-            db1a += dz;
-#pragma unroll
-            for (int o = 0; o < kMaxH2; ++o)
-                if (o < Mo) dW2a[o] += dz2s[o] * h1;
+        if (t < Mo) {
+            float s = 0.f;
+            for (int r = 0; r < kTailRows; ++r) s += dz2s[r * kTailLDo + t];
+            db2a += s;
         }
-        __syncthreads();
+        if (wave_on) {
+            // dH1 = dZ2 W2 : rows x [i0, i0 + 64), K = 64 (padded o)
+            v16f acc[2] = {(v16f){}, (v16f){}};
+#pragma unroll
+            for (int k0 = 0; k0 < kMaxH2; k0 += 32) {
+                float a[16], b[2][16];
+                const float *pa = &dz2s[r32 * kTailLDo + k0 + 16 * h];
+#pragma unroll
+                for (int q = 0; q < 4; ++q) *(float4 *)&a[4 * q] = *(const float4 *)(pa + 4 * q);
+#pragma unroll
+                for (int nb = 0; nb < 2; ++nb) {
+                    const float *pb = &W2t[(i0 + nb * 32 + r32) * kTailLDo + k0 + 16 * h];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) *(float4 *)&b[nb][4 * q] = *(const float4 *)(pb + 4 * q);
+                }
+#pragma unroll
+                for (int i = 0; i < 16; ++i)
+#pragma unroll
+                    for (int nb = 0; nb < 2; ++nb) acc[nb] = mfma_f32(a[i], b[nb][i], acc[nb]);
+            }
+            // dZ1 = dH1 * [H1 > 0]; write it out and sum it per column for db1
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb) {
+                const int i = i0 + nb * 32 + r32;
+                float colsum = 0.f;
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    const int r = acc_row(j, lane);
+                    const float dz = Hc[r * kTailLD + i] > 0.f ? acc[nb][j] : 0.f;
+                    colsum += dz;
+                    if (c0 + r < r1) {
+                        const size_t x = (size_t)(c0 + r) * H + i;
+                        if (dz1_bf16)
+                            ((uint16_t *)dZ1)[x] = ams_f32_to_bf16(dz);
+                        else
+                            ((float *)dZ1)[x] = dz;
+                    }
+                }
+                colsum += __shfl_xor(colsum, 32, AMS_WAVE);   // the other 16 rows of this column
+                db1a[nb] += colsum;
+            }
+            // dW2 += dZ2^T H1 : o in [0, 64) x i in [i0, i0 + 64), K = 32 rows
+#pragma unroll
+            for (int kk = 0; kk < kTailRows / 2; ++kk) {
+                const int r = 2 * kk + h;
+                float av[2], bv[2];
+#pragma unroll
+                for (int ob = 0; ob < 2; ++ob) av[ob] = dz2s[r * kTailLDo + ob * 32 + r32];
+#pragma unroll
+                for (int ib = 0; ib < 2; ++ib) bv[ib] = Hc[r * kTailLD + i0 + ib * 32 + r32];
+#pragma unroll
+                for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+                    for (int ib = 0; ib < 2; ++ib) dw2[ob][ib] = mfma_f32(av[ob], bv[ib], dw2[ob][ib]);
+            }
+        }
     }
 
     float *p = part + (size_t)blockIdx.x * PS;
-    if (t < H)
+    if (wave_on) {
 #pragma unroll
-        for (int o = 0; o < kMaxH2; ++o)
-            if (o < Mo) p[o * H + t] = dW2a[o];
+        for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+            for (int ib = 0; ib < 2; ++ib)
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    const int o = ob * 32 + acc_row(j, lane);
+                    if (o < Mo) p[o * H + i0 + ib * 32 + r32] = dw2[ob][ib][j];
+                }
+    }
     p += Mo * H;
     if (t < Mo) p[t] = db2a;
     p += Mo;
@@ -464,7 +642,10 @@ __global__ __launch_bounds__(kThreads) void tail_bwd(const void *__restrict__ H1
         if (t < D) p[t] = db3a;
         p += D;
     }
-    if (t < H) p[t] = db1a;
+    if (wave_on && h == 0) {
+        p[i0 + r32] = db1a[0];
+        p[i0 + 32 + r32] = db1a[1];
+    }
 }
 
 // out[e] = sum over g = 0..G-1 (in order) of part[g * PS + e].
@@ -617,6 +798,160 @@ __global__ __launch_bounds__(kThreads) void dw1_part(const TT *__restrict__ T, i
         }
 }
 
+// fp32 dW1 partial of chunk c with the same 3-slot DMA ring as the forward.
+// Block tile 128 (m, dZ1 columns) x 64 (n, feature columns), K step 32 unique
+// images.  Per stage the A tile is 32 rows x 512 B of dZ1 (16 DMA
+// instructions of 2 rows) and the B tile 32 rows x 256 B of gathered feature
+// rows (8 instructions of 4 rows); every wave issues 4 A and 2 B instructions.
+// The 16-byte chunk index of odd rows is XOR-ed with 8 (a 128-byte shift) so
+// that lanes 0-31 (row k) and 32-63 (row k+1) of one 4-byte operand read fall
+// in different banks.  Rows past the chunk and rows with an out-of-range ID
+// read the zero row.
+//
+// The image IDs that address the B rows are loaded two stages ahead, before
+// the DMA of the stage that is issued with them, so at the top of stage s
+// "wait until at most 8 vector-memory ops are outstanding" leaves exactly the
+// IDs of stage s+4 and the DMA of stage s+2 in flight.
+struct DwRing {
+    static constexpr int BM = 128, BN = 64, BK = 32;
+    static constexpr int A_FLOATS = BK * BM, B_FLOATS = BK * BN;
+    static constexpr int SLOT = A_FLOATS + B_FLOATS;
+    static constexpr int PA = 4, PB = 2;                 // A / B DMA instructions per wave
+    static constexpr int OUTSTANDING = PA + PB + PB;     // vm ops allowed in flight at a stage top
+};
+
+__device__ __forceinline__ int dw_chunk_swz(int row) { return (row & 1) << 3; }
+
+// IDs of this lane's two B rows of the stage starting at image u_base.
+__device__ __forceinline__ void dw1_load_ids(const int32_t *__restrict__ uniq, int u_base, int u1, int wave,
+                                             int lane, int (&id)[2])
+{
+#pragma unroll
+    for (int q = 0; q < DwRing::PB; ++q) {
+        const int row = 4 * (DwRing::PB * wave + q) + (lane >> 4);
+        const int u = u_base + row;
+        const int v = uniq[min(u, u1 - 1)];          // always issued: uniform op count
+        id[q] = u < u1 ? v : -1;
+    }
+}
+
+__device__ __forceinline__ void dw1_issue(float *slot, const float *__restrict__ T, int64_t n_rows, int F,
+                                          const float *__restrict__ dZ1, int H, int m0, int n0, int u_base,
+                                          int u1, const float *__restrict__ zero_row, const int (&id)[2],
+                                          int wave, int lane)
+{
+#pragma unroll
+    for (int q = 0; q < DwRing::PA; ++q) {
+        const int j = DwRing::PA * wave + q;
+        const int row = 2 * j + (lane >> 5);
+        const int c = (lane & 31) ^ dw_chunk_swz(row);
+        const int u = u_base + row;
+        dma16((u < u1 ? dZ1 + (size_t)u * H + m0 : zero_row) + 4 * c, slot + j * 256);
+    }
+#pragma unroll
+    for (int q = 0; q < DwRing::PB; ++q) {
+        const int jb = DwRing::PB * wave + q;
+        const int row = 4 * jb + (lane >> 4);
+        const int c = (lane & 15) ^ dw_chunk_swz(row);
+        const bool ok = id[q] >= 0 && (int64_t)id[q] < n_rows;
+        dma16((ok ? T + (size_t)id[q] * F + n0 : zero_row) + 4 * c, slot + DwRing::A_FLOATS + jb * 256);
+    }
+}
+
+__device__ __forceinline__ void dw1_compute(const float *slot, v16f *acc, int lane, int wave)
+{
+    const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
+    const float *A = slot, *B = slot + DwRing::A_FLOATS;
+#pragma unroll
+    for (int kk = 0; kk < DwRing::BK / 2; ++kk) {
+        const int k = 2 * kk + h;
+        const int sw = dw_chunk_swz(k) << 2;
+        const int n = wn * 32 + r32;
+        const float bv = B[k * DwRing::BN + (n ^ sw)];
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+            const int m = wm * 64 + mb * 32 + r32;
+            acc[mb] = mfma_f32(A[k * DwRing::BM + (m ^ sw)], bv, acc[mb]);
+        }
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void dw1_part_f32(const float *__restrict__ T, int64_t n_rows,
+                                                          int F, const int32_t *__restrict__ uniq,
+                                                          const int32_t *__restrict__ n_uniq_p, int cap,
+                                                          const float *__restrict__ dZ1, int H, int KC,
+                                                          const float *__restrict__ zero_row,
+                                                          float *__restrict__ part)
+{
+    using R = DwRing;
+    __shared__ __attribute__((aligned(16))) float ring0[R::SLOT];
+    __shared__ __attribute__((aligned(16))) float ring1[R::SLOT];
+    __shared__ __attribute__((aligned(16))) float ring2[R::SLOT];
+
+    const int nmt = H / R::BM, nnt = F / R::BN;
+    int outer, mt;
+    if (!xcd_tile(blockIdx.x, nnt * KC, nmt, outer, mt)) return;
+    const int nt = outer % nnt, c = outer / nnt;
+    const int n_u = min(*n_uniq_p, cap);
+    const int u0 = (int)((int64_t)c * n_u / KC), u1 = (int)((int64_t)(c + 1) * n_u / KC);
+    const int m0 = mt * R::BM, n0 = nt * R::BN;
+    const int lane = ams_lane(), wave = threadIdx.x / AMS_WAVE;
+
+    v16f acc[2] = {(v16f){}, (v16f){}};
+    const int S = (u1 - u0 + R::BK - 1) / R::BK;
+    if (S > 0) {
+        int id0[2], id1[2], id2[2];                       // IDs of stages = 0, 1, 2 (mod 3)
+#define DW_BASE(s) (u0 + min((s), S - 1) * R::BK)
+        // prologue: IDs of stages 0..2 resident, IDs of stage 3 in flight, DMA 0 and 1 issued
+        dw1_load_ids(uniq, DW_BASE(0), u1, wave, lane, id0);
+        dw1_load_ids(uniq, DW_BASE(1), u1, wave, lane, id1);
+        dw1_load_ids(uniq, DW_BASE(2), u1, wave, lane, id2);
+        AMS_WAIT_VM(0);
+        int idn[2];
+        dw1_load_ids(uniq, DW_BASE(3), u1, wave, lane, idn);
+        dw1_issue(ring0, T, n_rows, F, dZ1, H, m0, n0, DW_BASE(0), u1, zero_row, id0, wave, lane);
+        dw1_issue(ring1, T, n_rows, F, dZ1, H, m0, n0, DW_BASE(1), u1, zero_row, id1, wave, lane);
+        // id0 now holds stage 3's IDs (in flight); idn is the register they land in
+#define DW_STAGE(cur, nxt, ids_next_dma, ids_load, s)                                          \
+    do {                                                                                        \
+        AMS_WAIT_VM(R::OUTSTANDING);                                                            \
+        __builtin_amdgcn_s_barrier();                                                           \
+        __builtin_amdgcn_sched_barrier(0);                                                      \
+        dw1_load_ids(uniq, DW_BASE((s) + 4), u1, wave, lane, ids_load);                         \
+        dw1_issue(nxt, T, n_rows, F, dZ1, H, m0, n0, DW_BASE((s) + 2), u1, zero_row, ids_next_dma, \
+                  wave, lane);                                                                  \
+        __builtin_amdgcn_sched_barrier(0);                                                      \
+        dw1_compute(cur, acc, lane, wave);                                                      \
+    } while (0)
+        // register roles rotate with the 3-stage unroll: at stage s the IDs of
+        // stage s+2 feed the DMA and those of stage s+4 are loaded
+        id0[0] = idn[0];
+        id0[1] = idn[1];
+        // now: id2 = stage 2, id0 = stage 3 (in flight), id1 free
+        int s = 0;
+        for (; s + 3 <= S; s += 3) {
+            DW_STAGE(ring0, ring2, id2, id1, s);       // DMA stage s+2, load stage s+4
+            DW_STAGE(ring1, ring0, id0, id2, s + 1);   // DMA stage s+3, load stage s+5
+            DW_STAGE(ring2, ring1, id1, id0, s + 2);   // DMA stage s+4, load stage s+6
+        }
+        if (s < S) DW_STAGE(ring0, ring2, id2, id1, s);
+        if (s + 1 < S) DW_STAGE(ring1, ring0, id0, id2, s + 1);
+#undef DW_STAGE
+#undef DW_BASE
+        AMS_WAIT_VM(0);
+    }
+
+    float *out = part + (size_t)c * H * F;
+    const int col = n0 + (wave & 1) * 32 + (lane & 31);
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int row = m0 + (wave >> 1) * 64 + mb * 32 + acc_row(j, lane);
+            out[(size_t)row * F + col] = acc[mb][j];
+        }
+}
+
 // ----------------------------------------------------------------- host
 
 bool mlp_ok(const ams_mlp *m)
@@ -650,7 +985,7 @@ int tail_part_size(const ams_mlp *m)
 }
 
 struct BwdPlan {
-    size_t off_dz1, off_tail, off_tailsum, off_dw1, total;
+    size_t off_zero, off_dz1, off_tail, off_tailsum, off_dw1, total;
     int kc;
 };
 
@@ -661,6 +996,7 @@ BwdPlan plan_bwd(const ams_mlp *m, int32_t cap)
     const size_t es = (m->dtype == AMS_BF16) ? 2 : 4;
     p.kc = dw1_chunks(H, F);
     size_t o = 0;
+    p.off_zero = o; o += al256((size_t)(F > H ? F : H) * 4);
     p.off_dz1 = o; o += al256((size_t)cap * H * es);
     p.off_tail = o; o += al256((size_t)kTailBlocks * tail_part_size(m) * 4);
     p.off_tailsum = o; o += al256((size_t)tail_part_size(m) * 4);
@@ -669,12 +1005,19 @@ BwdPlan plan_bwd(const ams_mlp *m, int32_t cap)
     return p;
 }
 
+// Forward workspace: [zero row, max(F, H) floats][H1 fp32, cap x H (when the
+// caller gives no fp32 H1_save)].
+size_t zero_row_bytes(const ams_mlp *m)
+{
+    return al256((size_t)(m->dims[0] > m->dims[1] ? m->dims[0] : m->dims[1]) * 4);
+}
+
 }  // namespace
 
 extern "C" size_t ams_embed_workspace(const ams_mlp *mlp, int32_t n_uniq_cap)
 {
     if (!mlp_ok(mlp) || n_uniq_cap < 0) return 0;
-    const size_t fwd = al256((size_t)n_uniq_cap * mlp->dims[1] * 4);
+    const size_t fwd = zero_row_bytes(mlp) + al256((size_t)n_uniq_cap * mlp->dims[1] * 4);
     const size_t bwd = plan_bwd(mlp, n_uniq_cap).total;
     return fwd > bwd ? fwd : bwd;
 }
@@ -698,9 +1041,12 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
     const int M = (L == 3) ? mlp->dims[2] : D;
     const bool bf = mlp->dtype == AMS_BF16;
     const bool h1_in_ws = bf || !H1_save;
-    if (h1_in_ws && (!ws || ws_bytes < al256((size_t)cap * H * 4))) return AMS_ERR_WORKSPACE;
+    const size_t zb = zero_row_bytes(mlp);
+    if (!ws || ws_bytes < zb + (h1_in_ws ? al256((size_t)cap * H * 4) : 0)) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
-    float *H1f = h1_in_ws ? (float *)ws : (float *)H1_save;
+    float *zero = (float *)ws;
+    float *H1f = h1_in_ws ? (float *)((char *)ws + zb) : (float *)H1_save;
+    fill_zero<<<4, kThreads, 0, st>>>(zero, (int)(zb / 4));
 
     const int n_mt = (cap + 63) / 64;
     const int NT = (H % 128 == 0) ? 128 : 64;
@@ -708,10 +1054,10 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
     if (!bf) {
         if (NT == 128)
             l1_fwd_f32<128><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, n_mt,
-                                                       (const float *)W1, b1, H, H1f);
+                                                       (const float *)W1, b1, H, zero, H1f);
         else
             l1_fwd_f32<64><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, n_mt,
-                                                      (const float *)W1, b1, H, H1f);
+                                                      (const float *)W1, b1, H, zero, H1f);
     } else {
         if (NT == 128)
             l1_fwd_bf16<128><<<grid, kThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq, n_uniq,
@@ -722,7 +1068,7 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
                                                        cap, n_mt, (const uint16_t *)W1, b1, H, H1f,
                                                        (uint16_t *)H1_save);
     }
-    int tg = (cap + 3) / 4;
+    int tg = (cap + kTailRows - 1) / kTailRows;
     if (tg > 256) tg = 256;
     if (L == 3)
         tail_fwd<3><<<tg, kThreads, 0, st>>>(H1f, H, M, D, W2, b2, W3, b3, bf, mlp->final_relu, n_uniq,
@@ -758,6 +1104,7 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
     const bool bf = mlp->dtype == AMS_BF16;
     hipStream_t st = (hipStream_t)stream;
     char *w = (char *)ws;
+    float *zero = (float *)(w + p.off_zero);
     void *dz1 = w + p.off_dz1;
     float *tail = (float *)(w + p.off_tail);
     float *tailsum = (float *)(w + p.off_tailsum);
@@ -778,7 +1125,11 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
     const int bm = (H % 128 == 0) ? 128 : 64;
     const int nmt = H / bm, outer = (F / 64) * p.kc;
     const int grid = ((outer + 7) / 8) * 8 * nmt;
-    if (!bf) {
+    fill_zero<<<4, kThreads, 0, st>>>(zero, F > H ? F : H);
+    if (!bf && bm == 128) {
+        dw1_part_f32<<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
+                                                (const float *)dz1, H, p.kc, zero, dw1p);
+    } else if (!bf) {
         if (bm == 128)
             dw1_part<128, float><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
                                                              (const float *)dz1, H, p.kc, dw1p);
