@@ -79,7 +79,10 @@ __device__ __forceinline__ int acc_row(int j, int lane) { return 8 * (j >> 2) + 
 // distinct banks.  Within a K step lane l supplies k = 16*(l/32) + i to MFMA
 // i (A and B agree, so the sum over k is unchanged).
 //
-// Rows past n_u and rows whose ID is outside the table read the zero row.
+// Rows past n_u and rows whose ID is outside the table stream a row of W1
+// instead (always a valid address); rows past n_u are never stored and rows
+// with an out-of-range ID get the exact result of a zero feature row,
+// ReLU(b1), in the epilogue.
 __device__ __forceinline__ int ring_swz(int row) { return (row & 7) ^ ((row >> 1) & 4); }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
@@ -109,27 +112,45 @@ __device__ __forceinline__ void l1_issue(float *slot, const float *const *src, i
         dma16(src[q] + k0, slot + (wave * L1Ring<NT>::PER_WAVE + q) * 256);
 }
 
+// Operands of one K step: for k-group g (4 consecutive k per lane) the A
+// row's 16 bytes and the 16 bytes of each B row; the reads of group g+1 are
+// issued while the MFMAs of group g run (sched_group_barrier fixes the
+// interleave: 1 + NB LDS reads, then 4 NB MFMAs).
 template <int NT>
 __device__ __forceinline__ void l1_compute(const float *slot, v16f *acc, int lane, int wave)
 {
     constexpr int NB = NT / 64;
     const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
     const int ra = wm * 32 + r32;
-    float a[16], b[NB][16];
+    float4 a[4], b[4][NB];
 #pragma unroll
-    for (int i4 = 0; i4 < 4; ++i4) {
-        const int q = h * 4 + i4;
-        *(float4 *)&a[4 * i4] = *(const float4 *)&slot[ra * 32 + ((q ^ ring_swz(ra)) << 2)];
+    for (int g = 0; g < 4; ++g) {
+        const int q = h * 4 + g;
+        a[g] = *(const float4 *)&slot[ra * 32 + ((q ^ ring_swz(ra)) << 2)];
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) {
             const int rb = 64 + wn * (NT / 2) + nb * 32 + r32;
-            *(float4 *)&b[nb][4 * i4] = *(const float4 *)&slot[rb * 32 + ((q ^ ring_swz(rb)) << 2)];
+            b[g][nb] = *(const float4 *)&slot[rb * 32 + ((q ^ ring_swz(rb)) << 2)];
         }
     }
 #pragma unroll
-    for (int i = 0; i < 16; ++i)
+    for (int g = 0; g < 4; ++g) {
+        const float av[4] = {a[g].x, a[g].y, a[g].z, a[g].w};
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) acc[nb] = mfma_f32(a[i], b[nb][i], acc[nb]);
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) {
+                const float bv[4] = {b[g][nb].x, b[g][nb].y, b[g][nb].z, b[g][nb].w};
+                acc[nb] = mfma_f32(av[e], bv[e], acc[nb]);
+            }
+    }
+    // group 0's reads first, then (reads of g+1, MFMAs of g)
+    __builtin_amdgcn_sched_group_barrier(0x100, 1 + NB, 0);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        if (g < 3) __builtin_amdgcn_sched_group_barrier(0x100, 1 + NB, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 4 * NB, 0);
+    }
 }
 
 template <int NT>
@@ -138,7 +159,6 @@ __global__ __launch_bounds__(kThreads) void l1_fwd_f32(const float *__restrict__
                                                         const int32_t *__restrict__ n_uniq_p,
                                                         int cap, int n_mt, const float *__restrict__ W1,
                                                         const float *__restrict__ b1, int H,
-                                                        const float *__restrict__ zero_row,
                                                         float *__restrict__ H1)
 {
     using R = L1Ring<NT>;
@@ -174,7 +194,7 @@ __global__ __launch_bounds__(kThreads) void l1_fwd_f32(const float *__restrict__
         const int chunk = (lane & 7) ^ ring_swz(row);
         if (row < R::BM) {
             const int id = rid[row];
-            src[q] = (id >= 0 ? T + (size_t)id * F : zero_row) + chunk * 4;
+            src[q] = (id >= 0 ? T + (size_t)id * F : W1) + chunk * 4;
         } else {
             src[q] = W1 + (size_t)(n0 + row - R::BM) * F + chunk * 4;
         }
@@ -217,15 +237,188 @@ __global__ __launch_bounds__(kThreads) void l1_fwd_f32(const float *__restrict__
         const float bias = b1[col];
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-            const int row = m0 + (wave >> 1) * 32 + acc_row(j, lane);
-            if (row < n_u) H1[(size_t)row * H + col] = fmaxf(acc[nb][j] + bias, 0.f);
+            const int r = (wave >> 1) * 32 + acc_row(j, lane);
+            const int row = m0 + r;
+            const float z = rid[r] >= 0 ? acc[nb][j] + bias : bias;
+            if (row < n_u) H1[(size_t)row * H + col] = fmaxf(z, 0.f);
         }
     }
 }
 
-__global__ void fill_zero(float *p, int n)
+// Stream-K fp32 forward of the 4096-wide layer (used when H is a multiple of
+// 128).  Work = (128-row x 128-column tile, 32-wide K stage) iterations in
+// tile-major order; each of G persistent workers (one 8-wave block per CU)
+// takes an equal contiguous share, so every CU gets the same MFMA work for
+// any number of unique images.  A tile fully inside one worker's share is
+// finished in place (bias, ReLU); a tile cut by a share boundary leaves one
+// partial accumulator tile per worker, and the tail forward (which reads H1
+// anyway) adds the pieces in K order.  Waves are 4 (M) x 2 (N), 32 x 64 each; the 3-slot DMA ring and the
+// row swizzle are those of l1_fwd_f32 with 256 tile rows (128 A + 128 B).
+constexpr int kSkThreads = 512;
+constexpr int kSkBM = 128, kSkBN = 128, kSkBK = 32;
+constexpr int kSkSlot = (kSkBM + kSkBN) * kSkBK;          // floats per ring slot (32 KB)
+constexpr int kSkPW = (kSkBM + kSkBN) / 8 / 8;            // DMA instructions per wave: 4
+constexpr int kSkTile = kSkBM * kSkBN;
+constexpr int kSkMinIters = 32;                           // smallest share worth a worker
+
+struct SkPlan {
+    int n_u, n_cb, S, g;            // g = workers in use
+    int64_t total;
+    __device__ int64_t it0(int w) const { return total * w / g; }
+    __device__ int owner(int64_t it) const { return (int)(((it + 1) * g - 1) / total); }
+};
+
+__device__ __forceinline__ SkPlan sk_plan(int n_u, int H, int F, int G)
 {
-    for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) p[i] = 0.f;
+    SkPlan p;
+    p.n_u = n_u;
+    p.n_cb = H / kSkBN;
+    p.S = F / kSkBK;
+    const int64_t tiles = (int64_t)((n_u + kSkBM - 1) / kSkBM) * p.n_cb;
+    p.total = tiles * p.S;
+    const int64_t want = (p.total + kSkMinIters - 1) / kSkMinIters;
+    p.g = (int)(want < G ? want : G);
+    if (p.g < 1) p.g = 1;
+    return p;
+}
+
+__device__ __forceinline__ void sk_issue(float *slot, const float *const *src, int k0, int wave)
+{
+#pragma unroll
+    for (int q = 0; q < kSkPW; ++q) dma16(src[q] + k0, slot + (wave * kSkPW + q) * 256);
+}
+
+__device__ __forceinline__ void sk_compute(const float *slot, v16f *acc, int lane, int wave)
+{
+    const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
+    const int ra = wm * 32 + r32;
+    float4 a[4], b[4][2];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const int q = h * 4 + g;
+        a[g] = *(const float4 *)&slot[ra * 32 + ((q ^ ring_swz(ra)) << 2)];
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+            const int rb = kSkBM + wn * 64 + nb * 32 + r32;
+            b[g][nb] = *(const float4 *)&slot[rb * 32 + ((q ^ ring_swz(rb)) << 2)];
+        }
+    }
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        const float av[4] = {a[g].x, a[g].y, a[g].z, a[g].w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb) {
+                const float bv[4] = {b[g][nb].x, b[g][nb].y, b[g][nb].z, b[g][nb].w};
+                acc[nb] = mfma_f32(av[e], bv[e], acc[nb]);
+            }
+    }
+    __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        if (g < 3) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    }
+}
+
+__global__ __launch_bounds__(kSkThreads) void l1sk_f32(const float *__restrict__ T, int64_t n_rows, int F,
+                                                        const int32_t *__restrict__ uniq,
+                                                        const int32_t *__restrict__ n_uniq_p, int cap,
+                                                        const float *__restrict__ W1,
+                                                        const float *__restrict__ b1, int H, int G,
+                                                        float *__restrict__ H1, float *__restrict__ pbuf)
+{
+    __shared__ __attribute__((aligned(16))) float ring0[kSkSlot];
+    __shared__ __attribute__((aligned(16))) float ring1[kSkSlot];
+    __shared__ __attribute__((aligned(16))) float ring2[kSkSlot];
+    __shared__ int rid[kSkBM];
+
+    const int n_u = min(*n_uniq_p, cap);
+    if (n_u <= 0) return;
+    const SkPlan P = sk_plan(n_u, H, F, G);
+    // workers with consecutive shares sit on one XCD (blocks go round-robin)
+    const int w = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+    if (w >= P.g) return;
+    const int64_t it1 = P.it0(w + 1);
+    const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
+    const int S = P.S;
+    bool first = true;
+    for (int64_t it = P.it0(w); it < it1;) {
+        const int tile = (int)(it / S);
+        const int ks = (int)(it % S);
+        const int ke = (int)min<int64_t>(S, ks + (it1 - it));
+        const int m0 = (tile / P.n_cb) * kSkBM, n0 = (tile % P.n_cb) * kSkBN;
+        __syncthreads();                        // previous segment done with rid and the ring
+        if (t < kSkBM) {
+            int id = -1;
+            if (m0 + t < n_u) {
+                id = uniq[m0 + t];
+                if (id < 0 || (int64_t)id >= n_rows) id = -1;
+            }
+            rid[t] = id;
+        }
+        __syncthreads();
+        const float *src[kSkPW];
+#pragma unroll
+        for (int q = 0; q < kSkPW; ++q) {
+            const int row = (wave * kSkPW + q) * 8 + (lane >> 3);
+            const int chunk = (lane & 7) ^ ring_swz(row);
+            if (row < kSkBM) {
+                const int id = rid[row];
+                src[q] = (id >= 0 ? T + (size_t)id * F : W1) + chunk * 4;
+            } else {
+                src[q] = W1 + (size_t)(n0 + row - kSkBM) * F + chunk * 4;
+            }
+        }
+        v16f acc[2] = {(v16f){}, (v16f){}};
+        const int n = ke - ks;
+#define SK_STAGE(cur, nxt, s)                                                      \
+    do {                                                                           \
+        AMS_WAIT_VM(kSkPW);                                                        \
+        __builtin_amdgcn_s_barrier();                                              \
+        __builtin_amdgcn_sched_barrier(0);                                         \
+        sk_issue(nxt, src, (ks + min((s) + 2, n - 1)) * kSkBK, wave);              \
+        __builtin_amdgcn_sched_barrier(0);                                         \
+        sk_compute(cur, acc, lane, wave);                                          \
+    } while (0)
+        sk_issue(ring0, src, ks * kSkBK, wave);
+        sk_issue(ring1, src, (ks + min(1, n - 1)) * kSkBK, wave);
+        int s = 0;
+        for (; s + 3 <= n; s += 3) {
+            SK_STAGE(ring0, ring2, s);
+            SK_STAGE(ring1, ring0, s + 1);
+            SK_STAGE(ring2, ring1, s + 2);
+        }
+        if (s < n) SK_STAGE(ring0, ring2, s);
+        if (s + 1 < n) SK_STAGE(ring1, ring0, s + 1);
+#undef SK_STAGE
+        AMS_WAIT_VM(0);
+
+        const int wm = wave >> 1, wn = wave & 1, r32 = lane & 31;
+        if (ks == 0 && ke == S) {
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb) {
+                const int col = n0 + wn * 64 + nb * 32 + r32;
+                const float bias = b1[col];
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    const int r = wm * 32 + acc_row(j, lane);
+                    const float z = rid[r] >= 0 ? acc[nb][j] + bias : bias;
+                    if (m0 + r < n_u) H1[(size_t)(m0 + r) * H + col] = fmaxf(z, 0.f);
+                }
+            }
+        } else {
+            float *piece = pbuf + ((size_t)w * 2 + (first ? 0 : 1)) * kSkTile;
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+                for (int j = 0; j < 16; ++j)
+                    piece[(wm * 32 + acc_row(j, lane)) * kSkBN + wn * 64 + nb * 32 + r32] = acc[nb][j];
+        }
+        first = false;
+        it += n;
+    }
 }
 
 // bf16: same tiling with K step 64; lane l supplies k = 32*(l/32) + 8*i + e to
@@ -351,6 +544,17 @@ __device__ __forceinline__ float ld_w(const void *W, int bf16, size_t i)
     return bf16 ? ams_bf16_to_f32(((const uint16_t *)W)[i]) : ((const float *)W)[i];
 }
 
+// Four consecutive elements (index i, a multiple of 4) of a float32 or bf16 array.
+__device__ __forceinline__ float4 ld4_any(const void *p, int bf16, size_t i)
+{
+    if (bf16) {
+        const uint2 v = *(const uint2 *)((const uint16_t *)p + i);
+        return make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
+                           __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u));
+    }
+    return *(const float4 *)((const float *)p + i);
+}
+
 // Both tail kernels walk their unique images in chunks of 32 rows and run
 // the small contractions on fp32 MFMA (32x32x2) with operands in LDS.  Layer
 // widths: H = dims[1] (64..256, a multiple of 64), Mo = width of the second
@@ -361,9 +565,18 @@ constexpr int kTailLDo = kMaxH2 + 4;      // row stride of [row][o] tiles
 
 // Forward: Z2 = H1 W2^T + b2 for a chunk of 32 rows.  Wave w computes output
 // columns 32 (w & 1) .. +32 over the K half w >> 1; the two halves are added
-// in a fixed order.  Then H2 = ReLU(Z2) and, for 3 layers, E = H2 W3^T + b3.
+// in a fixed order.  Each lane keeps its W2 operands for the whole kernel in
+// registers (row o of W2, 16 consecutive k per 32-k block) and reads its H1
+// row straight from global memory, so only the small combine tiles use LDS.
+// Then H2 = ReLU(Z2) and, for 3 layers, E = H2 W3^T + b3.
+//
+// After the stream-K forward (sk != 0, H = 256) the K half of wave w is the
+// 128-column tile (row block, w >> 1) of layer 1.  If a worker finished that
+// tile in place its H1 is read as is; otherwise the wave adds the workers'
+// partial tiles in K order, applies b1 and ReLU (ReLU(b1) for a row whose ID
+// is out of range) and writes the finished H1 for the backward.
 template <int L>
-__global__ __launch_bounds__(kThreads) void tail_fwd(const float *__restrict__ H1, int H, int M,
+__global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int H, int M,
                                                       int D, const void *__restrict__ W2,
                                                       const float *__restrict__ b2,
                                                       const void *__restrict__ W3,
@@ -371,60 +584,112 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(const float *__restrict__ H
                                                       int final_relu,
                                                       const int32_t *__restrict__ n_uniq_p, int cap,
                                                       float *__restrict__ H2_save,
-                                                      float *__restrict__ E)
+                                                      float *__restrict__ E, int sk, int F, int G,
+                                                      const float *__restrict__ pbuf,
+                                                      const float *__restrict__ b1,
+                                                      const int32_t *__restrict__ uniq, int64_t n_rows)
 {
-    __shared__ __attribute__((aligned(16))) float W2s[kMaxH2 * kTailLD];     // [o][i]
-    __shared__ __attribute__((aligned(16))) float Hs[kTailRows * kTailLD];   // [row][i]
+    constexpr int KB = kMaxH1 / 2 / 32;       // 32-k blocks in a K half (at most 4)
     __shared__ float Zp[2][kTailRows][kMaxH2 + 1];
-    __shared__ float W3s[kMaxD * kMaxH2];
+    __shared__ float W3s[kMaxD * (kMaxH2 + 1)];
     __shared__ float h2s[kTailRows][kMaxH2 + 1];
     const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
     const int h = lane >> 5, r32 = lane & 31;
-    // M = width of the second layer's output (D for a 2-layer model)
-    for (int e = t; e < kMaxH2 * H; e += kThreads) {
-        const int o = e / H, i = e % H;
-        W2s[o * kTailLD + i] = o < M ? ld_w(W2, wbf16, (size_t)o * H + i) : 0.f;
-    }
+    const int kh = wave >> 1, nb = wave & 1, khalf = H / 2, nkb = khalf / 32;
+    const int o = nb * 32 + r32;              // this lane's B row (output column)
+    float4 breg[KB][4];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q)
+            breg[kb][q] = (kb < nkb && o < M)
+                              ? ld4_any(W2, wbf16, (size_t)o * H + kh * khalf + kb * 32 + 16 * h + 4 * q)
+                              : make_float4(0.f, 0.f, 0.f, 0.f);
     if (L == 3)
-        for (int e = t; e < D * M; e += kThreads) W3s[e] = ld_w(W3, wbf16, e);
+        for (int e = t; e < D * M; e += kThreads) W3s[(e / M) * (kMaxH2 + 1) + e % M] = ld_w(W3, wbf16, e);
     const int n_u = min(*n_uniq_p, cap);
     const bool relu_a = (L == 3) || final_relu;
-    const int kh = wave >> 1, nb = wave & 1, khalf = H / 2;
     for (int c0 = blockIdx.x * kTailRows; c0 < n_u; c0 += gridDim.x * kTailRows) {
-        __syncthreads();
-        for (int e = t; e < kTailRows * (H / 4); e += kThreads) {
-            const int r = e / (H / 4), q = e % (H / 4);
-            const float4 v = c0 + r < n_u ? *(const float4 *)(H1 + (size_t)(c0 + r) * H + 4 * q)
-                                          : make_float4(0.f, 0.f, 0.f, 0.f);
-            *(float4 *)&Hs[r * kTailLD + 4 * q] = v;
+        const int row = c0 + r32;
+        const int rowc = min(row, n_u - 1);
+        float *hrow = H1 + (size_t)rowc * H + kh * khalf + 16 * h;
+        float4 areg[KB][4];
+        // this wave's K half lies in one 128-column tile of the stream-K grid
+        const int cbase = kh * khalf;                    // first column of the half
+        const int cb = cbase / kSkBN;
+        int wa = 0, wb = -1, slot_a = 0;
+        if (sk) {
+            const SkPlan P = sk_plan(n_u, H, F, G);
+            const int tile = (rowc / kSkBM) * P.n_cb + cb;
+            wa = P.owner((int64_t)tile * P.S);
+            wb = P.owner((int64_t)(tile + 1) * P.S - 1);
+            // only the first contributor can hold this tile as its second piece
+            slot_a = (tile == (int)(P.it0(wa) / P.S)) ? 0 : 1;
         }
-        __syncthreads();
+        if (wb > wa) {
+            // tile cut by share boundaries: add the pieces in K order
+            const int id = uniq[rowc];
+            const bool ok = id >= 0 && (int64_t)id < n_rows;
+            const int rl = rowc % kSkBM;
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int col = cbase + kb * 32 + 16 * h + 4 * q;
+                    const int cl = col - cb * kSkBN;
+                    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+                    if (kb < nkb) {
+                        for (int w = wa; w <= wb; ++w) {
+                            const int sl = w == wa ? slot_a : 0;
+                            const float4 v =
+                                *(const float4 *)&pbuf[((size_t)w * 2 + sl) * kSkTile + rl * kSkBN + cl];
+                            a.x += v.x;
+                            a.y += v.y;
+                            a.z += v.z;
+                            a.w += v.w;
+                        }
+                        const float4 bb = *(const float4 *)&b1[col];
+                        a.x = fmaxf(ok ? a.x + bb.x : bb.x, 0.f);
+                        a.y = fmaxf(ok ? a.y + bb.y : bb.y, 0.f);
+                        a.z = fmaxf(ok ? a.z + bb.z : bb.z, 0.f);
+                        a.w = fmaxf(ok ? a.w + bb.w : bb.w, 0.f);
+                        if (nb == 0 && row < n_u) *(float4 *)(hrow + kb * 32 + 4 * q) = a;
+                    }
+                    areg[kb][q] = a;
+                }
+        } else {
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    areg[kb][q] = kb < nkb ? *(const float4 *)(hrow + kb * 32 + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
         v16f acc = (v16f){};
-        for (int k0 = kh * khalf; k0 < (kh + 1) * khalf; k0 += 32) {
-            float a[16], b[16];
-            const float *pa = &Hs[r32 * kTailLD + k0 + 16 * h];
-            const float *pb = &W2s[(nb * 32 + r32) * kTailLD + k0 + 16 * h];
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb) {
+            if (kb >= nkb) break;
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                *(float4 *)&a[4 * q] = *(const float4 *)(pa + 4 * q);
-                *(float4 *)&b[4 * q] = *(const float4 *)(pb + 4 * q);
+                acc = mfma_f32(areg[kb][q].x, breg[kb][q].x, acc);
+                acc = mfma_f32(areg[kb][q].y, breg[kb][q].y, acc);
+                acc = mfma_f32(areg[kb][q].z, breg[kb][q].z, acc);
+                acc = mfma_f32(areg[kb][q].w, breg[kb][q].w, acc);
             }
-#pragma unroll
-            for (int i = 0; i < 16; ++i) acc = mfma_f32(a[i], b[i], acc);
         }
+        __syncthreads();                       // previous chunk's readers of Zp / h2s are done
 #pragma unroll
-        for (int j = 0; j < 16; ++j) Zp[kh][acc_row(j, lane)][nb * 32 + r32] = acc[j];
+        for (int j = 0; j < 16; ++j) Zp[kh][acc_row(j, lane)][o] = acc[j];
         __syncthreads();
         for (int e = t; e < kTailRows * M; e += kThreads) {
-            const int r = e / M, o = e % M;
-            float z = Zp[0][r][o] + Zp[1][r][o] + b2[o];
+            const int r = e / M, oo = e % M;
+            float z = Zp[0][r][oo] + Zp[1][r][oo] + b2[oo];
             if (relu_a) z = fmaxf(z, 0.f);
-            h2s[r][o] = z;
+            h2s[r][oo] = z;
             if (c0 + r < n_u) {
                 if (L == 3) {
-                    if (H2_save) H2_save[(size_t)(c0 + r) * M + o] = z;
+                    if (H2_save) H2_save[(size_t)(c0 + r) * M + oo] = z;
                 } else {
-                    E[(size_t)(c0 + r) * M + o] = z;
+                    E[(size_t)(c0 + r) * M + oo] = z;
                 }
             }
         }
@@ -434,7 +699,7 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(const float *__restrict__ H
                 const int r = e / D, d = e % D;
                 if (c0 + r >= n_u) continue;
                 float v = b3[d];
-                for (int o = 0; o < M; ++o) v += W3s[d * M + o] * h2s[r][o];
+                for (int oo = 0; oo < M; ++oo) v += W3s[d * (kMaxH2 + 1) + oo] * h2s[r][oo];
                 if (final_relu) v = fmaxf(v, 0.f);
                 E[(size_t)(c0 + r) * D + d] = v;
             }
@@ -460,9 +725,12 @@ __global__ __launch_bounds__(kThreads) void tail_bwd(const void *__restrict__ H1
                                                       int H, int M, int D, int final_relu,
                                                       const int32_t *__restrict__ n_uniq_p, int cap,
                                                       void *__restrict__ dZ1, int dz1_bf16,
-                                                      float *__restrict__ part, int PS)
+                                                      float *__restrict__ part, int PS,
+                                                      float *__restrict__ zero_row, int zero_n)
 {
-    __shared__ __attribute__((aligned(16))) float W2t[kMaxH1 * kTailLDo];    // [i][o]
+    // the zero row that dW1's padding rows stream (read by the next launch)
+    if (blockIdx.x == 0)
+        for (int i = threadIdx.x; i < zero_n; i += kThreads) zero_row[i] = 0.f;
     __shared__ __attribute__((aligned(16))) float Hc[kTailRows * kTailLD];   // [row][i]
     __shared__ __attribute__((aligned(16))) float dz2s[kTailRows * kTailLDo];// [row][o]
     __shared__ float W3s[kMaxD * kMaxH2];
@@ -471,19 +739,27 @@ __global__ __launch_bounds__(kThreads) void tail_bwd(const void *__restrict__ H1
     const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
     const int h = lane >> 5, r32 = lane & 31;
     const int Mo = (L == 3) ? M : D;
-    for (int e = t; e < kMaxH2 * H; e += kThreads) {
-        const int o = e / H, i = e % H;
-        W2t[i * kTailLDo + o] = o < Mo ? ld_w(W2, wbf16, (size_t)o * H + i) : 0.f;
-    }
+    // this wave's share of H: columns [64 wave, 64 wave + 64) (H <= 256)
+    const int i0 = 64 * wave;
+    const bool wave_on = i0 < H;
+    // B operand of dH1 = dZ2 W2, kept in registers: W2[o][i] for this lane's
+    // column i and o = k0 + 16 h + e (k0 = 0, 32; e = 0..15; o >= Mo reads 0)
+    float w2r[2][2][16];
+#pragma unroll
+    for (int nb = 0; nb < 2; ++nb)
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) {
+                const int o = kb * 32 + 16 * h + e, i = i0 + nb * 32 + r32;
+                w2r[nb][kb][e] = (wave_on && o < Mo) ? ld_w(W2, wbf16, (size_t)o * H + i) : 0.f;
+            }
     if (L == 3)
         for (int e = t; e < D * M; e += kThreads) W3s[e] = ld_w(W3, wbf16, e);
     const int n_u = min(*n_uniq_p, cap);
     const int r0 = (int)((int64_t)blockIdx.x * n_u / gridDim.x);
     const int r1 = (int)((int64_t)(blockIdx.x + 1) * n_u / gridDim.x);
 
-    // this wave's share of H: columns [64 wave, 64 wave + 64) (H <= 256)
-    const int i0 = 64 * wave;
-    const bool wave_on = i0 < H;
     v16f dw2[2][2];                          // [o block][i block]
 #pragma unroll
     for (int a = 0; a < 2; ++a)
@@ -497,15 +773,11 @@ __global__ __launch_bounds__(kThreads) void tail_bwd(const void *__restrict__ H1
 
     for (int c0 = r0; c0 < r1; c0 += kTailRows) {
         __syncthreads();
-        for (int e = t; e < kTailRows * H; e += kThreads) {
-            const int r = e / H, i = e % H;
-            float v = 0.f;
-            if (c0 + r < r1) {
-                const size_t x = (size_t)(c0 + r) * H + i;
-                v = h1_bf16 ? ams_bf16_to_f32(((const uint16_t *)H1s)[x]) : ((const float *)H1s)[x];
-            }
-            Hc[r * kTailLD + i] = v;
-        }
+        for (int r = wave; r < kTailRows; r += kThreads / AMS_WAVE)
+            for (int c = lane; c < H / 4; c += AMS_WAVE)
+                *(float4 *)&Hc[r * kTailLD + 4 * c] =
+                    c0 + r < r1 ? ld4_any(H1s, h1_bf16, (size_t)(c0 + r) * H + 4 * c)
+                                : make_float4(0.f, 0.f, 0.f, 0.f);
         for (int e = t; e < kTailRows * D; e += kThreads) {
             const int r = e / D, d = e % D;
             float g = 0.f;
@@ -523,7 +795,7 @@ __global__ __launch_bounds__(kThreads) void tail_bwd(const void *__restrict__ H1
         __syncthreads();
         // dZ2, db2 (thread o), dW3 / db3 (vector units)
         for (int e = t; e < kTailRows * kMaxH2; e += kThreads) {
-            const int r = e / kMaxH2, o = e % kMaxH2;
+            const int r = e >> 6, o = e & (kMaxH2 - 1);
             float dz = 0.f;
             if (o < Mo) {
                 if (L == 3) {
@@ -563,21 +835,15 @@ __global__ __launch_bounds__(kThreads) void tail_bwd(const void *__restrict__ H1
             // dH1 = dZ2 W2 : rows x [i0, i0 + 64), K = 64 (padded o)
             v16f acc[2] = {(v16f){}, (v16f){}};
 #pragma unroll
-            for (int k0 = 0; k0 < kMaxH2; k0 += 32) {
-                float a[16], b[2][16];
-                const float *pa = &dz2s[r32 * kTailLDo + k0 + 16 * h];
+            for (int kb = 0; kb < 2; ++kb) {
+                float a[16];
+                const float *pa = &dz2s[r32 * kTailLDo + kb * 32 + 16 * h];
 #pragma unroll
                 for (int q = 0; q < 4; ++q) *(float4 *)&a[4 * q] = *(const float4 *)(pa + 4 * q);
 #pragma unroll
-                for (int nb = 0; nb < 2; ++nb) {
-                    const float *pb = &W2t[(i0 + nb * 32 + r32) * kTailLDo + k0 + 16 * h];
-#pragma unroll
-                    for (int q = 0; q < 4; ++q) *(float4 *)&b[nb][4 * q] = *(const float4 *)(pb + 4 * q);
-                }
-#pragma unroll
                 for (int i = 0; i < 16; ++i)
 #pragma unroll
-                    for (int nb = 0; nb < 2; ++nb) acc[nb] = mfma_f32(a[i], b[nb][i], acc[nb]);
+                    for (int nb = 0; nb < 2; ++nb) acc[nb] = mfma_f32(a[i], w2r[nb][kb][i], acc[nb]);
             }
             // dZ1 = dH1 * [H1 > 0]; write it out and sum it per column for db1
 #pragma unroll
@@ -648,15 +914,24 @@ __global__ __launch_bounds__(kThreads) void tail_bwd(const void *__restrict__ H1
     }
 }
 
-// out[e] = sum over g = 0..G-1 (in order) of part[g * PS + e].
+// out[e] = sum of part[g * PS + e] over g = 0..G-1, in a fixed association:
+// eight running sums over g = 8i + r, added r = 0..7 at the end (the eight
+// independent load chains keep the reads in flight).
 __global__ __launch_bounds__(kThreads) void partial_reduce(const float *__restrict__ part, int G,
                                                            size_t PS, float *__restrict__ out)
 {
     const size_t e = (size_t)blockIdx.x * kThreads + threadIdx.x;
     if (e >= PS) return;
-    float s = 0.f;
-    for (int g = 0; g < G; ++g) s += part[(size_t)g * PS + e];
-    out[e] = s;
+    float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    int g = 0;
+    for (; g + 8 <= G; g += 8)
+#pragma unroll
+        for (int r = 0; r < 8; ++r) s[r] += part[(size_t)(g + r) * PS + e];
+    for (int r = 0; g + r < G; ++r) s[r] += part[(size_t)(g + r) * PS + e];
+    float tot = 0.f;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) tot += s[r];
+    out[e] = tot;
 }
 
 // Scatter the reduced tail partials into the caller's gradient arrays.
@@ -858,21 +1133,31 @@ __device__ __forceinline__ void dw1_issue(float *slot, const float *__restrict__
     }
 }
 
+// 16 MFMA steps of 2 k per stage; step kk needs one B and two A values per
+// lane.  Reads run two steps ahead of the MFMAs (sched_group_barrier fixes
+// the interleave), so the 4-byte LDS reads are never waited on.
 __device__ __forceinline__ void dw1_compute(const float *slot, v16f *acc, int lane, int wave)
 {
     const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
     const float *A = slot, *B = slot + DwRing::A_FLOATS;
+    float av[DwRing::BK / 2][2], bv[DwRing::BK / 2];
 #pragma unroll
     for (int kk = 0; kk < DwRing::BK / 2; ++kk) {
         const int k = 2 * kk + h;
         const int sw = dw_chunk_swz(k) << 2;
-        const int n = wn * 32 + r32;
-        const float bv = B[k * DwRing::BN + (n ^ sw)];
+        bv[kk] = B[k * DwRing::BN + ((wn * 32 + r32) ^ sw)];
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-            const int m = wm * 64 + mb * 32 + r32;
-            acc[mb] = mfma_f32(A[k * DwRing::BM + (m ^ sw)], bv, acc[mb]);
-        }
+        for (int mb = 0; mb < 2; ++mb) av[kk][mb] = A[k * DwRing::BM + ((wm * 64 + mb * 32 + r32) ^ sw)];
+    }
+#pragma unroll
+    for (int kk = 0; kk < DwRing::BK / 2; ++kk)
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) acc[mb] = mfma_f32(av[kk][mb], bv[kk], acc[mb]);
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+#pragma unroll
+    for (int kk = 0; kk < DwRing::BK / 2; ++kk) {
+        if (kk + 2 < DwRing::BK / 2) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
     }
 }
 
@@ -973,7 +1258,7 @@ int dw1_chunks(int H, int F)
 {
     const int bm = (H % 128 == 0) ? 128 : 64;
     const int tiles = (H / bm) * (F / 64);
-    int kc = 2048 / tiles;
+    int kc = 1024 / tiles;
     return kc < 1 ? 1 : (kc > 32 ? 32 : kc);
 }
 
@@ -1005,19 +1290,28 @@ BwdPlan plan_bwd(const ams_mlp *m, int32_t cap)
     return p;
 }
 
-// Forward workspace: [zero row, max(F, H) floats][H1 fp32, cap x H (when the
-// caller gives no fp32 H1_save)].
-size_t zero_row_bytes(const ams_mlp *m)
+// Stream-K workers: one per compute unit of the current device (a multiple
+// of 8, the XCD count), 256 on MI355X.
+int sk_workers()
 {
-    return al256((size_t)(m->dims[0] > m->dims[1] ? m->dims[0] : m->dims[1]) * 4);
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 8)
+        n = 256;
+    return (n / 8) * 8;
 }
+
+bool use_stream_k(const ams_mlp *m) { return m->dtype == AMS_F32 && m->dims[1] % kSkBN == 0; }
 
 }  // namespace
 
 extern "C" size_t ams_embed_workspace(const ams_mlp *mlp, int32_t n_uniq_cap)
 {
     if (!mlp_ok(mlp) || n_uniq_cap < 0) return 0;
-    const size_t fwd = zero_row_bytes(mlp) + al256((size_t)n_uniq_cap * mlp->dims[1] * 4);
+    // forward: fp32 H1 (bf16 mode, or when the caller keeps no fp32 H1_save),
+    // then the stream-K partial tiles (two per worker)
+    size_t fwd = al256((size_t)n_uniq_cap * mlp->dims[1] * 4);
+    if (use_stream_k(mlp)) fwd += al256((size_t)sk_workers() * 2 * kSkTile * 4);
     const size_t bwd = plan_bwd(mlp, n_uniq_cap).total;
     return fwd > bwd ? fwd : bwd;
 }
@@ -1041,23 +1335,28 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
     const int M = (L == 3) ? mlp->dims[2] : D;
     const bool bf = mlp->dtype == AMS_BF16;
     const bool h1_in_ws = bf || !H1_save;
-    const size_t zb = zero_row_bytes(mlp);
-    if (!ws || ws_bytes < zb + (h1_in_ws ? al256((size_t)cap * H * 4) : 0)) return AMS_ERR_WORKSPACE;
+    const bool sk = use_stream_k(mlp);
+    const int G = sk ? sk_workers() : 0;
+    const size_t h1_bytes = al256((size_t)cap * H * 4);
+    const size_t need = h1_bytes + (sk ? al256((size_t)G * 2 * kSkTile * 4) : 0);
+    if ((h1_in_ws || sk) && (!ws || ws_bytes < need)) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
-    float *zero = (float *)ws;
-    float *H1f = h1_in_ws ? (float *)((char *)ws + zb) : (float *)H1_save;
-    fill_zero<<<4, kThreads, 0, st>>>(zero, (int)(zb / 4));
+    float *H1f = h1_in_ws ? (float *)ws : (float *)H1_save;
+    float *pbuf = (float *)((char *)ws + h1_bytes);
 
     const int n_mt = (cap + 63) / 64;
     const int NT = (H % 128 == 0) ? 128 : 64;
     const int grid = ((n_mt + 7) / 8) * 8 * (H / NT);
-    if (!bf) {
+    if (sk) {
+        l1sk_f32<<<G, kSkThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, (const float *)W1, b1,
+                                           H, G, H1f, pbuf);
+    } else if (!bf) {
         if (NT == 128)
             l1_fwd_f32<128><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, n_mt,
-                                                       (const float *)W1, b1, H, zero, H1f);
+                                                       (const float *)W1, b1, H, H1f);
         else
             l1_fwd_f32<64><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, n_mt,
-                                                      (const float *)W1, b1, H, zero, H1f);
+                                                      (const float *)W1, b1, H, H1f);
     } else {
         if (NT == 128)
             l1_fwd_bf16<128><<<grid, kThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq, n_uniq,
@@ -1069,13 +1368,13 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
                                                        (uint16_t *)H1_save);
     }
     int tg = (cap + kTailRows - 1) / kTailRows;
-    if (tg > 256) tg = 256;
+    if (tg > 1024) tg = 1024;
     if (L == 3)
         tail_fwd<3><<<tg, kThreads, 0, st>>>(H1f, H, M, D, W2, b2, W3, b3, bf, mlp->final_relu, n_uniq,
-                                             cap, H2_save, E);
+                                             cap, H2_save, E, sk, F, G, pbuf, b1, uniq, n_rows);
     else
         tail_fwd<2><<<tg, kThreads, 0, st>>>(H1f, H, M, D, W2, b2, W3, b3, bf, mlp->final_relu, n_uniq,
-                                             cap, H2_save, E);
+                                             cap, H2_save, E, sk, F, G, pbuf, b1, uniq, n_rows);
     return ams_launch_status();
 }
 
@@ -1113,10 +1412,12 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
 
     if (L == 3)
         tail_bwd<3><<<kTailBlocks, kThreads, 0, st>>>(H1_save, bf, H2_save, E_fwd, dE, W2, W3, bf, H, M, D,
-                                                      mlp->final_relu, n_uniq, cap, dz1, bf, tail, PS);
+                                                      mlp->final_relu, n_uniq, cap, dz1, bf, tail, PS,
+                                                      zero, F > H ? F : H);
     else
         tail_bwd<2><<<kTailBlocks, kThreads, 0, st>>>(H1_save, bf, H2_save, E_fwd, dE, W2, W3, bf, H, M, D,
-                                                      mlp->final_relu, n_uniq, cap, dz1, bf, tail, PS);
+                                                      mlp->final_relu, n_uniq, cap, dz1, bf, tail, PS,
+                                                      zero, F > H ? F : H);
     partial_reduce<<<(PS + kThreads - 1) / kThreads, kThreads, 0, st>>>(tail, kTailBlocks, (size_t)PS,
                                                                          tailsum);
     tail_unpack<<<(PS + kThreads - 1) / kThreads, kThreads, 0, st>>>(tailsum, L, H, M, D, dW2, db2,
@@ -1125,7 +1426,6 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
     const int bm = (H % 128 == 0) ? 128 : 64;
     const int nmt = H / bm, outer = (F / 64) * p.kc;
     const int grid = ((outer + 7) / 8) * 8 * nmt;
-    fill_zero<<<4, kThreads, 0, st>>>(zero, F > H ? F : H);
     if (!bf && bm == 128) {
         dw1_part_f32<<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
                                                 (const float *)dz1, H, p.kc, zero, dw1p);
