@@ -115,8 +115,9 @@ const char *ams_build_info(void);
  * dev_status[1]     out: AMS_OK, or AMS_ERR_ID_RANGE if some ID is out of range.
  * ws, ws_bytes      workspace of at least ams_dedup_workspace(n_occ, n_ids) bytes.
  * n_occ == 0 is valid (n_u = 0).  Host errors: NULL, SIZE (n_occ < 0,
- * n_occ > 2^31 - 2, n_ids < 1), WORKSPACE.  Outputs are bit-exact: they are
- * the unique canonical answer. */
+ * n_occ > 2^30 - 1, n_ids < 1), WORKSPACE.  Outputs are bit-exact: they are
+ * the unique canonical answer.  *dev_status = AMS_ERR_HIP reports an internal
+ * wait that did not complete (outputs then unspecified). */
 size_t ams_dedup_workspace(int64_t n_occ, int32_t n_ids);
 ams_status ams_dedup(const int32_t *ids, int64_t n_occ, int32_t n_ids,
                      int32_t *uniq, int32_t *inv, int32_t *occ_perm,

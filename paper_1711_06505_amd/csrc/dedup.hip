@@ -5,118 +5,219 @@
 //
 // Method: a stable LSD radix sort of (ID, occurrence index) over the
 // ceil(log2 n_ids) significant bits, at most 8 bits per pass, then head flags
-// and an exclusive scan give the unique set, its CSR offsets and the inverse.
+// and a scan give the unique set, its CSR offsets and the inverse index.
 //
-// Per radix pass three kernels run: a per-tile digit histogram, one exclusive
-// scan over the digit-major [digit][tile] counts, and a scatter in which every
-// wave ranks its keys with 64-lane ballots (lanes holding the same digit find
-// each other bit by bit) and running per-wave digit counters in LDS.  Tiles,
-// waves, rows and lanes are visited in index order, so the sort is stable and
-// the result bit-exact.
+// Kernels (P = number of radix passes):
+//   dd_prep        global digit histograms of every pass in one read of the
+//                  IDs (per-block partials, no atomics across blocks), the ID
+//                  range check, and zeroing of the look-back words;
+//   dd_pass  x P   per 2048-key tile: local ranks from 64-lane ballots (lanes
+//                  holding the same digit find each other bit by bit) and
+//                  per-wave running counters in LDS; the tile's position among
+//                  earlier tiles comes from decoupled look-back over the
+//                  per-tile digit counts they publish; then a stable scatter;
+//   dd_unique      head flags of the sorted keys, rank by the same look-back,
+//                  and the outputs.
+// Tiles, waves, rows and lanes are visited in index order, so the sort is
+// stable and every output bit-exact.  A tile only waits for earlier tiles to
+// publish, and blocks are dispatched in index order, so every wait ends.
 #include "ams_device.h"
 
 namespace {
 
 constexpr int kThreads = 256;                 // 4 waves
+constexpr int kWaves = kThreads / AMS_WAVE;
 constexpr int kRows = 8;                      // rows of 64 keys per wave
 constexpr int kTile = kThreads * kRows;       // 2048 keys per tile
 constexpr int kMaxBits = 8;
-constexpr int kUniqItems = 8;                 // positions per thread, unique pass
-constexpr int kUniqTile = kThreads * kUniqItems;
-constexpr int kScanThreads = 1024;
+constexpr int kRadix = 1 << kMaxBits;
+constexpr int kMaxPasses = 4;
+constexpr int kPrepBlocks = 32;                // partial histograms a pass sums
 
-__global__ void dd_init(int32_t *n_uniq, int32_t *dev_status, int32_t *uniq_off, int n_occ)
+// look-back words: 2-bit state in the top bits, count below
+constexpr uint32_t kAgg = 1u << 30;           // this tile's own count is published
+constexpr uint32_t kPrefix = 2u << 30;        // the inclusive prefix up to this tile
+constexpr uint32_t kValMask = (1u << 30) - 1;
+constexpr int64_t kMaxOcc = (1 << 30) - 1;    // prefix counts stay below the state bits
+
+__device__ __forceinline__ uint32_t ld_relaxed(const uint32_t *p)
 {
-    if (threadIdx.x == 0 && blockIdx.x == 0) {
-        *dev_status = AMS_OK;
-        *n_uniq = 0;
-        if (n_occ == 0) uniq_off[0] = 0;
-    }
+    return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// Per-tile histogram of one digit; the first pass also range-checks the IDs.
-__global__ __launch_bounds__(kThreads) void dd_hist(const uint32_t *__restrict__ keys, int n,
-                                                    int shift, int bits, int32_t *__restrict__ hist,
-                                                    int ntiles, uint32_t n_ids,
-                                                    int32_t *__restrict__ dev_status, int check)
+// The look-back words carry everything they communicate (no other data is
+// published through them), so relaxed device-scope atomics suffice; they go
+// around the per-XCD caches without the cache write-back/invalidate that
+// release/acquire ordering would add.
+__device__ __forceinline__ void st_relaxed(uint32_t *p, uint32_t v)
 {
-    __shared__ int h[1 << kMaxBits];
+    __hip_atomic_store(p, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Exclusive prefix of this tile's count over all earlier tiles (decoupled
+// look-back).  words[t * stride] is this tile's word, earlier tiles' words at
+// words[(t - 1) * stride], ...; with stride = the radix, the threads of a
+// block (one digit each) read consecutive words.  Publishes the aggregate
+// first, then the inclusive prefix.  Every tile publishes before it waits, so
+// each wait ends; the wait is nevertheless bounded (kSpinLimit re-reads), and
+// a bound that is hit is recorded in *err instead of spinning on.
+constexpr int kSpinLimit = 1 << 22;
+
+__device__ uint32_t lookback(uint32_t *words, int stride, int t, uint32_t count, int32_t *err)
+{
+    if (t == 0) {
+        st_relaxed(&words[0], kPrefix | count);
+        return 0;
+    }
+    st_relaxed(&words[(size_t)t * stride], kAgg | count);
+    // walk back in batches of independent reads (one round trip each)
+    constexpr int kBatch = 32;
+    uint32_t excl = 0;
+    int spins = 0;
+    for (int hi = t - 1; hi >= 0;) {
+        const int nb = hi + 1 < kBatch ? hi + 1 : kBatch;
+        uint32_t w[kBatch];
+        bool ready = true;
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) {
+            w[i] = i < nb ? ld_relaxed(&words[(size_t)(hi - i) * stride]) : kPrefix;
+            ready &= (w[i] & ~kValMask) != 0;
+        }
+        if (!ready) {                             // some tile of the batch has not published
+            if (++spins < kSpinLimit) continue;
+            *err = 1;
+            break;
+        }
+        spins = 0;
+        bool done = false;
+#pragma unroll
+        for (int i = 0; i < kBatch; ++i) {
+            if (done || i >= nb) continue;
+            excl += w[i] & kValMask;
+            done = (w[i] & ~kValMask) == kPrefix;
+        }
+        if (done) break;
+        hi -= nb;
+    }
+    st_relaxed(&words[(size_t)t * stride], kPrefix | (excl + count));
+    return excl;
+}
+
+// The same look-back walked by one whole wave: lane i reads the word of tile
+// (hi - i), so 64 earlier tiles cost one round trip.  The lowest lane holding
+// an inclusive prefix is the nearest one; the sum runs up to it.
+__device__ uint32_t lookback_wave(uint32_t *words, int t, uint32_t count, int32_t *err)
+{
+    const int lane = ams_lane();
+    if (t == 0) {
+        if (lane == 0) st_relaxed(&words[0], kPrefix | count);
+        return 0;
+    }
+    if (lane == 0) st_relaxed(&words[t], kAgg | count);
+    uint32_t excl = 0;
+    int spins = 0;
+    for (int hi = t - 1; hi >= 0;) {
+        const int j = hi - lane;
+        const uint32_t w = j >= 0 ? ld_relaxed(&words[j]) : kPrefix;   // before tile 0: prefix 0
+        if (ams_ballot((w & ~kValMask) == 0) != 0) {                   // not all published yet
+            if (++spins < kSpinLimit) continue;
+            if (lane == 0) *err = 1;
+            break;
+        }
+        spins = 0;
+        const uint64_t pre = ams_ballot((w & ~kValMask) == kPrefix);
+        const int stop = pre ? __ffsll((unsigned long long)pre) - 1 : AMS_WAVE - 1;
+        const int v = lane <= stop ? (int)(w & kValMask) : 0;
+        excl += (uint32_t)__shfl(ams_wave_incl_scan(v), AMS_WAVE - 1, AMS_WAVE);
+        if (pre) break;
+        hi -= AMS_WAVE;
+    }
+    if (lane == 0) st_relaxed(&words[t], kPrefix | (excl + count));
+    return excl;
+}
+
+struct Plan {
+    int bits, passes, width, ntiles;
+};
+
+__device__ __forceinline__ int pass_bits(const Plan &P, int pass)
+{
+    const int shift = pass * P.width;
+    return (P.bits - shift) < P.width ? (P.bits - shift) : P.width;
+}
+
+// Global digit histograms (partials per prep block), range check, zeroing.
+__global__ __launch_bounds__(kThreads) void dd_prep(const uint32_t *__restrict__ keys, int n, Plan P,
+                                                    uint32_t n_ids, int32_t *__restrict__ hpart,
+                                                    int32_t *__restrict__ bad,
+                                                    uint32_t *__restrict__ words, int n_words)
+{
+    __shared__ int h[kMaxPasses][kRadix];
     const int t = threadIdx.x;
-    const uint32_t mask = (1u << bits) - 1u;
-    h[t] = 0;
+    for (int p = 0; p < kMaxPasses; ++p) h[p][t] = 0;
+    for (int i = blockIdx.x * kThreads + t; i < n_words; i += gridDim.x * kThreads) words[i] = 0;
     __syncthreads();
-    const int base = blockIdx.x * kTile;
-    bool bad = false;
-    for (int i = t; i < kTile; i += kThreads) {
-        const int idx = base + i;
-        if (idx < n) {
-            const uint32_t k = keys[idx];
-            bad |= (k >= n_ids);
-            atomicAdd(&h[(k >> shift) & mask], 1);
+    bool out = false;
+    for (int i = blockIdx.x * kThreads + t; i < n; i += gridDim.x * kThreads) {
+        const uint32_t k = keys[i];
+        out |= (k >= n_ids);
+        for (int p = 0; p < P.passes; ++p) {
+            const uint32_t mask = (1u << pass_bits(P, p)) - 1u;
+            atomicAdd(&h[p][(k >> (p * P.width)) & mask], 1);
         }
     }
-    if (check && bad) *dev_status = AMS_ERR_ID_RANGE;
-    __syncthreads();
-    if (t < (1 << bits)) hist[t * ntiles + blockIdx.x] = h[t];
+    const int any_out = __syncthreads_or(out);
+    for (int p = 0; p < P.passes; ++p) hpart[((size_t)blockIdx.x * kMaxPasses + p) * kRadix + t] = h[p][t];
+    if (t == 0) bad[blockIdx.x] = any_out;
 }
 
-// Exclusive scan of len ints in place by one workgroup; *total (optional)
-// receives the sum.  Each thread owns one contiguous run.
-__global__ __launch_bounds__(kScanThreads) void dd_scan(int32_t *__restrict__ a, int len,
-                                                        int32_t *__restrict__ total)
+// One stable radix pass.  vin == nullptr means the identity (first pass).
+__global__ __launch_bounds__(kThreads) void dd_pass(const uint32_t *__restrict__ kin,
+                                                    const int32_t *__restrict__ vin,
+                                                    uint32_t *__restrict__ kout, int32_t *__restrict__ vout,
+                                                    int n, Plan P, int pass,
+                                                    const int32_t *__restrict__ hpart, int n_prep,
+                                                    uint32_t *__restrict__ words, int32_t *__restrict__ err)
 {
-    __shared__ int wsum[kScanThreads / AMS_WAVE];
-    const int t = threadIdx.x;
-    const int per = (len + kScanThreads - 1) / kScanThreads;
-    const int lo = min(len, t * per), hi = min(len, lo + per);
-    int s = 0;
-    for (int i = lo; i < hi; ++i) s += a[i];
-    const int incl = ams_wave_incl_scan(s);
-    const int w = t / AMS_WAVE;
-    if (ams_lane() == AMS_WAVE - 1) wsum[w] = incl;
-    __syncthreads();
-    if (t < AMS_WAVE) {
-        int v = t < kScanThreads / AMS_WAVE ? wsum[t] : 0;
-        int vi = ams_wave_incl_scan(v);
-        if (t < kScanThreads / AMS_WAVE) wsum[t] = vi - v;   // exclusive per wave
-        if (t == kScanThreads / AMS_WAVE - 1 && total) *total = vi;
-    }
-    __syncthreads();
-    int run = wsum[w] + incl - s;
-    for (int i = lo; i < hi; ++i) {
-        const int v = a[i];
-        a[i] = run;
-        run += v;
-    }
-}
-
-// Stable scatter of one radix pass.  vals_in == nullptr means the identity
-// (occurrence index) for the first pass.
-__global__ __launch_bounds__(kThreads) void dd_scatter(const uint32_t *__restrict__ kin,
-                                                       const int32_t *__restrict__ vin,
-                                                       uint32_t *__restrict__ kout,
-                                                       int32_t *__restrict__ vout, int n, int shift,
-                                                       int bits, const int32_t *__restrict__ offs,
-                                                       int ntiles)
-{
-    __shared__ int cnt[kThreads / AMS_WAVE][1 << kMaxBits];
-    __shared__ int woff[kThreads / AMS_WAVE][1 << kMaxBits];
+    __shared__ int cnt[kWaves][kRadix];
+    __shared__ int scan_tmp[kWaves];
     const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
+    const int shift = pass * P.width, bits = pass_bits(P, pass);
     const uint32_t mask = (1u << bits) - 1u;
-    for (int d = lane; d < (1 << kMaxBits); d += AMS_WAVE) cnt[wave][d] = 0;
-    __syncthreads();
-
-    const int base = blockIdx.x * kTile + wave * (kRows * AMS_WAVE);
+    const int tbase = blockIdx.x * kTile + wave * (kRows * AMS_WAVE);
     const uint64_t lt = ams_lanemask_lt();
     uint32_t key[kRows];
     int32_t val[kRows];
     int rank[kRows];
+    // every load of the block first, all independent (one memory round trip):
+    // the tile's keys and values (clamped, branch-free), then this pass's
+    // per-block digit partials
 #pragma unroll
     for (int r = 0; r < kRows; ++r) {
-        const int idx = base + r * AMS_WAVE + lane;
+        const int idx = min(tbase + r * AMS_WAVE + lane, n - 1);
+        key[r] = kin[idx];
+        val[r] = vin ? vin[idx] : idx;
+    }
+    int part[kPrepBlocks];
+#pragma unroll
+    for (int b = 0; b < kPrepBlocks; ++b)
+        part[b] = hpart[((size_t)min(b, n_prep - 1) * kMaxPasses + pass) * kRadix + t];
+    for (int d = lane; d < kRadix; d += AMS_WAVE) cnt[wave][d] = 0;
+
+    // global exclusive digit offsets of this pass (the same in every tile)
+    int tot = 0;
+#pragma unroll
+    for (int b = 0; b < kPrepBlocks; ++b) tot += b < n_prep ? part[b] : 0;
+    const int incl = ams_wave_incl_scan(tot);
+    if (lane == AMS_WAVE - 1) scan_tmp[wave] = incl;
+    __syncthreads();
+    int gbase = incl - tot;
+    for (int w = 0; w < wave; ++w) gbase += scan_tmp[w];
+
+#pragma unroll
+    for (int r = 0; r < kRows; ++r) {
+        const int idx = tbase + r * AMS_WAVE + lane;
         const bool valid = idx < n;
-        key[r] = valid ? kin[idx] : 0u;
-        val[r] = valid ? (vin ? vin[idx] : idx) : 0;
         const uint32_t d = (key[r] >> shift) & mask;
         uint64_t peers = ams_ballot(valid);
         for (int b = 0; b < bits; ++b) {
@@ -134,66 +235,53 @@ __global__ __launch_bounds__(kThreads) void dd_scatter(const uint32_t *__restric
         __builtin_amdgcn_wave_barrier();
     }
     __syncthreads();
-    if (t < (1 << bits)) {
-        int run = offs[t * ntiles + blockIdx.x];
-#pragma unroll
-        for (int w = 0; w < kThreads / AMS_WAVE; ++w) {
-            woff[w][t] = run;
-            run += cnt[w][t];
-        }
+    // this tile's count of digit t, and its position among earlier tiles
+    int tile_cnt = 0;
+    for (int w = 0; w < kWaves; ++w) tile_cnt += cnt[w][t];
+    uint32_t before = 0;
+    if (t < (1 << bits))
+        before = lookback(words + ((size_t)pass * P.ntiles) * kRadix + t, kRadix, blockIdx.x,
+                          (uint32_t)tile_cnt, err);
+    // wave offsets inside the tile
+    int run = gbase + (int)before;
+    for (int w = 0; w < kWaves; ++w) {
+        const int c = cnt[w][t];
+        cnt[w][t] = run;
+        run += c;
     }
     __syncthreads();
 #pragma unroll
     for (int r = 0; r < kRows; ++r) {
-        const int idx = base + r * AMS_WAVE + lane;
+        const int idx = tbase + r * AMS_WAVE + lane;
         if (idx < n) {
             const uint32_t d = (key[r] >> shift) & mask;
-            const int pos = woff[wave][d] + rank[r];
+            const int pos = cnt[wave][d] + rank[r];
             kout[pos] = key[r];
             vout[pos] = val[r];
         }
     }
 }
 
-// Head flags of the sorted keys, counted per tile.
-__global__ __launch_bounds__(kThreads) void dd_head_count(const uint32_t *__restrict__ k, int n,
-                                                          int32_t *__restrict__ bsum)
+// Unique set, CSR offsets, stable occurrence order, inverse index, count.
+__global__ __launch_bounds__(kThreads) void dd_unique(const uint32_t *__restrict__ k,
+                                                      const int32_t *__restrict__ v, int n,
+                                                      uint32_t *__restrict__ words, int32_t *__restrict__ err,
+                                                      const int32_t *__restrict__ bad, int n_prep,
+                                                      int32_t *__restrict__ uniq, int32_t *__restrict__ inv,
+                                                      int32_t *__restrict__ occ_perm,
+                                                      int32_t *__restrict__ uniq_off,
+                                                      int32_t *__restrict__ n_uniq,
+                                                      int32_t *__restrict__ dev_status)
 {
-    __shared__ int ws[kThreads / AMS_WAVE];
-    const int t = threadIdx.x;
-    const int i0 = blockIdx.x * kUniqTile + t * kUniqItems;
-    int c = 0;
-#pragma unroll
-    for (int q = 0; q < kUniqItems; ++q) {
-        const int i = i0 + q;
-        if (i < n) c += (i == 0 || k[i] != k[i - 1]) ? 1 : 0;
-    }
-    const int incl = ams_wave_incl_scan(c);
-    if (ams_lane() == AMS_WAVE - 1) ws[t / AMS_WAVE] = incl;
-    __syncthreads();
-    if (t == 0) {
-        int s = 0;
-        for (int w = 0; w < kThreads / AMS_WAVE; ++w) s += ws[w];
-        bsum[blockIdx.x] = s;
-    }
-}
-
-// Unique set, CSR offsets, stable occurrence order and inverse index.
-__global__ __launch_bounds__(kThreads) void dd_finalize(const uint32_t *__restrict__ k,
-                                                        const int32_t *__restrict__ v, int n,
-                                                        const int32_t *__restrict__ boff,
-                                                        int32_t *__restrict__ uniq,
-                                                        int32_t *__restrict__ inv,
-                                                        int32_t *__restrict__ occ_perm,
-                                                        int32_t *__restrict__ uniq_off)
-{
-    __shared__ int ws[kThreads / AMS_WAVE];
+    constexpr int kItems = kTile / kThreads;  // 8 consecutive positions per thread
+    __shared__ int ws[kWaves];
+    __shared__ uint32_t tile_base;
     const int t = threadIdx.x, w = t / AMS_WAVE;
-    const int i0 = blockIdx.x * kUniqTile + t * kUniqItems;
-    int flag[kUniqItems];
+    const int i0 = blockIdx.x * kTile + t * kItems;
+    int flag[kItems];
     int c = 0;
 #pragma unroll
-    for (int q = 0; q < kUniqItems; ++q) {
+    for (int q = 0; q < kItems; ++q) {
         const int i = i0 + q;
         flag[q] = (i < n && (i == 0 || k[i] != k[i - 1])) ? 1 : 0;
         c += flag[q];
@@ -201,11 +289,29 @@ __global__ __launch_bounds__(kThreads) void dd_finalize(const uint32_t *__restri
     const int incl = ams_wave_incl_scan(c);
     if (ams_lane() == AMS_WAVE - 1) ws[w] = incl;
     __syncthreads();
-    int before = boff[blockIdx.x];
-    for (int x = 0; x < w; ++x) before += ws[x];
-    int run = before + incl - c;   // heads strictly before position i0
+    if (w == 0) {
+        int tot = 0;
+        for (int x = 0; x < kWaves; ++x) tot += ws[x];
+        const uint32_t b = lookback_wave(words, blockIdx.x, (uint32_t)tot, err);
+        if (t == 0) tile_base = b;
+    }
+    int any_bad = 0;
+    if (blockIdx.x == 0) {
+        int mine = 0;
+        for (int b = t; b < n_prep; b += kThreads) mine |= bad[b];
+        any_bad = __syncthreads_or(mine);
+    }
+    if (blockIdx.x == 0 && t == 0) {
+        // a look-back bound hit in an earlier pass is a runtime failure
+        *dev_status = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                          ? AMS_ERR_HIP
+                          : (any_bad ? AMS_ERR_ID_RANGE : AMS_OK);
+    }
+    __syncthreads();
+    int run = (int)tile_base + incl - c;      // heads strictly before position i0
+    for (int x = 0; x < w; ++x) run += ws[x];
 #pragma unroll
-    for (int q = 0; q < kUniqItems; ++q) {
+    for (int q = 0; q < kItems; ++q) {
         const int i = i0 + q;
         if (i >= n) break;
         run += flag[q];
@@ -217,7 +323,19 @@ __global__ __launch_bounds__(kThreads) void dd_finalize(const uint32_t *__restri
             uniq[rank] = (int32_t)k[i];
             uniq_off[rank] = i;
         }
-        if (i == n - 1) uniq_off[rank + 1] = n;
+        if (i == n - 1) {
+            uniq_off[rank + 1] = n;
+            *n_uniq = rank + 1;
+        }
+    }
+}
+
+__global__ void dd_empty(int32_t *n_uniq, int32_t *dev_status, int32_t *uniq_off)
+{
+    if (threadIdx.x == 0 && blockIdx.x == 0) {
+        *dev_status = AMS_OK;
+        *n_uniq = 0;
+        uniq_off[0] = 0;
     }
 }
 
@@ -228,32 +346,32 @@ int id_bits(int32_t n_ids)
     return b;
 }
 
-struct DedupPlan {
-    int bits, passes, width, ntiles, nutiles;
-    size_t off_kb, off_va, off_vb, off_hist, off_bsum, total;
+struct Layout {
+    Plan P;
+    int n_prep, n_words;
+    size_t off_kb, off_va, off_vb, off_hpart, off_bad, off_words, total;
 };
 
-DedupPlan plan_dedup(int64_t n_occ, int32_t n_ids)
+Layout layout(int64_t n_occ, int32_t n_ids)
 {
-    DedupPlan p{};
-    p.bits = id_bits(n_ids);
-    p.passes = (p.bits + kMaxBits - 1) / kMaxBits;
-    p.width = (p.bits + p.passes - 1) / p.passes;
-    p.ntiles = (int)((n_occ + kTile - 1) / kTile);
-    p.nutiles = (int)((n_occ + kUniqTile - 1) / kUniqTile);
+    Layout L{};
+    L.P.bits = id_bits(n_ids);
+    L.P.passes = (L.P.bits + kMaxBits - 1) / kMaxBits;
+    L.P.width = (L.P.bits + L.P.passes - 1) / L.P.passes;
+    L.P.ntiles = (int)((n_occ + kTile - 1) / kTile);
+    L.n_prep = L.P.ntiles < kPrepBlocks ? (L.P.ntiles > 0 ? L.P.ntiles : 1) : kPrepBlocks;
+    L.n_words = L.P.passes * L.P.ntiles * kRadix + L.P.ntiles + 1;   // last word: look-back error flag
     auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
     const size_t nb = al((size_t)n_occ * 4);
-    size_t o = 0;
-    // keys_a aliases nothing: the caller's ids are read directly in pass 0
-    const size_t off_ka = o; o += nb;
-    p.off_kb = o; o += nb;
-    p.off_va = o; o += nb;
-    p.off_vb = o; o += nb;
-    p.off_hist = o; o += al((size_t)(1 << p.width) * (size_t)(p.ntiles > 0 ? p.ntiles : 1) * 4);
-    p.off_bsum = o; o += al((size_t)(p.nutiles > 0 ? p.nutiles : 1) * 4);
-    p.total = o;
-    (void)off_ka;
-    return p;
+    size_t o = nb;                           // keys ping (pong is the caller's ids on pass 0)
+    L.off_kb = o; o += nb;
+    L.off_va = o; o += nb;
+    L.off_vb = o; o += nb;
+    L.off_hpart = o; o += al((size_t)L.n_prep * kMaxPasses * kRadix * 4);
+    L.off_bad = o; o += al((size_t)L.n_prep * 4);
+    L.off_words = o; o += al((size_t)L.n_words * 4);
+    L.total = o;
+    return L;
 }
 
 }  // namespace
@@ -261,7 +379,7 @@ DedupPlan plan_dedup(int64_t n_occ, int32_t n_ids)
 extern "C" size_t ams_dedup_workspace(int64_t n_occ, int32_t n_ids)
 {
     if (n_occ < 0 || n_ids < 1) return 0;
-    return plan_dedup(n_occ, n_ids).total;
+    return layout(n_occ, n_ids).total;
 }
 
 extern "C" ams_status ams_dedup(const int32_t *ids, int64_t n_occ, int32_t n_ids, int32_t *uniq,
@@ -269,44 +387,42 @@ extern "C" ams_status ams_dedup(const int32_t *ids, int64_t n_occ, int32_t n_ids
                                 int32_t *n_uniq, int32_t *dev_status, void *ws, size_t ws_bytes,
                                 void *stream)
 {
-    if (n_occ < 0 || n_occ > (int64_t)INT32_MAX - 1 || n_ids < 1) return AMS_ERR_SIZE;
+    if (n_occ < 0 || n_occ > kMaxOcc || n_ids < 1) return AMS_ERR_SIZE;
     if (!uniq_off || !n_uniq || !dev_status) return AMS_ERR_NULL;
     if (n_occ > 0 && (!ids || !uniq || !inv || !occ_perm || !ws)) return AMS_ERR_NULL;
-    const DedupPlan p = plan_dedup(n_occ, n_ids);
-    if (n_occ > 0 && ws_bytes < p.total) return AMS_ERR_WORKSPACE;
+    const Layout L = layout(n_occ, n_ids);
+    if (n_occ > 0 && ws_bytes < L.total) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     const int n = (int)n_occ;
-
-    dd_init<<<1, 64, 0, st>>>(n_uniq, dev_status, uniq_off, n);
-    if (n == 0) return ams_launch_status();
-
+    if (n == 0) {
+        dd_empty<<<1, 64, 0, st>>>(n_uniq, dev_status, uniq_off);
+        return ams_launch_status();
+    }
     char *w = (char *)ws;
     uint32_t *ka = (uint32_t *)w;
-    uint32_t *kb = (uint32_t *)(w + p.off_kb);
-    int32_t *va = (int32_t *)(w + p.off_va);
-    int32_t *vb = (int32_t *)(w + p.off_vb);
-    int32_t *hist = (int32_t *)(w + p.off_hist);
-    int32_t *bsum = (int32_t *)(w + p.off_bsum);
+    uint32_t *kb = (uint32_t *)(w + L.off_kb);
+    int32_t *va = (int32_t *)(w + L.off_va);
+    int32_t *vb = (int32_t *)(w + L.off_vb);
+    int32_t *hpart = (int32_t *)(w + L.off_hpart);
+    int32_t *bad = (int32_t *)(w + L.off_bad);
+    uint32_t *words = (uint32_t *)(w + L.off_words);
+    int32_t *err = (int32_t *)(words + L.n_words - 1);
 
+    dd_prep<<<L.n_prep, kThreads, 0, st>>>((const uint32_t *)ids, n, L.P, (uint32_t)n_ids, hpart, bad, words,
+                                          L.n_words);
     const uint32_t *kin = (const uint32_t *)ids;
     const int32_t *vin = nullptr;
     uint32_t *bufk[2] = {ka, kb};
     int32_t *bufv[2] = {va, vb};
-    for (int pass = 0; pass < p.passes; ++pass) {
-        const int shift = pass * p.width;
-        const int bits = (p.bits - shift) < p.width ? (p.bits - shift) : p.width;
+    for (int pass = 0; pass < L.P.passes; ++pass) {
         uint32_t *kout = bufk[pass & 1];
         int32_t *vout = bufv[pass & 1];
-        dd_hist<<<p.ntiles, kThreads, 0, st>>>(kin, n, shift, bits, hist, p.ntiles,
-                                               (uint32_t)n_ids, dev_status, pass == 0);
-        dd_scan<<<1, kScanThreads, 0, st>>>(hist, (1 << bits) * p.ntiles, nullptr);
-        dd_scatter<<<p.ntiles, kThreads, 0, st>>>(kin, vin, kout, vout, n, shift, bits, hist,
-                                                  p.ntiles);
+        dd_pass<<<L.P.ntiles, kThreads, 0, st>>>(kin, vin, kout, vout, n, L.P, pass, hpart, L.n_prep, words,
+                                                 err);
         kin = kout;
         vin = vout;
     }
-    dd_head_count<<<p.nutiles, kThreads, 0, st>>>(kin, n, bsum);
-    dd_scan<<<1, kScanThreads, 0, st>>>(bsum, p.nutiles, n_uniq);
-    dd_finalize<<<p.nutiles, kThreads, 0, st>>>(kin, vin, n, bsum, uniq, inv, occ_perm, uniq_off);
+    dd_unique<<<L.P.ntiles, kThreads, 0, st>>>(kin, vin, n, words + (size_t)L.P.passes * L.P.ntiles * kRadix,
+                                              err, bad, L.n_prep, uniq, inv, occ_perm, uniq_off, n_uniq, dev_status);
     return ams_launch_status();
 }

@@ -1074,26 +1074,28 @@ __global__ __launch_bounds__(kThreads) void dw1_part(const TT *__restrict__ T, i
 }
 
 // fp32 dW1 partial of chunk c with the same 3-slot DMA ring as the forward.
-// Block tile 128 (m, dZ1 columns) x 64 (n, feature columns), K step 32 unique
-// images.  Per stage the A tile is 32 rows x 512 B of dZ1 (16 DMA
-// instructions of 2 rows) and the B tile 32 rows x 256 B of gathered feature
-// rows (8 instructions of 4 rows); every wave issues 4 A and 2 B instructions.
-// The 16-byte chunk index of odd rows is XOR-ed with 8 (a 128-byte shift) so
-// that lanes 0-31 (row k) and 32-63 (row k+1) of one 4-byte operand read fall
-// in different banks.  Rows past the chunk and rows with an out-of-range ID
-// read the zero row.
+// Block tile 128 (m, dZ1 columns) x 128 (n, feature columns), K step 32
+// unique images, 8 waves in 2 (m) x 4 (n), each 64 x 32.  Per stage the A
+// tile is 32 rows x 512 B of dZ1 and the B tile 32 rows x 512 B of gathered
+// feature rows, 16 DMA instructions of 2 rows each; every wave issues 2 A and
+// 2 B instructions.  The 16-byte chunk index of odd rows is XOR-ed with 8 (a
+// 128-byte shift) so that lanes 0-31 (row k) and 32-63 (row k+1) of one
+// 4-byte operand read fall in different banks.  Rows past the chunk and rows
+// with an out-of-range ID read the zero row.  One block per CU: the host
+// picks the chunk count so that tiles x chunks = CUs.
 //
 // The image IDs that address the B rows are loaded two stages ahead, before
 // the DMA of the stage that is issued with them, so at the top of stage s
-// "wait until at most 8 vector-memory ops are outstanding" leaves exactly the
-// IDs of stage s+4 and the DMA of stage s+2 in flight.
+// "wait until at most 6 vector-memory ops are outstanding" leaves exactly the
+// IDs of stage s+3 and the DMA of stage s+1 in flight.
 struct DwRing {
-    static constexpr int BM = 128, BN = 64, BK = 32;
+    static constexpr int BM = 128, BN = 128, BK = 32, WAVES = 8;
     static constexpr int A_FLOATS = BK * BM, B_FLOATS = BK * BN;
     static constexpr int SLOT = A_FLOATS + B_FLOATS;
-    static constexpr int PA = 4, PB = 2;                 // A / B DMA instructions per wave
+    static constexpr int PA = 2, PB = 2;                 // A / B DMA instructions per wave
     static constexpr int OUTSTANDING = PA + PB + PB;     // vm ops allowed in flight at a stage top
 };
+constexpr int kDwThreads = DwRing::WAVES * AMS_WAVE;
 
 __device__ __forceinline__ int dw_chunk_swz(int row) { return (row & 1) << 3; }
 
@@ -1103,7 +1105,7 @@ __device__ __forceinline__ void dw1_load_ids(const int32_t *__restrict__ uniq, i
 {
 #pragma unroll
     for (int q = 0; q < DwRing::PB; ++q) {
-        const int row = 4 * (DwRing::PB * wave + q) + (lane >> 4);
+        const int row = 2 * (DwRing::PB * wave + q) + (lane >> 5);
         const int u = u_base + row;
         const int v = uniq[min(u, u1 - 1)];          // always issued: uniform op count
         id[q] = u < u1 ? v : -1;
@@ -1115,21 +1117,21 @@ __device__ __forceinline__ void dw1_issue(float *slot, const float *__restrict__
                                           int u1, const float *__restrict__ zero_row, const int (&id)[2],
                                           int wave, int lane)
 {
+    const int c = lane & 31;
 #pragma unroll
     for (int q = 0; q < DwRing::PA; ++q) {
         const int j = DwRing::PA * wave + q;
         const int row = 2 * j + (lane >> 5);
-        const int c = (lane & 31) ^ dw_chunk_swz(row);
         const int u = u_base + row;
-        dma16((u < u1 ? dZ1 + (size_t)u * H + m0 : zero_row) + 4 * c, slot + j * 256);
+        dma16((u < u1 ? dZ1 + (size_t)u * H + m0 : zero_row) + 4 * (c ^ dw_chunk_swz(row)), slot + j * 256);
     }
 #pragma unroll
     for (int q = 0; q < DwRing::PB; ++q) {
-        const int jb = DwRing::PB * wave + q;
-        const int row = 4 * jb + (lane >> 4);
-        const int c = (lane & 15) ^ dw_chunk_swz(row);
+        const int j = DwRing::PB * wave + q;
+        const int row = 2 * j + (lane >> 5);
         const bool ok = id[q] >= 0 && (int64_t)id[q] < n_rows;
-        dma16((ok ? T + (size_t)id[q] * F + n0 : zero_row) + 4 * c, slot + DwRing::A_FLOATS + jb * 256);
+        dma16((ok ? T + (size_t)id[q] * F + n0 : zero_row) + 4 * (c ^ dw_chunk_swz(row)),
+              slot + DwRing::A_FLOATS + j * 256);
     }
 }
 
@@ -1138,7 +1140,7 @@ __device__ __forceinline__ void dw1_issue(float *slot, const float *__restrict__
 // the interleave), so the 4-byte LDS reads are never waited on.
 __device__ __forceinline__ void dw1_compute(const float *slot, v16f *acc, int lane, int wave)
 {
-    const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
+    const int h = lane >> 5, r32 = lane & 31, wm = wave >> 2, wn = wave & 3;
     const float *A = slot, *B = slot + DwRing::A_FLOATS;
     float av[DwRing::BK / 2][2], bv[DwRing::BK / 2];
 #pragma unroll
@@ -1161,12 +1163,12 @@ __device__ __forceinline__ void dw1_compute(const float *slot, v16f *acc, int la
     }
 }
 
-__global__ __launch_bounds__(kThreads) void dw1_part_f32(const float *__restrict__ T, int64_t n_rows,
-                                                          int F, const int32_t *__restrict__ uniq,
-                                                          const int32_t *__restrict__ n_uniq_p, int cap,
-                                                          const float *__restrict__ dZ1, int H, int KC,
-                                                          const float *__restrict__ zero_row,
-                                                          float *__restrict__ part)
+__global__ __launch_bounds__(kDwThreads) void dw1_part_f32(const float *__restrict__ T, int64_t n_rows,
+                                                            int F, const int32_t *__restrict__ uniq,
+                                                            const int32_t *__restrict__ n_uniq_p, int cap,
+                                                            const float *__restrict__ dZ1, int H, int KC,
+                                                            const float *__restrict__ zero_row,
+                                                            float *__restrict__ part)
 {
     using R = DwRing;
     __shared__ __attribute__((aligned(16))) float ring0[R::SLOT];
@@ -1185,7 +1187,7 @@ __global__ __launch_bounds__(kThreads) void dw1_part_f32(const float *__restrict
     v16f acc[2] = {(v16f){}, (v16f){}};
     const int S = (u1 - u0 + R::BK - 1) / R::BK;
     if (S > 0) {
-        int id0[2], id1[2], id2[2];                       // IDs of stages = 0, 1, 2 (mod 3)
+        int id0[2], id1[2], id2[2];
 #define DW_BASE(s) (u0 + min((s), S - 1) * R::BK)
         // prologue: IDs of stages 0..2 resident, IDs of stage 3 in flight, DMA 0 and 1 issued
         dw1_load_ids(uniq, DW_BASE(0), u1, wave, lane, id0);
@@ -1196,7 +1198,6 @@ __global__ __launch_bounds__(kThreads) void dw1_part_f32(const float *__restrict
         dw1_load_ids(uniq, DW_BASE(3), u1, wave, lane, idn);
         dw1_issue(ring0, T, n_rows, F, dZ1, H, m0, n0, DW_BASE(0), u1, zero_row, id0, wave, lane);
         dw1_issue(ring1, T, n_rows, F, dZ1, H, m0, n0, DW_BASE(1), u1, zero_row, id1, wave, lane);
-        // id0 now holds stage 3's IDs (in flight); idn is the register they land in
 #define DW_STAGE(cur, nxt, ids_next_dma, ids_load, s)                                          \
     do {                                                                                        \
         AMS_WAIT_VM(R::OUTSTANDING);                                                            \
@@ -1227,12 +1228,12 @@ __global__ __launch_bounds__(kThreads) void dw1_part_f32(const float *__restrict
     }
 
     float *out = part + (size_t)c * H * F;
-    const int col = n0 + (wave & 1) * 32 + (lane & 31);
+    const int col = n0 + (wave & 3) * 32 + (lane & 31);
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-            const int row = m0 + (wave >> 1) * 64 + mb * 32 + acc_row(j, lane);
+            const int row = m0 + (wave >> 2) * 64 + mb * 32 + acc_row(j, lane);
             out[(size_t)row * F + col] = acc[mb][j];
         }
 }
@@ -1254,11 +1255,22 @@ bool mlp_ok(const ams_mlp *m)
 
 size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-int dw1_chunks(int H, int F)
+int sk_workers();
+
+bool use_dw_ring(const ams_mlp *m) { return m->dtype == AMS_F32 && m->dims[1] % 128 == 0 && m->dims[0] % 128 == 0; }
+
+// Split-K chunk count of dW1: the DMA-ring kernel takes one block per CU
+// (tiles x chunks = CUs); the fallback kernel aims at ~1024 blocks.
+int dw1_chunks(const ams_mlp *m)
 {
-    const int bm = (H % 128 == 0) ? 128 : 64;
-    const int tiles = (H / bm) * (F / 64);
-    int kc = 1024 / tiles;
+    const int H = m->dims[1], F = m->dims[0];
+    int kc;
+    if (use_dw_ring(m)) {
+        kc = sk_workers() / ((H / 128) * (F / 128));
+    } else {
+        const int bm = (H % 128 == 0) ? 128 : 64;
+        kc = 1024 / ((H / bm) * (F / 64));
+    }
     return kc < 1 ? 1 : (kc > 32 ? 32 : kc);
 }
 
@@ -1279,7 +1291,7 @@ BwdPlan plan_bwd(const ams_mlp *m, int32_t cap)
     BwdPlan p{};
     const int H = m->dims[1], F = m->dims[0];
     const size_t es = (m->dtype == AMS_BF16) ? 2 : 4;
-    p.kc = dw1_chunks(H, F);
+    p.kc = dw1_chunks(m);
     size_t o = 0;
     p.off_zero = o; o += al256((size_t)(F > H ? F : H) * 4);
     p.off_dz1 = o; o += al256((size_t)cap * H * es);
@@ -1426,9 +1438,11 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
     const int bm = (H % 128 == 0) ? 128 : 64;
     const int nmt = H / bm, outer = (F / 64) * p.kc;
     const int grid = ((outer + 7) / 8) * 8 * nmt;
-    if (!bf && bm == 128) {
-        dw1_part_f32<<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
-                                                (const float *)dz1, H, p.kc, zero, dw1p);
+    if (use_dw_ring(mlp)) {
+        const int outer8 = (F / DwRing::BN) * p.kc;
+        const int grid8 = ((outer8 + 7) / 8) * 8 * (H / DwRing::BM);
+        dw1_part_f32<<<grid8, kDwThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
+                                                   (const float *)dz1, H, p.kc, zero, dw1p);
     } else if (!bf) {
         if (bm == 128)
             dw1_part<128, float><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
