@@ -8,10 +8,14 @@ is never replayed against its own warm cache.  Prints ONE JSON line.
     python bench.py [--steps K] [--warmup W] [--workload c1_f32] [--mode att]
 
 Throughput = behavior images embedded and pooled per second (fwd + bwd).
-The roofline entry covers the dominant call, the gather-fused embedding
-forward (4096-wide MFMA GEMM plus the small tail layers), timed with events on
-the stream it runs on.  The CPU baseline is the float64 oracle, timed on this
-host on one whole batch of the same workload.
+Passes after the timed one (none of them enters `value`):
+  * per call: events between the five calls of each step;
+  * per kernel: the library's own event pairs around every launch
+    (ams_timing_enable); the roofline entry is taken for the kernel with the
+    largest total time, from its algorithmic flops and bytes per unique image;
+  * cold: each step timed alone after a 512 MiB write that evicts the caches.
+The CPU baseline is the float64 oracle, timed on this host on one whole batch
+of the same workload, repeated for about ten seconds (median run).
 """
 from __future__ import annotations
 
@@ -31,29 +35,20 @@ PEAK_MFMA = {"f32": 157.3e12, "bf16": 2.5e15}
 
 
 def flops_per_unique(dims):
-    F, H = dims[0], dims[1]
     fwd = 2 * sum(a * b for a, b in zip(dims[:-1], dims[1:]))
     # backward: every weight gradient, plus dH of every layer but the first
     bwd = 2 * sum(a * b for a, b in zip(dims[:-1], dims[1:])) + 2 * sum(
         a * b for a, b in zip(dims[1:-1], dims[2:]))
-    return fwd, bwd, 2 * F * H
+    return fwd, bwd
 
 
-def traffic_from_profile(kernel_src_hash: str, unique_count: float):
-    """HBM bytes per launch from committed PMC summaries, if they were taken
-    on the current kernel source; else None."""
-    path = os.path.join(ROOT, "profiles", "embed_fwd_c1_f32_traffic.json")
-    if not os.path.exists(path):
-        return None
-    try:
-        d = json.load(open(path))
-    except Exception:
-        return None
-    if d.get("source_sha256") != kernel_src_hash:
-        return None
-    # bytes scale with the unique rows a launch gathers: per-unique figure of
-    # the profiled batch times this run's mean unique count
-    return d["hbm_bytes_per_unique"] * unique_count
+# Algorithmic work of the layer-1 GEMM kernels per unique image: 2*F*H flops
+# and one read of the image's F-wide feature row.
+GEMM_KERNELS = ("l1sk_f32", "l1_fwd_f32", "l1_fwd_bf16", "dw1_part_f32", "dw1_part")
+
+
+def gemm_work_per_unique(dims, esz):
+    return 2 * dims[0] * dims[1], dims[0] * esz
 
 
 def src_hash():
@@ -63,7 +58,34 @@ def src_hash():
     return h.hexdigest()
 
 
-def cpu_baseline(w, batch, mode):
+def traffic_from_profile(workload: str, kernel: str, unique_count: float):
+    """HBM bytes per launch of `kernel` from the committed PMC record, if it
+    was taken on the current kernel source; else None."""
+    path = os.path.join(ROOT, "profiles", f"traffic_{workload}.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        d = json.load(open(path))
+    except Exception:
+        return None
+    if d.get("source_sha256") != src_hash() or kernel not in d.get("kernels", {}):
+        return None
+    # bytes scale with the unique rows a launch gathers: per-unique figure of
+    # the profiled batch times this run's mean unique count
+    return d["kernels"][kernel]["hbm_bytes_per_unique"] * unique_count
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(w, batch, mode, min_runs=3, min_seconds=10.0, max_runs=30):
     import numpy as np
 
     from oracle import oracle
@@ -72,14 +94,21 @@ def cpu_baseline(w, batch, mode):
     occ = synth.occurrences(batch)
     uniq = np.unique(occ)
     T_u = synth.table_rows(w, uniq)
-    t0 = time.perf_counter()
-    oracle.step(batch, w.n_images, T_u, Ws, bs, mode, table_is_compact=True)
-    dt = time.perf_counter() - t0
+    # repeated until about min_seconds of CPU work, then the median run
+    times = []
+    while len(times) < min_runs or (sum(times) < min_seconds and len(times) < max_runs):
+        t0 = time.perf_counter()
+        oracle.step(batch, w.n_images, T_u, Ws, bs, mode, table_is_compact=True)
+        times.append(time.perf_counter() - t0)
+    dt = sorted(times)[len(times) // 2]
+    runs = len(times)
     n_beh = int(batch["seg_off"][-1])
     return {"value": n_beh / dt, "unit": "behavior images/s", "cores": oracle.num_threads(),
             "kind": "oracle",
-            "sample": f"one whole batch of the same workload ({w.batch} samples, {n_beh} behaviors), "
-                      f"float64 C oracle, {dt:.2f} s"}
+            "sample": f"one whole batch of the same workload ({w.batch} samples, {n_beh} behaviors, "
+                      f"{uniq.size} unique images), float64 C oracle with OpenMP, median of {runs} runs "
+                      f"(total {sum(times):.1f} s, min {min(times):.2f} s, max {max(times):.2f} s), "
+                      f"CPU: {cpu_model()}"}
 
 
 def main():
@@ -197,18 +226,59 @@ def main():
         per["embed_bwd"] += e[3].elapsed_time(e[4])
     per = {k: v / args.steps for k, v in per.items()}
 
-    fwd_f, bwd_f, l1_f = flops_per_unique(w.dims)
+    # per-kernel durations: the library's event pairs on the launching stream
+    ams.ams_timing_read()                      # drop anything recorded before
+    ams.ams_timing_enable(True)
+    for s in range(args.steps):
+        one(dev_batches[s % len(dev_batches)])
+    torch.cuda.synchronize()
+    ams.ams_timing_enable(False)
+    ktimes = ams.ams_timing_read()
+    kernels = {k: {"launches": n, "ms_per_launch": t / n} for k, (n, t) in ktimes.items() if n}
+
+    # cold caches: each step timed alone after a 512 MiB write
+    scratch = torch.empty(512 << 18, dtype=torch.float32, device="cuda")
+    cold_ms = []
+    for s in range(args.steps):
+        scratch.fill_(float(s))
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        one(dev_batches[s % len(dev_batches)])
+        e1.record(stream)
+        torch.cuda.synchronize()
+        cold_ms.append(e0.elapsed_time(e1))
+    del scratch
+    cold_step = sum(cold_ms) / len(cold_ms)
+
+    fwd_f, bwd_f = flops_per_unique(w.dims)
     u_mean = uniq_total / args.steps
     esz = 2 if w.dtype == "bf16" else 4
     step_flops = u_mean * (fwd_f + bwd_f)
     step_bytes = u_mean * 2 * w.in_dim * esz           # the two reads of every unique feature row
     peak = PEAK_MFMA[w.dtype]
-    ach = u_mean * fwd_f / (per["embed_fwd"] * 1e-3)
-    traffic = traffic_from_profile(src_hash(), u_mean)
-    roof = {"kernel": "ams_embed_fwd (l1_fwd gather+MFMA GEMM, tail layers)",
-            "bound": "mfma", "achieved": ach / 1e12, "peak": peak / 1e12, "unit": "TFLOP/s",
-            "frac": ach / peak, "traffic": traffic,
-            "algorithmic_flops_per_launch": u_mean * fwd_f, "avg_launch_ms": per["embed_fwd"]}
+
+    # roofline of the dominant kernel (largest total time over the pass)
+    dom = max(ktimes, key=lambda k: ktimes[k][1])
+    t_launch = kernels[dom]["ms_per_launch"] * 1e-3
+    if dom in GEMM_KERNELS:
+        fl_u, by_u = gemm_work_per_unique(w.dims, esz)
+        # bound: whichever peak the algorithmic work would take longer on
+        bound = "mfma" if fl_u / peak >= by_u / PEAK_HBM else "hbm"
+        if bound == "mfma":
+            ach, pk, unit, alg = u_mean * fl_u / t_launch / 1e12, peak / 1e12, "TFLOP/s", u_mean * fl_u
+        else:
+            ach, pk, unit, alg = u_mean * by_u / t_launch / 1e9, PEAK_HBM / 1e9, "GB/s", u_mean * by_u
+        roof = {"kernel": dom, "bound": bound, "achieved": ach, "peak": pk, "unit": unit, "frac": ach / pk,
+                "traffic": traffic_from_profile(w.name, dom, u_mean),
+                "algorithmic_per_launch": alg, "avg_launch_ms": t_launch * 1e3,
+                "unit_of_work": f"{fl_u} flop and {by_u} B per unique image, {u_mean:.0f} unique per launch"}
+    else:
+        roof = {"kernel": dom, "bound": None, "achieved": None, "peak": None, "unit": None, "frac": None,
+                "traffic": None, "avg_launch_ms": t_launch * 1e3}
+    for k, v in kernels.items():
+        if k in GEMM_KERNELS:
+            fl_u, _ = gemm_work_per_unique(w.dims, esz)
+            v["mfma_frac"] = u_mean * fl_u / (v["ms_per_launch"] * 1e-3) / peak
 
     out = {
         "metric": METRIC, "value": value, "unit": "behavior images/s", "n_gpus": 1,
@@ -222,7 +292,12 @@ def main():
                    "rotating_batches": len(dev_batches)},
         "step_mfma_frac": step_flops / (ms_step * 1e-3) / peak,
         "step_hbm_frac": step_bytes / (ms_step * 1e-3) / PEAK_HBM,
+        "unique_images_per_s": uniq_total / (ms_total * 1e-3),
+        "samples_per_s": w.batch * args.steps / (ms_total * 1e-3),
+        "cold": {"value": beh_total / (sum(cold_ms) * 1e-3), "ms_per_step": cold_step,
+                 "note": "each step timed alone after a 512 MiB device write"},
         "per_call_ms": per,
+        "kernels": kernels,
         "roofline": roof,
         "cpu_baseline": None,
     }

@@ -101,6 +101,28 @@ const char *ams_status_str(ams_status s);
 /* Library version and the GPU architecture it was built for (host). */
 const char *ams_build_info(void);
 
+/* ------------------------------------------------------------ timing ----
+ * Per-kernel timing, for benchmarks and diagnostics.  While enabled, every
+ * kernel that a call enqueues is bracketed by two HIP events recorded on the
+ * call's stream; ams_timing_read waits for the recorded events, sums the
+ * elapsed times per kernel name and clears the record.  The switch and the
+ * record are process-wide: use it from one host thread at a time.  Off by
+ * default; when off it costs one relaxed load per launch.
+ *
+ * ams_timing_read: out[cap] receives up to cap entries in order of first
+ * launch; *n_out is the number of distinct kernels recorded (may exceed cap).
+ * Returns AMS_ERR_NULL for a NULL n_out (or NULL out with cap > 0), and
+ * AMS_ERR_HIP if an event could not be created, recorded or read (those
+ * launches are left out of the sums; the record is cleared all the same). */
+typedef struct {
+    char name[32];       /* kernel name, NUL-terminated */
+    int64_t launches;    /* timed launches since the last read */
+    double total_ms;     /* summed event-to-event time of those launches */
+} ams_kernel_time;
+
+ams_status ams_timing_enable(int on);
+ams_status ams_timing_read(ams_kernel_time *out, int cap, int *n_out);
+
 /* ------------------------------------------------------------- dedup ----
  * Requests for the same image are processed once (section 4.2).
  *

@@ -22,13 +22,17 @@ STATUS = {0: "AMS_OK", 1: "AMS_ERR_NULL", 2: "AMS_ERR_SIZE", 3: "AMS_ERR_DTYPE",
           5: "AMS_ERR_WORKSPACE", 6: "AMS_ERR_HIP", 7: "AMS_ERR_ID_RANGE", 8: "AMS_ERR_MODE"}
 EXPORTS = ["ams_status_str", "ams_build_info", "ams_dedup_workspace", "ams_dedup",
            "ams_embed_workspace", "ams_embed_fwd", "ams_embed_bwd", "ams_pool_fwd",
-           "ams_pool_workspace", "ams_pool_bwd"]
+           "ams_pool_workspace", "ams_pool_bwd", "ams_timing_enable", "ams_timing_read"]
 
 
 class AmsError(RuntimeError):
     def __init__(self, status: int, where: str):
         self.status = status
         super().__init__(f"{where}: {STATUS.get(status, status)} ({_text(status)})")
+
+
+class ams_kernel_time(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 32), ("launches", ctypes.c_int64), ("total_ms", ctypes.c_double)]
 
 
 class ams_mlp(ctypes.Structure):
@@ -68,6 +72,10 @@ def load() -> ctypes.CDLL:
     lib.ams_pool_workspace.argtypes = [i32, i32, i64, i32, i32]
     lib.ams_pool_bwd.restype = ctypes.c_int
     lib.ams_pool_bwd.argtypes = [i32, i32, i32, P, i64, P, P, P, P, i32, P, P, P, P, P, P, P, P, sz, P]
+    lib.ams_timing_enable.restype = ctypes.c_int
+    lib.ams_timing_enable.argtypes = [ctypes.c_int]
+    lib.ams_timing_read.restype = ctypes.c_int
+    lib.ams_timing_read.argtypes = [ctypes.POINTER(ams_kernel_time), ctypes.c_int, ctypes.POINTER(ctypes.c_int)]
     _lib = lib
     return lib
 
@@ -170,6 +178,21 @@ def ams_pool_bwd(mode, seg_off, n_beh, inv, occ_perm, uniq_off, n_uniq, n_uniq_c
 
 
 # ------------------------------------------------------- one whole step
+
+def ams_timing_enable(on: bool):
+    _check(load().ams_timing_enable(1 if on else 0), "ams_timing_enable")
+
+
+def ams_timing_read(cap: int = 64) -> dict:
+    """{kernel name: (launches, total ms)} recorded since the last read
+    (waits for the recorded events; clears the record)."""
+    buf = (ams_kernel_time * cap)()
+    n = ctypes.c_int(0)
+    _check(load().ams_timing_read(buf, cap, ctypes.byref(n)), "ams_timing_read")
+    if n.value > cap:
+        raise RuntimeError(f"ams_timing_read: {n.value} kernels recorded, buffer holds {cap}")
+    return {buf[k].name.decode(): (int(buf[k].launches), float(buf[k].total_ms)) for k in range(n.value)}
+
 
 class Step:
     """Buffers for one training step of the embedding hot path, and the five

@@ -14,6 +14,20 @@
         if ((expr) != hipSuccess) return AMS_ERR_HIP;       \
     } while (0)
 
+// Per-kernel timing (ams_timing_enable): when on, every launch is bracketed by
+// a pair of HIP events on the launching stream, read back by ams_timing_read.
+extern int ams_timing_flag;
+void ams_timing_begin(const char *name, hipStream_t st);
+void ams_timing_end(hipStream_t st);
+
+#define AMS_LAUNCH(name, st, ...)                                    \
+    do {                                                             \
+        const bool ams_timed_ = __atomic_load_n(&ams_timing_flag, __ATOMIC_RELAXED) != 0; \
+        if (ams_timed_) ams_timing_begin(name, st);                  \
+        __VA_ARGS__;                                                 \
+        if (ams_timed_) ams_timing_end(st);                          \
+    } while (0)
+
 // Launch check: a failed enqueue is reported as AMS_ERR_HIP.
 static inline ams_status ams_launch_status()
 {

@@ -395,7 +395,7 @@ extern "C" ams_status ams_dedup(const int32_t *ids, int64_t n_occ, int32_t n_ids
     hipStream_t st = (hipStream_t)stream;
     const int n = (int)n_occ;
     if (n == 0) {
-        dd_empty<<<1, 64, 0, st>>>(n_uniq, dev_status, uniq_off);
+        AMS_LAUNCH("dd_empty", st, dd_empty<<<1, 64, 0, st>>>(n_uniq, dev_status, uniq_off));
         return ams_launch_status();
     }
     char *w = (char *)ws;
@@ -408,8 +408,8 @@ extern "C" ams_status ams_dedup(const int32_t *ids, int64_t n_occ, int32_t n_ids
     uint32_t *words = (uint32_t *)(w + L.off_words);
     int32_t *err = (int32_t *)(words + L.n_words - 1);
 
-    dd_prep<<<L.n_prep, kThreads, 0, st>>>((const uint32_t *)ids, n, L.P, (uint32_t)n_ids, hpart, bad, words,
-                                          L.n_words);
+    AMS_LAUNCH("dd_prep", st, dd_prep<<<L.n_prep, kThreads, 0, st>>>((const uint32_t *)ids, n, L.P, (uint32_t)n_ids, hpart, bad, words,
+                                          L.n_words));
     const uint32_t *kin = (const uint32_t *)ids;
     const int32_t *vin = nullptr;
     uint32_t *bufk[2] = {ka, kb};
@@ -417,12 +417,12 @@ extern "C" ams_status ams_dedup(const int32_t *ids, int64_t n_occ, int32_t n_ids
     for (int pass = 0; pass < L.P.passes; ++pass) {
         uint32_t *kout = bufk[pass & 1];
         int32_t *vout = bufv[pass & 1];
-        dd_pass<<<L.P.ntiles, kThreads, 0, st>>>(kin, vin, kout, vout, n, L.P, pass, hpart, L.n_prep, words,
-                                                 err);
+        AMS_LAUNCH("dd_pass", st, dd_pass<<<L.P.ntiles, kThreads, 0, st>>>(kin, vin, kout, vout, n, L.P, pass, hpart, L.n_prep, words,
+                                                 err));
         kin = kout;
         vin = vout;
     }
-    dd_unique<<<L.P.ntiles, kThreads, 0, st>>>(kin, vin, n, words + (size_t)L.P.passes * L.P.ntiles * kRadix,
-                                              err, bad, L.n_prep, uniq, inv, occ_perm, uniq_off, n_uniq, dev_status);
+    AMS_LAUNCH("dd_unique", st, dd_unique<<<L.P.ntiles, kThreads, 0, st>>>(kin, vin, n, words + (size_t)L.P.passes * L.P.ntiles * kRadix,
+                                              err, bad, L.n_prep, uniq, inv, occ_perm, uniq_off, n_uniq, dev_status));
     return ams_launch_status();
 }

@@ -1360,33 +1360,33 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
     const int NT = (H % 128 == 0) ? 128 : 64;
     const int grid = ((n_mt + 7) / 8) * 8 * (H / NT);
     if (sk) {
-        l1sk_f32<<<G, kSkThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, (const float *)W1, b1,
-                                           H, G, H1f, pbuf);
+        AMS_LAUNCH("l1sk_f32", st, l1sk_f32<<<G, kSkThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, (const float *)W1, b1,
+                                           H, G, H1f, pbuf));
     } else if (!bf) {
         if (NT == 128)
-            l1_fwd_f32<128><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, n_mt,
-                                                       (const float *)W1, b1, H, H1f);
+            AMS_LAUNCH("l1_fwd_f32", st, l1_fwd_f32<128><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, n_mt,
+                                                       (const float *)W1, b1, H, H1f));
         else
-            l1_fwd_f32<64><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, n_mt,
-                                                      (const float *)W1, b1, H, H1f);
+            AMS_LAUNCH("l1_fwd_f32", st, l1_fwd_f32<64><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, n_mt,
+                                                      (const float *)W1, b1, H, H1f));
     } else {
         if (NT == 128)
-            l1_fwd_bf16<128><<<grid, kThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq, n_uniq,
+            AMS_LAUNCH("l1_fwd_bf16", st, l1_fwd_bf16<128><<<grid, kThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq, n_uniq,
                                                         cap, n_mt, (const uint16_t *)W1, b1, H, H1f,
-                                                        (uint16_t *)H1_save);
+                                                        (uint16_t *)H1_save));
         else
-            l1_fwd_bf16<64><<<grid, kThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq, n_uniq,
+            AMS_LAUNCH("l1_fwd_bf16", st, l1_fwd_bf16<64><<<grid, kThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq, n_uniq,
                                                        cap, n_mt, (const uint16_t *)W1, b1, H, H1f,
-                                                       (uint16_t *)H1_save);
+                                                       (uint16_t *)H1_save));
     }
     int tg = (cap + kTailRows - 1) / kTailRows;
     if (tg > 1024) tg = 1024;
     if (L == 3)
-        tail_fwd<3><<<tg, kThreads, 0, st>>>(H1f, H, M, D, W2, b2, W3, b3, bf, mlp->final_relu, n_uniq,
-                                             cap, H2_save, E, sk, F, G, pbuf, b1, uniq, n_rows);
+        AMS_LAUNCH("tail_fwd", st, tail_fwd<3><<<tg, kThreads, 0, st>>>(H1f, H, M, D, W2, b2, W3, b3, bf, mlp->final_relu, n_uniq,
+                                             cap, H2_save, E, sk, F, G, pbuf, b1, uniq, n_rows));
     else
-        tail_fwd<2><<<tg, kThreads, 0, st>>>(H1f, H, M, D, W2, b2, W3, b3, bf, mlp->final_relu, n_uniq,
-                                             cap, H2_save, E, sk, F, G, pbuf, b1, uniq, n_rows);
+        AMS_LAUNCH("tail_fwd", st, tail_fwd<2><<<tg, kThreads, 0, st>>>(H1f, H, M, D, W2, b2, W3, b3, bf, mlp->final_relu, n_uniq,
+                                             cap, H2_save, E, sk, F, G, pbuf, b1, uniq, n_rows));
     return ams_launch_status();
 }
 
@@ -1423,17 +1423,17 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
     const int PS = tail_part_size(mlp);
 
     if (L == 3)
-        tail_bwd<3><<<kTailBlocks, kThreads, 0, st>>>(H1_save, bf, H2_save, E_fwd, dE, W2, W3, bf, H, M, D,
+        AMS_LAUNCH("tail_bwd", st, tail_bwd<3><<<kTailBlocks, kThreads, 0, st>>>(H1_save, bf, H2_save, E_fwd, dE, W2, W3, bf, H, M, D,
                                                       mlp->final_relu, n_uniq, cap, dz1, bf, tail, PS,
-                                                      zero, F > H ? F : H);
+                                                      zero, F > H ? F : H));
     else
-        tail_bwd<2><<<kTailBlocks, kThreads, 0, st>>>(H1_save, bf, H2_save, E_fwd, dE, W2, W3, bf, H, M, D,
+        AMS_LAUNCH("tail_bwd", st, tail_bwd<2><<<kTailBlocks, kThreads, 0, st>>>(H1_save, bf, H2_save, E_fwd, dE, W2, W3, bf, H, M, D,
                                                       mlp->final_relu, n_uniq, cap, dz1, bf, tail, PS,
-                                                      zero, F > H ? F : H);
-    partial_reduce<<<(PS + kThreads - 1) / kThreads, kThreads, 0, st>>>(tail, kTailBlocks, (size_t)PS,
-                                                                         tailsum);
-    tail_unpack<<<(PS + kThreads - 1) / kThreads, kThreads, 0, st>>>(tailsum, L, H, M, D, dW2, db2,
-                                                                      dW3, db3, db1);
+                                                      zero, F > H ? F : H));
+    AMS_LAUNCH("reduce_tail", st, partial_reduce<<<(PS + kThreads - 1) / kThreads, kThreads, 0, st>>>(tail, kTailBlocks, (size_t)PS,
+                                                                         tailsum));
+    AMS_LAUNCH("tail_unpack", st, tail_unpack<<<(PS + kThreads - 1) / kThreads, kThreads, 0, st>>>(tailsum, L, H, M, D, dW2, db2,
+                                                                      dW3, db3, db1));
 
     const int bm = (H % 128 == 0) ? 128 : 64;
     const int nmt = H / bm, outer = (F / 64) * p.kc;
@@ -1441,26 +1441,26 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
     if (use_dw_ring(mlp)) {
         const int outer8 = (F / DwRing::BN) * p.kc;
         const int grid8 = ((outer8 + 7) / 8) * 8 * (H / DwRing::BM);
-        dw1_part_f32<<<grid8, kDwThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
-                                                   (const float *)dz1, H, p.kc, zero, dw1p);
+        AMS_LAUNCH("dw1_part_f32", st, dw1_part_f32<<<grid8, kDwThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
+                                                   (const float *)dz1, H, p.kc, zero, dw1p));
     } else if (!bf) {
         if (bm == 128)
-            dw1_part<128, float><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
-                                                             (const float *)dz1, H, p.kc, dw1p);
+            AMS_LAUNCH("dw1_part", st, dw1_part<128, float><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
+                                                             (const float *)dz1, H, p.kc, dw1p));
         else
-            dw1_part<64, float><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
-                                                            (const float *)dz1, H, p.kc, dw1p);
+            AMS_LAUNCH("dw1_part", st, dw1_part<64, float><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
+                                                            (const float *)dz1, H, p.kc, dw1p));
     } else {
         if (bm == 128)
-            dw1_part<128, uint16_t><<<grid, kThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq,
+            AMS_LAUNCH("dw1_part", st, dw1_part<128, uint16_t><<<grid, kThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq,
                                                                 n_uniq, cap, (const uint16_t *)dz1, H, p.kc,
-                                                                dw1p);
+                                                                dw1p));
         else
-            dw1_part<64, uint16_t><<<grid, kThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq,
+            AMS_LAUNCH("dw1_part", st, dw1_part<64, uint16_t><<<grid, kThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq,
                                                                n_uniq, cap, (const uint16_t *)dz1, H, p.kc,
-                                                               dw1p);
+                                                               dw1p));
     }
     const size_t nw = (size_t)H * F;
-    partial_reduce<<<(unsigned)((nw + kThreads - 1) / kThreads), kThreads, 0, st>>>(dw1p, p.kc, nw, dW1);
+    AMS_LAUNCH("reduce_dw1", st, partial_reduce<<<(unsigned)((nw + kThreads - 1) / kThreads), kThreads, 0, st>>>(dw1p, p.kc, nw, dW1));
     return ams_launch_status();
 }

@@ -340,8 +340,8 @@ template <int MODE, int DM>
 void launch_fwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32_t *inv, const float *E,
                 float *U, float *A, void *saved, hipStream_t st)
 {
-    pool_fwd_k<MODE, DM><<<(B + kWaves - 1) / kWaves, kThreads, 0, st>>>(B, D, seg_off, n_beh, inv, E, U, A,
-                                                                         saved);
+    AMS_LAUNCH("pool_fwd_k", st, pool_fwd_k<MODE, DM><<<(B + kWaves - 1) / kWaves, kThreads, 0, st>>>(B, D, seg_off, n_beh, inv, E, U, A,
+                                                                         saved));
 }
 
 template <int MODE, int DM>
@@ -358,12 +358,12 @@ void launch_bwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32
     int32_t *cross = (int32_t *)(ws + p.off_cross);
     const int n_occ = (int)(n_beh + B);
     if (B > 0)
-        pool_bwd_sample<MODE, DM><<<(B + kWaves - 1) / kWaves, kThreads, 0, st>>>(
-            B, D, seg_off, inv, E, U, (const float *)saved, dU, samp, cvec, da);
+        AMS_LAUNCH("pool_bwd_sample", st, pool_bwd_sample<MODE, DM><<<(B + kWaves - 1) / kWaves, kThreads, 0, st>>>(
+            B, D, seg_off, inv, E, U, (const float *)saved, dU, samp, cvec, da));
     const int g = (p.nch + kWaves - 1) / kWaves;
-    pool_bwd_seg<MODE, DM><<<g, kThreads, 0, st>>>(D, n_beh, n_occ, inv, occ_perm, uniq_off, E, A, saved, dU,
-                                                   dA, samp, cvec, da, p.nch, dE, head, tail, cross);
-    pool_bwd_fix<DM><<<g, kThreads, 0, st>>>(D, p.nch, uniq_off, cross, head, tail, dE);
+    AMS_LAUNCH("pool_bwd_seg", st, pool_bwd_seg<MODE, DM><<<g, kThreads, 0, st>>>(D, n_beh, n_occ, inv, occ_perm, uniq_off, E, A, saved, dU,
+                                                   dA, samp, cvec, da, p.nch, dE, head, tail, cross));
+    AMS_LAUNCH("pool_bwd_fix", st, pool_bwd_fix<DM><<<g, kThreads, 0, st>>>(D, p.nch, uniq_off, cross, head, tail, dE));
 }
 
 ams_status check_common(int32_t mode, int32_t B, int32_t D, int64_t n_beh)

@@ -132,3 +132,14 @@ def test_pool_host_errors(lib):
     assert lib.ams_pool_bwd(*a) == NULL
     a = list(b); a[9] = -3
     assert lib.ams_pool_bwd(*a) == SIZE
+
+
+def test_timing_switch_and_empty_read(lib):
+    # no launch is recorded without a GPU: the read returns an empty record
+    assert lib.ams_timing_enable(1) == OK
+    assert ams.ams_timing_read() == {}
+    assert lib.ams_timing_enable(0) == OK
+    n = ctypes.c_int(-1)
+    assert lib.ams_timing_read(None, 0, ctypes.byref(n)) == OK and n.value == 0
+    assert lib.ams_timing_read(None, 0, None) == NULL
+    assert lib.ams_timing_read(None, 4, ctypes.byref(n)) == NULL
