@@ -71,7 +71,10 @@ __device__ __forceinline__ int acc_row(int j, int lane) { return 8 * (j >> 2) + 
 // while stage s feeds the MFMAs.  Each slot is its own __shared__ array and
 // the loop is unrolled by 3 so that the compiler can tell the slot being
 // filled from the slot being read, and each wave waits only for its own
-// oldest stage (s_waitcnt vmcnt) before a bare s_barrier.
+// oldest stage (s_waitcnt vmcnt) and its own LDS reads (lgkmcnt) before a
+// bare s_barrier; after the barrier the slot read in the previous stage is
+// refilled.  A scheduling barrier keeps each stage's MFMAs ahead of the next
+// stage's wait, so the wait finds the LDS reads long completed.
 //
 // One DMA instruction moves 1 KB = 8 tile rows of 128 B; lane l writes 16 B
 // to slot (l % 8) of row l / 8.  Rows are XOR-swizzled by ring_swz(row) so
@@ -95,6 +98,10 @@ __device__ __forceinline__ void dma16(const void *src, void *lds_dst)
 // s_waitcnt with only the vector-memory counter constrained (gfx9 encoding).
 #define AMS_WAIT_VM(n) \
     __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (((n) >> 4) << 14) | (0x7 << 4) | (0xF << 8))
+// ... and every LDS access of this wave completed as well (before a barrier
+// after which another wave's DMA may overwrite what this wave read).
+#define AMS_WAIT_VM_LDS(n) \
+    __builtin_amdgcn_s_waitcnt(((n) & 0xF) | (((n) >> 4) << 14) | (0x7 << 4))
 
 template <int NT>
 struct L1Ring {
@@ -210,7 +217,8 @@ __global__ __launch_bounds__(kThreads) void l1_fwd_f32(const float *__restrict__
     // which keeps every wave's count of outstanding DMA uniform.
 #define L1_STAGE(cur, nxt, s)                                                    \
     do {                                                                         \
-        AMS_WAIT_VM(PW);                                                         \
+        __builtin_amdgcn_sched_barrier(0);                                         \
+        AMS_WAIT_VM_LDS(PW);                                                     \
         __builtin_amdgcn_s_barrier();                                            \
         __builtin_amdgcn_sched_barrier(0);                                       \
         l1_issue<NT>(nxt, src, min((s) + 2, S - 1) * R::BK, wave);               \
@@ -246,18 +254,22 @@ __global__ __launch_bounds__(kThreads) void l1_fwd_f32(const float *__restrict__
 }
 
 // Stream-K fp32 forward of the 4096-wide layer (used when H is a multiple of
-// 128).  Work = (128-row x 128-column tile, 32-wide K stage) iterations in
+// 256).  Work = (128-row x 256-column tile, 32-wide K stage) iterations in
 // tile-major order; each of G persistent workers (one 8-wave block per CU)
 // takes an equal contiguous share, so every CU gets the same MFMA work for
 // any number of unique images.  A tile fully inside one worker's share is
 // finished in place (bias, ReLU); a tile cut by a share boundary leaves one
 // partial accumulator tile per worker, and the tail forward (which reads H1
-// anyway) adds the pieces in K order.  Waves are 4 (M) x 2 (N), 32 x 64 each; the 3-slot DMA ring and the
-// row swizzle are those of l1_fwd_f32 with 256 tile rows (128 A + 128 B).
+// anyway) adds the pieces in K order.  Waves are 4 (M) x 2 (N), 32 x 128
+// each; the 3-slot DMA ring and the row swizzle are those of l1_fwd_f32 with
+// 384 tile rows (128 A + 256 B).  With the whole hidden width in one tile a
+// feature row is read from HBM once, and a K stage carries 64 MFMAs per wave
+// for its 6 DMA instructions.
 constexpr int kSkThreads = 512;
-constexpr int kSkBM = 128, kSkBN = 128, kSkBK = 32;
-constexpr int kSkSlot = (kSkBM + kSkBN) * kSkBK;          // floats per ring slot (32 KB)
-constexpr int kSkPW = (kSkBM + kSkBN) / 8 / 8;            // DMA instructions per wave: 4
+constexpr int kSkBM = 128, kSkBN = 256, kSkBK = 32;
+constexpr int kSkNB = kSkBN / 64;                         // 32-column MFMA blocks per wave: 4
+constexpr int kSkSlot = (kSkBM + kSkBN) * kSkBK;          // floats per ring slot (48 KB)
+constexpr int kSkPW = (kSkBM + kSkBN) / 8 / 8;            // DMA instructions per wave: 6
 constexpr int kSkTile = kSkBM * kSkBN;
 constexpr int kSkMinIters = 32;                           // smallest share worth a worker
 
@@ -292,14 +304,14 @@ __device__ __forceinline__ void sk_compute(const float *slot, v16f *acc, int lan
 {
     const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
     const int ra = wm * 32 + r32;
-    float4 a[4], b[4][2];
+    float4 a[4], b[4][kSkNB];
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
         const int q = h * 4 + g;
         a[g] = *(const float4 *)&slot[ra * 32 + ((q ^ ring_swz(ra)) << 2)];
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
-            const int rb = kSkBM + wn * 64 + nb * 32 + r32;
+        for (int nb = 0; nb < kSkNB; ++nb) {
+            const int rb = kSkBM + wn * (kSkBN / 2) + nb * 32 + r32;
             b[g][nb] = *(const float4 *)&slot[rb * 32 + ((q ^ ring_swz(rb)) << 2)];
         }
     }
@@ -309,16 +321,17 @@ __device__ __forceinline__ void sk_compute(const float *slot, v16f *acc, int lan
 #pragma unroll
         for (int e = 0; e < 4; ++e)
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
+            for (int nb = 0; nb < kSkNB; ++nb) {
                 const float bv[4] = {b[g][nb].x, b[g][nb].y, b[g][nb].z, b[g][nb].w};
                 acc[nb] = mfma_f32(av[e], bv[e], acc[nb]);
             }
     }
-    __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
+    // group 0's reads first, then (reads of g+1, MFMAs of g)
+    __builtin_amdgcn_sched_group_barrier(0x100, 1 + kSkNB, 0);
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-        if (g < 3) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+        if (g < 3) __builtin_amdgcn_sched_group_barrier(0x100, 1 + kSkNB, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 4 * kSkNB, 0);
     }
 }
 
@@ -371,11 +384,14 @@ __global__ __launch_bounds__(kSkThreads) void l1sk_f32(const float *__restrict__
                 src[q] = W1 + (size_t)(n0 + row - kSkBM) * F + chunk * 4;
             }
         }
-        v16f acc[2] = {(v16f){}, (v16f){}};
+        v16f acc[kSkNB];
+#pragma unroll
+        for (int nb = 0; nb < kSkNB; ++nb) acc[nb] = (v16f){};
         const int n = ke - ks;
 #define SK_STAGE(cur, nxt, s)                                                      \
     do {                                                                           \
-        AMS_WAIT_VM(kSkPW);                                                        \
+        __builtin_amdgcn_sched_barrier(0);                                         \
+        AMS_WAIT_VM_LDS(kSkPW);                                                    \
         __builtin_amdgcn_s_barrier();                                              \
         __builtin_amdgcn_sched_barrier(0);                                         \
         sk_issue(nxt, src, (ks + min((s) + 2, n - 1)) * kSkBK, wave);              \
@@ -398,8 +414,8 @@ __global__ __launch_bounds__(kSkThreads) void l1sk_f32(const float *__restrict__
         const int wm = wave >> 1, wn = wave & 1, r32 = lane & 31;
         if (ks == 0 && ke == S) {
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
-                const int col = n0 + wn * 64 + nb * 32 + r32;
+            for (int nb = 0; nb < kSkNB; ++nb) {
+                const int col = n0 + wn * (kSkBN / 2) + nb * 32 + r32;
                 const float bias = b1[col];
 #pragma unroll
                 for (int j = 0; j < 16; ++j) {
@@ -411,10 +427,10 @@ __global__ __launch_bounds__(kSkThreads) void l1sk_f32(const float *__restrict__
         } else {
             float *piece = pbuf + ((size_t)w * 2 + (first ? 0 : 1)) * kSkTile;
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb)
+            for (int nb = 0; nb < kSkNB; ++nb)
 #pragma unroll
                 for (int j = 0; j < 16; ++j)
-                    piece[(wm * 32 + acc_row(j, lane)) * kSkBN + wn * 64 + nb * 32 + r32] = acc[nb][j];
+                    piece[(wm * 32 + acc_row(j, lane)) * kSkBN + wn * (kSkBN / 2) + nb * 32 + r32] = acc[nb][j];
         }
         first = false;
         it += n;
@@ -570,11 +586,12 @@ constexpr int kTailLDo = kMaxH2 + 4;      // row stride of [row][o] tiles
 // row straight from global memory, so only the small combine tiles use LDS.
 // Then H2 = ReLU(Z2) and, for 3 layers, E = H2 W3^T + b3.
 //
-// After the stream-K forward (sk != 0, H = 256) the K half of wave w is the
-// 128-column tile (row block, w >> 1) of layer 1.  If a worker finished that
-// tile in place its H1 is read as is; otherwise the wave adds the workers'
-// partial tiles in K order, applies b1 and ReLU (ReLU(b1) for a row whose ID
-// is out of range) and writes the finished H1 for the backward.
+// After the stream-K forward (sk != 0) the K half of wave w lies in one
+// column tile of layer 1 (the row block's only tile when H = 256).  If a
+// worker finished that tile in place its H1 is read as is; otherwise the wave
+// adds the workers' partial tiles in K order, applies b1 and ReLU (ReLU(b1)
+// for a row whose ID is out of range) and writes the finished H1 for the
+// backward.
 template <int L>
 __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int H, int M,
                                                       int D, const void *__restrict__ W2,
@@ -614,7 +631,7 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
         const int rowc = min(row, n_u - 1);
         float *hrow = H1 + (size_t)rowc * H + kh * khalf + 16 * h;
         float4 areg[KB][4];
-        // this wave's K half lies in one 128-column tile of the stream-K grid
+        // this wave's K half lies in one column tile of the stream-K grid
         const int cbase = kh * khalf;                    // first column of the half
         const int cb = cbase / kSkBN;
         int wa = 0, wb = -1, slot_a = 0;
@@ -1200,7 +1217,8 @@ __global__ __launch_bounds__(kDwThreads) void dw1_part_f32(const float *__restri
         dw1_issue(ring1, T, n_rows, F, dZ1, H, m0, n0, DW_BASE(1), u1, zero_row, id1, wave, lane);
 #define DW_STAGE(cur, nxt, ids_next_dma, ids_load, s)                                          \
     do {                                                                                        \
-        AMS_WAIT_VM(R::OUTSTANDING);                                                            \
+        __builtin_amdgcn_sched_barrier(0);                                         \
+        AMS_WAIT_VM_LDS(R::OUTSTANDING);                                                        \
         __builtin_amdgcn_s_barrier();                                                           \
         __builtin_amdgcn_sched_barrier(0);                                                      \
         dw1_load_ids(uniq, DW_BASE((s) + 4), u1, wave, lane, ids_load);                         \
