@@ -253,25 +253,35 @@ __global__ __launch_bounds__(kThreads) void l1_fwd_f32(const float *__restrict__
     }
 }
 
-// Stream-K fp32 forward of the 4096-wide layer (used when H is a multiple of
-// 256).  Work = (128-row x 256-column tile, 32-wide K stage) iterations in
-// tile-major order; each of G persistent workers (one 8-wave block per CU)
-// takes an equal contiguous share, so every CU gets the same MFMA work for
-// any number of unique images.  A tile fully inside one worker's share is
-// finished in place (bias, ReLU); a tile cut by a share boundary leaves one
-// partial accumulator tile per worker, and the tail forward (which reads H1
-// anyway) adds the pieces in K order.  Waves are 4 (M) x 2 (N), 32 x 128
-// each; the 3-slot DMA ring and the row swizzle are those of l1_fwd_f32 with
-// 384 tile rows (128 A + 256 B).  With the whole hidden width in one tile a
-// feature row is read from HBM once, and a K stage carries 64 MFMAs per wave
+// Stream-K forward of the 4096-wide layer (used when H is a multiple of
+// 256).  Work = (128-row x 256-column tile, K stage) iterations in tile-major
+// order; a K stage is 128 bytes of every operand row (32 fp32 or 64 bf16).
+// Each of G persistent workers (one 8-wave block per CU) takes an equal
+// contiguous share, so every CU gets the same MFMA work for any number of
+// unique images.  A tile fully inside one worker's share is finished in place
+// (bias, ReLU); a tile cut by a share boundary leaves one partial accumulator
+// tile per worker, and the tail forward (which reads H1 anyway) adds the
+// pieces in K order.  Waves are 4 (M) x 2 (N), 32 x 128 each; the 3-slot DMA
+// ring and the row swizzle are those of l1_fwd_f32 with 384 tile rows (128 A
+// + 256 B).  With the whole hidden width in one tile a feature row is read
+// from HBM once, and a K stage carries 64 fp32 (or 16 bf16) MFMAs per wave
 // for its 6 DMA instructions.
+//
+// fp32: within a stage lane l supplies k = 16*(l/32) + 4*g + e to element e
+// of k-group g (one 32x32x2 MFMA per element).  bf16: the same 16-byte chunk
+// holds 8 values, k = 32*(l/32) + 8*g + e, one 32x32x16 MFMA per group.  A
+// and B agree, so the sum over the stage's k is unchanged.
 constexpr int kSkThreads = 512;
-constexpr int kSkBM = 128, kSkBN = 256, kSkBK = 32;
+constexpr int kSkBM = 128, kSkBN = 256;
 constexpr int kSkNB = kSkBN / 64;                         // 32-column MFMA blocks per wave: 4
-constexpr int kSkSlot = (kSkBM + kSkBN) * kSkBK;          // floats per ring slot (48 KB)
+constexpr int kSkRowBytes = 128;                          // bytes of an operand row per stage
+constexpr int kSkSlot = (kSkBM + kSkBN) * kSkRowBytes / 4;  // floats per ring slot (48 KB)
 constexpr int kSkPW = (kSkBM + kSkBN) / 8 / 8;            // DMA instructions per wave: 6
 constexpr int kSkTile = kSkBM * kSkBN;
 constexpr int kSkMinIters = 32;                           // smallest share worth a worker
+
+template <typename TT>
+constexpr int sk_bk() { return kSkRowBytes / (int)sizeof(TT); }   // K per stage
 
 struct SkPlan {
     int n_u, n_cb, S, g;            // g = workers in use
@@ -280,12 +290,12 @@ struct SkPlan {
     __device__ int owner(int64_t it) const { return (int)(((it + 1) * g - 1) / total); }
 };
 
-__device__ __forceinline__ SkPlan sk_plan(int n_u, int H, int F, int G)
+__device__ __forceinline__ SkPlan sk_plan(int n_u, int H, int F, int G, int bk)
 {
     SkPlan p;
     p.n_u = n_u;
     p.n_cb = H / kSkBN;
-    p.S = F / kSkBK;
+    p.S = F / bk;
     const int64_t tiles = (int64_t)((n_u + kSkBM - 1) / kSkBM) * p.n_cb;
     p.total = tiles * p.S;
     const int64_t want = (p.total + kSkMinIters - 1) / kSkMinIters;
@@ -294,54 +304,68 @@ __device__ __forceinline__ SkPlan sk_plan(int n_u, int H, int F, int G)
     return p;
 }
 
-__device__ __forceinline__ void sk_issue(float *slot, const float *const *src, int k0, int wave)
+// src[q] are byte pointers; k0b is the stage's byte offset within a row
+__device__ __forceinline__ void sk_issue(float *slot, const char *const *src, int64_t k0b, int wave)
 {
 #pragma unroll
-    for (int q = 0; q < kSkPW; ++q) dma16(src[q] + k0, slot + (wave * kSkPW + q) * 256);
+    for (int q = 0; q < kSkPW; ++q) dma16(src[q] + k0b, slot + (wave * kSkPW + q) * 256);
 }
 
+template <typename TT>
 __device__ __forceinline__ void sk_compute(const float *slot, v16f *acc, int lane, int wave)
 {
     const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
     const int ra = wm * 32 + r32;
-    float4 a[4], b[4][kSkNB];
+    uint4 a[4], b[4][kSkNB];
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
         const int q = h * 4 + g;
-        a[g] = *(const float4 *)&slot[ra * 32 + ((q ^ ring_swz(ra)) << 2)];
+        a[g] = *(const uint4 *)&slot[ra * 32 + ((q ^ ring_swz(ra)) << 2)];
 #pragma unroll
         for (int nb = 0; nb < kSkNB; ++nb) {
             const int rb = kSkBM + wn * (kSkBN / 2) + nb * 32 + r32;
-            b[g][nb] = *(const float4 *)&slot[rb * 32 + ((q ^ ring_swz(rb)) << 2)];
+            b[g][nb] = *(const uint4 *)&slot[rb * 32 + ((q ^ ring_swz(rb)) << 2)];
         }
     }
+    constexpr int PER_G = sizeof(TT) == 4 ? 4 : 1;           // MFMAs per (group, block)
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-        const float av[4] = {a[g].x, a[g].y, a[g].z, a[g].w};
+        if constexpr (sizeof(TT) == 4) {
+            const float av[4] = {__uint_as_float(a[g].x), __uint_as_float(a[g].y), __uint_as_float(a[g].z),
+                                 __uint_as_float(a[g].w)};
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
+            for (int e = 0; e < 4; ++e)
 #pragma unroll
-            for (int nb = 0; nb < kSkNB; ++nb) {
-                const float bv[4] = {b[g][nb].x, b[g][nb].y, b[g][nb].z, b[g][nb].w};
-                acc[nb] = mfma_f32(av[e], bv[e], acc[nb]);
-            }
+                for (int nb = 0; nb < kSkNB; ++nb) {
+                    const float bv[4] = {__uint_as_float(b[g][nb].x), __uint_as_float(b[g][nb].y),
+                                         __uint_as_float(b[g][nb].z), __uint_as_float(b[g][nb].w)};
+                    acc[nb] = mfma_f32(av[e], bv[e], acc[nb]);
+                }
+        } else {
+#pragma unroll
+            for (int nb = 0; nb < kSkNB; ++nb) acc[nb] = mfma_bf16(a[g], b[g][nb], acc[nb]);
+        }
     }
     // group 0's reads first, then (reads of g+1, MFMAs of g)
     __builtin_amdgcn_sched_group_barrier(0x100, 1 + kSkNB, 0);
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
         if (g < 3) __builtin_amdgcn_sched_group_barrier(0x100, 1 + kSkNB, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 4 * kSkNB, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, PER_G * kSkNB, 0);
     }
 }
 
-__global__ __launch_bounds__(kSkThreads) void l1sk_f32(const float *__restrict__ T, int64_t n_rows, int F,
-                                                        const int32_t *__restrict__ uniq,
-                                                        const int32_t *__restrict__ n_uniq_p, int cap,
-                                                        const float *__restrict__ W1,
-                                                        const float *__restrict__ b1, int H, int G,
-                                                        float *__restrict__ H1, float *__restrict__ pbuf)
+// H1b (bf16 mode): the bf16 copy of H1 kept for the backward, written with H1
+// for tiles finished in place.
+template <typename TT>
+__global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int64_t n_rows, int F,
+                                                   const int32_t *__restrict__ uniq,
+                                                   const int32_t *__restrict__ n_uniq_p, int cap,
+                                                   const TT *__restrict__ W1, const float *__restrict__ b1,
+                                                   int H, int G, float *__restrict__ H1,
+                                                   uint16_t *__restrict__ H1b, float *__restrict__ pbuf)
 {
+    constexpr int BK = sk_bk<TT>();
     __shared__ __attribute__((aligned(16))) float ring0[kSkSlot];
     __shared__ __attribute__((aligned(16))) float ring1[kSkSlot];
     __shared__ __attribute__((aligned(16))) float ring2[kSkSlot];
@@ -349,13 +373,14 @@ __global__ __launch_bounds__(kSkThreads) void l1sk_f32(const float *__restrict__
 
     const int n_u = min(*n_uniq_p, cap);
     if (n_u <= 0) return;
-    const SkPlan P = sk_plan(n_u, H, F, G);
+    const SkPlan P = sk_plan(n_u, H, F, G, BK);
     // workers with consecutive shares sit on one XCD (blocks go round-robin)
     const int w = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
     if (w >= P.g) return;
     const int64_t it1 = P.it0(w + 1);
     const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
     const int S = P.S;
+    const size_t row_bytes = (size_t)F * sizeof(TT);
     bool first = true;
     for (int64_t it = P.it0(w); it < it1;) {
         const int tile = (int)(it / S);
@@ -372,16 +397,16 @@ __global__ __launch_bounds__(kSkThreads) void l1sk_f32(const float *__restrict__
             rid[t] = id;
         }
         __syncthreads();
-        const float *src[kSkPW];
+        const char *src[kSkPW];
 #pragma unroll
         for (int q = 0; q < kSkPW; ++q) {
             const int row = (wave * kSkPW + q) * 8 + (lane >> 3);
             const int chunk = (lane & 7) ^ ring_swz(row);
             if (row < kSkBM) {
                 const int id = rid[row];
-                src[q] = (id >= 0 ? T + (size_t)id * F : W1) + chunk * 4;
+                src[q] = (id >= 0 ? (const char *)T + (size_t)id * row_bytes : (const char *)W1) + chunk * 16;
             } else {
-                src[q] = W1 + (size_t)(n0 + row - kSkBM) * F + chunk * 4;
+                src[q] = (const char *)W1 + (size_t)(n0 + row - kSkBM) * row_bytes + chunk * 16;
             }
         }
         v16f acc[kSkNB];
@@ -394,12 +419,12 @@ __global__ __launch_bounds__(kSkThreads) void l1sk_f32(const float *__restrict__
         AMS_WAIT_VM_LDS(kSkPW);                                                    \
         __builtin_amdgcn_s_barrier();                                              \
         __builtin_amdgcn_sched_barrier(0);                                         \
-        sk_issue(nxt, src, (ks + min((s) + 2, n - 1)) * kSkBK, wave);              \
+        sk_issue(nxt, src, (int64_t)(ks + min((s) + 2, n - 1)) * kSkRowBytes, wave); \
         __builtin_amdgcn_sched_barrier(0);                                         \
-        sk_compute(cur, acc, lane, wave);                                          \
+        sk_compute<TT>(cur, acc, lane, wave);                                      \
     } while (0)
-        sk_issue(ring0, src, ks * kSkBK, wave);
-        sk_issue(ring1, src, (ks + min(1, n - 1)) * kSkBK, wave);
+        sk_issue(ring0, src, (int64_t)ks * kSkRowBytes, wave);
+        sk_issue(ring1, src, (int64_t)(ks + min(1, n - 1)) * kSkRowBytes, wave);
         int s = 0;
         for (; s + 3 <= n; s += 3) {
             SK_STAGE(ring0, ring2, s);
@@ -420,8 +445,11 @@ __global__ __launch_bounds__(kSkThreads) void l1sk_f32(const float *__restrict__
 #pragma unroll
                 for (int j = 0; j < 16; ++j) {
                     const int r = wm * 32 + acc_row(j, lane);
-                    const float z = rid[r] >= 0 ? acc[nb][j] + bias : bias;
-                    if (m0 + r < n_u) H1[(size_t)(m0 + r) * H + col] = fmaxf(z, 0.f);
+                    const float z = fmaxf(rid[r] >= 0 ? acc[nb][j] + bias : bias, 0.f);
+                    if (m0 + r < n_u) {
+                        H1[(size_t)(m0 + r) * H + col] = z;
+                        if (H1b) H1b[(size_t)(m0 + r) * H + col] = ams_f32_to_bf16(z);
+                    }
                 }
             }
         } else {
@@ -586,7 +614,7 @@ constexpr int kTailLDo = kMaxH2 + 4;      // row stride of [row][o] tiles
 // row straight from global memory, so only the small combine tiles use LDS.
 // Then H2 = ReLU(Z2) and, for 3 layers, E = H2 W3^T + b3.
 //
-// After the stream-K forward (sk != 0) the K half of wave w lies in one
+// After the stream-K forward (sk_bk != 0: its K per stage) the K half of wave w lies in one
 // column tile of layer 1 (the row block's only tile when H = 256).  If a
 // worker finished that tile in place its H1 is read as is; otherwise the wave
 // adds the workers' partial tiles in K order, applies b1 and ReLU (ReLU(b1)
@@ -601,8 +629,9 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
                                                       int final_relu,
                                                       const int32_t *__restrict__ n_uniq_p, int cap,
                                                       float *__restrict__ H2_save,
-                                                      float *__restrict__ E, int sk, int F, int G,
+                                                      float *__restrict__ E, int sk_bk, int F, int G,
                                                       const float *__restrict__ pbuf,
+                                                      uint16_t *__restrict__ H1b,
                                                       const float *__restrict__ b1,
                                                       const int32_t *__restrict__ uniq, int64_t n_rows)
 {
@@ -635,8 +664,8 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
         const int cbase = kh * khalf;                    // first column of the half
         const int cb = cbase / kSkBN;
         int wa = 0, wb = -1, slot_a = 0;
-        if (sk) {
-            const SkPlan P = sk_plan(n_u, H, F, G);
+        if (sk_bk) {
+            const SkPlan P = sk_plan(n_u, H, F, G, sk_bk);
             const int tile = (rowc / kSkBM) * P.n_cb + cb;
             wa = P.owner((int64_t)tile * P.S);
             wb = P.owner((int64_t)(tile + 1) * P.S - 1);
@@ -670,7 +699,15 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
                         a.y = fmaxf(ok ? a.y + bb.y : bb.y, 0.f);
                         a.z = fmaxf(ok ? a.z + bb.z : bb.z, 0.f);
                         a.w = fmaxf(ok ? a.w + bb.w : bb.w, 0.f);
-                        if (nb == 0 && row < n_u) *(float4 *)(hrow + kb * 32 + 4 * q) = a;
+                        if (nb == 0 && row < n_u) {
+                            *(float4 *)(hrow + kb * 32 + 4 * q) = a;
+                            if (H1b) {
+                                uint16_t *hb = H1b + (size_t)rowc * H + col;
+                                const uint32_t lo = ams_f32_to_bf16(a.x) | ((uint32_t)ams_f32_to_bf16(a.y) << 16);
+                                const uint32_t hi = ams_f32_to_bf16(a.z) | ((uint32_t)ams_f32_to_bf16(a.w) << 16);
+                                *(uint2 *)hb = make_uint2(lo, hi);
+                            }
+                        }
                     }
                     areg[kb][q] = a;
                 }
@@ -1256,6 +1293,207 @@ __global__ __launch_bounds__(kDwThreads) void dw1_part_f32(const float *__restri
         }
 }
 
+// bf16 partial dW1 = dZ1^T T[uniq] over one fixed chunk of unique images,
+// for H = 256: a block owns all 256 rows of dW1 and 128 of its columns, so a
+// feature row is read once per chunk.  The contraction runs over unique
+// images, the row index of both operands, while the bf16 MFMA wants 8
+// consecutive k per lane: both tiles sit in LDS row-major ([image][column])
+// and are read with ds_read_b64_tr_b16, which hands lane j of a 16-lane group
+// column (base + j) of four consecutive rows when lane i of the group points
+// at row (i / 4), columns 4 (i % 4) .. +3.  Two such reads give the 8 values
+// of one operand.
+//
+// Stage = 64 images (4 MFMA k-steps of 16): A = dZ1 rows (64 x 256 bf16,
+// 32 KB), B = feature rows (64 x 128 bf16, 16 KB), DMA'd through a 3-slot
+// ring like the fp32 kernel.  16-byte chunks are stored at chunk ^ 4 (row & 3):
+// the 4 rows x 64 bytes that a half-wave's transpose reads touch then fall
+// in distinct banks.  Waves are 4 (h) x 2 (f), 64 x 64 each.
+struct DwTr {
+    static constexpr int BM = 256, BN = 128, BK = 64, WAVES = 8;
+    static constexpr int A_BYTES = BK * BM * 2, B_BYTES = BK * BN * 2;
+    static constexpr int SLOT = (A_BYTES + B_BYTES) / 4;           // floats per slot (48 KB)
+    static constexpr int PA = A_BYTES / 1024 / WAVES;             // 4 DMA instructions per wave
+    static constexpr int PB = B_BYTES / 1024 / WAVES;             // 2
+    static constexpr int OUTSTANDING = PA + PB + PB;              // DMA of s+1, IDs of s+3
+};
+
+__device__ __forceinline__ int dwtr_swz(int row) { return (row & 3) << 2; }
+
+typedef short v4s __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s lds_v4s_t;
+
+__device__ __forceinline__ uint2 ds_read_tr16(const void *p)
+{
+    const v4s v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s_t *)p);
+    return __builtin_bit_cast(uint2, v);
+}
+
+// IDs of this lane's B rows (one per B DMA instruction) of the stage at u_base
+__device__ __forceinline__ void dwtr_load_ids(const int32_t *__restrict__ uniq, int u_base, int u1, int wave,
+                                              int lane, int (&id)[2])
+{
+#pragma unroll
+    for (int q = 0; q < DwTr::PB; ++q) {
+        const int row = 4 * (DwTr::PB * wave + q) + (lane >> 4);
+        const int u = u_base + row;
+        const int v = uniq[min(u, u1 - 1)];           // always issued: uniform op count
+        id[q] = u < u1 ? v : -1;
+    }
+}
+
+__device__ __forceinline__ void dwtr_issue(float *slot, const uint16_t *__restrict__ T, int64_t n_rows, int F,
+                                           const uint16_t *__restrict__ dZ1, int n0, int u_base, int u1,
+                                           const void *__restrict__ zero_row, const int (&id)[2], int wave,
+                                           int lane)
+{
+    // A: 512-byte rows, 2 per instruction
+#pragma unroll
+    for (int q = 0; q < DwTr::PA; ++q) {
+        const int j = DwTr::PA * wave + q;
+        const int row = 2 * j + (lane >> 5), pc = lane & 31;
+        const int u = u_base + row;
+        const int lc = pc ^ dwtr_swz(row);
+        const char *src = u < u1 ? (const char *)(dZ1 + (size_t)u * DwTr::BM) + lc * 16
+                                 : (const char *)zero_row + lc * 16;
+        dma16(src, slot + j * 256);
+    }
+    // B: 256-byte rows (128 columns from n0), 4 per instruction
+#pragma unroll
+    for (int q = 0; q < DwTr::PB; ++q) {
+        const int j = DwTr::PB * wave + q;
+        const int row = 4 * j + (lane >> 4), pc = lane & 15;
+        const int lc = pc ^ dwtr_swz(row);
+        const bool ok = id[q] >= 0 && (int64_t)id[q] < n_rows;
+        const char *src = ok ? (const char *)(T + (size_t)id[q] * F + n0) + lc * 16
+                             : (const char *)zero_row + lc * 16;
+        dma16(src, slot + DwTr::A_BYTES / 4 + j * 256);
+    }
+}
+
+// Byte offset of (row, col) in a swizzled bf16 tile with `rb`-byte rows.
+__device__ __forceinline__ int dwtr_off(int row, int col, int rb)
+{
+    return row * rb + (((col >> 3) ^ dwtr_swz(row)) << 4) + ((col & 7) << 1);
+}
+
+__device__ __forceinline__ void dwtr_compute(const float *slot, v16f *acc, int lane, int wave)
+{
+    const char *A = (const char *)slot, *B = (const char *)slot + DwTr::A_BYTES;
+    const int g = lane >> 4, i = lane & 15;
+    const int wm = wave >> 1, wn = wave & 1;
+    // this lane's transpose-read address: row (i / 4) of its group's 4-row
+    // block, columns 4 (i % 4) .. +3 of its group's 16-column half
+    const int r_in = 8 * (g >> 1) + (i >> 2);
+    const int c_in = 16 * (g & 1) + 4 * (i & 3);
+    uint4 a[4][2], b[4][2];
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+        const int r0 = 16 * kk + r_in;
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+            const int col = wm * 64 + mb * 32 + c_in;
+            const uint2 lo = ds_read_tr16(A + dwtr_off(r0, col, DwTr::BM * 2));
+            const uint2 hi = ds_read_tr16(A + dwtr_off(r0 + 4, col, DwTr::BM * 2));
+            a[kk][mb] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        }
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+            const int col = wn * 64 + nb * 32 + c_in;
+            const uint2 lo = ds_read_tr16(B + dwtr_off(r0, col, DwTr::BN * 2));
+            const uint2 hi = ds_read_tr16(B + dwtr_off(r0 + 4, col, DwTr::BN * 2));
+            b[kk][nb] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        }
+    }
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk)
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb) acc[mb * 2 + nb] = mfma_bf16(a[kk][mb], b[kk][nb], acc[mb * 2 + nb]);
+    // k-step 0's reads first, then (reads of kk+1, MFMAs of kk)
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+#pragma unroll
+    for (int kk = 0; kk < 4; ++kk) {
+        if (kk < 3) __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    }
+}
+
+__global__ __launch_bounds__(DwTr::WAVES * AMS_WAVE) void dw1_part_bf16(
+    const uint16_t *__restrict__ T, int64_t n_rows, int F, const int32_t *__restrict__ uniq,
+    const int32_t *__restrict__ n_uniq_p, int cap, const uint16_t *__restrict__ dZ1, int KC,
+    const void *__restrict__ zero_row, float *__restrict__ part)
+{
+    using R = DwTr;
+    __shared__ __attribute__((aligned(16))) float ring0[R::SLOT];
+    __shared__ __attribute__((aligned(16))) float ring1[R::SLOT];
+    __shared__ __attribute__((aligned(16))) float ring2[R::SLOT];
+
+    const int nnt = F / R::BN;
+    // the column tiles of one chunk go to one XCD: they share its dZ1 rows
+    int c, nt;
+    if (!xcd_tile(blockIdx.x, KC, nnt, c, nt)) return;
+    const int n_u = min(*n_uniq_p, cap);
+    const int u0 = (int)((int64_t)c * n_u / KC), u1 = (int)((int64_t)(c + 1) * n_u / KC);
+    const int n0 = nt * R::BN;
+    const int lane = ams_lane(), wave = threadIdx.x / AMS_WAVE;
+
+    v16f acc[4] = {(v16f){}, (v16f){}, (v16f){}, (v16f){}};
+    const int S = (u1 - u0 + R::BK - 1) / R::BK;
+    if (S > 0) {
+        int id0[2], id1[2], id2[2];
+#define DT_BASE(s) (u0 + min((s), S - 1) * R::BK)
+        dwtr_load_ids(uniq, DT_BASE(0), u1, wave, lane, id0);
+        dwtr_load_ids(uniq, DT_BASE(1), u1, wave, lane, id1);
+        dwtr_load_ids(uniq, DT_BASE(2), u1, wave, lane, id2);
+        AMS_WAIT_VM(0);
+        int idn[2];
+        dwtr_load_ids(uniq, DT_BASE(3), u1, wave, lane, idn);
+        dwtr_issue(ring0, T, n_rows, F, dZ1, n0, DT_BASE(0), u1, zero_row, id0, wave, lane);
+        dwtr_issue(ring1, T, n_rows, F, dZ1, n0, DT_BASE(1), u1, zero_row, id1, wave, lane);
+#define DT_STAGE(cur, nxt, ids_next_dma, ids_load, s)                                           \
+    do {                                                                                         \
+        __builtin_amdgcn_sched_barrier(0);                                                       \
+        AMS_WAIT_VM_LDS(R::OUTSTANDING);                                                         \
+        __builtin_amdgcn_s_barrier();                                                            \
+        __builtin_amdgcn_sched_barrier(0);                                                       \
+        dwtr_load_ids(uniq, DT_BASE((s) + 4), u1, wave, lane, ids_load);                         \
+        dwtr_issue(nxt, T, n_rows, F, dZ1, n0, DT_BASE((s) + 2), u1, zero_row, ids_next_dma, wave, \
+                   lane);                                                                        \
+        __builtin_amdgcn_sched_barrier(0);                                                       \
+        dwtr_compute(cur, acc, lane, wave);                                                      \
+    } while (0)
+        id0[0] = idn[0];
+        id0[1] = idn[1];
+        // id2 = stage 2, id0 = stage 3 (in flight), id1 free
+        int s = 0;
+        for (; s + 3 <= S; s += 3) {
+            DT_STAGE(ring0, ring2, id2, id1, s);
+            DT_STAGE(ring1, ring0, id0, id2, s + 1);
+            DT_STAGE(ring2, ring1, id1, id0, s + 2);
+        }
+        if (s < S) DT_STAGE(ring0, ring2, id2, id1, s);
+        if (s + 1 < S) DT_STAGE(ring1, ring0, id0, id2, s + 1);
+#undef DT_STAGE
+#undef DT_BASE
+        AMS_WAIT_VM(0);
+    }
+
+    float *out = part + (size_t)c * R::BM * F;
+    const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) {
+            const int col = n0 + wn * 64 + nb * 32 + (lane & 31);
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const int row = wm * 64 + mb * 32 + acc_row(j, lane);
+                out[(size_t)row * F + col] = acc[mb * 2 + nb][j];
+            }
+        }
+}
+
 // ----------------------------------------------------------------- host
 
 bool mlp_ok(const ams_mlp *m)
@@ -1276,6 +1514,7 @@ size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 int sk_workers();
 
 bool use_dw_ring(const ams_mlp *m) { return m->dtype == AMS_F32 && m->dims[1] % 128 == 0 && m->dims[0] % 128 == 0; }
+bool use_dw_tr(const ams_mlp *m) { return m->dtype == AMS_BF16 && m->dims[1] == DwTr::BM && m->dims[0] % DwTr::BN == 0; }
 
 // Split-K chunk count of dW1: the DMA-ring kernel takes one block per CU
 // (tiles x chunks = CUs); the fallback kernel aims at ~1024 blocks.
@@ -1285,6 +1524,8 @@ int dw1_chunks(const ams_mlp *m)
     int kc;
     if (use_dw_ring(m)) {
         kc = sk_workers() / ((H / 128) * (F / 128));
+    } else if (use_dw_tr(m)) {
+        kc = sk_workers() / (F / DwTr::BN);
     } else {
         const int bm = (H % 128 == 0) ? 128 : 64;
         kc = 1024 / ((H / bm) * (F / 64));
@@ -1331,7 +1572,7 @@ int sk_workers()
     return (n / 8) * 8;
 }
 
-bool use_stream_k(const ams_mlp *m) { return m->dtype == AMS_F32 && m->dims[1] % kSkBN == 0; }
+bool use_stream_k(const ams_mlp *m) { return m->dims[1] % kSkBN == 0; }
 
 }  // namespace
 
@@ -1377,9 +1618,13 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
     const int n_mt = (cap + 63) / 64;
     const int NT = (H % 128 == 0) ? 128 : 64;
     const int grid = ((n_mt + 7) / 8) * 8 * (H / NT);
-    if (sk) {
-        AMS_LAUNCH("l1sk_f32", st, l1sk_f32<<<G, kSkThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, (const float *)W1, b1,
-                                           H, G, H1f, pbuf));
+    if (sk && !bf) {
+        AMS_LAUNCH("l1sk_f32", st, l1sk<float><<<G, kSkThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
+                                                                      (const float *)W1, b1, H, G, H1f, nullptr, pbuf));
+    } else if (sk) {
+        AMS_LAUNCH("l1sk_bf16", st, l1sk<uint16_t><<<G, kSkThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq, n_uniq,
+                                                                           cap, (const uint16_t *)W1, b1, H, G, H1f,
+                                                                           (uint16_t *)H1_save, pbuf));
     } else if (!bf) {
         if (NT == 128)
             AMS_LAUNCH("l1_fwd_f32", st, l1_fwd_f32<128><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, n_mt,
@@ -1397,14 +1642,17 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
                                                        cap, n_mt, (const uint16_t *)W1, b1, H, H1f,
                                                        (uint16_t *)H1_save));
     }
+    const int sk_bk = sk ? (bf ? 64 : 32) : 0;      // K per stream-K stage (128 bytes of a row)
     int tg = (cap + kTailRows - 1) / kTailRows;
     if (tg > 1024) tg = 1024;
     if (L == 3)
         AMS_LAUNCH("tail_fwd", st, tail_fwd<3><<<tg, kThreads, 0, st>>>(H1f, H, M, D, W2, b2, W3, b3, bf, mlp->final_relu, n_uniq,
-                                             cap, H2_save, E, sk, F, G, pbuf, b1, uniq, n_rows));
+                                             cap, H2_save, E, sk_bk, F, G, pbuf, bf ? (uint16_t *)H1_save : nullptr,
+                                             b1, uniq, n_rows));
     else
         AMS_LAUNCH("tail_fwd", st, tail_fwd<2><<<tg, kThreads, 0, st>>>(H1f, H, M, D, W2, b2, W3, b3, bf, mlp->final_relu, n_uniq,
-                                             cap, H2_save, E, sk, F, G, pbuf, b1, uniq, n_rows));
+                                             cap, H2_save, E, sk_bk, F, G, pbuf, bf ? (uint16_t *)H1_save : nullptr,
+                                             b1, uniq, n_rows));
     return ams_launch_status();
 }
 
@@ -1461,6 +1709,11 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
         const int grid8 = ((outer8 + 7) / 8) * 8 * (H / DwRing::BM);
         AMS_LAUNCH("dw1_part_f32", st, dw1_part_f32<<<grid8, kDwThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
                                                    (const float *)dz1, H, p.kc, zero, dw1p));
+    } else if (use_dw_tr(mlp)) {
+        const int gtr = ((p.kc + 7) / 8) * 8 * (F / DwTr::BN);
+        AMS_LAUNCH("dw1_part_bf16", st, dw1_part_bf16<<<gtr, DwTr::WAVES * AMS_WAVE, 0, st>>>(
+                                            (const uint16_t *)T, n_rows, F, uniq, n_uniq, cap, (const uint16_t *)dz1,
+                                            p.kc, zero, dw1p));
     } else if (!bf) {
         if (bm == 128)
             AMS_LAUNCH("dw1_part", st, dw1_part<128, float><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
