@@ -761,211 +761,320 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
     }
 }
 
-// Backward of the small layers.  Block g owns unique images
-// [g n_u / G, (g+1) n_u / G), walked in chunks of 32 rows.  Per chunk:
-//   dz_last = dE (masked by the last ReLU if any); for 3 layers
-//   dZ2 = (dz_last W3) * [H2 > 0], else dZ2 = dz_last;
-//   dH1 = dZ2 W2 on MFMA, dZ1 = dH1 * [H1 > 0] (written out for dW1);
-//   dW2 += dZ2^T H1 on MFMA (accumulators live across chunks);
-//   dW3, db1, db2, db3 accumulate on the vector units.
+// Backward of the small layers, entirely in registers.  Block g owns unique
+// images [g n_u / G, (g+1) n_u / G), walked in chunks of 32 rows; wave w of
+// the 4 owns H1 columns [64 w, 64 w + 64).  Per chunk, with dzl = dE (masked
+// by the last ReLU if any):
+//   dZ2 = (dzl W3) * [H2 > 0] on MFMA (for 2 layers dZ2 = dzl), computed in
+//       two layouts by swapping the MFMA operands: lanes <-> rows (operand of
+//       dH1) and lanes <-> outputs o (operand of dW2);
+//   dH1 = dZ2 W2 on MFMA, dZ1 = dH1 * [H1 > 0], written out for dW1;
+//   dW2 += dZ2^T H1, dW3 += dzl^T H2 (waves 0, 1) on MFMA; db* by lane sums.
+// The 32 k of each MFMA sum are assigned to (lane half, step) so that the k
+// of step j in half h is the accumulator row acc_row(j, lane): an
+// accumulator then serves as an operand of the next product unchanged, and
+// the H1 values that mask dZ1 are the same registers that feed dW2.
 // Partials per block: [dW2: Mo x H][db2: Mo][dW3: D x M][db3: D][db1: H].
-template <int L>
-__global__ __launch_bounds__(kThreads) void tail_bwd(const void *__restrict__ H1s, int h1_bf16,
-                                                      const float *__restrict__ H2s,
-                                                      const float *__restrict__ Efwd,
-                                                      const float *__restrict__ dE,
-                                                      const void *__restrict__ W2,
-                                                      const void *__restrict__ W3, int wbf16,
-                                                      int H, int M, int D, int final_relu,
-                                                      const int32_t *__restrict__ n_uniq_p, int cap,
-                                                      void *__restrict__ dZ1, int dz1_bf16,
-                                                      float *__restrict__ part, int PS,
-                                                      float *__restrict__ zero_row, int zero_n)
+// One wave per SIMD (4 waves x 64 columns), so that a whole chunk's loads fit
+// in registers and are in flight together.
+constexpr int kTbThreads = 256;
+constexpr int kTbCols = kMaxH1 / (kTbThreads / AMS_WAVE);   // 64 columns per wave
+
+template <typename T>
+__device__ __forceinline__ float ldf(const T *p, size_t i)
+{
+    if constexpr (sizeof(T) == 2) return ams_bf16_to_f32(p[i]);
+    else return p[i];
+}
+
+template <typename T>
+__device__ __forceinline__ void stf(T *p, size_t i, float v)
+{
+    if constexpr (sizeof(T) == 2) p[i] = ams_f32_to_bf16(v);
+    else p[i] = v;
+}
+
+// Buffer loads: a resource descriptor carries the byte size of the valid
+// range, and the hardware returns 0 for an offset past it, so the loads of a
+// chunk need no row bounds checks or branches (gfx9 descriptor word 3).
+typedef __amdgpu_buffer_rsrc_t brsrc_t;
+
+__device__ __forceinline__ brsrc_t make_buf(const void *p, uint32_t bytes)
+{
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(p), 0, bytes, 0x00020000);
+}
+
+template <typename T>
+__device__ __forceinline__ float buf_ld(brsrc_t r, uint32_t elem)
+{
+    if constexpr (sizeof(T) == 2)
+        return ams_bf16_to_f32(__builtin_amdgcn_raw_buffer_load_b16(r, elem * 2, 0, 0));
+    else
+        return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, elem * 4, 0, 0));
+}
+
+// Buffer store: dropped by the hardware past the descriptor's size.
+template <typename T>
+__device__ __forceinline__ void buf_st(brsrc_t r, uint32_t elem, float v)
+{
+    if constexpr (sizeof(T) == 2)
+        __builtin_amdgcn_raw_buffer_store_b16(ams_f32_to_bf16(v), r, elem * 2, 0, 0);
+    else
+        __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), r, elem * 4, 0, 0);
+}
+
+// Upstream gradient of the last layer at (chunk row rr, d), masked by its
+// ReLU; 0 for d >= D and (by the descriptor) for rows past the chunk.
+// (rE has size 0 when there is no final ReLU: its loads read 0 and are not
+// used.)
+__device__ __forceinline__ float tb_dzl(brsrc_t rdE, brsrc_t rE, int final_relu, int rr, int d, int D)
+{
+    const uint32_t x = (uint32_t)(rr * D + d);   // d >= D reads a neighbour (or 0) and is masked
+    const float g = buf_ld<float>(rdE, x), e = buf_ld<float>(rE, x);
+    return (d < D && (!final_relu || e > 0.f)) ? g : 0.f;
+}
+
+template <int L, int SD, typename TW, typename TH>
+__global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1s,
+                                                        const float *__restrict__ H2s,
+                                                        const float *__restrict__ Efwd,
+                                                        const float *__restrict__ dE,
+                                                        const TW *__restrict__ W2,
+                                                        const TW *__restrict__ W3, int H, int M, int D,
+                                                        int final_relu, const int32_t *__restrict__ n_uniq_p,
+                                                        int cap, TH *__restrict__ dZ1, float *__restrict__ part,
+                                                        int PS, float *__restrict__ zero_row, int zero_n)
 {
     // the zero row that dW1's padding rows stream (read by the next launch)
     if (blockIdx.x == 0)
-        for (int i = threadIdx.x; i < zero_n; i += kThreads) zero_row[i] = 0.f;
-    __shared__ __attribute__((aligned(16))) float Hc[kTailRows * kTailLD];   // [row][i]
-    __shared__ __attribute__((aligned(16))) float dz2s[kTailRows * kTailLDo];// [row][o]
-    __shared__ float W3s[kMaxD * kMaxH2];
-    __shared__ float h2c[kTailRows][kMaxH2 + 1];
-    __shared__ float dzl[kTailRows][kMaxD + 1];
-    const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
+        for (int i = threadIdx.x; i < zero_n; i += kTbThreads) zero_row[i] = 0.f;
+    const int lane = ams_lane(), wave = threadIdx.x / AMS_WAVE;
     const int h = lane >> 5, r32 = lane & 31;
     const int Mo = (L == 3) ? M : D;
-    // this wave's share of H: columns [64 wave, 64 wave + 64) (H <= 256)
-    const int i0 = 64 * wave;
-    const bool wave_on = i0 < H;
-    // B operand of dH1 = dZ2 W2, kept in registers: W2[o][i] for this lane's
-    // column i and o = k0 + 16 h + e (k0 = 0, 32; e = 0..15; o >= Mo reads 0)
-    float w2r[2][2][16];
-#pragma unroll
-    for (int nb = 0; nb < 2; ++nb)
-#pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-                const int o = kb * 32 + 16 * h + e, i = i0 + nb * 32 + r32;
-                w2r[nb][kb][e] = (wave_on && o < Mo) ? ld_w(W2, wbf16, (size_t)o * H + i) : 0.f;
-            }
-    if (L == 3)
-        for (int e = t; e < D * M; e += kThreads) W3s[e] = ld_w(W3, wbf16, e);
+    const int i0 = kTbCols * wave;            // this wave's H1 columns: icol(ib) = i0 + 32 ib + r32
+
+    // W2 (fp32, zero-padded to 64 x 256) and W3 (2 SD x 64) in LDS: operands of
+    // dH1 and dZ2, re-read per chunk (registers hold the chunk's data)
+    __shared__ float W2s[kMaxH2 * kMaxH1];
+    __shared__ float W3s[2 * SD * kMaxH2];
+    {
+        const brsrc_t rW2 = make_buf(W2, (uint32_t)(Mo * H * sizeof(TW)));   // rows o >= Mo read 0
+#pragma unroll 8
+        for (int e = threadIdx.x; e < kMaxH2 * kMaxH1; e += kTbThreads) {
+            const int o = e / kMaxH1, i = e % kMaxH1;
+            const float x = buf_ld<TW>(rW2, (uint32_t)(o * H + min(i, H - 1)));
+            W2s[e] = i < H ? x : 0.f;
+        }
+        const brsrc_t rW3 = make_buf(L == 3 ? W3 : W2, L == 3 ? (uint32_t)(D * M * sizeof(TW)) : 0u);
+        for (int e = threadIdx.x; e < 2 * SD * kMaxH2; e += kTbThreads) {
+            const int d = e / kMaxH2, o = e % kMaxH2;
+            const float x = buf_ld<TW>(rW3, (uint32_t)(d * M + min(o, M - 1)));
+            W3s[e] = o < M ? x : 0.f;
+        }
+    }
+    __syncthreads();
+
     const int n_u = min(*n_uniq_p, cap);
     const int r0 = (int)((int64_t)blockIdx.x * n_u / gridDim.x);
     const int r1 = (int)((int64_t)(blockIdx.x + 1) * n_u / gridDim.x);
 
-    v16f dw2[2][2];                          // [o block][i block]
-#pragma unroll
-    for (int a = 0; a < 2; ++a)
-#pragma unroll
-        for (int b = 0; b < 2; ++b) dw2[a][b] = (v16f){};
-    float db1a[2] = {0.f, 0.f};              // columns i0 + 32 nb + r32 (h == 0 lanes)
-    float dW3a[8];
-#pragma unroll
-    for (int q = 0; q < 8; ++q) dW3a[q] = 0.f;
-    float db2a = 0.f, db3a = 0.f;
+    v16f dw2[2][2] = {{(v16f){}, (v16f){}}, {(v16f){}, (v16f){}}};   // [o block][i block]
+    v16f dw3 = (v16f){};                     // wave ob < 2: lanes <-> o, rows d
+    float db1a[2] = {0.f, 0.f}, db2a[2] = {0.f, 0.f}, db3a = 0.f;
+    const bool w3_wave = (L == 3) && wave < 2 && 32 * wave < M;
 
-    for (int c0 = r0; c0 < r1; c0 += kTailRows) {
-        __syncthreads();
-        for (int r = wave; r < kTailRows; r += kThreads / AMS_WAVE)
-            for (int c = lane; c < H / 4; c += AMS_WAVE)
-                *(float4 *)&Hc[r * kTailLD + 4 * c] =
-                    c0 + r < r1 ? ld4_any(H1s, h1_bf16, (size_t)(c0 + r) * H + 4 * c)
-                                : make_float4(0.f, 0.f, 0.f, 0.f);
-        for (int e = t; e < kTailRows * D; e += kThreads) {
-            const int r = e / D, d = e % D;
-            float g = 0.f;
-            if (c0 + r < r1) {
-                g = dE[(size_t)(c0 + r) * D + d];
-                if (final_relu && !(Efwd[(size_t)(c0 + r) * D + d] > 0.f)) g = 0.f;
+    for (int c0 = r0; c0 < r1; c0 += 32) {
+        // descriptors over the chunk's rows [c0, min(c0 + 32, r1))
+        const uint32_t nr = (uint32_t)min(32, r1 - c0);
+        const brsrc_t rdE = make_buf(dE + (size_t)c0 * D, nr * D * 4);
+        const brsrc_t rE = make_buf(final_relu ? Efwd + (size_t)c0 * D : dE, final_relu ? nr * D * 4 : 0);
+        const brsrc_t rH2 = make_buf(L == 3 ? H2s + (size_t)c0 * M : dE, L == 3 ? nr * M * 4 : 0);
+        const brsrc_t rH1 = make_buf(H1s + (size_t)c0 * H, nr * H * (uint32_t)sizeof(TH));
+        const brsrc_t rZ1 = make_buf(dZ1 + (size_t)c0 * H, nr * H * (uint32_t)sizeof(TH));
+        // ==== phase 1: dZ2 with lanes <-> rows, dH1, dZ1 (one o block at a time)
+        float dzB[SD];                         // dzl[r32][2 s + h]
+#pragma unroll
+        for (int st = 0; st < SD; ++st) dzB[st] = tb_dzl(rdE, rE, final_relu, r32, 2 * st + h, D);
+        float h1v[2][16];                       // (columns past H read other data; never stored)
+#pragma unroll
+        for (int ib = 0; ib < 2; ++ib)
+#pragma unroll
+            for (int jj = 0; jj < 16; ++jj)
+                h1v[ib][jj] = buf_ld<TH>(rH1, (uint32_t)(acc_row(jj, lane) * H + i0 + 32 * ib + r32));
+        v16f a1[2] = {(v16f){}, (v16f){}};
+#pragma unroll
+        for (int ob = 0; ob < 2; ++ob) {
+            float dz2B[16];
+            if constexpr (L == 3) {
+                float h2B[16];
+#pragma unroll
+                for (int jj = 0; jj < 16; ++jj) {
+                    const int o = acc_row(jj, lane) + 32 * ob;
+                    const float x = buf_ld<float>(rH2, (uint32_t)(r32 * M + o));
+                    h2B[jj] = o < M ? x : 0.f;
+                }
+                v16f aB = (v16f){};
+#pragma unroll
+                for (int st = 0; st < SD; ++st)   // [o][row]: lanes <-> rows (zeros past D)
+                    aB = mfma_f32(W3s[(2 * st + h) * kMaxH2 + r32 + 32 * ob], dzB[st], aB);
+#pragma unroll
+                for (int jj = 0; jj < 16; ++jj) dz2B[jj] = h2B[jj] > 0.f ? aB[jj] : 0.f;
+            } else {   // 2 layers: dZ2 = dzl itself
+#pragma unroll
+                for (int jj = 0; jj < 16; ++jj)
+                    dz2B[jj] = tb_dzl(rdE, rE, final_relu, r32, acc_row(jj, lane) + 32 * ob, D);
             }
-            dzl[r][d] = g;
+#pragma unroll
+            for (int ib = 0; ib < 2; ++ib) {
+                float w2v[16];
+#pragma unroll
+                for (int jj = 0; jj < 16; ++jj)
+                    w2v[jj] = W2s[(acc_row(jj, lane) + 32 * ob) * kMaxH1 + ((i0 + 32 * ib + r32) & (kMaxH1 - 1))];
+#pragma unroll
+                for (int jj = 0; jj < 16; ++jj) a1[ib] = mfma_f32(dz2B[jj], w2v[jj], a1[ib]);
+            }
         }
-        if (L == 3)
-            for (int e = t; e < kTailRows * M; e += kThreads) {
-                const int r = e / M, o = e % M;
-                h2c[r][o] = c0 + r < r1 ? H2s[(size_t)(c0 + r) * M + o] : 0.f;
+#pragma unroll
+        for (int ib = 0; ib < 2; ++ib) {
+            // dZ1 = dH1 * [H1 > 0], written out (stores past the chunk are
+            // dropped by the descriptor; columns past H are not stored); db1
+            const int icol = i0 + 32 * ib + r32;
+            float cs = 0.f;
+#pragma unroll
+            for (int jj = 0; jj < 16; ++jj) {
+                const float dz = h1v[ib][jj] > 0.f ? a1[ib][jj] : 0.f;
+                cs += dz;
+                if (icol < H) buf_st<TH>(rZ1, (uint32_t)(acc_row(jj, lane) * H + icol), dz);
             }
-        __syncthreads();
-        // dZ2, db2 (thread o), dW3 / db3 (vector units)
-        for (int e = t; e < kTailRows * kMaxH2; e += kThreads) {
-            const int r = e >> 6, o = e & (kMaxH2 - 1);
-            float dz = 0.f;
-            if (o < Mo) {
+            db1a[ib] += cs + __shfl_xor(cs, 32, AMS_WAVE);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+
+        // ==== phase 2: dZ2 with lanes <-> o; dW2, db2, dW3, db3 (one o block at a time)
+        float dA3[16];                          // dzl[row][d = r32] (dW3's operand, db3)
+#pragma unroll
+        for (int jj = 0; jj < 16; ++jj) dA3[jj] = tb_dzl(rdE, rE, final_relu, acc_row(jj, lane), r32, D);
+        {
+            float c3 = 0.f;
+#pragma unroll
+            for (int jj = 0; jj < 16; ++jj) c3 += dA3[jj];
+            db3a += c3 + __shfl_xor(c3, 32, AMS_WAVE);
+        }
+#pragma unroll
+        for (int ob = 0; ob < 2; ++ob) {
+            float h2A[16], dz2A[16];
+#pragma unroll
+            for (int jj = 0; jj < 16; ++jj) {
+                const int rr = acc_row(jj, lane), o = r32 + 32 * ob;
                 if (L == 3) {
-                    float dh = 0.f;
-                    for (int d = 0; d < D; ++d) dh += W3s[d * M + o] * dzl[r][d];
-                    dz = h2c[r][o] > 0.f ? dh : 0.f;
+                    const float x = buf_ld<float>(rH2, (uint32_t)(rr * M + o));
+                    h2A[jj] = o < M ? x : 0.f;
                 } else {
-                    dz = dzl[r][o];
+                    h2A[jj] = tb_dzl(rdE, rE, final_relu, rr, o, D);
                 }
             }
-            dz2s[r * kTailLDo + o] = dz;
-        }
-        if (L == 3) {
+            if constexpr (L == 3) {
+                v16f aA = (v16f){};
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                const int e = t + kThreads * q;
-                if (e < D * M) {
-                    const int d = e / M, o = e % M;
-                    float s = 0.f;
-                    for (int r = 0; r < kTailRows; ++r) s += dzl[r][d] * h2c[r][o];
-                    dW3a[q] += s;
-                }
+                for (int st = 0; st < SD; ++st)   // [row][o]: lanes <-> o (zeros past D)
+                    aA = mfma_f32(dzB[st], W3s[(2 * st + h) * kMaxH2 + r32 + 32 * ob], aA);
+#pragma unroll
+                for (int jj = 0; jj < 16; ++jj) dz2A[jj] = h2A[jj] > 0.f ? aA[jj] : 0.f;
+            } else {
+#pragma unroll
+                for (int jj = 0; jj < 16; ++jj) dz2A[jj] = h2A[jj];
             }
-            if (t < D) {
-                float s = 0.f;
-                for (int r = 0; r < kTailRows; ++r) s += dzl[r][t];
-                db3a += s;
-            }
-        }
-        __syncthreads();
-        if (t < Mo) {
-            float s = 0.f;
-            for (int r = 0; r < kTailRows; ++r) s += dz2s[r * kTailLDo + t];
-            db2a += s;
-        }
-        if (wave_on) {
-            // dH1 = dZ2 W2 : rows x [i0, i0 + 64), K = 64 (padded o)
-            v16f acc[2] = {(v16f){}, (v16f){}};
 #pragma unroll
-            for (int kb = 0; kb < 2; ++kb) {
-                float a[16];
-                const float *pa = &dz2s[r32 * kTailLDo + kb * 32 + 16 * h];
+            for (int ib = 0; ib < 2; ++ib)   // dW2 += dZ2^T H1
 #pragma unroll
-                for (int q = 0; q < 4; ++q) *(float4 *)&a[4 * q] = *(const float4 *)(pa + 4 * q);
+                for (int jj = 0; jj < 16; ++jj) dw2[ob][ib] = mfma_f32(dz2A[jj], h1v[ib][jj], dw2[ob][ib]);
+            float cs = 0.f;
 #pragma unroll
-                for (int i = 0; i < 16; ++i)
+            for (int jj = 0; jj < 16; ++jj) cs += dz2A[jj];
+            db2a[ob] += cs + __shfl_xor(cs, 32, AMS_WAVE);
+            if (w3_wave && wave == ob) {   // dW3 += dzl^T H2 over this o block
 #pragma unroll
-                    for (int nb = 0; nb < 2; ++nb) acc[nb] = mfma_f32(a[i], w2r[nb][kb][i], acc[nb]);
-            }
-            // dZ1 = dH1 * [H1 > 0]; write it out and sum it per column for db1
-#pragma unroll
-            for (int nb = 0; nb < 2; ++nb) {
-                const int i = i0 + nb * 32 + r32;
-                float colsum = 0.f;
-#pragma unroll
-                for (int j = 0; j < 16; ++j) {
-                    const int r = acc_row(j, lane);
-                    const float dz = Hc[r * kTailLD + i] > 0.f ? acc[nb][j] : 0.f;
-                    colsum += dz;
-                    if (c0 + r < r1) {
-                        const size_t x = (size_t)(c0 + r) * H + i;
-                        if (dz1_bf16)
-                            ((uint16_t *)dZ1)[x] = ams_f32_to_bf16(dz);
-                        else
-                            ((float *)dZ1)[x] = dz;
-                    }
-                }
-                colsum += __shfl_xor(colsum, 32, AMS_WAVE);   // the other 16 rows of this column
-                db1a[nb] += colsum;
-            }
-            // dW2 += dZ2^T H1 : o in [0, 64) x i in [i0, i0 + 64), K = 32 rows
-#pragma unroll
-            for (int kk = 0; kk < kTailRows / 2; ++kk) {
-                const int r = 2 * kk + h;
-                float av[2], bv[2];
-#pragma unroll
-                for (int ob = 0; ob < 2; ++ob) av[ob] = dz2s[r * kTailLDo + ob * 32 + r32];
-#pragma unroll
-                for (int ib = 0; ib < 2; ++ib) bv[ib] = Hc[r * kTailLD + i0 + ib * 32 + r32];
-#pragma unroll
-                for (int ob = 0; ob < 2; ++ob)
-#pragma unroll
-                    for (int ib = 0; ib < 2; ++ib) dw2[ob][ib] = mfma_f32(av[ob], bv[ib], dw2[ob][ib]);
+                for (int jj = 0; jj < 16; ++jj) dw3 = mfma_f32(dA3[jj], h2A[jj], dw3);
             }
         }
     }
 
     float *p = part + (size_t)blockIdx.x * PS;
-    if (wave_on) {
 #pragma unroll
-        for (int ob = 0; ob < 2; ++ob)
+    for (int ob = 0; ob < 2; ++ob)
 #pragma unroll
-            for (int ib = 0; ib < 2; ++ib)
+        for (int ib = 0; ib < 2; ++ib) {
+            const int icol = i0 + 32 * ib + r32;
 #pragma unroll
-                for (int j = 0; j < 16; ++j) {
-                    const int o = ob * 32 + acc_row(j, lane);
-                    if (o < Mo) p[o * H + i0 + ib * 32 + r32] = dw2[ob][ib][j];
-                }
-    }
+            for (int jj = 0; jj < 16; ++jj) {
+                const int o = acc_row(jj, lane) + 32 * ob;
+                if (o < Mo && icol < H) p[(size_t)o * H + icol] = dw2[ob][ib][jj];
+            }
+        }
     p += Mo * H;
-    if (t < Mo) p[t] = db2a;
+    if (wave == 0 && h == 0) {
+        if (r32 < Mo) p[r32] = db2a[0];
+        if (32 + r32 < Mo) p[32 + r32] = db2a[1];
+    }
     p += Mo;
     if (L == 3) {
+        if (w3_wave) {
+            const int o = 32 * wave + r32;
 #pragma unroll
-        for (int q = 0; q < 8; ++q) {
-            const int e = t + kThreads * q;
-            if (e < D * M) p[e] = dW3a[q];
+            for (int jj = 0; jj < 16; ++jj) {
+                const int d = acc_row(jj, lane);
+                if (d < D && o < M) p[d * M + o] = dw3[jj];
+            }
         }
         p += D * M;
-        if (t < D) p[t] = db3a;
+        if (wave == 0 && h == 0 && r32 < D) p[r32] = db3a;
         p += D;
     }
-    if (wave_on && h == 0) {
-        p[i0 + r32] = db1a[0];
-        p[i0 + 32 + r32] = db1a[1];
+    if (h == 0) {
+        if (i0 + r32 < H) p[i0 + r32] = db1a[0];
+        if (i0 + 32 + r32 < H) p[i0 + 32 + r32] = db1a[1];
     }
+}
+
+// Sum of the tail backward's block partials, written straight into dW2, db2,
+// dW3, db3 and db1.  Thread (e, q) of a block sums partials g = q, q + 4, ...
+// in eight running chains (independent loads in flight); the chains, then the
+// four q, are added in a fixed order, so the result is deterministic.
+__global__ __launch_bounds__(256) void tail_reduce(const float *__restrict__ part, int G, int PS, int L,
+                                                   int H, int M, int D, float *__restrict__ dW2,
+                                                   float *__restrict__ db2, float *__restrict__ dW3,
+                                                   float *__restrict__ db3, float *__restrict__ db1)
+{
+    __shared__ float sq[4][64];
+    const int t = threadIdx.x, q = t >> 6;
+    const int e = blockIdx.x * 64 + (t & 63);
+    float c[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    if (e < PS) {
+        int k = 0;
+        for (; q + 4 * (k + 7) < G; k += 8)
+#pragma unroll
+            for (int r = 0; r < 8; ++r) c[r] += part[(size_t)(q + 4 * (k + r)) * PS + e];
+        for (int r = 0; r < 8 && q + 4 * (k + r) < G; ++r) c[r] += part[(size_t)(q + 4 * (k + r)) * PS + e];
+    }
+    float tot = 0.f;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) tot += c[r];
+    sq[q][t & 63] = tot;
+    __syncthreads();
+    if (q != 0 || e >= PS) return;
+    const float v = ((sq[0][t] + sq[1][t]) + sq[2][t]) + sq[3][t];
+    const int Mo = (L == 3) ? M : D;
+    const int n2 = Mo * H, n3 = (L == 3) ? D * M : 0, nb3 = (L == 3) ? D : 0;
+    int x = e;
+    if (x < n2) { dW2[x] = v; return; }
+    x -= n2;
+    if (x < Mo) { db2[x] = v; return; }
+    x -= Mo;
+    if (x < n3) { dW3[x] = v; return; }
+    x -= n3;
+    if (x < nb3) { db3[x] = v; return; }
+    x -= nb3;
+    db1[x] = v;
 }
 
 // out[e] = sum of part[g * PS + e] over g = 0..G-1, in a fixed association:
@@ -989,29 +1098,6 @@ __global__ __launch_bounds__(kThreads) void partial_reduce(const float *__restri
 }
 
 // Scatter the reduced tail partials into the caller's gradient arrays.
-__global__ __launch_bounds__(kThreads) void tail_unpack(const float *__restrict__ r, int L, int H,
-                                                         int M, int D, float *__restrict__ dW2,
-                                                         float *__restrict__ db2,
-                                                         float *__restrict__ dW3,
-                                                         float *__restrict__ db3,
-                                                         float *__restrict__ db1)
-{
-    const int Mo = (L == 3) ? M : D;
-    const int n2 = Mo * H, n3 = (L == 3) ? D * M : 0, nb3 = (L == 3) ? D : 0;
-    const int total = n2 + Mo + n3 + nb3 + H;
-    for (int e = blockIdx.x * kThreads + threadIdx.x; e < total; e += gridDim.x * kThreads) {
-        int x = e;
-        if (x < n2) { dW2[x] = r[e]; continue; }
-        x -= n2;
-        if (x < Mo) { db2[x] = r[e]; continue; }
-        x -= Mo;
-        if (x < n3) { dW3[x] = r[e]; continue; }
-        x -= n3;
-        if (x < nb3) { db3[x] = r[e]; continue; }
-        x -= nb3;
-        db1[x] = r[e];
-    }
-}
 
 // ------------------------------------------------------------- dW1 split-K
 
@@ -1541,7 +1627,7 @@ int tail_part_size(const ams_mlp *m)
 }
 
 struct BwdPlan {
-    size_t off_zero, off_dz1, off_tail, off_tailsum, off_dw1, total;
+    size_t off_zero, off_dz1, off_tail, off_dw1, total;
     int kc;
 };
 
@@ -1555,7 +1641,6 @@ BwdPlan plan_bwd(const ams_mlp *m, int32_t cap)
     p.off_zero = o; o += al256((size_t)(F > H ? F : H) * 4);
     p.off_dz1 = o; o += al256((size_t)cap * H * es);
     p.off_tail = o; o += al256((size_t)kTailBlocks * tail_part_size(m) * 4);
-    p.off_tailsum = o; o += al256((size_t)tail_part_size(m) * 4);
     p.off_dw1 = o; o += al256((size_t)p.kc * H * F * 4);
     p.total = o;
     return p;
@@ -1684,22 +1769,32 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
     float *zero = (float *)(w + p.off_zero);
     void *dz1 = w + p.off_dz1;
     float *tail = (float *)(w + p.off_tail);
-    float *tailsum = (float *)(w + p.off_tailsum);
     float *dw1p = (float *)(w + p.off_dw1);
     const int PS = tail_part_size(mlp);
 
-    if (L == 3)
-        AMS_LAUNCH("tail_bwd", st, tail_bwd<3><<<kTailBlocks, kThreads, 0, st>>>(H1_save, bf, H2_save, E_fwd, dE, W2, W3, bf, H, M, D,
-                                                      mlp->final_relu, n_uniq, cap, dz1, bf, tail, PS,
-                                                      zero, F > H ? F : H));
-    else
-        AMS_LAUNCH("tail_bwd", st, tail_bwd<2><<<kTailBlocks, kThreads, 0, st>>>(H1_save, bf, H2_save, E_fwd, dE, W2, W3, bf, H, M, D,
-                                                      mlp->final_relu, n_uniq, cap, dz1, bf, tail, PS,
-                                                      zero, F > H ? F : H));
-    AMS_LAUNCH("reduce_tail", st, partial_reduce<<<(PS + kThreads - 1) / kThreads, kThreads, 0, st>>>(tail, kTailBlocks, (size_t)PS,
-                                                                         tailsum));
-    AMS_LAUNCH("tail_unpack", st, tail_unpack<<<(PS + kThreads - 1) / kThreads, kThreads, 0, st>>>(tailsum, L, H, M, D, dW2, db2,
-                                                                      dW3, db3, db1));
+#define TB_LAUNCH(LL, TW, TH)                                                                          \
+    if (D <= 16)                                                                                        \
+        AMS_LAUNCH("tail_bwd", st, (tail_bwd<LL, 8, TW, TH><<<kTailBlocks, kTbThreads, 0, st>>>(         \
+                                       (const TH *)H1_save, H2_save, E_fwd, dE, (const TW *)W2, (const TW *)W3, \
+                                       H, M, D, mlp->final_relu, n_uniq, cap, (TH *)dz1, tail, PS, zero, \
+                                       F > H ? F : H)));                                                 \
+    else                                                                                                \
+    AMS_LAUNCH("tail_bwd", st, (tail_bwd<LL, 16, TW, TH><<<kTailBlocks, kTbThreads, 0, st>>>(                \
+                                   (const TH *)H1_save, H2_save, E_fwd, dE, (const TW *)W2, (const TW *)W3, \
+                                   H, M, D, mlp->final_relu, n_uniq, cap, (TH *)dz1, tail, PS, zero,     \
+                                   F > H ? F : H)))
+    if (L == 3 && bf) {
+        TB_LAUNCH(3, uint16_t, uint16_t);
+    } else if (L == 3) {
+        TB_LAUNCH(3, float, float);
+    } else if (bf) {
+        TB_LAUNCH(2, uint16_t, uint16_t);
+    } else {
+        TB_LAUNCH(2, float, float);
+    }
+#undef TB_LAUNCH
+    AMS_LAUNCH("tail_reduce", st, tail_reduce<<<(PS + 63) / 64, 256, 0, st>>>(tail, kTailBlocks, PS, L, H, M, D, dW2,
+                                                                          db2, dW3, db3, db1));
 
     const int bm = (H % 128 == 0) ? 128 : 64;
     const int nmt = H / bm, outer = (F / 64) * p.kc;
