@@ -342,6 +342,26 @@ def test_step_full_size_fp32_attentive():
     compare_step(w, "att", batch, Ws, T_u, g, o)
 
 
+@pytest.mark.parametrize("mode", ["att", "max"])
+def test_step_full_size_bf16(mode):
+    """The bf16 workload (1024 samples, 200k x 4096 bf16 table and weights) end
+    to end at full size, grids sized by n_occ as in the bench."""
+    w = synth.get("c2_bf16")
+    print(f"step c2_bf16 {mode} full size", flush=True)
+    batch, Ws, T_u, g, o = step_case(w, mode)
+    compare_step(w, mode, batch, Ws, T_u, g, o)
+
+
+def test_step_full_size_long_sequences():
+    """The long-sequence workload (4096 samples of up to 500 behaviors, 2M x
+    4096 bf16 table, ~160k unique images, an image repeated ~69k times) end to
+    end at full size against the whole float64 oracle step."""
+    w = synth.get("c3_long")
+    print("step c3_long att full size", flush=True)
+    batch, Ws, T_u, g, o = step_case(w, "att")
+    compare_step(w, "att", batch, Ws, T_u, g, o)
+
+
 def test_step_is_bitwise_deterministic():
     w = mid("f32", B=64)
     batch = synth.make_batch(w)
