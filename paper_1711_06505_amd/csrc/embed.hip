@@ -1229,10 +1229,10 @@ __global__ __launch_bounds__(kThreads) void dw1_part(const TT *__restrict__ T, i
 // "wait until at most 6 vector-memory ops are outstanding" leaves exactly the
 // IDs of stage s+3 and the DMA of stage s+1 in flight.
 struct DwRing {
-    static constexpr int BM = 128, BN = 128, BK = 32, WAVES = 8;
+    static constexpr int BM = 256, BN = 128, BK = 32, WAVES = 8;   // BM = H: a block owns all of dW1's rows
     static constexpr int A_FLOATS = BK * BM, B_FLOATS = BK * BN;
-    static constexpr int SLOT = A_FLOATS + B_FLOATS;
-    static constexpr int PA = 2, PB = 2;                 // A / B DMA instructions per wave
+    static constexpr int SLOT = A_FLOATS + B_FLOATS;              // 48 KB
+    static constexpr int PA = 4, PB = 2;                 // A / B DMA instructions per wave
     static constexpr int OUTSTANDING = PA + PB + PB;     // vm ops allowed in flight at a stage top
 };
 constexpr int kDwThreads = DwRing::WAVES * AMS_WAVE;
@@ -1258,12 +1258,12 @@ __device__ __forceinline__ void dw1_issue(float *slot, const float *__restrict__
                                           int wave, int lane)
 {
     const int c = lane & 31;
+    // A: one 1-KB dZ1 row per instruction, lane = 16-byte chunk
 #pragma unroll
     for (int q = 0; q < DwRing::PA; ++q) {
-        const int j = DwRing::PA * wave + q;
-        const int row = 2 * j + (lane >> 5);
+        const int row = DwRing::PA * wave + q;
         const int u = u_base + row;
-        dma16((u < u1 ? dZ1 + (size_t)u * H + m0 : zero_row) + 4 * (c ^ dw_chunk_swz(row)), slot + j * 256);
+        dma16((u < u1 ? dZ1 + (size_t)u * H + m0 : zero_row) + 4 * (lane ^ dw_chunk_swz(row)), slot + row * 256);
     }
 #pragma unroll
     for (int q = 0; q < DwRing::PB; ++q) {
@@ -1275,31 +1275,34 @@ __device__ __forceinline__ void dw1_issue(float *slot, const float *__restrict__
     }
 }
 
-// 16 MFMA steps of 2 k per stage; step kk needs one B and two A values per
-// lane.  Reads run two steps ahead of the MFMAs (sched_group_barrier fixes
+// 16 MFMA steps of 2 k per stage; step kk needs two B and two A values per
+// lane (waves are 4 (h) x 2 (f), 64 x 64 each).  Reads run two steps ahead of the MFMAs (sched_group_barrier fixes
 // the interleave), so the 4-byte LDS reads are never waited on.
 __device__ __forceinline__ void dw1_compute(const float *slot, v16f *acc, int lane, int wave)
 {
-    const int h = lane >> 5, r32 = lane & 31, wm = wave >> 2, wn = wave & 3;
+    const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
     const float *A = slot, *B = slot + DwRing::A_FLOATS;
-    float av[DwRing::BK / 2][2], bv[DwRing::BK / 2];
+    float av[DwRing::BK / 2][2], bv[DwRing::BK / 2][2];
 #pragma unroll
     for (int kk = 0; kk < DwRing::BK / 2; ++kk) {
         const int k = 2 * kk + h;
         const int sw = dw_chunk_swz(k) << 2;
-        bv[kk] = B[k * DwRing::BN + ((wn * 32 + r32) ^ sw)];
+#pragma unroll
+        for (int nb = 0; nb < 2; ++nb) bv[kk][nb] = B[k * DwRing::BN + ((wn * 64 + nb * 32 + r32) ^ sw)];
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb) av[kk][mb] = A[k * DwRing::BM + ((wm * 64 + mb * 32 + r32) ^ sw)];
     }
 #pragma unroll
     for (int kk = 0; kk < DwRing::BK / 2; ++kk)
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) acc[mb] = mfma_f32(av[kk][mb], bv[kk], acc[mb]);
-    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < 2; ++nb) acc[mb * 2 + nb] = mfma_f32(av[kk][mb], bv[kk][nb], acc[mb * 2 + nb]);
+    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
 #pragma unroll
     for (int kk = 0; kk < DwRing::BK / 2; ++kk) {
-        if (kk + 2 < DwRing::BK / 2) __builtin_amdgcn_sched_group_barrier(0x100, 3, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        if (kk + 2 < DwRing::BK / 2) __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
     }
 }
 
@@ -1315,16 +1318,16 @@ __global__ __launch_bounds__(kDwThreads) void dw1_part_f32(const float *__restri
     __shared__ __attribute__((aligned(16))) float ring1[R::SLOT];
     __shared__ __attribute__((aligned(16))) float ring2[R::SLOT];
 
-    const int nmt = H / R::BM, nnt = F / R::BN;
-    int outer, mt;
-    if (!xcd_tile(blockIdx.x, nnt * KC, nmt, outer, mt)) return;
-    const int nt = outer % nnt, c = outer / nnt;
+    const int nnt = F / R::BN;
+    // the column tiles of one chunk go to one XCD: they share its dZ1 rows
+    int c, nt;
+    if (!xcd_tile(blockIdx.x, KC, nnt, c, nt)) return;
     const int n_u = min(*n_uniq_p, cap);
     const int u0 = (int)((int64_t)c * n_u / KC), u1 = (int)((int64_t)(c + 1) * n_u / KC);
-    const int m0 = mt * R::BM, n0 = nt * R::BN;
+    const int m0 = 0, n0 = nt * R::BN;
     const int lane = ams_lane(), wave = threadIdx.x / AMS_WAVE;
 
-    v16f acc[2] = {(v16f){}, (v16f){}};
+    v16f acc[4] = {(v16f){}, (v16f){}, (v16f){}, (v16f){}};
     const int S = (u1 - u0 + R::BK - 1) / R::BK;
     if (S > 0) {
         int id0[2], id1[2], id2[2];
@@ -1369,13 +1372,16 @@ __global__ __launch_bounds__(kDwThreads) void dw1_part_f32(const float *__restri
     }
 
     float *out = part + (size_t)c * H * F;
-    const int col = n0 + (wave & 3) * 32 + (lane & 31);
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const int row = m0 + (wave >> 2) * 64 + mb * 32 + acc_row(j, lane);
-            out[(size_t)row * F + col] = acc[mb][j];
+        for (int nb = 0; nb < 2; ++nb) {
+            const int col = n0 + (wave & 1) * 64 + nb * 32 + (lane & 31);
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const int row = m0 + (wave >> 1) * 64 + mb * 32 + acc_row(j, lane);
+                out[(size_t)row * F + col] = acc[mb * 2 + nb][j];
+            }
         }
 }
 
@@ -1599,7 +1605,7 @@ size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 int sk_workers();
 
-bool use_dw_ring(const ams_mlp *m) { return m->dtype == AMS_F32 && m->dims[1] % 128 == 0 && m->dims[0] % 128 == 0; }
+bool use_dw_ring(const ams_mlp *m) { return m->dtype == AMS_F32 && m->dims[1] == DwRing::BM && m->dims[0] % DwRing::BN == 0; }
 bool use_dw_tr(const ams_mlp *m) { return m->dtype == AMS_BF16 && m->dims[1] == DwTr::BM && m->dims[0] % DwTr::BN == 0; }
 
 // Split-K chunk count of dW1: the DMA-ring kernel takes one block per CU
@@ -1609,7 +1615,7 @@ int dw1_chunks(const ams_mlp *m)
     const int H = m->dims[1], F = m->dims[0];
     int kc;
     if (use_dw_ring(m)) {
-        kc = sk_workers() / ((H / 128) * (F / 128));
+        kc = sk_workers() / (F / DwRing::BN);
     } else if (use_dw_tr(m)) {
         kc = sk_workers() / (F / DwTr::BN);
     } else {
@@ -1800,8 +1806,7 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
     const int nmt = H / bm, outer = (F / 64) * p.kc;
     const int grid = ((outer + 7) / 8) * 8 * nmt;
     if (use_dw_ring(mlp)) {
-        const int outer8 = (F / DwRing::BN) * p.kc;
-        const int grid8 = ((outer8 + 7) / 8) * 8 * (H / DwRing::BM);
+        const int grid8 = ((p.kc + 7) / 8) * 8 * (F / DwRing::BN);
         AMS_LAUNCH("dw1_part_f32", st, dw1_part_f32<<<grid8, kDwThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
                                                    (const float *)dz1, H, p.kc, zero, dw1p));
     } else if (use_dw_tr(mlp)) {
