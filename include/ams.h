@@ -42,9 +42,14 @@
  * Precision:  AMS_F32: T and W float32, float32 MFMA with float32 accumulation.
  *             AMS_BF16: T and W bfloat16; bf16 MFMA with float32 accumulation
  *             for the 4096-wide layer and its weight gradient (whose
- *             activation-gradient operand is rounded to bf16); all other
- *             arithmetic, E, U, A, the attention weights and every gradient
- *             are float32.  H1_save is bf16 in this mode, float32 otherwise.
+ *             activation-gradient operand is rounded to bf16).  The smaller
+ *             layers also run on bf16 MFMA, but each float32 activation or
+ *             gradient operand enters as a pair of bf16 values (high part
+ *             plus the rounded remainder, together within 2^-18 of the
+ *             float32 value) against the exact bf16 weights, so they keep
+ *             float32-level accuracy.  E, U, A, the attention weights and
+ *             every gradient are float32.  H1_save is bf16 in this mode
+ *             (the rounding of the float32 H1), float32 otherwise.
  * Determinism: every output is bitwise reproducible for identical inputs on
  *             the same device (fixed reduction orders, no float atomics).
  * Errors:     calls return an ams_status.  Problems visible on the host are

@@ -356,14 +356,17 @@ __device__ __forceinline__ void sk_compute(const float *slot, v16f *acc, int lan
 }
 
 // H1b (bf16 mode): the bf16 copy of H1 kept for the backward, written with H1
-// for tiles finished in place.
+// for tiles finished in place; H1lo, if given, the bf16 rounding of what H1b
+// leaves out (H1 = H1b + H1lo to 2^-18 relative), the fp32-level operand of
+// the bf16 layer-2 product.
 template <typename TT>
 __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int64_t n_rows, int F,
                                                    const int32_t *__restrict__ uniq,
                                                    const int32_t *__restrict__ n_uniq_p, int cap,
                                                    const TT *__restrict__ W1, const float *__restrict__ b1,
                                                    int H, int G, float *__restrict__ H1,
-                                                   uint16_t *__restrict__ H1b, float *__restrict__ pbuf)
+                                                   uint16_t *__restrict__ H1b, uint16_t *__restrict__ H1lo,
+                                                   float *__restrict__ pbuf)
 {
     constexpr int BK = sk_bk<TT>();
     __shared__ __attribute__((aligned(16))) float ring0[kSkSlot];
@@ -447,8 +450,12 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
                     const int r = wm * 32 + acc_row(j, lane);
                     const float z = fmaxf(rid[r] >= 0 ? acc[nb][j] + bias : bias, 0.f);
                     if (m0 + r < n_u) {
-                        H1[(size_t)(m0 + r) * H + col] = z;
-                        if (H1b) H1b[(size_t)(m0 + r) * H + col] = ams_f32_to_bf16(z);
+                        if (H1) H1[(size_t)(m0 + r) * H + col] = z;
+                        if (H1b) {
+                            const uint16_t hi = ams_f32_to_bf16(z);
+                            H1b[(size_t)(m0 + r) * H + col] = hi;
+                            if (H1lo) H1lo[(size_t)(m0 + r) * H + col] = ams_f32_to_bf16(z - ams_bf16_to_f32(hi));
+                        }
                     }
                 }
             }
@@ -756,6 +763,229 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
                 for (int oo = 0; oo < M; ++oo) v += W3s[d * (kMaxH2 + 1) + oo] * h2s[r][oo];
                 if (final_relu) v = fmaxf(v, 0.f);
                 E[(size_t)(c0 + r) * D + d] = v;
+            }
+        }
+    }
+}
+
+// ---- bf16 forward tail (stream-K layer 1, H = 256) ----
+//
+// tail_fwd_bf16: the small layers after the bf16 stream-K first layer, for
+// 32-row chunks (one chunk per wave at a time, no block-level sync in the
+// loop).  Every product runs on v_mfma_f32_32x32x16_bf16 with its fp32
+// activation split into a high and a low bf16 part (x = hi + lo to 2^-18
+// relative); the weights are exact in bf16 and each part's products are exact
+// in fp32, so the results carry fp32 accumulation of fp32-level operands.
+//
+// Layer 2: Z2^T = W2 H1^T.  First operand a W2 row (16 bytes of 8
+// consecutive k, LDS), second the chunk's H1 row: for a tile finished in place
+// by one stream-K worker the (H1b, H1lo) pair it stored; for a tile cut
+// between workers the workers' fp32 partial tiles added in K order, b1 and
+// ReLU applied (ReLU(b1) for an ID outside the table), split, and H1b stored
+// for the backward.  K step s covers k = 16 s .. +15, lane half h supplying
+// k = 16 s + 8 h + e.  The accumulator holds Z2[row = lane % 32][o = 32 ob +
+// acc_row(j, lane)]: each lane owns one image row and 32 of its outputs.
+// H2 = ReLU(Z2 + b2) is stored as float4 runs of 4 outputs.
+// Layer 3 (3 layers): Z3^T = W3 H2^T; k step (ob, p) takes the outputs this
+// lane already holds, o = 32 ob + 16 p + 4 h + {0..3} and the same + 8, so
+// H2 goes into the MFMA straight from the registers; W3 rows sit in LDS padded
+// to 68 bf16 (conflict-free 8-byte reads).  E = Z3 + b3 (ReLU if final).
+// W2 sits in LDS [64 o][256 k] bf16, rows past the layer width zero, 16-byte
+// chunks stored at chunk ^ (o & 7) so a half-wave's 32 rows spread over all
+// banks.
+constexpr int kW3S = kMaxH2 + 4;               // bf16 per W3 row in LDS
+
+__device__ __forceinline__ uint32_t pack_bf16(float a, float b)
+{
+    return (uint32_t)ams_f32_to_bf16(a) | ((uint32_t)ams_f32_to_bf16(b) << 16);
+}
+
+// hi/lo split of 8 fp32 values into two bf16x8 operands
+__device__ __forceinline__ void split8(const float (&x)[8], uint4 &hi, uint4 &lo)
+{
+    uint16_t hb[8];
+    float r[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        hb[e] = ams_f32_to_bf16(x[e]);
+        r[e] = x[e] - ams_bf16_to_f32(hb[e]);
+    }
+    hi = make_uint4(hb[0] | ((uint32_t)hb[1] << 16), hb[2] | ((uint32_t)hb[3] << 16),
+                    hb[4] | ((uint32_t)hb[5] << 16), hb[6] | ((uint32_t)hb[7] << 16));
+    lo = make_uint4(pack_bf16(r[0], r[1]), pack_bf16(r[2], r[3]), pack_bf16(r[4], r[5]), pack_bf16(r[6], r[7]));
+}
+
+template <int L>
+__global__ __launch_bounds__(kThreads) void tail_fwd_bf16(uint16_t *__restrict__ H1b,
+                                                          const uint16_t *__restrict__ H1lo,
+                                                          const float *__restrict__ pbuf, int F, int G,
+                                                          const float *__restrict__ b1,
+                                                          const int32_t *__restrict__ uniq, int64_t n_rows,
+                                                          int M, int D, const uint16_t *__restrict__ W2,
+                                                          const float *__restrict__ b2,
+                                                          const uint16_t *__restrict__ W3,
+                                                          const float *__restrict__ b3, int final_relu,
+                                                          const int32_t *__restrict__ n_uniq_p, int cap,
+                                                          float *__restrict__ H2_save, float *__restrict__ E)
+{
+    constexpr int H = kMaxH1;
+    constexpr int KS = H / 16;                 // k steps
+    __shared__ __attribute__((aligned(16))) uint16_t W2s[kMaxH2 * kMaxH1];
+    __shared__ __attribute__((aligned(16))) uint16_t W3s[32 * kW3S];
+    const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
+    const int h = lane >> 5, r32 = lane & 31;
+    const int Mo = (L == 3) ? M : D;           // width of the second layer's output
+    constexpr int cpr = H / 8;                 // 16-byte chunks per W2 row
+    for (int idx = t; idx < kMaxH2 * cpr; idx += kThreads) {
+        const int o = idx / cpr, c = idx % cpr;
+        const uint4 v = o < Mo ? *(const uint4 *)&W2[(size_t)o * H + c * 8] : make_uint4(0, 0, 0, 0);
+        *(uint4 *)&W2s[o * H + ((c ^ (o & 7)) << 3)] = v;
+    }
+    if (L == 3)
+        for (int e = t; e < 32 * kW3S; e += kThreads) {
+            const int d = e / kW3S, o = e % kW3S;
+            W3s[e] = (d < D && o < M) ? W3[d * M + o] : (uint16_t)0;
+        }
+    // this lane's outputs o = 32 ob + 8 q + 4 h + r and their biases
+    float bias[2][16];
+#pragma unroll
+    for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int o = 32 * ob + acc_row(j, lane);
+            bias[ob][j] = o < Mo ? b2[o] : 0.f;
+        }
+    __syncthreads();
+
+    const int n_u = min(*n_uniq_p, cap);
+    if (n_u <= 0) return;
+    const bool relu2 = (L == 3) || final_relu;
+    const SkPlan P = sk_plan(n_u, H, F, G, sk_bk<uint16_t>());
+    for (int c0 = (blockIdx.x * (kThreads / AMS_WAVE) + wave) * 32; c0 < n_u;
+         c0 += gridDim.x * (kThreads / AMS_WAVE) * 32) {
+        const int row = c0 + r32;
+        const bool live = row < n_u;
+        const int rowc = min(row, n_u - 1);
+        // the chunk lies in one 128-row stream-K tile: finished in place or cut
+        const int tile = c0 / kSkBM;
+        const int wa = P.owner((int64_t)tile * P.S), wb = P.owner((int64_t)(tile + 1) * P.S - 1);
+        const bool split = wb > wa;
+        const int slot_a = (tile == (int)(P.it0(wa) / P.S)) ? 0 : 1;   // first contributor's piece
+        bool id_ok = true;
+        if (split) {
+            const int id = uniq[rowc];
+            id_ok = id >= 0 && (int64_t)id < n_rows;
+        }
+        const int rl = rowc % kSkBM;
+        const size_t roff = (size_t)rowc * H + 8 * h;
+        v16f acc[2] = {(v16f){}, (v16f){}};
+#pragma unroll
+        for (int qt = 0; qt < 4; ++qt) {
+            uint4 bh[KS / 4], bl[KS / 4];
+            if (split) {
+#pragma unroll
+                for (int s4 = 0; s4 < KS / 4; ++s4) {
+                    const int k0 = 16 * (qt * (KS / 4) + s4) + 8 * h;
+                    float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                    for (int pi = 0; pi < 3; ++pi) {
+                        const int w = wa + pi;
+                        if (w <= wb) {
+                            const float *pc = pbuf + ((size_t)w * 2 + (pi == 0 ? slot_a : 0)) * kSkTile +
+                                              rl * kSkBN + k0;
+                            const float4 v0 = *(const float4 *)pc, v1 = *(const float4 *)(pc + 4);
+                            x[0] += v0.x; x[1] += v0.y; x[2] += v0.z; x[3] += v0.w;
+                            x[4] += v1.x; x[5] += v1.y; x[6] += v1.z; x[7] += v1.w;
+                        }
+                    }
+                    for (int w = wa + 3; w <= wb; ++w) {     // (a tile spans at most 3 shares)
+                        const float *pc = pbuf + ((size_t)w * 2) * kSkTile + rl * kSkBN + k0;
+                        const float4 v0 = *(const float4 *)pc, v1 = *(const float4 *)(pc + 4);
+                        x[0] += v0.x; x[1] += v0.y; x[2] += v0.z; x[3] += v0.w;
+                        x[4] += v1.x; x[5] += v1.y; x[6] += v1.z; x[7] += v1.w;
+                    }
+                    const float4 c0v = *(const float4 *)&b1[k0], c1v = *(const float4 *)&b1[k0 + 4];
+                    const float bb[8] = {c0v.x, c0v.y, c0v.z, c0v.w, c1v.x, c1v.y, c1v.z, c1v.w};
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) x[e] = fmaxf(id_ok ? x[e] + bb[e] : bb[e], 0.f);
+                    split8(x, bh[s4], bl[s4]);
+                    if (live) *(uint4 *)(H1b + (size_t)row * H + k0) = bh[s4];
+                }
+            } else {
+#pragma unroll
+                for (int s4 = 0; s4 < KS / 4; ++s4) {
+                    bh[s4] = *(const uint4 *)(H1b + roff + 16 * (qt * (KS / 4) + s4));
+                    bl[s4] = *(const uint4 *)(H1lo + roff + 16 * (qt * (KS / 4) + s4));
+                }
+            }
+#pragma unroll
+            for (int s4 = 0; s4 < KS / 4; ++s4) {
+                const int ss = qt * (KS / 4) + s4;
+#pragma unroll
+                for (int ob = 0; ob < 2; ++ob) {
+                    const int o = 32 * ob + r32;
+                    const uint4 av = *(const uint4 *)&W2s[o * H + (((2 * ss + h) ^ (o & 7)) << 3)];
+                    acc[ob] = mfma_bf16(av, bh[s4], acc[ob]);
+                    acc[ob] = mfma_bf16(av, bl[s4], acc[ob]);
+                }
+            }
+        }
+        float z[2][16];
+#pragma unroll
+        for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const float v = acc[ob][j] + bias[ob][j];
+                z[ob][j] = relu2 ? fmaxf(v, 0.f) : v;
+            }
+        float *out2 = (L == 3) ? H2_save : E;  // where the second layer's output goes
+        const int w2 = (L == 3) ? M : D;
+        if (live && out2) {
+#pragma unroll
+            for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const int o = 32 * ob + 8 * q + 4 * h;
+                    float *dst = out2 + (size_t)row * w2 + o;
+                    if ((w2 & 3) == 0 && o + 3 < w2) {
+                        *(float4 *)dst = make_float4(z[ob][4 * q], z[ob][4 * q + 1], z[ob][4 * q + 2], z[ob][4 * q + 3]);
+                    } else {
+#pragma unroll
+                        for (int r = 0; r < 4; ++r)
+                            if (o + r < w2) dst[r] = z[ob][4 * q + r];
+                    }
+                }
+        }
+        if constexpr (L == 3) {
+            v16f a3 = (v16f){};
+#pragma unroll
+            for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+                for (int p = 0; p < 2; ++p) {
+                    float x[8];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        x[e] = z[ob][8 * p + e];           // o = 32 ob + 16 p + 4 h + e
+                        x[4 + e] = z[ob][8 * p + 4 + e];   // o = 32 ob + 16 p + 8 + 4 h + e
+                    }
+                    uint4 hi, lo;
+                    split8(x, hi, lo);
+                    const uint16_t *wr = &W3s[r32 * kW3S + 32 * ob + 16 * p + 4 * h];
+                    const uint2 w0 = *(const uint2 *)wr, w1 = *(const uint2 *)(wr + 8);
+                    const uint4 wv = make_uint4(w0.x, w0.y, w1.x, w1.y);
+                    a3 = mfma_bf16(wv, hi, a3);
+                    a3 = mfma_bf16(wv, lo, a3);
+                }
+            if (live) {
+#pragma unroll
+                for (int j = 0; j < 16; ++j) {
+                    const int d = acc_row(j, lane);
+                    if (d < D) {
+                        float v = a3[j] + b3[d];
+                        if (final_relu) v = fmaxf(v, 0.f);
+                        E[(size_t)row * D + d] = v;
+                    }
+                }
             }
         }
     }
@@ -1586,6 +1816,306 @@ __global__ __launch_bounds__(DwTr::WAVES * AMS_WAVE) void dw1_part_bf16(
         }
 }
 
+// ---- bf16 backward tail (H = 256) ----
+//
+// Per 32-row chunk of the block's unique images, all in LDS + registers:
+//   phase A (all 256 threads, fp32): thread (o = t % 64, row group g = t / 64)
+//     takes rows g + 4 k; with dzl = dE (masked by a final ReLU) and its W3
+//     column in registers it forms dZ2 = (dzl W3) * [H2 > 0] (3 layers; dZ2 =
+//     dzl for 2), splits it into a high and a low bf16 part (dZ2 = hi + lo to
+//     2^-18 relative) in two tiles, and keeps running sums of db2 and (3
+//     layers) dW3 = dzl^T H2 over its rows; the four row groups are added in
+//     a fixed order at the end; threads d < D sum db3 over the chunk's rows;
+//   phase B (wave w owns H1 columns i in [64 w, 64 w + 64)):
+//     dH1 = dZ2 W2 on v_mfma_f32_32x32x16_bf16, one product per part (first
+//     operand a dZ2 row, second a row of W2^T, both 16-byte LDS reads; W2 and
+//     the saved H1 are exact in bf16, so both products are fp32-accurate), so
+//     a lane holds dH1[rows 8 q + 4 h + r][i]; the H1 values of exactly those
+//     (row, i) come from transposed LDS reads (ds_read_b64_tr_b16) of the H1
+//     tile, give the ReLU mask dZ1 = dH1 * [H1 > 0] (summed into db1 in fp32,
+//     rounded to bf16 into the wave's own columns of the H1 tile, from where
+//     the block stores whole rows), and are at once the second operand of
+//     dW2 += dZ2^T H1 (k = the chunk's rows, lane half h supplying rows
+//     8 q + 4 h + r, q = 2 s, 2 s + 1), whose first operand is read
+//     transposed from the dZ2 tiles.
+// The next chunk's H1, H2 and dE are loaded into registers while the current
+// one is computed.  Block partials have the layout of tail_bwd's
+// ([dW2][db2][dW3][db3][db1]) and go through the same fixed-order reduction.
+// Tiles are padded by 16 bytes per row so that the 16-byte and transposed
+// reads of a half-wave spread over the banks.
+constexpr int kTbfBlocks = 512;
+constexpr int kH1S = kMaxH1 * 2 + 16;       // bytes per H1 tile row
+constexpr int kZ2S = kMaxH2 * 2 + 16;       // bytes per dZ2 tile row
+constexpr int kW2S = kMaxH2 * 2 + 16;       // bytes per W2^T tile row
+
+// Transposed read of a bf16 tile (stride bytes per row) for the 16-lane
+// group of `lane`: rows R0..R0+3, columns C0..C0+15; the lane receives column
+// C0 + (lane % 16) of the four rows.
+__device__ __forceinline__ uint2 tr4(const char *tile, int stride, int R0, int C0, int lane)
+{
+    const int i16 = lane & 15;
+    return ds_read_tr16(tile + (R0 + (i16 >> 2)) * stride + (C0 + 4 * (i16 & 3)) * 2);
+}
+
+__device__ __forceinline__ float bf16_elem(uint2 v, int r)
+{
+    const uint32_t w = r < 2 ? v.x : v.y;
+    return __uint_as_float((r & 1) ? (w & 0xffff0000u) : (w << 16));
+}
+
+// DM: upper bound of D (16 or 32), the length of the per-thread dzl rows.
+template <int L, int DM>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
+void tail_bwd_bf16(const uint16_t *__restrict__ H1b, const float *__restrict__ H2s,
+                   const float *__restrict__ Efwd, const float *__restrict__ dE,
+                   const uint16_t *__restrict__ W2, const uint16_t *__restrict__ W3, int M, int D,
+                   int final_relu, const int32_t *__restrict__ n_uniq_p, int cap,
+                   uint16_t *__restrict__ dZ1, float *__restrict__ part, int PS,
+                   float *__restrict__ zero_row, int zero_n)
+{
+    constexpr int H = kMaxH1;
+    __shared__ __attribute__((aligned(16))) char H1t[32 * kH1S];      // H1, then dZ1, of the chunk
+    __shared__ __attribute__((aligned(16))) char Z2t[32 * kZ2S];      // dZ2, high bf16 part
+    __shared__ __attribute__((aligned(16))) char Z2l[32 * kZ2S];      // dZ2, low bf16 part
+    __shared__ __attribute__((aligned(16))) char W2T[H * kW2S];
+    __shared__ __attribute__((aligned(16))) float H2t[32 * kMaxH2];
+    __shared__ __attribute__((aligned(16))) float Lt[32 * DM];
+
+    const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
+    const int h = lane >> 5, r32 = lane & 31;
+    // the zero row that dW1's padding rows stream (read by the next launch)
+    if (blockIdx.x == 0)
+        for (int i = t; i < zero_n; i += kThreads) zero_row[i] = 0.f;
+    const int Mo = (L == 3) ? M : D;
+    for (int e = t; e < kMaxH2 * H; e += kThreads) {
+        const int o = e / H, i = e % H;
+        *(uint16_t *)(W2T + i * kW2S + o * 2) = o < Mo ? W2[(size_t)o * H + i] : (uint16_t)0;
+    }
+    const int po = t & 63, pg = t >> 6;        // phase-A role: output o, row group
+    float w3c[DM];                             // W3[:, po] (3 layers)
+#pragma unroll
+    for (int d = 0; d < DM; ++d) w3c[d] = (L == 3 && d < D && po < M) ? ams_bf16_to_f32(W3[d * M + po]) : 0.f;
+
+    const int n_u = min(*n_uniq_p, cap);
+    const int r0 = (int)((int64_t)blockIdx.x * n_u / gridDim.x);
+    const int r1 = (int)((int64_t)(blockIdx.x + 1) * n_u / gridDim.x);
+
+    v16f dw2[2][2] = {{(v16f){}, (v16f){}}, {(v16f){}, (v16f){}}};   // [o block][i block]
+    float db1a[2] = {0.f, 0.f};
+    float db2p = 0.f, db3p = 0.f;
+    float dw3a[DM];
+#pragma unroll
+    for (int d = 0; d < DM; ++d) dw3a[d] = 0.f;
+    uint4 pH1[4];
+    float4 pH2[2];
+    float pdz[4];
+    auto fetch = [&](int c0) {
+        const int nr = min(32, r1 - c0);
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const int idx = t + kThreads * m, row = idx >> 5, ch = idx & 31;
+            pH1[m] = row < nr ? *(const uint4 *)(H1b + (size_t)(c0 + row) * H + ch * 8) : make_uint4(0, 0, 0, 0);
+        }
+        if (L == 3) {
+#pragma unroll
+            for (int m = 0; m < 2; ++m) {
+                const int idx = t + kThreads * m, row = idx >> 4, c4 = idx & 15;
+                pH2[m] = (row < nr && 4 * c4 < M) ? *(const float4 *)(H2s + (size_t)(c0 + row) * M + 4 * c4)
+                                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+        }
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const int idx = t + kThreads * m;
+            float g = 0.f;
+            if (idx < nr * D) {
+                g = dE[(size_t)c0 * D + idx];
+                if (final_relu && !(Efwd[(size_t)c0 * D + idx] > 0.f)) g = 0.f;
+            }
+            pdz[m] = g;
+        }
+    };
+
+    if (r0 < r1) fetch(r0);
+    for (int c0 = r0; c0 < r1; c0 += 32) {
+        const int nr = min(32, r1 - c0);
+        __syncthreads();                       // the previous chunk's tiles are consumed
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const int idx = t + kThreads * m, row = idx >> 5, ch = idx & 31;
+            *(uint4 *)(H1t + row * kH1S + ch * 16) = pH1[m];
+        }
+        if (L == 3) {
+#pragma unroll
+            for (int m = 0; m < 2; ++m) {
+                const int idx = t + kThreads * m, row = idx >> 4, c4 = idx & 15;
+                *(float4 *)&H2t[row * kMaxH2 + 4 * c4] = pH2[m];
+            }
+        }
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const int idx = t + kThreads * m;
+            if (idx < 32 * DM) Lt[idx] = 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const int idx = t + kThreads * m;
+            if (idx < 32 * D) Lt[(idx / D) * DM + idx % D] = pdz[m];
+        }
+        __syncthreads();
+        if (c0 + 32 < r1) fetch(c0 + 32);
+
+        // ---- phase A: dZ2 (fp32, split into two bf16 tiles), db2, dW3, db3
+        if (L == 3 && t < D) {
+            float a = 0.f;
+            for (int rr = 0; rr < 32; ++rr) a += Lt[rr * DM + t];
+            db3p += a;
+        }
+#pragma unroll 2
+        for (int k = 0; k < 8; ++k) {
+            const int rr = pg + 4 * k;
+            float zl[DM];
+#pragma unroll
+            for (int d4 = 0; d4 < DM / 4; ++d4) {
+                const float4 v = *(const float4 *)&Lt[rr * DM + 4 * d4];
+                zl[4 * d4] = v.x;
+                zl[4 * d4 + 1] = v.y;
+                zl[4 * d4 + 2] = v.z;
+                zl[4 * d4 + 3] = v.w;
+            }
+            float dz2;
+            if constexpr (L == 3) {
+                float a = 0.f;
+#pragma unroll
+                for (int d = 0; d < DM; ++d) a = fmaf(zl[d], w3c[d], a);
+                const float h2 = H2t[rr * kMaxH2 + po];
+                dz2 = h2 > 0.f ? a : 0.f;
+#pragma unroll
+                for (int d = 0; d < DM; ++d) dw3a[d] = fmaf(zl[d], h2, dw3a[d]);
+            } else {
+                dz2 = 0.f;
+#pragma unroll
+                for (int d = 0; d < DM; ++d)
+                    if (d == po) dz2 = zl[d];
+            }
+            db2p += dz2;
+            const uint16_t zh = ams_f32_to_bf16(dz2);
+            *(uint16_t *)(Z2t + rr * kZ2S + po * 2) = zh;
+            *(uint16_t *)(Z2l + rr * kZ2S + po * 2) = ams_f32_to_bf16(dz2 - ams_bf16_to_f32(zh));
+        }
+        __syncthreads();                       // dZ2 tiles complete
+
+        // ---- phase B: dH1, dZ1, db1, dW2 for this wave's 64 columns
+        {
+            const int i0 = 64 * wave;
+            v16f acc[2] = {(v16f){}, (v16f){}};
+#pragma unroll
+            for (int s = 0; s < 4; ++s) {
+                const uint4 ah = *(const uint4 *)(Z2t + r32 * kZ2S + (16 * s + 8 * h) * 2);
+                const uint4 al = *(const uint4 *)(Z2l + r32 * kZ2S + (16 * s + 8 * h) * 2);
+#pragma unroll
+                for (int ib = 0; ib < 2; ++ib) {
+                    const uint4 b = *(const uint4 *)(W2T + (i0 + 32 * ib + r32) * kW2S + (16 * s + 8 * h) * 2);
+                    acc[ib] = mfma_bf16(ah, b, acc[ib]);
+                    acc[ib] = mfma_bf16(al, b, acc[ib]);
+                }
+            }
+            const int cg = 16 * ((lane >> 4) & 1);
+            uint2 hv[2][4];
+#pragma unroll
+            for (int ib = 0; ib < 2; ++ib)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) hv[ib][q] = tr4(H1t, kH1S, 8 * q + 4 * h, i0 + 32 * ib + cg, lane);
+#pragma unroll
+            for (int ib = 0; ib < 2; ++ib) {
+                const int icol = i0 + 32 * ib + r32;
+                float cs = 0.f;
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float dz = bf16_elem(hv[ib][q], r) > 0.f ? acc[ib][4 * q + r] : 0.f;
+                        cs += dz;
+                        // this wave's own columns of the H1 tile now hold dZ1
+                        *(uint16_t *)(H1t + (8 * q + 4 * h + r) * kH1S + icol * 2) = ams_f32_to_bf16(dz);
+                    }
+                db1a[ib] += cs + __shfl_xor(cs, 32, AMS_WAVE);
+            }
+#pragma unroll
+            for (int s = 0; s < 2; ++s) {
+                uint4 a[2][2];                 // [part][o block]
+#pragma unroll
+                for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+                    for (int pt = 0; pt < 2; ++pt) {
+                        const char *zt = pt ? Z2l : Z2t;
+                        const uint2 r0v = tr4(zt, kZ2S, 16 * s + 4 * h, 32 * ob + cg, lane);
+                        const uint2 r1v = tr4(zt, kZ2S, 16 * s + 8 + 4 * h, 32 * ob + cg, lane);
+                        a[pt][ob] = make_uint4(r0v.x, r0v.y, r1v.x, r1v.y);
+                    }
+#pragma unroll
+                for (int ib = 0; ib < 2; ++ib) {
+                    const uint4 b = make_uint4(hv[ib][2 * s].x, hv[ib][2 * s].y, hv[ib][2 * s + 1].x,
+                                               hv[ib][2 * s + 1].y);
+#pragma unroll
+                    for (int ob = 0; ob < 2; ++ob) {
+                        dw2[ob][ib] = mfma_bf16(a[0][ob], b, dw2[ob][ib]);
+                        dw2[ob][ib] = mfma_bf16(a[1][ob], b, dw2[ob][ib]);
+                    }
+                }
+            }
+        }
+        __syncthreads();                       // dZ1 tile complete: whole rows out
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const int idx = t + kThreads * m, row = idx >> 5, ch = idx & 31;
+            if (row < nr) *(uint4 *)(dZ1 + (size_t)(c0 + row) * H + ch * 8) = *(const uint4 *)(H1t + row * kH1S + ch * 16);
+        }
+    }
+
+    float *p = part + (size_t)blockIdx.x * PS;
+    const int i0 = 64 * wave;
+#pragma unroll
+    for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+        for (int ib = 0; ib < 2; ++ib)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const int o = acc_row(j, lane) + 32 * ob;
+                if (o < Mo) p[(size_t)o * H + i0 + 32 * ib + r32] = dw2[ob][ib][j];
+            }
+    p += Mo * H;
+    // the four row groups of db2, dW3 and db3, added in a fixed order
+    float *red = (float *)H1t;                 // 4 x DM x 64 floats (16 KB at DM = 16)
+    __syncthreads();
+    H2t[t] = db2p;
+    __syncthreads();
+    if (t < Mo) p[t] = ((H2t[t] + H2t[64 + t]) + H2t[128 + t]) + H2t[192 + t];
+    p += Mo;
+    if (L == 3) {
+        for (int d0 = 0; d0 < DM; d0 += 16) {  // in slices of 16 d (the tile holds 4 x 16 x 64)
+            __syncthreads();
+#pragma unroll
+            for (int d = 0; d < 16; ++d) red[(pg * 16 + d) * 64 + po] = dw3a[d0 + d];
+            __syncthreads();
+            for (int e = t; e < 16 * 64; e += kThreads) {
+                const int d = d0 + e / 64, o = e % 64;
+                if (d < D && o < M)
+                    p[d * M + o] = ((red[(0 * 16 + e / 64) * 64 + o] + red[(1 * 16 + e / 64) * 64 + o]) +
+                                    red[(2 * 16 + e / 64) * 64 + o]) + red[(3 * 16 + e / 64) * 64 + o];
+            }
+        }
+        p += D * M;
+        if (t < D) p[t] = db3p;
+        p += D;
+    }
+    if (h == 0) {
+        p[i0 + r32] = db1a[0];
+        p[i0 + 32 + r32] = db1a[1];
+    }
+}
+
 // ----------------------------------------------------------------- host
 
 bool mlp_ok(const ams_mlp *m)
@@ -1632,6 +2162,16 @@ int tail_part_size(const ams_mlp *m)
     return M * H + M + ((L == 3) ? D * M + D : 0) + H;
 }
 
+// The bf16 backward tail (bf16 MFMA) serves H = 256 with a second-layer
+// width that is a multiple of 4; other shapes use the fp32-MFMA tail.
+bool use_tail_bf16(const ams_mlp *m)
+{
+    return m->dtype == AMS_BF16 && m->dims[1] == kMaxH1 &&
+           (m->n_layers == 2 || (m->dims[2] % 4 == 0 && m->dims[2] * m->dims[3] <= 4 * kThreads));
+}
+
+int tail_blocks(const ams_mlp *m) { return use_tail_bf16(m) ? kTbfBlocks : kTailBlocks; }
+
 struct BwdPlan {
     size_t off_zero, off_dz1, off_tail, off_dw1, total;
     int kc;
@@ -1646,7 +2186,7 @@ BwdPlan plan_bwd(const ams_mlp *m, int32_t cap)
     size_t o = 0;
     p.off_zero = o; o += al256((size_t)(F > H ? F : H) * 4);
     p.off_dz1 = o; o += al256((size_t)cap * H * es);
-    p.off_tail = o; o += al256((size_t)kTailBlocks * tail_part_size(m) * 4);
+    p.off_tail = o; o += al256((size_t)tail_blocks(m) * tail_part_size(m) * 4);
     p.off_dw1 = o; o += al256((size_t)p.kc * H * F * 4);
     p.total = o;
     return p;
@@ -1704,6 +2244,11 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
     if ((h1_in_ws || sk) && (!ws || ws_bytes < need)) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     float *H1f = h1_in_ws ? (float *)ws : (float *)H1_save;
+    // bf16 stream-K path: H1 as a pair of bf16 arrays in the workspace's H1
+    // region, the low part first, then the high part unless the caller keeps
+    // it (H1_save, read by the backward)
+    uint16_t *h1lo = (uint16_t *)ws;
+    uint16_t *h1b = H1_save ? (uint16_t *)H1_save : (uint16_t *)ws + (size_t)cap * H;
     float *pbuf = (float *)((char *)ws + h1_bytes);
 
     const int n_mt = (cap + 63) / 64;
@@ -1711,11 +2256,11 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
     const int grid = ((n_mt + 7) / 8) * 8 * (H / NT);
     if (sk && !bf) {
         AMS_LAUNCH("l1sk_f32", st, l1sk<float><<<G, kSkThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
-                                                                      (const float *)W1, b1, H, G, H1f, nullptr, pbuf));
+                                                                      (const float *)W1, b1, H, G, H1f, nullptr, nullptr, pbuf));
     } else if (sk) {
         AMS_LAUNCH("l1sk_bf16", st, l1sk<uint16_t><<<G, kSkThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq, n_uniq,
-                                                                           cap, (const uint16_t *)W1, b1, H, G, H1f,
-                                                                           (uint16_t *)H1_save, pbuf));
+                                                                           cap, (const uint16_t *)W1, b1, H, G, nullptr,
+                                                                           h1b, h1lo, pbuf));
     } else if (!bf) {
         if (NT == 128)
             AMS_LAUNCH("l1_fwd_f32", st, l1_fwd_f32<128><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, n_mt,
@@ -1732,6 +2277,21 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
             AMS_LAUNCH("l1_fwd_bf16", st, l1_fwd_bf16<64><<<grid, kThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq, n_uniq,
                                                        cap, n_mt, (const uint16_t *)W1, b1, H, H1f,
                                                        (uint16_t *)H1_save));
+    }
+    if (sk && bf) {
+        // the small layers on bf16 MFMA (split tiles of layer 1 finished on the way)
+        int tg = (cap + 4 * 32 - 1) / (4 * 32);
+        if (tg > 2048) tg = 2048;
+        if (L == 3)
+            AMS_LAUNCH("tail_fwd_bf16", st, tail_fwd_bf16<3><<<tg, kThreads, 0, st>>>(
+                                                h1b, h1lo, pbuf, F, G, b1, uniq, n_rows, M, D, (const uint16_t *)W2,
+                                                b2, (const uint16_t *)W3, b3, mlp->final_relu, n_uniq, cap, H2_save,
+                                                E));
+        else
+            AMS_LAUNCH("tail_fwd_bf16", st, tail_fwd_bf16<2><<<tg, kThreads, 0, st>>>(
+                                                h1b, h1lo, pbuf, F, G, b1, uniq, n_rows, M, D, (const uint16_t *)W2,
+                                                b2, nullptr, nullptr, mlp->final_relu, n_uniq, cap, H2_save, E));
+        return ams_launch_status();
     }
     const int sk_bk = sk ? (bf ? 64 : 32) : 0;      // K per stream-K stage (128 bytes of a row)
     int tg = (cap + kTailRows - 1) / kTailRows;
@@ -1789,7 +2349,19 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
                                    (const TH *)H1_save, H2_save, E_fwd, dE, (const TW *)W2, (const TW *)W3, \
                                    H, M, D, mlp->final_relu, n_uniq, cap, (TH *)dz1, tail, PS, zero,     \
                                    F > H ? F : H)))
-    if (L == 3 && bf) {
+    const int TG = tail_blocks(mlp);
+    if (use_tail_bf16(mlp)) {
+#define TBF_LAUNCH(LL, DM)                                                                              \
+    AMS_LAUNCH("tail_bwd_bf16", st, (tail_bwd_bf16<LL, DM><<<TG, kThreads, 0, st>>>(                     \
+                                        (const uint16_t *)H1_save, H2_save, E_fwd, dE, (const uint16_t *)W2, \
+                                        (const uint16_t *)W3, M, D, mlp->final_relu, n_uniq, cap,          \
+                                        (uint16_t *)dz1, tail, PS, zero, F > H ? F : H)))
+        if (L == 3 && D <= 16) TBF_LAUNCH(3, 16);
+        else if (L == 3) TBF_LAUNCH(3, 32);
+        else if (D <= 16) TBF_LAUNCH(2, 16);
+        else TBF_LAUNCH(2, 32);
+#undef TBF_LAUNCH
+    } else if (L == 3 && bf) {
         TB_LAUNCH(3, uint16_t, uint16_t);
     } else if (L == 3) {
         TB_LAUNCH(3, float, float);
@@ -1799,7 +2371,7 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
         TB_LAUNCH(2, float, float);
     }
 #undef TB_LAUNCH
-    AMS_LAUNCH("tail_reduce", st, tail_reduce<<<(PS + 63) / 64, 256, 0, st>>>(tail, kTailBlocks, PS, L, H, M, D, dW2,
+    AMS_LAUNCH("tail_reduce", st, tail_reduce<<<(PS + 63) / 64, 256, 0, st>>>(tail, TG, PS, L, H, M, D, dW2,
                                                                           db2, dW3, db3, db1));
 
     const int bm = (H % 128 == 0) ? 128 : 64;
