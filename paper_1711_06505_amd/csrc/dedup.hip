@@ -152,22 +152,40 @@ __global__ __launch_bounds__(kThreads) void dd_prep(const uint32_t *__restrict__
                                                     int32_t *__restrict__ bad,
                                                     uint32_t *__restrict__ words, int n_words)
 {
-    __shared__ int h[kMaxPasses][kRadix];
-    const int t = threadIdx.x;
-    for (int p = 0; p < kMaxPasses; ++p) h[p][t] = 0;
+    // one histogram per wave (a hot ID's digit then contends within one wave
+    // only); eight keys per thread are loaded before their counts are added
+    constexpr int U = 8;
+    __shared__ int h[kWaves][kMaxPasses][kRadix];
+    const int t = threadIdx.x, wave = t / AMS_WAVE;
+    for (int w = 0; w < kWaves; ++w)
+        for (int p = 0; p < kMaxPasses; ++p) h[w][p][t] = 0;
     for (int i = blockIdx.x * kThreads + t; i < n_words; i += gridDim.x * kThreads) words[i] = 0;
     __syncthreads();
     bool out = false;
-    for (int i = blockIdx.x * kThreads + t; i < n; i += gridDim.x * kThreads) {
-        const uint32_t k = keys[i];
-        out |= (k >= n_ids);
-        for (int p = 0; p < P.passes; ++p) {
-            const uint32_t mask = (1u << pass_bits(P, p)) - 1u;
-            atomicAdd(&h[p][(k >> (p * P.width)) & mask], 1);
+    const int stride = gridDim.x * kThreads;
+    for (int i0 = blockIdx.x * kThreads + t; i0 < n; i0 += U * stride) {
+        uint32_t k[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int i = i0 + u * stride;
+            k[u] = i < n ? keys[i] : 0xffffffffu;
+        }
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            if (k[u] == 0xffffffffu && i0 + u * stride >= n) continue;
+            out |= (k[u] >= n_ids);
+            for (int p = 0; p < P.passes; ++p) {
+                const uint32_t mask = (1u << pass_bits(P, p)) - 1u;
+                atomicAdd(&h[wave][p][(k[u] >> (p * P.width)) & mask], 1);
+            }
         }
     }
     const int any_out = __syncthreads_or(out);
-    for (int p = 0; p < P.passes; ++p) hpart[((size_t)blockIdx.x * kMaxPasses + p) * kRadix + t] = h[p][t];
+    for (int p = 0; p < P.passes; ++p) {
+        int c = 0;
+        for (int w = 0; w < kWaves; ++w) c += h[w][p][t];
+        hpart[((size_t)blockIdx.x * kMaxPasses + p) * kRadix + t] = c;
+    }
     if (t == 0) bad[blockIdx.x] = any_out;
 }
 

@@ -254,31 +254,42 @@ __global__ __launch_bounds__(kThreads) void l1_fwd_f32(const float *__restrict__
 }
 
 // Stream-K forward of the 4096-wide layer (used when H is a multiple of
-// 256).  Work = (128-row x 256-column tile, K stage) iterations in tile-major
+// 256).  Work = (BM-row x 256-column tile, K stage) iterations in tile-major
 // order; a K stage is 128 bytes of every operand row (32 fp32 or 64 bf16).
 // Each of G persistent workers (one 8-wave block per CU) takes an equal
 // contiguous share, so every CU gets the same MFMA work for any number of
 // unique images.  A tile fully inside one worker's share is finished in place
 // (bias, ReLU); a tile cut by a share boundary leaves one partial accumulator
 // tile per worker, and the tail forward (which reads H1 anyway) adds the
-// pieces in K order.  Waves are 4 (M) x 2 (N), 32 x 128 each; the 3-slot DMA
-// ring and the row swizzle are those of l1_fwd_f32 with 384 tile rows (128 A
-// + 256 B).  With the whole hidden width in one tile a feature row is read
-// from HBM once, and a K stage carries 64 fp32 (or 16 bf16) MFMAs per wave
-// for its 6 DMA instructions.
+// pieces in K order.  Waves are 4 (M) x 2 (N), each BM/4 rows x 128 columns;
+// rows stream HBM->LDS by DMA with the row swizzle of l1_fwd_f32, through a
+// ring of R slots of BM + 256 rows (BM = 128, R = 3: 48 KB per slot, two
+// stages in flight while one is consumed).  Sk<> also admits BM = 256 with
+// R = 2 (64 KB slots): half the W1 bytes per gathered byte, but measured
+// slower on bf16 at every workload here (one stage in flight, and too few
+// tiles to fill the chip at ~13k unique images).
+// With the whole hidden width in one tile a feature row is read from HBM once.
 //
 // fp32: within a stage lane l supplies k = 16*(l/32) + 4*g + e to element e
 // of k-group g (one 32x32x2 MFMA per element).  bf16: the same 16-byte chunk
 // holds 8 values, k = 32*(l/32) + 8*g + e, one 32x32x16 MFMA per group.  A
 // and B agree, so the sum over the stage's k is unchanged.
 constexpr int kSkThreads = 512;
-constexpr int kSkBM = 128, kSkBN = 256;
+constexpr int kSkBN = 256;
 constexpr int kSkNB = kSkBN / 64;                         // 32-column MFMA blocks per wave: 4
 constexpr int kSkRowBytes = 128;                          // bytes of an operand row per stage
-constexpr int kSkSlot = (kSkBM + kSkBN) * kSkRowBytes / 4;  // floats per ring slot (48 KB)
-constexpr int kSkPW = (kSkBM + kSkBN) / 8 / 8;            // DMA instructions per wave: 6
-constexpr int kSkTile = kSkBM * kSkBN;
 constexpr int kSkMinIters = 32;                           // smallest share worth a worker
+
+template <typename TT>
+struct Sk {
+    static constexpr int BM = 128;                           // image rows per tile
+    static constexpr int R = 3;                              // ring slots
+    static constexpr int MB = BM / 128;                      // 32-row MFMA blocks per wave
+    static constexpr int ROWS = BM + kSkBN;                  // A rows then B rows
+    static constexpr int SLOT = ROWS * kSkRowBytes / 4;      // floats per ring slot
+    static constexpr int PW = ROWS / 64;                     // DMA instructions per wave
+    static constexpr int TILE = BM * kSkBN;                  // floats per partial tile
+};
 
 template <typename TT>
 constexpr int sk_bk() { return kSkRowBytes / (int)sizeof(TT); }   // K per stage
@@ -290,13 +301,13 @@ struct SkPlan {
     __device__ int owner(int64_t it) const { return (int)(((it + 1) * g - 1) / total); }
 };
 
-__device__ __forceinline__ SkPlan sk_plan(int n_u, int H, int F, int G, int bk)
+__device__ __forceinline__ SkPlan sk_plan(int n_u, int H, int F, int G, int bk, int bm)
 {
     SkPlan p;
     p.n_u = n_u;
     p.n_cb = H / kSkBN;
     p.S = F / bk;
-    const int64_t tiles = (int64_t)((n_u + kSkBM - 1) / kSkBM) * p.n_cb;
+    const int64_t tiles = (int64_t)((n_u + bm - 1) / bm) * p.n_cb;
     p.total = tiles * p.S;
     const int64_t want = (p.total + kSkMinIters - 1) / kSkMinIters;
     p.g = (int)(want < G ? want : G);
@@ -305,25 +316,74 @@ __device__ __forceinline__ SkPlan sk_plan(int n_u, int H, int F, int G, int bk)
 }
 
 // src[q] are byte pointers; k0b is the stage's byte offset within a row
+template <typename TT>
 __device__ __forceinline__ void sk_issue(float *slot, const char *const *src, int64_t k0b, int wave)
 {
 #pragma unroll
-    for (int q = 0; q < kSkPW; ++q) dma16(src[q] + k0b, slot + (wave * kSkPW + q) * 256);
+    for (int q = 0; q < Sk<TT>::PW; ++q) dma16(src[q] + k0b, slot + (wave * Sk<TT>::PW + q) * 256);
+}
+
+// Two 32-row blocks per wave (a 256-row tile, bf16): the operands of k-group
+// g+1 are read while the MFMAs of group g run, two groups of fragments live at
+// a time.
+__device__ __forceinline__ void sk_compute_bf16(const float *slot, v16f (*acc)[kSkNB], int lane, int wave)
+{
+    using K = Sk<uint16_t>;
+    const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
+    // byte offset of this lane's 16-byte chunk of k-group 0 in each operand
+    // row; group g's chunk is (4 h + g) ^ swz = (4 h ^ swz) ^ g, i.e. the
+    // offset XOR (g << 4) (rows are 128 bytes)
+    const char *sl = (const char *)slot;
+    int aoff[K::MB], boff[kSkNB];
+#pragma unroll
+    for (int mb = 0; mb < K::MB; ++mb) {
+        const int r = wm * 32 * K::MB + mb * 32 + r32;
+        aoff[mb] = r * 128 + (((4 * h) ^ ring_swz(r)) << 4);
+    }
+#pragma unroll
+    for (int nb = 0; nb < kSkNB; ++nb) {
+        const int r = K::BM + wn * (kSkBN / 2) + nb * 32 + r32;
+        boff[nb] = r * 128 + (((4 * h) ^ ring_swz(r)) << 4);
+    }
+    uint4 a[2][K::MB], b[2][kSkNB];
+    auto rd = [&](int g, int buf) {
+#pragma unroll
+        for (int mb = 0; mb < K::MB; ++mb) a[buf][mb] = *(const uint4 *)(sl + (aoff[mb] ^ (g << 4)));
+#pragma unroll
+        for (int nb = 0; nb < kSkNB; ++nb) b[buf][nb] = *(const uint4 *)(sl + (boff[nb] ^ (g << 4)));
+    };
+    rd(0, 0);
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+        if (g < 3) rd(g + 1, (g + 1) & 1);
+#pragma unroll
+        for (int mb = 0; mb < K::MB; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < kSkNB; ++nb) acc[mb][nb] = mfma_bf16(a[g & 1][mb], b[g & 1][nb], acc[mb][nb]);
+    }
 }
 
 template <typename TT>
-__device__ __forceinline__ void sk_compute(const float *slot, v16f *acc, int lane, int wave)
+__device__ __forceinline__ void sk_compute(const float *slot, v16f (*acc)[kSkNB], int lane, int wave)
 {
+    using K = Sk<TT>;
+    if constexpr (K::MB == 2) {
+        sk_compute_bf16(slot, acc, lane, wave);
+        return;
+    }
     const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
-    const int ra = wm * 32 + r32;
-    uint4 a[4], b[4][kSkNB];
+    uint4 a[4][K::MB], b[4][kSkNB];
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
         const int q = h * 4 + g;
-        a[g] = *(const uint4 *)&slot[ra * 32 + ((q ^ ring_swz(ra)) << 2)];
+#pragma unroll
+        for (int mb = 0; mb < K::MB; ++mb) {
+            const int ra = wm * 32 * K::MB + mb * 32 + r32;
+            a[g][mb] = *(const uint4 *)&slot[ra * 32 + ((q ^ ring_swz(ra)) << 2)];
+        }
 #pragma unroll
         for (int nb = 0; nb < kSkNB; ++nb) {
-            const int rb = kSkBM + wn * (kSkBN / 2) + nb * 32 + r32;
+            const int rb = K::BM + wn * (kSkBN / 2) + nb * 32 + r32;
             b[g][nb] = *(const uint4 *)&slot[rb * 32 + ((q ^ ring_swz(rb)) << 2)];
         }
     }
@@ -331,27 +391,32 @@ __device__ __forceinline__ void sk_compute(const float *slot, v16f *acc, int lan
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
         if constexpr (sizeof(TT) == 4) {
-            const float av[4] = {__uint_as_float(a[g].x), __uint_as_float(a[g].y), __uint_as_float(a[g].z),
-                                 __uint_as_float(a[g].w)};
 #pragma unroll
-            for (int e = 0; e < 4; ++e)
+            for (int mb = 0; mb < K::MB; ++mb) {
+                const float av[4] = {__uint_as_float(a[g][mb].x), __uint_as_float(a[g][mb].y),
+                                     __uint_as_float(a[g][mb].z), __uint_as_float(a[g][mb].w)};
 #pragma unroll
-                for (int nb = 0; nb < kSkNB; ++nb) {
-                    const float bv[4] = {__uint_as_float(b[g][nb].x), __uint_as_float(b[g][nb].y),
-                                         __uint_as_float(b[g][nb].z), __uint_as_float(b[g][nb].w)};
-                    acc[nb] = mfma_f32(av[e], bv[e], acc[nb]);
-                }
+                for (int e = 0; e < 4; ++e)
+#pragma unroll
+                    for (int nb = 0; nb < kSkNB; ++nb) {
+                        const float bv[4] = {__uint_as_float(b[g][nb].x), __uint_as_float(b[g][nb].y),
+                                             __uint_as_float(b[g][nb].z), __uint_as_float(b[g][nb].w)};
+                        acc[mb][nb] = mfma_f32(av[e], bv[e], acc[mb][nb]);
+                    }
+            }
         } else {
 #pragma unroll
-            for (int nb = 0; nb < kSkNB; ++nb) acc[nb] = mfma_bf16(a[g], b[g][nb], acc[nb]);
+            for (int mb = 0; mb < K::MB; ++mb)
+#pragma unroll
+                for (int nb = 0; nb < kSkNB; ++nb) acc[mb][nb] = mfma_bf16(a[g][mb], b[g][nb], acc[mb][nb]);
         }
     }
     // group 0's reads first, then (reads of g+1, MFMAs of g)
-    __builtin_amdgcn_sched_group_barrier(0x100, 1 + kSkNB, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, K::MB + kSkNB, 0);
 #pragma unroll
     for (int g = 0; g < 4; ++g) {
-        if (g < 3) __builtin_amdgcn_sched_group_barrier(0x100, 1 + kSkNB, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, PER_G * kSkNB, 0);
+        if (g < 3) __builtin_amdgcn_sched_group_barrier(0x100, K::MB + kSkNB, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, PER_G * K::MB * kSkNB, 0);
     }
 }
 
@@ -368,15 +433,16 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
                                                    uint16_t *__restrict__ H1b, uint16_t *__restrict__ H1lo,
                                                    float *__restrict__ pbuf)
 {
+    using K = Sk<TT>;
     constexpr int BK = sk_bk<TT>();
-    __shared__ __attribute__((aligned(16))) float ring0[kSkSlot];
-    __shared__ __attribute__((aligned(16))) float ring1[kSkSlot];
-    __shared__ __attribute__((aligned(16))) float ring2[kSkSlot];
-    __shared__ int rid[kSkBM];
+    __shared__ __attribute__((aligned(16))) float ring0[K::SLOT];
+    __shared__ __attribute__((aligned(16))) float ring1[K::SLOT];
+    __shared__ __attribute__((aligned(16))) float ring2[K::R == 3 ? K::SLOT : 4];
+    __shared__ int rid[K::BM];
 
     const int n_u = min(*n_uniq_p, cap);
     if (n_u <= 0) return;
-    const SkPlan P = sk_plan(n_u, H, F, G, BK);
+    const SkPlan P = sk_plan(n_u, H, F, G, BK, K::BM);
     // workers with consecutive shares sit on one XCD (blocks go round-robin)
     const int w = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
     if (w >= P.g) return;
@@ -389,9 +455,9 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
         const int tile = (int)(it / S);
         const int ks = (int)(it % S);
         const int ke = (int)min<int64_t>(S, ks + (it1 - it));
-        const int m0 = (tile / P.n_cb) * kSkBM, n0 = (tile % P.n_cb) * kSkBN;
+        const int m0 = (tile / P.n_cb) * K::BM, n0 = (tile % P.n_cb) * kSkBN;
         __syncthreads();                        // previous segment done with rid and the ring
-        if (t < kSkBM) {
+        if (t < K::BM) {
             int id = -1;
             if (m0 + t < n_u) {
                 id = uniq[m0 + t];
@@ -400,43 +466,69 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
             rid[t] = id;
         }
         __syncthreads();
-        const char *src[kSkPW];
+        const char *src[K::PW];
 #pragma unroll
-        for (int q = 0; q < kSkPW; ++q) {
-            const int row = (wave * kSkPW + q) * 8 + (lane >> 3);
+        for (int q = 0; q < K::PW; ++q) {
+            const int row = (wave * K::PW + q) * 8 + (lane >> 3);
             const int chunk = (lane & 7) ^ ring_swz(row);
-            if (row < kSkBM) {
+            if (row < K::BM) {
                 const int id = rid[row];
                 src[q] = (id >= 0 ? (const char *)T + (size_t)id * row_bytes : (const char *)W1) + chunk * 16;
             } else {
-                src[q] = (const char *)W1 + (size_t)(n0 + row - kSkBM) * row_bytes + chunk * 16;
+                src[q] = (const char *)W1 + (size_t)(n0 + row - K::BM) * row_bytes + chunk * 16;
             }
         }
-        v16f acc[kSkNB];
+        v16f acc[K::MB][kSkNB];
 #pragma unroll
-        for (int nb = 0; nb < kSkNB; ++nb) acc[nb] = (v16f){};
+        for (int mb = 0; mb < K::MB; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < kSkNB; ++nb) acc[mb][nb] = (v16f){};
         const int n = ke - ks;
+        if constexpr (K::R == 3) {
 #define SK_STAGE(cur, nxt, s)                                                      \
     do {                                                                           \
         __builtin_amdgcn_sched_barrier(0);                                         \
-        AMS_WAIT_VM_LDS(kSkPW);                                                    \
+        AMS_WAIT_VM_LDS(K::PW);                                                    \
         __builtin_amdgcn_s_barrier();                                              \
         __builtin_amdgcn_sched_barrier(0);                                         \
-        sk_issue(nxt, src, (int64_t)(ks + min((s) + 2, n - 1)) * kSkRowBytes, wave); \
+        sk_issue<TT>(nxt, src, (int64_t)(ks + min((s) + 2, n - 1)) * kSkRowBytes, wave); \
         __builtin_amdgcn_sched_barrier(0);                                         \
         sk_compute<TT>(cur, acc, lane, wave);                                      \
     } while (0)
-        sk_issue(ring0, src, (int64_t)ks * kSkRowBytes, wave);
-        sk_issue(ring1, src, (int64_t)(ks + min(1, n - 1)) * kSkRowBytes, wave);
-        int s = 0;
-        for (; s + 3 <= n; s += 3) {
-            SK_STAGE(ring0, ring2, s);
-            SK_STAGE(ring1, ring0, s + 1);
-            SK_STAGE(ring2, ring1, s + 2);
-        }
-        if (s < n) SK_STAGE(ring0, ring2, s);
-        if (s + 1 < n) SK_STAGE(ring1, ring0, s + 1);
+            sk_issue<TT>(ring0, src, (int64_t)ks * kSkRowBytes, wave);
+            sk_issue<TT>(ring1, src, (int64_t)(ks + min(1, n - 1)) * kSkRowBytes, wave);
+            int s = 0;
+            for (; s + 3 <= n; s += 3) {
+                SK_STAGE(ring0, ring2, s);
+                SK_STAGE(ring1, ring0, s + 1);
+                SK_STAGE(ring2, ring1, s + 2);
+            }
+            if (s < n) SK_STAGE(ring0, ring2, s);
+            if (s + 1 < n) SK_STAGE(ring1, ring0, s + 1);
 #undef SK_STAGE
+        } else {
+            // 2 slots: at the top of stage s only stage s is in flight; after the
+            // barrier (everyone is done with the other slot) stage s+1 is issued
+            // into it and stage s is computed meanwhile.
+#define SK_STAGE2(cur, nxt, s)                                                     \
+    do {                                                                           \
+        __builtin_amdgcn_sched_barrier(0);                                         \
+        AMS_WAIT_VM_LDS(0);                                                        \
+        __builtin_amdgcn_s_barrier();                                              \
+        __builtin_amdgcn_sched_barrier(0);                                         \
+        if ((s) + 1 < n) sk_issue<TT>(nxt, src, (int64_t)(ks + (s) + 1) * kSkRowBytes, wave); \
+        __builtin_amdgcn_sched_barrier(0);                                         \
+        sk_compute<TT>(cur, acc, lane, wave);                                      \
+    } while (0)
+            sk_issue<TT>(ring0, src, (int64_t)ks * kSkRowBytes, wave);
+            int s = 0;
+            for (; s + 2 <= n; s += 2) {
+                SK_STAGE2(ring0, ring1, s);
+                SK_STAGE2(ring1, ring0, s + 1);
+            }
+            if (s < n) SK_STAGE2(ring0, ring1, s);
+#undef SK_STAGE2
+        }
         AMS_WAIT_VM(0);
 
         const int wm = wave >> 1, wn = wave & 1, r32 = lane & 31;
@@ -446,26 +538,31 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
                 const int col = n0 + wn * (kSkBN / 2) + nb * 32 + r32;
                 const float bias = b1[col];
 #pragma unroll
-                for (int j = 0; j < 16; ++j) {
-                    const int r = wm * 32 + acc_row(j, lane);
-                    const float z = fmaxf(rid[r] >= 0 ? acc[nb][j] + bias : bias, 0.f);
-                    if (m0 + r < n_u) {
-                        if (H1) H1[(size_t)(m0 + r) * H + col] = z;
-                        if (H1b) {
-                            const uint16_t hi = ams_f32_to_bf16(z);
-                            H1b[(size_t)(m0 + r) * H + col] = hi;
-                            if (H1lo) H1lo[(size_t)(m0 + r) * H + col] = ams_f32_to_bf16(z - ams_bf16_to_f32(hi));
+                for (int mb = 0; mb < K::MB; ++mb)
+#pragma unroll
+                    for (int j = 0; j < 16; ++j) {
+                        const int r = wm * 32 * K::MB + mb * 32 + acc_row(j, lane);
+                        const float z = fmaxf(rid[r] >= 0 ? acc[mb][nb][j] + bias : bias, 0.f);
+                        if (m0 + r < n_u) {
+                            if (H1) H1[(size_t)(m0 + r) * H + col] = z;
+                            if (H1b) {
+                                const uint16_t hi = ams_f32_to_bf16(z);
+                                H1b[(size_t)(m0 + r) * H + col] = hi;
+                                if (H1lo) H1lo[(size_t)(m0 + r) * H + col] = ams_f32_to_bf16(z - ams_bf16_to_f32(hi));
+                            }
                         }
                     }
-                }
             }
         } else {
-            float *piece = pbuf + ((size_t)w * 2 + (first ? 0 : 1)) * kSkTile;
+            float *piece = pbuf + ((size_t)w * 2 + (first ? 0 : 1)) * K::TILE;
 #pragma unroll
-            for (int nb = 0; nb < kSkNB; ++nb)
+            for (int mb = 0; mb < K::MB; ++mb)
 #pragma unroll
-                for (int j = 0; j < 16; ++j)
-                    piece[(wm * 32 + acc_row(j, lane)) * kSkBN + wn * (kSkBN / 2) + nb * 32 + r32] = acc[nb][j];
+                for (int nb = 0; nb < kSkNB; ++nb)
+#pragma unroll
+                    for (int j = 0; j < 16; ++j)
+                        piece[(wm * 32 * K::MB + mb * 32 + acc_row(j, lane)) * kSkBN + wn * (kSkBN / 2) + nb * 32 +
+                              r32] = acc[mb][nb][j];
         }
         first = false;
         it += n;
@@ -672,8 +769,8 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
         const int cb = cbase / kSkBN;
         int wa = 0, wb = -1, slot_a = 0;
         if (sk_bk) {
-            const SkPlan P = sk_plan(n_u, H, F, G, sk_bk);
-            const int tile = (rowc / kSkBM) * P.n_cb + cb;
+            const SkPlan P = sk_plan(n_u, H, F, G, sk_bk, Sk<float>::BM);
+            const int tile = (rowc / Sk<float>::BM) * P.n_cb + cb;
             wa = P.owner((int64_t)tile * P.S);
             wb = P.owner((int64_t)(tile + 1) * P.S - 1);
             // only the first contributor can hold this tile as its second piece
@@ -683,7 +780,7 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
             // tile cut by share boundaries: add the pieces in K order
             const int id = uniq[rowc];
             const bool ok = id >= 0 && (int64_t)id < n_rows;
-            const int rl = rowc % kSkBM;
+            const int rl = rowc % Sk<float>::BM;
 #pragma unroll
             for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
@@ -695,7 +792,7 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
                         for (int w = wa; w <= wb; ++w) {
                             const int sl = w == wa ? slot_a : 0;
                             const float4 v =
-                                *(const float4 *)&pbuf[((size_t)w * 2 + sl) * kSkTile + rl * kSkBN + cl];
+                                *(const float4 *)&pbuf[((size_t)w * 2 + sl) * Sk<float>::TILE + rl * kSkBN + cl];
                             a.x += v.x;
                             a.y += v.y;
                             a.z += v.z;
@@ -860,14 +957,15 @@ __global__ __launch_bounds__(kThreads) void tail_fwd_bf16(uint16_t *__restrict__
     const int n_u = min(*n_uniq_p, cap);
     if (n_u <= 0) return;
     const bool relu2 = (L == 3) || final_relu;
-    const SkPlan P = sk_plan(n_u, H, F, G, sk_bk<uint16_t>());
+    using K = Sk<uint16_t>;
+    const SkPlan P = sk_plan(n_u, H, F, G, sk_bk<uint16_t>(), K::BM);
     for (int c0 = (blockIdx.x * (kThreads / AMS_WAVE) + wave) * 32; c0 < n_u;
          c0 += gridDim.x * (kThreads / AMS_WAVE) * 32) {
         const int row = c0 + r32;
         const bool live = row < n_u;
         const int rowc = min(row, n_u - 1);
-        // the chunk lies in one 128-row stream-K tile: finished in place or cut
-        const int tile = c0 / kSkBM;
+        // the chunk lies in one stream-K row tile: finished in place or cut
+        const int tile = c0 / K::BM;
         const int wa = P.owner((int64_t)tile * P.S), wb = P.owner((int64_t)(tile + 1) * P.S - 1);
         const bool split = wb > wa;
         const int slot_a = (tile == (int)(P.it0(wa) / P.S)) ? 0 : 1;   // first contributor's piece
@@ -876,7 +974,7 @@ __global__ __launch_bounds__(kThreads) void tail_fwd_bf16(uint16_t *__restrict__
             const int id = uniq[rowc];
             id_ok = id >= 0 && (int64_t)id < n_rows;
         }
-        const int rl = rowc % kSkBM;
+        const int rl = rowc % K::BM;
         const size_t roff = (size_t)rowc * H + 8 * h;
         v16f acc[2] = {(v16f){}, (v16f){}};
 #pragma unroll
@@ -891,7 +989,7 @@ __global__ __launch_bounds__(kThreads) void tail_fwd_bf16(uint16_t *__restrict__
                     for (int pi = 0; pi < 3; ++pi) {
                         const int w = wa + pi;
                         if (w <= wb) {
-                            const float *pc = pbuf + ((size_t)w * 2 + (pi == 0 ? slot_a : 0)) * kSkTile +
+                            const float *pc = pbuf + ((size_t)w * 2 + (pi == 0 ? slot_a : 0)) * K::TILE +
                                               rl * kSkBN + k0;
                             const float4 v0 = *(const float4 *)pc, v1 = *(const float4 *)(pc + 4);
                             x[0] += v0.x; x[1] += v0.y; x[2] += v0.z; x[3] += v0.w;
@@ -899,7 +997,7 @@ __global__ __launch_bounds__(kThreads) void tail_fwd_bf16(uint16_t *__restrict__
                         }
                     }
                     for (int w = wa + 3; w <= wb; ++w) {     // (a tile spans at most 3 shares)
-                        const float *pc = pbuf + ((size_t)w * 2) * kSkTile + rl * kSkBN + k0;
+                        const float *pc = pbuf + ((size_t)w * 2) * K::TILE + rl * kSkBN + k0;
                         const float4 v0 = *(const float4 *)pc, v1 = *(const float4 *)(pc + 4);
                         x[0] += v0.x; x[1] += v0.y; x[2] += v0.z; x[3] += v0.w;
                         x[4] += v1.x; x[5] += v1.y; x[6] += v1.z; x[7] += v1.w;
@@ -2213,7 +2311,8 @@ extern "C" size_t ams_embed_workspace(const ams_mlp *mlp, int32_t n_uniq_cap)
     // forward: fp32 H1 (bf16 mode, or when the caller keeps no fp32 H1_save),
     // then the stream-K partial tiles (two per worker)
     size_t fwd = al256((size_t)n_uniq_cap * mlp->dims[1] * 4);
-    if (use_stream_k(mlp)) fwd += al256((size_t)sk_workers() * 2 * kSkTile * 4);
+    if (use_stream_k(mlp))
+        fwd += al256((size_t)sk_workers() * 2 * (mlp->dtype == AMS_BF16 ? Sk<uint16_t>::TILE : Sk<float>::TILE) * 4);
     const size_t bwd = plan_bwd(mlp, n_uniq_cap).total;
     return fwd > bwd ? fwd : bwd;
 }
@@ -2240,7 +2339,7 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
     const bool sk = use_stream_k(mlp);
     const int G = sk ? sk_workers() : 0;
     const size_t h1_bytes = al256((size_t)cap * H * 4);
-    const size_t need = h1_bytes + (sk ? al256((size_t)G * 2 * kSkTile * 4) : 0);
+    const size_t need = h1_bytes + (sk ? al256((size_t)G * 2 * (bf ? Sk<uint16_t>::TILE : Sk<float>::TILE) * 4) : 0);
     if ((h1_in_ws || sk) && (!ws || ws_bytes < need)) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     float *H1f = h1_in_ws ? (float *)ws : (float *)H1_save;
@@ -2279,9 +2378,10 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
                                                        (uint16_t *)H1_save));
     }
     if (sk && bf) {
-        // the small layers on bf16 MFMA (split tiles of layer 1 finished on the way)
+        // the small layers on bf16 MFMA (split tiles of layer 1 finished on the
+        // way); two resident blocks per CU stage W2 once and loop over chunks
         int tg = (cap + 4 * 32 - 1) / (4 * 32);
-        if (tg > 2048) tg = 2048;
+        if (tg > 2 * G) tg = 2 * G;
         if (L == 3)
             AMS_LAUNCH("tail_fwd_bf16", st, tail_fwd_bf16<3><<<tg, kThreads, 0, st>>>(
                                                 h1b, h1lo, pbuf, F, G, b1, uniq, n_rows, M, D, (const uint16_t *)W2,
