@@ -28,6 +28,23 @@
  *              weight and bias gradients summed over unique images in ascending
  *              order.  No gradient flows into the fixed feature table.
  *
+ * For the joint step (the worker of Algorithm 1 next to the image path):
+ *
+ *   bag fwd    per sample and ID table, the sum of the table rows of its
+ *              behaviors' IDs and of its ad's ID (the sparse ID features of
+ *              section 3.2, embedded from key-value tables as in section 4.1,
+ *              sum-pooled like the behavior images).
+ *   ctr        the CTR MLP on [pooled user image vector, ad image embedding,
+ *              one bag per table], ReLU between layers, softmax over the
+ *              classes and cross-entropy with the click label (section 3.1),
+ *              averaged over the batch; its backward gives the worker
+ *              gradients and the gradients of every input field, among them
+ *              delta_e for the image path (Algorithm 1, WORKERITERATION).
+ *   adagrad    the sparse Adagrad step of the touched ID rows: accum += g^2,
+ *              row -= lr g / (sqrt(accum) + eps), elementwise.
+ * The merged gradient of an ID row is the SUM aggregator's backward with the
+ * bag gradient as upstream (orc_pool_bwd, mode SUM).
+ *
  * Readings where the paper is silent (documented with the library): no
  * activation after the last layer unless final_relu is set; ReLU'(0) = 0;
  * the max-pool argmax is the first (lowest) position attaining the maximum;
@@ -401,5 +418,159 @@ int orc_pool_bwd(int mode, int32_t B, int32_t D, const int32_t *seg_off,
         for (int d = 0; d < D; ++d)
             dE[(size_t)inv[k] * D + d] += ge[(size_t)k * D + d];
     if (!ge_out) free(ge);
+    return 0;
+}
+
+/* ---------------------------------------------------------------- bag fwd */
+
+/*
+ * bag[i][d] = sum_{j in [seg_off[i], seg_off[i+1])} table[idx[j]][d]
+ *             + table[idx[n_beh + i]][d]
+ * summed in ascending j, the ad row last.  table is float32 [n_rows x D];
+ * idx holds row numbers of `table` (raw IDs of a whole table, or positions
+ * in a table of just the touched rows).
+ */
+int orc_bag_fwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
+                const int32_t *idx, int64_t n_rows, const float *table, double *bag)
+{
+    if (B < 0 || D < 1) return 1;
+    for (int64_t k = 0; k < n_beh + B; ++k)
+        if (idx[k] < 0 || idx[k] >= n_rows) return 2;
+#pragma omp parallel for schedule(static)
+    for (int32_t i = 0; i < B; ++i) {
+        double *o = bag + (size_t)i * D;
+        for (int d = 0; d < D; ++d) o[d] = 0.0;
+        for (int64_t j = seg_off[i]; j < seg_off[i + 1]; ++j)
+            for (int d = 0; d < D; ++d) o[d] += (double)table[(size_t)idx[j] * D + d];
+        for (int d = 0; d < D; ++d) o[d] += (double)table[(size_t)idx[n_beh + i] * D + d];
+    }
+    return 0;
+}
+
+/* --------------------------------------------------------------- CTR MLP */
+
+/*
+ * X [B x dims[0]] float64 input rows; W[l] float32 [dims[l+1] x dims[l]],
+ * b[l] float32 [dims[l+1]]; labels int32 [B] in [0, C), C = dims[n_layers].
+ * Forward: Z_l = H_{l-1} W_l^T + b_l, H_l = ReLU(Z_l) below the last layer,
+ * logits Z_L; p = softmax(Z_L) (max subtracted); loss = mean_i (lse_i - Z_L[i][y_i]).
+ * Backward of the mean loss: dZ_L = (p - onehot(y)) / B; dW_l = sum_i dZ_l[i]^T
+ * H_{l-1}[i] and db_l = sum_i dZ_l[i] (ascending i); dH_{l-1} = dZ_l W_l,
+ * dZ_{l-1} = dH_{l-1} * [Z_{l-1} > 0]; dX = dZ_1 W_1.
+ * Outputs: *loss, prob [B x C], Z (concatenated per layer, [B x dims[l+1]]),
+ * dW, db (concatenated per layer), dX [B x dims[0]].
+ */
+int orc_ctr_fwd_bwd(int32_t B, int n_layers, const int32_t *dims, const float *const *W,
+                    const float *const *b, const double *X, const int32_t *labels,
+                    double *loss, double *prob, double *Z, double *dW, double *db, double *dX)
+{
+    if (B < 1 || n_layers < 1 || n_layers > 15) return 1;
+    const int C = dims[n_layers];
+    for (int32_t i = 0; i < B; ++i)
+        if (labels[i] < 0 || labels[i] >= C) return 1;
+    size_t zoff[16], woff[16], boff[16];
+    zoff[0] = woff[0] = boff[0] = 0;
+    int wmax = 0;
+    for (int l = 0; l < n_layers; ++l) {
+        zoff[l + 1] = zoff[l] + (size_t)B * dims[l + 1];
+        woff[l + 1] = woff[l] + (size_t)dims[l] * dims[l + 1];
+        boff[l + 1] = boff[l] + (size_t)dims[l + 1];
+    }
+    for (int l = 0; l <= n_layers; ++l) if (dims[l] > wmax) wmax = dims[l];
+    /* forward, sample by sample */
+    double *lossv = (double *)malloc(sizeof(double) * (size_t)B);
+#pragma omp parallel
+    {
+        double *h = (double *)malloc(sizeof(double) * (size_t)wmax);
+#pragma omp for schedule(static)
+        for (int32_t i = 0; i < B; ++i) {
+            for (int k = 0; k < dims[0]; ++k) h[k] = X[(size_t)i * dims[0] + k];
+            for (int l = 0; l < n_layers; ++l) {
+                const int in = dims[l], out = dims[l + 1];
+                double *z = Z + zoff[l] + (size_t)i * out;
+                for (int o = 0; o < out; ++o) {
+                    double acc = (double)b[l][o];
+                    for (int k = 0; k < in; ++k) acc += (double)W[l][(size_t)o * in + k] * h[k];
+                    z[o] = acc;
+                }
+                for (int o = 0; o < out; ++o) h[o] = (l < n_layers - 1) ? (z[o] > 0.0 ? z[o] : 0.0) : z[o];
+            }
+            const double *zl = Z + zoff[n_layers - 1] + (size_t)i * C;
+            double m = zl[0];
+            for (int c = 1; c < C; ++c) if (zl[c] > m) m = zl[c];
+            double se = 0.0;
+            for (int c = 0; c < C; ++c) se += exp(zl[c] - m);
+            const double lse = m + log(se);
+            for (int c = 0; c < C; ++c) prob[(size_t)i * C + c] = exp(zl[c] - lse);
+            lossv[i] = lse - zl[labels[i]];
+        }
+        free(h);
+    }
+    double tot = 0.0;
+    for (int32_t i = 0; i < B; ++i) tot += lossv[i];
+    *loss = tot / B;
+    free(lossv);
+    /* backward: dZ of every layer, then the weight gradients */
+    double *dZ = (double *)malloc(sizeof(double) * zoff[n_layers]);
+    for (int32_t i = 0; i < B; ++i)
+        for (int c = 0; c < C; ++c)
+            dZ[zoff[n_layers - 1] + (size_t)i * C + c] =
+                (prob[(size_t)i * C + c] - (c == labels[i] ? 1.0 : 0.0)) / B;
+    for (int l = n_layers - 1; l >= 0; --l) {
+        const int in = dims[l], out = dims[l + 1];
+        const double *dz = dZ + zoff[l];
+#pragma omp parallel for schedule(static)
+        for (int32_t i = 0; i < B; ++i) {
+            for (int k = 0; k < in; ++k) {
+                double acc = 0.0;
+                for (int o = 0; o < out; ++o) acc += dz[(size_t)i * out + o] * (double)W[l][(size_t)o * in + k];
+                if (l > 0) {
+                    const double zp = Z[zoff[l - 1] + (size_t)i * in + k];
+                    dZ[zoff[l - 1] + (size_t)i * in + k] = zp > 0.0 ? acc : 0.0;
+                } else {
+                    dX[(size_t)i * in + k] = acc;
+                }
+            }
+        }
+        /* dW_l[o][k] = sum_i dz[i][o] h_{l-1}[i][k], h_{-1} = X */
+#pragma omp parallel for schedule(static)
+        for (int o = 0; o < out; ++o) {
+            double *row = dW + woff[l] + (size_t)o * in;
+            for (int k = 0; k < in; ++k) row[k] = 0.0;
+            double bsum = 0.0;
+            for (int32_t i = 0; i < B; ++i) {
+                const double g = dz[(size_t)i * out + o];
+                bsum += g;
+                for (int k = 0; k < in; ++k) {
+                    double hk;
+                    if (l == 0) hk = X[(size_t)i * in + k];
+                    else {
+                        const double zp = Z[zoff[l - 1] + (size_t)i * in + k];
+                        hk = zp > 0.0 ? zp : 0.0;
+                    }
+                    row[k] += g * hk;
+                }
+            }
+            db[boff[l] + o] = bsum;
+        }
+    }
+    free(dZ);
+    return 0;
+}
+
+/* ---------------------------------------------------------------- adagrad */
+
+/*
+ * Sparse Adagrad on n touched rows (row-compact arrays [n x D]):
+ * accum += g^2; rows -= lr * g / (sqrt(accum) + eps), elementwise.
+ */
+int orc_adagrad_rows(int32_t n, int32_t D, const double *grad, double lr, double eps,
+                     double *rows, double *accum)
+{
+    if (n < 0 || D < 1) return 1;
+    for (size_t e = 0; e < (size_t)n * D; ++e) {
+        accum[e] += grad[e] * grad[e];
+        rows[e] -= lr * grad[e] / (sqrt(accum[e]) + eps);
+    }
     return 0;
 }

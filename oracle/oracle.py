@@ -53,6 +53,9 @@ def _load():
     lib.orc_mlp_bwd.argtypes = [ctypes.c_int, P, ctypes.c_int, P, i64, P, i32, P, ctypes.c_int, P, P, P, P, P]
     lib.orc_pool_fwd.argtypes = [ctypes.c_int, i32, i32, P, i64, P, P, P, P, P, P]
     lib.orc_pool_bwd.argtypes = [ctypes.c_int, i32, i32, P, i64, P, i32, P, P, P, P, P, P, P, P, P, P]
+    lib.orc_bag_fwd.argtypes = [i32, i32, P, i64, P, i64, P, P]
+    lib.orc_ctr_fwd_bwd.argtypes = [i32, ctypes.c_int, P, P, P, P, P, P, P, P, P, P, P]
+    lib.orc_adagrad_rows.argtypes = [i32, i32, P, ctypes.c_double, ctypes.c_double, P, P]
     lib.orc_num_threads.restype = ctypes.c_int
     lib.orc_set_threads.argtypes = [ctypes.c_int]
     _lib = lib
@@ -255,3 +258,136 @@ def step(batch: dict, n_ids: int, T, Ws, bs, mode: str, final_relu: bool = False
                   batch["g_u"], batch.get("g_a"))
     bw = mlp_bwd(T, rows, Ws, fw, pb["dE"], final_relu)
     return {"dedup": dd, "fwd": fw, "pool": pf, "pool_bwd": pb, "bwd": bw}
+
+
+# ------------------------------------------------- joint step (worker side)
+
+def bag_fwd(seg_off, idx, table) -> np.ndarray:
+    """Per sample: sum of table[idx[j]] over its behaviors plus table[idx[n_beh + i]]."""
+    lib = _load()
+    seg_off = _i32(seg_off)
+    idx = _i32(idx)
+    tab = np.ascontiguousarray(np.asarray(table.detach().cpu() if hasattr(table, "detach") else table),
+                               dtype=np.float32)
+    B = seg_off.size - 1
+    D = tab.shape[1]
+    n_beh = int(seg_off[-1])
+    if idx.size != n_beh + B:
+        raise ValueError("idx must hold the behaviors then one ad per sample")
+    bag = np.zeros((max(B, 1), D), np.float64)
+    _check(lib.orc_bag_fwd(B, D, _ptr(seg_off), n_beh, _ptr(idx), tab.shape[0], _ptr(tab), _ptr(bag)),
+           "bag_fwd")
+    return bag[:B].copy()
+
+
+def _f32list(xs):
+    return [np.ascontiguousarray(np.asarray(x.detach().cpu() if hasattr(x, "detach") else x),
+                                 dtype=np.float32) for x in xs]
+
+
+def ctr_fwd_bwd(X, labels, Ws, bs) -> dict:
+    """CTR MLP with softmax cross-entropy (mean over the batch): loss, prob,
+    pre-activations Z[l], gradients dW[l], db[l] and dX."""
+    lib = _load()
+    X = _f64(X)
+    labels = _i32(labels)
+    Wn, bn = _f32list(Ws), _f32list(bs)
+    L = len(Wn)
+    dims = [Wn[0].shape[1]] + [W.shape[0] for W in Wn]
+    B = X.shape[0]
+    if X.shape[1] != dims[0] or labels.size != B:
+        raise ValueError("shapes")
+    loss = np.zeros(1, np.float64)
+    prob = np.zeros((B, dims[-1]), np.float64)
+    Z = np.zeros(sum(B * d for d in dims[1:]), np.float64)
+    dW = np.zeros(sum(a * b for a, b in zip(dims[:-1], dims[1:])), np.float64)
+    db = np.zeros(sum(dims[1:]), np.float64)
+    dX = np.zeros_like(X)
+    Wp = (ctypes.c_void_p * L)(*[W.ctypes.data for W in Wn])
+    bp = (ctypes.c_void_p * L)(*[b.ctypes.data for b in bn])
+    dims_a = np.array(dims, np.int32)
+    _check(lib.orc_ctr_fwd_bwd(B, L, _ptr(dims_a), Wp, bp, _ptr(X), _ptr(labels), _ptr(loss), _ptr(prob),
+                               _ptr(Z), _ptr(dW), _ptr(db), _ptr(dX)), "ctr_fwd_bwd")
+    Zs, dWs, dbs = [], [], []
+    oz = ow = ob = 0
+    for fi, fo in zip(dims[:-1], dims[1:]):
+        Zs.append(Z[oz:oz + B * fo].reshape(B, fo).copy())
+        dWs.append(dW[ow:ow + fi * fo].reshape(fo, fi).copy())
+        dbs.append(db[ob:ob + fo].copy())
+        oz += B * fo
+        ow += fi * fo
+        ob += fo
+    return {"loss": float(loss[0]), "prob": prob, "Z": Zs, "dW": dWs, "db": dbs, "dX": dX}
+
+
+def adagrad_rows(grad, rows, accum, lr: float, eps: float):
+    """One sparse Adagrad step of the touched rows (row-compact): returns the
+    new rows and accumulators (float64)."""
+    lib = _load()
+    g = _f64(grad)
+    r = _f64(rows).copy()
+    a = _f64(accum).copy()
+    n, D = g.shape
+    _check(lib.orc_adagrad_rows(n, D, _ptr(g), float(lr), float(eps), _ptr(r), _ptr(a)), "adagrad_rows")
+    return r, a
+
+
+def merged_row_grad(seg_off, inv, n_uniq: int, dbag) -> np.ndarray:
+    """Gradient of every touched row: the sum over its occurrences (ascending)
+    of the bag gradient of the sample each belongs to (the SUM aggregator's
+    backward with the bag gradient as upstream for behaviors and ad alike)."""
+    dbag = _f64(dbag)
+    D = dbag.shape[1]
+    B = dbag.shape[0]
+    fwd = {"U": np.zeros((B, D)), "A": np.zeros((B, D)), "w": np.zeros(1), "argmax": np.full((B, D), -1, np.int32)}
+    return pool_bwd("sum", seg_off, inv, n_uniq, np.zeros((max(n_uniq, 1), D)), fwd, dbag, dbag)["dE"]
+
+
+def joint_step(batch: dict, jb: dict, spec, n_ids: int, T, Ws, bs, id_rows, ctr_Ws, ctr_bs, accum,
+               mode: str = "att", table_is_compact: bool = True) -> dict:
+    """One joint training step (Algorithm 1: worker iteration, server embed and
+    update) in float64.
+
+    batch / jb:  image batch (make_batch) and its ID features (make_joint)
+    T:           image feature rows of the batch's unique images (compact, ascending
+                 ID) or the whole table
+    id_rows[t]:  rows of ID table t for its unique IDs (ascending), float32
+    accum[t]:    their Adagrad accumulators
+    spec:        the workload's JointSpec (lr, eps)
+    Returns the image-step pieces (dedup, fwd, pool, pool_bwd, bwd), the ID
+    dedups, bags, the CTR forward/backward, the merged row gradients and the
+    Adagrad results (new rows and accumulators, float64).
+    """
+    occ = np.concatenate([_i32(batch["beh_ids"]), _i32(batch["ad_ids"])])
+    dd = dedup(occ, n_ids)
+    rows = np.arange(dd["n_uniq"], dtype=np.int32) if table_is_compact else dd["uniq"]
+    fw = mlp_fwd(T, rows, Ws, bs)
+    pf = pool_fwd(mode, batch["seg_off"], dd["inv"], fw["E"])
+    n_t = len(jb["beh_ids"])
+    idd, bags = [], []
+    for t in range(n_t):
+        o_t = np.concatenate([_i32(jb["beh_ids"][t]), _i32(jb["ad_ids"][t])])
+        idd.append(dedup(o_t, spec.id_rows[t]))
+        bags.append(bag_fwd(batch["seg_off"], idd[t]["inv"], id_rows[t]))
+    X = np.concatenate([pf["U"], pf["A"]] + bags, axis=1)
+    cf = ctr_fwd_bwd(X, jb["labels"], ctr_Ws, ctr_bs)
+    D = pf["U"].shape[1]
+    dU, dA = cf["dX"][:, :D], cf["dX"][:, D:2 * D]
+    dbags = []
+    o = 2 * D
+    for t in range(n_t):
+        w_t = bags[t].shape[1]
+        dbags.append(cf["dX"][:, o:o + w_t])
+        o += w_t
+    pb = pool_bwd(mode, batch["seg_off"], dd["inv"], dd["n_uniq"], fw["E"], pf, dU, dA)
+    bw = mlp_bwd(T, rows, Ws, fw, pb["dE"])
+    grads, new_rows, new_acc = [], [], []
+    for t in range(n_t):
+        g = merged_row_grad(batch["seg_off"], idd[t]["inv"], idd[t]["n_uniq"], dbags[t])
+        grads.append(g)
+        r, a = adagrad_rows(g, id_rows[t], accum[t], spec.lr, spec.eps)
+        new_rows.append(r)
+        new_acc.append(a)
+    return {"dedup": dd, "fwd": fw, "pool": pf, "pool_bwd": pb, "bwd": bw, "id_dedup": idd, "bags": bags,
+            "X": X, "ctr": cf, "dU": dU, "dA": dA, "dbags": dbags, "row_grads": grads,
+            "new_rows": new_rows, "new_accum": new_acc}

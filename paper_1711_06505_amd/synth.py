@@ -27,9 +27,39 @@ import numpy as np
 import torch
 
 __all__ = [
-    "Workload", "WORKLOADS", "get", "make_batch", "make_weights",
+    "Workload", "JointSpec", "WORKLOADS", "get", "make_batch", "make_weights",
     "table_rows", "table_full", "table_chunks", "occurrences",
+    "ctr_dims", "make_joint", "joint_occurrences", "make_ctr_weights",
+    "id_table_rows", "id_table_full",
 ]
+
+
+@dataclasses.dataclass(frozen=True)
+class JointSpec:
+    """Worker side of a joint step (Algorithm 1, WORKERITERATION): sparse ID
+    features embedded from key-value tables (section 4.1) next to the image
+    embeddings, and the CTR model on top of them, trained with cross-entropy
+    (section 3.1).
+
+    id_rows:    rows of each ID table (one ID of each table per behavior and
+                per ad), id_dim-wide float32 rows
+    id_zipf:    Zipf exponent of the IDs of every table (ranks scattered by a
+                seeded permutation per table)
+    ctr_hidden: hidden widths of the CTR MLP; its input is the pooled user
+                image vector, the ad image embedding and one bag per table
+    n_classes:  softmax classes (2: click / no click)
+    label_p:    probability of a click label
+    lr, eps, acc0: sparse Adagrad on the touched ID rows
+    """
+    id_rows: tuple
+    id_dim: int
+    id_zipf: float
+    ctr_hidden: tuple
+    n_classes: int
+    label_p: float
+    lr: float = 0.01
+    eps: float = 1e-8
+    acc0: float = 0.0
 
 
 @dataclasses.dataclass(frozen=True)
@@ -45,6 +75,7 @@ class Workload:
     stream:  seed stream; workloads that differ only in storage dtype share it,
              so they see the same batch, the same table values and the same
              weights (rounded to bf16 where stored in bf16)
+    joint:   the ID features and CTR model of a joint step, or None
     """
     name: str
     index: int
@@ -57,6 +88,7 @@ class Workload:
     table: str
     pools: tuple
     stream: int = -1
+    joint: JointSpec | None = None
 
     @property
     def seed_stream(self) -> int:
@@ -94,6 +126,20 @@ WORKLOADS = {
     "c3_long": Workload("c3_long", 3, 4096, ("geometric", 200, 500), 2_000_000,
                         ("zipf", 1.05), (4096, 256, 64, 12), "bf16",
                         "relu_normal", ("att",)),
+    # Joint step: the long-behavior image path (same stream: same batch, table
+    # and weights) plus three ID tables (10M, 1M, 10k rows x 12 fp32), each
+    # ID Zipf(1.05), bag-summed over the behaviors and the ad; CTR MLP
+    # 60-200-80-2 fp32 with softmax cross-entropy; sparse Adagrad on the
+    # touched ID rows.
+    "c4_joint": Workload("c4_joint", 4, 4096, ("geometric", 200, 500), 2_000_000,
+                         ("zipf", 1.05), (4096, 256, 64, 12), "bf16",
+                         "relu_normal", ("att",), stream=3,
+                         joint=JointSpec((10_000_000, 1_000_000, 10_000), 12, 1.05, (200, 80), 2, 0.05)),
+    # Small joint step for tests: the tiny image path, small ID tables, a
+    # narrow CTR MLP, clicks frequent enough that both classes occur.
+    "tiny_joint": Workload("tiny_joint", 5, 64, ("fixed", 8), 512, ("uniform",),
+                           (256, 64, 16), "f32", "normal", ("att",), stream=0,
+                           joint=JointSpec((1000, 100, 10), 12, 1.05, (32, 16), 2, 0.3)),
 }
 _BY_INDEX = {w.index: w for w in WORKLOADS.values()}
 
@@ -129,24 +175,27 @@ def _lengths(w: Workload, rng) -> np.ndarray:
 _ZIPF_CACHE: dict = {}
 
 
+def _zipf_ids(rng, n: int, N: int, s: float, perm: np.ndarray) -> np.ndarray:
+    key = (N, s)
+    cdf = _ZIPF_CACHE.get(key)
+    if cdf is None:
+        # finite Zipf: P(rank r) proportional to r^-s for r = 1..N
+        pmf = np.arange(1, N + 1, dtype=np.float64) ** (-s)
+        cdf = np.cumsum(pmf)
+        cdf /= cdf[-1]
+        _ZIPF_CACHE[key] = cdf
+    u = rng.random(n)
+    rank = np.minimum(np.searchsorted(cdf, u, side="right"), N - 1)
+    # scatter hot ranks over the table with a seeded permutation
+    return perm[rank].astype(np.int32)
+
+
 def _draw_ids(w: Workload, rng, n: int, perm: np.ndarray | None) -> np.ndarray:
     if n == 0:
         return np.zeros(0, dtype=np.int32)
     if w.ids[0] == "uniform":
         return rng.integers(0, w.n_images, size=n, dtype=np.int64).astype(np.int32)
-    s = float(w.ids[1])
-    key = (w.n_images, s)
-    cdf = _ZIPF_CACHE.get(key)
-    if cdf is None:
-        # finite Zipf: P(rank r) proportional to r^-s for r = 1..N
-        pmf = np.arange(1, w.n_images + 1, dtype=np.float64) ** (-s)
-        cdf = np.cumsum(pmf)
-        cdf /= cdf[-1]
-        _ZIPF_CACHE[key] = cdf
-    u = rng.random(n)
-    rank = np.minimum(np.searchsorted(cdf, u, side="right"), w.n_images - 1)
-    # scatter hot ranks over the table with a seeded permutation
-    return perm[rank].astype(np.int32)
+    return _zipf_ids(rng, n, w.n_images, float(w.ids[1]), perm)
 
 
 def make_batch(w, k: int = 0, seed: int = 0, batch: int | None = None) -> dict:
@@ -278,4 +327,108 @@ def table_full(w, device="cpu", seed: int = 0, chunk_rows: int = 16384) -> torch
     out = torch.empty((w.n_images, w.in_dim), dtype=_storage(w), device=device)
     for s, vals in table_chunks(w, device, seed, chunk_rows):
         out[s:s + vals.shape[0]] = vals
+    return out
+
+
+# ---- joint step: ID features, labels, CTR weights ----------------------------
+
+def ctr_dims(w) -> tuple:
+    """Layer widths of the CTR MLP: [pooled user image vector, ad image
+    embedding, one bag per ID table] -> hidden -> classes (60-200-80-2)."""
+    w = get(w)
+    j = w.joint
+    return (2 * w.out_dim + len(j.id_rows) * j.id_dim,) + tuple(j.ctr_hidden) + (j.n_classes,)
+
+
+_PERM_CACHE: dict = {}
+
+
+def _id_perm(w: Workload, t: int, seed: int) -> np.ndarray:
+    key = (w.seed_stream, seed, t, w.joint.id_rows[t])
+    p = _PERM_CACHE.get(key)
+    if p is None:
+        p = np.random.default_rng(np.random.SeedSequence([seed, w.seed_stream, 1 << 21, t])).permutation(
+            w.joint.id_rows[t])
+        _PERM_CACHE.clear()
+        _PERM_CACHE[key] = p
+    return p
+
+
+def make_joint(w, batch: dict, k: int = 0, seed: int = 0) -> dict:
+    """The ID features and click labels of batch `batch` (from make_batch):
+    beh_ids[t] int32[n_beh] and ad_ids[t] int32[B] for every ID table t
+    (behavior IDs in the same sample order as the image IDs), labels int32[B]
+    in {0, 1} ~ Bernoulli(label_p).  Drawn from streams of their own, so the
+    image part of the batch is that of the plain workload."""
+    w = get(w)
+    j = w.joint
+    n_beh = int(batch["seg_off"][-1])
+    B = batch["seg_off"].size - 1
+    kids = np.random.SeedSequence([seed, w.seed_stream, k, 99]).spawn(2 * len(j.id_rows) + 1)
+    rngs = [np.random.default_rng(x) for x in kids]
+    beh, ad = [], []
+    for t, N in enumerate(j.id_rows):
+        perm = _id_perm(w, t, seed)
+        beh.append(_zipf_ids(rngs[2 * t], n_beh, N, j.id_zipf, perm) if n_beh else np.zeros(0, np.int32))
+        ad.append(_zipf_ids(rngs[2 * t + 1], B, N, j.id_zipf, perm))
+    labels = (rngs[-1].random(B) < j.label_p).astype(np.int32)
+    return {"beh_ids": beh, "ad_ids": ad, "labels": labels}
+
+
+def joint_occurrences(jb: dict, t: int) -> np.ndarray:
+    """Behavior IDs then ad IDs of ID table t: the list one step deduplicates."""
+    return np.concatenate([jb["beh_ids"][t], jb["ad_ids"][t]]).astype(np.int32)
+
+
+def make_ctr_weights(w, seed: int = 0, bias_scale: float = 0.1):
+    """Glorot-uniform float32 weights [out, in] and U(-bias_scale, bias_scale)
+    biases of the CTR MLP (torch CPU tensors)."""
+    w = get(w)
+    rng = np.random.default_rng(np.random.SeedSequence([seed, w.seed_stream, 8]))
+    dims = ctr_dims(w)
+    Ws, bs = [], []
+    for fi, fo in zip(dims[:-1], dims[1:]):
+        lim = math.sqrt(6.0 / (fi + fo))
+        Ws.append(torch.from_numpy(rng.uniform(-lim, lim, size=(fo, fi)).astype(np.float32)))
+        bs.append(torch.from_numpy(rng.uniform(-bias_scale, bias_scale, size=(fo,)).astype(np.float32)))
+    return Ws, bs
+
+
+def _id_values(w: Workload, t: int, rows: torch.Tensor, seed: int) -> torch.Tensor:
+    """float32 [len(rows), id_dim] rows of ID table t: 0.1 x Irwin-Hall(3) from
+    the same counter-based hash as the feature table, salted per table."""
+    Dd = w.joint.id_dim
+    cols = torch.arange(Dd, device=rows.device, dtype=torch.int64)
+    c = rows.to(torch.int64)[:, None] * Dd + cols[None, :]
+    lo = c & _M32
+    hi = c >> 32
+    sa = (0x27D4EB2F * (2 * seed + 1) + 0x165667B1 * (w.seed_stream + 16 * (t + 1))) & _M32
+    sb = (0xC2B2AE3D * (2 * seed + 1) + 0x9E3779B9 * (w.seed_stream + 16 * (t + 1))) & _M32
+    ha = _mix32(_mix32(lo ^ sa) ^ hi)
+    hb = _mix32(_mix32(lo ^ sb) ^ hi)
+    u1, u2 = ha >> 11, hb >> 11
+    u3 = ((ha & 0x7FF) << 10) | (hb & 0x3FF)
+    s = 2 * (u1 + u2 + u3) - 3 * ((1 << 21) - 1)
+    return s.to(torch.float32) * (0.1 / (1 << 21))
+
+
+def id_table_rows(w, t: int, rows, device="cpu", seed: int = 0, chunk_rows: int = 1 << 20) -> torch.Tensor:
+    """Rows `rows` of ID table t, float32 [len(rows), id_dim]."""
+    w = get(w)
+    rows = torch.as_tensor(np.asarray(rows), dtype=torch.int64).to(device)
+    out = torch.empty((rows.numel(), w.joint.id_dim), dtype=torch.float32, device=device)
+    for s0 in range(0, rows.numel(), chunk_rows):
+        e = min(rows.numel(), s0 + chunk_rows)
+        out[s0:e] = _id_values(w, t, rows[s0:e], seed)
+    return out
+
+
+def id_table_full(w, t: int, device="cpu", seed: int = 0, chunk_rows: int = 1 << 20) -> torch.Tensor:
+    """The whole ID table t, float32 [id_rows[t], id_dim] on `device`."""
+    w = get(w)
+    N = w.joint.id_rows[t]
+    out = torch.empty((N, w.joint.id_dim), dtype=torch.float32, device=device)
+    for s0 in range(0, N, chunk_rows):
+        e = min(N, s0 + chunk_rows)
+        out[s0:e] = _id_values(w, t, torch.arange(s0, e, device=device, dtype=torch.int64), seed)
     return out

@@ -64,3 +64,72 @@ def step_autograd(batch, T, Ws, bs, mode: str, final_relu: bool = False):
         "ge": E_occ.grad.numpy(), "L": float(L.detach()),
         "dW": [w.grad.numpy() for w in W], "db": [x.grad.numpy() for x in b],
     }
+
+
+def joint_autograd(batch, jb, T, Ws, bs, id_tables, ctr_Ws, ctr_bs, mode: str = "att"):
+    """The joint step in float64 autograd, every occurrence embedded on its own.
+
+    Image path as step_autograd (no dedup); each ID table is bag-summed over a
+    sample's behaviors and its ad with torch's embedding_bag; the CTR MLP (ReLU
+    between layers) runs on [U, A, bag_0, bag_1, ...] and the loss is torch's
+    mean softmax cross-entropy.  T and id_tables are whole tables.  Returns the
+    loss, U, A, the bags, X, the gradient of X, the image-model and CTR
+    gradients, and the dense gradient of every ID table.
+    """
+    seg = np.asarray(batch["seg_off"], dtype=np.int64)
+    beh = np.asarray(batch["beh_ids"], dtype=np.int64)
+    ad = np.asarray(batch["ad_ids"], dtype=np.int64)
+    occ = np.concatenate([beh, ad])
+    n_beh = beh.size
+    B = seg.size - 1
+    X_img = _f64(T)[torch.as_tensor(occ)]
+    W = [_f64(w).requires_grad_() for w in Ws]
+    b = [_f64(x).requires_grad_() for x in bs]
+    h = X_img
+    for l in range(len(W)):
+        h = torch.nn.functional.linear(h, W[l], b[l])
+        if l < len(W) - 1:
+            h = torch.relu(h)
+    E_occ = h
+    A = E_occ[n_beh:]
+    outs = []
+    for i in range(B):
+        e = E_occ[seg[i]:seg[i + 1]]
+        if mode == "sum":
+            outs.append(e.sum(0))
+        elif mode == "att":
+            outs.append(torch.softmax(e @ A[i], dim=0) @ e)
+        else:
+            raise ValueError(mode)
+    U = torch.stack(outs)
+    tabs = [_f64(x).requires_grad_() for x in id_tables]
+    bags = []
+    for t, tab in enumerate(tabs):
+        bt = np.asarray(jb["beh_ids"][t], np.int64)
+        at = np.asarray(jb["ad_ids"][t], np.int64)
+        # one bag per sample: its behaviors' IDs then its ad's ID
+        flat, offs = [], []
+        for i in range(B):
+            offs.append(len(flat))
+            flat.extend(bt[seg[i]:seg[i + 1]].tolist())
+            flat.append(int(at[i]))
+        bags.append(torch.nn.functional.embedding_bag(torch.as_tensor(flat), tab, torch.as_tensor(offs),
+                                                      mode="sum"))
+    X = torch.cat([U, A] + bags, dim=1)
+    X.retain_grad()
+    cW = [_f64(w).requires_grad_() for w in ctr_Ws]
+    cb = [_f64(x).requires_grad_() for x in ctr_bs]
+    z = X
+    for l in range(len(cW)):
+        z = torch.nn.functional.linear(z, cW[l], cb[l])
+        if l < len(cW) - 1:
+            z = torch.relu(z)
+    loss = torch.nn.functional.cross_entropy(z, torch.as_tensor(np.asarray(jb["labels"], np.int64)))
+    loss.backward()
+    return {
+        "loss": float(loss.detach()), "U": U.detach().numpy(), "A": A.detach().numpy(),
+        "bags": [x.detach().numpy() for x in bags], "X": X.detach().numpy(), "dX": X.grad.numpy(),
+        "dW": [w.grad.numpy() for w in W], "db": [x.grad.numpy() for x in b],
+        "ctr_dW": [w.grad.numpy() for w in cW], "ctr_db": [x.grad.numpy() for x in cb],
+        "id_grad": [x.grad.numpy() for x in tabs],
+    }
