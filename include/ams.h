@@ -236,6 +236,91 @@ ams_status ams_pool_bwd(int32_t mode, int32_t B, int32_t D,
                         const void *saved, const float *dU, const float *dA,
                         float *dE, void *ws, size_t ws_bytes, void *stream);
 
+/* =================================================== joint step (worker) ====
+ * The worker side of a joint training step (Algorithm 1, WORKERITERATION):
+ * sparse ID features embedded from key-value tables (section 4.1) next to the
+ * image embeddings, the CTR model on top of them trained with cross-entropy
+ * (section 3.1), whose input gradients are the delta_e pushed to the image
+ * path (ams_pool_bwd / ams_embed_bwd), and a sparse Adagrad step on the ID
+ * rows the batch touched.  ID tables are float32 [n_rows x D] row-major;
+ * their IDs per table are laid out like the image IDs: one per behavior
+ * (sample by sample) then one per ad. */
+
+/* ---------------------------------------------------------- bag fwd ----
+ * bag[i][d] = sum over j in [seg_off[i], seg_off[i+1]) of table[ids[j]][d]
+ *             + table[ids[n_beh + i]][d]
+ * B samples, 1 <= D <= 32, ids[n_beh + B] (device), table [n_rows x D]
+ * (device), bag [B x D] out (device).  An ID outside [0, n_rows) reads as a
+ * zero row (ams_dedup over the same IDs reports it).  The sum over a
+ * sample's behaviors has a fixed association; the ad row is added last.
+ * Host errors: SIZE, DIMS (D), NULL. */
+ams_status ams_bag_fwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
+                       const int32_t *ids, const float *table, int64_t n_rows,
+                       float *bag, void *stream);
+
+/* ---------------------------------------------------------- bag bwd ----
+ * Merged gradient of the touched rows of one ID table.  With inv, occ_perm,
+ * uniq_off, n_uniq from ams_dedup over that table's IDs and dbag [B x D] the
+ * loss gradient of the bags: grad[u] = sum over the occurrences k of uniq[u]
+ * (ascending k) of dbag[sample of k], for u < n_u; grad is [n_uniq_cap x D]
+ * and fully written for u < n_u.  This is the SUM aggregator's backward with
+ * dbag as the upstream gradient of behaviors and ads (ams_pool_bwd, SUM):
+ * deterministic, no atomics, hot IDs split at fixed boundaries.
+ * ws: at least ams_bag_workspace(B, n_beh, D, n_uniq_cap) bytes. */
+size_t ams_bag_workspace(int32_t B, int64_t n_beh, int32_t D, int32_t n_uniq_cap);
+ams_status ams_bag_bwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
+                       const int32_t *inv, const int32_t *occ_perm, const int32_t *uniq_off,
+                       const int32_t *n_uniq, int32_t n_uniq_cap, const float *dbag,
+                       float *grad, void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------------------------- CTR -----
+ * The CTR MLP (the basic net's MLP, section 3.2): dims[0] inputs (the
+ * concatenated fields), ReLU between layers, dims[n_layers] = C classes,
+ * softmax and cross-entropy with the labels, averaged over the B samples.
+ * Supported: n_layers 2 or 3; dims[0] <= 128; hidden widths <= 256;
+ * 2 <= C <= 8; 1..8 input fields.  float32 throughout. */
+typedef struct {
+    int32_t n_layers;
+    int32_t dims[4];
+} ams_ctr;
+
+/* fields, field_dims, W, b, dW, db, dfields are HOST arrays of DEVICE
+ * pointers (field_dims: host widths):
+ *   fields[f]   [B x field_dims[f]]: sample i's input row is fields[0][i] ++
+ *               fields[1][i] ++ ...; the widths sum to dims[0];
+ *   labels      [B] int32 in [0, C) (device); a sample whose label is outside
+ *               that range adds nothing to the loss or to any gradient;
+ *   W[l], b[l]  [dims[l+1] x dims[l]] and [dims[l+1]] float32 (device);
+ *   loss        [1] out: mean cross-entropy over the B samples (device);
+ *   prob        [B x C] out, softmax probabilities (device, may be NULL);
+ *   dW[l], db[l] out: gradients of the mean loss, overwritten (device);
+ *   dfields     gradients of the mean loss w.r.t. each field, [B x
+ *               field_dims[f]] (device); dfields itself or any entry may be
+ *               NULL (not written).
+ * Every gradient is a sum over samples in a fixed order.
+ * ws: at least ams_ctr_workspace(net, B) bytes.  Host errors: NULL, DIMS,
+ * SIZE (B < 1), WORKSPACE. */
+size_t ams_ctr_workspace(const ams_ctr *net, int32_t B);
+ams_status ams_ctr_fwd_bwd(const ams_ctr *net, int32_t B, int32_t n_fields,
+                           const float *const *fields, const int32_t *field_dims,
+                           const int32_t *labels, const float *const *W,
+                           const float *const *b, float *loss, float *prob,
+                           float *const *dW, float *const *db, float *const *dfields,
+                           void *ws, size_t ws_bytes, void *stream);
+
+/* ---------------------------------------------------------- Adagrad ----
+ * Sparse Adagrad on the touched rows of an ID table, in place: for u < n_u
+ * (uniq, n_uniq from ams_dedup over the table's IDs) and d < D, with
+ * g = grad[u][d] and r = uniq[u]:
+ *   accum[r][d] += g * g;  table[r][d] -= lr * g / (sqrt(accum[r][d]) + eps).
+ * Rows are distinct, so the update has no races; untouched rows are left as
+ * they are.  A row index outside [0, n_rows) is skipped.  table and accum are
+ * [n_rows x D] float32 (device).  Host errors: SIZE, NULL. */
+ams_status ams_adagrad_rows(int32_t D, const int32_t *uniq, const int32_t *n_uniq,
+                            int32_t n_uniq_cap, const float *grad, float *table,
+                            int64_t n_rows, float *accum, float lr, float eps,
+                            void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -22,7 +22,9 @@ STATUS = {0: "AMS_OK", 1: "AMS_ERR_NULL", 2: "AMS_ERR_SIZE", 3: "AMS_ERR_DTYPE",
           5: "AMS_ERR_WORKSPACE", 6: "AMS_ERR_HIP", 7: "AMS_ERR_ID_RANGE", 8: "AMS_ERR_MODE"}
 EXPORTS = ["ams_status_str", "ams_build_info", "ams_dedup_workspace", "ams_dedup",
            "ams_embed_workspace", "ams_embed_fwd", "ams_embed_bwd", "ams_pool_fwd",
-           "ams_pool_workspace", "ams_pool_bwd", "ams_timing_enable", "ams_timing_read"]
+           "ams_pool_workspace", "ams_pool_bwd", "ams_timing_enable", "ams_timing_read",
+           "ams_bag_fwd", "ams_bag_workspace", "ams_bag_bwd", "ams_ctr_workspace", "ams_ctr_fwd_bwd",
+           "ams_adagrad_rows"]
 
 
 class AmsError(RuntimeError):
@@ -38,6 +40,10 @@ class ams_kernel_time(ctypes.Structure):
 class ams_mlp(ctypes.Structure):
     _fields_ = [("n_layers", ctypes.c_int32), ("dims", ctypes.c_int32 * 4),
                 ("dtype", ctypes.c_int32), ("final_relu", ctypes.c_int32)]
+
+
+class ams_ctr(ctypes.Structure):
+    _fields_ = [("n_layers", ctypes.c_int32), ("dims", ctypes.c_int32 * 4)]
 
 
 _lib = None
@@ -72,6 +78,21 @@ def load() -> ctypes.CDLL:
     lib.ams_pool_workspace.argtypes = [i32, i32, i64, i32, i32]
     lib.ams_pool_bwd.restype = ctypes.c_int
     lib.ams_pool_bwd.argtypes = [i32, i32, i32, P, i64, P, P, P, P, i32, P, P, P, P, P, P, P, P, sz, P]
+    C = ctypes.POINTER(ams_ctr)
+    PP = ctypes.POINTER(ctypes.c_void_p)
+    lib.ams_bag_fwd.restype = ctypes.c_int
+    lib.ams_bag_fwd.argtypes = [i32, i32, P, i64, P, P, i64, P, P]
+    lib.ams_bag_workspace.restype = sz
+    lib.ams_bag_workspace.argtypes = [i32, i64, i32, i32]
+    lib.ams_bag_bwd.restype = ctypes.c_int
+    lib.ams_bag_bwd.argtypes = [i32, i32, P, i64, P, P, P, P, i32, P, P, P, sz, P]
+    lib.ams_ctr_workspace.restype = sz
+    lib.ams_ctr_workspace.argtypes = [C, i32]
+    lib.ams_ctr_fwd_bwd.restype = ctypes.c_int
+    lib.ams_ctr_fwd_bwd.argtypes = [C, i32, i32, PP, ctypes.POINTER(i32), P, PP, PP, P, P, PP, PP, PP, P,
+                                    sz, P]
+    lib.ams_adagrad_rows.restype = ctypes.c_int
+    lib.ams_adagrad_rows.argtypes = [i32, P, P, i32, P, P, i64, P, ctypes.c_float, ctypes.c_float, P]
     lib.ams_timing_enable.restype = ctypes.c_int
     lib.ams_timing_enable.argtypes = [ctypes.c_int]
     lib.ams_timing_read.restype = ctypes.c_int
@@ -194,6 +215,56 @@ def ams_timing_read(cap: int = 64) -> dict:
     return {buf[k].name.decode(): (int(buf[k].launches), float(buf[k].total_ms)) for k in range(n.value)}
 
 
+def make_ctr(dims) -> ams_ctr:
+    c = ams_ctr()
+    c.n_layers = len(dims) - 1
+    for i, d in enumerate(dims):
+        c.dims[i] = int(d)
+    return c
+
+
+def _parray(ts):
+    """Host array of device pointers (None -> NULL)."""
+    return (ctypes.c_void_p * len(ts))(*[t.data_ptr() if t is not None else None for t in ts])
+
+
+def ams_bag_fwd(seg_off, n_beh: int, ids, table, bag, stream=None):
+    B, D = bag.shape
+    _check(load().ams_bag_fwd(B, D, _p(seg_off), int(n_beh), _p(ids), _p(table), table.shape[0], _p(bag),
+                              _stream(stream)), "ams_bag_fwd")
+
+
+def ams_bag_workspace(B: int, n_beh: int, D: int, n_uniq_cap: int) -> int:
+    return load().ams_bag_workspace(int(B), int(n_beh), int(D), int(n_uniq_cap))
+
+
+def ams_bag_bwd(seg_off, n_beh: int, inv, occ_perm, uniq_off, n_uniq, n_uniq_cap: int, dbag, grad, ws,
+                stream=None):
+    B, D = dbag.shape
+    _check(load().ams_bag_bwd(B, D, _p(seg_off), int(n_beh), _p(inv), _p(occ_perm), _p(uniq_off), _p(n_uniq),
+                              int(n_uniq_cap), _p(dbag), _p(grad), _p(ws), ws.numel() * ws.element_size(),
+                              _stream(stream)), "ams_bag_bwd")
+
+
+def ams_ctr_workspace(net: ams_ctr, B: int) -> int:
+    return load().ams_ctr_workspace(ctypes.byref(net), int(B))
+
+
+def ams_ctr_fwd_bwd(net: ams_ctr, fields, labels, W, b, loss, prob, dW, db, dfields, ws, stream=None):
+    B = fields[0].shape[0]
+    widths = (ctypes.c_int32 * len(fields))(*[int(f.shape[1]) for f in fields])
+    _check(load().ams_ctr_fwd_bwd(ctypes.byref(net), B, len(fields), _parray(fields), widths, _p(labels),
+                                  _parray(W), _parray(b), _p(loss), _p(prob), _parray(dW), _parray(db),
+                                  _parray(dfields) if dfields is not None else None, _p(ws),
+                                  ws.numel() * ws.element_size(), _stream(stream)), "ams_ctr_fwd_bwd")
+
+
+def ams_adagrad_rows(uniq, n_uniq, n_uniq_cap: int, grad, table, accum, lr: float, eps: float, stream=None):
+    _check(load().ams_adagrad_rows(table.shape[1], _p(uniq), _p(n_uniq), int(n_uniq_cap), _p(grad), _p(table),
+                                   table.shape[0], _p(accum), float(lr), float(eps), _stream(stream)),
+           "ams_adagrad_rows")
+
+
 class Step:
     """Buffers for one training step of the embedding hot path, and the five
     calls in order on one stream: dedup -> embed fwd -> pool fwd -> pool bwd
@@ -282,3 +353,93 @@ class Step:
         self.pool_fwd(seg_off, n_beh, stream)
         self.pool_bwd(seg_off, n_beh, dU, dA, stream)
         self.embed_bwd(T, W, stream)
+
+
+class JointStep:
+    """Buffers and calls of one joint training step (Algorithm 1: worker
+    iteration with the server's embed and update), on one stream:
+
+      image dedup, ID dedups          ams_dedup x (1 + tables)
+      image embed + pool forward      ams_embed_fwd, ams_pool_fwd
+      ID bags                         ams_bag_fwd x tables
+      CTR forward + backward          ams_ctr_fwd_bwd (fields: U, A, bags)
+      image pool + embed backward     ams_pool_bwd(dU, dA), ams_embed_bwd
+      ID rows: merged grad, Adagrad   ams_bag_bwd, ams_adagrad_rows x tables
+
+    The ID tables and their Adagrad accumulators are caller tensors updated in
+    place; everything else is held here.
+    """
+
+    def __init__(self, dims, dtype: str, mode: str, B: int, n_beh_max: int, id_rows, id_dim: int, ctr_dims,
+                 device="cuda"):
+        self.img = Step(dims, dtype, mode, B, n_beh_max, device=device)
+        self.B, self.n_beh = int(B), int(n_beh_max)
+        self.n_occ = self.B + self.n_beh
+        self.id_rows = [int(x) for x in id_rows]
+        self.id_dim = int(id_dim)
+        self.ctr = make_ctr(ctr_dims)
+        self.ctr_dims = tuple(ctr_dims)
+        dev = torch.device(device)
+        i32, f32 = torch.int32, torch.float32
+        n = max(self.n_occ, 1)
+        T = len(self.id_rows)
+        self.t_uniq = [torch.empty(n, dtype=i32, device=dev) for _ in range(T)]
+        self.t_inv = [torch.empty(n, dtype=i32, device=dev) for _ in range(T)]
+        self.t_perm = [torch.empty(n, dtype=i32, device=dev) for _ in range(T)]
+        self.t_off = [torch.empty(n + 1, dtype=i32, device=dev) for _ in range(T)]
+        self.t_nu = [torch.zeros(1, dtype=i32, device=dev) for _ in range(T)]
+        self.t_status = [torch.zeros(1, dtype=i32, device=dev) for _ in range(T)]
+        Bm = max(self.B, 1)
+        self.bags = [torch.empty((Bm, self.id_dim), dtype=f32, device=dev) for _ in range(T)]
+        self.dbags = [torch.empty((Bm, self.id_dim), dtype=f32, device=dev) for _ in range(T)]
+        self.row_grad = [torch.empty((n, self.id_dim), dtype=f32, device=dev) for _ in range(T)]
+        D = dims[-1]
+        self.dU = torch.empty((Bm, D), dtype=f32, device=dev)
+        self.dA = torch.empty((Bm, D), dtype=f32, device=dev)
+        self.loss = torch.zeros(1, dtype=f32, device=dev)
+        self.prob = torch.empty((Bm, self.ctr_dims[-1]), dtype=f32, device=dev)
+        self.ctr_dW = [torch.empty((o, i), dtype=f32, device=dev) for i, o in zip(ctr_dims[:-1], ctr_dims[1:])]
+        self.ctr_db = [torch.empty((o,), dtype=f32, device=dev) for o in ctr_dims[1:]]
+        self.ws = None
+
+    def alloc_workspace(self, n_ids: int):
+        need = max(ams_dedup_workspace(self.n_occ, max([n_ids] + self.id_rows)),
+                   ams_embed_workspace(self.img.mlp, self.img.cap),
+                   ams_pool_workspace(self.img.mode, self.B, self.n_beh, self.img.dims[-1], self.img.cap),
+                   ams_bag_workspace(self.B, self.n_beh, self.id_dim, self.n_occ),
+                   ams_ctr_workspace(self.ctr, max(self.B, 1)), 256)
+        self.img.ws = torch.empty(need, dtype=torch.uint8, device=self.loss.device)
+        self.img.n_ids = int(n_ids)
+        self.ws = self.img.ws
+
+    def run(self, ids, n_ids, T, W, b, seg_off, id_ids, id_tables, accum, labels, ctr_W, ctr_b, lr: float,
+            eps: float, stream=None):
+        """The whole joint step, enqueued with no host synchronisation.
+        id_ids[t]: behavior then ad IDs of table t; id_tables[t] and accum[t]
+        are updated in place on the touched rows."""
+        n_beh = ids.numel() - (seg_off.numel() - 1)
+        if n_beh > self.n_beh or seg_off.numel() - 1 > self.B:
+            raise ValueError("batch larger than the buffers of this JointStep")
+        if self.ws is None or self.img.n_ids != int(n_ids):
+            self.alloc_workspace(n_ids)
+        st = self.img
+        st.dedup(ids, n_ids, stream)
+        for t in range(len(self.id_rows)):
+            ams_dedup(id_ids[t], self.id_rows[t], self.t_uniq[t], self.t_inv[t], self.t_perm[t], self.t_off[t],
+                      self.t_nu[t], self.t_status[t], self.ws, stream)
+        st.embed_fwd(T, W, b, stream)
+        st.pool_fwd(seg_off, n_beh, stream)
+        for t in range(len(self.id_rows)):
+            ams_bag_fwd(seg_off, n_beh, id_ids[t], id_tables[t], self.bags[t], stream)
+        B = seg_off.numel() - 1
+        fields = [st.U[:B], st.A[:B]] + [x[:B] for x in self.bags]
+        dfields = [self.dU[:B], self.dA[:B]] + [x[:B] for x in self.dbags]
+        ams_ctr_fwd_bwd(self.ctr, fields, labels, ctr_W, ctr_b, self.loss, self.prob, self.ctr_dW, self.ctr_db,
+                        dfields, self.ws, stream)
+        st.pool_bwd(seg_off, n_beh, self.dU, self.dA, stream)
+        st.embed_bwd(T, W, stream)
+        for t in range(len(self.id_rows)):
+            ams_bag_bwd(seg_off, n_beh, self.t_inv[t], self.t_perm[t], self.t_off[t], self.t_nu[t], self.n_occ,
+                        self.dbags[t][:B], self.row_grad[t], self.ws, stream)
+            ams_adagrad_rows(self.t_uniq[t], self.t_nu[t], self.n_occ, self.row_grad[t], id_tables[t], accum[t],
+                             lr, eps, stream)

@@ -1,0 +1,439 @@
+// ctr.hip -- the worker side of one joint training step (Algorithm 1,
+// WORKERITERATION) next to the image path:
+//   ams_bag_fwd      per sample and ID table, the sum of the table rows of its
+//                    behaviors' IDs and of its ad's ID (sparse ID features
+//                    embedded from key-value tables, section 4.1);
+//   ams_bag_bwd      the gradient of every touched row: the bag gradient of
+//                    each occurrence's sample, summed per unique ID in
+//                    ascending occurrence order (the segmented reduction of
+//                    the SUM aggregator's backward);
+//   ams_ctr_fwd_bwd  the CTR MLP on the concatenated input fields, softmax over
+//                    the classes and mean cross-entropy with the click labels
+//                    (section 3.1), and its backward: the worker's weight
+//                    gradients and the gradient of every input field (among
+//                    them delta_e of the image path);
+//   ams_adagrad_rows sparse Adagrad on the touched rows of an ID table.
+// No float atomics: every sum runs in a fixed order.
+#include "ams_device.h"
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kWaves = kThreads / AMS_WAVE;
+constexpr int kCtrBS = 16;                  // samples per block of the CTR kernel
+constexpr int kCtrMaxIn = 128, kCtrMaxHidden = 256, kCtrMaxC = 8;
+constexpr int kCtrMaxLayers = 3, kCtrMaxFields = 8;
+
+// ------------------------------------------------------------ bag forward
+
+// One wave per sample: lane l adds the rows of behaviors l, l + 64, ...;
+// the lanes' partial rows are summed by a fixed butterfly, then the ad row.
+// An ID outside [0, n_rows) reads as a zero row (dedup reports it).
+template <int DM>
+__global__ __launch_bounds__(kThreads) void bag_fwd_k(int B, int D, const int32_t *__restrict__ seg_off,
+                                                      int64_t n_beh, const int32_t *__restrict__ ids,
+                                                      const float *__restrict__ table, int64_t n_rows,
+                                                      float *__restrict__ bag)
+{
+    const int lane = ams_lane();
+    const int i = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
+    if (i >= B) return;
+    const int j0 = seg_off[i], j1 = seg_off[i + 1];
+    float acc[DM];
+#pragma unroll
+    for (int d = 0; d < DM; ++d) acc[d] = 0.f;
+    const bool vec4 = (D & 3) == 0;
+    for (int j = j0 + lane; j < j1; j += AMS_WAVE) {
+        const int id = ids[j];
+        if (id < 0 || (int64_t)id >= n_rows) continue;
+        const float *r = table + (size_t)id * D;
+        if (vec4) {
+#pragma unroll
+            for (int d4 = 0; d4 < DM / 4; ++d4)
+                if (4 * d4 < D) {
+                    const float4 v = *(const float4 *)(r + 4 * d4);
+                    acc[4 * d4] += v.x;
+                    acc[4 * d4 + 1] += v.y;
+                    acc[4 * d4 + 2] += v.z;
+                    acc[4 * d4 + 3] += v.w;
+                }
+        } else {
+#pragma unroll
+            for (int d = 0; d < DM; ++d)
+                if (d < D) acc[d] += r[d];
+        }
+    }
+    float mine = 0.f;
+#pragma unroll
+    for (int d = 0; d < DM; ++d) {
+        const float s = ams_wave_sum(acc[d]);
+        if (lane == d) mine = s;
+    }
+    if (lane < D) {
+        const int id = ids[n_beh + i];
+        const float a = (id >= 0 && (int64_t)id < n_rows) ? table[(size_t)id * D + lane] : 0.f;
+        bag[(size_t)i * D + lane] = mine + a;
+    }
+}
+
+// ---------------------------------------------------------------- CTR MLP
+
+struct CtrArgs {
+    int L;                                   // layers (2 or 3)
+    int dims[kCtrMaxLayers + 1];
+    int n_fields;
+    int fdim[kCtrMaxFields];
+    const float *field[kCtrMaxFields];
+    float *dfield[kCtrMaxFields];
+    const float *W[kCtrMaxLayers];
+    const float *b[kCtrMaxLayers];
+};
+
+__host__ __device__ inline int ctr_part_size(const CtrArgs &a)
+{
+    int n = 1;                               // + the block's loss sum
+    for (int l = 0; l < a.L; ++l) n += a.dims[l + 1] * a.dims[l] + a.dims[l + 1];
+    return n;
+}
+
+// out[s][o] = (bias + sum_k in[s][k] W[o][k]), ReLU'd unless last; thread
+// (o = t % O, group g = t / O) takes samples g, g + G, ... (G = 256 / O).
+__device__ __forceinline__ void ctr_dense_fwd(const float *in, int K, float *out, int O, const float *__restrict__ W,
+                                              const float *__restrict__ bias, bool relu, int t)
+{
+    const int G = max(1, min(kCtrBS, kThreads / O));
+    const int o = t % O, g = t / O;
+    if (g >= G) return;
+    float acc[kCtrBS];
+    const float bo = bias[o];
+#pragma unroll
+    for (int s = 0; s < kCtrBS; ++s) acc[s] = bo;
+    const float *wr = W + (size_t)o * K;
+    for (int k = 0; k < K; ++k) {
+        const float w = wr[k];
+#pragma unroll
+        for (int s = 0; s < kCtrBS; ++s)
+            if (s % G == g) acc[s] = fmaf(in[s * K + k], w, acc[s]);
+    }
+#pragma unroll
+    for (int s = 0; s < kCtrBS; ++s)
+        if (s % G == g) out[s * O + o] = relu ? fmaxf(acc[s], 0.f) : acc[s];
+}
+
+// gin[s][k] = sum_o gout[s][o] W[o][k] (masked by [in > 0] when `mask`);
+// thread (k = t % K, group g = t / K) takes samples g, g + G, ...
+__device__ __forceinline__ void ctr_dense_bwd_data(const float *gout, int O, float *gin, const float *in, int K,
+                                                   const float *__restrict__ W, bool mask, int t)
+{
+    const int G = max(1, min(kCtrBS, kThreads / K));
+    const int k = t % K, g = t / K;
+    if (g >= G) return;
+    float acc[kCtrBS];
+#pragma unroll
+    for (int s = 0; s < kCtrBS; ++s) acc[s] = 0.f;
+    for (int o = 0; o < O; ++o) {
+        const float w = W[(size_t)o * K + k];
+#pragma unroll
+        for (int s = 0; s < kCtrBS; ++s)
+            if (s % G == g) acc[s] = fmaf(gout[s * O + o], w, acc[s]);
+    }
+#pragma unroll
+    for (int s = 0; s < kCtrBS; ++s)
+        if (s % G == g) gin[s * K + k] = (!mask || in[s * K + k] > 0.f) ? acc[s] : 0.f;
+}
+
+// One block = kCtrBS samples: forward through every layer in LDS, softmax
+// and cross-entropy, then the backward; the block's weight-gradient and loss
+// sums (over its samples, ascending) go to its partial row.
+__global__ __launch_bounds__(kThreads) void ctr_fb_k(CtrArgs a, int B, const int32_t *__restrict__ labels,
+                                                     float *__restrict__ prob, float *__restrict__ part, int PS)
+{
+    constexpr int kAct = kCtrBS * (kCtrMaxIn + 2 * kCtrMaxHidden + kCtrMaxC);
+    __shared__ float act[kAct];              // act[l]: [kCtrBS][dims[l]] per layer
+    __shared__ float grd[kAct];              // the loss gradient of each act[l]
+    __shared__ float lossv[kCtrBS];
+    const int t = threadIdx.x;
+    const int b0 = blockIdx.x * kCtrBS;
+    const int L = a.L;
+    int off[kCtrMaxLayers + 1];
+    off[0] = 0;
+    for (int l = 0; l < L; ++l) off[l + 1] = off[l] + kCtrBS * a.dims[l];
+    const int K0 = a.dims[0], C = a.dims[L];
+    // input fields, concatenated; rows past B read 0
+    {
+        int c0 = 0;
+        for (int f = 0; f < a.n_fields; ++f) {
+            const int w = a.fdim[f];
+            for (int e = t; e < kCtrBS * w; e += kThreads) {
+                const int s = e / w, k = e % w;
+                act[s * K0 + c0 + k] = (b0 + s < B) ? a.field[f][(size_t)(b0 + s) * w + k] : 0.f;
+            }
+            c0 += w;
+        }
+    }
+    __syncthreads();
+    for (int l = 0; l < L; ++l) {
+        ctr_dense_fwd(act + off[l], a.dims[l], act + off[l + 1], a.dims[l + 1], a.W[l], a.b[l], l < L - 1, t);
+        __syncthreads();
+    }
+    // softmax, cross-entropy, dlogits = (p - onehot(y)) / B
+    if (t < kCtrBS) {
+        const int s = t, n = b0 + s;
+        const float *z = act + off[L] + s * C;
+        float *gz = grd + off[L] + s * C;
+        float ls = 0.f;
+        const int y = n < B ? labels[n] : -1;
+        if (n < B && y >= 0 && y < C) {
+            float m = z[0];
+            for (int c = 1; c < C; ++c) m = fmaxf(m, z[c]);
+            float se = 0.f;
+            for (int c = 0; c < C; ++c) se += expf(z[c] - m);
+            const float lse = m + logf(se);
+            for (int c = 0; c < C; ++c) {
+                const float p = expf(z[c] - lse);
+                if (prob) prob[(size_t)n * C + c] = p;
+                gz[c] = (p - (c == y ? 1.f : 0.f)) / (float)B;
+            }
+            ls = lse - z[y];
+        } else {
+            for (int c = 0; c < C; ++c) gz[c] = 0.f;
+            if (n < B && prob)
+                for (int c = 0; c < C; ++c) prob[(size_t)n * C + c] = 0.f;
+        }
+        lossv[s] = ls;
+    }
+    __syncthreads();
+    float *p = part + (size_t)blockIdx.x * PS;
+    int woff = 0;
+    int wo[kCtrMaxLayers];
+    for (int l = 0; l < L; ++l) {
+        wo[l] = woff;
+        woff += a.dims[l + 1] * a.dims[l] + a.dims[l + 1];
+    }
+    for (int l = L - 1; l >= 0; --l) {
+        const int K = a.dims[l], O = a.dims[l + 1];
+        const float *gout = grd + off[l + 1], *in = act + off[l];
+        // weight and bias gradients of layer l over this block's samples
+        for (int e = t; e < O * K; e += kThreads) {
+            const int o = e / K, k = e % K;
+            float acc = 0.f;
+#pragma unroll
+            for (int s = 0; s < kCtrBS; ++s) acc = fmaf(gout[s * O + o], in[s * K + k], acc);
+            p[wo[l] + e] = acc;
+        }
+        for (int o = t; o < O; o += kThreads) {
+            float acc = 0.f;
+#pragma unroll
+            for (int s = 0; s < kCtrBS; ++s) acc += gout[s * O + o];
+            p[wo[l] + O * K + o] = acc;
+        }
+        if (l > 0) {
+            ctr_dense_bwd_data(gout, O, grd + off[l], in, K, a.W[l], true, t);
+        } else {
+            ctr_dense_bwd_data(gout, O, grd, in, K, a.W[0], false, t);
+        }
+        __syncthreads();
+    }
+    // input-field gradients
+    {
+        int c0 = 0;
+        for (int f = 0; f < a.n_fields; ++f) {
+            const int w = a.fdim[f];
+            if (a.dfield[f])
+                for (int e = t; e < kCtrBS * w; e += kThreads) {
+                    const int s = e / w, k = e % w;
+                    if (b0 + s < B) a.dfield[f][(size_t)(b0 + s) * w + k] = grd[s * K0 + c0 + k];
+                }
+            c0 += w;
+        }
+    }
+    if (t == 0) {
+        float ls = 0.f;
+        for (int s = 0; s < kCtrBS; ++s) ls += lossv[s];
+        p[PS - 1] = ls;
+    }
+}
+
+struct CtrOut {
+    int L;
+    int dims[kCtrMaxLayers + 1];
+    float *dW[kCtrMaxLayers];
+    float *db[kCtrMaxLayers];
+    float *loss;
+    int B;
+};
+
+// Fixed-order sum of the blocks' partial rows (eight running chains over
+// g = 8 i + r, added r = 0..7), scattered into dW, db and the mean loss.
+__global__ __launch_bounds__(kThreads) void ctr_reduce_k(const float *__restrict__ part, int G, int PS, CtrOut o)
+{
+    const int e = blockIdx.x * kThreads + threadIdx.x;
+    if (e >= PS) return;
+    float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    int g = 0;
+    for (; g + 8 <= G; g += 8)
+#pragma unroll
+        for (int r = 0; r < 8; ++r) s[r] += part[(size_t)(g + r) * PS + e];
+    for (int r = 0; g + r < G; ++r) s[r] += part[(size_t)(g + r) * PS + e];
+    float tot = 0.f;
+#pragma unroll
+    for (int r = 0; r < 8; ++r) tot += s[r];
+    if (e == PS - 1) {
+        *o.loss = tot / (float)o.B;
+        return;
+    }
+    int x = e;
+    for (int l = 0; l < o.L; ++l) {
+        const int nw = o.dims[l + 1] * o.dims[l];
+        if (x < nw) {
+            o.dW[l][x] = tot;
+            return;
+        }
+        x -= nw;
+        if (x < o.dims[l + 1]) {
+            o.db[l][x] = tot;
+            return;
+        }
+        x -= o.dims[l + 1];
+    }
+}
+
+// ---------------------------------------------------------------- Adagrad
+
+__global__ __launch_bounds__(kThreads) void adagrad_k(int D, const int32_t *__restrict__ uniq,
+                                                      const int32_t *__restrict__ n_uniq_p, int cap,
+                                                      const float *__restrict__ grad, float *__restrict__ table,
+                                                      int64_t n_rows, float *__restrict__ accum, float lr, float eps)
+{
+    const int n_u = min(*n_uniq_p, cap);
+    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (e >= (int64_t)n_u * D) return;
+    const int u = (int)(e / D), d = (int)(e % D);
+    const int r = uniq[u];
+    if (r < 0 || (int64_t)r >= n_rows) return;
+    const float g = grad[e];
+    const size_t x = (size_t)r * D + d;
+    const float acc = accum[x] + g * g;
+    accum[x] = acc;
+    table[x] -= lr * g / (sqrtf(acc) + eps);
+}
+
+size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+bool ctr_ok(const ams_ctr *net)
+{
+    if (!net || net->n_layers < 2 || net->n_layers > kCtrMaxLayers) return false;
+    if (net->dims[0] < 1 || net->dims[0] > kCtrMaxIn) return false;
+    for (int l = 1; l < net->n_layers; ++l)
+        if (net->dims[l] < 1 || net->dims[l] > kCtrMaxHidden) return false;
+    const int C = net->dims[net->n_layers];
+    return C >= 2 && C <= kCtrMaxC;
+}
+
+}  // namespace
+
+extern "C" ams_status ams_bag_fwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
+                                  const int32_t *ids, const float *table, int64_t n_rows, float *bag, void *stream)
+{
+    if (B < 0 || n_beh < 0 || n_beh > INT32_MAX || n_rows < 0) return AMS_ERR_SIZE;
+    if (D < 1 || D > 32) return AMS_ERR_DIMS;
+    if (B == 0) return AMS_OK;
+    if (!seg_off || !ids || !table || !bag) return AMS_ERR_NULL;
+    hipStream_t st = (hipStream_t)stream;
+    const int grid = (B + kWaves - 1) / kWaves;
+    if (D <= 16)
+        AMS_LAUNCH("bag_fwd", st, bag_fwd_k<16><<<grid, kThreads, 0, st>>>(B, D, seg_off, n_beh, ids, table, n_rows, bag));
+    else
+        AMS_LAUNCH("bag_fwd", st, bag_fwd_k<32><<<grid, kThreads, 0, st>>>(B, D, seg_off, n_beh, ids, table, n_rows, bag));
+    return ams_launch_status();
+}
+
+extern "C" size_t ams_bag_workspace(int32_t B, int64_t n_beh, int32_t D, int32_t n_uniq_cap)
+{
+    return ams_pool_workspace(AMS_POOL_SUM, B, n_beh, D, n_uniq_cap);
+}
+
+extern "C" ams_status ams_bag_bwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh, const int32_t *inv,
+                                  const int32_t *occ_perm, const int32_t *uniq_off, const int32_t *n_uniq,
+                                  int32_t n_uniq_cap, const float *dbag, float *grad, void *ws, size_t ws_bytes,
+                                  void *stream)
+{
+    if (B > 0 && !dbag) return AMS_ERR_NULL;
+    // the SUM aggregator's backward with the bag gradient as the upstream
+    // gradient of behaviors and ads alike (it reads neither E, U nor A)
+    return ams_pool_bwd(AMS_POOL_SUM, B, D, seg_off, n_beh, inv, occ_perm, uniq_off, n_uniq, n_uniq_cap,
+                        grad, dbag, dbag, nullptr, dbag, dbag, grad, ws, ws_bytes, stream);
+}
+
+extern "C" size_t ams_ctr_workspace(const ams_ctr *net, int32_t B)
+{
+    if (!ctr_ok(net) || B < 0) return 0;
+    CtrArgs a{};
+    a.L = net->n_layers;
+    for (int l = 0; l <= a.L; ++l) a.dims[l] = net->dims[l];
+    const int G = (B + kCtrBS - 1) / kCtrBS;
+    return al256((size_t)(G > 0 ? G : 1) * ctr_part_size(a) * 4);
+}
+
+extern "C" ams_status ams_ctr_fwd_bwd(const ams_ctr *net, int32_t B, int32_t n_fields, const float *const *fields,
+                                      const int32_t *field_dims, const int32_t *labels, const float *const *W,
+                                      const float *const *b, float *loss, float *prob, float *const *dW,
+                                      float *const *db, float *const *dfields, void *ws, size_t ws_bytes,
+                                      void *stream)
+{
+    if (!net || !fields || !field_dims || !W || !b || !dW || !db) return AMS_ERR_NULL;
+    if (!ctr_ok(net)) return AMS_ERR_DIMS;
+    if (B < 1) return AMS_ERR_SIZE;
+    if (n_fields < 1 || n_fields > kCtrMaxFields) return AMS_ERR_DIMS;
+    CtrArgs a{};
+    a.L = net->n_layers;
+    for (int l = 0; l <= a.L; ++l) a.dims[l] = net->dims[l];
+    a.n_fields = n_fields;
+    int width = 0;
+    for (int f = 0; f < n_fields; ++f) {
+        if (field_dims[f] < 1) return AMS_ERR_DIMS;
+        if (!fields[f]) return AMS_ERR_NULL;
+        a.fdim[f] = field_dims[f];
+        a.field[f] = fields[f];
+        a.dfield[f] = dfields ? dfields[f] : nullptr;
+        width += field_dims[f];
+    }
+    if (width != a.dims[0]) return AMS_ERR_DIMS;
+    for (int l = 0; l < a.L; ++l) {
+        if (!W[l] || !b[l] || !dW[l] || !db[l]) return AMS_ERR_NULL;
+        a.W[l] = W[l];
+        a.b[l] = b[l];
+    }
+    if (!labels || !loss) return AMS_ERR_NULL;
+    const int G = (B + kCtrBS - 1) / kCtrBS;
+    const int PS = ctr_part_size(a);
+    if (!ws || ws_bytes < (size_t)G * PS * 4) return AMS_ERR_WORKSPACE;
+    hipStream_t st = (hipStream_t)stream;
+    float *part = (float *)ws;
+    AMS_LAUNCH("ctr_fwd_bwd", st, ctr_fb_k<<<G, kThreads, 0, st>>>(a, B, labels, prob, part, PS));
+    CtrOut o{};
+    o.L = a.L;
+    for (int l = 0; l <= a.L; ++l) o.dims[l] = a.dims[l];
+    for (int l = 0; l < a.L; ++l) {
+        o.dW[l] = dW[l];
+        o.db[l] = db[l];
+    }
+    o.loss = loss;
+    o.B = B;
+    AMS_LAUNCH("ctr_reduce", st, ctr_reduce_k<<<(PS + kThreads - 1) / kThreads, kThreads, 0, st>>>(part, G, PS, o));
+    return ams_launch_status();
+}
+
+extern "C" ams_status ams_adagrad_rows(int32_t D, const int32_t *uniq, const int32_t *n_uniq, int32_t n_uniq_cap,
+                                       const float *grad, float *table, int64_t n_rows, float *accum, float lr,
+                                       float eps, void *stream)
+{
+    if (D < 1 || n_uniq_cap < 0 || n_rows < 0) return AMS_ERR_SIZE;
+    if (n_uniq_cap == 0) return AMS_OK;
+    if (!uniq || !n_uniq || !grad || !table || !accum) return AMS_ERR_NULL;
+    hipStream_t st = (hipStream_t)stream;
+    const int64_t n = (int64_t)n_uniq_cap * D;
+    AMS_LAUNCH("adagrad_rows", st, adagrad_k<<<(unsigned)((n + kThreads - 1) / kThreads), kThreads, 0, st>>>(
+                                       D, uniq, n_uniq, n_uniq_cap, grad, table, n_rows, accum, lr, eps));
+    return ams_launch_status();
+}

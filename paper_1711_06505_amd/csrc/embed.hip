@@ -264,10 +264,10 @@ __global__ __launch_bounds__(kThreads) void l1_fwd_f32(const float *__restrict__
 // pieces in K order.  Waves are 4 (M) x 2 (N), each BM/4 rows x 128 columns;
 // rows stream HBM->LDS by DMA with the row swizzle of l1_fwd_f32, through a
 // ring of R slots of BM + 256 rows (BM = 128, R = 3: 48 KB per slot, two
-// stages in flight while one is consumed).  Sk<> also admits BM = 256 with
-// R = 2 (64 KB slots): half the W1 bytes per gathered byte, but measured
-// slower on bf16 at every workload here (one stage in flight, and too few
-// tiles to fill the chip at ~13k unique images).
+// stages in flight while one is consumed).  A 256-row tile with a 2-slot ring
+// (64 KB slots) halves the W1 bytes per gathered byte but measured slower in
+// bf16 at every workload here: one stage in flight, and too few tiles to fill
+// the chip at ~13k unique images.
 // With the whole hidden width in one tile a feature row is read from HBM once.
 //
 // fp32: within a stage lane l supplies k = 16*(l/32) + 4*g + e to element e
@@ -323,54 +323,10 @@ __device__ __forceinline__ void sk_issue(float *slot, const char *const *src, in
     for (int q = 0; q < Sk<TT>::PW; ++q) dma16(src[q] + k0b, slot + (wave * Sk<TT>::PW + q) * 256);
 }
 
-// Two 32-row blocks per wave (a 256-row tile, bf16): the operands of k-group
-// g+1 are read while the MFMAs of group g run, two groups of fragments live at
-// a time.
-__device__ __forceinline__ void sk_compute_bf16(const float *slot, v16f (*acc)[kSkNB], int lane, int wave)
-{
-    using K = Sk<uint16_t>;
-    const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
-    // byte offset of this lane's 16-byte chunk of k-group 0 in each operand
-    // row; group g's chunk is (4 h + g) ^ swz = (4 h ^ swz) ^ g, i.e. the
-    // offset XOR (g << 4) (rows are 128 bytes)
-    const char *sl = (const char *)slot;
-    int aoff[K::MB], boff[kSkNB];
-#pragma unroll
-    for (int mb = 0; mb < K::MB; ++mb) {
-        const int r = wm * 32 * K::MB + mb * 32 + r32;
-        aoff[mb] = r * 128 + (((4 * h) ^ ring_swz(r)) << 4);
-    }
-#pragma unroll
-    for (int nb = 0; nb < kSkNB; ++nb) {
-        const int r = K::BM + wn * (kSkBN / 2) + nb * 32 + r32;
-        boff[nb] = r * 128 + (((4 * h) ^ ring_swz(r)) << 4);
-    }
-    uint4 a[2][K::MB], b[2][kSkNB];
-    auto rd = [&](int g, int buf) {
-#pragma unroll
-        for (int mb = 0; mb < K::MB; ++mb) a[buf][mb] = *(const uint4 *)(sl + (aoff[mb] ^ (g << 4)));
-#pragma unroll
-        for (int nb = 0; nb < kSkNB; ++nb) b[buf][nb] = *(const uint4 *)(sl + (boff[nb] ^ (g << 4)));
-    };
-    rd(0, 0);
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-        if (g < 3) rd(g + 1, (g + 1) & 1);
-#pragma unroll
-        for (int mb = 0; mb < K::MB; ++mb)
-#pragma unroll
-            for (int nb = 0; nb < kSkNB; ++nb) acc[mb][nb] = mfma_bf16(a[g & 1][mb], b[g & 1][nb], acc[mb][nb]);
-    }
-}
-
 template <typename TT>
 __device__ __forceinline__ void sk_compute(const float *slot, v16f (*acc)[kSkNB], int lane, int wave)
 {
     using K = Sk<TT>;
-    if constexpr (K::MB == 2) {
-        sk_compute_bf16(slot, acc, lane, wave);
-        return;
-    }
     const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
     uint4 a[4][K::MB], b[4][kSkNB];
 #pragma unroll
@@ -708,8 +664,6 @@ __device__ __forceinline__ float4 ld4_any(const void *p, int bf16, size_t i)
 // widths: H = dims[1] (64..256, a multiple of 64), Mo = width of the second
 // layer's output (dims[2] for 3 layers, D for 2), padded to 64 with zeros.
 constexpr int kTailRows = 32;
-constexpr int kTailLD = kMaxH1 + 4;       // row stride of [row][k] operand tiles
-constexpr int kTailLDo = kMaxH2 + 4;      // row stride of [row][o] tiles
 
 // Forward: Z2 = H1 W2^T + b2 for a chunk of 32 rows.  Wave w computes output
 // columns 32 (w & 1) .. +32 over the K half w >> 1; the two halves are added

@@ -143,3 +143,48 @@ def test_timing_switch_and_empty_read(lib):
     assert lib.ams_timing_read(None, 0, ctypes.byref(n)) == OK and n.value == 0
     assert lib.ams_timing_read(None, 0, None) == NULL
     assert lib.ams_timing_read(None, 4, ctypes.byref(n)) == NULL
+
+
+def test_joint_host_errors(lib):
+    # bag forward
+    assert lib.ams_bag_fwd(-1, 12, FAKE, 40, FAKE, FAKE, 100, FAKE, None) == SIZE
+    assert lib.ams_bag_fwd(4, 0, FAKE, 40, FAKE, FAKE, 100, FAKE, None) == DIMS
+    assert lib.ams_bag_fwd(4, 33, FAKE, 40, FAKE, FAKE, 100, FAKE, None) == DIMS
+    assert lib.ams_bag_fwd(4, 12, FAKE, 40, None, FAKE, 100, FAKE, None) == NULL
+    assert lib.ams_bag_fwd(0, 12, None, 0, None, None, 100, None, None) == OK
+    # bag backward = the SUM aggregator's backward: its checks apply
+    assert lib.ams_bag_workspace(4, 40, 12, 44) == lib.ams_pool_workspace(0, 4, 40, 12, 44) > 0
+    bb = [4, 12, FAKE, 40, FAKE, FAKE, FAKE, FAKE, 44, FAKE, FAKE, FAKE, 16, None]
+    assert lib.ams_bag_bwd(*bb) == WS
+    a = list(bb); a[9] = None                 # dbag
+    assert lib.ams_bag_bwd(*a) == NULL
+    a = list(bb); a[5] = None                 # occ_perm
+    assert lib.ams_bag_bwd(*a) == NULL
+    # CTR
+    net = ams.make_ctr((60, 200, 80, 2))
+    assert lib.ams_ctr_workspace(ctypes.byref(net), 4096) >= 256 * (60 * 200 + 200 * 80 + 80 * 2) * 4
+    for dims in [(129, 200, 80, 2), (60, 257, 80, 2), (60, 200, 80, 1), (60, 200, 80, 9)]:
+        assert lib.ams_ctr_workspace(ctypes.byref(ams.make_ctr(dims)), 10) == 0, dims
+    P = ctypes.c_void_p
+    fields = (P * 5)(*[0x1000] * 5)
+    widths = (ctypes.c_int32 * 5)(12, 12, 12, 12, 12)
+    ptr3 = (P * 3)(*[0x1000] * 3)
+    args = [ctypes.byref(net), 4096, 5, fields, widths, FAKE, ptr3, ptr3, FAKE, None, ptr3, ptr3, None,
+            FAKE, 1 << 30, None]
+    a = list(args); a[14] = 16
+    assert lib.ams_ctr_fwd_bwd(*a) == WS
+    a = list(args); a[1] = 0
+    assert lib.ams_ctr_fwd_bwd(*a) == SIZE
+    bad_w = (ctypes.c_int32 * 5)(12, 12, 12, 12, 11)      # widths must sum to dims[0]
+    a = list(args); a[4] = bad_w
+    assert lib.ams_ctr_fwd_bwd(*a) == DIMS
+    a = list(args); a[2] = 9
+    assert lib.ams_ctr_fwd_bwd(*a) == DIMS
+    a = list(args); a[5] = None               # labels
+    assert lib.ams_ctr_fwd_bwd(*a) == NULL
+    a = list(args); a[8] = None               # loss
+    assert lib.ams_ctr_fwd_bwd(*a) == NULL
+    # Adagrad
+    assert lib.ams_adagrad_rows(12, FAKE, FAKE, -1, FAKE, FAKE, 100, FAKE, 0.01, 1e-8, None) == SIZE
+    assert lib.ams_adagrad_rows(12, FAKE, FAKE, 0, None, None, 100, None, 0.01, 1e-8, None) == OK
+    assert lib.ams_adagrad_rows(12, FAKE, FAKE, 10, FAKE, None, 100, FAKE, 0.01, 1e-8, None) == NULL
