@@ -150,6 +150,8 @@ def main():
     mode = args.mode or w.pools[-1]
     torch.cuda.set_device(0)
     ams.load()
+    if w.joint is not None:
+        return bench_joint(w, mode, args)
 
     # inputs, resident in HBM before timing starts
     T = synth.table_full(w, device="cuda")
@@ -304,6 +306,127 @@ def main():
     }
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(w, host_batches[0], mode)
+    print(json.dumps(out))
+
+
+def bench_joint(w, mode, args):
+    """The joint step (image path + ID bags + CTR model + sparse Adagrad), the
+    ID tables and accumulators updated in place every step."""
+    import numpy as np
+    import torch
+
+    from paper_1711_06505_amd import ams, synth
+
+    T = synth.table_full(w, device="cuda")
+    Ws, bs = synth.make_weights(w)
+    Wd = [x.cuda() for x in Ws]
+    bd = [x.cuda() for x in bs]
+    cW, cb = synth.make_ctr_weights(w)
+    cWd = [x.cuda() for x in cW]
+    cbd = [x.cuda() for x in cb]
+    n_t = len(w.joint.id_rows)
+    tabs = [synth.id_table_full(w, t, device="cuda") for t in range(n_t)]
+    accs = [torch.full_like(x, w.joint.acc0) for x in tabs]
+    dev_batches = []
+    for k in range(args.batches):
+        hb = synth.make_batch(w, k=k)
+        jb = synth.make_joint(w, hb, k=k)
+        dev_batches.append({
+            "ids": torch.from_numpy(synth.occurrences(hb)).cuda(),
+            "seg_off": torch.from_numpy(hb["seg_off"]).cuda(),
+            "id_ids": [torch.from_numpy(synth.joint_occurrences(jb, t)).cuda() for t in range(n_t)],
+            "labels": torch.from_numpy(jb["labels"]).cuda(),
+            "n_beh": int(hb["seg_off"][-1]),
+        })
+    n_beh_max = max(b["n_beh"] for b in dev_batches)
+    js = ams.JointStep(w.dims, w.dtype, mode, w.batch, n_beh_max, w.joint.id_rows, w.joint.id_dim,
+                       synth.ctr_dims(w))
+    js.alloc_workspace(w.n_images)
+    stream = torch.cuda.current_stream()
+
+    def one(b):
+        js.run(b["ids"], w.n_images, T, Wd, bd, b["seg_off"], b["id_ids"], tabs, accs, b["labels"], cWd, cbd,
+               w.joint.lr, w.joint.eps)
+
+    n_uniq, n_rows = [], []
+    for b in dev_batches:
+        one(b)
+        torch.cuda.synchronize()
+        assert int(js.img.dev_status.item()) == 0 and all(int(x.item()) == 0 for x in js.t_status)
+        n_uniq.append(int(js.img.n_uniq.item()))
+        n_rows.append(sum(int(x.item()) for x in js.t_nu))
+    for s in range(args.warmup):
+        one(dev_batches[s % len(dev_batches)])
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record(stream)
+    for s in range(args.steps):
+        one(dev_batches[s % len(dev_batches)])
+    t1.record(stream)
+    torch.cuda.synchronize()
+    ms_total = t0.elapsed_time(t1)
+    order = [s % len(dev_batches) for s in range(args.steps)]
+    beh_total = sum(dev_batches[i]["n_beh"] for i in order)
+    uniq_total = sum(n_uniq[i] for i in order)
+    rows_total = sum(n_rows[i] for i in order)
+    loss = float(js.loss.item())
+
+    ams.ams_timing_read()
+    ams.ams_timing_enable(True)
+    for s in range(args.steps):
+        one(dev_batches[s % len(dev_batches)])
+    torch.cuda.synchronize()
+    ams.ams_timing_enable(False)
+    ktimes = ams.ams_timing_read()
+    kernels = {k: {"launches": n, "ms_per_launch": t / n} for k, (n, t) in ktimes.items() if n}
+
+    esz = 2 if w.dtype == "bf16" else 4
+    u_mean = uniq_total / args.steps
+    peak = PEAK_MFMA[w.dtype]
+    dom = max(ktimes, key=lambda k: ktimes[k][1])
+    t_launch = kernels[dom]["ms_per_launch"] * 1e-3
+    if dom in GEMM_KERNELS:
+        fl_u, by_u = gemm_work_per_unique(w.dims, esz)
+        bound = "mfma" if fl_u / peak >= by_u / PEAK_HBM else "hbm"
+        if bound == "mfma":
+            ach, pk, unit, alg = u_mean * fl_u / t_launch / 1e12, peak / 1e12, "TFLOP/s", u_mean * fl_u
+        else:
+            ach, pk, unit, alg = u_mean * by_u / t_launch / 1e9, PEAK_HBM / 1e9, "GB/s", u_mean * by_u
+        roof = {"kernel": dom, "bound": bound, "achieved": ach, "peak": pk, "unit": unit, "frac": ach / pk,
+                "traffic": traffic_from_profile(w.name, dom, u_mean), "algorithmic_per_launch": alg,
+                "avg_launch_ms": t_launch * 1e3,
+                "unit_of_work": f"{fl_u} flop and {by_u} B per unique image, {u_mean:.0f} unique per launch"}
+    else:
+        roof = {"kernel": dom, "bound": None, "achieved": None, "peak": None, "unit": None, "frac": None,
+                "traffic": None, "avg_launch_ms": t_launch * 1e3}
+    for k, v in kernels.items():
+        if k in GEMM_KERNELS:
+            fl_u, _ = gemm_work_per_unique(w.dims, esz)
+            v["mfma_frac"] = u_mean * fl_u / (v["ms_per_launch"] * 1e-3) / peak
+    fwd_f, bwd_f = flops_per_unique(w.dims)
+    ms_step = ms_total / args.steps
+    out = {
+        "metric": METRIC, "value": beh_total / (ms_total * 1e-3), "unit": "behavior images/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms_step, "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": f"{w.name}: B={w.batch}, lengths {w.lengths}, image ids {w.ids} over "
+                               f"{w.n_images} images, table {w.n_images}x{w.in_dim} {w.dtype}, MLP "
+                               f"{'-'.join(map(str, w.dims))}, pooling {mode}; ID tables "
+                               f"{'/'.join(str(n) for n in w.joint.id_rows)} x {w.joint.id_dim} fp32 "
+                               f"Zipf({w.joint.id_zipf}); CTR MLP {'-'.join(map(str, synth.ctr_dims(w)))} fp32, "
+                               f"softmax cross-entropy; sparse Adagrad lr {w.joint.lr}; fwd+bwd+update",
+                   "batch": w.batch, "behaviors_per_step": beh_total / args.steps, "unique_per_step": u_mean,
+                   "id_rows_touched_per_step": rows_total / args.steps, "rotating_batches": len(dev_batches)},
+        "step_mfma_frac": u_mean * (fwd_f + bwd_f) / (ms_step * 1e-3) / peak,
+        "step_hbm_frac": u_mean * 2 * w.in_dim * esz / (ms_step * 1e-3) / PEAK_HBM,
+        "unique_images_per_s": uniq_total / (ms_total * 1e-3),
+        "id_rows_per_s": rows_total / (ms_total * 1e-3),
+        "samples_per_s": w.batch * args.steps / (ms_total * 1e-3),
+        "loss_last_step": loss,
+        "kernels": kernels,
+        "roofline": roof,
+        "cpu_baseline": None,
+    }
     print(json.dumps(out))
 
 

@@ -96,62 +96,211 @@ __host__ __device__ inline int ctr_part_size(const CtrArgs &a)
     return n;
 }
 
-// out[s][o] = (bias + sum_k in[s][k] W[o][k]), ReLU'd unless last; thread
-// (o = t % O, group g = t / O) takes samples g, g + G, ... (G = 256 / O).
-__device__ __forceinline__ void ctr_dense_fwd(const float *in, int K, float *out, int O, const float *__restrict__ W,
-                                              const float *__restrict__ bias, bool relu, int t)
+// Parts of a layer split over threads: forward P * kCtrBS * O, backward-data
+// P * kCtrBS * K (P is chosen as in ctr_dense_fwd / ctr_dense_bwd_data).
+__host__ __device__ inline int ctr_fwd_parts(int K, int O)
 {
-    const int G = max(1, min(kCtrBS, kThreads / O));
-    const int o = t % O, g = t / O;
-    if (g >= G) return;
-    float acc[kCtrBS];
-    const float bo = bias[o];
-#pragma unroll
-    for (int s = 0; s < kCtrBS; ++s) acc[s] = bo;
-    const float *wr = W + (size_t)o * K;
-    for (int k = 0; k < K; ++k) {
-        const float w = wr[k];
-#pragma unroll
-        for (int s = 0; s < kCtrBS; ++s)
-            if (s % G == g) acc[s] = fmaf(in[s * K + k], w, acc[s]);
-    }
-#pragma unroll
-    for (int s = 0; s < kCtrBS; ++s)
-        if (s % G == g) out[s * O + o] = relu ? fmaxf(acc[s], 0.f) : acc[s];
+    int P = kThreads / O;
+    if (P < 1) P = 1;
+    if (P > (K + 15) / 16) P = (K + 15) / 16;
+    return P;
 }
 
-// gin[s][k] = sum_o gout[s][o] W[o][k] (masked by [in > 0] when `mask`);
-// thread (k = t % K, group g = t / K) takes samples g, g + G, ...
-__device__ __forceinline__ void ctr_dense_bwd_data(const float *gout, int O, float *gin, const float *in, int K,
-                                                   const float *__restrict__ W, bool mask, int t)
+__host__ __device__ inline int ctr_bwd_parts(int K, int O)
 {
-    const int G = max(1, min(kCtrBS, kThreads / K));
-    const int k = t % K, g = t / K;
-    if (g >= G) return;
-    float acc[kCtrBS];
+    int P = kThreads / K;
+    if (P < 1) P = 1;
+    if (P > (O + 7) / 8) P = (O + 7) / 8;
+    return P;
+}
+
+// out[s][o] = bias[o] + sum_k in[s][k] W[o][k] (ReLU'd unless last) for the
+// block's kCtrBS samples.  Work item (o, part p of P): the K range of part p
+// (a multiple of 4 wide), its W row streamed in float4 runs of 16, all
+// samples accumulated together (in[s][k] is the same LDS word for the whole
+// wave: a broadcast).  With P > 1 (narrow layers) the parts go to `scr`
+// [P][kCtrBS][O] and are added in part order.
+__device__ __forceinline__ void ctr_dense_fwd(const float *in, int K, float *out, int O, const float *__restrict__ W,
+                                              const float *__restrict__ bias, bool relu, float *scr, int t)
+{
+    const int P = ctr_fwd_parts(K, O);
+    const int KC = (((K + P - 1) / P) + 3) & ~3;
+    for (int it = t; it < O * P; it += kThreads) {
+        const int o = it % O, pp = it / O;
+        const int k0 = pp * KC, k1 = min(K, k0 + KC);
+        float acc[kCtrBS];
 #pragma unroll
-    for (int s = 0; s < kCtrBS; ++s) acc[s] = 0.f;
-    for (int o = 0; o < O; ++o) {
-        const float w = W[(size_t)o * K + k];
+        for (int s = 0; s < kCtrBS; ++s) acc[s] = 0.f;
+        const float *wr = W + (size_t)o * K;
+        const bool v4 = (K & 3) == 0;
+        for (int kb = k0; kb < k1; kb += 16) {
+            float w[16];
+            if (v4 && kb + 16 <= k1) {
 #pragma unroll
-        for (int s = 0; s < kCtrBS; ++s)
-            if (s % G == g) acc[s] = fmaf(gout[s * O + o], w, acc[s]);
+                for (int q = 0; q < 4; ++q) {
+                    const float4 x = *(const float4 *)(wr + kb + 4 * q);
+                    w[4 * q] = x.x;
+                    w[4 * q + 1] = x.y;
+                    w[4 * q + 2] = x.z;
+                    w[4 * q + 3] = x.w;
+                }
+            } else {
+#pragma unroll
+                for (int q = 0; q < 16; ++q) w[q] = kb + q < k1 ? wr[kb + q] : 0.f;
+            }
+#pragma unroll
+            for (int q = 0; q < 16; ++q) {
+                if (kb + q >= k1) break;
+#pragma unroll
+                for (int s = 0; s < kCtrBS; ++s) acc[s] = fmaf(in[s * K + kb + q], w[q], acc[s]);
+            }
+        }
+        if (P == 1) {
+            const float bo = bias[o];
+#pragma unroll
+            for (int s = 0; s < kCtrBS; ++s) {
+                const float v = acc[s] + bo;
+                out[s * O + o] = relu ? fmaxf(v, 0.f) : v;
+            }
+        } else {
+#pragma unroll
+            for (int s = 0; s < kCtrBS; ++s) scr[(pp * kCtrBS + s) * O + o] = acc[s];
+        }
     }
+    if (P > 1) {
+        __syncthreads();
+        for (int e = t; e < kCtrBS * O; e += kThreads) {
+            const int o = e % O;
+            float v = bias[o];
+            for (int pp = 0; pp < P; ++pp) v += scr[pp * kCtrBS * O + e];
+            out[e] = relu ? fmaxf(v, 0.f) : v;
+        }
+    }
+}
+
+// gin[s][k] = sum_o gout[s][o] W[o][k] (masked by [in > 0] when `mask`).
+// Work item (k, part p of P over O); the lanes of a wave take consecutive k,
+// so each W row read is contiguous across the wave; 8 rows in flight.  Parts
+// are added in order through `scr` as in the forward.
+__device__ __forceinline__ void ctr_dense_bwd_data(const float *gout, int O, float *gin, const float *in, int K,
+                                                   const float *__restrict__ W, bool mask, float *scr, int t)
+{
+    const int P = ctr_bwd_parts(K, O);
+    const int OC = (O + P - 1) / P;
+    for (int it = t; it < K * P; it += kThreads) {
+        const int k = it % K, pp = it / K;
+        const int o0 = pp * OC, o1 = min(O, o0 + OC);
+        float acc[kCtrBS];
 #pragma unroll
-    for (int s = 0; s < kCtrBS; ++s)
-        if (s % G == g) gin[s * K + k] = (!mask || in[s * K + k] > 0.f) ? acc[s] : 0.f;
+        for (int s = 0; s < kCtrBS; ++s) acc[s] = 0.f;
+        for (int ob = o0; ob < o1; ob += 8) {
+            float w[8];
+#pragma unroll
+            for (int q = 0; q < 8; ++q) w[q] = ob + q < o1 ? W[(size_t)(ob + q) * K + k] : 0.f;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                if (ob + q >= o1) break;
+#pragma unroll
+                for (int s = 0; s < kCtrBS; ++s) acc[s] = fmaf(gout[s * O + ob + q], w[q], acc[s]);
+            }
+        }
+        if (P == 1) {
+#pragma unroll
+            for (int s = 0; s < kCtrBS; ++s) gin[s * K + k] = (!mask || in[s * K + k] > 0.f) ? acc[s] : 0.f;
+        } else {
+#pragma unroll
+            for (int s = 0; s < kCtrBS; ++s) scr[(pp * kCtrBS + s) * K + k] = acc[s];
+        }
+    }
+    if (P > 1) {
+        __syncthreads();
+        for (int e = t; e < kCtrBS * K; e += kThreads) {
+            float v = 0.f;
+            for (int pp = 0; pp < P; ++pp) v += scr[pp * kCtrBS * K + e];
+            gin[e] = (!mask || in[e] > 0.f) ? v : 0.f;
+        }
+    }
+}
+
+// Partial dW[o][k] = sum_s gout[s][o] in[s][k] over the block's samples and
+// db[o] = sum_s gout[s][o], in 4 x 4 register tiles (8 LDS words per sample
+// feed 16 FMAs); written to the block's partial row at p (dW, then db).
+__device__ __forceinline__ void ctr_dense_bwd_weight(const float *gout, int O, const float *in, int K,
+                                                     float *__restrict__ p, int t)
+{
+    const int to = (O + 3) / 4, tk = (K + 3) / 4;
+    for (int it = t; it < to * tk; it += kThreads) {
+        const int o0 = 4 * (it / tk), k0 = 4 * (it % tk);
+        float acc[4][4];
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+#pragma unroll 4
+        for (int s = 0; s < kCtrBS; ++s) {
+            float g[4], x[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) g[i] = o0 + i < O ? gout[s * O + o0 + i] : 0.f;
+#pragma unroll
+            for (int j = 0; j < 4; ++j) x[j] = k0 + j < K ? in[s * K + k0 + j] : 0.f;
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(g[i], x[j], acc[i][j]);
+        }
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+                if (o0 + i < O && k0 + j < K) p[(o0 + i) * K + k0 + j] = acc[i][j];
+    }
+    for (int o = t; o < O; o += kThreads) {
+        float acc = 0.f;
+#pragma unroll
+        for (int s = 0; s < kCtrBS; ++s) acc += gout[s * O + o];
+        p[O * K + o] = acc;
+    }
 }
 
 // One block = kCtrBS samples: forward through every layer in LDS, softmax
 // and cross-entropy, then the backward; the block's weight-gradient and loss
 // sums (over its samples, ascending) go to its partial row.
+// Dynamic LDS, sized by ctr_lds_floats for the actual widths: act (every
+// layer's activations, [kCtrBS][dims[l]] each), grd (their loss gradients),
+// scr (parts of narrow layers in the backward), the samples' losses.
+__host__ __device__ inline int ctr_act_floats(const CtrArgs &a)
+{
+    int n = 0;
+    for (int l = 0; l <= a.L; ++l) n += kCtrBS * a.dims[l];
+    return n;
+}
+
+__host__ __device__ inline int ctr_scr_floats(const CtrArgs &a)
+{
+    int n = 0;
+    for (int l = 0; l < a.L; ++l) {
+        const int K = a.dims[l], O = a.dims[l + 1];
+        const int pf = ctr_fwd_parts(K, O), pb = ctr_bwd_parts(K, O);
+        if (pf > 1 && pf * kCtrBS * O > n) n = pf * kCtrBS * O;
+        if (pb > 1 && pb * kCtrBS * K > n) n = pb * kCtrBS * K;
+    }
+    return n;
+}
+
+inline size_t ctr_lds_bytes(const CtrArgs &a)
+{
+    return (size_t)(2 * ctr_act_floats(a) + ctr_scr_floats(a) + kCtrBS) * 4;
+}
+
 __global__ __launch_bounds__(kThreads) void ctr_fb_k(CtrArgs a, int B, const int32_t *__restrict__ labels,
                                                      float *__restrict__ prob, float *__restrict__ part, int PS)
 {
-    constexpr int kAct = kCtrBS * (kCtrMaxIn + 2 * kCtrMaxHidden + kCtrMaxC);
-    __shared__ float act[kAct];              // act[l]: [kCtrBS][dims[l]] per layer
-    __shared__ float grd[kAct];              // the loss gradient of each act[l]
-    __shared__ float lossv[kCtrBS];
+    extern __shared__ float lds[];
+    const int na = ctr_act_floats(a);
+    float *act = lds;                        // act[l]: [kCtrBS][dims[l]] per layer
+    float *grd = lds + na;                   // the loss gradient of each act[l]
+    float *scr = lds + 2 * na;               // parts of narrow layers in the backward
+    float *lossv = scr + ctr_scr_floats(a);
     const int t = threadIdx.x;
     const int b0 = blockIdx.x * kCtrBS;
     const int L = a.L;
@@ -173,7 +322,7 @@ __global__ __launch_bounds__(kThreads) void ctr_fb_k(CtrArgs a, int B, const int
     }
     __syncthreads();
     for (int l = 0; l < L; ++l) {
-        ctr_dense_fwd(act + off[l], a.dims[l], act + off[l + 1], a.dims[l + 1], a.W[l], a.b[l], l < L - 1, t);
+        ctr_dense_fwd(act + off[l], a.dims[l], act + off[l + 1], a.dims[l + 1], a.W[l], a.b[l], l < L - 1, scr, t);
         __syncthreads();
     }
     // softmax, cross-entropy, dlogits = (p - onehot(y)) / B
@@ -214,24 +363,8 @@ __global__ __launch_bounds__(kThreads) void ctr_fb_k(CtrArgs a, int B, const int
         const int K = a.dims[l], O = a.dims[l + 1];
         const float *gout = grd + off[l + 1], *in = act + off[l];
         // weight and bias gradients of layer l over this block's samples
-        for (int e = t; e < O * K; e += kThreads) {
-            const int o = e / K, k = e % K;
-            float acc = 0.f;
-#pragma unroll
-            for (int s = 0; s < kCtrBS; ++s) acc = fmaf(gout[s * O + o], in[s * K + k], acc);
-            p[wo[l] + e] = acc;
-        }
-        for (int o = t; o < O; o += kThreads) {
-            float acc = 0.f;
-#pragma unroll
-            for (int s = 0; s < kCtrBS; ++s) acc += gout[s * O + o];
-            p[wo[l] + O * K + o] = acc;
-        }
-        if (l > 0) {
-            ctr_dense_bwd_data(gout, O, grd + off[l], in, K, a.W[l], true, t);
-        } else {
-            ctr_dense_bwd_data(gout, O, grd, in, K, a.W[0], false, t);
-        }
+        ctr_dense_bwd_weight(gout, O, in, K, p + wo[l], t);
+        ctr_dense_bwd_data(gout, O, grd + off[l], in, K, a.W[l], l > 0, scr, t);
         __syncthreads();
     }
     // input-field gradients
@@ -410,7 +543,7 @@ extern "C" ams_status ams_ctr_fwd_bwd(const ams_ctr *net, int32_t B, int32_t n_f
     if (!ws || ws_bytes < (size_t)G * PS * 4) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     float *part = (float *)ws;
-    AMS_LAUNCH("ctr_fwd_bwd", st, ctr_fb_k<<<G, kThreads, 0, st>>>(a, B, labels, prob, part, PS));
+    AMS_LAUNCH("ctr_fwd_bwd", st, ctr_fb_k<<<G, kThreads, ctr_lds_bytes(a), st>>>(a, B, labels, prob, part, PS));
     CtrOut o{};
     o.L = a.L;
     for (int l = 0; l <= a.L; ++l) o.dims[l] = a.dims[l];
