@@ -45,6 +45,13 @@
  * The merged gradient of an ID row is the SUM aggregator's backward with the
  * bag gradient as upstream (orc_pool_bwd, mode SUM).
  *
+ *   query pool one channel of the multiple-query attentive pooling of section
+ *              5.2: attention over the behavior image embeddings with a query
+ *              given per sample (the ad's ID embedding for the ID channel),
+ *              w = softmax_j(e_j . q_i), u_i = sum_j w_j e_j; its backward
+ *              gives the behaviors' embedding gradients (merged per unique
+ *              image) and the query gradient.
+ *
  * Readings where the paper is silent (documented with the library): no
  * activation after the last layer unless final_relu is set; ReLU'(0) = 0;
  * the max-pool argmax is the first (lowest) position attaining the maximum;
@@ -572,5 +579,83 @@ int orc_adagrad_rows(int32_t n, int32_t D, const double *grad, double lr, double
         accum[e] += grad[e] * grad[e];
         rows[e] -= lr * grad[e] / (sqrt(accum[e]) + eps);
     }
+    return 0;
+}
+
+/* ------------------------------------------------------ query attention */
+
+/*
+ * Q [B x D]: the query of each sample.  For sample i with behaviors
+ * j in [seg_off[i], seg_off[i+1]): s_j = e_j . q_i, w = softmax(s) (max
+ * subtracted), u_i = sum_j w_j e_j; an empty segment pools to 0.  U [B x D],
+ * w [n_beh] out.
+ */
+int orc_pool_query_fwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
+                       const int32_t *inv, const double *E, const double *Q, double *U, double *w)
+{
+    if (B < 0 || D <= 0) return 1;
+    if (B > 0 && (seg_off[0] != 0 || seg_off[B] != n_beh)) return 1;
+#pragma omp parallel for schedule(static)
+    for (int32_t i = 0; i < B; ++i) {
+        const int64_t j0 = seg_off[i], j1 = seg_off[i + 1];
+        const double *q = Q + (size_t)i * D;
+        double *u = U + (size_t)i * D;
+        for (int d = 0; d < D; ++d) u[d] = 0.0;
+        if (j1 == j0) continue;
+        double smax = -INFINITY;
+        for (int64_t j = j0; j < j1; ++j) {
+            const double *e = E + (size_t)inv[j] * D;
+            double sv = 0.0;
+            for (int d = 0; d < D; ++d) sv += e[d] * q[d];
+            w[j] = sv;
+            if (sv > smax) smax = sv;
+        }
+        double den = 0.0;
+        for (int64_t j = j0; j < j1; ++j) den += exp(w[j] - smax);
+        for (int64_t j = j0; j < j1; ++j) w[j] = exp(w[j] - smax) / den;
+        for (int64_t j = j0; j < j1; ++j) {
+            const double *e = E + (size_t)inv[j] * D;
+            for (int d = 0; d < D; ++d) u[d] += w[j] * e[d];
+        }
+    }
+    return 0;
+}
+
+/*
+ * Backward of orc_pool_query_fwd for the loss sum(gU * U): with
+ * c_i = gU_i . u_i and ds_j = w_j (gU_i . e_j - c_i), the gradient of
+ * occurrence j is ge_j = w_j gU_i + ds_j q_i (the ads' occurrences get none
+ * from this channel); dE[u] = sum of ge_j over the behaviors j of image u in
+ * ascending j (dE [n_u x D], overwritten); dQ_i = sum_j ds_j e_j.
+ */
+int orc_pool_query_bwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
+                       const int32_t *inv, int32_t n_u, const double *E, const double *Q,
+                       const double *U, const double *w, const double *gU, double *dE, double *dQ)
+{
+    if (B < 0 || D <= 0 || n_u < 0) return 1;
+    double *ge = (double *)malloc(sizeof(double) * (size_t)(n_beh > 0 ? n_beh : 1) * D);
+#pragma omp parallel for schedule(static)
+    for (int32_t i = 0; i < B; ++i) {
+        const int64_t j0 = seg_off[i], j1 = seg_off[i + 1];
+        const double *g = gU + (size_t)i * D, *u = U + (size_t)i * D, *q = Q + (size_t)i * D;
+        double c = 0.0;
+        for (int d = 0; d < D; ++d) c += g[d] * u[d];
+        double *dq = dQ + (size_t)i * D;
+        for (int d = 0; d < D; ++d) dq[d] = 0.0;
+        for (int64_t j = j0; j < j1; ++j) {
+            const double *e = E + (size_t)inv[j] * D;
+            double dw = 0.0;
+            for (int d = 0; d < D; ++d) dw += g[d] * e[d];
+            const double ds = w[j] * (dw - c);
+            for (int d = 0; d < D; ++d) {
+                ge[(size_t)j * D + d] = w[j] * g[d] + ds * q[d];
+                dq[d] += ds * e[d];
+            }
+        }
+    }
+    memset(dE, 0, sizeof(double) * (size_t)n_u * D);
+    for (int64_t j = 0; j < n_beh; ++j)
+        for (int d = 0; d < D; ++d) dE[(size_t)inv[j] * D + d] += ge[(size_t)j * D + d];
+    free(ge);
     return 0;
 }

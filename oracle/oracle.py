@@ -56,6 +56,8 @@ def _load():
     lib.orc_bag_fwd.argtypes = [i32, i32, P, i64, P, i64, P, P]
     lib.orc_ctr_fwd_bwd.argtypes = [i32, ctypes.c_int, P, P, P, P, P, P, P, P, P, P, P]
     lib.orc_adagrad_rows.argtypes = [i32, i32, P, ctypes.c_double, ctypes.c_double, P, P]
+    lib.orc_pool_query_fwd.argtypes = [i32, i32, P, i64, P, P, P, P, P]
+    lib.orc_pool_query_bwd.argtypes = [i32, i32, P, i64, P, i32, P, P, P, P, P, P, P]
     lib.orc_num_threads.restype = ctypes.c_int
     lib.orc_set_threads.argtypes = [ctypes.c_int]
     _lib = lib
@@ -391,3 +393,38 @@ def joint_step(batch: dict, jb: dict, spec, n_ids: int, T, Ws, bs, id_rows, ctr_
     return {"dedup": dd, "fwd": fw, "pool": pf, "pool_bwd": pb, "bwd": bw, "id_dedup": idd, "bags": bags,
             "X": X, "ctr": cf, "dU": dU, "dA": dA, "dbags": dbags, "row_grads": grads,
             "new_rows": new_rows, "new_accum": new_acc}
+
+
+# ------------------------------------------------- multiple-query attention
+
+def pool_query_fwd(seg_off, inv, E, Q) -> dict:
+    """One attentive channel with a per-sample query Q [B x D]."""
+    lib = _load()
+    seg_off = _i32(seg_off)
+    inv = _i32(inv)
+    E, Q = _f64(E), _f64(Q)
+    B, D = seg_off.size - 1, E.shape[1]
+    n_beh = int(seg_off[-1])
+    U = np.zeros((max(B, 1), D))
+    w = np.zeros(max(n_beh, 1))
+    _check(lib.orc_pool_query_fwd(B, D, _ptr(seg_off), n_beh, _ptr(inv), _ptr(E), _ptr(Q), _ptr(U), _ptr(w)),
+           "pool_query_fwd")
+    return {"U": U[:B].copy(), "w": w[:n_beh].copy()}
+
+
+def pool_query_bwd(seg_off, inv, n_uniq: int, E, Q, fwd: dict, gU) -> dict:
+    """dE (merged per unique image, behaviors only) and dQ of one query channel."""
+    lib = _load()
+    seg_off = _i32(seg_off)
+    inv = _i32(inv)
+    E, Q, gU = _f64(E), _f64(Q), _f64(gU)
+    B, D = seg_off.size - 1, E.shape[1]
+    n_beh = int(seg_off[-1])
+    w = np.ascontiguousarray(fwd["w"], np.float64)
+    if w.size == 0:
+        w = np.zeros(1)
+    dE = np.zeros((max(n_uniq, 1), D))
+    dQ = np.zeros((max(B, 1), D))
+    _check(lib.orc_pool_query_bwd(B, D, _ptr(seg_off), n_beh, _ptr(inv), int(n_uniq), _ptr(E), _ptr(Q),
+                                  _ptr(_f64(fwd["U"])), _ptr(w), _ptr(gU), _ptr(dE), _ptr(dQ)), "pool_query_bwd")
+    return {"dE": dE[:n_uniq].copy(), "dQ": dQ[:B].copy()}
