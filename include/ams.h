@@ -236,6 +236,37 @@ ams_status ams_pool_bwd(int32_t mode, int32_t B, int32_t D,
                         const void *saved, const float *dU, const float *dA,
                         float *dE, void *ws, size_t ws_bytes, void *stream);
 
+/* --------------------------------------------------- query pooling ----
+ * One channel of multiple-query attentive pooling (section 5.2): attention
+ * over a sample's behavior image embeddings with a query given per sample
+ * (for the ID channel, the ad's ID embedding; the image channel is
+ * ams_pool_fwd's AMS_POOL_ATT, whose query is the ad image embedding).  The
+ * channels' pooled vectors are concatenated by the caller.
+ *
+ * fwd:  Q [B x D] queries (device); U [B x D] out: u_i = sum_j w_j e_j with
+ *       w = softmax_j(e_j . q_i) (max subtracted; an empty segment pools to
+ *       0); w [n_beh] out: the attention weights.  Other arguments as in
+ *       ams_pool_fwd.
+ * bwd:  with dU [B x D] the loss gradient of U, the gradient of behavior j is
+ *       w_j dU_i + ds_j q_i, ds_j = w_j (dU_i . e_j - dU_i . u_i); dE[u]
+ *       receives the sum over the behaviors of image u in ascending order
+ *       (the ads' occurrences get nothing from this channel): overwritten
+ *       when accumulate = 0, added to the existing dE when accumulate = 1
+ *       (so the two channels of one step merge into one dE; every row u < n_u
+ *       is written by one thread, no atomics); dQ [B x D] out: sum_j ds_j e_j.
+ *       ws: at least ams_pool_workspace(AMS_POOL_ATT, B, n_beh, D, cap) bytes.
+ * Host errors as ams_pool_fwd / ams_pool_bwd. */
+ams_status ams_pool_query_fwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
+                              const int32_t *inv, const float *E, const float *Q,
+                              float *U, float *w, void *stream);
+ams_status ams_pool_query_bwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
+                              const int32_t *inv, const int32_t *occ_perm,
+                              const int32_t *uniq_off, const int32_t *n_uniq,
+                              int32_t n_uniq_cap, const float *E, const float *Q,
+                              const float *U, const float *w, const float *dU,
+                              float *dQ, float *dE, int32_t accumulate,
+                              void *ws, size_t ws_bytes, void *stream);
+
 /* =================================================== joint step (worker) ====
  * The worker side of a joint training step (Algorithm 1, WORKERITERATION):
  * sparse ID features embedded from key-value tables (section 4.1) next to the

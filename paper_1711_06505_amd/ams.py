@@ -24,7 +24,7 @@ EXPORTS = ["ams_status_str", "ams_build_info", "ams_dedup_workspace", "ams_dedup
            "ams_embed_workspace", "ams_embed_fwd", "ams_embed_bwd", "ams_pool_fwd",
            "ams_pool_workspace", "ams_pool_bwd", "ams_timing_enable", "ams_timing_read",
            "ams_bag_fwd", "ams_bag_workspace", "ams_bag_bwd", "ams_ctr_workspace", "ams_ctr_fwd_bwd",
-           "ams_adagrad_rows"]
+           "ams_adagrad_rows", "ams_pool_query_fwd", "ams_pool_query_bwd"]
 
 
 class AmsError(RuntimeError):
@@ -93,6 +93,10 @@ def load() -> ctypes.CDLL:
                                     sz, P]
     lib.ams_adagrad_rows.restype = ctypes.c_int
     lib.ams_adagrad_rows.argtypes = [i32, P, P, i32, P, P, i64, P, ctypes.c_float, ctypes.c_float, P]
+    lib.ams_pool_query_fwd.restype = ctypes.c_int
+    lib.ams_pool_query_fwd.argtypes = [i32, i32, P, i64, P, P, P, P, P, P]
+    lib.ams_pool_query_bwd.restype = ctypes.c_int
+    lib.ams_pool_query_bwd.argtypes = [i32, i32, P, i64, P, P, P, P, i32, P, P, P, P, P, P, P, i32, P, sz, P]
     lib.ams_timing_enable.restype = ctypes.c_int
     lib.ams_timing_enable.argtypes = [ctypes.c_int]
     lib.ams_timing_read.restype = ctypes.c_int
@@ -213,6 +217,21 @@ def ams_timing_read(cap: int = 64) -> dict:
     if n.value > cap:
         raise RuntimeError(f"ams_timing_read: {n.value} kernels recorded, buffer holds {cap}")
     return {buf[k].name.decode(): (int(buf[k].launches), float(buf[k].total_ms)) for k in range(n.value)}
+
+
+def ams_pool_query_fwd(seg_off, n_beh: int, inv, E, Q, U, w, stream=None):
+    B, D = Q.shape
+    _check(load().ams_pool_query_fwd(B, D, _p(seg_off), int(n_beh), _p(inv), _p(E), _p(Q), _p(U), _p(w),
+                                     _stream(stream)), "ams_pool_query_fwd")
+
+
+def ams_pool_query_bwd(seg_off, n_beh: int, inv, occ_perm, uniq_off, n_uniq, n_uniq_cap: int, E, Q, U, w, dU, dQ,
+                       dE, accumulate: bool, ws, stream=None):
+    B, D = Q.shape
+    _check(load().ams_pool_query_bwd(B, D, _p(seg_off), int(n_beh), _p(inv), _p(occ_perm), _p(uniq_off),
+                                     _p(n_uniq), int(n_uniq_cap), _p(E), _p(Q), _p(U), _p(w), _p(dU), _p(dQ),
+                                     _p(dE), int(bool(accumulate)), _p(ws), ws.numel() * ws.element_size(),
+                                     _stream(stream)), "ams_pool_query_bwd")
 
 
 def make_ctr(dims) -> ams_ctr:

@@ -22,6 +22,12 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / AMS_WAVE;
+// Internal mode: attentive pooling with a query given per sample (one channel
+// of multiple-query attentive pooling, section 5.2).  It runs the attentive
+// kernels with the query read from Q[i] instead of the ad's embedding; the
+// ads' occurrences get no gradient from it and the attention term
+// sum_j ds_j e_j is the query's gradient.
+constexpr int kPoolQuery = 3;
 
 template <int DM>
 __device__ __forceinline__ void load_row(const float *__restrict__ E, int row, int D, float (&e)[DM])
@@ -35,14 +41,15 @@ template <int MODE, int DM>
 __global__ __launch_bounds__(kThreads) void pool_fwd_k(int B, int D, const int32_t *__restrict__ seg_off,
                                                        int64_t n_beh, const int32_t *__restrict__ inv,
                                                        const float *__restrict__ E, float *__restrict__ U,
-                                                       float *__restrict__ A, void *__restrict__ saved)
+                                                       float *__restrict__ A, void *__restrict__ saved,
+                                                       const float *__restrict__ Q)
 {
     const int lane = ams_lane();
     const int i = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
     if (i >= B) return;
     const int j0 = seg_off[i], j1 = seg_off[i + 1];
     const int ad_row = inv[n_beh + i];
-    if (lane < D) A[(size_t)i * D + lane] = E[(size_t)ad_row * D + lane];
+    if (MODE != kPoolQuery && lane < D) A[(size_t)i * D + lane] = E[(size_t)ad_row * D + lane];
     float out[DM];
     if (MODE == AMS_POOL_SUM) {
         float acc[DM];
@@ -94,7 +101,8 @@ __global__ __launch_bounds__(kThreads) void pool_fwd_k(int B, int D, const int32
         }
     } else {
         float a[DM];
-        load_row<DM>(E, ad_row, D, a);
+        if (MODE == kPoolQuery) load_row<DM>(Q, i, D, a);
+        else load_row<DM>(E, ad_row, D, a);
         float *w = (float *)saved;
         float m = -INFINITY;
         for (int j = j0 + lane; j < j1; j += AMS_WAVE) {
@@ -150,7 +158,7 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_sample(int B, int D, const 
     if (i >= B) return;
     const int j0 = seg_off[i], j1 = seg_off[i + 1];
     for (int j = j0 + lane; j < j1; j += AMS_WAVE) samp[j] = i;
-    if (MODE != AMS_POOL_ATT) return;
+    if (MODE != AMS_POOL_ATT && MODE != kPoolQuery) return;
     float g[DM], u[DM];
     load_row<DM>(dU, i, D, g);
     load_row<DM>(U, i, D, u);
@@ -197,7 +205,7 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int64_t n_beh, i
                                                          float *__restrict__ dE,
                                                          float *__restrict__ head_part,
                                                          float *__restrict__ tail_part,
-                                                         int32_t *__restrict__ cross)
+                                                         int32_t *__restrict__ cross, int accumulate)
 {
     const int lane = ams_lane();
     const int ch = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
@@ -223,7 +231,7 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int64_t n_beh, i
                 const int32_t *am = (const int32_t *)saved + (size_t)i * D;
 #pragma unroll
                 for (int d = 0; d < DM; ++d) v[d] = (d < D && am[d] == k) ? g[d] : 0.f;
-            } else {
+            } else {   // attentive; A holds the query rows in the query mode
                 const float wk = ((const float *)saved)[k];
                 float e[DM], a[DM];
                 load_row<DM>(E, u, D, e);
@@ -235,7 +243,7 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int64_t n_beh, i
 #pragma unroll
                 for (int d = 0; d < DM; ++d) v[d] = wk * g[d] + ds * a[d];
             }
-        } else {
+        } else if (MODE != kPoolQuery) {
             const int i = (int)(k - n_beh);
             if (dA) load_row<DM>(dA, i, D, v);
             if (MODE == AMS_POOL_ATT) {
@@ -270,6 +278,11 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int64_t n_beh, i
             cross_u = u;
         } else {
             dst = dE + (size_t)u * D;                   // whole run inside this chunk
+            if (accumulate) {
+#pragma unroll
+                for (int d = 0; d < DM; ++d)
+                    if (d < D) v[d] += dst[d];
+            }
         }
 #pragma unroll
         for (int d = 0; d < DM; ++d)
@@ -287,7 +300,7 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_fix(int D, int nch, const i
                                                          const int32_t *__restrict__ cross,
                                                          const float *__restrict__ head_part,
                                                          const float *__restrict__ tail_part,
-                                                         float *__restrict__ dE)
+                                                         float *__restrict__ dE, int accumulate)
 {
     const int lane = ams_lane();
     const int ch = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
@@ -310,7 +323,10 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_fix(int D, int nch, const i
         const float s = ams_wave_sum(acc[d]);
         if (lane == d) mine = s;
     }
-    if (lane < D) dE[(size_t)u * D + lane] = tail_part[(size_t)ch * D + lane] + mine;
+    if (lane < D) {
+        const float r = tail_part[(size_t)ch * D + lane] + mine;
+        dE[(size_t)u * D + lane] = accumulate ? dE[(size_t)u * D + lane] + r : r;
+    }
 }
 
 size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -338,21 +354,22 @@ PoolPlan plan_pool(int32_t B, int64_t n_beh, int32_t D)
 
 template <int MODE, int DM>
 void launch_fwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32_t *inv, const float *E,
-                float *U, float *A, void *saved, hipStream_t st)
+                float *U, float *A, void *saved, hipStream_t st, const float *Q = nullptr)
 {
     AMS_LAUNCH("pool_fwd_k", st, pool_fwd_k<MODE, DM><<<(B + kWaves - 1) / kWaves, kThreads, 0, st>>>(B, D, seg_off, n_beh, inv, E, U, A,
-                                                                         saved));
+                                                                         saved, Q));
 }
 
 template <int MODE, int DM>
 void launch_bwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32_t *inv,
                 const int32_t *occ_perm, const int32_t *uniq_off, const float *E, const float *U,
                 const float *A, const void *saved, const float *dU, const float *dA, float *dE,
-                char *ws, const PoolPlan &p, hipStream_t st)
+                char *ws, const PoolPlan &p, hipStream_t st, float *dQ = nullptr, int accumulate = 0)
 {
     int32_t *samp = (int32_t *)(ws + p.off_samp);
     float *cvec = (float *)(ws + p.off_c);
-    float *da = (float *)(ws + p.off_da);
+    // the attention term of each sample: the query's gradient in the query mode
+    float *da = MODE == kPoolQuery ? dQ : (float *)(ws + p.off_da);
     float *head = (float *)(ws + p.off_head);
     float *tail = (float *)(ws + p.off_tail);
     int32_t *cross = (int32_t *)(ws + p.off_cross);
@@ -362,8 +379,9 @@ void launch_bwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32
             B, D, seg_off, inv, E, U, (const float *)saved, dU, samp, cvec, da));
     const int g = (p.nch + kWaves - 1) / kWaves;
     AMS_LAUNCH("pool_bwd_seg", st, pool_bwd_seg<MODE, DM><<<g, kThreads, 0, st>>>(D, n_beh, n_occ, inv, occ_perm, uniq_off, E, A, saved, dU,
-                                                   dA, samp, cvec, da, p.nch, dE, head, tail, cross));
-    AMS_LAUNCH("pool_bwd_fix", st, pool_bwd_fix<DM><<<g, kThreads, 0, st>>>(D, p.nch, uniq_off, cross, head, tail, dE));
+                                                   dA, samp, cvec, da, p.nch, dE, head, tail, cross, accumulate));
+    AMS_LAUNCH("pool_bwd_fix", st, pool_bwd_fix<DM><<<g, kThreads, 0, st>>>(D, p.nch, uniq_off, cross, head, tail, dE,
+                                                                          accumulate));
 }
 
 ams_status check_common(int32_t mode, int32_t B, int32_t D, int64_t n_beh)
@@ -443,5 +461,48 @@ extern "C" ams_status ams_pool_bwd(int32_t mode, int32_t B, int32_t D, const int
         if (small) AMS_POOL_BWD(AMS_POOL_ATT, 16); else AMS_POOL_BWD(AMS_POOL_ATT, 32);
     }
 #undef AMS_POOL_BWD
+    return ams_launch_status();
+}
+
+extern "C" ams_status ams_pool_query_fwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
+                                         const int32_t *inv, const float *E, const float *Q, float *U, float *w,
+                                         void *stream)
+{
+    ams_status s = check_common(AMS_POOL_ATT, B, D, n_beh);
+    if (s != AMS_OK) return s;
+    if (B == 0) return AMS_OK;
+    if (!seg_off || !inv || !E || !Q || !U || !w) return AMS_ERR_NULL;
+    hipStream_t st = (hipStream_t)stream;
+    if (D <= 16)
+        launch_fwd<kPoolQuery, 16>(B, D, seg_off, n_beh, inv, E, U, nullptr, w, st, Q);
+    else
+        launch_fwd<kPoolQuery, 32>(B, D, seg_off, n_beh, inv, E, U, nullptr, w, st, Q);
+    return ams_launch_status();
+}
+
+extern "C" ams_status ams_pool_query_bwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
+                                         const int32_t *inv, const int32_t *occ_perm, const int32_t *uniq_off,
+                                         const int32_t *n_uniq, int32_t n_uniq_cap, const float *E, const float *Q,
+                                         const float *U, const float *w, const float *dU, float *dQ, float *dE,
+                                         int32_t accumulate, void *ws, size_t ws_bytes, void *stream)
+{
+    ams_status s = check_common(AMS_POOL_ATT, B, D, n_beh);
+    if (s != AMS_OK) return s;
+    (void)n_uniq;
+    if (n_uniq_cap < 0) return AMS_ERR_SIZE;
+    const int64_t n_occ = n_beh + B;
+    if (n_occ == 0) return AMS_OK;
+    if (!seg_off || !inv || !occ_perm || !uniq_off || !E || !dE) return AMS_ERR_NULL;
+    if (B > 0 && (!Q || !U || !w || !dU || !dQ)) return AMS_ERR_NULL;
+    const PoolPlan p = plan_pool(B, n_beh, D);
+    if (!ws || ws_bytes < p.total) return AMS_ERR_WORKSPACE;
+    hipStream_t st = (hipStream_t)stream;
+    char *wsc = (char *)ws;
+    if (D <= 16)
+        launch_bwd<kPoolQuery, 16>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, Q, w, dU, nullptr, dE, wsc, p,
+                                   st, dQ, accumulate != 0);
+    else
+        launch_bwd<kPoolQuery, 32>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, Q, w, dU, nullptr, dE, wsc, p,
+                                   st, dQ, accumulate != 0);
     return ams_launch_status();
 }

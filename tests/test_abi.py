@@ -188,3 +188,18 @@ def test_joint_host_errors(lib):
     assert lib.ams_adagrad_rows(12, FAKE, FAKE, -1, FAKE, FAKE, 100, FAKE, 0.01, 1e-8, None) == SIZE
     assert lib.ams_adagrad_rows(12, FAKE, FAKE, 0, None, None, 100, None, 0.01, 1e-8, None) == OK
     assert lib.ams_adagrad_rows(12, FAKE, FAKE, 10, FAKE, None, 100, FAKE, 0.01, 1e-8, None) == NULL
+
+
+def test_query_pool_host_errors(lib):
+    f = [4, 12, FAKE, 40, FAKE, FAKE, None, FAKE, FAKE, None]
+    assert lib.ams_pool_query_fwd(*f) == NULL                # Q
+    a = list(f); a[1] = 33
+    assert lib.ams_pool_query_fwd(*a) == SIZE
+    a = list(f); a[0] = 0
+    assert lib.ams_pool_query_fwd(*a) == OK
+    b = [4, 12, FAKE, 40, FAKE, FAKE, FAKE, FAKE, 44, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, FAKE, 16, None]
+    assert lib.ams_pool_query_bwd(*b) == WS
+    a = list(b); a[14] = None                                 # dQ
+    assert lib.ams_pool_query_bwd(*a) == NULL
+    a = list(b); a[8] = -1
+    assert lib.ams_pool_query_bwd(*a) == SIZE
