@@ -45,6 +45,10 @@
  * The merged gradient of an ID row is the SUM aggregator's backward with the
  * bag gradient as upstream (orc_pool_bwd, mode SUM).
  *
+ *   adam       the dense update of the server's embedding model and the
+ *              worker's CTR model (Algorithm 1: update E, update W; section
+ *              7.2 trains with Adam): m = b1 m + (1-b1) g, v = b2 v + (1-b2) g^2,
+ *              p -= lr (m / (1-b1^t)) / (sqrt(v / (1-b2^t)) + eps).
  *   query pool one channel of the multiple-query attentive pooling of section
  *              5.2: attention over the behavior image embeddings with a query
  *              given per sample (the ad's ID embedding for the ID channel),
@@ -657,5 +661,21 @@ int orc_pool_query_bwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_b
     for (int64_t j = 0; j < n_beh; ++j)
         for (int d = 0; d < D; ++d) dE[(size_t)inv[j] * D + d] += ge[(size_t)j * D + d];
     free(ge);
+    return 0;
+}
+
+/* ------------------------------------------------------------------- Adam */
+
+/* One Adam step t >= 1 on n parameters, in place (all float64). */
+int orc_adam(int64_t n, double *param, const double *grad, double *m, double *v, double lr, double b1,
+             double b2, double eps, int64_t t)
+{
+    if (n < 0 || t < 1) return 1;
+    const double c1 = 1.0 - pow(b1, (double)t), c2 = 1.0 - pow(b2, (double)t);
+    for (int64_t i = 0; i < n; ++i) {
+        m[i] = b1 * m[i] + (1.0 - b1) * grad[i];
+        v[i] = b2 * v[i] + (1.0 - b2) * grad[i] * grad[i];
+        param[i] -= lr * (m[i] / c1) / (sqrt(v[i] / c2) + eps);
+    }
     return 0;
 }

@@ -58,6 +58,7 @@ def _load():
     lib.orc_adagrad_rows.argtypes = [i32, i32, P, ctypes.c_double, ctypes.c_double, P, P]
     lib.orc_pool_query_fwd.argtypes = [i32, i32, P, i64, P, P, P, P, P]
     lib.orc_pool_query_bwd.argtypes = [i32, i32, P, i64, P, i32, P, P, P, P, P, P, P]
+    lib.orc_adam.argtypes = [i64, P, P, P, P, ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double, i64]
     lib.orc_num_threads.restype = ctypes.c_int
     lib.orc_set_threads.argtypes = [ctypes.c_int]
     _lib = lib
@@ -428,3 +429,21 @@ def pool_query_bwd(seg_off, inv, n_uniq: int, E, Q, fwd: dict, gU) -> dict:
     _check(lib.orc_pool_query_bwd(B, D, _ptr(seg_off), n_beh, _ptr(inv), int(n_uniq), _ptr(E), _ptr(Q),
                                   _ptr(_f64(fwd["U"])), _ptr(w), _ptr(gU), _ptr(dE), _ptr(dQ)), "pool_query_bwd")
     return {"dE": dE[:n_uniq].copy(), "dQ": dQ[:B].copy()}
+
+
+# ------------------------------------------------------------- dense update
+
+def adam(param, grad, m, v, lr: float, t: int, b1: float = 0.9, b2: float = 0.999, eps: float = 1e-8):
+    """One Adam step (t >= 1) in float64; returns new (param, m, v)."""
+    lib = _load()
+    p, g = _f64(param).copy(), _f64(grad)
+    mm, vv = _f64(m).copy(), _f64(v).copy()
+    _check(lib.orc_adam(p.size, _ptr(p), _ptr(g), _ptr(mm), _ptr(vv), float(lr), float(b1), float(b2), float(eps),
+                        int(t)), "adam")
+    return p, mm, vv
+
+
+def paper_lr(step: int, lr0: float = 1e-3, decay: float = 0.9, every: int = 24000) -> float:
+    """Section 7.2: the learning rate starts at 1e-3 and is multiplied by 0.9
+    after every 24,000 batches (step counts from 1)."""
+    return lr0 * decay ** ((step - 1) // every)
