@@ -352,6 +352,21 @@ ams_status ams_adagrad_rows(int32_t D, const int32_t *uniq, const int32_t *n_uni
                             int64_t n_rows, float *accum, float lr, float eps,
                             void *stream);
 
+/* ------------------------------------------------------------- Adam -----
+ * The dense update (Algorithm 1: update E on the servers and W on the
+ * workers; section 7.2 trains with Adam).  For i < n, with g = grad[i]:
+ *   m[i] = b1 m[i] + (1 - b1) g;   v[i] = b2 v[i] + (1 - b2) g^2;
+ *   param[i] -= lr (m[i] / (1 - b1^t)) / (sqrt(v[i] / (1 - b2^t)) + eps)
+ * in float32, in place (device arrays of n floats); t >= 1 is the step
+ * number (host), lr the step's learning rate (section 7.2: 1e-3, times 0.9
+ * after every 24,000 batches; the schedule is the caller's).  param is the
+ * float32 master copy; param_bf16 (device, may be NULL) receives its
+ * round-to-nearest-even bf16 copy, the weights the bf16 kernels read.
+ * Host errors: SIZE (n < 0 or t < 1), NULL. */
+ams_status ams_adam_update(int64_t n, float *param, const float *grad, float *m, float *v,
+                           float lr, float b1, float b2, float eps, int64_t t,
+                           uint16_t *param_bf16, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

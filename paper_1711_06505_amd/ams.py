@@ -24,7 +24,8 @@ EXPORTS = ["ams_status_str", "ams_build_info", "ams_dedup_workspace", "ams_dedup
            "ams_embed_workspace", "ams_embed_fwd", "ams_embed_bwd", "ams_pool_fwd",
            "ams_pool_workspace", "ams_pool_bwd", "ams_timing_enable", "ams_timing_read",
            "ams_bag_fwd", "ams_bag_workspace", "ams_bag_bwd", "ams_ctr_workspace", "ams_ctr_fwd_bwd",
-           "ams_adagrad_rows", "ams_pool_query_fwd", "ams_pool_query_bwd"]
+           "ams_adagrad_rows", "ams_pool_query_fwd", "ams_pool_query_bwd",
+           "ams_adam_update"]
 
 
 class AmsError(RuntimeError):
@@ -97,6 +98,9 @@ def load() -> ctypes.CDLL:
     lib.ams_pool_query_fwd.argtypes = [i32, i32, P, i64, P, P, P, P, P, P]
     lib.ams_pool_query_bwd.restype = ctypes.c_int
     lib.ams_pool_query_bwd.argtypes = [i32, i32, P, i64, P, P, P, P, i32, P, P, P, P, P, P, P, i32, P, sz, P]
+    f = ctypes.c_float
+    lib.ams_adam_update.restype = ctypes.c_int
+    lib.ams_adam_update.argtypes = [i64, P, P, P, P, f, f, f, f, i64, P, P]
     lib.ams_timing_enable.restype = ctypes.c_int
     lib.ams_timing_enable.argtypes = [ctypes.c_int]
     lib.ams_timing_read.restype = ctypes.c_int
@@ -232,6 +236,12 @@ def ams_pool_query_bwd(seg_off, n_beh: int, inv, occ_perm, uniq_off, n_uniq, n_u
                                      _p(n_uniq), int(n_uniq_cap), _p(E), _p(Q), _p(U), _p(w), _p(dU), _p(dQ),
                                      _p(dE), int(bool(accumulate)), _p(ws), ws.numel() * ws.element_size(),
                                      _stream(stream)), "ams_pool_query_bwd")
+
+
+def ams_adam_update(param, grad, m, v, lr: float, t: int, b1: float = 0.9, b2: float = 0.999, eps: float = 1e-8,
+                    param_bf16=None, stream=None):
+    _check(load().ams_adam_update(param.numel(), _p(param), _p(grad), _p(m), _p(v), float(lr), float(b1), float(b2),
+                                  float(eps), int(t), _p(param_bf16), _stream(stream)), "ams_adam_update")
 
 
 def make_ctr(dims) -> ams_ctr:

@@ -451,6 +451,25 @@ __global__ __launch_bounds__(kThreads) void adagrad_k(int D, const int32_t *__re
     table[x] -= lr * g / (sqrtf(acc) + eps);
 }
 
+// ------------------------------------------------------------------- Adam
+
+__global__ __launch_bounds__(kThreads) void adam_k(int64_t n, float *__restrict__ param,
+                                                   const float *__restrict__ grad, float *__restrict__ m,
+                                                   float *__restrict__ v, float lr, float b1, float b2, float eps,
+                                                   float c1, float c2, uint16_t *__restrict__ pb)
+{
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kThreads) {
+        const float g = grad[i];
+        const float mi = b1 * m[i] + (1.f - b1) * g;
+        const float vi = b2 * v[i] + (1.f - b2) * g * g;
+        m[i] = mi;
+        v[i] = vi;
+        const float p = param[i] - lr * (mi / c1) / (sqrtf(vi / c2) + eps);
+        param[i] = p;
+        if (pb) pb[i] = ams_f32_to_bf16(p);
+    }
+}
+
 size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 bool ctr_ok(const ams_ctr *net)
@@ -568,5 +587,22 @@ extern "C" ams_status ams_adagrad_rows(int32_t D, const int32_t *uniq, const int
     const int64_t n = (int64_t)n_uniq_cap * D;
     AMS_LAUNCH("adagrad_rows", st, adagrad_k<<<(unsigned)((n + kThreads - 1) / kThreads), kThreads, 0, st>>>(
                                        D, uniq, n_uniq, n_uniq_cap, grad, table, n_rows, accum, lr, eps));
+    return ams_launch_status();
+}
+
+extern "C" ams_status ams_adam_update(int64_t n, float *param, const float *grad, float *m, float *v, float lr,
+                                      float b1, float b2, float eps, int64_t t, uint16_t *param_bf16, void *stream)
+{
+    if (n < 0 || t < 1) return AMS_ERR_SIZE;
+    if (n == 0) return AMS_OK;
+    if (!param || !grad || !m || !v) return AMS_ERR_NULL;
+    // bias corrections of step t, formed in double on the host
+    const float c1 = (float)(1.0 - pow((double)b1, (double)t));
+    const float c2 = (float)(1.0 - pow((double)b2, (double)t));
+    hipStream_t st = (hipStream_t)stream;
+    int64_t g = (n + kThreads - 1) / kThreads;
+    if (g > 4096) g = 4096;
+    AMS_LAUNCH("adam_update", st, adam_k<<<(unsigned)g, kThreads, 0, st>>>(n, param, grad, m, v, lr, b1, b2, eps, c1,
+                                                                          c2, param_bf16));
     return ams_launch_status();
 }

@@ -203,3 +203,10 @@ def test_query_pool_host_errors(lib):
     assert lib.ams_pool_query_bwd(*a) == NULL
     a = list(b); a[8] = -1
     assert lib.ams_pool_query_bwd(*a) == SIZE
+
+
+def test_adam_host_errors(lib):
+    assert lib.ams_adam_update(-1, FAKE, FAKE, FAKE, FAKE, 1e-3, 0.9, 0.999, 1e-8, 1, None, None) == SIZE
+    assert lib.ams_adam_update(10, FAKE, FAKE, FAKE, FAKE, 1e-3, 0.9, 0.999, 1e-8, 0, None, None) == SIZE
+    assert lib.ams_adam_update(10, FAKE, None, FAKE, FAKE, 1e-3, 0.9, 0.999, 1e-8, 1, None, None) == NULL
+    assert lib.ams_adam_update(0, None, None, None, None, 1e-3, 0.9, 0.999, 1e-8, 1, None, None) == OK
