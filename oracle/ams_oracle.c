@@ -56,6 +56,18 @@
  *              gives the behaviors' embedding gradients (merged per unique
  *              image) and the query gradient.
  *
+ *   concat     the concatenate aggregator of section 5.2: a sample's behavior
+ *              embeddings side by side, padded with zeros or truncated to a
+ *              fixed count; its backward hands each kept position its slice
+ *              of the upstream gradient, merged per unique image.
+ *   dense      a fully connected net with PReLU (a learnable slope per
+ *              channel, the activation of section 7.2) or ReLU between
+ *              layers, forward and backward from the last layer's gradient,
+ *              with the slopes' gradients.  With it the oracle's Python side
+ *              composes the CTR model with PReLU and the pre-rank model of
+ *              section 6: a user tower and an ad tower, the score their inner
+ *              product, the logistic loss with the click label.
+ *
  * Readings where the paper is silent (documented with the library): no
  * activation after the last layer unless final_relu is set; ReLU'(0) = 0;
  * the max-pool argmax is the first (lowest) position attaining the maximum;
@@ -677,5 +689,161 @@ int orc_adam(int64_t n, double *param, const double *grad, double *m, double *v,
         v[i] = b2 * v[i] + (1.0 - b2) * grad[i] * grad[i];
         param[i] -= lr * (m[i] / c1) / (sqrt(v[i] / c2) + eps);
     }
+    return 0;
+}
+
+/* --------------------------------------------------- concatenate aggregator */
+
+/*
+ * U [B x Lc*D]: sample i's first Lc behavior embeddings in list order, one
+ * after the other (U[i][p*D + d] = E[inv[seg_off[i] + p]][d]); positions past
+ * the sample's length are zero (pad), behaviors past Lc are dropped
+ * (truncate).  A [B x D]: the ad's embedding E[inv[n_beh + i]].
+ */
+int orc_pool_concat_fwd(int32_t B, int32_t D, int32_t Lc, const int32_t *seg_off, int64_t n_beh,
+                        const int32_t *inv, const double *E, double *U, double *A)
+{
+    if (B < 0 || D <= 0 || Lc < 1) return 1;
+    if (B > 0 && (seg_off[0] != 0 || seg_off[B] != n_beh)) return 1;
+    for (int32_t i = 0; i < B; ++i) {
+        const int64_t j0 = seg_off[i], n = seg_off[i + 1] - j0;
+        for (int32_t p = 0; p < Lc; ++p)
+            for (int d = 0; d < D; ++d)
+                U[((size_t)i * Lc + p) * D + d] = p < n ? E[(size_t)inv[j0 + p] * D + d] : 0.0;
+        for (int d = 0; d < D; ++d) A[(size_t)i * D + d] = E[(size_t)inv[n_beh + i] * D + d];
+    }
+    return 0;
+}
+
+/*
+ * Backward of orc_pool_concat_fwd for the loss sum(gU * U) + sum(gA * A)
+ * (gA may be NULL: zero).  Behavior j at position p of its sample i gets
+ * gU[i][p] if p < Lc and zero otherwise; the ad of sample i gets gA[i].
+ * dE [n_u x D] (overwritten): those summed per unique image in ascending
+ * occurrence order.
+ */
+int orc_pool_concat_bwd(int32_t B, int32_t D, int32_t Lc, const int32_t *seg_off, int64_t n_beh,
+                        const int32_t *inv, int32_t n_u, const double *gU, const double *gA, double *dE)
+{
+    if (B < 0 || D <= 0 || Lc < 1 || n_u < 0) return 1;
+    memset(dE, 0, sizeof(double) * (size_t)n_u * D);
+    int32_t i = 0;
+    for (int64_t k = 0; k < n_beh + B; ++k) {
+        double *o = dE + (size_t)inv[k] * D;
+        if (k < n_beh) {
+            while (seg_off[i + 1] <= k) ++i;
+            const int64_t p = k - seg_off[i];
+            if (p < Lc)
+                for (int d = 0; d < D; ++d) o[d] += gU[((size_t)i * Lc + p) * D + d];
+        } else if (gA) {
+            for (int d = 0; d < D; ++d) o[d] += gA[(size_t)(k - n_beh) * D + d];
+        }
+    }
+    return 0;
+}
+
+/* ------------------------------------------------- dense net with PReLU */
+
+/*
+ * A fully connected net dims[0] -> ... -> dims[L] on B rows X [B x dims[0]],
+ * float32 weights W[l] [dims[l+1] x dims[l]] and biases b[l], float64
+ * arithmetic: Z_l = H_{l-1} W_l^T + b_l with H_{-1} = X, and below the last
+ * layer H_l = act(Z_l) with act(z) = z for z > 0 and a z otherwise, a the
+ * layer's per-channel slope slope[l][o] (PReLU, the activation of section
+ * 7.2); slope == NULL or slope[l] == NULL means a = 0 (ReLU).  The last
+ * layer is linear.  Z (out): every layer's Z_l, concatenated.
+ */
+static double act_slope(const float *const *slope, int l, int o)
+{
+    return (slope && slope[l]) ? (double)slope[l][o] : 0.0;
+}
+
+int orc_dense_fwd(int32_t B, int L, const int32_t *dims, const float *const *W, const float *const *b,
+                  const float *const *slope, const double *X, double *Z)
+{
+    if (B < 0 || L < 1 || L > 15) return 1;
+    size_t zoff = 0;
+    for (int l = 0; l < L; ++l) {
+        const int in = dims[l], out = dims[l + 1];
+        const double *Zp = Z + zoff - (l > 0 ? (size_t)B * in : 0);
+        for (int32_t i = 0; i < B; ++i)
+            for (int o = 0; o < out; ++o) {
+                double acc = (double)b[l][o];
+                for (int k = 0; k < in; ++k) {
+                    double h;
+                    if (l == 0) h = X[(size_t)i * in + k];
+                    else {
+                        const double z = Zp[(size_t)i * in + k];
+                        h = z > 0.0 ? z : act_slope(slope, l - 1, k) * z;
+                    }
+                    acc += (double)W[l][(size_t)o * in + k] * h;
+                }
+                Z[zoff + (size_t)i * out + o] = acc;
+            }
+        zoff += (size_t)B * out;
+    }
+    return 0;
+}
+
+/*
+ * Backward of orc_dense_fwd from dZL [B x dims[L]], the gradient of the last
+ * layer's output: dW_l = sum_i dZ_l[i]^T H_{l-1}[i] and db_l = sum_i dZ_l[i]
+ * (ascending i); dH_{l-1} = dZ_l W_l; dZ_{l-1} = dH_{l-1} act'(Z_{l-1}) with
+ * act'(z) = 1 for z > 0 and a otherwise (ReLU'(0) = 0); the slope gradient
+ * dslope_{l-1}[k] = sum_i dH_{l-1}[i][k] min(Z_{l-1}[i][k], 0); dX = dZ_0 W_0.
+ * dW, db, dslope (the hidden layers' widths) are concatenated per layer.
+ */
+int orc_dense_bwd(int32_t B, int L, const int32_t *dims, const float *const *W, const float *const *slope,
+                  const double *X, const double *Z, const double *dZL, double *dW, double *db,
+                  double *dslope, double *dX)
+{
+    if (B < 0 || L < 1 || L > 15) return 1;
+    size_t zoff[16], woff[16], boff[16], soff[16];
+    zoff[0] = woff[0] = boff[0] = soff[0] = 0;
+    for (int l = 0; l < L; ++l) {
+        zoff[l + 1] = zoff[l] + (size_t)B * dims[l + 1];
+        woff[l + 1] = woff[l] + (size_t)dims[l] * dims[l + 1];
+        boff[l + 1] = boff[l] + (size_t)dims[l + 1];
+        soff[l + 1] = soff[l] + (l < L - 1 ? (size_t)dims[l + 1] : 0);
+    }
+    double *dZ = (double *)malloc(sizeof(double) * (zoff[L] > 0 ? zoff[L] : 1));
+    memcpy(dZ + zoff[L - 1], dZL, sizeof(double) * (size_t)B * dims[L]);
+    for (int l = L - 1; l >= 0; --l) {
+        const int in = dims[l], out = dims[l + 1];
+        const double *dz = dZ + zoff[l];
+        for (int o = 0; o < out; ++o) {
+            double bs = 0.0;
+            for (int k = 0; k < in; ++k) dW[woff[l] + (size_t)o * in + k] = 0.0;
+            for (int32_t i = 0; i < B; ++i) {
+                const double g = dz[(size_t)i * out + o];
+                bs += g;
+                for (int k = 0; k < in; ++k) {
+                    double h;
+                    if (l == 0) h = X[(size_t)i * in + k];
+                    else {
+                        const double z = Z[zoff[l - 1] + (size_t)i * in + k];
+                        h = z > 0.0 ? z : act_slope(slope, l - 1, k) * z;
+                    }
+                    dW[woff[l] + (size_t)o * in + k] += g * h;
+                }
+            }
+            db[boff[l] + o] = bs;
+        }
+        if (l > 0)
+            for (int k = 0; k < in; ++k) dslope[soff[l - 1] + k] = 0.0;
+        for (int32_t i = 0; i < B; ++i)
+            for (int k = 0; k < in; ++k) {
+                double dh = 0.0;
+                for (int o = 0; o < out; ++o) dh += dz[(size_t)i * out + o] * (double)W[l][(size_t)o * in + k];
+                if (l == 0) {
+                    dX[(size_t)i * in + k] = dh;
+                } else {
+                    const double z = Z[zoff[l - 1] + (size_t)i * in + k];
+                    dZ[zoff[l - 1] + (size_t)i * in + k] = z > 0.0 ? dh : act_slope(slope, l - 1, k) * dh;
+                    if (!(z > 0.0)) dslope[soff[l - 1] + k] += dh * z;
+                }
+            }
+    }
+    free(dZ);
     return 0;
 }

@@ -59,6 +59,10 @@ def _load():
     lib.orc_pool_query_fwd.argtypes = [i32, i32, P, i64, P, P, P, P, P]
     lib.orc_pool_query_bwd.argtypes = [i32, i32, P, i64, P, i32, P, P, P, P, P, P, P]
     lib.orc_adam.argtypes = [i64, P, P, P, P, ctypes.c_double, ctypes.c_double, ctypes.c_double, ctypes.c_double, i64]
+    lib.orc_pool_concat_fwd.argtypes = [i32, i32, i32, P, i64, P, P, P, P]
+    lib.orc_pool_concat_bwd.argtypes = [i32, i32, i32, P, i64, P, i32, P, P, P]
+    lib.orc_dense_fwd.argtypes = [i32, ctypes.c_int, P, P, P, P, P, P]
+    lib.orc_dense_bwd.argtypes = [i32, ctypes.c_int, P, P, P, P, P, P, P, P, P, P]
     lib.orc_num_threads.restype = ctypes.c_int
     lib.orc_set_threads.argtypes = [ctypes.c_int]
     _lib = lib
@@ -447,3 +451,132 @@ def paper_lr(step: int, lr0: float = 1e-3, decay: float = 0.9, every: int = 2400
     """Section 7.2: the learning rate starts at 1e-3 and is multiplied by 0.9
     after every 24,000 batches (step counts from 1)."""
     return lr0 * decay ** ((step - 1) // every)
+
+
+# ------------------------------------------------- concatenate aggregator
+
+def pool_concat_fwd(seg_off, inv, E, Lc: int) -> dict:
+    """U [B x Lc*D]: the first Lc behavior embeddings side by side (zero
+    padded); A: the ads' embeddings."""
+    lib = _load()
+    seg_off, inv, E = _i32(seg_off), _i32(inv), _f64(E)
+    B, D = seg_off.size - 1, E.shape[1]
+    n_beh = int(seg_off[-1])
+    U = np.zeros((max(B, 1), Lc * D))
+    A = np.zeros((max(B, 1), D))
+    _check(lib.orc_pool_concat_fwd(B, D, int(Lc), _ptr(seg_off), n_beh, _ptr(inv), _ptr(E), _ptr(U), _ptr(A)),
+           "pool_concat_fwd")
+    return {"U": U[:B].copy(), "A": A[:B].copy()}
+
+
+def pool_concat_bwd(seg_off, inv, n_uniq: int, D: int, Lc: int, gU, gA=None) -> np.ndarray:
+    """dE [n_u x D]: each kept position's slice of gU (and gA for the ads),
+    merged per unique image in ascending occurrence order."""
+    lib = _load()
+    seg_off, inv = _i32(seg_off), _i32(inv)
+    B = seg_off.size - 1
+    n_beh = int(seg_off[-1])
+    gU = _f64(gU).reshape(B, Lc * D) if B else np.zeros((1, Lc * D))
+    gA = _f64(gA) if gA is not None else None
+    dE = np.zeros((max(n_uniq, 1), D))
+    _check(lib.orc_pool_concat_bwd(B, D, int(Lc), _ptr(seg_off), n_beh, _ptr(inv), int(n_uniq), _ptr(gU),
+                                   _ptr(gA), _ptr(dE)), "pool_concat_bwd")
+    return dE[:n_uniq].copy()
+
+
+# ------------------------------------------- dense nets with PReLU, pre-rank
+
+def _ptr_list(xs):
+    return (ctypes.c_void_p * len(xs))(*[None if x is None else x.ctypes.data for x in xs])
+
+
+def dense_fwd(X, Ws, bs, slopes=None) -> list:
+    """Z of every layer of a fully connected net (PReLU with per-channel
+    slopes between layers, ReLU where a slope is None, last layer linear)."""
+    lib = _load()
+    X = _f64(X)
+    Wn, bn = _f32list(Ws), _f32list(bs)
+    L = len(Wn)
+    dims = [Wn[0].shape[1]] + [W.shape[0] for W in Wn]
+    sl = [None] * L if slopes is None else [None if s is None else _f32list([s])[0] for s in slopes] + [None]
+    B = X.shape[0]
+    Z = np.zeros(max(sum(B * d for d in dims[1:]), 1))
+    _check(lib.orc_dense_fwd(B, L, _ptr(np.array(dims, np.int32)), _ptr_list(Wn), _ptr_list(bn), _ptr_list(sl[:L]),
+                             _ptr(X), _ptr(Z)), "dense_fwd")
+    out, o = [], 0
+    for d in dims[1:]:
+        out.append(Z[o:o + B * d].reshape(B, d).copy())
+        o += B * d
+    return out
+
+
+def dense_bwd(X, Ws, slopes, Z: list, dZL) -> dict:
+    """dW, db, dslope (one per hidden layer) and dX of dense_fwd's net."""
+    lib = _load()
+    X = _f64(X)
+    Wn = _f32list(Ws)
+    L = len(Wn)
+    dims = [Wn[0].shape[1]] + [W.shape[0] for W in Wn]
+    sl = [None] * L if slopes is None else [None if s is None else _f32list([s])[0] for s in slopes] + [None]
+    B = X.shape[0]
+    Zc = np.ascontiguousarray(np.concatenate([np.asarray(z, np.float64).ravel() for z in Z]))
+    dW = np.zeros(sum(a * b for a, b in zip(dims[:-1], dims[1:])))
+    db = np.zeros(sum(dims[1:]))
+    ds = np.zeros(max(sum(dims[1:-1]), 1))
+    dX = np.zeros_like(X)
+    _check(lib.orc_dense_bwd(B, L, _ptr(np.array(dims, np.int32)), _ptr_list(Wn), _ptr_list(sl[:L]), _ptr(X),
+                             _ptr(Zc), _ptr(_f64(dZL)), _ptr(dW), _ptr(db), _ptr(ds), _ptr(dX)), "dense_bwd")
+    dWs, dbs, dss = [], [], []
+    ow = ob = os_ = 0
+    for l, (fi, fo) in enumerate(zip(dims[:-1], dims[1:])):
+        dWs.append(dW[ow:ow + fi * fo].reshape(fo, fi).copy())
+        dbs.append(db[ob:ob + fo].copy())
+        ow += fi * fo
+        ob += fo
+        if l < L - 1:
+            dss.append(ds[os_:os_ + fo].copy())
+            os_ += fo
+    return {"dW": dWs, "db": dbs, "dslope": dss, "dX": dX}
+
+
+def ctr_act_fwd_bwd(X, labels, Ws, bs, slopes=None) -> dict:
+    """The CTR model with PReLU (or ReLU) between layers: softmax over the
+    classes, cross-entropy summed over the samples whose label is a class and
+    divided by B (others add nothing); its gradients, slopes' included."""
+    labels = np.asarray(labels, np.int64)
+    Z = dense_fwd(X, Ws, bs, slopes)
+    z = Z[-1]
+    B, C = z.shape
+    m = z.max(axis=1, keepdims=True)
+    lse = m[:, 0] + np.log(np.exp(z - m).sum(axis=1))
+    prob = np.exp(z - lse[:, None])
+    ok = (labels >= 0) & (labels < C)
+    y = np.where(ok, labels, 0)
+    loss = float(np.where(ok, lse - z[np.arange(B), y], 0.0).sum() / B)
+    dz = (prob - np.eye(C)[y]) / B
+    dz[~ok] = 0.0
+    g = dense_bwd(X, Ws, slopes, Z, dz)
+    return {"loss": loss, "prob": prob, "Z": Z, **g}
+
+
+def dssm_fwd_bwd(Xu, Xa, labels, user, ad) -> dict:
+    """Pre-rank model of section 6: user tower on Xu, ad tower on Xa (each
+    ``(Ws, bs, slopes)``, equal output widths), score s = <u, a>, click
+    probability sigmoid(s), logistic loss softplus(s) - y s summed over the
+    samples with y in {0, 1} and divided by B; gradients of both towers and
+    of both inputs."""
+    labels = np.asarray(labels, np.int64)
+    Zu = dense_fwd(Xu, *user)
+    Za = dense_fwd(Xa, *ad)
+    u, a = Zu[-1], Za[-1]
+    B = u.shape[0]
+    s = (u * a).sum(axis=1)
+    prob = 1.0 / (1.0 + np.exp(-s))
+    ok = (labels == 0) | (labels == 1)
+    y = np.where(ok, labels, 0).astype(np.float64)
+    softplus = np.maximum(s, 0.0) + np.log1p(np.exp(-np.abs(s)))
+    loss = float(np.where(ok, softplus - y * s, 0.0).sum() / B)
+    dS = np.where(ok, (prob - y) / B, 0.0)
+    gu = dense_bwd(Xu, user[0], user[2], Zu, dS[:, None] * a)
+    ga = dense_bwd(Xa, ad[0], ad[2], Za, dS[:, None] * u)
+    return {"loss": loss, "prob": prob, "score": s, "u": u, "a": a, "user": gu, "ad": ga}

@@ -3,7 +3,7 @@ Algorithm 1, trained with Adam in section 7.2) through the C ABI against the
 float64 oracle.  Each step is checked on the GPU's own float32 state: the
 oracle takes the GPU's parameters and moments before the step, and the move
 of the parameters, m and v are compared after it.  Sizes: one element, a
-ragged 257, the image model's 1,065,804 parameters (4096-256-64-12 weights
+ragged 257, the image model's 1,066,060 parameters (4096-256-64-12 weights
 and biases), and 2^21 + 77 (past one pass of the grid-stride loop).  The
 bf16 copy must be bit-exact: round-to-nearest-even of the float32 result."""
 import numpy as np
