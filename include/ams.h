@@ -267,6 +267,30 @@ ams_status ams_pool_query_bwd(int32_t B, int32_t D, const int32_t *seg_off, int6
                               float *dQ, float *dE, int32_t accumulate,
                               void *ws, size_t ws_bytes, void *stream);
 
+/* -------------------------------------------------- concat pooling ----
+ * The concatenate aggregator (section 5.2): a sample's behavior embeddings
+ * side by side, padded or truncated to Lc of them.
+ *
+ * fwd:  U [B x Lc*D] out: U[i][p*D + d] = E[inv[seg_off[i] + p]][d] for the
+ *       first Lc behaviors of sample i in list order, zero for positions
+ *       past its length; later behaviors are dropped.  A [B x D] out: the
+ *       ad's embedding E[inv[n_beh + i]].  Lc >= 1, Lc * D <= INT32_MAX.
+ * bwd:  dU [B x Lc*D], dA [B x D] (NULL = zero) the loss gradients of U and
+ *       A.  The behavior at position p of sample i gets dU[i][p*D .. p*D+D)
+ *       when p < Lc and nothing otherwise; the ad of sample i gets dA[i].
+ *       dE [cap x D] (overwritten for u < n_u): their sums per unique image
+ *       in ascending occurrence order, as ams_pool_bwd merges them.
+ *       ws: at least ams_pool_workspace(AMS_POOL_SUM, B, n_beh, D, cap).
+ * Other arguments and host errors as ams_pool_fwd / ams_pool_bwd. */
+ams_status ams_pool_concat_fwd(int32_t B, int32_t D, int32_t Lc, const int32_t *seg_off,
+                               int64_t n_beh, const int32_t *inv, const float *E,
+                               float *U, float *A, void *stream);
+ams_status ams_pool_concat_bwd(int32_t B, int32_t D, int32_t Lc, const int32_t *seg_off,
+                               int64_t n_beh, const int32_t *inv, const int32_t *occ_perm,
+                               const int32_t *uniq_off, const int32_t *n_uniq,
+                               int32_t n_uniq_cap, const float *dU, const float *dA,
+                               float *dE, void *ws, size_t ws_bytes, void *stream);
+
 /* =================================================== joint step (worker) ====
  * The worker side of a joint training step (Algorithm 1, WORKERITERATION):
  * sparse ID features embedded from key-value tables (section 4.1) next to the

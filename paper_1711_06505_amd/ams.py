@@ -25,7 +25,7 @@ EXPORTS = ["ams_status_str", "ams_build_info", "ams_dedup_workspace", "ams_dedup
            "ams_pool_workspace", "ams_pool_bwd", "ams_timing_enable", "ams_timing_read",
            "ams_bag_fwd", "ams_bag_workspace", "ams_bag_bwd", "ams_ctr_workspace", "ams_ctr_fwd_bwd",
            "ams_adagrad_rows", "ams_pool_query_fwd", "ams_pool_query_bwd",
-           "ams_adam_update"]
+           "ams_adam_update", "ams_pool_concat_fwd", "ams_pool_concat_bwd"]
 
 
 class AmsError(RuntimeError):
@@ -98,6 +98,10 @@ def load() -> ctypes.CDLL:
     lib.ams_pool_query_fwd.argtypes = [i32, i32, P, i64, P, P, P, P, P, P]
     lib.ams_pool_query_bwd.restype = ctypes.c_int
     lib.ams_pool_query_bwd.argtypes = [i32, i32, P, i64, P, P, P, P, i32, P, P, P, P, P, P, P, i32, P, sz, P]
+    lib.ams_pool_concat_fwd.restype = ctypes.c_int
+    lib.ams_pool_concat_fwd.argtypes = [i32, i32, i32, P, i64, P, P, P, P, P]
+    lib.ams_pool_concat_bwd.restype = ctypes.c_int
+    lib.ams_pool_concat_bwd.argtypes = [i32, i32, i32, P, i64, P, P, P, P, i32, P, P, P, P, sz, P]
     f = ctypes.c_float
     lib.ams_adam_update.restype = ctypes.c_int
     lib.ams_adam_update.argtypes = [i64, P, P, P, P, f, f, f, f, i64, P, P]
@@ -242,6 +246,20 @@ def ams_adam_update(param, grad, m, v, lr: float, t: int, b1: float = 0.9, b2: f
                     param_bf16=None, stream=None):
     _check(load().ams_adam_update(param.numel(), _p(param), _p(grad), _p(m), _p(v), float(lr), float(b1), float(b2),
                                   float(eps), int(t), _p(param_bf16), _stream(stream)), "ams_adam_update")
+
+
+def ams_pool_concat_fwd(Lc: int, seg_off, n_beh: int, inv, E, U, A, stream=None):
+    B, D = seg_off.numel() - 1, E.shape[1]
+    _check(load().ams_pool_concat_fwd(B, D, int(Lc), _p(seg_off), int(n_beh), _p(inv), _p(E), _p(U), _p(A),
+                                      _stream(stream)), "ams_pool_concat_fwd")
+
+
+def ams_pool_concat_bwd(Lc: int, seg_off, n_beh: int, inv, occ_perm, uniq_off, n_uniq, n_uniq_cap: int, dU, dA,
+                        dE, ws, stream=None):
+    B, D = seg_off.numel() - 1, dE.shape[1]
+    _check(load().ams_pool_concat_bwd(B, D, int(Lc), _p(seg_off), int(n_beh), _p(inv), _p(occ_perm), _p(uniq_off),
+                                      _p(n_uniq), int(n_uniq_cap), _p(dU), _p(dA), _p(dE), _p(ws),
+                                      ws.numel() * ws.element_size(), _stream(stream)), "ams_pool_concat_bwd")
 
 
 def make_ctr(dims) -> ams_ctr:

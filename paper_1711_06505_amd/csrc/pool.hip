@@ -28,6 +28,10 @@ constexpr int kWaves = kThreads / AMS_WAVE;
 // ads' occurrences get no gradient from it and the attention term
 // sum_j ds_j e_j is the query's gradient.
 constexpr int kPoolQuery = 3;
+// Internal mode: the concatenate aggregator's backward (section 5.2).  The
+// behavior at position p of sample i takes row p of the sample's upstream
+// block dU[i] ([Lc x D]) when p < Lc and nothing otherwise; an ad takes dA.
+constexpr int kPoolConcat = 4;
 
 template <int DM>
 __device__ __forceinline__ void load_row(const float *__restrict__ E, int row, int D, float (&e)[DM])
@@ -140,6 +144,32 @@ __global__ __launch_bounds__(kThreads) void pool_fwd_k(int B, int D, const int32
     if (lane < D) U[(size_t)i * D + lane] = mine;
 }
 
+// Concatenate aggregator: U[i] = the embeddings of sample i's first Lc
+// behaviors side by side (zero rows past its length), A[i] = its ad's.  One
+// thread per output element, grid-stride: the writes are contiguous, the
+// embedding rows come from L2.
+__global__ __launch_bounds__(kThreads) void pool_concat_fwd_k(int B, int D, int Lc,
+                                                              const int32_t *__restrict__ seg_off, int64_t n_beh,
+                                                              const int32_t *__restrict__ inv,
+                                                              const float *__restrict__ E, float *__restrict__ U,
+                                                              float *__restrict__ A)
+{
+    const int64_t row = (int64_t)Lc * D, nU = (int64_t)B * row, n = nU + (int64_t)B * D;
+    for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < n; e += (int64_t)gridDim.x * kThreads) {
+        if (e < nU) {
+            const int i = (int)(e / row);
+            const int r = (int)(e - (int64_t)i * row);
+            const int p = r / D, d = r - p * D;
+            const int j0 = seg_off[i], len = seg_off[i + 1] - j0;
+            U[e] = p < len ? E[(size_t)inv[j0 + p] * D + d] : 0.f;
+        } else {
+            const int64_t x = e - nU;
+            const int i = (int)(x / D), d = (int)(x - (int64_t)i * D);
+            A[x] = E[(size_t)inv[n_beh + i] * D + d];
+        }
+    }
+}
+
 // (1) per sample: tag occurrences with their sample; attention terms
 // c_i = g_i . u_i and da_i = sum_j ds_j e_j, ds_j = w_j (g_i . e_j - c_i).
 template <int MODE, int DM>
@@ -205,7 +235,8 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int64_t n_beh, i
                                                          float *__restrict__ dE,
                                                          float *__restrict__ head_part,
                                                          float *__restrict__ tail_part,
-                                                         int32_t *__restrict__ cross, int accumulate)
+                                                         int32_t *__restrict__ cross, int accumulate,
+                                                         const int32_t *__restrict__ seg_off, int Lc)
 {
     const int lane = ams_lane();
     const int ch = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
@@ -223,10 +254,13 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int64_t n_beh, i
         if (k < n_beh) {
             const int i = samp[k];
             float g[DM];
-            load_row<DM>(dU, i, D, g);
+            if (MODE != kPoolConcat) load_row<DM>(dU, i, D, g);
             if (MODE == AMS_POOL_SUM) {
 #pragma unroll
                 for (int d = 0; d < DM; ++d) v[d] = g[d];
+            } else if (MODE == kPoolConcat) {
+                const int pos = k - seg_off[i];
+                if (pos < Lc) load_row<DM>(dU + (size_t)i * Lc * D, pos, D, v);
             } else if (MODE == AMS_POOL_MAX) {
                 const int32_t *am = (const int32_t *)saved + (size_t)i * D;
 #pragma unroll
@@ -364,7 +398,8 @@ template <int MODE, int DM>
 void launch_bwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32_t *inv,
                 const int32_t *occ_perm, const int32_t *uniq_off, const float *E, const float *U,
                 const float *A, const void *saved, const float *dU, const float *dA, float *dE,
-                char *ws, const PoolPlan &p, hipStream_t st, float *dQ = nullptr, int accumulate = 0)
+                char *ws, const PoolPlan &p, hipStream_t st, float *dQ = nullptr, int accumulate = 0,
+                int Lc = 0)
 {
     int32_t *samp = (int32_t *)(ws + p.off_samp);
     float *cvec = (float *)(ws + p.off_c);
@@ -379,7 +414,8 @@ void launch_bwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32
             B, D, seg_off, inv, E, U, (const float *)saved, dU, samp, cvec, da));
     const int g = (p.nch + kWaves - 1) / kWaves;
     AMS_LAUNCH("pool_bwd_seg", st, pool_bwd_seg<MODE, DM><<<g, kThreads, 0, st>>>(D, n_beh, n_occ, inv, occ_perm, uniq_off, E, A, saved, dU,
-                                                   dA, samp, cvec, da, p.nch, dE, head, tail, cross, accumulate));
+                                                   dA, samp, cvec, da, p.nch, dE, head, tail, cross, accumulate,
+                                                   seg_off, Lc));
     AMS_LAUNCH("pool_bwd_fix", st, pool_bwd_fix<DM><<<g, kThreads, 0, st>>>(D, p.nch, uniq_off, cross, head, tail, dE,
                                                                           accumulate));
 }
@@ -504,5 +540,48 @@ extern "C" ams_status ams_pool_query_bwd(int32_t B, int32_t D, const int32_t *se
     else
         launch_bwd<kPoolQuery, 32>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, Q, w, dU, nullptr, dE, wsc, p,
                                    st, dQ, accumulate != 0);
+    return ams_launch_status();
+}
+
+extern "C" ams_status ams_pool_concat_fwd(int32_t B, int32_t D, int32_t Lc, const int32_t *seg_off, int64_t n_beh,
+                                          const int32_t *inv, const float *E, float *U, float *A, void *stream)
+{
+    ams_status s = check_common(AMS_POOL_SUM, B, D, n_beh);
+    if (s != AMS_OK) return s;
+    if (Lc < 1 || (int64_t)Lc * D > INT32_MAX) return AMS_ERR_SIZE;
+    if (B == 0) return AMS_OK;
+    if (!seg_off || !inv || !E || !U || !A) return AMS_ERR_NULL;
+    hipStream_t st = (hipStream_t)stream;
+    const int64_t n = (int64_t)B * ((int64_t)Lc * D + D);
+    int64_t g = (n + kThreads - 1) / kThreads;
+    if (g > 8192) g = 8192;
+    AMS_LAUNCH("pool_concat_fwd", st, pool_concat_fwd_k<<<(unsigned)g, kThreads, 0, st>>>(B, D, Lc, seg_off, n_beh, inv,
+                                                                                          E, U, A));
+    return ams_launch_status();
+}
+
+extern "C" ams_status ams_pool_concat_bwd(int32_t B, int32_t D, int32_t Lc, const int32_t *seg_off, int64_t n_beh,
+                                          const int32_t *inv, const int32_t *occ_perm, const int32_t *uniq_off,
+                                          const int32_t *n_uniq, int32_t n_uniq_cap, const float *dU,
+                                          const float *dA, float *dE, void *ws, size_t ws_bytes, void *stream)
+{
+    ams_status s = check_common(AMS_POOL_SUM, B, D, n_beh);
+    if (s != AMS_OK) return s;
+    (void)n_uniq;
+    if (n_uniq_cap < 0 || Lc < 1 || (int64_t)Lc * D > INT32_MAX) return AMS_ERR_SIZE;
+    const int64_t n_occ = n_beh + B;
+    if (n_occ == 0) return AMS_OK;
+    if (!seg_off || !inv || !occ_perm || !uniq_off || !dE) return AMS_ERR_NULL;
+    if (B > 0 && !dU) return AMS_ERR_NULL;
+    const PoolPlan p = plan_pool(B, n_beh, D);
+    if (!ws || ws_bytes < p.total) return AMS_ERR_WORKSPACE;
+    hipStream_t st = (hipStream_t)stream;
+    char *w = (char *)ws;
+    if (D <= 16)
+        launch_bwd<kPoolConcat, 16>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, nullptr, nullptr, nullptr, nullptr,
+                                    dU, dA, dE, w, p, st, nullptr, 0, Lc);
+    else
+        launch_bwd<kPoolConcat, 32>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, nullptr, nullptr, nullptr, nullptr,
+                                    dU, dA, dE, w, p, st, nullptr, 0, Lc);
     return ams_launch_status();
 }

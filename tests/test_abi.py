@@ -210,3 +210,20 @@ def test_adam_host_errors(lib):
     assert lib.ams_adam_update(10, FAKE, FAKE, FAKE, FAKE, 1e-3, 0.9, 0.999, 1e-8, 0, None, None) == SIZE
     assert lib.ams_adam_update(10, FAKE, None, FAKE, FAKE, 1e-3, 0.9, 0.999, 1e-8, 1, None, None) == NULL
     assert lib.ams_adam_update(0, None, None, None, None, 1e-3, 0.9, 0.999, 1e-8, 1, None, None) == OK
+
+
+def test_concat_pool_host_errors(lib):
+    f = [4, 12, 5, FAKE, 40, FAKE, FAKE, FAKE, None, None]
+    assert lib.ams_pool_concat_fwd(*f) == NULL                # A
+    a = list(f); a[2] = 0
+    assert lib.ams_pool_concat_fwd(*a) == SIZE                # Lc
+    a = list(f); a[1] = 33
+    assert lib.ams_pool_concat_fwd(*a) == SIZE
+    a = list(f); a[0] = 0
+    assert lib.ams_pool_concat_fwd(*a) == OK
+    b = [4, 12, 5, FAKE, 40, FAKE, FAKE, FAKE, FAKE, 44, FAKE, None, FAKE, FAKE, 16, None]
+    assert lib.ams_pool_concat_bwd(*b) == WS
+    a = list(b); a[10] = None                                 # dU
+    assert lib.ams_pool_concat_bwd(*a) == NULL
+    a = list(b); a[2] = -3
+    assert lib.ams_pool_concat_bwd(*a) == SIZE
