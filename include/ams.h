@@ -330,10 +330,12 @@ ams_status ams_bag_bwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_b
 
 /* ------------------------------------------------------------- CTR -----
  * The CTR MLP (the basic net's MLP, section 3.2): dims[0] inputs (the
- * concatenated fields), ReLU between layers, dims[n_layers] = C classes,
- * softmax and cross-entropy with the labels, averaged over the B samples.
- * Supported: n_layers 2 or 3; dims[0] <= 128; hidden widths <= 256;
- * 2 <= C <= 8; 1..8 input fields.  float32 throughout. */
+ * concatenated fields), ReLU or PReLU between layers (section 7.2: PReLU,
+ * z for z > 0 and a z otherwise with a learnable slope a per channel),
+ * dims[n_layers] = C classes, softmax and cross-entropy with the labels,
+ * averaged over the B samples.  Supported: n_layers 2 or 3; dims[0] <= 128;
+ * hidden widths <= 256; 2 <= C <= 8; 1..8 input fields; widths whose
+ * activations fit the block's LDS (DIMS otherwise).  float32 throughout. */
 typedef struct {
     int32_t n_layers;
     int32_t dims[4];
@@ -346,9 +348,15 @@ typedef struct {
  *   labels      [B] int32 in [0, C) (device); a sample whose label is outside
  *               that range adds nothing to the loss or to any gradient;
  *   W[l], b[l]  [dims[l+1] x dims[l]] and [dims[l+1]] float32 (device);
+ *   slope       NULL (ReLU everywhere) or, for each layer l < n_layers-1,
+ *               the PReLU slopes [dims[l+1]] of its activation (device;
+ *               an entry NULL: ReLU there); ReLU'(0) = 0, PReLU'(0) = a;
  *   loss        [1] out: mean cross-entropy over the B samples (device);
  *   prob        [B x C] out, softmax probabilities (device, may be NULL);
  *   dW[l], db[l] out: gradients of the mean loss, overwritten (device);
+ *   dslope      NULL or per hidden layer the slope gradient [dims[l+1]]
+ *               (device, out; written where that layer has slopes):
+ *               sum over samples of dH * min(Z, 0), Z the pre-activation;
  *   dfields     gradients of the mean loss w.r.t. each field, [B x
  *               field_dims[f]] (device); dfields itself or any entry may be
  *               NULL (not written).
@@ -359,9 +367,42 @@ size_t ams_ctr_workspace(const ams_ctr *net, int32_t B);
 ams_status ams_ctr_fwd_bwd(const ams_ctr *net, int32_t B, int32_t n_fields,
                            const float *const *fields, const int32_t *field_dims,
                            const int32_t *labels, const float *const *W,
-                           const float *const *b, float *loss, float *prob,
-                           float *const *dW, float *const *db, float *const *dfields,
+                           const float *const *b, const float *const *slope,
+                           float *loss, float *prob, float *const *dW, float *const *db,
+                           float *const *dslope, float *const *dfields,
                            void *ws, size_t ws_bytes, void *stream);
+
+/* --------------------------------------------------------- pre-rank ----
+ * The pre-rank model of section 6: a user tower and an ad tower, each a
+ * net of the CTR kind (ams_ctr: 1 to 3 layers, ReLU or PReLU between them,
+ * the last layer linear) on its own fields, with outputs of equal width R
+ * (1..64), the user and ad representations; the score of a sample is
+ * their inner product s = <u, a>, its click probability sigmoid(s).  The
+ * loss is softplus(s) - y s (the logistic loss) for labels y in {0, 1},
+ * summed over the samples and divided by B; a sample with another label
+ * adds nothing to the loss or any gradient.  The behavior images enter the
+ * user tower sum-pooled (ams_pool_fwd, AMS_POOL_SUM) and the ad image the
+ * ad tower; the input-field gradients carry delta_e back to them.
+ * Per tower, arguments as ams_ctr_fwd_bwd's (u: user, a: ad): fields and
+ * field_dims, W, b, slope, and the outputs dW, db, dslope, dfields.
+ * prob [B] out (may be NULL): sigmoid(s) of every sample, labels aside.
+ * ws: at least ams_dssm_workspace(user_net, ad_net, B) bytes.
+ * Host errors: NULL, DIMS (widths, or R unequal), SIZE (B < 1), WORKSPACE. */
+size_t ams_dssm_workspace(const ams_ctr *user_net, const ams_ctr *ad_net, int32_t B);
+ams_status ams_dssm_fwd_bwd(const ams_ctr *user_net, const ams_ctr *ad_net, int32_t B,
+                            int32_t n_user_fields, const float *const *user_fields,
+                            const int32_t *user_field_dims, int32_t n_ad_fields,
+                            const float *const *ad_fields, const int32_t *ad_field_dims,
+                            const int32_t *labels,
+                            const float *const *Wu, const float *const *bu,
+                            const float *const *slope_u,
+                            const float *const *Wa, const float *const *ba,
+                            const float *const *slope_a,
+                            float *loss, float *prob,
+                            float *const *dWu, float *const *dbu, float *const *dslope_u,
+                            float *const *dWa, float *const *dba, float *const *dslope_a,
+                            float *const *duser_fields, float *const *dad_fields,
+                            void *ws, size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------- Adagrad ----
  * Sparse Adagrad on the touched rows of an ID table, in place: for u < n_u

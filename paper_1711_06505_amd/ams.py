@@ -25,7 +25,8 @@ EXPORTS = ["ams_status_str", "ams_build_info", "ams_dedup_workspace", "ams_dedup
            "ams_pool_workspace", "ams_pool_bwd", "ams_timing_enable", "ams_timing_read",
            "ams_bag_fwd", "ams_bag_workspace", "ams_bag_bwd", "ams_ctr_workspace", "ams_ctr_fwd_bwd",
            "ams_adagrad_rows", "ams_pool_query_fwd", "ams_pool_query_bwd",
-           "ams_adam_update", "ams_pool_concat_fwd", "ams_pool_concat_bwd"]
+           "ams_adam_update", "ams_pool_concat_fwd", "ams_pool_concat_bwd", "ams_dssm_workspace",
+           "ams_dssm_fwd_bwd"]
 
 
 class AmsError(RuntimeError):
@@ -90,8 +91,13 @@ def load() -> ctypes.CDLL:
     lib.ams_ctr_workspace.restype = sz
     lib.ams_ctr_workspace.argtypes = [C, i32]
     lib.ams_ctr_fwd_bwd.restype = ctypes.c_int
-    lib.ams_ctr_fwd_bwd.argtypes = [C, i32, i32, PP, ctypes.POINTER(i32), P, PP, PP, P, P, PP, PP, PP, P,
-                                    sz, P]
+    lib.ams_ctr_fwd_bwd.argtypes = [C, i32, i32, PP, ctypes.POINTER(i32), P, PP, PP, PP, P, P, PP, PP, PP, PP,
+                                    P, sz, P]
+    lib.ams_dssm_workspace.restype = sz
+    lib.ams_dssm_workspace.argtypes = [C, C, i32]
+    lib.ams_dssm_fwd_bwd.restype = ctypes.c_int
+    lib.ams_dssm_fwd_bwd.argtypes = [C, C, i32, i32, PP, ctypes.POINTER(i32), i32, PP, ctypes.POINTER(i32), P,
+                                     PP, PP, PP, PP, PP, PP, P, P, PP, PP, PP, PP, PP, PP, PP, PP, P, sz, P]
     lib.ams_adagrad_rows.restype = ctypes.c_int
     lib.ams_adagrad_rows.argtypes = [i32, P, P, i32, P, P, i64, P, ctypes.c_float, ctypes.c_float, P]
     lib.ams_pool_query_fwd.restype = ctypes.c_int
@@ -297,13 +303,41 @@ def ams_ctr_workspace(net: ams_ctr, B: int) -> int:
     return load().ams_ctr_workspace(ctypes.byref(net), int(B))
 
 
-def ams_ctr_fwd_bwd(net: ams_ctr, fields, labels, W, b, loss, prob, dW, db, dfields, ws, stream=None):
+def _opt_parray(ts):
+    return _parray(ts) if ts is not None else None
+
+
+def _widths(fields):
+    return (ctypes.c_int32 * len(fields))(*[int(f.shape[1]) for f in fields])
+
+
+def ams_ctr_fwd_bwd(net: ams_ctr, fields, labels, W, b, loss, prob, dW, db, dfields, ws, stream=None, slopes=None,
+                    dslopes=None):
+    """slopes: PReLU slopes of the hidden layers (None, or None entries: ReLU);
+    dslopes: where their gradients go (None: not stored)."""
     B = fields[0].shape[0]
-    widths = (ctypes.c_int32 * len(fields))(*[int(f.shape[1]) for f in fields])
-    _check(load().ams_ctr_fwd_bwd(ctypes.byref(net), B, len(fields), _parray(fields), widths, _p(labels),
-                                  _parray(W), _parray(b), _p(loss), _p(prob), _parray(dW), _parray(db),
-                                  _parray(dfields) if dfields is not None else None, _p(ws),
+    _check(load().ams_ctr_fwd_bwd(ctypes.byref(net), B, len(fields), _parray(fields), _widths(fields), _p(labels),
+                                  _parray(W), _parray(b), _opt_parray(slopes), _p(loss), _p(prob), _parray(dW),
+                                  _parray(db), _opt_parray(dslopes), _opt_parray(dfields), _p(ws),
                                   ws.numel() * ws.element_size(), _stream(stream)), "ams_ctr_fwd_bwd")
+
+
+def ams_dssm_workspace(user_net: ams_ctr, ad_net: ams_ctr, B: int) -> int:
+    return load().ams_dssm_workspace(ctypes.byref(user_net), ctypes.byref(ad_net), int(B))
+
+
+def ams_dssm_fwd_bwd(user_net: ams_ctr, ad_net: ams_ctr, user_fields, ad_fields, labels, user, ad, loss, prob,
+                     duser, dad, duser_fields, dad_fields, ws, stream=None):
+    """user / ad: (W, b, slopes) of each tower; duser / dad: (dW, db, dslopes)."""
+    B = user_fields[0].shape[0]
+    _check(load().ams_dssm_fwd_bwd(ctypes.byref(user_net), ctypes.byref(ad_net), B, len(user_fields),
+                                   _parray(user_fields), _widths(user_fields), len(ad_fields), _parray(ad_fields),
+                                   _widths(ad_fields), _p(labels), _parray(user[0]), _parray(user[1]),
+                                   _opt_parray(user[2]), _parray(ad[0]), _parray(ad[1]), _opt_parray(ad[2]),
+                                   _p(loss), _p(prob), _parray(duser[0]), _parray(duser[1]), _opt_parray(duser[2]),
+                                   _parray(dad[0]), _parray(dad[1]), _opt_parray(dad[2]),
+                                   _opt_parray(duser_fields), _opt_parray(dad_fields), _p(ws),
+                                   ws.numel() * ws.element_size(), _stream(stream)), "ams_dssm_fwd_bwd")
 
 
 def ams_adagrad_rows(uniq, n_uniq, n_uniq_cap: int, grad, table, accum, lr: float, eps: float, stream=None):

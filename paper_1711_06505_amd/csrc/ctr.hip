@@ -21,7 +21,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / AMS_WAVE;
 constexpr int kCtrBS = 16;                  // samples per block of the CTR kernel
-constexpr int kCtrMaxIn = 128, kCtrMaxHidden = 256, kCtrMaxC = 8;
+constexpr int kCtrMaxIn = 128, kCtrMaxHidden = 256, kCtrMaxC = 8, kTowerMaxOut = 64;
 constexpr int kCtrMaxLayers = 3, kCtrMaxFields = 8;
 
 // ------------------------------------------------------------ bag forward
@@ -79,7 +79,7 @@ __global__ __launch_bounds__(kThreads) void bag_fwd_k(int B, int D, const int32_
 // ---------------------------------------------------------------- CTR MLP
 
 struct CtrArgs {
-    int L;                                   // layers (2 or 3)
+    int L;                                   // layers (1 to 3)
     int dims[kCtrMaxLayers + 1];
     int n_fields;
     int fdim[kCtrMaxFields];
@@ -87,12 +87,15 @@ struct CtrArgs {
     float *dfield[kCtrMaxFields];
     const float *W[kCtrMaxLayers];
     const float *b[kCtrMaxLayers];
+    const float *slope[kCtrMaxLayers];       // PReLU slopes after layer l < L-1; NULL: ReLU
 };
 
-__host__ __device__ inline int ctr_part_size(const CtrArgs &a)
+// A block's partial row holds, per layer, dW [O x K], db [O] and, below the
+// last layer, the slope gradient [O]; the CTR row ends with the loss sum.
+__host__ __device__ inline int net_part_size(const CtrArgs &a)
 {
-    int n = 1;                               // + the block's loss sum
-    for (int l = 0; l < a.L; ++l) n += a.dims[l + 1] * a.dims[l] + a.dims[l + 1];
+    int n = 0;
+    for (int l = 0; l < a.L; ++l) n += a.dims[l + 1] * a.dims[l] + a.dims[l + 1] * (l < a.L - 1 ? 2 : 1);
     return n;
 }
 
@@ -114,14 +117,25 @@ __host__ __device__ inline int ctr_bwd_parts(int K, int O)
     return P;
 }
 
-// out[s][o] = bias[o] + sum_k in[s][k] W[o][k] (ReLU'd unless last) for the
-// block's kCtrBS samples.  Work item (o, part p of P): the K range of part p
-// (a multiple of 4 wide), its W row streamed in float4 runs of 16, all
-// samples accumulated together (in[s][k] is the same LDS word for the whole
-// wave: a broadcast).  With P > 1 (narrow layers) the parts go to `scr`
-// [P][kCtrBS][O] and are added in part order.
+// Activation of a hidden unit: ReLU, or PReLU with slope a (z for z > 0,
+// a z otherwise), whose pre-activation is kept in z_out for the backward.
+__device__ __forceinline__ float ctr_act(float v, const float *slope, int o, float *z_out)
+{
+    if (!slope) return fmaxf(v, 0.f);
+    *z_out = v;
+    return v > 0.f ? v : slope[o] * v;
+}
+
+// out[s][o] = bias[o] + sum_k in[s][k] W[o][k] for the block's kCtrBS
+// samples, activated below the last layer (`hidden`).  Work item (o, part p
+// of P): the K range of part p (a multiple of 4 wide), its W row streamed in
+// float4 runs of 16, all samples accumulated together (in[s][k] is the same
+// LDS word for the whole wave: a broadcast).  With P > 1 (narrow layers) the
+// parts go to `scr` [P][kCtrBS][O] and are added in part order.  With PReLU
+// the pre-activations go to zout [kCtrBS][O].
 __device__ __forceinline__ void ctr_dense_fwd(const float *in, int K, float *out, int O, const float *__restrict__ W,
-                                              const float *__restrict__ bias, bool relu, float *scr, int t)
+                                              const float *__restrict__ bias, bool hidden,
+                                              const float *__restrict__ slope, float *zout, float *scr, int t)
 {
     const int P = ctr_fwd_parts(K, O);
     const int KC = (((K + P - 1) / P) + 3) & ~3;
@@ -160,7 +174,7 @@ __device__ __forceinline__ void ctr_dense_fwd(const float *in, int K, float *out
 #pragma unroll
             for (int s = 0; s < kCtrBS; ++s) {
                 const float v = acc[s] + bo;
-                out[s * O + o] = relu ? fmaxf(v, 0.f) : v;
+                out[s * O + o] = hidden ? ctr_act(v, slope, o, zout + s * O + o) : v;
             }
         } else {
 #pragma unroll
@@ -173,17 +187,47 @@ __device__ __forceinline__ void ctr_dense_fwd(const float *in, int K, float *out
             const int o = e % O;
             float v = bias[o];
             for (int pp = 0; pp < P; ++pp) v += scr[pp * kCtrBS * O + e];
-            out[e] = relu ? fmaxf(v, 0.f) : v;
+            out[e] = hidden ? ctr_act(v, slope, o, zout + e) : v;
         }
     }
 }
 
-// gin[s][k] = sum_o gout[s][o] W[o][k] (masked by [in > 0] when `mask`).
-// Work item (k, part p of P over O); the lanes of a wave take consecutive k,
-// so each W row read is contiguous across the wave; 8 rows in flight.  Parts
-// are added in order through `scr` as in the forward.
+// Gradient into a layer's input: d[s][k] = sum_o gout[s][o] W[o][k], then
+// through the activation that produced the input when `act` (below the
+// first layer): ReLU takes d where in > 0; PReLU reads its pre-activation z
+// from gin (left there by the forward) and takes d for z > 0, slope[k] d
+// otherwise, and adds d min(z, 0) over the block's samples (ascending) into
+// the slope gradient dsl[k].  Work item (k, part p of P over O); the lanes of
+// a wave take consecutive k, so each W row read is contiguous across the
+// wave; 8 rows in flight.  Parts are added in order through `scr` as in the
+// forward.
+__device__ __forceinline__ void ctr_act_bwd(float *gin, const float *in, int K, int k, const float (&d)[kCtrBS],
+                                            bool act, const float *__restrict__ slope, float *dsl)
+{
+    if (!act) {
+#pragma unroll
+        for (int s = 0; s < kCtrBS; ++s) gin[s * K + k] = d[s];
+    } else if (!slope) {
+#pragma unroll
+        for (int s = 0; s < kCtrBS; ++s) gin[s * K + k] = in[s * K + k] > 0.f ? d[s] : 0.f;
+        if (dsl) dsl[k] = 0.f;
+    } else {
+        const float a = slope[k];
+        float ds = 0.f;
+#pragma unroll
+        for (int s = 0; s < kCtrBS; ++s) {
+            const float z = gin[s * K + k];
+            const bool pos = z > 0.f;
+            gin[s * K + k] = pos ? d[s] : a * d[s];
+            ds = fmaf(pos ? 0.f : z, d[s], ds);
+        }
+        dsl[k] = ds;
+    }
+}
+
 __device__ __forceinline__ void ctr_dense_bwd_data(const float *gout, int O, float *gin, const float *in, int K,
-                                                   const float *__restrict__ W, bool mask, float *scr, int t)
+                                                   const float *__restrict__ W, bool act,
+                                                   const float *__restrict__ slope, float *dsl, float *scr, int t)
 {
     const int P = ctr_bwd_parts(K, O);
     const int OC = (O + P - 1) / P;
@@ -205,8 +249,7 @@ __device__ __forceinline__ void ctr_dense_bwd_data(const float *gout, int O, flo
             }
         }
         if (P == 1) {
-#pragma unroll
-            for (int s = 0; s < kCtrBS; ++s) gin[s * K + k] = (!mask || in[s * K + k] > 0.f) ? acc[s] : 0.f;
+            ctr_act_bwd(gin, in, K, k, acc, act, slope, dsl);
         } else {
 #pragma unroll
             for (int s = 0; s < kCtrBS; ++s) scr[(pp * kCtrBS + s) * K + k] = acc[s];
@@ -214,10 +257,15 @@ __device__ __forceinline__ void ctr_dense_bwd_data(const float *gout, int O, flo
     }
     if (P > 1) {
         __syncthreads();
-        for (int e = t; e < kCtrBS * K; e += kThreads) {
-            float v = 0.f;
-            for (int pp = 0; pp < P; ++pp) v += scr[pp * kCtrBS * K + e];
-            gin[e] = (!mask || in[e] > 0.f) ? v : 0.f;
+        for (int k = t; k < K; k += kThreads) {
+            float d[kCtrBS];
+#pragma unroll
+            for (int s = 0; s < kCtrBS; ++s) {
+                float v = 0.f;
+                for (int pp = 0; pp < P; ++pp) v += scr[(pp * kCtrBS + s) * K + k];
+                d[s] = v;
+            }
+            ctr_act_bwd(gin, in, K, k, d, act, slope, dsl);
         }
     }
 }
@@ -262,12 +310,10 @@ __device__ __forceinline__ void ctr_dense_bwd_weight(const float *gout, int O, c
     }
 }
 
-// One block = kCtrBS samples: forward through every layer in LDS, softmax
-// and cross-entropy, then the backward; the block's weight-gradient and loss
-// sums (over its samples, ascending) go to its partial row.
-// Dynamic LDS, sized by ctr_lds_floats for the actual widths: act (every
-// layer's activations, [kCtrBS][dims[l]] each), grd (their loss gradients),
-// scr (parts of narrow layers in the backward), the samples' losses.
+// LDS of one net for a block of kCtrBS samples: act (every layer's
+// activations, [kCtrBS][dims[l]] each, the input fields first) and grd (the
+// loss gradient of each act[l]; with PReLU a hidden layer's slot holds its
+// pre-activations between the forward and the backward).
 __host__ __device__ inline int ctr_act_floats(const CtrArgs &a)
 {
     int n = 0;
@@ -275,6 +321,7 @@ __host__ __device__ inline int ctr_act_floats(const CtrArgs &a)
     return n;
 }
 
+// scr: the parts of narrow layers, forward and backward.
 __host__ __device__ inline int ctr_scr_floats(const CtrArgs &a)
 {
     int n = 0;
@@ -287,99 +334,137 @@ __host__ __device__ inline int ctr_scr_floats(const CtrArgs &a)
     return n;
 }
 
+struct NetLds {
+    float *act, *grd;
+    int off[kCtrMaxLayers + 1];
+};
+
+__device__ __forceinline__ NetLds net_lds(const CtrArgs &a, float *base)
+{
+    NetLds n;
+    n.act = base;
+    n.grd = base + ctr_act_floats(a);
+    n.off[0] = 0;
+    for (int l = 0; l < a.L; ++l) n.off[l + 1] = n.off[l] + kCtrBS * a.dims[l];
+    return n;
+}
+
+// input fields, concatenated; rows past B read 0
+__device__ __forceinline__ void net_load(const CtrArgs &a, const NetLds &n, int b0, int B, int t)
+{
+    const int K0 = a.dims[0];
+    int c0 = 0;
+    for (int f = 0; f < a.n_fields; ++f) {
+        const int w = a.fdim[f];
+        for (int e = t; e < kCtrBS * w; e += kThreads) {
+            const int s = e / w, k = e % w;
+            n.act[s * K0 + c0 + k] = (b0 + s < B) ? a.field[f][(size_t)(b0 + s) * w + k] : 0.f;
+        }
+        c0 += w;
+    }
+}
+
+// Every layer in turn (the caller synchronises before: act[0] loaded).
+__device__ __forceinline__ void net_forward(const CtrArgs &a, const NetLds &n, float *scr, int t)
+{
+    for (int l = 0; l < a.L; ++l) {
+        const bool hidden = l < a.L - 1;
+        ctr_dense_fwd(n.act + n.off[l], a.dims[l], n.act + n.off[l + 1], a.dims[l + 1], a.W[l], a.b[l], hidden,
+                      hidden ? a.slope[l] : nullptr, n.grd + n.off[l + 1], scr, t);
+        __syncthreads();
+    }
+}
+
+// From the loss gradient of the last layer's output (in grd, synchronised):
+// each layer's weight, bias and slope gradients over the block's samples into
+// the partial row p, and the gradient of the input fields into grd[0].
+__device__ __forceinline__ void net_backward(const CtrArgs &a, const NetLds &n, float *scr, float *p, int t)
+{
+    int wo[kCtrMaxLayers];
+    int woff = 0;
+    for (int l = 0; l < a.L; ++l) {
+        wo[l] = woff;
+        woff += a.dims[l + 1] * a.dims[l] + a.dims[l + 1] * (l < a.L - 1 ? 2 : 1);
+    }
+    for (int l = a.L - 1; l >= 0; --l) {
+        const int K = a.dims[l], O = a.dims[l + 1];
+        const float *gout = n.grd + n.off[l + 1], *in = n.act + n.off[l];
+        ctr_dense_bwd_weight(gout, O, in, K, p + wo[l], t);
+        // the activation below layer l belongs to layer l - 1: its slot
+        // follows that layer's dW and db
+        float *dsl = l > 0 ? p + wo[l - 1] + K * a.dims[l - 1] + K : nullptr;
+        ctr_dense_bwd_data(gout, O, n.grd + n.off[l], in, K, a.W[l], l > 0, l > 0 ? a.slope[l - 1] : nullptr, dsl,
+                           scr, t);
+        __syncthreads();
+    }
+}
+
+__device__ __forceinline__ void net_store_dfields(const CtrArgs &a, const NetLds &n, int b0, int B, int t)
+{
+    const int K0 = a.dims[0];
+    int c0 = 0;
+    for (int f = 0; f < a.n_fields; ++f) {
+        const int w = a.fdim[f];
+        if (a.dfield[f])
+            for (int e = t; e < kCtrBS * w; e += kThreads) {
+                const int s = e / w, k = e % w;
+                if (b0 + s < B) a.dfield[f][(size_t)(b0 + s) * w + k] = n.grd[s * K0 + c0 + k];
+            }
+        c0 += w;
+    }
+}
+
 inline size_t ctr_lds_bytes(const CtrArgs &a)
 {
     return (size_t)(2 * ctr_act_floats(a) + ctr_scr_floats(a) + kCtrBS) * 4;
 }
 
+// One block = kCtrBS samples: forward through every layer in LDS, softmax
+// and cross-entropy, then the backward; the block's gradient and loss sums
+// (over its samples, ascending) go to its partial row.
 __global__ __launch_bounds__(kThreads) void ctr_fb_k(CtrArgs a, int B, const int32_t *__restrict__ labels,
                                                      float *__restrict__ prob, float *__restrict__ part, int PS)
 {
     extern __shared__ float lds[];
-    const int na = ctr_act_floats(a);
-    float *act = lds;                        // act[l]: [kCtrBS][dims[l]] per layer
-    float *grd = lds + na;                   // the loss gradient of each act[l]
-    float *scr = lds + 2 * na;               // parts of narrow layers in the backward
+    const NetLds n = net_lds(a, lds);
+    float *scr = lds + 2 * ctr_act_floats(a);
     float *lossv = scr + ctr_scr_floats(a);
     const int t = threadIdx.x;
     const int b0 = blockIdx.x * kCtrBS;
-    const int L = a.L;
-    int off[kCtrMaxLayers + 1];
-    off[0] = 0;
-    for (int l = 0; l < L; ++l) off[l + 1] = off[l] + kCtrBS * a.dims[l];
-    const int K0 = a.dims[0], C = a.dims[L];
-    // input fields, concatenated; rows past B read 0
-    {
-        int c0 = 0;
-        for (int f = 0; f < a.n_fields; ++f) {
-            const int w = a.fdim[f];
-            for (int e = t; e < kCtrBS * w; e += kThreads) {
-                const int s = e / w, k = e % w;
-                act[s * K0 + c0 + k] = (b0 + s < B) ? a.field[f][(size_t)(b0 + s) * w + k] : 0.f;
-            }
-            c0 += w;
-        }
-    }
+    const int L = a.L, C = a.dims[L];
+    net_load(a, n, b0, B, t);
     __syncthreads();
-    for (int l = 0; l < L; ++l) {
-        ctr_dense_fwd(act + off[l], a.dims[l], act + off[l + 1], a.dims[l + 1], a.W[l], a.b[l], l < L - 1, scr, t);
-        __syncthreads();
-    }
+    net_forward(a, n, scr, t);
     // softmax, cross-entropy, dlogits = (p - onehot(y)) / B
     if (t < kCtrBS) {
-        const int s = t, n = b0 + s;
-        const float *z = act + off[L] + s * C;
-        float *gz = grd + off[L] + s * C;
+        const int s = t, i = b0 + s;
+        const float *z = n.act + n.off[L] + s * C;
+        float *gz = n.grd + n.off[L] + s * C;
         float ls = 0.f;
-        const int y = n < B ? labels[n] : -1;
-        if (n < B && y >= 0 && y < C) {
+        const int y = i < B ? labels[i] : -1;
+        if (i < B && y >= 0 && y < C) {
             float m = z[0];
             for (int c = 1; c < C; ++c) m = fmaxf(m, z[c]);
             float se = 0.f;
             for (int c = 0; c < C; ++c) se += expf(z[c] - m);
             const float lse = m + logf(se);
             for (int c = 0; c < C; ++c) {
-                const float p = expf(z[c] - lse);
-                if (prob) prob[(size_t)n * C + c] = p;
-                gz[c] = (p - (c == y ? 1.f : 0.f)) / (float)B;
+                const float pc = expf(z[c] - lse);
+                if (prob) prob[(size_t)i * C + c] = pc;
+                gz[c] = (pc - (c == y ? 1.f : 0.f)) / (float)B;
             }
             ls = lse - z[y];
         } else {
             for (int c = 0; c < C; ++c) gz[c] = 0.f;
-            if (n < B && prob)
-                for (int c = 0; c < C; ++c) prob[(size_t)n * C + c] = 0.f;
+            if (i < B && prob)
+                for (int c = 0; c < C; ++c) prob[(size_t)i * C + c] = 0.f;
         }
         lossv[s] = ls;
     }
     __syncthreads();
     float *p = part + (size_t)blockIdx.x * PS;
-    int woff = 0;
-    int wo[kCtrMaxLayers];
-    for (int l = 0; l < L; ++l) {
-        wo[l] = woff;
-        woff += a.dims[l + 1] * a.dims[l] + a.dims[l + 1];
-    }
-    for (int l = L - 1; l >= 0; --l) {
-        const int K = a.dims[l], O = a.dims[l + 1];
-        const float *gout = grd + off[l + 1], *in = act + off[l];
-        // weight and bias gradients of layer l over this block's samples
-        ctr_dense_bwd_weight(gout, O, in, K, p + wo[l], t);
-        ctr_dense_bwd_data(gout, O, grd + off[l], in, K, a.W[l], l > 0, scr, t);
-        __syncthreads();
-    }
-    // input-field gradients
-    {
-        int c0 = 0;
-        for (int f = 0; f < a.n_fields; ++f) {
-            const int w = a.fdim[f];
-            if (a.dfield[f])
-                for (int e = t; e < kCtrBS * w; e += kThreads) {
-                    const int s = e / w, k = e % w;
-                    if (b0 + s < B) a.dfield[f][(size_t)(b0 + s) * w + k] = grd[s * K0 + c0 + k];
-                }
-            c0 += w;
-        }
-    }
+    net_backward(a, n, scr, p, t);
+    net_store_dfields(a, n, b0, B, t);
     if (t == 0) {
         float ls = 0.f;
         for (int s = 0; s < kCtrBS; ++s) ls += lossv[s];
@@ -387,17 +472,80 @@ __global__ __launch_bounds__(kThreads) void ctr_fb_k(CtrArgs a, int B, const int
     }
 }
 
+// Pre-rank model (section 6): a user tower and an ad tower on their own
+// fields, score s = <u, a> of their outputs, click probability sigmoid(s),
+// logistic loss softplus(s) - y s for y in {0, 1} (other labels add
+// nothing), divided by B.  Same block layout as the CTR kernel with both
+// towers in LDS; the partial row holds the user tower's gradients, then the
+// ad tower's, then the loss sum.
+__global__ __launch_bounds__(kThreads) void dssm_fb_k(CtrArgs u, CtrArgs v, int B, const int32_t *__restrict__ labels,
+                                                      float *__restrict__ prob, float *__restrict__ part, int PS)
+{
+    extern __shared__ float lds[];
+    const NetLds nu = net_lds(u, lds);
+    const NetLds nv = net_lds(v, lds + 2 * ctr_act_floats(u));
+    float *scr = lds + 2 * ctr_act_floats(u) + 2 * ctr_act_floats(v);
+    float *lossv = scr + max(ctr_scr_floats(u), ctr_scr_floats(v));
+    const int t = threadIdx.x;
+    const int b0 = blockIdx.x * kCtrBS;
+    const int R = u.dims[u.L];
+    net_load(u, nu, b0, B, t);
+    net_load(v, nv, b0, B, t);
+    __syncthreads();
+    net_forward(u, nu, scr, t);
+    net_forward(v, nv, scr, t);
+    if (t < kCtrBS) {
+        const int s = t, i = b0 + s;
+        const float *zu = nu.act + nu.off[u.L] + s * R, *zv = nv.act + nv.off[v.L] + s * R;
+        float sc = 0.f;
+        for (int r = 0; r < R; ++r) sc = fmaf(zu[r], zv[r], sc);
+        const float pr = 1.f / (1.f + expf(-sc));
+        const int y = i < B ? labels[i] : -1;
+        float ls = 0.f, g = 0.f;
+        if (i < B) {
+            if (prob) prob[i] = pr;
+            if (y == 0 || y == 1) {
+                ls = fmaxf(sc, 0.f) + log1pf(expf(-fabsf(sc))) - (float)y * sc;
+                g = (pr - (float)y) / (float)B;
+            }
+        }
+        float *gu = nu.grd + nu.off[u.L] + s * R, *gv = nv.grd + nv.off[v.L] + s * R;
+        for (int r = 0; r < R; ++r) {
+            gu[r] = g * zv[r];
+            gv[r] = g * zu[r];
+        }
+        lossv[s] = ls;
+    }
+    __syncthreads();
+    float *p = part + (size_t)blockIdx.x * PS;
+    net_backward(u, nu, scr, p, t);
+    net_backward(v, nv, scr, p + net_part_size(u), t);
+    net_store_dfields(u, nu, b0, B, t);
+    net_store_dfields(v, nv, b0, B, t);
+    if (t == 0) {
+        float ls = 0.f;
+        for (int s = 0; s < kCtrBS; ++s) ls += lossv[s];
+        p[PS - 1] = ls;
+    }
+}
+
+// Where the reduced partial rows go: per layer (of one net, or of the two
+// towers one after the other) dW, db and, below a net's last layer, the
+// slope gradient (NULL: not stored); the last element is the loss sum.
+struct RedLayer {
+    int K, O, hidden;
+    float *dW, *db, *ds;
+};
+
 struct CtrOut {
-    int L;
-    int dims[kCtrMaxLayers + 1];
-    float *dW[kCtrMaxLayers];
-    float *db[kCtrMaxLayers];
+    int nl;
+    RedLayer ly[2 * kCtrMaxLayers];
     float *loss;
     int B;
 };
 
 // Fixed-order sum of the blocks' partial rows (eight running chains over
-// g = 8 i + r, added r = 0..7), scattered into dW, db and the mean loss.
+// g = 8 i + r, added r = 0..7), scattered into the gradients and the mean loss.
 __global__ __launch_bounds__(kThreads) void ctr_reduce_k(const float *__restrict__ part, int G, int PS, CtrOut o)
 {
     const int e = blockIdx.x * kThreads + threadIdx.x;
@@ -416,18 +564,26 @@ __global__ __launch_bounds__(kThreads) void ctr_reduce_k(const float *__restrict
         return;
     }
     int x = e;
-    for (int l = 0; l < o.L; ++l) {
-        const int nw = o.dims[l + 1] * o.dims[l];
+    for (int l = 0; l < o.nl; ++l) {
+        const RedLayer &y = o.ly[l];
+        const int nw = y.O * y.K;
         if (x < nw) {
-            o.dW[l][x] = tot;
+            y.dW[x] = tot;
             return;
         }
         x -= nw;
-        if (x < o.dims[l + 1]) {
-            o.db[l][x] = tot;
+        if (x < y.O) {
+            y.db[x] = tot;
             return;
         }
-        x -= o.dims[l + 1];
+        x -= y.O;
+        if (y.hidden) {
+            if (x < y.O) {
+                if (y.ds) y.ds[x] = tot;
+                return;
+            }
+            x -= y.O;
+        }
     }
 }
 
@@ -472,14 +628,87 @@ __global__ __launch_bounds__(kThreads) void adam_k(int64_t n, float *__restrict_
 
 size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-bool ctr_ok(const ams_ctr *net)
+// Widths a net of the CTR kind accepts: 1..kCtrMaxLayers layers, inputs up
+// to kCtrMaxIn, hidden widths up to kCtrMaxHidden; the output width is
+// checked by the caller (classes, or a tower's representation).
+bool net_dims_ok(const ams_ctr *net, int min_layers)
 {
-    if (!net || net->n_layers < 2 || net->n_layers > kCtrMaxLayers) return false;
+    if (!net || net->n_layers < min_layers || net->n_layers > kCtrMaxLayers) return false;
     if (net->dims[0] < 1 || net->dims[0] > kCtrMaxIn) return false;
     for (int l = 1; l < net->n_layers; ++l)
         if (net->dims[l] < 1 || net->dims[l] > kCtrMaxHidden) return false;
+    return true;
+}
+
+bool ctr_ok(const ams_ctr *net)
+{
+    if (!net_dims_ok(net, 2)) return false;
     const int C = net->dims[net->n_layers];
     return C >= 2 && C <= kCtrMaxC;
+}
+
+bool tower_ok(const ams_ctr *net)
+{
+    if (!net_dims_ok(net, 1)) return false;
+    const int R = net->dims[net->n_layers];
+    return R >= 1 && R <= kTowerMaxOut;
+}
+
+// LDS a block may have on the current device (64 KiB if it cannot be asked).
+size_t lds_limit()
+{
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || n <= 0)
+        n = 65536;
+    return (size_t)n;
+}
+
+// Fill a net's arguments; NULL pointers where the ABI requires them give NULL.
+ams_status net_args(const ams_ctr *net, int32_t n_fields, const float *const *fields, const int32_t *field_dims,
+                    const float *const *W, const float *const *b, const float *const *slope,
+                    float *const *dfields, CtrArgs &a)
+{
+    if (!fields || !field_dims || !W || !b) return AMS_ERR_NULL;
+    if (n_fields < 1 || n_fields > kCtrMaxFields) return AMS_ERR_DIMS;
+    a = CtrArgs{};
+    a.L = net->n_layers;
+    for (int l = 0; l <= a.L; ++l) a.dims[l] = net->dims[l];
+    a.n_fields = n_fields;
+    int width = 0;
+    for (int f = 0; f < n_fields; ++f) {
+        if (field_dims[f] < 1) return AMS_ERR_DIMS;
+        if (!fields[f]) return AMS_ERR_NULL;
+        a.fdim[f] = field_dims[f];
+        a.field[f] = fields[f];
+        a.dfield[f] = dfields ? dfields[f] : nullptr;
+        width += field_dims[f];
+    }
+    if (width != a.dims[0]) return AMS_ERR_DIMS;
+    for (int l = 0; l < a.L; ++l) {
+        if (!W[l] || !b[l]) return AMS_ERR_NULL;
+        a.W[l] = W[l];
+        a.b[l] = b[l];
+        a.slope[l] = (slope && l < a.L - 1) ? slope[l] : nullptr;
+    }
+    return AMS_OK;
+}
+
+// Reduction targets of one net's layers, appended to o.
+ams_status net_out(const CtrArgs &a, float *const *dW, float *const *db, float *const *dslope, CtrOut &o)
+{
+    if (!dW || !db) return AMS_ERR_NULL;
+    for (int l = 0; l < a.L; ++l) {
+        if (!dW[l] || !db[l]) return AMS_ERR_NULL;
+        RedLayer &y = o.ly[o.nl++];
+        y.K = a.dims[l];
+        y.O = a.dims[l + 1];
+        y.hidden = l < a.L - 1;
+        y.dW = dW[l];
+        y.db = db[l];
+        y.ds = (y.hidden && dslope && a.slope[l]) ? dslope[l] : nullptr;
+    }
+    return AMS_OK;
 }
 
 }  // namespace
@@ -524,52 +753,87 @@ extern "C" size_t ams_ctr_workspace(const ams_ctr *net, int32_t B)
     a.L = net->n_layers;
     for (int l = 0; l <= a.L; ++l) a.dims[l] = net->dims[l];
     const int G = (B + kCtrBS - 1) / kCtrBS;
-    return al256((size_t)(G > 0 ? G : 1) * ctr_part_size(a) * 4);
+    return al256((size_t)(G > 0 ? G : 1) * (net_part_size(a) + 1) * 4);
 }
 
 extern "C" ams_status ams_ctr_fwd_bwd(const ams_ctr *net, int32_t B, int32_t n_fields, const float *const *fields,
                                       const int32_t *field_dims, const int32_t *labels, const float *const *W,
-                                      const float *const *b, float *loss, float *prob, float *const *dW,
-                                      float *const *db, float *const *dfields, void *ws, size_t ws_bytes,
-                                      void *stream)
+                                      const float *const *b, const float *const *slope, float *loss, float *prob,
+                                      float *const *dW, float *const *db, float *const *dslope,
+                                      float *const *dfields, void *ws, size_t ws_bytes, void *stream)
 {
-    if (!net || !fields || !field_dims || !W || !b || !dW || !db) return AMS_ERR_NULL;
+    if (!net) return AMS_ERR_NULL;
     if (!ctr_ok(net)) return AMS_ERR_DIMS;
     if (B < 1) return AMS_ERR_SIZE;
-    if (n_fields < 1 || n_fields > kCtrMaxFields) return AMS_ERR_DIMS;
-    CtrArgs a{};
-    a.L = net->n_layers;
-    for (int l = 0; l <= a.L; ++l) a.dims[l] = net->dims[l];
-    a.n_fields = n_fields;
-    int width = 0;
-    for (int f = 0; f < n_fields; ++f) {
-        if (field_dims[f] < 1) return AMS_ERR_DIMS;
-        if (!fields[f]) return AMS_ERR_NULL;
-        a.fdim[f] = field_dims[f];
-        a.field[f] = fields[f];
-        a.dfield[f] = dfields ? dfields[f] : nullptr;
-        width += field_dims[f];
-    }
-    if (width != a.dims[0]) return AMS_ERR_DIMS;
-    for (int l = 0; l < a.L; ++l) {
-        if (!W[l] || !b[l] || !dW[l] || !db[l]) return AMS_ERR_NULL;
-        a.W[l] = W[l];
-        a.b[l] = b[l];
-    }
+    CtrArgs a;
+    ams_status s = net_args(net, n_fields, fields, field_dims, W, b, slope, dfields, a);
+    if (s != AMS_OK) return s;
+    CtrOut o{};
+    s = net_out(a, dW, db, dslope, o);
+    if (s != AMS_OK) return s;
     if (!labels || !loss) return AMS_ERR_NULL;
+    const size_t lds = ctr_lds_bytes(a);
+    if (lds > lds_limit()) return AMS_ERR_DIMS;
     const int G = (B + kCtrBS - 1) / kCtrBS;
-    const int PS = ctr_part_size(a);
+    const int PS = net_part_size(a) + 1;
     if (!ws || ws_bytes < (size_t)G * PS * 4) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     float *part = (float *)ws;
-    AMS_LAUNCH("ctr_fwd_bwd", st, ctr_fb_k<<<G, kThreads, ctr_lds_bytes(a), st>>>(a, B, labels, prob, part, PS));
+    AMS_LAUNCH("ctr_fwd_bwd", st, ctr_fb_k<<<G, kThreads, lds, st>>>(a, B, labels, prob, part, PS));
+    o.loss = loss;
+    o.B = B;
+    AMS_LAUNCH("ctr_reduce", st, ctr_reduce_k<<<(PS + kThreads - 1) / kThreads, kThreads, 0, st>>>(part, G, PS, o));
+    return ams_launch_status();
+}
+
+extern "C" size_t ams_dssm_workspace(const ams_ctr *user_net, const ams_ctr *ad_net, int32_t B)
+{
+    if (!tower_ok(user_net) || !tower_ok(ad_net) || B < 0) return 0;
+    CtrArgs u{}, v{};
+    u.L = user_net->n_layers;
+    v.L = ad_net->n_layers;
+    for (int l = 0; l <= u.L; ++l) u.dims[l] = user_net->dims[l];
+    for (int l = 0; l <= v.L; ++l) v.dims[l] = ad_net->dims[l];
+    const int G = (B + kCtrBS - 1) / kCtrBS;
+    return al256((size_t)(G > 0 ? G : 1) * (net_part_size(u) + net_part_size(v) + 1) * 4);
+}
+
+extern "C" ams_status ams_dssm_fwd_bwd(const ams_ctr *user_net, const ams_ctr *ad_net, int32_t B,
+                                       int32_t n_user_fields, const float *const *user_fields,
+                                       const int32_t *user_field_dims, int32_t n_ad_fields,
+                                       const float *const *ad_fields, const int32_t *ad_field_dims,
+                                       const int32_t *labels, const float *const *Wu, const float *const *bu,
+                                       const float *const *slope_u, const float *const *Wa,
+                                       const float *const *ba, const float *const *slope_a, float *loss,
+                                       float *prob, float *const *dWu, float *const *dbu,
+                                       float *const *dslope_u, float *const *dWa, float *const *dba,
+                                       float *const *dslope_a, float *const *duser_fields,
+                                       float *const *dad_fields, void *ws, size_t ws_bytes, void *stream)
+{
+    if (!user_net || !ad_net) return AMS_ERR_NULL;
+    if (!tower_ok(user_net) || !tower_ok(ad_net)) return AMS_ERR_DIMS;
+    if (user_net->dims[user_net->n_layers] != ad_net->dims[ad_net->n_layers]) return AMS_ERR_DIMS;
+    if (B < 1) return AMS_ERR_SIZE;
+    CtrArgs u, v;
+    ams_status s = net_args(user_net, n_user_fields, user_fields, user_field_dims, Wu, bu, slope_u, duser_fields, u);
+    if (s != AMS_OK) return s;
+    s = net_args(ad_net, n_ad_fields, ad_fields, ad_field_dims, Wa, ba, slope_a, dad_fields, v);
+    if (s != AMS_OK) return s;
     CtrOut o{};
-    o.L = a.L;
-    for (int l = 0; l <= a.L; ++l) o.dims[l] = a.dims[l];
-    for (int l = 0; l < a.L; ++l) {
-        o.dW[l] = dW[l];
-        o.db[l] = db[l];
-    }
+    s = net_out(u, dWu, dbu, dslope_u, o);
+    if (s != AMS_OK) return s;
+    s = net_out(v, dWa, dba, dslope_a, o);
+    if (s != AMS_OK) return s;
+    if (!labels || !loss) return AMS_ERR_NULL;
+    const size_t lds = (size_t)(2 * ctr_act_floats(u) + 2 * ctr_act_floats(v) +
+                                max(ctr_scr_floats(u), ctr_scr_floats(v)) + kCtrBS) * 4;
+    if (lds > lds_limit()) return AMS_ERR_DIMS;
+    const int G = (B + kCtrBS - 1) / kCtrBS;
+    const int PS = net_part_size(u) + net_part_size(v) + 1;
+    if (!ws || ws_bytes < (size_t)G * PS * 4) return AMS_ERR_WORKSPACE;
+    hipStream_t st = (hipStream_t)stream;
+    float *part = (float *)ws;
+    AMS_LAUNCH("dssm_fwd_bwd", st, dssm_fb_k<<<G, kThreads, lds, st>>>(u, v, B, labels, prob, part, PS));
     o.loss = loss;
     o.B = B;
     AMS_LAUNCH("ctr_reduce", st, ctr_reduce_k<<<(PS + kThreads - 1) / kThreads, kThreads, 0, st>>>(part, G, PS, o));

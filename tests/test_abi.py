@@ -169,9 +169,9 @@ def test_joint_host_errors(lib):
     fields = (P * 5)(*[0x1000] * 5)
     widths = (ctypes.c_int32 * 5)(12, 12, 12, 12, 12)
     ptr3 = (P * 3)(*[0x1000] * 3)
-    args = [ctypes.byref(net), 4096, 5, fields, widths, FAKE, ptr3, ptr3, FAKE, None, ptr3, ptr3, None,
+    args = [ctypes.byref(net), 4096, 5, fields, widths, FAKE, ptr3, ptr3, None, FAKE, None, ptr3, ptr3, None, None,
             FAKE, 1 << 30, None]
-    a = list(args); a[14] = 16
+    a = list(args); a[16] = 16
     assert lib.ams_ctr_fwd_bwd(*a) == WS
     a = list(args); a[1] = 0
     assert lib.ams_ctr_fwd_bwd(*a) == SIZE
@@ -182,7 +182,9 @@ def test_joint_host_errors(lib):
     assert lib.ams_ctr_fwd_bwd(*a) == DIMS
     a = list(args); a[5] = None               # labels
     assert lib.ams_ctr_fwd_bwd(*a) == NULL
-    a = list(args); a[8] = None               # loss
+    a = list(args); a[9] = None               # loss
+    assert lib.ams_ctr_fwd_bwd(*a) == NULL
+    a = list(args); a[12] = None              # db
     assert lib.ams_ctr_fwd_bwd(*a) == NULL
     # Adagrad
     assert lib.ams_adagrad_rows(12, FAKE, FAKE, -1, FAKE, FAKE, 100, FAKE, 0.01, 1e-8, None) == SIZE
@@ -227,3 +229,28 @@ def test_concat_pool_host_errors(lib):
     assert lib.ams_pool_concat_bwd(*a) == NULL
     a = list(b); a[2] = -3
     assert lib.ams_pool_concat_bwd(*a) == SIZE
+
+
+def test_dssm_host_errors(lib):
+    P = ctypes.c_void_p
+    user, ad = ams.make_ctr((36, 64, 32)), ams.make_ctr((24, 32))
+    assert lib.ams_dssm_workspace(ctypes.byref(user), ctypes.byref(ad), 4096) >= 256 * (36 * 64 + 64 * 32) * 4
+    assert lib.ams_dssm_workspace(ctypes.byref(user), ctypes.byref(ams.make_ctr((24, 65))), 10) == 0
+    uf, uw = (P * 3)(*[0x1000] * 3), (ctypes.c_int32 * 3)(12, 12, 12)
+    af, aw = (P * 2)(*[0x1000] * 2), (ctypes.c_int32 * 2)(12, 12)
+    p2 = (P * 2)(*[0x1000] * 2)
+    p1 = (P * 1)(0x1000)
+    args = [ctypes.byref(user), ctypes.byref(ad), 4096, 3, uf, uw, 2, af, aw, FAKE, p2, p2, None, p1, p1, None,
+            FAKE, None, p2, p2, None, p1, p1, None, None, None, FAKE, 1 << 30, None]
+    a = list(args); a[27] = 16
+    assert lib.ams_dssm_fwd_bwd(*a) == WS
+    a = list(args); a[1] = ctypes.byref(ams.make_ctr((24, 31)))   # towers of unequal width
+    assert lib.ams_dssm_fwd_bwd(*a) == DIMS
+    a = list(args); a[2] = 0
+    assert lib.ams_dssm_fwd_bwd(*a) == SIZE
+    a = list(args); a[8] = (ctypes.c_int32 * 2)(12, 11)
+    assert lib.ams_dssm_fwd_bwd(*a) == DIMS
+    a = list(args); a[9] = None                                     # labels
+    assert lib.ams_dssm_fwd_bwd(*a) == NULL
+    a = list(args); a[21] = None                                    # dWa
+    assert lib.ams_dssm_fwd_bwd(*a) == NULL
