@@ -121,6 +121,9 @@ def main():
     ap.add_argument("--mode", default=None)
     ap.add_argument("--batches", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--ops", action="store_true",
+                    help="instead of the step, time the widened operations one by one at their real shapes "
+                         "(one JSON line each)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="instead of the step, run a plain device copy of this many MiB "
                          "(calibrates the FETCH_SIZE / WRITE_SIZE counters)")
@@ -145,6 +148,11 @@ def main():
         print(json.dumps({"copy_probe_bytes_read_per_launch": n * 4, "copy_probe_bytes_written_per_launch": n * 4,
                           "launches": 3}))
         return
+
+    if args.ops:
+        torch.cuda.set_device(0)
+        ams.load()
+        return bench_ops(args)
 
     w = synth.get(args.workload)
     mode = args.mode or w.pools[-1]
@@ -428,6 +436,164 @@ def bench_joint(w, mode, args):
         "cpu_baseline": None,
     }
     print(json.dumps(out))
+
+
+PEAK_F32_VALU = 157.3e12
+
+
+def bench_ops(args):
+    """The operations beside the step, each timed alone at its real shape on
+    inputs resident in HBM: one channel of multiple-query attentive pooling
+    and the concatenate aggregator on the long-sequence batch, the Adam update
+    of the image model, the CTR model with PReLU and the pre-rank towers at
+    4096 samples.  Per op: ms per call over --steps calls (HIP events on the
+    launch stream) after --warmup calls, the library's per-kernel times, and
+    a roofline entry: compulsory HBM bytes (every input read once, every
+    output written once) against 8 TB/s, or for the small fp32 nets their
+    multiply-adds against the fp32 vector peak."""
+    import numpy as np
+    import torch
+
+    from paper_1711_06505_amd import ams, synth
+    stream = torch.cuda.current_stream()
+    f32, i32 = torch.float32, torch.int32
+
+    def timed(name, fn, shape, bound, work, unit_note):
+        for _ in range(args.warmup):
+            fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        for _ in range(args.steps):
+            fn()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / args.steps
+        ams.ams_timing_read()
+        ams.ams_timing_enable(True)
+        for _ in range(args.steps):
+            fn()
+        torch.cuda.synchronize()
+        ams.ams_timing_enable(False)
+        kt = {k: {"launches": n, "ms_per_launch": t / n} for k, (n, t) in ams.ams_timing_read().items() if n}
+        if bound == "hbm":
+            ach, pk, unit = work / (ms * 1e-3) / 1e9, PEAK_HBM / 1e9, "GB/s"
+        else:
+            ach, pk, unit = work / (ms * 1e-3) / 1e12, PEAK_F32_VALU / 1e12, "TFLOP/s"
+        print(json.dumps({"op": name, "shape": shape, "ms_per_call": ms, "calls": args.steps,
+                          "roofline": {"bound": bound, "achieved": ach, "peak": pk, "unit": unit, "frac": ach / pk,
+                                       "work_per_call": work, "unit_of_work": unit_note},
+                          "kernels": kt}), flush=True)
+
+    # ---- pooling variants on the long-sequence batch
+    w = synth.get("c3_long")
+    hb = synth.make_batch(w)
+    occ = torch.from_numpy(synth.occurrences(hb)).cuda()
+    seg = torch.from_numpy(hb["seg_off"]).cuda()
+    B, n_beh, D = w.batch, int(hb["seg_off"][-1]), 12
+    st = ams.Step(w.dims, w.dtype, "att", B, n_beh)
+    st.dedup(occ, w.n_images)
+    torch.cuda.synchronize()
+    n_u = int(st.n_uniq.item())
+    cap = st.cap
+    g = torch.Generator(device="cuda").manual_seed(5)
+    E = torch.randn((cap, D), generator=g, device="cuda") * 0.5
+    Q = torch.randn((B, D), generator=g, device="cuda") * 0.5
+    U = torch.empty((B, D), device="cuda")
+    wq = torch.empty(n_beh, device="cuda")
+    dU = torch.randn((B, D), generator=g, device="cuda")
+    dQ = torch.empty((B, D), device="cuda")
+    dE = torch.zeros((cap, D), device="cuda")
+    ws = torch.empty(ams.load().ams_pool_workspace(2, B, n_beh, D, cap), dtype=torch.uint8, device="cuda")
+
+    def mqap():
+        ams.ams_pool_query_fwd(seg, n_beh, st.inv, E, Q, U, wq)
+        ams.ams_pool_query_bwd(seg, n_beh, st.inv, st.occ_perm, st.uniq_off, st.n_uniq, cap, E, Q, U, wq, dU, dQ,
+                               dE, True, ws)
+    # fwd: inv, E, Q, seg in; U, w out.  bwd: inv, occ_perm, uniq_off, E, Q, U, w, dU in; dE (read and
+    # written: accumulate), dQ out
+    fwd_b = n_beh * 4 + n_u * D * 4 + B * D * 4 + (B + 1) * 4 + B * D * 4 + n_beh * 4
+    bwd_b = n_beh * 4 * 3 + (n_u + 1) * 4 + n_u * D * 4 * 3 + B * D * 4 * 4
+    timed("mqap_query_channel", mqap, f"c3_long batch: B={B}, {n_beh} behaviors, {n_u} unique, D={D}", "hbm",
+          fwd_b + bwd_b, "compulsory bytes of the forward and backward (accumulating into dE)")
+
+    Lc = 64
+    Uc = torch.empty((B, Lc * D), device="cuda")
+    Ac = torch.empty((B, D), device="cuda")
+    dUc = torch.randn((B, Lc * D), generator=g, device="cuda")
+    dAc = torch.randn((B, D), generator=g, device="cuda")
+    wsc = torch.empty(ams.load().ams_pool_workspace(0, B, n_beh, D, cap), dtype=torch.uint8, device="cuda")
+
+    def concat():
+        ams.ams_pool_concat_fwd(Lc, seg, n_beh, st.inv, E, Uc, Ac)
+        ams.ams_pool_concat_bwd(Lc, seg, n_beh, st.inv, st.occ_perm, st.uniq_off, st.n_uniq, cap, dUc, dAc, dE,
+                                wsc)
+    kept = int(np.minimum(np.diff(hb["seg_off"]), Lc).sum())
+    fwd_b = kept * 4 + (B + 1) * 4 + B * 4 + min(kept + B, n_u) * D * 4 + B * Lc * D * 4 + B * D * 4
+    bwd_b = (n_beh + B) * 4 * 2 + (n_u + 1) * 4 + B * Lc * D * 4 + B * D * 4 + n_u * D * 4
+    timed("concat_aggregator", concat, f"c3_long batch, Lc={Lc}: U {B}x{Lc * D}", "hbm", fwd_b + bwd_b,
+          "compulsory bytes of the forward and backward")
+    del st, E, Q, U, wq, dU, dQ, dE, ws, Uc, Ac, dUc, dAc, wsc
+
+    # ---- Adam on the image model's parameters (float32 master + bf16 copy)
+    n = sum(o * i + o for i, o in zip((4096, 256, 64), (256, 64, 12)))
+    prm = torch.randn(n, generator=g, device="cuda") * 0.05
+    grd = torch.randn(n, generator=g, device="cuda") * 1e-3
+    m, v = torch.zeros(n, device="cuda"), torch.zeros(n, device="cuda")
+    pb = torch.empty(n, dtype=torch.int16, device="cuda")
+    t_step = [0]
+
+    def adam():
+        t_step[0] += 1
+        ams.ams_adam_update(prm, grd, m, v, 1e-3, t_step[0], param_bf16=pb)
+    timed("adam_update", adam, f"{n} parameters (4096-256-64-12), bf16 copy", "hbm", n * 30,
+          "30 B per parameter: param, grad, m, v read; param, m, v written; bf16 copy written")
+
+    # ---- CTR model with PReLU and the pre-rank towers, 4096 samples
+    rng = np.random.default_rng(3)
+
+    def net(dims, prelu=True):
+        Ws = [torch.from_numpy(rng.uniform(-0.1, 0.1, (o, i)).astype(np.float32)).cuda()
+              for i, o in zip(dims[:-1], dims[1:])]
+        bs = [torch.zeros(o, device="cuda") for o in dims[1:]]
+        sl = [torch.full((o,), 0.25, device="cuda") for o in dims[1:-1]] if prelu else None
+        dW = [torch.empty_like(x) for x in Ws]
+        db = [torch.empty_like(x) for x in bs]
+        ds = [torch.empty_like(x) for x in sl] if prelu else None
+        return (Ws, bs, sl), (dW, db, ds)
+
+    Bc = 4096
+    cd = (60, 200, 80, 2)
+    (cW, cb, cs), (cdW, cdb, cds) = net(cd)
+    fields = [torch.randn((Bc, 12), generator=g, device="cuda") for _ in range(5)]
+    dfields = [torch.empty_like(x) for x in fields]
+    labels = torch.from_numpy((rng.random(Bc) < 0.05).astype(np.int32)).cuda()
+    loss, prob = torch.zeros(1, device="cuda"), torch.empty((Bc, 2), device="cuda")
+    cnet = ams.make_ctr(cd)
+    wsn = torch.empty(ams.ams_ctr_workspace(cnet, Bc), dtype=torch.uint8, device="cuda")
+
+    def ctr():
+        ams.ams_ctr_fwd_bwd(cnet, fields, labels, cW, cb, loss, prob, cdW, cdb, dfields, wsn, slopes=cs,
+                            dslopes=cds)
+    macs = sum(i * o for i, o in zip(cd[:-1], cd[1:]))
+    timed("ctr_prelu", ctr, f"B={Bc}, CTR MLP {'-'.join(map(str, cd))} PReLU, 5 fields of 12", "alu",
+          2.0 * Bc * macs * 3, "2 flop per multiply-add, forward + input gradient + weight gradient")
+
+    ud, ad = (48, 64, 32), (48, 64, 32)
+    user, duser = net(ud)
+    adn, dad = net(ad)
+    uf = [torch.randn((Bc, 12), generator=g, device="cuda") for _ in range(4)]
+    af = [torch.randn((Bc, 12), generator=g, device="cuda") for _ in range(4)]
+    duf, daf = [torch.empty_like(x) for x in uf], [torch.empty_like(x) for x in af]
+    pr = torch.empty(Bc, device="cuda")
+    un, an = ams.make_ctr(ud), ams.make_ctr(ad)
+    wsd = torch.empty(ams.ams_dssm_workspace(un, an, Bc), dtype=torch.uint8, device="cuda")
+
+    def dssm():
+        ams.ams_dssm_fwd_bwd(un, an, uf, af, labels, user, adn, loss, pr, duser, dad, duf, daf, wsd)
+    macs = sum(i * o for i, o in zip(ud[:-1], ud[1:])) + sum(i * o for i, o in zip(ad[:-1], ad[1:]))
+    timed("prerank_dssm", dssm, f"B={Bc}, towers {'-'.join(map(str, ud))} / {'-'.join(map(str, ad))} PReLU",
+          "alu", 2.0 * Bc * macs * 3, "2 flop per multiply-add, forward + input gradient + weight gradient")
 
 
 if __name__ == "__main__":
