@@ -438,21 +438,26 @@ class Step:
 
 class JointStep:
     """Buffers and calls of one joint training step (Algorithm 1: worker
-    iteration with the server's embed and update), on one stream:
+    iteration with the server's embed and update):
 
-      image dedup, ID dedups          ams_dedup x (1 + tables)
+      image dedup                     ams_dedup
       image embed + pool forward      ams_embed_fwd, ams_pool_fwd
-      ID bags                         ams_bag_fwd x tables
+      ID dedups, ID bags              ams_dedup, ams_bag_fwd x tables       (side stream)
       CTR forward + backward          ams_ctr_fwd_bwd (fields: U, A, bags)
       image pool + embed backward     ams_pool_bwd(dU, dA), ams_embed_bwd
-      ID rows: merged grad, Adagrad   ams_bag_bwd, ams_adagrad_rows x tables
+      ID rows: merged grad, Adagrad   ams_bag_bwd, ams_adagrad_rows x tables (side stream)
 
-    The ID tables and their Adagrad accumulators are caller tensors updated in
-    place; everything else is held here.
+    With ``overlap`` (the default) the ID-table work runs on a second stream
+    of default priority, forked from the caller's stream at the start and
+    joined before the CTR call and at the end, so it hides behind the image
+    path; each stream has its own workspace.  Without it, every call is on
+    the caller's stream in the order above.  The ID tables and their Adagrad
+    accumulators are caller tensors updated in place; everything else is held
+    here.
     """
 
     def __init__(self, dims, dtype: str, mode: str, B: int, n_beh_max: int, id_rows, id_dim: int, ctr_dims,
-                 device="cuda"):
+                 device="cuda", overlap: bool = True):
         self.img = Step(dims, dtype, mode, B, n_beh_max, device=device)
         self.B, self.n_beh = int(B), int(n_beh_max)
         self.n_occ = self.B + self.n_beh
@@ -482,16 +487,22 @@ class JointStep:
         self.ctr_dW = [torch.empty((o, i), dtype=f32, device=dev) for i, o in zip(ctr_dims[:-1], ctr_dims[1:])]
         self.ctr_db = [torch.empty((o,), dtype=f32, device=dev) for o in ctr_dims[1:]]
         self.ws = None
+        self.ws_id = None
+        self.side = torch.cuda.Stream(device=dev) if overlap else None
 
     def alloc_workspace(self, n_ids: int):
-        need = max(ams_dedup_workspace(self.n_occ, max([n_ids] + self.id_rows)),
-                   ams_embed_workspace(self.img.mlp, self.img.cap),
-                   ams_pool_workspace(self.img.mode, self.B, self.n_beh, self.img.dims[-1], self.img.cap),
-                   ams_bag_workspace(self.B, self.n_beh, self.id_dim, self.n_occ),
-                   ams_ctr_workspace(self.ctr, max(self.B, 1)), 256)
-        self.img.ws = torch.empty(need, dtype=torch.uint8, device=self.loss.device)
+        id_need = max(ams_dedup_workspace(self.n_occ, max(self.id_rows)),
+                      ams_bag_workspace(self.B, self.n_beh, self.id_dim, self.n_occ), 256)
+        img_need = max(ams_dedup_workspace(self.n_occ, n_ids), ams_embed_workspace(self.img.mlp, self.img.cap),
+                       ams_pool_workspace(self.img.mode, self.B, self.n_beh, self.img.dims[-1], self.img.cap),
+                       ams_ctr_workspace(self.ctr, max(self.B, 1)), 256)
+        if self.side is None:
+            img_need = max(img_need, id_need)
+        self.img.ws = torch.empty(img_need, dtype=torch.uint8, device=self.loss.device)
         self.img.n_ids = int(n_ids)
         self.ws = self.img.ws
+        self.ws_id = (torch.empty(id_need, dtype=torch.uint8, device=self.loss.device) if self.side is not None
+                      else self.ws)
 
     def run(self, ids, n_ids, T, W, b, seg_off, id_ids, id_tables, accum, labels, ctr_W, ctr_b, lr: float,
             eps: float, stream=None):
@@ -504,23 +515,36 @@ class JointStep:
         if self.ws is None or self.img.n_ids != int(n_ids):
             self.alloc_workspace(n_ids)
         st = self.img
-        st.dedup(ids, n_ids, stream)
+        main = stream if stream is not None else torch.cuda.current_stream()
+        side = self.side if self.side is not None else main
+        B = seg_off.numel() - 1
+        if side is not main:
+            side.wait_stream(main)                  # the caller's inputs are ready
+            for x in [seg_off, labels] + list(id_ids) + list(id_tables) + list(accum):
+                x.record_stream(side)
+        # ID tables: dedup (needed from bag_bwd on) and bags, beside the image forward
         for t in range(len(self.id_rows)):
             ams_dedup(id_ids[t], self.id_rows[t], self.t_uniq[t], self.t_inv[t], self.t_perm[t], self.t_off[t],
-                      self.t_nu[t], self.t_status[t], self.ws, stream)
-        st.embed_fwd(T, W, b, stream)
-        st.pool_fwd(seg_off, n_beh, stream)
-        for t in range(len(self.id_rows)):
-            ams_bag_fwd(seg_off, n_beh, id_ids[t], id_tables[t], self.bags[t], stream)
-        B = seg_off.numel() - 1
+                      self.t_nu[t], self.t_status[t], self.ws_id, side)
+            ams_bag_fwd(seg_off, n_beh, id_ids[t], id_tables[t], self.bags[t], side)
+        st.dedup(ids, n_ids, main)
+        st.embed_fwd(T, W, b, main)
+        st.pool_fwd(seg_off, n_beh, main)
+        if side is not main:
+            main.wait_stream(side)                  # bags ready
         fields = [st.U[:B], st.A[:B]] + [x[:B] for x in self.bags]
         dfields = [self.dU[:B], self.dA[:B]] + [x[:B] for x in self.dbags]
         ams_ctr_fwd_bwd(self.ctr, fields, labels, ctr_W, ctr_b, self.loss, self.prob, self.ctr_dW, self.ctr_db,
-                        dfields, self.ws, stream)
-        st.pool_bwd(seg_off, n_beh, self.dU, self.dA, stream)
-        st.embed_bwd(T, W, stream)
+                        dfields, self.ws, main)
+        if side is not main:
+            side.wait_stream(main)                  # bag gradients ready
+        # ID rows: merged gradients and Adagrad, beside the image backward
         for t in range(len(self.id_rows)):
             ams_bag_bwd(seg_off, n_beh, self.t_inv[t], self.t_perm[t], self.t_off[t], self.t_nu[t], self.n_occ,
-                        self.dbags[t][:B], self.row_grad[t], self.ws, stream)
+                        self.dbags[t][:B], self.row_grad[t], self.ws_id, side)
             ams_adagrad_rows(self.t_uniq[t], self.t_nu[t], self.n_occ, self.row_grad[t], id_tables[t], accum[t],
-                             lr, eps, stream)
+                             lr, eps, side)
+        st.pool_bwd(seg_off, n_beh, self.dU, self.dA, main)
+        st.embed_bwd(T, W, main)
+        if side is not main:
+            main.wait_stream(side)                  # the whole step is ordered before later work on main
