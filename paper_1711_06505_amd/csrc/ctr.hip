@@ -128,9 +128,10 @@ __device__ __forceinline__ float ctr_act(float v, const float *slope, int o, flo
 
 // out[s][o] = bias[o] + sum_k in[s][k] W[o][k] for the block's kCtrBS
 // samples, activated below the last layer (`hidden`).  Work item (o, part p
-// of P): the K range of part p (a multiple of 4 wide), its W row streamed in
-// float4 runs of 16, all samples accumulated together (in[s][k] is the same
-// LDS word for the whole wave: a broadcast).  With P > 1 (narrow layers) the
+// of P): the K range of part p (a multiple of 4 wide), its W row streamed as
+// float4 (the next one loaded while the current one is used), all samples
+// accumulated together, k ascending (in[s][k..k+3] is one 16-byte LDS read,
+// the same address for the whole wave: a broadcast).  With P > 1 (narrow layers) the
 // parts go to `scr` [P][kCtrBS][O] and are added in part order.  With PReLU
 // the pre-activations go to zout [kCtrBS][O].
 __device__ __forceinline__ void ctr_dense_fwd(const float *in, int K, float *out, int O, const float *__restrict__ W,
@@ -146,27 +147,29 @@ __device__ __forceinline__ void ctr_dense_fwd(const float *in, int K, float *out
 #pragma unroll
         for (int s = 0; s < kCtrBS; ++s) acc[s] = 0.f;
         const float *wr = W + (size_t)o * K;
-        const bool v4 = (K & 3) == 0;
-        for (int kb = k0; kb < k1; kb += 16) {
-            float w[16];
-            if (v4 && kb + 16 <= k1) {
+        if ((K & 3) == 0) {
+            // k0 and k1 are multiples of 4: four k per step, each sample's
+            // inputs one 16-byte LDS read, the next step's weights in flight
+            float4 wn = k0 < k1 ? *(const float4 *)(wr + k0) : make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int kb = k0; kb < k1; kb += 4) {
+                const float4 wv = wn;
+                if (kb + 4 < k1) wn = *(const float4 *)(wr + kb + 4);
+                float4 x[kCtrBS];
 #pragma unroll
-                for (int q = 0; q < 4; ++q) {
-                    const float4 x = *(const float4 *)(wr + kb + 4 * q);
-                    w[4 * q] = x.x;
-                    w[4 * q + 1] = x.y;
-                    w[4 * q + 2] = x.z;
-                    w[4 * q + 3] = x.w;
+                for (int s = 0; s < kCtrBS; ++s) x[s] = *(const float4 *)(in + s * K + kb);
+#pragma unroll
+                for (int s = 0; s < kCtrBS; ++s) {
+                    acc[s] = fmaf(x[s].x, wv.x, acc[s]);
+                    acc[s] = fmaf(x[s].y, wv.y, acc[s]);
+                    acc[s] = fmaf(x[s].z, wv.z, acc[s]);
+                    acc[s] = fmaf(x[s].w, wv.w, acc[s]);
                 }
-            } else {
-#pragma unroll
-                for (int q = 0; q < 16; ++q) w[q] = kb + q < k1 ? wr[kb + q] : 0.f;
             }
+        } else {
+            for (int k = k0; k < k1; ++k) {
+                const float wk = wr[k];
 #pragma unroll
-            for (int q = 0; q < 16; ++q) {
-                if (kb + q >= k1) break;
-#pragma unroll
-                for (int s = 0; s < kCtrBS; ++s) acc[s] = fmaf(in[s * K + kb + q], w[q], acc[s]);
+                for (int s = 0; s < kCtrBS; ++s) acc[s] = fmaf(in[s * K + k], wk, acc[s]);
             }
         }
         if (P == 1) {
@@ -197,9 +200,9 @@ __device__ __forceinline__ void ctr_dense_fwd(const float *in, int K, float *out
 // first layer): ReLU takes d where in > 0; PReLU reads its pre-activation z
 // from gin (left there by the forward) and takes d for z > 0, slope[k] d
 // otherwise, and adds d min(z, 0) over the block's samples (ascending) into
-// the slope gradient dsl[k].  Work item (k, part p of P over O); the lanes of
-// a wave take consecutive k, so each W row read is contiguous across the
-// wave; 8 rows in flight.  Parts are added in order through `scr` as in the
+// the slope gradient dsl[k].  Work item (k, part p of P over O, o ascending);
+// the lanes of a wave take consecutive k, so each W row read is contiguous
+// across the wave.  Parts are added in order through `scr` as in the
 // forward.
 __device__ __forceinline__ void ctr_act_bwd(float *gin, const float *in, int K, int k, const float (&d)[kCtrBS],
                                             bool act, const float *__restrict__ slope, float *dsl)
@@ -230,22 +233,43 @@ __device__ __forceinline__ void ctr_dense_bwd_data(const float *gout, int O, flo
                                                    const float *__restrict__ slope, float *dsl, float *scr, int t)
 {
     const int P = ctr_bwd_parts(K, O);
-    const int OC = (O + P - 1) / P;
+    const int OC = (((O + P - 1) / P) + 3) & ~3;
     for (int it = t; it < K * P; it += kThreads) {
         const int k = it % K, pp = it / K;
         const int o0 = pp * OC, o1 = min(O, o0 + OC);
         float acc[kCtrBS];
 #pragma unroll
         for (int s = 0; s < kCtrBS; ++s) acc[s] = 0.f;
-        for (int ob = o0; ob < o1; ob += 8) {
-            float w[8];
+        if ((O & 3) == 0) {
+            // four o per step: the samples' gradients as 16-byte LDS reads,
+            // the next step's four W values in flight
+            float wn[4];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) w[q] = ob + q < o1 ? W[(size_t)(ob + q) * K + k] : 0.f;
+            for (int q = 0; q < 4; ++q) wn[q] = o0 < o1 ? W[(size_t)(o0 + q) * K + k] : 0.f;
+            for (int ob = o0; ob < o1; ob += 4) {
+                float w[4];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) {
-                if (ob + q >= o1) break;
+                for (int q = 0; q < 4; ++q) w[q] = wn[q];
+                if (ob + 4 < o1) {
 #pragma unroll
-                for (int s = 0; s < kCtrBS; ++s) acc[s] = fmaf(gout[s * O + ob + q], w[q], acc[s]);
+                    for (int q = 0; q < 4; ++q) wn[q] = W[(size_t)(ob + 4 + q) * K + k];
+                }
+                float4 g[kCtrBS];
+#pragma unroll
+                for (int s = 0; s < kCtrBS; ++s) g[s] = *(const float4 *)(gout + s * O + ob);
+#pragma unroll
+                for (int s = 0; s < kCtrBS; ++s) {
+                    acc[s] = fmaf(g[s].x, w[0], acc[s]);
+                    acc[s] = fmaf(g[s].y, w[1], acc[s]);
+                    acc[s] = fmaf(g[s].z, w[2], acc[s]);
+                    acc[s] = fmaf(g[s].w, w[3], acc[s]);
+                }
+            }
+        } else {
+            for (int o = o0; o < o1; ++o) {
+                const float wo = W[(size_t)o * K + k];
+#pragma unroll
+                for (int s = 0; s < kCtrBS; ++s) acc[s] = fmaf(gout[s * O + o], wo, acc[s]);
             }
         }
         if (P == 1) {
@@ -277,6 +301,7 @@ __device__ __forceinline__ void ctr_dense_bwd_weight(const float *gout, int O, c
                                                      float *__restrict__ p, int t)
 {
     const int to = (O + 3) / 4, tk = (K + 3) / 4;
+    const bool v4 = ((O | K) & 3) == 0;
     for (int it = t; it < to * tk; it += kThreads) {
         const int o0 = 4 * (it / tk), k0 = 4 * (it % tk);
         float acc[4][4];
@@ -284,17 +309,31 @@ __device__ __forceinline__ void ctr_dense_bwd_weight(const float *gout, int O, c
         for (int i = 0; i < 4; ++i)
 #pragma unroll
             for (int j = 0; j < 4; ++j) acc[i][j] = 0.f;
+        if (v4) {
+            // two 16-byte LDS reads per sample feed 16 FMAs
 #pragma unroll 4
-        for (int s = 0; s < kCtrBS; ++s) {
-            float g[4], x[4];
+            for (int s = 0; s < kCtrBS; ++s) {
+                const float4 g = *(const float4 *)(gout + s * O + o0);
+                const float4 x = *(const float4 *)(in + s * K + k0);
+                const float gv[4] = {g.x, g.y, g.z, g.w}, xv[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
-            for (int i = 0; i < 4; ++i) g[i] = o0 + i < O ? gout[s * O + o0 + i] : 0.f;
+                for (int i = 0; i < 4; ++i)
 #pragma unroll
-            for (int j = 0; j < 4; ++j) x[j] = k0 + j < K ? in[s * K + k0 + j] : 0.f;
+                    for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(gv[i], xv[j], acc[i][j]);
+            }
+        } else {
+#pragma unroll 4
+            for (int s = 0; s < kCtrBS; ++s) {
+                float g[4], x[4];
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
+                for (int i = 0; i < 4; ++i) g[i] = o0 + i < O ? gout[s * O + o0 + i] : 0.f;
 #pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(g[i], x[j], acc[i][j]);
+                for (int j = 0; j < 4; ++j) x[j] = k0 + j < K ? in[s * K + k0 + j] : 0.f;
+#pragma unroll
+                for (int i = 0; i < 4; ++i)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(g[i], x[j], acc[i][j]);
+            }
         }
 #pragma unroll
         for (int i = 0; i < 4; ++i)
@@ -609,18 +648,60 @@ __global__ __launch_bounds__(kThreads) void adagrad_k(int D, const int32_t *__re
 
 // ------------------------------------------------------------------- Adam
 
+struct AdamK {
+    float lr, b1, b2, eps, c1, c2;
+};
+
+__device__ __forceinline__ float adam_one(float p, float g, float &m, float &v, const AdamK &k)
+{
+    m = k.b1 * m + (1.f - k.b1) * g;
+    v = k.b2 * v + (1.f - k.b2) * g * g;
+    return p - k.lr * (m / k.c1) / (sqrtf(v / k.c2) + k.eps);
+}
+
+// Scalar form: any alignment.
 __global__ __launch_bounds__(kThreads) void adam_k(int64_t n, float *__restrict__ param,
                                                    const float *__restrict__ grad, float *__restrict__ m,
-                                                   float *__restrict__ v, float lr, float b1, float b2, float eps,
-                                                   float c1, float c2, uint16_t *__restrict__ pb)
+                                                   float *__restrict__ v, AdamK k, uint16_t *__restrict__ pb)
 {
     for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n; i += (int64_t)gridDim.x * kThreads) {
-        const float g = grad[i];
-        const float mi = b1 * m[i] + (1.f - b1) * g;
-        const float vi = b2 * v[i] + (1.f - b2) * g * g;
+        float mi = m[i], vi = v[i];
+        const float p = adam_one(param[i], grad[i], mi, vi, k);
         m[i] = mi;
         v[i] = vi;
-        const float p = param[i] - lr * (mi / c1) / (sqrtf(vi / c2) + eps);
+        param[i] = p;
+        if (pb) pb[i] = ams_f32_to_bf16(p);
+    }
+}
+
+// 16-byte form (param, grad, m, v 16-byte aligned, the bf16 copy 8-byte
+// aligned): quad q = elements 4q..4q+3; the n % 4 last elements go to the
+// first threads of the grid.  Same arithmetic per element as adam_k.
+__global__ __launch_bounds__(kThreads) void adam4_k(int64_t n, float *__restrict__ param,
+                                                    const float *__restrict__ grad, float *__restrict__ m,
+                                                    float *__restrict__ v, AdamK k, uint16_t *__restrict__ pb)
+{
+    const int64_t nq = n / 4, t0 = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    for (int64_t q = t0; q < nq; q += (int64_t)gridDim.x * kThreads) {
+        const float4 g = ((const float4 *)grad)[q];
+        float4 p = ((float4 *)param)[q], mm = ((float4 *)m)[q], vv = ((float4 *)v)[q];
+        p.x = adam_one(p.x, g.x, mm.x, vv.x, k);
+        p.y = adam_one(p.y, g.y, mm.y, vv.y, k);
+        p.z = adam_one(p.z, g.z, mm.z, vv.z, k);
+        p.w = adam_one(p.w, g.w, mm.w, vv.w, k);
+        ((float4 *)param)[q] = p;
+        ((float4 *)m)[q] = mm;
+        ((float4 *)v)[q] = vv;
+        if (pb)
+            ((uint2 *)pb)[q] = make_uint2((uint32_t)ams_f32_to_bf16(p.x) | ((uint32_t)ams_f32_to_bf16(p.y) << 16),
+                                          (uint32_t)ams_f32_to_bf16(p.z) | ((uint32_t)ams_f32_to_bf16(p.w) << 16));
+    }
+    const int64_t i = 4 * nq + t0;
+    if (i < n) {
+        float mi = m[i], vi = v[i];
+        const float p = adam_one(param[i], grad[i], mi, vi, k);
+        m[i] = mi;
+        v[i] = vi;
         param[i] = p;
         if (pb) pb[i] = ams_f32_to_bf16(p);
     }
@@ -861,12 +942,16 @@ extern "C" ams_status ams_adam_update(int64_t n, float *param, const float *grad
     if (n == 0) return AMS_OK;
     if (!param || !grad || !m || !v) return AMS_ERR_NULL;
     // bias corrections of step t, formed in double on the host
-    const float c1 = (float)(1.0 - pow((double)b1, (double)t));
-    const float c2 = (float)(1.0 - pow((double)b2, (double)t));
+    AdamK k{lr, b1, b2, eps, (float)(1.0 - pow((double)b1, (double)t)), (float)(1.0 - pow((double)b2, (double)t))};
     hipStream_t st = (hipStream_t)stream;
-    int64_t g = (n + kThreads - 1) / kThreads;
+    const bool v4 = ((((uintptr_t)param | (uintptr_t)grad | (uintptr_t)m | (uintptr_t)v) & 15) == 0) &&
+                    (((uintptr_t)param_bf16 & 7) == 0);
+    const int64_t work = v4 ? (n + 3) / 4 : n;
+    int64_t g = (work + kThreads - 1) / kThreads;
     if (g > 4096) g = 4096;
-    AMS_LAUNCH("adam_update", st, adam_k<<<(unsigned)g, kThreads, 0, st>>>(n, param, grad, m, v, lr, b1, b2, eps, c1,
-                                                                          c2, param_bf16));
+    if (v4)
+        AMS_LAUNCH("adam_update", st, adam4_k<<<(unsigned)g, kThreads, 0, st>>>(n, param, grad, m, v, k, param_bf16));
+    else
+        AMS_LAUNCH("adam_update", st, adam_k<<<(unsigned)g, kThreads, 0, st>>>(n, param, grad, m, v, k, param_bf16));
     return ams_launch_status();
 }
