@@ -91,11 +91,18 @@ struct CtrArgs {
 };
 
 // A block's partial row holds, per layer, dW [O x K], db [O] and, below the
-// last layer, the slope gradient [O]; the CTR row ends with the loss sum.
+// last layer, the slope gradient [O], each layer's part starting on a
+// 16-byte boundary (padded to 4 floats); after the net(s) come 4 floats
+// whose first is the loss sum, so rows are 16-byte multiples.
+__host__ __device__ inline int net_layer_size(const CtrArgs &a, int l)
+{
+    return (a.dims[l + 1] * a.dims[l] + a.dims[l + 1] * (l < a.L - 1 ? 2 : 1) + 3) & ~3;
+}
+
 __host__ __device__ inline int net_part_size(const CtrArgs &a)
 {
     int n = 0;
-    for (int l = 0; l < a.L; ++l) n += a.dims[l + 1] * a.dims[l] + a.dims[l + 1] * (l < a.L - 1 ? 2 : 1);
+    for (int l = 0; l < a.L; ++l) n += net_layer_size(a, l);
     return n;
 }
 
@@ -148,21 +155,34 @@ __device__ __forceinline__ void ctr_dense_fwd(const float *in, int K, float *out
         for (int s = 0; s < kCtrBS; ++s) acc[s] = 0.f;
         const float *wr = W + (size_t)o * K;
         if ((K & 3) == 0) {
-            // k0 and k1 are multiples of 4: four k per step, each sample's
-            // inputs one 16-byte LDS read, the next step's weights in flight
-            float4 wn = k0 < k1 ? *(const float4 *)(wr + k0) : make_float4(0.f, 0.f, 0.f, 0.f);
-            for (int kb = k0; kb < k1; kb += 4) {
-                const float4 wv = wn;
-                if (kb + 4 < k1) wn = *(const float4 *)(wr + kb + 4);
-                float4 x[kCtrBS];
+            // k0 and k1 are multiples of 4: 16 k per step in four groups of
+            // four, each sample's inputs of a group one 16-byte LDS read; the
+            // next step's 16 weights are loaded while this step computes
+            float4 wn[4];
 #pragma unroll
-                for (int s = 0; s < kCtrBS; ++s) x[s] = *(const float4 *)(in + s * K + kb);
+            for (int q = 0; q < 4; ++q)
+                wn[q] = k0 + 4 * q < k1 ? *(const float4 *)(wr + k0 + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+            for (int kb = k0; kb < k1; kb += 16) {
+                float4 wv[4];
 #pragma unroll
-                for (int s = 0; s < kCtrBS; ++s) {
-                    acc[s] = fmaf(x[s].x, wv.x, acc[s]);
-                    acc[s] = fmaf(x[s].y, wv.y, acc[s]);
-                    acc[s] = fmaf(x[s].z, wv.z, acc[s]);
-                    acc[s] = fmaf(x[s].w, wv.w, acc[s]);
+                for (int q = 0; q < 4; ++q) wv[q] = wn[q];
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (kb + 16 + 4 * q < k1) wn[q] = *(const float4 *)(wr + kb + 16 + 4 * q);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    if (kb + 4 * q < k1) {
+                        float4 x[kCtrBS];
+#pragma unroll
+                        for (int s = 0; s < kCtrBS; ++s) x[s] = *(const float4 *)(in + s * K + kb + 4 * q);
+#pragma unroll
+                        for (int s = 0; s < kCtrBS; ++s) {
+                            acc[s] = fmaf(x[s].x, wv[q].x, acc[s]);
+                            acc[s] = fmaf(x[s].y, wv[q].y, acc[s]);
+                            acc[s] = fmaf(x[s].z, wv[q].z, acc[s]);
+                            acc[s] = fmaf(x[s].w, wv[q].w, acc[s]);
+                        }
+                    }
                 }
             }
         } else {
@@ -241,28 +261,33 @@ __device__ __forceinline__ void ctr_dense_bwd_data(const float *gout, int O, flo
 #pragma unroll
         for (int s = 0; s < kCtrBS; ++s) acc[s] = 0.f;
         if ((O & 3) == 0) {
-            // four o per step: the samples' gradients as 16-byte LDS reads,
-            // the next step's four W values in flight
-            float wn[4];
+            // 16 o per step in groups of four: the samples' gradients of a
+            // group as 16-byte LDS reads; the next step's 16 W values are
+            // loaded while this step computes
+            float wn[16];
 #pragma unroll
-            for (int q = 0; q < 4; ++q) wn[q] = o0 < o1 ? W[(size_t)(o0 + q) * K + k] : 0.f;
-            for (int ob = o0; ob < o1; ob += 4) {
-                float w[4];
+            for (int q = 0; q < 16; ++q) wn[q] = o0 + q < o1 ? W[(size_t)(o0 + q) * K + k] : 0.f;
+            for (int ob = o0; ob < o1; ob += 16) {
+                float w[16];
 #pragma unroll
-                for (int q = 0; q < 4; ++q) w[q] = wn[q];
-                if (ob + 4 < o1) {
+                for (int q = 0; q < 16; ++q) w[q] = wn[q];
 #pragma unroll
-                    for (int q = 0; q < 4; ++q) wn[q] = W[(size_t)(ob + 4 + q) * K + k];
-                }
-                float4 g[kCtrBS];
+                for (int q = 0; q < 16; ++q)
+                    if (ob + 16 + q < o1) wn[q] = W[(size_t)(ob + 16 + q) * K + k];
 #pragma unroll
-                for (int s = 0; s < kCtrBS; ++s) g[s] = *(const float4 *)(gout + s * O + ob);
+                for (int q = 0; q < 4; ++q) {
+                    if (ob + 4 * q < o1) {
+                        float4 g[kCtrBS];
 #pragma unroll
-                for (int s = 0; s < kCtrBS; ++s) {
-                    acc[s] = fmaf(g[s].x, w[0], acc[s]);
-                    acc[s] = fmaf(g[s].y, w[1], acc[s]);
-                    acc[s] = fmaf(g[s].z, w[2], acc[s]);
-                    acc[s] = fmaf(g[s].w, w[3], acc[s]);
+                        for (int s = 0; s < kCtrBS; ++s) g[s] = *(const float4 *)(gout + s * O + ob + 4 * q);
+#pragma unroll
+                        for (int s = 0; s < kCtrBS; ++s) {
+                            acc[s] = fmaf(g[s].x, w[4 * q], acc[s]);
+                            acc[s] = fmaf(g[s].y, w[4 * q + 1], acc[s]);
+                            acc[s] = fmaf(g[s].z, w[4 * q + 2], acc[s]);
+                            acc[s] = fmaf(g[s].w, w[4 * q + 3], acc[s]);
+                        }
+                    }
                 }
             }
         } else {
@@ -335,11 +360,19 @@ __device__ __forceinline__ void ctr_dense_bwd_weight(const float *gout, int O, c
                     for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(g[i], x[j], acc[i][j]);
             }
         }
+        if (v4) {
+            // a row of the tile is 16 contiguous bytes; across the lanes of a
+            // wave (consecutive k0) the stores are contiguous
 #pragma unroll
-        for (int i = 0; i < 4; ++i)
+            for (int i = 0; i < 4; ++i)
+                *(float4 *)(p + (o0 + i) * K + k0) = make_float4(acc[i][0], acc[i][1], acc[i][2], acc[i][3]);
+        } else {
 #pragma unroll
-            for (int j = 0; j < 4; ++j)
-                if (o0 + i < O && k0 + j < K) p[(o0 + i) * K + k0 + j] = acc[i][j];
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j)
+                    if (o0 + i < O && k0 + j < K) p[(o0 + i) * K + k0 + j] = acc[i][j];
+        }
     }
     for (int o = t; o < O; o += kThreads) {
         float acc = 0.f;
@@ -423,7 +456,7 @@ __device__ __forceinline__ void net_backward(const CtrArgs &a, const NetLds &n, 
     int woff = 0;
     for (int l = 0; l < a.L; ++l) {
         wo[l] = woff;
-        woff += a.dims[l + 1] * a.dims[l] + a.dims[l + 1] * (l < a.L - 1 ? 2 : 1);
+        woff += net_layer_size(a, l);
     }
     for (int l = a.L - 1; l >= 0; --l) {
         const int K = a.dims[l], O = a.dims[l + 1];
@@ -507,7 +540,7 @@ __global__ __launch_bounds__(kThreads) void ctr_fb_k(CtrArgs a, int B, const int
     if (t == 0) {
         float ls = 0.f;
         for (int s = 0; s < kCtrBS; ++s) ls += lossv[s];
-        p[PS - 1] = ls;
+        p[PS - 4] = ls;
     }
 }
 
@@ -564,15 +597,15 @@ __global__ __launch_bounds__(kThreads) void dssm_fb_k(CtrArgs u, CtrArgs v, int 
     if (t == 0) {
         float ls = 0.f;
         for (int s = 0; s < kCtrBS; ++s) ls += lossv[s];
-        p[PS - 1] = ls;
+        p[PS - 4] = ls;
     }
 }
 
 // Where the reduced partial rows go: per layer (of one net, or of the two
 // towers one after the other) dW, db and, below a net's last layer, the
-// slope gradient (NULL: not stored); the last element is the loss sum.
+// slope gradient (NULL: not stored), at the offsets of the partial row; the loss sum sits at PS - 4.
 struct RedLayer {
-    int K, O, hidden;
+    int off, K, O, hidden;
     float *dW, *db, *ds;
 };
 
@@ -583,28 +616,41 @@ struct CtrOut {
     int B;
 };
 
-// Fixed-order sum of the blocks' partial rows (eight running chains over
-// g = 8 i + r, added r = 0..7), scattered into the gradients and the mean loss.
+// Fixed-order sum of the blocks' partial rows, scattered into the gradients
+// and the mean loss.  A block takes 64 elements; wave q of its 4 sums the
+// q-th quarter of the G rows (eight running chains over g = 8 i + r, added
+// r = 0..7), and the quarters are added in order.
+constexpr int kRedCols = kThreads / 4;
+
 __global__ __launch_bounds__(kThreads) void ctr_reduce_k(const float *__restrict__ part, int G, int PS, CtrOut o)
 {
-    const int e = blockIdx.x * kThreads + threadIdx.x;
-    if (e >= PS) return;
+    __shared__ float q4[4][kRedCols];
+    const int c = threadIdx.x % kRedCols, qt = threadIdx.x / kRedCols;
+    const int e = blockIdx.x * kRedCols + c;
+    const int g0 = (int)((int64_t)qt * G / 4), g1 = (int)((int64_t)(qt + 1) * G / 4);
     float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-    int g = 0;
-    for (; g + 8 <= G; g += 8)
+    if (e < PS) {
+        int g = g0;
+        for (; g + 8 <= g1; g += 8)
 #pragma unroll
-        for (int r = 0; r < 8; ++r) s[r] += part[(size_t)(g + r) * PS + e];
-    for (int r = 0; g + r < G; ++r) s[r] += part[(size_t)(g + r) * PS + e];
-    float tot = 0.f;
+            for (int r = 0; r < 8; ++r) s[r] += part[(size_t)(g + r) * PS + e];
+        for (int r = 0; g + r < g1; ++r) s[r] += part[(size_t)(g + r) * PS + e];
+    }
+    float sub = 0.f;
 #pragma unroll
-    for (int r = 0; r < 8; ++r) tot += s[r];
-    if (e == PS - 1) {
+    for (int r = 0; r < 8; ++r) sub += s[r];
+    q4[qt][c] = sub;
+    __syncthreads();
+    if (qt != 0 || e >= PS) return;
+    const float tot = ((q4[0][c] + q4[1][c]) + q4[2][c]) + q4[3][c];
+    if (e == PS - 4) {
         *o.loss = tot / (float)o.B;
         return;
     }
-    int x = e;
     for (int l = 0; l < o.nl; ++l) {
         const RedLayer &y = o.ly[l];
+        int x = e - y.off;
+        if (x < 0) return;                     // padding before this layer
         const int nw = y.O * y.K;
         if (x < nw) {
             y.dW[x] = tot;
@@ -616,12 +662,9 @@ __global__ __launch_bounds__(kThreads) void ctr_reduce_k(const float *__restrict
             return;
         }
         x -= y.O;
-        if (y.hidden) {
-            if (x < y.O) {
-                if (y.ds) y.ds[x] = tot;
-                return;
-            }
-            x -= y.O;
+        if (y.hidden && x < y.O) {
+            if (y.ds) y.ds[x] = tot;
+            return;
         }
     }
 }
@@ -776,12 +819,15 @@ ams_status net_args(const ams_ctr *net, int32_t n_fields, const float *const *fi
 }
 
 // Reduction targets of one net's layers, appended to o.
-ams_status net_out(const CtrArgs &a, float *const *dW, float *const *db, float *const *dslope, CtrOut &o)
+// base: where this net's part of the partial row starts.
+ams_status net_out(const CtrArgs &a, float *const *dW, float *const *db, float *const *dslope, int base, CtrOut &o)
 {
     if (!dW || !db) return AMS_ERR_NULL;
     for (int l = 0; l < a.L; ++l) {
         if (!dW[l] || !db[l]) return AMS_ERR_NULL;
         RedLayer &y = o.ly[o.nl++];
+        y.off = base;
+        base += net_layer_size(a, l);
         y.K = a.dims[l];
         y.O = a.dims[l + 1];
         y.hidden = l < a.L - 1;
@@ -834,7 +880,7 @@ extern "C" size_t ams_ctr_workspace(const ams_ctr *net, int32_t B)
     a.L = net->n_layers;
     for (int l = 0; l <= a.L; ++l) a.dims[l] = net->dims[l];
     const int G = (B + kCtrBS - 1) / kCtrBS;
-    return al256((size_t)(G > 0 ? G : 1) * (net_part_size(a) + 1) * 4);
+    return al256((size_t)(G > 0 ? G : 1) * (net_part_size(a) + 4) * 4);
 }
 
 extern "C" ams_status ams_ctr_fwd_bwd(const ams_ctr *net, int32_t B, int32_t n_fields, const float *const *fields,
@@ -850,20 +896,20 @@ extern "C" ams_status ams_ctr_fwd_bwd(const ams_ctr *net, int32_t B, int32_t n_f
     ams_status s = net_args(net, n_fields, fields, field_dims, W, b, slope, dfields, a);
     if (s != AMS_OK) return s;
     CtrOut o{};
-    s = net_out(a, dW, db, dslope, o);
+    s = net_out(a, dW, db, dslope, 0, o);
     if (s != AMS_OK) return s;
     if (!labels || !loss) return AMS_ERR_NULL;
     const size_t lds = ctr_lds_bytes(a);
     if (lds > lds_limit()) return AMS_ERR_DIMS;
     const int G = (B + kCtrBS - 1) / kCtrBS;
-    const int PS = net_part_size(a) + 1;
+    const int PS = net_part_size(a) + 4;
     if (!ws || ws_bytes < (size_t)G * PS * 4) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     float *part = (float *)ws;
     AMS_LAUNCH("ctr_fwd_bwd", st, ctr_fb_k<<<G, kThreads, lds, st>>>(a, B, labels, prob, part, PS));
     o.loss = loss;
     o.B = B;
-    AMS_LAUNCH("ctr_reduce", st, ctr_reduce_k<<<(PS + kThreads - 1) / kThreads, kThreads, 0, st>>>(part, G, PS, o));
+    AMS_LAUNCH("ctr_reduce", st, ctr_reduce_k<<<(PS + kRedCols - 1) / kRedCols, kThreads, 0, st>>>(part, G, PS, o));
     return ams_launch_status();
 }
 
@@ -876,7 +922,7 @@ extern "C" size_t ams_dssm_workspace(const ams_ctr *user_net, const ams_ctr *ad_
     for (int l = 0; l <= u.L; ++l) u.dims[l] = user_net->dims[l];
     for (int l = 0; l <= v.L; ++l) v.dims[l] = ad_net->dims[l];
     const int G = (B + kCtrBS - 1) / kCtrBS;
-    return al256((size_t)(G > 0 ? G : 1) * (net_part_size(u) + net_part_size(v) + 1) * 4);
+    return al256((size_t)(G > 0 ? G : 1) * (net_part_size(u) + net_part_size(v) + 4) * 4);
 }
 
 extern "C" ams_status ams_dssm_fwd_bwd(const ams_ctr *user_net, const ams_ctr *ad_net, int32_t B,
@@ -901,23 +947,23 @@ extern "C" ams_status ams_dssm_fwd_bwd(const ams_ctr *user_net, const ams_ctr *a
     s = net_args(ad_net, n_ad_fields, ad_fields, ad_field_dims, Wa, ba, slope_a, dad_fields, v);
     if (s != AMS_OK) return s;
     CtrOut o{};
-    s = net_out(u, dWu, dbu, dslope_u, o);
+    s = net_out(u, dWu, dbu, dslope_u, 0, o);
     if (s != AMS_OK) return s;
-    s = net_out(v, dWa, dba, dslope_a, o);
+    s = net_out(v, dWa, dba, dslope_a, net_part_size(u), o);
     if (s != AMS_OK) return s;
     if (!labels || !loss) return AMS_ERR_NULL;
     const size_t lds = (size_t)(2 * ctr_act_floats(u) + 2 * ctr_act_floats(v) +
                                 max(ctr_scr_floats(u), ctr_scr_floats(v)) + kCtrBS) * 4;
     if (lds > lds_limit()) return AMS_ERR_DIMS;
     const int G = (B + kCtrBS - 1) / kCtrBS;
-    const int PS = net_part_size(u) + net_part_size(v) + 1;
+    const int PS = net_part_size(u) + net_part_size(v) + 4;
     if (!ws || ws_bytes < (size_t)G * PS * 4) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     float *part = (float *)ws;
     AMS_LAUNCH("dssm_fwd_bwd", st, dssm_fb_k<<<G, kThreads, lds, st>>>(u, v, B, labels, prob, part, PS));
     o.loss = loss;
     o.B = B;
-    AMS_LAUNCH("ctr_reduce", st, ctr_reduce_k<<<(PS + kThreads - 1) / kThreads, kThreads, 0, st>>>(part, G, PS, o));
+    AMS_LAUNCH("ctr_reduce", st, ctr_reduce_k<<<(PS + kRedCols - 1) / kRedCols, kThreads, 0, st>>>(part, G, PS, o));
     return ams_launch_status();
 }
 

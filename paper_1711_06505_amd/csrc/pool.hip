@@ -18,6 +18,8 @@
 // order.  Fixed orders throughout: no float atomics, bitwise reproducible.
 #include "ams_device.h"
 
+#include <type_traits>
+
 namespace {
 
 constexpr int kThreads = 256;
@@ -33,12 +35,35 @@ constexpr int kPoolQuery = 3;
 // block dU[i] ([Lc x D]) when p < Lc and nothing otherwise; an ad takes dA.
 constexpr int kPoolConcat = 4;
 
+// Row `row` of a [. x D] float array into DM registers (zero past D): 16-byte
+// loads when D is a multiple of 4 and the array starts on a 16-byte
+// boundary (then every row does), else one load per element.
 template <int DM>
 __device__ __forceinline__ void load_row(const float *__restrict__ E, int row, int D, float (&e)[DM])
 {
     const float *p = E + (size_t)row * D;
+    if (((D & 3) | ((uintptr_t)E & 15)) == 0) {
 #pragma unroll
-    for (int d = 0; d < DM; ++d) e[d] = d < D ? p[d] : 0.f;
+        for (int d4 = 0; d4 < DM / 4; ++d4) {
+            const float4 v = 4 * d4 < D ? *(const float4 *)(p + 4 * d4) : make_float4(0.f, 0.f, 0.f, 0.f);
+            e[4 * d4] = v.x;
+            e[4 * d4 + 1] = v.y;
+            e[4 * d4 + 2] = v.z;
+            e[4 * d4 + 3] = v.w;
+        }
+    } else {
+#pragma unroll
+        for (int d = 0; d < DM; ++d) e[d] = d < D ? p[d] : 0.f;
+    }
+}
+
+// Calls f with the register width DM (12, 16 or 32) that covers D.
+template <class F>
+void with_dm(int D, F f)
+{
+    if (D <= 12) f(std::integral_constant<int, 12>{});
+    else if (D <= 16) f(std::integral_constant<int, 16>{});
+    else f(std::integral_constant<int, 32>{});
 }
 
 template <int MODE, int DM>
@@ -440,20 +465,14 @@ extern "C" ams_status ams_pool_fwd(int32_t mode, int32_t B, int32_t D, const int
     if (!seg_off || !inv || !E || !U || !A) return AMS_ERR_NULL;
     if (mode != AMS_POOL_SUM && !saved) return AMS_ERR_NULL;
     hipStream_t st = (hipStream_t)stream;
-    const bool small = D <= 16;
-    switch (mode) {
-    case AMS_POOL_SUM:
-        small ? launch_fwd<AMS_POOL_SUM, 16>(B, D, seg_off, n_beh, inv, E, U, A, saved, st)
-              : launch_fwd<AMS_POOL_SUM, 32>(B, D, seg_off, n_beh, inv, E, U, A, saved, st);
-        break;
-    case AMS_POOL_MAX:
-        small ? launch_fwd<AMS_POOL_MAX, 16>(B, D, seg_off, n_beh, inv, E, U, A, saved, st)
-              : launch_fwd<AMS_POOL_MAX, 32>(B, D, seg_off, n_beh, inv, E, U, A, saved, st);
-        break;
-    default:
-        small ? launch_fwd<AMS_POOL_ATT, 16>(B, D, seg_off, n_beh, inv, E, U, A, saved, st)
-              : launch_fwd<AMS_POOL_ATT, 32>(B, D, seg_off, n_beh, inv, E, U, A, saved, st);
-    }
+    with_dm(D, [&](auto dm) {
+        constexpr int DM = decltype(dm)::value;
+        switch (mode) {
+        case AMS_POOL_SUM: launch_fwd<AMS_POOL_SUM, DM>(B, D, seg_off, n_beh, inv, E, U, A, saved, st); break;
+        case AMS_POOL_MAX: launch_fwd<AMS_POOL_MAX, DM>(B, D, seg_off, n_beh, inv, E, U, A, saved, st); break;
+        default: launch_fwd<AMS_POOL_ATT, DM>(B, D, seg_off, n_beh, inv, E, U, A, saved, st);
+        }
+    });
     return ams_launch_status();
 }
 
@@ -483,20 +502,22 @@ extern "C" ams_status ams_pool_bwd(int32_t mode, int32_t B, int32_t D, const int
     if (!ws || ws_bytes < p.total) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     char *w = (char *)ws;
-    const bool small = D <= 16;
-#define AMS_POOL_BWD(MODE, DM) \
-    launch_bwd<MODE, DM>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, A, saved, dU, dA, dE, w, p, st)
-    switch (mode) {
-    case AMS_POOL_SUM:
-        if (small) AMS_POOL_BWD(AMS_POOL_SUM, 16); else AMS_POOL_BWD(AMS_POOL_SUM, 32);
-        break;
-    case AMS_POOL_MAX:
-        if (small) AMS_POOL_BWD(AMS_POOL_MAX, 16); else AMS_POOL_BWD(AMS_POOL_MAX, 32);
-        break;
-    default:
-        if (small) AMS_POOL_BWD(AMS_POOL_ATT, 16); else AMS_POOL_BWD(AMS_POOL_ATT, 32);
-    }
-#undef AMS_POOL_BWD
+    with_dm(D, [&](auto dm) {
+        constexpr int DM = decltype(dm)::value;
+        switch (mode) {
+        case AMS_POOL_SUM:
+            launch_bwd<AMS_POOL_SUM, DM>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, A, saved, dU, dA, dE,
+                                         w, p, st);
+            break;
+        case AMS_POOL_MAX:
+            launch_bwd<AMS_POOL_MAX, DM>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, A, saved, dU, dA, dE,
+                                         w, p, st);
+            break;
+        default:
+            launch_bwd<AMS_POOL_ATT, DM>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, A, saved, dU, dA, dE,
+                                         w, p, st);
+        }
+    });
     return ams_launch_status();
 }
 
@@ -509,10 +530,9 @@ extern "C" ams_status ams_pool_query_fwd(int32_t B, int32_t D, const int32_t *se
     if (B == 0) return AMS_OK;
     if (!seg_off || !inv || !E || !Q || !U || !w) return AMS_ERR_NULL;
     hipStream_t st = (hipStream_t)stream;
-    if (D <= 16)
-        launch_fwd<kPoolQuery, 16>(B, D, seg_off, n_beh, inv, E, U, nullptr, w, st, Q);
-    else
-        launch_fwd<kPoolQuery, 32>(B, D, seg_off, n_beh, inv, E, U, nullptr, w, st, Q);
+    with_dm(D, [&](auto dm) {
+        launch_fwd<kPoolQuery, decltype(dm)::value>(B, D, seg_off, n_beh, inv, E, U, nullptr, w, st, Q);
+    });
     return ams_launch_status();
 }
 
@@ -534,12 +554,10 @@ extern "C" ams_status ams_pool_query_bwd(int32_t B, int32_t D, const int32_t *se
     if (!ws || ws_bytes < p.total) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     char *wsc = (char *)ws;
-    if (D <= 16)
-        launch_bwd<kPoolQuery, 16>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, Q, w, dU, nullptr, dE, wsc, p,
-                                   st, dQ, accumulate != 0);
-    else
-        launch_bwd<kPoolQuery, 32>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, Q, w, dU, nullptr, dE, wsc, p,
-                                   st, dQ, accumulate != 0);
+    with_dm(D, [&](auto dm) {
+        launch_bwd<kPoolQuery, decltype(dm)::value>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, Q, w, dU,
+                                                    nullptr, dE, wsc, p, st, dQ, accumulate != 0);
+    });
     return ams_launch_status();
 }
 
@@ -577,11 +595,9 @@ extern "C" ams_status ams_pool_concat_bwd(int32_t B, int32_t D, int32_t Lc, cons
     if (!ws || ws_bytes < p.total) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     char *w = (char *)ws;
-    if (D <= 16)
-        launch_bwd<kPoolConcat, 16>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, nullptr, nullptr, nullptr, nullptr,
-                                    dU, dA, dE, w, p, st, nullptr, 0, Lc);
-    else
-        launch_bwd<kPoolConcat, 32>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, nullptr, nullptr, nullptr, nullptr,
-                                    dU, dA, dE, w, p, st, nullptr, 0, Lc);
+    with_dm(D, [&](auto dm) {
+        launch_bwd<kPoolConcat, decltype(dm)::value>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, nullptr, nullptr,
+                                                     nullptr, nullptr, dU, dA, dE, w, p, st, nullptr, 0, Lc);
+    });
     return ams_launch_status();
 }
