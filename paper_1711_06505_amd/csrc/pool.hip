@@ -5,19 +5,21 @@
 //
 // Forward: one wave per sample; lanes stride over the sample's behaviors,
 // fetch E[inv[j]] (12 floats, L2 resident) and reduce across the wave in a
-// fixed butterfly order.  Attentive pooling makes three passes over its
-// segment: logits and their max, exp-weights and weighted sum, normalisation.
+// fixed butterfly order.  Attentive pooling reads its segment's embeddings
+// once (logits with a running softmax per lane, two rows in flight), then
+// normalises the stored logits into weights.
 //
 // Backward: (1) one wave per sample computes the per-sample terms of the
 // attention gradient and tags every behavior occurrence with its sample;
 // (2) one wave per chunk of 64 positions of the stable occurrence order
 // evaluates each occurrence's embedding gradient and sums runs of equal
-// unique image with a segmented lane scan -- runs wholly inside the chunk go
+// unique image with a segmented lane scan on DPP moves -- runs wholly inside the chunk go
 // straight to dE, runs that cross a chunk edge leave a partial; (3) one wave
 // per chunk in which a crossing run starts adds that run's partials in chunk
 // order.  Fixed orders throughout: no float atomics, bitwise reproducible.
 #include "ams_device.h"
 
+#include <climits>
 #include <type_traits>
 
 namespace {
@@ -129,38 +131,50 @@ __global__ __launch_bounds__(kThreads) void pool_fwd_k(int B, int D, const int32
             if (lane == d && d < D) ((int32_t *)saved)[(size_t)i * D + d] = x;
         }
     } else {
+        // one pass over the embeddings with a running (online) softmax per
+        // lane: max m, denominator den and weighted sum acc, rescaled when
+        // the max grows; the lanes are then brought to the wave's max M.
+        // The logits are kept in w and normalised in a second, cheap pass.
         float a[DM];
         if (MODE == kPoolQuery) load_row<DM>(Q, i, D, a);
         else load_row<DM>(E, ad_row, D, a);
         float *w = (float *)saved;
-        float m = -INFINITY;
-        for (int j = j0 + lane; j < j1; j += AMS_WAVE) {
-            float e[DM];
-            load_row<DM>(E, inv[j], D, e);
-            float s = 0.f;
-#pragma unroll
-            for (int d = 0; d < DM; ++d) s += e[d] * a[d];
-            w[j] = s;                                   // logit, rescaled below
-            m = fmaxf(m, s);
-        }
-        m = ams_wave_max(m);
-        float den = 0.f, acc[DM];
+        float m = -INFINITY, den = 0.f, acc[DM];
 #pragma unroll
         for (int d = 0; d < DM; ++d) acc[d] = 0.f;
-        for (int j = j0 + lane; j < j1; j += AMS_WAVE) {
-            float e[DM];
-            load_row<DM>(E, inv[j], D, e);
-            const float p = expf(w[j] - m);
-            w[j] = p;
-            den += p;
+        auto take = [&](int j, const float (&e)[DM]) {
+            float sc = 0.f;
 #pragma unroll
-            for (int d = 0; d < DM; ++d) acc[d] += p * e[d];
+            for (int d = 0; d < DM; ++d) sc += e[d] * a[d];
+            w[j] = sc;
+            const float mn = fmaxf(m, sc);
+            const float r = expf(m - mn), p = expf(sc - mn);    // m = -inf: r = 0
+            den = den * r + p;
+#pragma unroll
+            for (int d = 0; d < DM; ++d) acc[d] = acc[d] * r + p * e[d];
+            m = mn;
+        };
+        int j = j0 + lane;
+        for (; j + AMS_WAVE < j1; j += 2 * AMS_WAVE) {   // two rows in flight
+            const int r0 = inv[j], r1 = inv[j + AMS_WAVE];
+            float e0[DM], e1[DM];
+            load_row<DM>(E, r0, D, e0);
+            load_row<DM>(E, r1, D, e1);
+            take(j, e0);
+            take(j + AMS_WAVE, e1);
         }
-        den = ams_wave_sum(den);
+        if (j < j1) {
+            float e0[DM];
+            load_row<DM>(E, inv[j], D, e0);
+            take(j, e0);
+        }
+        const float M = ams_wave_max(m);
+        const float f = m == -INFINITY ? 0.f : expf(m - M);      // lanes without behaviors add nothing
+        den = ams_wave_sum(den * f);
         const float inv_den = j1 > j0 ? 1.f / den : 0.f;
 #pragma unroll
-        for (int d = 0; d < DM; ++d) out[d] = ams_wave_sum(acc[d]) * inv_den;
-        for (int j = j0 + lane; j < j1; j += AMS_WAVE) w[j] = w[j] * inv_den;
+        for (int d = 0; d < DM; ++d) out[d] = ams_wave_sum(acc[d] * f) * inv_den;
+        for (int jj = j0 + lane; jj < j1; jj += AMS_WAVE) w[jj] = expf(w[jj] - M) * inv_den;
     }
     float mine = 0.f;
 #pragma unroll
@@ -223,15 +237,27 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_sample(int B, int D, const 
     float acc[DM];
 #pragma unroll
     for (int d = 0; d < DM; ++d) acc[d] = 0.f;
-    for (int j = j0 + lane; j < j1; j += AMS_WAVE) {
-        float e[DM];
-        load_row<DM>(E, inv[j], D, e);
+    auto take = [&](int j, const float (&e)[DM]) {
         float dw = 0.f;
 #pragma unroll
         for (int d = 0; d < DM; ++d) dw += g[d] * e[d];
         const float ds = wsaved[j] * (dw - c);
 #pragma unroll
         for (int d = 0; d < DM; ++d) acc[d] += ds * e[d];
+    };
+    int j = j0 + lane;
+    for (; j + AMS_WAVE < j1; j += 2 * AMS_WAVE) {       // two rows in flight
+        const int r0 = inv[j], r1 = inv[j + AMS_WAVE];
+        float e0[DM], e1[DM];
+        load_row<DM>(E, r0, D, e0);
+        load_row<DM>(E, r1, D, e1);
+        take(j, e0);
+        take(j + AMS_WAVE, e1);
+    }
+    if (j < j1) {
+        float e0[DM];
+        load_row<DM>(E, inv[j], D, e0);
+        take(j, e0);
     }
     float mine = 0.f;
 #pragma unroll
@@ -241,6 +267,41 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_sample(int B, int D, const 
     }
     if (lane < D) da[(size_t)i * D + lane] = mine;
     if (lane == 0) cvec[i] = c;
+}
+
+// One step of the segmented scan: every lane reads (key, values) of the lane
+// that the DPP control CTRL names (row_mask RM: rows not in it read nothing)
+// and adds the values when the keys are equal.  Lanes with no source keep the
+// `old` operand: a key no lane holds, values 0.
+template <int CTRL, int RM, int DM>
+__device__ __forceinline__ void seg_step(int u, float (&v)[DM])
+{
+    const int ou = __builtin_amdgcn_update_dpp(INT_MIN, u, CTRL, RM, 0xF, false);
+    const bool join = ou == u;
+#pragma unroll
+    for (int d = 0; d < DM; ++d) {
+        const float ov = __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v[d]), CTRL, RM, 0xF, false));
+        if (join) v[d] += ov;
+    }
+}
+
+// Inclusive segmented scan over the 64 lanes (runs of equal u contiguous;
+// u is never INT_MIN) on DPP moves, no LDS: within each row of 16 lanes
+// Hillis-Steele steps from 1, 2, 4 and 8 lanes back (row_shr); then lane 15
+// of rows 0 and 2 into rows 1 and 3 (row_bcast:15), then lane 31 into rows 2
+// and 3 (row_bcast:31).  A lane joins a source only when the keys match, so
+// its run then covers every lane in between; after the last step a lane
+// holds the sum from its run's first lane in the wave.  Fixed order, so
+// deterministic.
+template <int DM>
+__device__ __forceinline__ void seg_scan(int u, float (&v)[DM])
+{
+    seg_step<0x111, 0xF, DM>(u, v);
+    seg_step<0x112, 0xF, DM>(u, v);
+    seg_step<0x114, 0xF, DM>(u, v);
+    seg_step<0x118, 0xF, DM>(u, v);
+    seg_step<0x142, 0xA, DM>(u, v);
+    seg_step<0x143, 0xC, DM>(u, v);
 }
 
 // (2) segmented sums over chunks of 64 positions of the stable occurrence order.
@@ -313,17 +374,7 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int64_t n_beh, i
             }
         }
     }
-    // inclusive segmented scan over lanes (runs of equal u are contiguous)
-#pragma unroll
-    for (int o = 1; o < AMS_WAVE; o <<= 1) {
-        const int ou = __shfl_up(u, o, AMS_WAVE);
-        const bool join = lane >= o && ou == u;
-#pragma unroll
-        for (int d = 0; d < DM; ++d) {
-            const float ov = __shfl_up(v[d], o, AMS_WAVE);
-            if (join) v[d] += ov;
-        }
-    }
+    seg_scan<DM>(u, v);
     const int nu_next = __shfl_down(u, 1, AMS_WAVE);
     const bool run_end = valid && (lane == AMS_WAVE - 1 || nu_next != u);
     int cross_u = -1;
