@@ -21,6 +21,7 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kWaves = kThreads / AMS_WAVE;
 constexpr int kCtrBS = 16;                  // samples per block of the CTR kernel
+constexpr int kCtrThreads = 512;            // threads per block of the CTR and tower kernels (2 waves per SIMD)
 constexpr int kCtrMaxIn = 128, kCtrMaxHidden = 256, kCtrMaxC = 8, kTowerMaxOut = 64;
 constexpr int kCtrMaxLayers = 3, kCtrMaxFields = 8;
 
@@ -110,7 +111,7 @@ __host__ __device__ inline int net_part_size(const CtrArgs &a)
 // P * kCtrBS * K (P is chosen as in ctr_dense_fwd / ctr_dense_bwd_data).
 __host__ __device__ inline int ctr_fwd_parts(int K, int O)
 {
-    int P = kThreads / O;
+    int P = kCtrThreads / O;
     if (P < 1) P = 1;
     if (P > (K + 15) / 16) P = (K + 15) / 16;
     return P;
@@ -118,7 +119,7 @@ __host__ __device__ inline int ctr_fwd_parts(int K, int O)
 
 __host__ __device__ inline int ctr_bwd_parts(int K, int O)
 {
-    int P = kThreads / K;
+    int P = kCtrThreads / K;
     if (P < 1) P = 1;
     if (P > (O + 7) / 8) P = (O + 7) / 8;
     return P;
@@ -147,7 +148,7 @@ __device__ __forceinline__ void ctr_dense_fwd(const float *in, int K, float *out
 {
     const int P = ctr_fwd_parts(K, O);
     const int KC = (((K + P - 1) / P) + 3) & ~3;
-    for (int it = t; it < O * P; it += kThreads) {
+    for (int it = t; it < O * P; it += kCtrThreads) {
         const int o = it % O, pp = it / O;
         const int k0 = pp * KC, k1 = min(K, k0 + KC);
         float acc[kCtrBS];
@@ -206,7 +207,7 @@ __device__ __forceinline__ void ctr_dense_fwd(const float *in, int K, float *out
     }
     if (P > 1) {
         __syncthreads();
-        for (int e = t; e < kCtrBS * O; e += kThreads) {
+        for (int e = t; e < kCtrBS * O; e += kCtrThreads) {
             const int o = e % O;
             float v = bias[o];
             for (int pp = 0; pp < P; ++pp) v += scr[pp * kCtrBS * O + e];
@@ -254,7 +255,7 @@ __device__ __forceinline__ void ctr_dense_bwd_data(const float *gout, int O, flo
 {
     const int P = ctr_bwd_parts(K, O);
     const int OC = (((O + P - 1) / P) + 3) & ~3;
-    for (int it = t; it < K * P; it += kThreads) {
+    for (int it = t; it < K * P; it += kCtrThreads) {
         const int k = it % K, pp = it / K;
         const int o0 = pp * OC, o1 = min(O, o0 + OC);
         float acc[kCtrBS];
@@ -306,7 +307,7 @@ __device__ __forceinline__ void ctr_dense_bwd_data(const float *gout, int O, flo
     }
     if (P > 1) {
         __syncthreads();
-        for (int k = t; k < K; k += kThreads) {
+        for (int k = t; k < K; k += kCtrThreads) {
             float d[kCtrBS];
 #pragma unroll
             for (int s = 0; s < kCtrBS; ++s) {
@@ -327,7 +328,7 @@ __device__ __forceinline__ void ctr_dense_bwd_weight(const float *gout, int O, c
 {
     const int to = (O + 3) / 4, tk = (K + 3) / 4;
     const bool v4 = ((O | K) & 3) == 0;
-    for (int it = t; it < to * tk; it += kThreads) {
+    for (int it = t; it < to * tk; it += kCtrThreads) {
         const int o0 = 4 * (it / tk), k0 = 4 * (it % tk);
         float acc[4][4];
 #pragma unroll
@@ -374,7 +375,7 @@ __device__ __forceinline__ void ctr_dense_bwd_weight(const float *gout, int O, c
                     if (o0 + i < O && k0 + j < K) p[(o0 + i) * K + k0 + j] = acc[i][j];
         }
     }
-    for (int o = t; o < O; o += kThreads) {
+    for (int o = t; o < O; o += kCtrThreads) {
         float acc = 0.f;
 #pragma unroll
         for (int s = 0; s < kCtrBS; ++s) acc += gout[s * O + o];
@@ -428,7 +429,7 @@ __device__ __forceinline__ void net_load(const CtrArgs &a, const NetLds &n, int 
     int c0 = 0;
     for (int f = 0; f < a.n_fields; ++f) {
         const int w = a.fdim[f];
-        for (int e = t; e < kCtrBS * w; e += kThreads) {
+        for (int e = t; e < kCtrBS * w; e += kCtrThreads) {
             const int s = e / w, k = e % w;
             n.act[s * K0 + c0 + k] = (b0 + s < B) ? a.field[f][(size_t)(b0 + s) * w + k] : 0.f;
         }
@@ -478,7 +479,7 @@ __device__ __forceinline__ void net_store_dfields(const CtrArgs &a, const NetLds
     for (int f = 0; f < a.n_fields; ++f) {
         const int w = a.fdim[f];
         if (a.dfield[f])
-            for (int e = t; e < kCtrBS * w; e += kThreads) {
+            for (int e = t; e < kCtrBS * w; e += kCtrThreads) {
                 const int s = e / w, k = e % w;
                 if (b0 + s < B) a.dfield[f][(size_t)(b0 + s) * w + k] = n.grd[s * K0 + c0 + k];
             }
@@ -494,7 +495,7 @@ inline size_t ctr_lds_bytes(const CtrArgs &a)
 // One block = kCtrBS samples: forward through every layer in LDS, softmax
 // and cross-entropy, then the backward; the block's gradient and loss sums
 // (over its samples, ascending) go to its partial row.
-__global__ __launch_bounds__(kThreads) void ctr_fb_k(CtrArgs a, int B, const int32_t *__restrict__ labels,
+__global__ __launch_bounds__(kCtrThreads) void ctr_fb_k(CtrArgs a, int B, const int32_t *__restrict__ labels,
                                                      float *__restrict__ prob, float *__restrict__ part, int PS)
 {
     extern __shared__ float lds[];
@@ -550,7 +551,7 @@ __global__ __launch_bounds__(kThreads) void ctr_fb_k(CtrArgs a, int B, const int
 // nothing), divided by B.  Same block layout as the CTR kernel with both
 // towers in LDS; the partial row holds the user tower's gradients, then the
 // ad tower's, then the loss sum.
-__global__ __launch_bounds__(kThreads) void dssm_fb_k(CtrArgs u, CtrArgs v, int B, const int32_t *__restrict__ labels,
+__global__ __launch_bounds__(kCtrThreads) void dssm_fb_k(CtrArgs u, CtrArgs v, int B, const int32_t *__restrict__ labels,
                                                       float *__restrict__ prob, float *__restrict__ part, int PS)
 {
     extern __shared__ float lds[];
@@ -906,7 +907,7 @@ extern "C" ams_status ams_ctr_fwd_bwd(const ams_ctr *net, int32_t B, int32_t n_f
     if (!ws || ws_bytes < (size_t)G * PS * 4) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     float *part = (float *)ws;
-    AMS_LAUNCH("ctr_fwd_bwd", st, ctr_fb_k<<<G, kThreads, lds, st>>>(a, B, labels, prob, part, PS));
+    AMS_LAUNCH("ctr_fwd_bwd", st, ctr_fb_k<<<G, kCtrThreads, lds, st>>>(a, B, labels, prob, part, PS));
     o.loss = loss;
     o.B = B;
     AMS_LAUNCH("ctr_reduce", st, ctr_reduce_k<<<(PS + kRedCols - 1) / kRedCols, kThreads, 0, st>>>(part, G, PS, o));
@@ -960,7 +961,7 @@ extern "C" ams_status ams_dssm_fwd_bwd(const ams_ctr *user_net, const ams_ctr *a
     if (!ws || ws_bytes < (size_t)G * PS * 4) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     float *part = (float *)ws;
-    AMS_LAUNCH("dssm_fwd_bwd", st, dssm_fb_k<<<G, kThreads, lds, st>>>(u, v, B, labels, prob, part, PS));
+    AMS_LAUNCH("dssm_fwd_bwd", st, dssm_fb_k<<<G, kCtrThreads, lds, st>>>(u, v, B, labels, prob, part, PS));
     o.loss = loss;
     o.B = B;
     AMS_LAUNCH("ctr_reduce", st, ctr_reduce_k<<<(PS + kRedCols - 1) / kRedCols, kThreads, 0, st>>>(part, G, PS, o));

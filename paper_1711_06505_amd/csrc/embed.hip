@@ -701,6 +701,8 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
     const int h = lane >> 5, r32 = lane & 31;
     const int kh = wave >> 1, nb = wave & 1, khalf = H / 2, nkb = khalf / 32;
     const int o = nb * 32 + r32;              // this lane's B row (output column)
+    const int n_u = min(*n_uniq_p, cap);
+    if (blockIdx.x * kTailRows >= n_u) return;    // the grid is sized by cap: no chunk for this block
     float4 breg[KB][4];
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb)
@@ -711,7 +713,6 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
                               : make_float4(0.f, 0.f, 0.f, 0.f);
     if (L == 3)
         for (int e = t; e < D * M; e += kThreads) W3s[(e / M) * (kMaxH2 + 1) + e % M] = ld_w(W3, wbf16, e);
-    const int n_u = min(*n_uniq_p, cap);
     const bool relu_a = (L == 3) || final_relu;
     for (int c0 = blockIdx.x * kTailRows; c0 < n_u; c0 += gridDim.x * kTailRows) {
         const int row = c0 + r32;
