@@ -766,6 +766,7 @@ int orc_dense_fwd(int32_t B, int L, const int32_t *dims, const float *const *W, 
     for (int l = 0; l < L; ++l) {
         const int in = dims[l], out = dims[l + 1];
         const double *Zp = Z + zoff - (l > 0 ? (size_t)B * in : 0);
+#pragma omp parallel for schedule(static)
         for (int32_t i = 0; i < B; ++i)
             for (int o = 0; o < out; ++o) {
                 double acc = (double)b[l][o];
@@ -811,6 +812,7 @@ int orc_dense_bwd(int32_t B, int L, const int32_t *dims, const float *const *W, 
     for (int l = L - 1; l >= 0; --l) {
         const int in = dims[l], out = dims[l + 1];
         const double *dz = dZ + zoff[l];
+#pragma omp parallel for schedule(static)
         for (int o = 0; o < out; ++o) {
             double bs = 0.0;
             for (int k = 0; k < in; ++k) dW[woff[l] + (size_t)o * in + k] = 0.0;
@@ -829,10 +831,11 @@ int orc_dense_bwd(int32_t B, int L, const int32_t *dims, const float *const *W, 
             }
             db[boff[l] + o] = bs;
         }
-        if (l > 0)
-            for (int k = 0; k < in; ++k) dslope[soff[l - 1] + k] = 0.0;
-        for (int32_t i = 0; i < B; ++i)
-            for (int k = 0; k < in; ++k) {
+        /* one thread per input unit k: rows i ascending, as in a serial loop */
+#pragma omp parallel for schedule(static)
+        for (int k = 0; k < in; ++k) {
+            double ds = 0.0;
+            for (int32_t i = 0; i < B; ++i) {
                 double dh = 0.0;
                 for (int o = 0; o < out; ++o) dh += dz[(size_t)i * out + o] * (double)W[l][(size_t)o * in + k];
                 if (l == 0) {
@@ -840,9 +843,11 @@ int orc_dense_bwd(int32_t B, int L, const int32_t *dims, const float *const *W, 
                 } else {
                     const double z = Z[zoff[l - 1] + (size_t)i * in + k];
                     dZ[zoff[l - 1] + (size_t)i * in + k] = z > 0.0 ? dh : act_slope(slope, l - 1, k) * dh;
-                    if (!(z > 0.0)) dslope[soff[l - 1] + k] += dh * z;
+                    if (!(z > 0.0)) ds += dh * z;
                 }
             }
+            if (l > 0) dslope[soff[l - 1] + k] = ds;
+        }
     }
     free(dZ);
     return 0;

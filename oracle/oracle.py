@@ -241,8 +241,9 @@ def pool_bwd(mode, seg_off, inv, n_uniq: int, E, fwd: dict, gU, gA=None) -> dict
     dE = np.zeros((max(n_uniq, 1), D), np.float64)
     ge = np.zeros((n_beh + B, D), np.float64) if n_beh + B > 0 else np.zeros((1, D))
     dA = np.zeros((max(B, 1), D), np.float64)
+    U, A = _f64(fwd["U"]), _f64(fwd["A"])      # held: read through raw pointers
     _check(lib.orc_pool_bwd(m, B, D, _ptr(seg_off), n_beh, _ptr(inv), int(n_uniq), _ptr(E),
-                            _ptr(_f64(fwd["U"])), _ptr(_f64(fwd["A"])), _ptr(am), _ptr(w),
+                            _ptr(U), _ptr(A), _ptr(am), _ptr(w),
                             _ptr(gU), _ptr(gA), _ptr(dE), _ptr(ge), _ptr(dA)), "pool_bwd")
     return {"dE": dE[:n_uniq].copy(), "ge": ge[:n_beh + B].copy(), "dA_att": dA[:B].copy()}
 
@@ -430,8 +431,9 @@ def pool_query_bwd(seg_off, inv, n_uniq: int, E, Q, fwd: dict, gU) -> dict:
         w = np.zeros(1)
     dE = np.zeros((max(n_uniq, 1), D))
     dQ = np.zeros((max(B, 1), D))
+    U = _f64(fwd["U"])                         # held: read through a raw pointer
     _check(lib.orc_pool_query_bwd(B, D, _ptr(seg_off), n_beh, _ptr(inv), int(n_uniq), _ptr(E), _ptr(Q),
-                                  _ptr(_f64(fwd["U"])), _ptr(w), _ptr(gU), _ptr(dE), _ptr(dQ)), "pool_query_bwd")
+                                  _ptr(U), _ptr(w), _ptr(gU), _ptr(dE), _ptr(dQ)), "pool_query_bwd")
     return {"dE": dE[:n_uniq].copy(), "dQ": dQ[:B].copy()}
 
 
@@ -501,7 +503,8 @@ def dense_fwd(X, Ws, bs, slopes=None) -> list:
     sl = [None] * L if slopes is None else [None if s is None else _f32list([s])[0] for s in slopes] + [None]
     B = X.shape[0]
     Z = np.zeros(max(sum(B * d for d in dims[1:]), 1))
-    _check(lib.orc_dense_fwd(B, L, _ptr(np.array(dims, np.int32)), _ptr_list(Wn), _ptr_list(bn), _ptr_list(sl[:L]),
+    dims_a = np.array(dims, np.int32)          # held: the C call reads it through a raw pointer
+    _check(lib.orc_dense_fwd(B, L, _ptr(dims_a), _ptr_list(Wn), _ptr_list(bn), _ptr_list(sl[:L]),
                              _ptr(X), _ptr(Z)), "dense_fwd")
     out, o = [], 0
     for d in dims[1:]:
@@ -524,8 +527,9 @@ def dense_bwd(X, Ws, slopes, Z: list, dZL) -> dict:
     db = np.zeros(sum(dims[1:]))
     ds = np.zeros(max(sum(dims[1:-1]), 1))
     dX = np.zeros_like(X)
-    _check(lib.orc_dense_bwd(B, L, _ptr(np.array(dims, np.int32)), _ptr_list(Wn), _ptr_list(sl[:L]), _ptr(X),
-                             _ptr(Zc), _ptr(_f64(dZL)), _ptr(dW), _ptr(db), _ptr(ds), _ptr(dX)), "dense_bwd")
+    dims_a, dZL = np.array(dims, np.int32), _f64(dZL)   # held: read through raw pointers
+    _check(lib.orc_dense_bwd(B, L, _ptr(dims_a), _ptr_list(Wn), _ptr_list(sl[:L]), _ptr(X),
+                             _ptr(Zc), _ptr(dZL), _ptr(dW), _ptr(db), _ptr(ds), _ptr(dX)), "dense_bwd")
     dWs, dbs, dss = [], [], []
     ow = ob = os_ = 0
     for l, (fi, fo) in enumerate(zip(dims[:-1], dims[1:])):

@@ -208,3 +208,26 @@ def test_dssm_linear_towers_closed_form_and_finite_differences():
             lp = oracle.dssm_fwd_bwd(*args_p, y, ([Wu], [bu], None), ([Wa], [ba], None))["loss"]
             lm = oracle.dssm_fwd_bwd(*args_m, y, ([Wu], [bu], None), ([Wa], [ba], None))["loss"]
             assert abs((lp - lm) / (2 * h) - r[key]["dX"][i, k]) < 1e-8
+
+
+def test_dense_with_relu_equals_the_image_model_routine():
+    """The ReLU dense net against the oracle's image-model routines (pinned on
+    their own against torch), at a size where a float32 upstream gradient and
+    every temporary array are large enough to be reused by the allocator if
+    the wrapper let them go before the C call."""
+    rng = np.random.default_rng(8)
+    dims = [512, 128, 64, 12]
+    Ws, bs, _ = _net(rng, dims, prelu=False)
+    T = torch.from_numpy(rng.standard_normal((1500, 512)).astype(np.float32))
+    rows = np.arange(1500, dtype=np.int32)
+    dE = rng.standard_normal((1500, 12)).astype(np.float32)
+    fo = oracle.mlp_fwd(T, rows, Ws, bs)
+    bo = oracle.mlp_bwd(T, rows, Ws, fo, dE)
+    X = T.double().numpy()
+    Z = oracle.dense_fwd(X, Ws, bs, None)
+    for a, b in zip(Z, fo["Z"]):
+        assert np.array_equal(a, b)
+    r = oracle.dense_bwd(X, Ws, None, Z, dE)
+    for l in range(3):
+        assert np.abs(r["dW"][l] - bo["dW"][l]).max() <= 1e-12 * np.abs(bo["dW"][l]).max()
+        assert np.abs(r["db"][l] - bo["db"][l]).max() <= 1e-12 * np.abs(bo["db"][l]).max()
