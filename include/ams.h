@@ -160,11 +160,18 @@ ams_status ams_dedup(const int32_t *ids, int64_t n_occ, int32_t n_ids,
  *                   A row index outside [0, n_rows) reads as a zero row.
  * W1,b1,W2,b2,W3,b3 weights (dtype) and float32 biases; W3/b3 ignored when
  *                   n_layers == 2.
- * H1_save           out, optional: post-ReLU first hidden layer [cap x dims[1]]
- *                   (bf16 in AMS_BF16 mode, float32 otherwise).  Needed by
+ * slope             NULL: ReLU between layers.  Otherwise a host array with
+ *                   one device array per hidden layer (slope[0] [dims[1]],
+ *                   and for 3 layers slope[1] [dims[2]], float32, none NULL):
+ *                   PReLU, z for z > 0 and slope[c] z otherwise, a learnable
+ *                   slope per channel (the activation of section 7.2).
+ *                   AMS_F32 only (DTYPE in AMS_BF16 mode).
+ * H1_save           out, optional: first hidden layer [cap x dims[1]] (bf16 in
+ *                   AMS_BF16 mode, float32 otherwise): post-ReLU, or with
+ *                   PReLU the pre-activation Z1 (bias included).  Needed by
  *                   ams_embed_bwd; pass NULL for inference only.
- * H2_save           out, optional (3 layers): post-ReLU second hidden layer
- *                   [cap x dims[2]] float32.
+ * H2_save           out, optional (3 layers): second hidden layer [cap x
+ *                   dims[2]] float32, post-ReLU, or with PReLU Z2.
  * E                 out: embeddings [cap x D] float32 (row u for uniq[u]).
  * ws                at least ams_embed_workspace(mlp, cap) bytes. */
 size_t ams_embed_workspace(const ams_mlp *mlp, int32_t n_uniq_cap);
@@ -174,6 +181,7 @@ ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n_rows,
                          const void *W1, const float *b1,
                          const void *W2, const float *b2,
                          const void *W3, const float *b3,
+                         const float *const *slope,
                          void *H1_save, float *H2_save, float *E,
                          void *ws, size_t ws_bytes, void *stream);
 
@@ -185,15 +193,20 @@ ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n_rows,
  * otherwise) and dE [cap x D] float32 (from ams_pool_bwd).  Outputs, all float32 and fully
  * overwritten (not accumulated): dW1 [dims[1] x dims[0]], db1, dW2, db2,
  * dW3, db3 (dW3/db3 ignored when n_layers == 2).  Every gradient is a sum over
- * the n_u unique images in a fixed order.  ReLU'(0) = 0. */
+ * the n_u unique images in a fixed order.  ReLU'(0) = 0.  slope as in
+ * ams_embed_fwd (the same arrays, and H1_save / H2_save from that call);
+ * with PReLU, act'(z) = 1 for z > 0 and slope otherwise, and dslope (host
+ * array of device arrays, or NULL: not stored) receives each hidden layer's
+ * slope gradient, sum over unique images of dH * min(Z, 0), overwritten. */
 ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n_rows,
                          const int32_t *uniq, const int32_t *n_uniq,
                          int32_t n_uniq_cap,
                          const void *W1, const void *W2, const void *W3,
+                         const float *const *slope,
                          const void *H1_save, const float *H2_save,
                          const float *E_fwd, const float *dE,
                          float *dW1, float *db1, float *dW2, float *db2,
-                         float *dW3, float *db3,
+                         float *dW3, float *db3, float *const *dslope,
                          void *ws, size_t ws_bytes, void *stream);
 
 /* ---------------------------------------------------------- pool fwd ----

@@ -61,6 +61,7 @@ def load() -> ctypes.CDLL:
     lib = ctypes.CDLL(LIB_PATH)
     P, i32, i64, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_size_t
     M = ctypes.POINTER(ams_mlp)
+    PP = ctypes.POINTER(ctypes.c_void_p)
     lib.ams_status_str.restype = ctypes.c_char_p
     lib.ams_status_str.argtypes = [ctypes.c_int]
     lib.ams_build_info.restype = ctypes.c_char_p
@@ -71,9 +72,10 @@ def load() -> ctypes.CDLL:
     lib.ams_embed_workspace.restype = sz
     lib.ams_embed_workspace.argtypes = [M, i32]
     lib.ams_embed_fwd.restype = ctypes.c_int
-    lib.ams_embed_fwd.argtypes = [M, P, i64, P, P, i32, P, P, P, P, P, P, P, P, P, P, sz, P]
+    lib.ams_embed_fwd.argtypes = [M, P, i64, P, P, i32, P, P, P, P, P, P, PP, P, P, P, P, sz, P]
     lib.ams_embed_bwd.restype = ctypes.c_int
-    lib.ams_embed_bwd.argtypes = [M, P, i64, P, P, i32, P, P, P, P, P, P, P, P, P, P, P, P, P, P, sz, P]
+    lib.ams_embed_bwd.argtypes = [M, P, i64, P, P, i32, P, P, P, PP, P, P, P, P, P, P, P, P, P, P, PP, P, sz,
+                                  P]
     lib.ams_pool_fwd.restype = ctypes.c_int
     lib.ams_pool_fwd.argtypes = [i32, i32, i32, P, i64, P, P, P, P, P, P]
     lib.ams_pool_workspace.restype = sz
@@ -81,7 +83,6 @@ def load() -> ctypes.CDLL:
     lib.ams_pool_bwd.restype = ctypes.c_int
     lib.ams_pool_bwd.argtypes = [i32, i32, i32, P, i64, P, P, P, P, i32, P, P, P, P, P, P, P, P, sz, P]
     C = ctypes.POINTER(ams_ctr)
-    PP = ctypes.POINTER(ctypes.c_void_p)
     lib.ams_bag_fwd.restype = ctypes.c_int
     lib.ams_bag_fwd.argtypes = [i32, i32, P, i64, P, P, i64, P, P]
     lib.ams_bag_workspace.restype = sz
@@ -171,26 +172,28 @@ def ams_embed_workspace(mlp: ams_mlp, n_uniq_cap: int) -> int:
     return load().ams_embed_workspace(ctypes.byref(mlp), int(n_uniq_cap))
 
 
-def ams_embed_fwd(mlp, T, uniq, n_uniq, n_uniq_cap, W, b, H1_save, H2_save, E, ws, stream=None):
+def ams_embed_fwd(mlp, T, uniq, n_uniq, n_uniq_cap, W, b, H1_save, H2_save, E, ws, stream=None, slopes=None):
+    """slopes: None (ReLU) or the PReLU slopes of every hidden layer (float32 mode)."""
     W3 = W[2] if len(W) > 2 else None
     b3 = b[2] if len(b) > 2 else None
     _check(load().ams_embed_fwd(ctypes.byref(mlp), _p(T), T.shape[0], _p(uniq), _p(n_uniq),
                                 int(n_uniq_cap), _p(W[0]), _p(b[0]), _p(W[1]), _p(b[1]), _p(W3), _p(b3),
-                                _p(H1_save), _p(H2_save), _p(E), _p(ws),
+                                _opt_parray(slopes), _p(H1_save), _p(H2_save), _p(E), _p(ws),
                                 ws.numel() * ws.element_size() if ws is not None else 0,
                                 _stream(stream)), "ams_embed_fwd")
 
 
 def ams_embed_bwd(mlp, T, uniq, n_uniq, n_uniq_cap, W, H1_save, H2_save, E_fwd, dE, dW, db, ws,
-                  stream=None):
+                  stream=None, slopes=None, dslopes=None):
+    """slopes as in ams_embed_fwd; dslopes: where the slope gradients go (None: not stored)."""
     W3 = W[2] if len(W) > 2 else None
     dW3 = dW[2] if len(dW) > 2 else None
     db3 = db[2] if len(db) > 2 else None
     _check(load().ams_embed_bwd(ctypes.byref(mlp), _p(T), T.shape[0], _p(uniq), _p(n_uniq),
-                                int(n_uniq_cap), _p(W[0]), _p(W[1]), _p(W3), _p(H1_save), _p(H2_save),
-                                _p(E_fwd), _p(dE), _p(dW[0]), _p(db[0]), _p(dW[1]), _p(db[1]), _p(dW3),
-                                _p(db3), _p(ws), ws.numel() * ws.element_size(), _stream(stream)),
-           "ams_embed_bwd")
+                                int(n_uniq_cap), _p(W[0]), _p(W[1]), _p(W3), _opt_parray(slopes), _p(H1_save),
+                                _p(H2_save), _p(E_fwd), _p(dE), _p(dW[0]), _p(db[0]), _p(dW[1]), _p(db[1]),
+                                _p(dW3), _p(db3), _opt_parray(dslopes), _p(ws), ws.numel() * ws.element_size(),
+                                _stream(stream)), "ams_embed_bwd")
 
 
 def ams_pool_fwd(mode, seg_off, n_beh, inv, E, U, A, saved, stream=None):
@@ -353,11 +356,13 @@ class Step:
 
     Buffers are sized for up to B samples and n_beh_max behaviors; `cap`
     (default B + n_beh_max) bounds the unique count used for grids, since n_u
-    is only known on the device.
+    is only known on the device.  With `prelu` (float32 models) the hidden
+    layers use PReLU: the slopes are passed to run / embed_fwd / embed_bwd
+    and their gradients land in `dslope`.
     """
 
     def __init__(self, dims, dtype: str, mode: str, B: int, n_beh_max: int, final_relu: bool = False,
-                 device="cuda", cap: int | None = None):
+                 device="cuda", cap: int | None = None, prelu: bool = False):
         self.mlp = make_mlp(dims, dtype, final_relu)
         self.dims = tuple(dims)
         self.dtype = dtype
@@ -391,6 +396,7 @@ class Step:
         self.dE = torch.empty((cap1, D), dtype=f32, device=dev)
         self.dW = [torch.empty((o, i), dtype=f32, device=dev) for i, o in zip(dims[:-1], dims[1:])]
         self.db = [torch.empty((o,), dtype=f32, device=dev) for o in dims[1:]]
+        self.dslope = [torch.empty((o,), dtype=f32, device=dev) for o in dims[1:-1]] if prelu else None
         self.ws = None
         self.n_ids = None
 
@@ -409,9 +415,9 @@ class Step:
         ams_dedup(ids, n_ids, self.uniq, self.inv, self.occ_perm, self.uniq_off, self.n_uniq,
                   self.dev_status, self.ws, stream)
 
-    def embed_fwd(self, T, W, b, stream=None):
+    def embed_fwd(self, T, W, b, stream=None, slopes=None):
         ams_embed_fwd(self.mlp, T, self.uniq, self.n_uniq, self.cap, W, b, self.H1, self.H2, self.E,
-                      self.ws, stream)
+                      self.ws, stream, slopes=slopes)
 
     def pool_fwd(self, seg_off, n_beh, stream=None):
         ams_pool_fwd(self.mode, seg_off, n_beh, self.inv, self.E, self.U, self.A, self.saved, stream)
@@ -420,20 +426,23 @@ class Step:
         ams_pool_bwd(self.mode, seg_off, n_beh, self.inv, self.occ_perm, self.uniq_off, self.n_uniq,
                      self.cap, self.E, self.U, self.A, self.saved, dU, dA, self.dE, self.ws, stream)
 
-    def embed_bwd(self, T, W, stream=None):
+    def embed_bwd(self, T, W, stream=None, slopes=None):
         ams_embed_bwd(self.mlp, T, self.uniq, self.n_uniq, self.cap, W, self.H1, self.H2, self.E,
-                      self.dE, self.dW, self.db, self.ws, stream)
+                      self.dE, self.dW, self.db, self.ws, stream, slopes=slopes,
+                      dslopes=self.dslope if slopes is not None else None)
 
-    def run(self, ids, n_ids, T, W, b, seg_off, dU, dA, stream=None):
+    def run(self, ids, n_ids, T, W, b, seg_off, dU, dA, stream=None, slopes=None):
         """The whole step, enqueued on one stream with no host synchronisation."""
         n_beh = ids.numel() - (seg_off.numel() - 1)
         if n_beh > self.n_beh or seg_off.numel() - 1 > self.B:
             raise ValueError("batch larger than the buffers of this Step")
+        if slopes is not None and self.dslope is None:
+            raise ValueError("this Step was built without prelu=True")
         self.dedup(ids, n_ids, stream)
-        self.embed_fwd(T, W, b, stream)
+        self.embed_fwd(T, W, b, stream, slopes=slopes)
         self.pool_fwd(seg_off, n_beh, stream)
         self.pool_bwd(seg_off, n_beh, dU, dA, stream)
-        self.embed_bwd(T, W, stream)
+        self.embed_bwd(T, W, stream, slopes=slopes)
 
 
 class JointStep:

@@ -779,13 +779,14 @@ bool tower_ok(const ams_ctr *net)
     return R >= 1 && R <= kTowerMaxOut;
 }
 
-// LDS a block may have on the current device (64 KiB if it cannot be asked).
+// LDS a block may have on the current device (gfx950's 160 KiB if it cannot
+// be asked).
 size_t lds_limit()
 {
     int dev = 0, n = 0;
     if (hipGetDevice(&dev) != hipSuccess ||
         hipDeviceGetAttribute(&n, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || n <= 0)
-        n = 65536;
+        n = 160 * 1024;
     return (size_t)n;
 }
 

@@ -166,7 +166,7 @@ __global__ __launch_bounds__(kThreads) void l1_fwd_f32(const float *__restrict__
                                                         const int32_t *__restrict__ n_uniq_p,
                                                         int cap, int n_mt, const float *__restrict__ W1,
                                                         const float *__restrict__ b1, int H,
-                                                        float *__restrict__ H1)
+                                                        float *__restrict__ H1, int keep_z)
 {
     using R = L1Ring<NT>;
     constexpr int NB = NT / 64;
@@ -248,7 +248,7 @@ __global__ __launch_bounds__(kThreads) void l1_fwd_f32(const float *__restrict__
             const int r = (wave >> 1) * 32 + acc_row(j, lane);
             const int row = m0 + r;
             const float z = rid[r] >= 0 ? acc[nb][j] + bias : bias;
-            if (row < n_u) H1[(size_t)row * H + col] = fmaxf(z, 0.f);
+            if (row < n_u) H1[(size_t)row * H + col] = keep_z ? z : fmaxf(z, 0.f);
         }
     }
 }
@@ -387,7 +387,7 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
                                                    const TT *__restrict__ W1, const float *__restrict__ b1,
                                                    int H, int G, float *__restrict__ H1,
                                                    uint16_t *__restrict__ H1b, uint16_t *__restrict__ H1lo,
-                                                   float *__restrict__ pbuf)
+                                                   float *__restrict__ pbuf, int keep_z)
 {
     using K = Sk<TT>;
     constexpr int BK = sk_bk<TT>();
@@ -498,7 +498,8 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
 #pragma unroll
                     for (int j = 0; j < 16; ++j) {
                         const int r = wm * 32 * K::MB + mb * 32 + acc_row(j, lane);
-                        const float z = fmaxf(rid[r] >= 0 ? acc[mb][nb][j] + bias : bias, 0.f);
+                        const float z0 = rid[r] >= 0 ? acc[mb][nb][j] + bias : bias;
+                        const float z = keep_z ? z0 : fmaxf(z0, 0.f);
                         if (m0 + r < n_u) {
                             if (H1) H1[(size_t)(m0 + r) * H + col] = z;
                             if (H1b) {
@@ -678,7 +679,7 @@ constexpr int kTailRows = 32;
 // adds the workers' partial tiles in K order, applies b1 and ReLU (ReLU(b1)
 // for a row whose ID is out of range) and writes the finished H1 for the
 // backward.
-template <int L>
+template <int L, bool PR>
 __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int H, int M,
                                                       int D, const void *__restrict__ W2,
                                                       const float *__restrict__ b2,
@@ -691,7 +692,8 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
                                                       const float *__restrict__ pbuf,
                                                       uint16_t *__restrict__ H1b,
                                                       const float *__restrict__ b1,
-                                                      const int32_t *__restrict__ uniq, int64_t n_rows)
+                                                      const int32_t *__restrict__ uniq, int64_t n_rows,
+                                                      const float *__restrict__ s1, const float *__restrict__ s2)
 {
     constexpr int KB = kMaxH1 / 2 / 32;       // 32-k blocks in a K half (at most 4)
     __shared__ float Zp[2][kTailRows][kMaxH2 + 1];
@@ -754,10 +756,12 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
                             a.w += v.w;
                         }
                         const float4 bb = *(const float4 *)&b1[col];
-                        a.x = fmaxf(ok ? a.x + bb.x : bb.x, 0.f);
-                        a.y = fmaxf(ok ? a.y + bb.y : bb.y, 0.f);
-                        a.z = fmaxf(ok ? a.z + bb.z : bb.z, 0.f);
-                        a.w = fmaxf(ok ? a.w + bb.w : bb.w, 0.f);
+                        a.x = ok ? a.x + bb.x : bb.x;
+                        a.y = ok ? a.y + bb.y : bb.y;
+                        a.z = ok ? a.z + bb.z : bb.z;
+                        a.w = ok ? a.w + bb.w : bb.w;
+                        // PReLU keeps Z1 in H1 (activated below); ReLU stores H1
+                        if (!PR) a = make_float4(fmaxf(a.x, 0.f), fmaxf(a.y, 0.f), fmaxf(a.z, 0.f), fmaxf(a.w, 0.f));
                         if (nb == 0 && row < n_u) {
                             *(float4 *)(hrow + kb * 32 + 4 * q) = a;
                             if (H1b) {
@@ -776,6 +780,21 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
 #pragma unroll
                 for (int q = 0; q < 4; ++q)
                     areg[kb][q] = kb < nkb ? *(const float4 *)(hrow + kb * 32 + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        if (PR) {
+            // layer 1's PReLU on this lane's operands (Z1 -> H1), slope per column
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (kb < nkb) {
+                        const float4 a = *(const float4 *)&s1[kh * khalf + kb * 32 + 16 * h + 4 * q];
+                        float4 &z = areg[kb][q];
+                        z.x = z.x > 0.f ? z.x : a.x * z.x;
+                        z.y = z.y > 0.f ? z.y : a.y * z.y;
+                        z.z = z.z > 0.f ? z.z : a.z * z.z;
+                        z.w = z.w > 0.f ? z.w : a.w * z.w;
+                    }
         }
         v16f acc = (v16f){};
 #pragma unroll
@@ -796,11 +815,13 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
         for (int e = t; e < kTailRows * M; e += kThreads) {
             const int r = e / M, oo = e % M;
             float z = Zp[0][r][oo] + Zp[1][r][oo] + b2[oo];
-            if (relu_a) z = fmaxf(z, 0.f);
+            const float zpre = z;                // saved for layer 2's PReLU backward
+            if (PR && L == 3) z = z > 0.f ? z : s2[oo] * z;
+            else if (relu_a) z = fmaxf(z, 0.f);
             h2s[r][oo] = z;
             if (c0 + r < n_u) {
                 if (L == 3) {
-                    if (H2_save) H2_save[(size_t)(c0 + r) * M + oo] = z;
+                    if (H2_save) H2_save[(size_t)(c0 + r) * M + oo] = PR ? zpre : z;
                 } else {
                     E[(size_t)(c0 + r) * M + oo] = z;
                 }
@@ -1117,7 +1138,7 @@ __device__ __forceinline__ float tb_dzl(brsrc_t rdE, brsrc_t rE, int final_relu,
     return (d < D && (!final_relu || e > 0.f)) ? g : 0.f;
 }
 
-template <int L, int SD, typename TW, typename TH>
+template <int L, int SD, typename TW, typename TH, bool PR>
 __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1s,
                                                         const float *__restrict__ H2s,
                                                         const float *__restrict__ Efwd,
@@ -1126,7 +1147,8 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
                                                         const TW *__restrict__ W3, int H, int M, int D,
                                                         int final_relu, const int32_t *__restrict__ n_uniq_p,
                                                         int cap, TH *__restrict__ dZ1, float *__restrict__ part,
-                                                        int PS, float *__restrict__ zero_row, int zero_n)
+                                                        int PS, float *__restrict__ zero_row, int zero_n,
+                                                        const float *__restrict__ s1, const float *__restrict__ s2)
 {
     // the zero row that dW1's padding rows stream (read by the next launch)
     if (blockIdx.x == 0)
@@ -1140,6 +1162,9 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
     // dH1 and dZ2, re-read per chunk (registers hold the chunk's data)
     __shared__ float W2s[kMaxH2 * kMaxH1];
     __shared__ float W3s[2 * SD * kMaxH2];
+    __shared__ float S2s[PR ? kMaxH2 : 1];     // layer 2's PReLU slopes (3 layers)
+    if (PR && L == 3)
+        for (int o = threadIdx.x; o < kMaxH2; o += kTbThreads) S2s[o] = o < M ? s2[o] : 0.f;
     {
         const brsrc_t rW2 = make_buf(W2, (uint32_t)(Mo * H * sizeof(TW)));   // rows o >= Mo read 0
 #pragma unroll 8
@@ -1164,6 +1189,13 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
     v16f dw2[2][2] = {{(v16f){}, (v16f){}}, {(v16f){}, (v16f){}}};   // [o block][i block]
     v16f dw3 = (v16f){};                     // wave ob < 2: lanes <-> o, rows d
     float db1a[2] = {0.f, 0.f}, db2a[2] = {0.f, 0.f}, db3a = 0.f;
+    // PReLU: slope gradients (sum of dH * min(Z, 0)) like db1 / db2, and this
+    // lane's two layer-1 slopes (columns i0 + 32 ib + r32)
+    float ds1a[2] = {0.f, 0.f}, ds2a[2] = {0.f, 0.f};
+    float sl1[2] = {0.f, 0.f};
+    if (PR)
+#pragma unroll
+        for (int ib = 0; ib < 2; ++ib) sl1[ib] = (i0 + 32 * ib + r32 < H) ? s1[i0 + 32 * ib + r32] : 0.f;
     const bool w3_wave = (L == 3) && wave < 2 && 32 * wave < M;
 
     for (int c0 = r0; c0 < r1; c0 += 32) {
@@ -1201,7 +1233,10 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
                 for (int st = 0; st < SD; ++st)   // [o][row]: lanes <-> rows (zeros past D)
                     aB = mfma_f32(W3s[(2 * st + h) * kMaxH2 + r32 + 32 * ob], dzB[st], aB);
 #pragma unroll
-                for (int jj = 0; jj < 16; ++jj) dz2B[jj] = h2B[jj] > 0.f ? aB[jj] : 0.f;
+                for (int jj = 0; jj < 16; ++jj) {
+                    if (PR) dz2B[jj] = h2B[jj] > 0.f ? aB[jj] : S2s[acc_row(jj, lane) + 32 * ob] * aB[jj];
+                    else dz2B[jj] = h2B[jj] > 0.f ? aB[jj] : 0.f;
+                }
             } else {   // 2 layers: dZ2 = dzl itself
 #pragma unroll
                 for (int jj = 0; jj < 16; ++jj)
@@ -1222,14 +1257,23 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
             // dZ1 = dH1 * [H1 > 0], written out (stores past the chunk are
             // dropped by the descriptor; columns past H are not stored); db1
             const int icol = i0 + 32 * ib + r32;
-            float cs = 0.f;
+            float cs = 0.f, css = 0.f;
 #pragma unroll
             for (int jj = 0; jj < 16; ++jj) {
-                const float dz = h1v[ib][jj] > 0.f ? a1[ib][jj] : 0.f;
+                const bool pos = h1v[ib][jj] > 0.f;
+                const float dz = pos ? a1[ib][jj] : (PR ? sl1[ib] * a1[ib][jj] : 0.f);
                 cs += dz;
+                if (PR) css += pos ? 0.f : a1[ib][jj] * h1v[ib][jj];
                 if (icol < H) buf_st<TH>(rZ1, (uint32_t)(acc_row(jj, lane) * H + icol), dz);
             }
             db1a[ib] += cs + __shfl_xor(cs, 32, AMS_WAVE);
+            if (PR) {
+                ds1a[ib] += css + __shfl_xor(css, 32, AMS_WAVE);
+                // from here on the H1 operand of dW2 is the activation
+#pragma unroll
+                for (int jj = 0; jj < 16; ++jj)
+                    if (!(h1v[ib][jj] > 0.f)) h1v[ib][jj] *= sl1[ib];
+            }
         }
         __builtin_amdgcn_sched_barrier(0);
 
@@ -1261,8 +1305,21 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
 #pragma unroll
                 for (int st = 0; st < SD; ++st)   // [row][o]: lanes <-> o (zeros past D)
                     aA = mfma_f32(dzB[st], W3s[(2 * st + h) * kMaxH2 + r32 + 32 * ob], aA);
+                if (PR) {
+                    const float a2 = S2s[r32 + 32 * ob];
+                    float css = 0.f;
 #pragma unroll
-                for (int jj = 0; jj < 16; ++jj) dz2A[jj] = h2A[jj] > 0.f ? aA[jj] : 0.f;
+                    for (int jj = 0; jj < 16; ++jj) {
+                        const bool pos = h2A[jj] > 0.f;
+                        dz2A[jj] = pos ? aA[jj] : a2 * aA[jj];
+                        css += pos ? 0.f : aA[jj] * h2A[jj];
+                        if (!pos) h2A[jj] *= a2;        // H2 = PReLU(Z2): dW3's operand
+                    }
+                    ds2a[ob] += css + __shfl_xor(css, 32, AMS_WAVE);
+                } else {
+#pragma unroll
+                    for (int jj = 0; jj < 16; ++jj) dz2A[jj] = h2A[jj] > 0.f ? aA[jj] : 0.f;
+                }
             } else {
 #pragma unroll
                 for (int jj = 0; jj < 16; ++jj) dz2A[jj] = h2A[jj];
@@ -1317,16 +1374,29 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
         if (i0 + r32 < H) p[i0 + r32] = db1a[0];
         if (i0 + 32 + r32 < H) p[i0 + 32 + r32] = db1a[1];
     }
+    if (PR) {
+        p += H;
+        if (h == 0) {
+            if (i0 + r32 < H) p[i0 + r32] = ds1a[0];
+            if (i0 + 32 + r32 < H) p[i0 + 32 + r32] = ds1a[1];
+        }
+        p += H;
+        if (L == 3 && wave == 0 && h == 0) {
+            if (r32 < M) p[r32] = ds2a[0];
+            if (32 + r32 < M) p[32 + r32] = ds2a[1];
+        }
+    }
 }
 
 // Sum of the tail backward's block partials, written straight into dW2, db2,
-// dW3, db3 and db1.  Thread (e, q) of a block sums partials g = q, q + 4, ...
+// dW3, db3, db1 and (PReLU) the slope gradients.  Thread (e, q) of a block sums partials g = q, q + 4, ...
 // in eight running chains (independent loads in flight); the chains, then the
 // four q, are added in a fixed order, so the result is deterministic.
 __global__ __launch_bounds__(256) void tail_reduce(const float *__restrict__ part, int G, int PS, int L,
                                                    int H, int M, int D, float *__restrict__ dW2,
                                                    float *__restrict__ db2, float *__restrict__ dW3,
-                                                   float *__restrict__ db3, float *__restrict__ db1)
+                                                   float *__restrict__ db3, float *__restrict__ db1,
+                                                   float *__restrict__ ds1, float *__restrict__ ds2)
 {
     __shared__ float sq[4][64];
     const int t = threadIdx.x, q = t >> 6;
@@ -1357,7 +1427,11 @@ __global__ __launch_bounds__(256) void tail_reduce(const float *__restrict__ par
     x -= n3;
     if (x < nb3) { db3[x] = v; return; }
     x -= nb3;
-    db1[x] = v;
+    if (x < H) { db1[x] = v; return; }
+    x -= H;                                     // PReLU slope gradients (slots unused with ReLU)
+    if (x < H) { if (ds1) ds1[x] = v; return; }
+    x -= H;
+    if (L == 3 && x < M && ds2) ds2[x] = v;
 }
 
 // out[e] = sum of part[g * PS + e] over g = 0..G-1, in a fixed association:
@@ -2208,11 +2282,13 @@ int dw1_chunks(const ams_mlp *m)
     return kc < 1 ? 1 : (kc > 32 ? 32 : kc);
 }
 
+// [dW2][db2][dW3][db3][db1], then the PReLU slope gradients [H][M] (their
+// slots are always there and written only in PReLU mode).
 int tail_part_size(const ams_mlp *m)
 {
     const int L = m->n_layers, H = m->dims[1], D = m->dims[L];
     const int M = (L == 3) ? m->dims[2] : D;
-    return M * H + M + ((L == 3) ? D * M + D : 0) + H;
+    return M * H + M + ((L == 3) ? D * M + D : 0) + H + H + ((L == 3) ? M : 0);
 }
 
 // The bf16 backward tail (bf16 MFMA) serves H = 256 with a second-layer
@@ -2272,12 +2348,26 @@ extern "C" size_t ams_embed_workspace(const ams_mlp *mlp, int32_t n_uniq_cap)
     return fwd > bwd ? fwd : bwd;
 }
 
+// PReLU slopes of the hidden layers: NULL (ReLU), or one array per hidden
+// layer, float32 path only.
+ams_status prelu_slopes(const ams_mlp *mlp, const float *const *slope, const float **s1, const float **s2)
+{
+    *s1 = *s2 = nullptr;
+    if (!slope) return AMS_OK;
+    if (mlp->dtype != AMS_F32) return AMS_ERR_DTYPE;
+    for (int l = 0; l < mlp->n_layers - 1; ++l)
+        if (!slope[l]) return AMS_ERR_NULL;
+    *s1 = slope[0];
+    if (mlp->n_layers == 3) *s2 = slope[1];
+    return AMS_OK;
+}
+
 extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n_rows,
                                     const int32_t *uniq, const int32_t *n_uniq, int32_t cap,
                                     const void *W1, const float *b1, const void *W2,
                                     const float *b2, const void *W3, const float *b3,
-                                    void *H1_save, float *H2_save, float *E, void *ws,
-                                    size_t ws_bytes, void *stream)
+                                    const float *const *slope, void *H1_save, float *H2_save, float *E,
+                                    void *ws, size_t ws_bytes, void *stream)
 {
     if (!mlp) return AMS_ERR_NULL;
     if (mlp->dtype != AMS_F32 && mlp->dtype != AMS_BF16) return AMS_ERR_DTYPE;
@@ -2286,6 +2376,12 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
     const int L = mlp->n_layers;
     if (!T || !uniq || !n_uniq || !W1 || !b1 || !W2 || !b2 || !E) return AMS_ERR_NULL;
     if (L == 3 && (!W3 || !b3)) return AMS_ERR_NULL;
+    const float *s1, *s2;
+    {
+        const ams_status ps = prelu_slopes(mlp, slope, &s1, &s2);
+        if (ps != AMS_OK) return ps;
+    }
+    const bool pr = s1 != nullptr;
     if (cap == 0) return AMS_OK;
     const int F = mlp->dims[0], H = mlp->dims[1], D = mlp->dims[L];
     const int M = (L == 3) ? mlp->dims[2] : D;
@@ -2310,18 +2406,19 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
     const int grid = ((n_mt + 7) / 8) * 8 * (H / NT);
     if (sk && !bf) {
         AMS_LAUNCH("l1sk_f32", st, l1sk<float><<<G, kSkThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
-                                                                      (const float *)W1, b1, H, G, H1f, nullptr, nullptr, pbuf));
+                                                                      (const float *)W1, b1, H, G, H1f, nullptr, nullptr, pbuf,
+                                                                      (int)pr));
     } else if (sk) {
         AMS_LAUNCH("l1sk_bf16", st, l1sk<uint16_t><<<G, kSkThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq, n_uniq,
                                                                            cap, (const uint16_t *)W1, b1, H, G, nullptr,
-                                                                           h1b, h1lo, pbuf));
+                                                                           h1b, h1lo, pbuf, 0));
     } else if (!bf) {
         if (NT == 128)
             AMS_LAUNCH("l1_fwd_f32", st, l1_fwd_f32<128><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, n_mt,
-                                                       (const float *)W1, b1, H, H1f));
+                                                       (const float *)W1, b1, H, H1f, (int)pr));
         else
             AMS_LAUNCH("l1_fwd_f32", st, l1_fwd_f32<64><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, n_mt,
-                                                      (const float *)W1, b1, H, H1f));
+                                                      (const float *)W1, b1, H, H1f, (int)pr));
     } else {
         if (NT == 128)
             AMS_LAUNCH("l1_fwd_bf16", st, l1_fwd_bf16<128><<<grid, kThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq, n_uniq,
@@ -2351,24 +2448,25 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
     const int sk_bk = sk ? (bf ? 64 : 32) : 0;      // K per stream-K stage (128 bytes of a row)
     int tg = (cap + kTailRows - 1) / kTailRows;
     if (tg > 1024) tg = 1024;
-    if (L == 3)
-        AMS_LAUNCH("tail_fwd", st, tail_fwd<3><<<tg, kThreads, 0, st>>>(H1f, H, M, D, W2, b2, W3, b3, bf, mlp->final_relu, n_uniq,
-                                             cap, H2_save, E, sk_bk, F, G, pbuf, bf ? (uint16_t *)H1_save : nullptr,
-                                             b1, uniq, n_rows));
-    else
-        AMS_LAUNCH("tail_fwd", st, tail_fwd<2><<<tg, kThreads, 0, st>>>(H1f, H, M, D, W2, b2, W3, b3, bf, mlp->final_relu, n_uniq,
-                                             cap, H2_save, E, sk_bk, F, G, pbuf, bf ? (uint16_t *)H1_save : nullptr,
-                                             b1, uniq, n_rows));
+#define TF_LAUNCH(LL, PRV)                                                                                 \
+    AMS_LAUNCH("tail_fwd", st, (tail_fwd<LL, PRV><<<tg, kThreads, 0, st>>>(                                   \
+                                   H1f, H, M, D, W2, b2, W3, b3, bf, mlp->final_relu, n_uniq, cap, H2_save, E, \
+                                   sk_bk, F, G, pbuf, bf ? (uint16_t *)H1_save : nullptr, b1, uniq, n_rows, s1, s2)))
+    if (L == 3 && pr) TF_LAUNCH(3, true);
+    else if (L == 3) TF_LAUNCH(3, false);
+    else if (pr) TF_LAUNCH(2, true);
+    else TF_LAUNCH(2, false);
+#undef TF_LAUNCH
     return ams_launch_status();
 }
 
 extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n_rows,
                                     const int32_t *uniq, const int32_t *n_uniq, int32_t cap,
                                     const void *W1, const void *W2, const void *W3,
-                                    const void *H1_save, const float *H2_save,
+                                    const float *const *slope, const void *H1_save, const float *H2_save,
                                     const float *E_fwd, const float *dE, float *dW1, float *db1,
-                                    float *dW2, float *db2, float *dW3, float *db3, void *ws,
-                                    size_t ws_bytes, void *stream)
+                                    float *dW2, float *db2, float *dW3, float *db3, float *const *dslope,
+                                    void *ws, size_t ws_bytes, void *stream)
 {
     (void)W1;
     if (!mlp) return AMS_ERR_NULL;
@@ -2380,6 +2478,14 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
         return AMS_ERR_NULL;
     if (L == 3 && (!W3 || !H2_save || !dW3 || !db3)) return AMS_ERR_NULL;
     if (mlp->final_relu && !E_fwd) return AMS_ERR_NULL;
+    const float *s1, *s2;
+    {
+        const ams_status ps = prelu_slopes(mlp, slope, &s1, &s2);
+        if (ps != AMS_OK) return ps;
+    }
+    const bool pr = s1 != nullptr;
+    float *ds1 = (pr && dslope) ? dslope[0] : nullptr;
+    float *ds2 = (pr && dslope && L == 3) ? dslope[1] : nullptr;
     const BwdPlan p = plan_bwd(mlp, cap);
     if (!ws || ws_bytes < p.total) return AMS_ERR_WORKSPACE;
     const int F = mlp->dims[0], H = mlp->dims[1], D = mlp->dims[L];
@@ -2393,17 +2499,17 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
     float *dw1p = (float *)(w + p.off_dw1);
     const int PS = tail_part_size(mlp);
 
-#define TB_LAUNCH(LL, TW, TH)                                                                          \
+#define TB_LAUNCH(LL, TW, TH, PRV)                                                                     \
     if (D <= 16)                                                                                        \
-        AMS_LAUNCH("tail_bwd", st, (tail_bwd<LL, 8, TW, TH><<<kTailBlocks, kTbThreads, 0, st>>>(         \
+        AMS_LAUNCH("tail_bwd", st, (tail_bwd<LL, 8, TW, TH, PRV><<<kTailBlocks, kTbThreads, 0, st>>>(    \
                                        (const TH *)H1_save, H2_save, E_fwd, dE, (const TW *)W2, (const TW *)W3, \
                                        H, M, D, mlp->final_relu, n_uniq, cap, (TH *)dz1, tail, PS, zero, \
-                                       F > H ? F : H)));                                                 \
+                                       F > H ? F : H, s1, s2)));                                         \
     else                                                                                                \
-    AMS_LAUNCH("tail_bwd", st, (tail_bwd<LL, 16, TW, TH><<<kTailBlocks, kTbThreads, 0, st>>>(                \
+    AMS_LAUNCH("tail_bwd", st, (tail_bwd<LL, 16, TW, TH, PRV><<<kTailBlocks, kTbThreads, 0, st>>>(           \
                                    (const TH *)H1_save, H2_save, E_fwd, dE, (const TW *)W2, (const TW *)W3, \
                                    H, M, D, mlp->final_relu, n_uniq, cap, (TH *)dz1, tail, PS, zero,     \
-                                   F > H ? F : H)))
+                                   F > H ? F : H, s1, s2)))
     const int TG = tail_blocks(mlp);
     if (use_tail_bf16(mlp)) {
 #define TBF_LAUNCH(LL, DM)                                                                              \
@@ -2417,17 +2523,21 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
         else TBF_LAUNCH(2, 32);
 #undef TBF_LAUNCH
     } else if (L == 3 && bf) {
-        TB_LAUNCH(3, uint16_t, uint16_t);
+        TB_LAUNCH(3, uint16_t, uint16_t, false);
+    } else if (L == 3 && pr) {
+        TB_LAUNCH(3, float, float, true);
     } else if (L == 3) {
-        TB_LAUNCH(3, float, float);
+        TB_LAUNCH(3, float, float, false);
     } else if (bf) {
-        TB_LAUNCH(2, uint16_t, uint16_t);
+        TB_LAUNCH(2, uint16_t, uint16_t, false);
+    } else if (pr) {
+        TB_LAUNCH(2, float, float, true);
     } else {
-        TB_LAUNCH(2, float, float);
+        TB_LAUNCH(2, float, float, false);
     }
 #undef TB_LAUNCH
     AMS_LAUNCH("tail_reduce", st, tail_reduce<<<(PS + 63) / 64, 256, 0, st>>>(tail, TG, PS, L, H, M, D, dW2,
-                                                                          db2, dW3, db3, db1));
+                                                                          db2, dW3, db3, db1, ds1, ds2));
 
     const int bm = (H % 128 == 0) ? 128 : 64;
     const int nmt = H / bm, outer = (F / 64) * p.kc;

@@ -76,8 +76,8 @@ def test_dedup_host_errors(lib):
     assert lib.ams_dedup(*a) == WS
 
 
-def _embed_args(m):
-    return [ctypes.byref(m), FAKE, 1000, FAKE, FAKE, 100, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE,
+def _embed_args(m, slope=None):
+    return [ctypes.byref(m), FAKE, 1000, FAKE, FAKE, 100, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, slope,
             FAKE, FAKE, FAKE, FAKE, 1 << 30, None]
 
 
@@ -99,16 +99,29 @@ def test_embed_host_errors(lib):
     a = _embed_args(m); a[5] = 0              # nothing to do: returns before any launch
     assert lib.ams_embed_fwd(*a) == OK
     # fp32 without H1_save keeps H1 in the workspace, which is then required
-    a = _embed_args(m); a[12] = None; a[15] = None; a[16] = 0
+    a = _embed_args(m); a[13] = None; a[16] = None; a[17] = 0
     assert lib.ams_embed_fwd(*a) == WS
-    bw = [ctypes.byref(m), FAKE, 1000, FAKE, FAKE, 100, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE,
-          FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 16, None]
+    # PReLU: float32 only, and every hidden layer needs its slopes
+    P = ctypes.c_void_p
+    two = (P * 2)(0x1000, 0x1000)
+    half = (P * 2)(0x1000, None)
+    mb = ams.make_mlp((4096, 256, 64, 12), "bf16")
+    assert lib.ams_embed_fwd(*_embed_args(mb, two)) == DTYPE
+    assert lib.ams_embed_fwd(*_embed_args(m, half)) == NULL
+    a = _embed_args(m, two); a[5] = 0
+    assert lib.ams_embed_fwd(*a) == OK
+    bw = [ctypes.byref(m), FAKE, 1000, FAKE, FAKE, 100, FAKE, FAKE, FAKE, None, FAKE, FAKE, None,
+          FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None, FAKE, 16, None]
     assert lib.ams_embed_bwd(*bw) == WS
-    b2 = list(bw); b2[9] = None               # H1_save
+    b2 = list(bw); b2[10] = None              # H1_save
     assert lib.ams_embed_bwd(*b2) == NULL
     fr = ams.make_mlp((4096, 256, 64, 12), "f32", final_relu=True)
     b3 = list(bw); b3[0] = ctypes.byref(fr)   # final_relu needs the forward's E
     assert lib.ams_embed_bwd(*b3) == NULL
+    b4 = list(bw); b4[0] = ctypes.byref(mb); b4[9] = two
+    assert lib.ams_embed_bwd(*b4) == DTYPE
+    b5 = list(bw); b5[9] = half
+    assert lib.ams_embed_bwd(*b5) == NULL
 
 
 def test_pool_host_errors(lib):
