@@ -2,8 +2,11 @@
 
 A step is the whole hot path on one batch already resident in HBM:
 ams_dedup -> ams_embed_fwd -> ams_pool_fwd -> ams_pool_bwd -> ams_embed_bwd,
-enqueued back to back on one stream.  Distinct seeded batches rotate so a batch
-is never replayed against its own warm cache.  Prints ONE JSON line.
+enqueued back to back on one stream.  The same steps through StepPipeline
+(batch k + 1's dedup on a second stream beside batch k's pooling and
+backward) are reported beside ("pipelined").  Distinct seeded batches rotate
+so a batch is never replayed against its own warm cache.  Prints ONE JSON
+line.
 
     python bench.py [--steps K] [--warmup W] [--workload c1_f32] [--mode att]
 
@@ -209,16 +212,30 @@ def main():
         one(dev_batches[s % len(dev_batches)])
     torch.cuda.synchronize()
 
-    # timed region: K whole steps back to back
+    # timed region: K whole steps back to back on one stream
+    seq = [dev_batches[s % len(dev_batches)] for s in range(args.steps)]
     t_start = torch.cuda.Event(enable_timing=True)
     t_end = torch.cuda.Event(enable_timing=True)
     t_start.record(stream)
-    for s in range(args.steps):
-        one(dev_batches[s % len(dev_batches)])
+    for b in seq:
+        one(b)
     t_end.record(stream)
     torch.cuda.synchronize()
     ms_total = t_start.elapsed_time(t_end)
     ms_step = ms_total / args.steps
+    # the same K steps through StepPipeline (dedup of batch k + 1 on a second
+    # stream beside batch k's pooling and backward), reported beside
+    pipe = ams.StepPipeline(step, w.n_images)
+    pipe.run(seq[:2], T, Wd, bd)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    last = pipe.run(seq, T, Wd, bd)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    assert int(pipe.sets[last]["dev_status"].item()) == 0
+    ms_step_pipe = t_start.elapsed_time(t_end) / args.steps
+    for key in pipe._SET:
+        setattr(step, key, pipe.sets[0][key])
     order = [s % len(dev_batches) for s in range(args.steps)]
     beh_total = sum(dev_batches[i]["n_beh"] for i in order)
     uniq_total = sum(n_uniq[i] for i in order)
@@ -305,6 +322,8 @@ def main():
         "step_hbm_frac": step_bytes / (ms_step * 1e-3) / PEAK_HBM,
         "unique_images_per_s": uniq_total / (ms_total * 1e-3),
         "samples_per_s": w.batch * args.steps / (ms_total * 1e-3),
+        "pipelined": {"value": beh_total / (ms_step_pipe * args.steps * 1e-3), "ms_per_step": ms_step_pipe,
+                      "note": "the same steps through StepPipeline (dedup of the next batch on a second stream)"},
         "cold": {"value": beh_total / (sum(cold_ms) * 1e-3), "ms_per_step": cold_step,
                  "note": "each step timed alone after a 512 MiB device write"},
         "per_call_ms": per,

@@ -445,6 +445,70 @@ class Step:
         self.embed_bwd(T, W, stream, slopes=slopes)
 
 
+class StepPipeline:
+    """Steps of a Step over a sequence of batches, with the dedup of batch
+    k + 1 on a second stream (default priority) beside batch k's pooling and
+    backward.  Two sets of dedup outputs are used alternately, each with its
+    own dedup workspace; events order every use: dedup k + 1 starts after
+    batch k's forward has been enqueued and after batch k - 1 (the last user
+    of its set) has finished, and batch k + 1 waits for it.  Each batch still
+    runs the whole path; only the dedup leaves the critical path.
+    """
+
+    _SET = ("uniq", "inv", "occ_perm", "uniq_off", "n_uniq", "dev_status")
+
+    def __init__(self, step: Step, n_ids: int):
+        self.st = step
+        self.n_ids = int(n_ids)
+        step.alloc_workspace(n_ids)
+        dev = step.uniq.device
+        self.side = torch.cuda.Stream(device=dev)
+        other = {k: torch.empty_like(getattr(step, k)) for k in self._SET}
+        self.sets = [{k: getattr(step, k) for k in self._SET}, other]
+        need = max(ams_dedup_workspace(step.n_occ, self.n_ids), 256)
+        self.dd_ws = [torch.empty(need, dtype=torch.uint8, device=dev) for _ in range(2)]
+        self.ev_dd = [torch.cuda.Event() for _ in range(2)]
+        self.ev_done = [torch.cuda.Event() for _ in range(2)]
+        self.ev_fwd = torch.cuda.Event()
+
+    def _dedup(self, b, s, stream):
+        b["ids"].record_stream(stream)
+        d = self.sets[s]
+        ams_dedup(b["ids"], self.n_ids, d["uniq"], d["inv"], d["occ_perm"], d["uniq_off"], d["n_uniq"],
+                  d["dev_status"], self.dd_ws[s], stream)
+
+    def run(self, batches, T, W, b, slopes=None):
+        """batches: dicts with ids, seg_off, dU, dA, n_beh (device tensors and
+        an int).  Enqueues everything; returns the dedup set index of the last
+        batch (whose outputs the Step's attributes then point at)."""
+        st, main = self.st, torch.cuda.current_stream()
+        n = len(batches)
+        if n == 0:
+            return None
+        self.side.wait_stream(main)               # inputs and earlier users of both sets
+        self._dedup(batches[0], 0, self.side)
+        self.ev_dd[0].record(self.side)
+        for k, bt in enumerate(batches):
+            s = k % 2
+            for key in self._SET:
+                setattr(st, key, self.sets[s][key])
+            main.wait_event(self.ev_dd[s])
+            st.embed_fwd(T, W, b, main, slopes=slopes)
+            if k + 1 < n:
+                self.ev_fwd.record(main)
+                self.side.wait_event(self.ev_fwd)
+                if k >= 1:
+                    self.side.wait_event(self.ev_done[(k + 1) % 2])   # batch k - 1 is done with that set
+                self._dedup(batches[k + 1], (k + 1) % 2, self.side)
+                self.ev_dd[(k + 1) % 2].record(self.side)
+            st.pool_fwd(bt["seg_off"], bt["n_beh"], main)
+            st.pool_bwd(bt["seg_off"], bt["n_beh"], bt["dU"], bt["dA"], main)
+            st.embed_bwd(T, W, main, slopes=slopes)
+            self.ev_done[s].record(main)
+        main.wait_stream(self.side)
+        return (n - 1) % 2
+
+
 class JointStep:
     """Buffers and calls of one joint training step (Algorithm 1: worker
     iteration with the server's embed and update):
