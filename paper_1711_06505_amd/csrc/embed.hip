@@ -734,27 +734,47 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
             slot_a = (tile == (int)(P.it0(wa) / P.S)) ? 0 : 1;
         }
         if (wb > wa) {
-            // tile cut by share boundaries: add the pieces in K order
+            // tile cut by share boundaries: add the pieces in K order, one
+            // share at a time with all of this lane's 16 loads of a share in
+            // flight together (a tile spans at most three shares; more are
+            // looped)
             const int id = uniq[rowc];
             const bool ok = id >= 0 && (int64_t)id < n_rows;
             const int rl = rowc % Sk<float>::BM;
+            const float *pr = pbuf + (size_t)rl * kSkBN + (cbase - cb * kSkBN) + 16 * h;
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) areg[kb][q] = make_float4(0.f, 0.f, 0.f, 0.f);
+            auto add_share = [&](int w, int sl) {
+                const float *pw = pr + ((size_t)w * 2 + sl) * Sk<float>::TILE;
+                float4 v[KB][4];
+#pragma unroll
+                for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q)
+                        v[kb][q] = kb < nkb ? *(const float4 *)(pw + kb * 32 + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+                for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        areg[kb][q].x += v[kb][q].x;
+                        areg[kb][q].y += v[kb][q].y;
+                        areg[kb][q].z += v[kb][q].z;
+                        areg[kb][q].w += v[kb][q].w;
+                    }
+            };
+            add_share(wa, slot_a);
+            if (wa + 1 <= wb) add_share(wa + 1, 0);
+            if (wa + 2 <= wb) add_share(wa + 2, 0);
+            for (int w = wa + 3; w <= wb; ++w) add_share(w, 0);
 #pragma unroll
             for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     const int col = cbase + kb * 32 + 16 * h + 4 * q;
-                    const int cl = col - cb * kSkBN;
-                    float4 a = make_float4(0.f, 0.f, 0.f, 0.f);
+                    float4 a = areg[kb][q];
                     if (kb < nkb) {
-                        for (int w = wa; w <= wb; ++w) {
-                            const int sl = w == wa ? slot_a : 0;
-                            const float4 v =
-                                *(const float4 *)&pbuf[((size_t)w * 2 + sl) * Sk<float>::TILE + rl * kSkBN + cl];
-                            a.x += v.x;
-                            a.y += v.y;
-                            a.z += v.z;
-                            a.w += v.w;
-                        }
                         const float4 bb = *(const float4 *)&b1[col];
                         a.x = ok ? a.x + bb.x : bb.x;
                         a.y = ok ? a.y + bb.y : bb.y;
