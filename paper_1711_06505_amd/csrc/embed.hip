@@ -1777,14 +1777,26 @@ __global__ __launch_bounds__(kDwThreads) void dw1_part_f32(const float *__restri
 // ring like the fp32 kernel.  16-byte chunks are stored at chunk ^ 4 (row & 3):
 // the 4 rows x 64 bytes that a half-wave's transpose reads touch then fall
 // in distinct banks.  Waves are 4 (h) x 2 (f), 64 x 64 each.
-struct DwTr {
-    static constexpr int BM = 256, BN = 128, BK = 64, WAVES = 8;
+// BN = 128: 64 unique images per stage (48 KB slots); BN = 256 (for large
+// unique counts): 32 per stage (32 KB slots), each feature row gathered in
+// 512-byte pieces, half the dZ1 re-reads of BN = 128.
+template <int BN_>
+struct DwTrT {
+    static constexpr int BM = 256, BN = BN_, BK = BN_ == 256 ? 32 : 64, WAVES = 8;
+    static constexpr int NB = BN / 64;                            // 32-column blocks per wave
+    static constexpr int KK = BK / 16;                            // MFMA k steps per stage
     static constexpr int A_BYTES = BK * BM * 2, B_BYTES = BK * BN * 2;
-    static constexpr int SLOT = (A_BYTES + B_BYTES) / 4;           // floats per slot (48 KB)
-    static constexpr int PA = A_BYTES / 1024 / WAVES;             // 4 DMA instructions per wave
-    static constexpr int PB = B_BYTES / 1024 / WAVES;             // 2
+    static constexpr int SLOT = (A_BYTES + B_BYTES) / 4;           // floats per slot
+    static constexpr int PA = A_BYTES / 1024 / WAVES;             // DMA instructions per wave
+    static constexpr int PB = B_BYTES / 1024 / WAVES;
+    static constexpr int CPR = BN * 2 / 16, RPI = 64 / CPR;       // B: 16-byte chunks per row, rows per DMA
     static constexpr int OUTSTANDING = PA + PB + PB;              // DMA of s+1, IDs of s+3
 };
+using DwTr = DwTrT<128>;
+// dW1 tile width for `cap` unique-image slots: the wide tile pays off once
+// each of its blocks has enough rows to amortise its 256 KB partial tile.
+constexpr int kDwTrWideCap = 131072;
+inline int dwtr_bn(int F, int32_t cap) { return (cap >= kDwTrWideCap && F % 256 == 0) ? 256 : 128; }
 
 __device__ __forceinline__ int dwtr_swz(int row) { return (row & 3) << 2; }
 
@@ -1798,44 +1810,46 @@ __device__ __forceinline__ uint2 ds_read_tr16(const void *p)
 }
 
 // IDs of this lane's B rows (one per B DMA instruction) of the stage at u_base
+template <class R>
 __device__ __forceinline__ void dwtr_load_ids(const int32_t *__restrict__ uniq, int u_base, int u1, int wave,
-                                              int lane, int (&id)[2])
+                                              int lane, int (&id)[R::PB])
 {
 #pragma unroll
-    for (int q = 0; q < DwTr::PB; ++q) {
-        const int row = 4 * (DwTr::PB * wave + q) + (lane >> 4);
+    for (int q = 0; q < R::PB; ++q) {
+        const int row = R::RPI * (R::PB * wave + q) + lane / R::CPR;
         const int u = u_base + row;
         const int v = uniq[min(u, u1 - 1)];           // always issued: uniform op count
         id[q] = u < u1 ? v : -1;
     }
 }
 
+template <class R>
 __device__ __forceinline__ void dwtr_issue(float *slot, const uint16_t *__restrict__ T, int64_t n_rows, int F,
                                            const uint16_t *__restrict__ dZ1, int n0, int u_base, int u1,
-                                           const void *__restrict__ zero_row, const int (&id)[2], int wave,
+                                           const void *__restrict__ zero_row, const int (&id)[R::PB], int wave,
                                            int lane)
 {
     // A: 512-byte rows, 2 per instruction
 #pragma unroll
-    for (int q = 0; q < DwTr::PA; ++q) {
-        const int j = DwTr::PA * wave + q;
+    for (int q = 0; q < R::PA; ++q) {
+        const int j = R::PA * wave + q;
         const int row = 2 * j + (lane >> 5), pc = lane & 31;
         const int u = u_base + row;
         const int lc = pc ^ dwtr_swz(row);
-        const char *src = u < u1 ? (const char *)(dZ1 + (size_t)u * DwTr::BM) + lc * 16
+        const char *src = u < u1 ? (const char *)(dZ1 + (size_t)u * R::BM) + lc * 16
                                  : (const char *)zero_row + lc * 16;
         dma16(src, slot + j * 256);
     }
-    // B: 256-byte rows (128 columns from n0), 4 per instruction
+    // B: BN columns from n0 per row, RPI rows per instruction
 #pragma unroll
-    for (int q = 0; q < DwTr::PB; ++q) {
-        const int j = DwTr::PB * wave + q;
-        const int row = 4 * j + (lane >> 4), pc = lane & 15;
+    for (int q = 0; q < R::PB; ++q) {
+        const int j = R::PB * wave + q;
+        const int row = R::RPI * j + lane / R::CPR, pc = lane % R::CPR;
         const int lc = pc ^ dwtr_swz(row);
         const bool ok = id[q] >= 0 && (int64_t)id[q] < n_rows;
         const char *src = ok ? (const char *)(T + (size_t)id[q] * F + n0) + lc * 16
                              : (const char *)zero_row + lc * 16;
-        dma16(src, slot + DwTr::A_BYTES / 4 + j * 256);
+        dma16(src, slot + R::A_BYTES / 4 + j * 256);
     }
 }
 
@@ -1845,55 +1859,58 @@ __device__ __forceinline__ int dwtr_off(int row, int col, int rb)
     return row * rb + (((col >> 3) ^ dwtr_swz(row)) << 4) + ((col & 7) << 1);
 }
 
+template <class R>
 __device__ __forceinline__ void dwtr_compute(const float *slot, v16f *acc, int lane, int wave)
 {
-    const char *A = (const char *)slot, *B = (const char *)slot + DwTr::A_BYTES;
+    const char *A = (const char *)slot, *B = (const char *)slot + R::A_BYTES;
     const int g = lane >> 4, i = lane & 15;
     const int wm = wave >> 1, wn = wave & 1;
     // this lane's transpose-read address: row (i / 4) of its group's 4-row
     // block, columns 4 (i % 4) .. +3 of its group's 16-column half
     const int r_in = 8 * (g >> 1) + (i >> 2);
     const int c_in = 16 * (g & 1) + 4 * (i & 3);
-    uint4 a[4][2], b[4][2];
+    constexpr int NB = R::NB, KK = R::KK;
+    uint4 a[KK][2], b[KK][NB];
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
+    for (int kk = 0; kk < KK; ++kk) {
         const int r0 = 16 * kk + r_in;
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb) {
             const int col = wm * 64 + mb * 32 + c_in;
-            const uint2 lo = ds_read_tr16(A + dwtr_off(r0, col, DwTr::BM * 2));
-            const uint2 hi = ds_read_tr16(A + dwtr_off(r0 + 4, col, DwTr::BM * 2));
+            const uint2 lo = ds_read_tr16(A + dwtr_off(r0, col, R::BM * 2));
+            const uint2 hi = ds_read_tr16(A + dwtr_off(r0 + 4, col, R::BM * 2));
             a[kk][mb] = make_uint4(lo.x, lo.y, hi.x, hi.y);
         }
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
-            const int col = wn * 64 + nb * 32 + c_in;
-            const uint2 lo = ds_read_tr16(B + dwtr_off(r0, col, DwTr::BN * 2));
-            const uint2 hi = ds_read_tr16(B + dwtr_off(r0 + 4, col, DwTr::BN * 2));
+        for (int nb = 0; nb < NB; ++nb) {
+            const int col = wn * (R::BN / 2) + nb * 32 + c_in;
+            const uint2 lo = ds_read_tr16(B + dwtr_off(r0, col, R::BN * 2));
+            const uint2 hi = ds_read_tr16(B + dwtr_off(r0 + 4, col, R::BN * 2));
             b[kk][nb] = make_uint4(lo.x, lo.y, hi.x, hi.y);
         }
     }
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk)
+    for (int kk = 0; kk < KK; ++kk)
 #pragma unroll
         for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-            for (int nb = 0; nb < 2; ++nb) acc[mb * 2 + nb] = mfma_bf16(a[kk][mb], b[kk][nb], acc[mb * 2 + nb]);
+            for (int nb = 0; nb < NB; ++nb) acc[mb * NB + nb] = mfma_bf16(a[kk][mb], b[kk][nb], acc[mb * NB + nb]);
     // k-step 0's reads first, then (reads of kk+1, MFMAs of kk)
-    __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 4 + 2 * NB, 0);
 #pragma unroll
-    for (int kk = 0; kk < 4; ++kk) {
-        if (kk < 3) __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, 4, 0);
+    for (int kk = 0; kk < KK; ++kk) {
+        if (kk < KK - 1) __builtin_amdgcn_sched_group_barrier(0x100, 4 + 2 * NB, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NB, 0);
     }
 }
 
-__global__ __launch_bounds__(DwTr::WAVES * AMS_WAVE) void dw1_part_bf16(
+template <int BN>
+__global__ __launch_bounds__(DwTrT<BN>::WAVES * AMS_WAVE) void dw1_part_bf16(
     const uint16_t *__restrict__ T, int64_t n_rows, int F, const int32_t *__restrict__ uniq,
     const int32_t *__restrict__ n_uniq_p, int cap, const uint16_t *__restrict__ dZ1, int KC,
     const void *__restrict__ zero_row, float *__restrict__ part)
 {
-    using R = DwTr;
+    using R = DwTrT<BN>;
     __shared__ __attribute__((aligned(16))) float ring0[R::SLOT];
     __shared__ __attribute__((aligned(16))) float ring1[R::SLOT];
     __shared__ __attribute__((aligned(16))) float ring2[R::SLOT];
@@ -1907,30 +1924,32 @@ __global__ __launch_bounds__(DwTr::WAVES * AMS_WAVE) void dw1_part_bf16(
     const int n0 = nt * R::BN;
     const int lane = ams_lane(), wave = threadIdx.x / AMS_WAVE;
 
-    v16f acc[4] = {(v16f){}, (v16f){}, (v16f){}, (v16f){}};
+    v16f acc[2 * R::NB];
+#pragma unroll
+    for (int x = 0; x < 2 * R::NB; ++x) acc[x] = (v16f){};
     const int S = (u1 - u0 + R::BK - 1) / R::BK;
     if (S > 0) {
         int id0[2], id1[2], id2[2];
 #define DT_BASE(s) (u0 + min((s), S - 1) * R::BK)
-        dwtr_load_ids(uniq, DT_BASE(0), u1, wave, lane, id0);
-        dwtr_load_ids(uniq, DT_BASE(1), u1, wave, lane, id1);
-        dwtr_load_ids(uniq, DT_BASE(2), u1, wave, lane, id2);
+        dwtr_load_ids<R>(uniq, DT_BASE(0), u1, wave, lane, id0);
+        dwtr_load_ids<R>(uniq, DT_BASE(1), u1, wave, lane, id1);
+        dwtr_load_ids<R>(uniq, DT_BASE(2), u1, wave, lane, id2);
         AMS_WAIT_VM(0);
         int idn[2];
-        dwtr_load_ids(uniq, DT_BASE(3), u1, wave, lane, idn);
-        dwtr_issue(ring0, T, n_rows, F, dZ1, n0, DT_BASE(0), u1, zero_row, id0, wave, lane);
-        dwtr_issue(ring1, T, n_rows, F, dZ1, n0, DT_BASE(1), u1, zero_row, id1, wave, lane);
+        dwtr_load_ids<R>(uniq, DT_BASE(3), u1, wave, lane, idn);
+        dwtr_issue<R>(ring0, T, n_rows, F, dZ1, n0, DT_BASE(0), u1, zero_row, id0, wave, lane);
+        dwtr_issue<R>(ring1, T, n_rows, F, dZ1, n0, DT_BASE(1), u1, zero_row, id1, wave, lane);
 #define DT_STAGE(cur, nxt, ids_next_dma, ids_load, s)                                           \
     do {                                                                                         \
         __builtin_amdgcn_sched_barrier(0);                                                       \
         AMS_WAIT_VM_LDS(R::OUTSTANDING);                                                         \
         __builtin_amdgcn_s_barrier();                                                            \
         __builtin_amdgcn_sched_barrier(0);                                                       \
-        dwtr_load_ids(uniq, DT_BASE((s) + 4), u1, wave, lane, ids_load);                         \
-        dwtr_issue(nxt, T, n_rows, F, dZ1, n0, DT_BASE((s) + 2), u1, zero_row, ids_next_dma, wave, \
+        dwtr_load_ids<R>(uniq, DT_BASE((s) + 4), u1, wave, lane, ids_load);                         \
+        dwtr_issue<R>(nxt, T, n_rows, F, dZ1, n0, DT_BASE((s) + 2), u1, zero_row, ids_next_dma, wave, \
                    lane);                                                                        \
         __builtin_amdgcn_sched_barrier(0);                                                       \
-        dwtr_compute(cur, acc, lane, wave);                                                      \
+        dwtr_compute<R>(cur, acc, lane, wave);                                                      \
     } while (0)
         id0[0] = idn[0];
         id0[1] = idn[1];
@@ -1953,12 +1972,12 @@ __global__ __launch_bounds__(DwTr::WAVES * AMS_WAVE) void dw1_part_bf16(
 #pragma unroll
     for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-        for (int nb = 0; nb < 2; ++nb) {
-            const int col = n0 + wn * 64 + nb * 32 + (lane & 31);
+        for (int nb = 0; nb < R::NB; ++nb) {
+            const int col = n0 + wn * (R::BN / 2) + nb * 32 + (lane & 31);
 #pragma unroll
             for (int j = 0; j < 16; ++j) {
                 const int row = wm * 64 + mb * 32 + acc_row(j, lane);
-                out[(size_t)row * F + col] = acc[mb * 2 + nb][j];
+                out[(size_t)row * F + col] = acc[mb * R::NB + nb][j];
             }
         }
 }
@@ -2287,14 +2306,14 @@ bool use_dw_tr(const ams_mlp *m) { return m->dtype == AMS_BF16 && m->dims[1] == 
 
 // Split-K chunk count of dW1: the DMA-ring kernel takes one block per CU
 // (tiles x chunks = CUs); the fallback kernel aims at ~1024 blocks.
-int dw1_chunks(const ams_mlp *m)
+int dw1_chunks(const ams_mlp *m, int32_t cap)
 {
     const int H = m->dims[1], F = m->dims[0];
     int kc;
     if (use_dw_ring(m)) {
         kc = sk_workers() / (F / DwRing::BN);
     } else if (use_dw_tr(m)) {
-        kc = sk_workers() / (F / DwTr::BN);
+        kc = sk_workers() / (F / dwtr_bn(F, cap));
     } else {
         const int bm = (H % 128 == 0) ? 128 : 64;
         kc = 1024 / ((H / bm) * (F / 64));
@@ -2331,7 +2350,7 @@ BwdPlan plan_bwd(const ams_mlp *m, int32_t cap)
     BwdPlan p{};
     const int H = m->dims[1], F = m->dims[0];
     const size_t es = (m->dtype == AMS_BF16) ? 2 : 4;
-    p.kc = dw1_chunks(m);
+    p.kc = dw1_chunks(m, cap);
     size_t o = 0;
     p.off_zero = o; o += al256((size_t)(F > H ? F : H) * 4);
     p.off_dz1 = o; o += al256((size_t)cap * H * es);
@@ -2567,10 +2586,16 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
         AMS_LAUNCH("dw1_part_f32", st, dw1_part_f32<<<grid8, kDwThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
                                                    (const float *)dz1, H, p.kc, zero, dw1p));
     } else if (use_dw_tr(mlp)) {
-        const int gtr = ((p.kc + 7) / 8) * 8 * (F / DwTr::BN);
-        AMS_LAUNCH("dw1_part_bf16", st, dw1_part_bf16<<<gtr, DwTr::WAVES * AMS_WAVE, 0, st>>>(
-                                            (const uint16_t *)T, n_rows, F, uniq, n_uniq, cap, (const uint16_t *)dz1,
-                                            p.kc, zero, dw1p));
+        const int bn = dwtr_bn(F, cap);
+        const int gtr = ((p.kc + 7) / 8) * 8 * (F / bn);
+        if (bn == 256)
+            AMS_LAUNCH("dw1_part_bf16", st, dw1_part_bf16<256><<<gtr, DwTrT<256>::WAVES * AMS_WAVE, 0, st>>>(
+                                                (const uint16_t *)T, n_rows, F, uniq, n_uniq, cap, (const uint16_t *)dz1,
+                                                p.kc, zero, dw1p));
+        else
+            AMS_LAUNCH("dw1_part_bf16", st, dw1_part_bf16<128><<<gtr, DwTr::WAVES * AMS_WAVE, 0, st>>>(
+                                                (const uint16_t *)T, n_rows, F, uniq, n_uniq, cap, (const uint16_t *)dz1,
+                                                p.kc, zero, dw1p));
     } else if (!bf) {
         if (bm == 128)
             AMS_LAUNCH("dw1_part", st, dw1_part<128, float><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
