@@ -277,22 +277,43 @@ __global__ __launch_bounds__(kThreads) void l1_fwd_f32(const float *__restrict__
 constexpr int kSkThreads = 512;
 constexpr int kSkBN = 256;
 constexpr int kSkNB = kSkBN / 64;                         // 32-column MFMA blocks per wave: 4
-constexpr int kSkRowBytes = 128;                          // bytes of an operand row per stage
 constexpr int kSkMinIters = 32;                           // smallest share worth a worker
 
-template <typename TT>
-struct Sk {
-    static constexpr int BM = 128;                           // image rows per tile
-    static constexpr int R = 3;                              // ring slots
+template <int BM_, int R_, int RB_>
+struct SkShape {
+    static constexpr int BM = BM_;                           // image rows per tile
+    static constexpr int R = R_;                             // ring slots
+    static constexpr int RB = RB_;                           // bytes of an operand row per stage
     static constexpr int MB = BM / 128;                      // 32-row MFMA blocks per wave
     static constexpr int ROWS = BM + kSkBN;                  // A rows then B rows
-    static constexpr int SLOT = ROWS * kSkRowBytes / 4;      // floats per ring slot
-    static constexpr int PW = ROWS / 64;                     // DMA instructions per wave
+    static constexpr int SLOT = ROWS * RB / 4;               // floats per ring slot
+    static constexpr int CPR = RB / 16;                      // 16-byte chunks per stage row
+    static constexpr int RPI = 64 / CPR;                     // rows per DMA instruction
+    static constexpr int PW = ROWS / RPI / (kSkThreads / 64); // DMA instructions per wave
+    static constexpr int G = CPR / 2;                        // k groups per stage (chunk h G + g)
     static constexpr int TILE = BM * kSkBN;                  // floats per partial tile
 };
 
+// 128-row tiles, 128-byte stage rows, 3 slots (48 KB each) for both types.
+// (256-row bf16 tiles with 64-byte stages and 4 slots, SkShape<256, 4, 64>,
+// cut the W1 stream per row in half and the layer-1 time by 7% on 163k
+// unique rows, but doubled the partial-tile bytes the tail kernel adds up,
+// which cost as much again.)
 template <typename TT>
-constexpr int sk_bk() { return kSkRowBytes / (int)sizeof(TT); }   // K per stage
+struct Sk : SkShape<128, 3, 128> {};
+
+template <typename TT>
+constexpr int sk_bk() { return Sk<TT>::RB / (int)sizeof(TT); }   // K per stage
+
+// Chunk swizzle of a stage row: 128-byte rows as the ring of the
+// one-tile-per-block kernel; 64-byte rows: rows r and r + 4 (same banks)
+// take different chunks.
+template <class K>
+__device__ __forceinline__ int sk_swz(int row)
+{
+    if constexpr (K::CPR == 8) return ring_swz(row);      // bits 0-3 of the row
+    else return (row >> 2) & 3;                           // bits 2-3 of the row
+}
 
 struct SkPlan {
     int n_u, n_cb, S, g;            // g = workers in use
@@ -327,25 +348,26 @@ template <typename TT>
 __device__ __forceinline__ void sk_compute(const float *slot, v16f (*acc)[kSkNB], int lane, int wave)
 {
     using K = Sk<TT>;
+    constexpr int G = K::G, RF = K::RB / 4;                    // k groups, floats per stage row
     const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
-    uint4 a[4][K::MB], b[4][kSkNB];
+    uint4 a[G][K::MB], b[G][kSkNB];
+    // every row this lane reads is r32 plus a multiple of 32, which leaves the
+    // swizzle unchanged: one lane offset per k group, the blocks at constant
+    // distances from it
+    const int sw = sk_swz<K>(r32);
+    const float *pa = slot + (wm * 32 * K::MB + r32) * RF;
+    const float *pb = slot + (K::BM + wn * (kSkBN / 2) + r32) * RF;
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-        const int q = h * 4 + g;
+    for (int g = 0; g < G; ++g) {
+        const int off = ((h * G + g) ^ sw) << 2;
 #pragma unroll
-        for (int mb = 0; mb < K::MB; ++mb) {
-            const int ra = wm * 32 * K::MB + mb * 32 + r32;
-            a[g][mb] = *(const uint4 *)&slot[ra * 32 + ((q ^ ring_swz(ra)) << 2)];
-        }
+        for (int mb = 0; mb < K::MB; ++mb) a[g][mb] = *(const uint4 *)(pa + mb * 32 * RF + off);
 #pragma unroll
-        for (int nb = 0; nb < kSkNB; ++nb) {
-            const int rb = K::BM + wn * (kSkBN / 2) + nb * 32 + r32;
-            b[g][nb] = *(const uint4 *)&slot[rb * 32 + ((q ^ ring_swz(rb)) << 2)];
-        }
+        for (int nb = 0; nb < kSkNB; ++nb) b[g][nb] = *(const uint4 *)(pb + nb * 32 * RF + off);
     }
     constexpr int PER_G = sizeof(TT) == 4 ? 4 : 1;           // MFMAs per (group, block)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
+    for (int g = 0; g < G; ++g) {
         if constexpr (sizeof(TT) == 4) {
 #pragma unroll
             for (int mb = 0; mb < K::MB; ++mb) {
@@ -370,8 +392,8 @@ __device__ __forceinline__ void sk_compute(const float *slot, v16f (*acc)[kSkNB]
     // group 0's reads first, then (reads of g+1, MFMAs of g)
     __builtin_amdgcn_sched_group_barrier(0x100, K::MB + kSkNB, 0);
 #pragma unroll
-    for (int g = 0; g < 4; ++g) {
-        if (g < 3) __builtin_amdgcn_sched_group_barrier(0x100, K::MB + kSkNB, 0);
+    for (int g = 0; g < G; ++g) {
+        if (g < G - 1) __builtin_amdgcn_sched_group_barrier(0x100, K::MB + kSkNB, 0);
         __builtin_amdgcn_sched_group_barrier(0x008, PER_G * K::MB * kSkNB, 0);
     }
 }
@@ -393,7 +415,8 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
     constexpr int BK = sk_bk<TT>();
     __shared__ __attribute__((aligned(16))) float ring0[K::SLOT];
     __shared__ __attribute__((aligned(16))) float ring1[K::SLOT];
-    __shared__ __attribute__((aligned(16))) float ring2[K::R == 3 ? K::SLOT : 4];
+    __shared__ __attribute__((aligned(16))) float ring2[K::R >= 3 ? K::SLOT : 4];
+    __shared__ __attribute__((aligned(16))) float ring3[K::R == 4 ? K::SLOT : 4];
     __shared__ int rid[K::BM];
 
     const int n_u = min(*n_uniq_p, cap);
@@ -425,8 +448,8 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
         const char *src[K::PW];
 #pragma unroll
         for (int q = 0; q < K::PW; ++q) {
-            const int row = (wave * K::PW + q) * 8 + (lane >> 3);
-            const int chunk = (lane & 7) ^ ring_swz(row);
+            const int row = (wave * K::PW + q) * K::RPI + lane / K::CPR;
+            const int chunk = (lane % K::CPR) ^ sk_swz<K>(row);
             if (row < K::BM) {
                 const int id = rid[row];
                 src[q] = (id >= 0 ? (const char *)T + (size_t)id * row_bytes : (const char *)W1) + chunk * 16;
@@ -440,19 +463,47 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
 #pragma unroll
             for (int nb = 0; nb < kSkNB; ++nb) acc[mb][nb] = (v16f){};
         const int n = ke - ks;
-        if constexpr (K::R == 3) {
+        if constexpr (K::R == 4) {
+            // 4 slots: at the top of stage s, stages s+1 and s+2 may still be
+            // in flight; after the barrier (everyone is done with the slot of
+            // s-1) stage s+3 is issued into it and stage s is computed.
+#define SK_STAGE4(cur, nxt, s)                                                     \
+    do {                                                                           \
+        __builtin_amdgcn_sched_barrier(0);                                         \
+        AMS_WAIT_VM_LDS(2 * K::PW);                                                \
+        __builtin_amdgcn_s_barrier();                                              \
+        __builtin_amdgcn_sched_barrier(0);                                         \
+        sk_issue<TT>(nxt, src, (int64_t)(ks + min((s) + 3, n - 1)) * K::RB, wave); \
+        __builtin_amdgcn_sched_barrier(0);                                         \
+        sk_compute<TT>(cur, acc, lane, wave);                                      \
+    } while (0)
+            sk_issue<TT>(ring0, src, (int64_t)ks * K::RB, wave);
+            sk_issue<TT>(ring1, src, (int64_t)(ks + min(1, n - 1)) * K::RB, wave);
+            sk_issue<TT>(ring2, src, (int64_t)(ks + min(2, n - 1)) * K::RB, wave);
+            int s = 0;
+            for (; s + 4 <= n; s += 4) {
+                SK_STAGE4(ring0, ring3, s);
+                SK_STAGE4(ring1, ring0, s + 1);
+                SK_STAGE4(ring2, ring1, s + 2);
+                SK_STAGE4(ring3, ring2, s + 3);
+            }
+            if (s < n) SK_STAGE4(ring0, ring3, s);
+            if (s + 1 < n) SK_STAGE4(ring1, ring0, s + 1);
+            if (s + 2 < n) SK_STAGE4(ring2, ring1, s + 2);
+#undef SK_STAGE4
+        } else if constexpr (K::R == 3) {
 #define SK_STAGE(cur, nxt, s)                                                      \
     do {                                                                           \
         __builtin_amdgcn_sched_barrier(0);                                         \
         AMS_WAIT_VM_LDS(K::PW);                                                    \
         __builtin_amdgcn_s_barrier();                                              \
         __builtin_amdgcn_sched_barrier(0);                                         \
-        sk_issue<TT>(nxt, src, (int64_t)(ks + min((s) + 2, n - 1)) * kSkRowBytes, wave); \
+        sk_issue<TT>(nxt, src, (int64_t)(ks + min((s) + 2, n - 1)) * K::RB, wave); \
         __builtin_amdgcn_sched_barrier(0);                                         \
         sk_compute<TT>(cur, acc, lane, wave);                                      \
     } while (0)
-            sk_issue<TT>(ring0, src, (int64_t)ks * kSkRowBytes, wave);
-            sk_issue<TT>(ring1, src, (int64_t)(ks + min(1, n - 1)) * kSkRowBytes, wave);
+            sk_issue<TT>(ring0, src, (int64_t)ks * K::RB, wave);
+            sk_issue<TT>(ring1, src, (int64_t)(ks + min(1, n - 1)) * K::RB, wave);
             int s = 0;
             for (; s + 3 <= n; s += 3) {
                 SK_STAGE(ring0, ring2, s);
@@ -472,11 +523,11 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
         AMS_WAIT_VM_LDS(0);                                                        \
         __builtin_amdgcn_s_barrier();                                              \
         __builtin_amdgcn_sched_barrier(0);                                         \
-        if ((s) + 1 < n) sk_issue<TT>(nxt, src, (int64_t)(ks + (s) + 1) * kSkRowBytes, wave); \
+        if ((s) + 1 < n) sk_issue<TT>(nxt, src, (int64_t)(ks + (s) + 1) * K::RB, wave); \
         __builtin_amdgcn_sched_barrier(0);                                         \
         sk_compute<TT>(cur, acc, lane, wave);                                      \
     } while (0)
-            sk_issue<TT>(ring0, src, (int64_t)ks * kSkRowBytes, wave);
+            sk_issue<TT>(ring0, src, (int64_t)ks * K::RB, wave);
             int s = 0;
             for (; s + 2 <= n; s += 2) {
                 SK_STAGE2(ring0, ring1, s);
@@ -488,38 +539,43 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
         AMS_WAIT_VM(0);
 
         const int wm = wave >> 1, wn = wave & 1, r32 = lane & 31;
+        // this lane's rows are rl0 + 32 mb + 8 (j / 4) + j % 4, its columns
+        // c0 + 32 nb (MFMA accumulator layout)
+        const int rl0 = wm * 32 * K::MB + 4 * (lane >> 5);
+        const int c0 = wn * (kSkBN / 2) + r32;
         if (ks == 0 && ke == S) {
+            float bias[kSkNB];
 #pragma unroll
-            for (int nb = 0; nb < kSkNB; ++nb) {
-                const int col = n0 + wn * (kSkBN / 2) + nb * 32 + r32;
-                const float bias = b1[col];
-#pragma unroll
-                for (int mb = 0; mb < K::MB; ++mb)
-#pragma unroll
-                    for (int j = 0; j < 16; ++j) {
-                        const int r = wm * 32 * K::MB + mb * 32 + acc_row(j, lane);
-                        const float z0 = rid[r] >= 0 ? acc[mb][nb][j] + bias : bias;
-                        const float z = keep_z ? z0 : fmaxf(z0, 0.f);
-                        if (m0 + r < n_u) {
-                            if (H1) H1[(size_t)(m0 + r) * H + col] = z;
-                            if (H1b) {
-                                const uint16_t hi = ams_f32_to_bf16(z);
-                                H1b[(size_t)(m0 + r) * H + col] = hi;
-                                if (H1lo) H1lo[(size_t)(m0 + r) * H + col] = ams_f32_to_bf16(z - ams_bf16_to_f32(hi));
-                            }
-                        }
-                    }
-            }
-        } else {
-            float *piece = pbuf + ((size_t)w * 2 + (first ? 0 : 1)) * K::TILE;
+            for (int nb = 0; nb < kSkNB; ++nb) bias[nb] = b1[n0 + c0 + nb * 32];
 #pragma unroll
             for (int mb = 0; mb < K::MB; ++mb)
 #pragma unroll
-                for (int nb = 0; nb < kSkNB; ++nb)
+                for (int j = 0; j < 16; ++j) {
+                    const int r = rl0 + mb * 32 + 8 * (j >> 2) + (j & 3);
+                    if (m0 + r >= n_u) continue;
+                    const bool ok = rid[r] >= 0;
+                    const size_t o = (size_t)(m0 + r) * H + n0 + c0;
 #pragma unroll
-                    for (int j = 0; j < 16; ++j)
-                        piece[(wm * 32 * K::MB + mb * 32 + acc_row(j, lane)) * kSkBN + wn * (kSkBN / 2) + nb * 32 +
-                              r32] = acc[mb][nb][j];
+                    for (int nb = 0; nb < kSkNB; ++nb) {
+                        const float z0 = ok ? acc[mb][nb][j] + bias[nb] : bias[nb];
+                        const float z = keep_z ? z0 : fmaxf(z0, 0.f);
+                        if (H1) H1[o + nb * 32] = z;
+                        if (H1b) {
+                            const uint16_t hi = ams_f32_to_bf16(z);
+                            H1b[o + nb * 32] = hi;
+                            if (H1lo) H1lo[o + nb * 32] = ams_f32_to_bf16(z - ams_bf16_to_f32(hi));
+                        }
+                    }
+                }
+        } else {
+            float *piece = pbuf + ((size_t)w * 2 + (first ? 0 : 1)) * K::TILE + rl0 * kSkBN + c0;
+#pragma unroll
+            for (int mb = 0; mb < K::MB; ++mb)
+#pragma unroll
+                for (int j = 0; j < 16; ++j)
+#pragma unroll
+                    for (int nb = 0; nb < kSkNB; ++nb)
+                        piece[(mb * 32 + 8 * (j >> 2) + (j & 3)) * kSkBN + nb * 32] = acc[mb][nb][j];
         }
         first = false;
         it += n;
@@ -2484,13 +2540,13 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
                                                 b2, nullptr, nullptr, mlp->final_relu, n_uniq, cap, H2_save, E));
         return ams_launch_status();
     }
-    const int sk_bk = sk ? (bf ? 64 : 32) : 0;      // K per stream-K stage (128 bytes of a row)
+    const int skk = sk ? sk_bk<float>() : 0;        // K per stream-K stage (the bf16 stream-K path returned above)
     int tg = (cap + kTailRows - 1) / kTailRows;
     if (tg > 1024) tg = 1024;
 #define TF_LAUNCH(LL, PRV)                                                                                 \
     AMS_LAUNCH("tail_fwd", st, (tail_fwd<LL, PRV><<<tg, kThreads, 0, st>>>(                                   \
                                    H1f, H, M, D, W2, b2, W3, b3, bf, mlp->final_relu, n_uniq, cap, H2_save, E, \
-                                   sk_bk, F, G, pbuf, bf ? (uint16_t *)H1_save : nullptr, b1, uniq, n_rows, s1, s2)))
+                                   skk, F, G, pbuf, bf ? (uint16_t *)H1_save : nullptr, b1, uniq, n_rows, s1, s2)))
     if (L == 3 && pr) TF_LAUNCH(3, true);
     else if (L == 3) TF_LAUNCH(3, false);
     else if (pr) TF_LAUNCH(2, true);
