@@ -23,6 +23,7 @@ of the same workload, repeated for about ten seconds (median run).
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -37,6 +38,17 @@ PEAK_HBM = 8.0e12
 PEAK_MFMA = {"f32": 157.3e12, "bf16": 2.5e15}
 
 
+def mfma_peak(kernel: str, dtype: str) -> float:
+    """Dense MFMA peak of the type a kernel's products run in: the split
+    float32 layer 1 (l1sk_x3) runs on bf16 MFMA; other float32-storage
+    kernels on float32 MFMA."""
+    if kernel.endswith("_bf16") or kernel == "l1sk_x3":
+        return PEAK_MFMA["bf16"]
+    if kernel.endswith("_f32"):
+        return PEAK_MFMA["f32"]
+    return PEAK_MFMA["bf16" if dtype == "bf16" else "f32"]
+
+
 def flops_per_unique(dims):
     fwd = 2 * sum(a * b for a, b in zip(dims[:-1], dims[1:]))
     # backward: every weight gradient, plus dH of every layer but the first
@@ -47,7 +59,7 @@ def flops_per_unique(dims):
 
 # Algorithmic work of the layer-1 GEMM kernels per unique image: 2*F*H flops
 # and one read of the image's F-wide feature row.
-GEMM_KERNELS = ("l1sk_f32", "l1sk_bf16", "l1_fwd_f32", "l1_fwd_bf16", "dw1_part_f32", "dw1_part_bf16",
+GEMM_KERNELS = ("l1sk_f32", "l1sk_bf16", "l1sk_x3", "l1_fwd_f32", "l1_fwd_bf16", "dw1_part_f32", "dw1_part_bf16",
                 "dw1_part")
 
 
@@ -122,6 +134,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="c1_f32")
     ap.add_argument("--mode", default=None)
+    ap.add_argument("--dtype", default=None, choices=("f32", "f32x3", "bf16"),
+                    help="override the workload's storage/arithmetic mode (f32x3: float32 storage, "
+                         "the 4096-wide forward product on bf16 MFMA with a three-part split)")
     ap.add_argument("--batches", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--ops", action="store_true",
@@ -158,6 +173,10 @@ def main():
         return bench_ops(args)
 
     w = synth.get(args.workload)
+    if args.dtype and args.dtype != w.dtype:
+        if (args.dtype == "bf16") != (w.dtype == "bf16"):
+            sys.exit("--dtype may switch between f32 and f32x3 only (bf16 has workloads of its own)")
+        w = dataclasses.replace(w, dtype=args.dtype, name=w.name.replace(w.dtype, args.dtype))
     mode = args.mode or w.pools[-1]
     torch.cuda.set_device(0)
     ams.load()
@@ -283,10 +302,11 @@ def main():
     esz = 2 if w.dtype == "bf16" else 4
     step_flops = u_mean * (fwd_f + bwd_f)
     step_bytes = u_mean * 2 * w.in_dim * esz           # the two reads of every unique feature row
-    peak = PEAK_MFMA[w.dtype]
+    step_peak = PEAK_MFMA["bf16" if w.dtype == "bf16" else "f32"]
 
     # roofline of the dominant kernel (largest total time over the pass)
     dom = max(ktimes, key=lambda k: ktimes[k][1])
+    peak = mfma_peak(dom, w.dtype)
     t_launch = kernels[dom]["ms_per_launch"] * 1e-3
     if dom in GEMM_KERNELS:
         fl_u, by_u = gemm_work_per_unique(w.dims, esz)
@@ -306,7 +326,7 @@ def main():
     for k, v in kernels.items():
         if k in GEMM_KERNELS:
             fl_u, _ = gemm_work_per_unique(w.dims, esz)
-            v["mfma_frac"] = u_mean * fl_u / (v["ms_per_launch"] * 1e-3) / peak
+            v["mfma_frac"] = u_mean * fl_u / (v["ms_per_launch"] * 1e-3) / mfma_peak(k, w.dtype)
 
     out = {
         "metric": METRIC, "value": value, "unit": "behavior images/s", "n_gpus": 1,
@@ -318,7 +338,7 @@ def main():
                    "batch": w.batch, "behaviors_per_step": beh_total / args.steps,
                    "unique_per_step": u_mean, "dedup_ratio": (beh_total + w.batch * args.steps) / uniq_total,
                    "rotating_batches": len(dev_batches)},
-        "step_mfma_frac": step_flops / (ms_step * 1e-3) / peak,
+        "step_mfma_frac": step_flops / (ms_step * 1e-3) / step_peak,
         "step_hbm_frac": step_bytes / (ms_step * 1e-3) / PEAK_HBM,
         "unique_images_per_s": uniq_total / (ms_total * 1e-3),
         "samples_per_s": w.batch * args.steps / (ms_total * 1e-3),
@@ -409,8 +429,9 @@ def bench_joint(w, mode, args):
 
     esz = 2 if w.dtype == "bf16" else 4
     u_mean = uniq_total / args.steps
-    peak = PEAK_MFMA[w.dtype]
+    step_peak = PEAK_MFMA["bf16" if w.dtype == "bf16" else "f32"]
     dom = max(ktimes, key=lambda k: ktimes[k][1])
+    peak = mfma_peak(dom, w.dtype)
     t_launch = kernels[dom]["ms_per_launch"] * 1e-3
     if dom in GEMM_KERNELS:
         fl_u, by_u = gemm_work_per_unique(w.dims, esz)
@@ -429,7 +450,7 @@ def bench_joint(w, mode, args):
     for k, v in kernels.items():
         if k in GEMM_KERNELS:
             fl_u, _ = gemm_work_per_unique(w.dims, esz)
-            v["mfma_frac"] = u_mean * fl_u / (v["ms_per_launch"] * 1e-3) / peak
+            v["mfma_frac"] = u_mean * fl_u / (v["ms_per_launch"] * 1e-3) / mfma_peak(k, w.dtype)
     fwd_f, bwd_f = flops_per_unique(w.dims)
     ms_step = ms_total / args.steps
     out = {
@@ -444,7 +465,7 @@ def bench_joint(w, mode, args):
                                f"softmax cross-entropy; sparse Adagrad lr {w.joint.lr}; fwd+bwd+update",
                    "batch": w.batch, "behaviors_per_step": beh_total / args.steps, "unique_per_step": u_mean,
                    "id_rows_touched_per_step": rows_total / args.steps, "rotating_batches": len(dev_batches)},
-        "step_mfma_frac": u_mean * (fwd_f + bwd_f) / (ms_step * 1e-3) / peak,
+        "step_mfma_frac": u_mean * (fwd_f + bwd_f) / (ms_step * 1e-3) / step_peak,
         "step_hbm_frac": u_mean * 2 * w.in_dim * esz / (ms_step * 1e-3) / PEAK_HBM,
         "unique_images_per_s": uniq_total / (ms_total * 1e-3),
         "id_rows_per_s": rows_total / (ms_total * 1e-3),

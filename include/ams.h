@@ -40,6 +40,14 @@
  *             [dims[l+1]].  E, U, A, dE, dU, dA have row stride D = dims[last]
  *             floats.  IDs are int32.
  * Precision:  AMS_F32: T and W float32, float32 MFMA with float32 accumulation.
+ *             AMS_F32_X3: T and W float32 as AMS_F32.  The 4096-wide layer's
+ *             forward product (dims[1] a multiple of 256) runs on bf16 MFMA:
+ *             every float32 operand is split exactly into three bf16 parts
+ *             h + m + l (round to nearest at each step) and six of the nine
+ *             part products (hh, hm, mh, hl, lh, mm) are accumulated in
+ *             float32; the three left out stay below 2^-22 |x y| per
+ *             product, about one float32 rounding.  Everything else as
+ *             AMS_F32.
  *             AMS_BF16: T and W bfloat16; bf16 MFMA with float32 accumulation
  *             for the 4096-wide layer and its weight gradient (whose
  *             activation-gradient operand is rounded to bf16).  The smaller
@@ -81,7 +89,7 @@ typedef enum {
     AMS_ERR_MODE = 8        /* unknown pooling mode */
 } ams_status;
 
-typedef enum { AMS_F32 = 0, AMS_BF16 = 1 } ams_dtype;
+typedef enum { AMS_F32 = 0, AMS_BF16 = 1, AMS_F32_X3 = 2 } ams_dtype;
 
 /* Aggregators of section 5.2.  ATT: w_j = softmax_j(e_j . a_i) over the
  * sample's behaviors, u_i = sum_j w_j e_j, with a_i the ad image embedding. */

@@ -15,7 +15,7 @@ import torch
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libams.so")
 
-AMS_F32, AMS_BF16 = 0, 1
+AMS_F32, AMS_BF16, AMS_F32_X3 = 0, 1, 2
 AMS_POOL_SUM, AMS_POOL_MAX, AMS_POOL_ATT = 0, 1, 2
 POOL = {"sum": AMS_POOL_SUM, "max": AMS_POOL_MAX, "att": AMS_POOL_ATT}
 STATUS = {0: "AMS_OK", 1: "AMS_ERR_NULL", 2: "AMS_ERR_SIZE", 3: "AMS_ERR_DTYPE", 4: "AMS_ERR_DIMS",
@@ -150,7 +150,7 @@ def make_mlp(dims, dtype: str = "f32", final_relu: bool = False) -> ams_mlp:
     m.n_layers = len(dims) - 1
     for i, d in enumerate(dims):
         m.dims[i] = int(d)
-    m.dtype = AMS_BF16 if dtype == "bf16" else AMS_F32
+    m.dtype = {"f32": AMS_F32, "bf16": AMS_BF16, "f32x3": AMS_F32_X3}[dtype]
     m.final_relu = int(final_relu)
     return m
 

@@ -24,6 +24,7 @@
 
 typedef float v16f __attribute__((ext_vector_type(16)));
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 
 namespace {
 
@@ -398,6 +399,57 @@ __device__ __forceinline__ void sk_compute(const float *slot, v16f (*acc)[kSkNB]
     }
 }
 
+// Epilogue of a stream-K segment.  whole: the segment covered the tile's full
+// K, so H1 = act(acc + b1) is written (b1 alone for a row whose ID is out of
+// range; keep_z keeps the pre-activation); otherwise acc goes to this
+// worker's partial tile `piece` (row-major, kSkBN floats per row).
+template <int MB>
+__device__ __forceinline__ void sk_store(const v16f (&acc)[MB][kSkNB], bool whole, const int *rid, int m0, int n0,
+                                         int n_u, int H, const float *__restrict__ b1, int keep_z,
+                                         float *__restrict__ H1, uint16_t *__restrict__ H1b,
+                                         uint16_t *__restrict__ H1lo, float *__restrict__ piece, int lane, int wave)
+{
+    const int wm = wave >> 1, wn = wave & 1, r32 = lane & 31;
+    // this lane's rows are rl0 + 32 mb + 8 (j / 4) + j % 4, its columns
+    // c0 + 32 nb (MFMA accumulator layout)
+    const int rl0 = wm * 32 * MB + 4 * (lane >> 5);
+    const int c0 = wn * (kSkBN / 2) + r32;
+    if (whole) {
+        float bias[kSkNB];
+#pragma unroll
+        for (int nb = 0; nb < kSkNB; ++nb) bias[nb] = b1[n0 + c0 + nb * 32];
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const int r = rl0 + mb * 32 + 8 * (j >> 2) + (j & 3);
+                if (m0 + r >= n_u) continue;
+                const bool ok = rid[r] >= 0;
+                const size_t o = (size_t)(m0 + r) * H + n0 + c0;
+#pragma unroll
+                for (int nb = 0; nb < kSkNB; ++nb) {
+                    const float z0 = ok ? acc[mb][nb][j] + bias[nb] : bias[nb];
+                    const float z = keep_z ? z0 : fmaxf(z0, 0.f);
+                    if (H1) H1[o + nb * 32] = z;
+                    if (H1b) {
+                        const uint16_t hi = ams_f32_to_bf16(z);
+                        H1b[o + nb * 32] = hi;
+                        if (H1lo) H1lo[o + nb * 32] = ams_f32_to_bf16(z - ams_bf16_to_f32(hi));
+                    }
+                }
+            }
+    } else {
+        float *pp = piece + rl0 * kSkBN + c0;
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int j = 0; j < 16; ++j)
+#pragma unroll
+                for (int nb = 0; nb < kSkNB; ++nb)
+                    pp[(mb * 32 + 8 * (j >> 2) + (j & 3)) * kSkBN + nb * 32] = acc[mb][nb][j];
+    }
+}
+
 // H1b (bf16 mode): the bf16 copy of H1 kept for the backward, written with H1
 // for tiles finished in place; H1lo, if given, the bf16 rounding of what H1b
 // leaves out (H1 = H1b + H1lo to 2^-18 relative), the fp32-level operand of
@@ -538,45 +590,209 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
         }
         AMS_WAIT_VM(0);
 
-        const int wm = wave >> 1, wn = wave & 1, r32 = lane & 31;
-        // this lane's rows are rl0 + 32 mb + 8 (j / 4) + j % 4, its columns
-        // c0 + 32 nb (MFMA accumulator layout)
-        const int rl0 = wm * 32 * K::MB + 4 * (lane >> 5);
-        const int c0 = wn * (kSkBN / 2) + r32;
-        if (ks == 0 && ke == S) {
-            float bias[kSkNB];
+        sk_store<K::MB>(acc, ks == 0 && ke == S, rid, m0, n0, n_u, H, b1, keep_z, H1, H1b, H1lo,
+                        pbuf + ((size_t)w * 2 + (first ? 0 : 1)) * K::TILE, lane, wave);
+        first = false;
+        it += n;
+    }
+}
+
+// ------------------------------------------- float32 layer 1 on bf16 MFMA
+// (AMS_F32_X3.)  A float32 x is the exact sum of three bf16 values h =
+// bf16(x), m = bf16(x - h), l = bf16(x - h - m), each rounded to nearest:
+// both residuals are exact in float32 (x and h are within a factor 2 of each
+// other), and at most 8 significant bits are left for l.  Of the nine part
+// products of x y the six kept (hh, hm, mh, hl, lh, mm) leave out
+// |ml + lm + ll| < 2^-22 |x y| (|m| <= 2^-8 |x|, |l| <= 2^-16 |x|), and each
+// part product is exact in the float32 accumulator.  A 16-deep k step is six
+// bf16 MFMAs (6 x 32 cycles) in place of eight float32 ones (8 x 64).
+
+__device__ __forceinline__ uint32_t cvt_pk_bf16(float a, float b)
+{
+    const bf16x2 v = {(__bf16)a, (__bf16)b};      // round to nearest even
+    return __builtin_bit_cast(uint32_t, v);
+}
+
+// x[0..7] -> the three bf16x8 parts (element e in bits 16 e .. 16 e + 15)
+__device__ __forceinline__ void split3x8(const float (&x)[8], uint4 &h, uint4 &m, uint4 &l)
+{
+    uint32_t hp[4], mp[4], lp[4];
 #pragma unroll
-            for (int nb = 0; nb < kSkNB; ++nb) bias[nb] = b1[n0 + c0 + nb * 32];
+    for (int e = 0; e < 4; ++e) {
+        const float x0 = x[2 * e], x1 = x[2 * e + 1];
+        hp[e] = cvt_pk_bf16(x0, x1);
+        const float r0 = x0 - __uint_as_float(hp[e] << 16), r1 = x1 - __uint_as_float(hp[e] & 0xffff0000u);
+        mp[e] = cvt_pk_bf16(r0, r1);
+        const float q0 = r0 - __uint_as_float(mp[e] << 16), q1 = r1 - __uint_as_float(mp[e] & 0xffff0000u);
+        lp[e] = cvt_pk_bf16(q0, q1);
+    }
+    h = make_uint4(hp[0], hp[1], hp[2], hp[3]);
+    m = make_uint4(mp[0], mp[1], mp[2], mp[3]);
+    l = make_uint4(lp[0], lp[1], lp[2], lp[3]);
+}
+
+// W[n] float32 -> bf16 planes P[0, n) = h, P[n, 2n) = m, P[2n, 3n) = l; n % 8 == 0
+__global__ __launch_bounds__(kThreads) void split3_k(const float *__restrict__ W, int64_t n, uint16_t *__restrict__ P)
+{
+    for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n / 8; i += (int64_t)gridDim.x * kThreads) {
+        const float4 a = *(const float4 *)(W + 8 * i), b = *(const float4 *)(W + 8 * i + 4);
+        const float x[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+        uint4 h, m, l;
+        split3x8(x, h, m, l);
+        *(uint4 *)(P + 8 * i) = h;
+        *(uint4 *)(P + n + 8 * i) = m;
+        *(uint4 *)(P + 2 * n + 8 * i) = l;
+    }
+}
+
+// Stream-K layer 1 with the split: the tiles, shares and partial tiles of
+// l1sk<float> (128 x 256 tiles, 32 k per stage).  A stage slot holds the
+// 128 feature rows (float32, 128 bytes each, chunks swizzled by ring_swz)
+// and the three bf16 planes of the tile's 256 W1 rows (64 bytes each,
+// chunk c at c ^ ((row >> 2) & 3)); 64 KB per slot, two slots.  Every wave
+// issues 2 DMA instructions of feature rows and 6 of planes per stage (the
+// gathers spread over all waves).  Each wave splits its feature operand after
+// the LDS read; W1 comes split (split3_k).
+struct X3 {
+    static constexpr int BM = 128;
+    static constexpr int BK = 32;                          // k per stage
+    static constexpr int A_FL = BM * 32;                   // floats of feature rows per slot
+    static constexpr int PL_FL = kSkBN * 16;               // floats per W1 plane per slot
+    static constexpr int SLOT = A_FL + 3 * PL_FL;          // 16384 floats
+    static constexpr int PW = SLOT / 256 / (kSkThreads / AMS_WAVE);   // DMA instructions per wave
+    static constexpr int TILE = BM * kSkBN;
+};
+static_assert(X3::TILE == Sk<float>::TILE && X3::BM == Sk<float>::BM && X3::BK == sk_bk<float>(),
+              "the split kernel leaves its partial tiles in the float32 layout");
+static_assert(X3::PW == 8 && X3::A_FL / 256 == 2 * (kSkThreads / AMS_WAVE), "2 feature-row instructions per wave");
+
+__device__ __forceinline__ void x3_compute(const float *slot, v16f (&acc)[1][kSkNB], int lane, int wave)
+{
+    const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
+    // rows read are r32 plus multiples of 32: one swizzle per lane
+    const float *pa = slot + (wm * 32 + r32) * 32;
+    const int swa = ring_swz(r32);
+    const float *pb = slot + X3::A_FL + (wn * (kSkBN / 2) + r32) * 16;
+    const int swb = (r32 >> 2) & 3;
 #pragma unroll
-            for (int mb = 0; mb < K::MB; ++mb)
+    for (int g = 0; g < 2; ++g) {
+        const int ca = 4 * g + 2 * h;                      // k = 16 g + 8 h .. + 7
+        const float4 x0 = *(const float4 *)(pa + ((ca ^ swa) << 2));
+        const float4 x1 = *(const float4 *)(pa + (((ca + 1) ^ swa) << 2));
+        const int cb = ((2 * g + h) ^ swb) << 2;
+        uint4 bh[kSkNB], bm[kSkNB], bl[kSkNB];
 #pragma unroll
-                for (int j = 0; j < 16; ++j) {
-                    const int r = rl0 + mb * 32 + 8 * (j >> 2) + (j & 3);
-                    if (m0 + r >= n_u) continue;
-                    const bool ok = rid[r] >= 0;
-                    const size_t o = (size_t)(m0 + r) * H + n0 + c0;
-#pragma unroll
-                    for (int nb = 0; nb < kSkNB; ++nb) {
-                        const float z0 = ok ? acc[mb][nb][j] + bias[nb] : bias[nb];
-                        const float z = keep_z ? z0 : fmaxf(z0, 0.f);
-                        if (H1) H1[o + nb * 32] = z;
-                        if (H1b) {
-                            const uint16_t hi = ams_f32_to_bf16(z);
-                            H1b[o + nb * 32] = hi;
-                            if (H1lo) H1lo[o + nb * 32] = ams_f32_to_bf16(z - ams_bf16_to_f32(hi));
-                        }
-                    }
-                }
-        } else {
-            float *piece = pbuf + ((size_t)w * 2 + (first ? 0 : 1)) * K::TILE + rl0 * kSkBN + c0;
-#pragma unroll
-            for (int mb = 0; mb < K::MB; ++mb)
-#pragma unroll
-                for (int j = 0; j < 16; ++j)
-#pragma unroll
-                    for (int nb = 0; nb < kSkNB; ++nb)
-                        piece[(mb * 32 + 8 * (j >> 2) + (j & 3)) * kSkBN + nb * 32] = acc[mb][nb][j];
+        for (int nb = 0; nb < kSkNB; ++nb) {
+            bh[nb] = *(const uint4 *)(pb + nb * 32 * 16 + cb);
+            bm[nb] = *(const uint4 *)(pb + X3::PL_FL + nb * 32 * 16 + cb);
+            bl[nb] = *(const uint4 *)(pb + 2 * X3::PL_FL + nb * 32 * 16 + cb);
         }
+        const float x[8] = {x0.x, x0.y, x0.z, x0.w, x1.x, x1.y, x1.z, x1.w};
+        uint4 ah, am, al;
+        split3x8(x, ah, am, al);
+#pragma unroll
+        for (int nb = 0; nb < kSkNB; ++nb) {
+            v16f c = acc[0][nb];
+            c = mfma_bf16(ah, bh[nb], c);
+            c = mfma_bf16(ah, bm[nb], c);
+            c = mfma_bf16(am, bh[nb], c);
+            c = mfma_bf16(ah, bl[nb], c);
+            c = mfma_bf16(al, bh[nb], c);
+            c = mfma_bf16(am, bm[nb], c);
+            acc[0][nb] = c;
+        }
+    }
+}
+
+__global__ __launch_bounds__(kSkThreads) void l1sk_x3(const float *__restrict__ T, int64_t n_rows, int F,
+                                                      const int32_t *__restrict__ uniq,
+                                                      const int32_t *__restrict__ n_uniq_p, int cap,
+                                                      const float *__restrict__ W1,
+                                                      const uint16_t *__restrict__ W1p,
+                                                      const float *__restrict__ b1, int H, int G,
+                                                      float *__restrict__ H1, float *__restrict__ pbuf,
+                                                      int keep_z)
+{
+    __shared__ __attribute__((aligned(16))) float ring0[X3::SLOT];
+    __shared__ __attribute__((aligned(16))) float ring1[X3::SLOT];
+    __shared__ int rid[X3::BM];
+
+    const int n_u = min(*n_uniq_p, cap);
+    if (n_u <= 0) return;
+    const SkPlan P = sk_plan(n_u, H, F, G, X3::BK, X3::BM);
+    const int w = (blockIdx.x & 7) * (G >> 3) + (blockIdx.x >> 3);
+    if (w >= P.g) return;
+    const int64_t it1 = P.it0(w + 1);
+    const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
+    const int S = P.S;
+    const size_t plane = (size_t)H * F;
+    bool first = true;
+    for (int64_t it = P.it0(w); it < it1;) {
+        const int tile = (int)(it / S);
+        const int ks = (int)(it % S);
+        const int ke = (int)min<int64_t>(S, ks + (it1 - it));
+        const int m0 = (tile / P.n_cb) * X3::BM, n0 = (tile % P.n_cb) * kSkBN;
+        __syncthreads();                        // previous segment done with rid and the ring
+        if (t < X3::BM) {
+            int id = -1;
+            if (m0 + t < n_u) {
+                id = uniq[m0 + t];
+                if (id < 0 || (int64_t)id >= n_rows) id = -1;
+            }
+            rid[t] = id;
+        }
+        __syncthreads();
+        const char *src[X3::PW];
+#pragma unroll
+        for (int q = 0; q < X3::PW; ++q) {
+            if (q < 2) {                        // feature rows 8 ja .. 8 ja + 7
+                const int ja = 2 * wave + q;
+                const int row = 8 * ja + (lane >> 3);
+                const int chunk = (lane & 7) ^ ring_swz(row);
+                const int id = rid[row];
+                src[q] = (id >= 0 ? (const char *)(T + (size_t)id * F) : (const char *)W1) + chunk * 16;
+            } else {                            // plane jb / 16, W1 rows 16 (jb % 16) .. + 15
+                const int jb = 6 * wave + q - 2, pl = jb >> 4;
+                const int rb = 16 * (jb & 15) + (lane >> 2);
+                const int chunk = (lane & 3) ^ ((rb >> 2) & 3);
+                src[q] = (const char *)(W1p + pl * plane + (size_t)(n0 + rb) * F) + chunk * 16;
+            }
+        }
+        v16f acc[1][kSkNB];
+#pragma unroll
+        for (int nb = 0; nb < kSkNB; ++nb) acc[0][nb] = (v16f){};
+        const int n = ke - ks;
+        auto issue = [&](float *slot, int st) {
+#pragma unroll
+            for (int q = 0; q < 2; ++q) dma16(src[q] + (int64_t)st * 128, slot + (2 * wave + q) * 256);
+#pragma unroll
+            for (int q = 2; q < X3::PW; ++q)
+                dma16(src[q] + (int64_t)st * 64, slot + X3::A_FL + (6 * wave + q - 2) * 256);
+        };
+        // 2 slots: at the top of stage s only stage s is in flight; after the
+        // barrier (everyone is done with the other slot) stage s+1 is issued
+        // into it and stage s is computed meanwhile.
+#define X3_STAGE(cur, nxt, s)                                                      \
+    do {                                                                           \
+        __builtin_amdgcn_sched_barrier(0);                                         \
+        AMS_WAIT_VM_LDS(0);                                                        \
+        __builtin_amdgcn_s_barrier();                                              \
+        __builtin_amdgcn_sched_barrier(0);                                         \
+        if ((s) + 1 < n) issue(nxt, ks + (s) + 1);                                 \
+        __builtin_amdgcn_sched_barrier(0);                                         \
+        x3_compute(cur, acc, lane, wave);                                          \
+    } while (0)
+        issue(ring0, ks);
+        int s = 0;
+        for (; s + 2 <= n; s += 2) {
+            X3_STAGE(ring0, ring1, s);
+            X3_STAGE(ring1, ring0, s + 1);
+        }
+        if (s < n) X3_STAGE(ring0, ring1, s);
+#undef X3_STAGE
+        AMS_WAIT_VM(0);
+        sk_store<1>(acc, ks == 0 && ke == S, rid, m0, n0, n_u, H, b1, keep_z, H1, nullptr, nullptr,
+                    pbuf + ((size_t)w * 2 + (first ? 0 : 1)) * X3::TILE, lane, wave);
         first = false;
         it += n;
     }
@@ -2357,7 +2573,7 @@ size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 int sk_workers();
 
-bool use_dw_ring(const ams_mlp *m) { return m->dtype == AMS_F32 && m->dims[1] == DwRing::BM && m->dims[0] % DwRing::BN == 0; }
+bool use_dw_ring(const ams_mlp *m) { return m->dtype != AMS_BF16 && m->dims[1] == DwRing::BM && m->dims[0] % DwRing::BN == 0; }
 bool use_dw_tr(const ams_mlp *m) { return m->dtype == AMS_BF16 && m->dims[1] == DwTr::BM && m->dims[0] % DwTr::BN == 0; }
 
 // Split-K chunk count of dW1: the DMA-ring kernel takes one block per CU
@@ -2437,8 +2653,10 @@ extern "C" size_t ams_embed_workspace(const ams_mlp *mlp, int32_t n_uniq_cap)
     // forward: fp32 H1 (bf16 mode, or when the caller keeps no fp32 H1_save),
     // then the stream-K partial tiles (two per worker)
     size_t fwd = al256((size_t)n_uniq_cap * mlp->dims[1] * 4);
-    if (use_stream_k(mlp))
+    if (use_stream_k(mlp)) {
         fwd += al256((size_t)sk_workers() * 2 * (mlp->dtype == AMS_BF16 ? Sk<uint16_t>::TILE : Sk<float>::TILE) * 4);
+        if (mlp->dtype == AMS_F32_X3) fwd += al256((size_t)3 * mlp->dims[0] * mlp->dims[1] * 2);   // W1 parts
+    }
     const size_t bwd = plan_bwd(mlp, n_uniq_cap).total;
     return fwd > bwd ? fwd : bwd;
 }
@@ -2449,7 +2667,7 @@ ams_status prelu_slopes(const ams_mlp *mlp, const float *const *slope, const flo
 {
     *s1 = *s2 = nullptr;
     if (!slope) return AMS_OK;
-    if (mlp->dtype != AMS_F32) return AMS_ERR_DTYPE;
+    if (mlp->dtype == AMS_BF16) return AMS_ERR_DTYPE;
     for (int l = 0; l < mlp->n_layers - 1; ++l)
         if (!slope[l]) return AMS_ERR_NULL;
     *s1 = slope[0];
@@ -2465,7 +2683,7 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
                                     void *ws, size_t ws_bytes, void *stream)
 {
     if (!mlp) return AMS_ERR_NULL;
-    if (mlp->dtype != AMS_F32 && mlp->dtype != AMS_BF16) return AMS_ERR_DTYPE;
+    if (mlp->dtype != AMS_F32 && mlp->dtype != AMS_BF16 && mlp->dtype != AMS_F32_X3) return AMS_ERR_DTYPE;
     if (!mlp_ok(mlp)) return AMS_ERR_DIMS;
     if (cap < 0 || n_rows < 0) return AMS_ERR_SIZE;
     const int L = mlp->n_layers;
@@ -2485,7 +2703,9 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
     const bool sk = use_stream_k(mlp);
     const int G = sk ? sk_workers() : 0;
     const size_t h1_bytes = al256((size_t)cap * H * 4);
-    const size_t need = h1_bytes + (sk ? al256((size_t)G * 2 * (bf ? Sk<uint16_t>::TILE : Sk<float>::TILE) * 4) : 0);
+    const bool x3 = sk && mlp->dtype == AMS_F32_X3;
+    const size_t pbuf_bytes = sk ? al256((size_t)G * 2 * (bf ? Sk<uint16_t>::TILE : Sk<float>::TILE) * 4) : 0;
+    const size_t need = h1_bytes + pbuf_bytes + (x3 ? al256((size_t)3 * F * H * 2) : 0);
     if ((h1_in_ws || sk) && (!ws || ws_bytes < need)) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     float *H1f = h1_in_ws ? (float *)ws : (float *)H1_save;
@@ -2499,7 +2719,16 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
     const int n_mt = (cap + 63) / 64;
     const int NT = (H % 128 == 0) ? 128 : 64;
     const int grid = ((n_mt + 7) / 8) * 8 * (H / NT);
-    if (sk && !bf) {
+    if (x3) {
+        // W1's three bf16 parts, then the split stream-K product
+        uint16_t *w1p = (uint16_t *)((char *)ws + h1_bytes + pbuf_bytes);
+        const int64_t nw = (int64_t)H * F;
+        const int sg = (int)std::min<int64_t>((nw / 8 + kThreads - 1) / kThreads, 2048);
+        AMS_LAUNCH("split3_w1", st, split3_k<<<sg, kThreads, 0, st>>>((const float *)W1, nw, w1p));
+        AMS_LAUNCH("l1sk_x3", st, l1sk_x3<<<G, kSkThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
+                                                                   (const float *)W1, w1p, b1, H, G, H1f, pbuf,
+                                                                   (int)pr));
+    } else if (sk && !bf) {
         AMS_LAUNCH("l1sk_f32", st, l1sk<float><<<G, kSkThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
                                                                       (const float *)W1, b1, H, G, H1f, nullptr, nullptr, pbuf,
                                                                       (int)pr));
@@ -2565,7 +2794,7 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
 {
     (void)W1;
     if (!mlp) return AMS_ERR_NULL;
-    if (mlp->dtype != AMS_F32 && mlp->dtype != AMS_BF16) return AMS_ERR_DTYPE;
+    if (mlp->dtype != AMS_F32 && mlp->dtype != AMS_BF16 && mlp->dtype != AMS_F32_X3) return AMS_ERR_DTYPE;
     if (!mlp_ok(mlp)) return AMS_ERR_DIMS;
     if (cap < 0 || n_rows < 0) return AMS_ERR_SIZE;
     const int L = mlp->n_layers;

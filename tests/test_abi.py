@@ -56,6 +56,10 @@ def test_workspace_sizes(lib):
     assert lib.ams_embed_workspace(ctypes.byref(m), 57_000) >= 57_000 * 256 * 4
     bad = ams.make_mlp((4000, 256, 64, 12), "f32")
     assert lib.ams_embed_workspace(ctypes.byref(bad), 100) == 0
+    # the split float32 forward also holds W1's three bf16 parts
+    x3 = ams.make_mlp((4096, 256, 64, 12), "f32x3")
+    assert (lib.ams_embed_workspace(ctypes.byref(x3), 57_000)
+            >= lib.ams_embed_workspace(ctypes.byref(m), 57_000) + 3 * 4096 * 256 * 2 - 256)
     assert lib.ams_pool_workspace(2, 1024, 56_000, 12, 57_000) > 0
     assert lib.ams_pool_workspace(9, 1024, 56_000, 12, 57_000) == 0
 
