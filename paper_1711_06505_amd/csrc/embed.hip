@@ -652,7 +652,9 @@ __global__ __launch_bounds__(kThreads) void split3_k(const float *__restrict__ W
 // chunk c at c ^ ((row >> 2) & 3)); 64 KB per slot, two slots.  Every wave
 // issues 2 DMA instructions of feature rows and 6 of planes per stage (the
 // gathers spread over all waves).  Each wave splits its feature operand after
-// the LDS read; W1 comes split (split3_k).
+// the LDS read; W1 comes split (split3_k).  (Deeper rings with 16-k stages,
+// and four waves with double-buffered operands, measured no faster: the
+// stream of W1 parts, 6 MB per tile, sets the pace.)
 struct X3 {
     static constexpr int BM = 128;
     static constexpr int BK = 32;                          // k per stage
@@ -2769,7 +2771,9 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
                                                 b2, nullptr, nullptr, mlp->final_relu, n_uniq, cap, H2_save, E));
         return ams_launch_status();
     }
-    const int skk = sk ? sk_bk<float>() : 0;        // K per stream-K stage (the bf16 stream-K path returned above)
+    // K per stream-K stage, which fixes the plan the tail reads the partial
+    // tiles by (the bf16 stream-K path returned above)
+    const int skk = !sk ? 0 : x3 ? X3::BK : sk_bk<float>();
     int tg = (cap + kTailRows - 1) / kTailRows;
     if (tg > 1024) tg = 1024;
 #define TF_LAUNCH(LL, PRV)                                                                                 \
