@@ -954,7 +954,7 @@ constexpr int kTailRows = 32;
 // for a row whose ID is out of range) and writes the finished H1 for the
 // backward.
 template <int L, bool PR>
-__global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int H, int M,
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void tail_fwd(float *__restrict__ H1, int H, int M,
                                                       int D, const void *__restrict__ W2,
                                                       const float *__restrict__ b2,
                                                       const void *__restrict__ W3,
@@ -970,9 +970,13 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
                                                       const float *__restrict__ s1, const float *__restrict__ s2)
 {
     constexpr int KB = kMaxH1 / 2 / 32;       // 32-k blocks in a K half (at most 4)
+    constexpr int KH = KB / 2;                // ... added up by each wave of a K half's pair
     __shared__ float Zp[2][kTailRows][kMaxH2 + 1];
     __shared__ float W3s[kMaxD * (kMaxH2 + 1)];
     __shared__ float h2s[kTailRows][kMaxH2 + 1];
+    __shared__ __attribute__((aligned(16))) float H1s[kTailRows][kMaxH1 + 4];   // finished rows of a cut tile
+    __shared__ __attribute__((aligned(16))) float b1s[kMaxH1];
+    __shared__ float b2s[kMaxH2], b3s[kMaxD];
     const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
     const int h = lane >> 5, r32 = lane & 31;
     const int kh = wave >> 1, nb = wave & 1, khalf = H / 2, nkb = khalf / 32;
@@ -987,8 +991,17 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
             breg[kb][q] = (kb < nkb && o < M)
                               ? ld4_any(W2, wbf16, (size_t)o * H + kh * khalf + kb * 32 + 16 * h + 4 * q)
                               : make_float4(0.f, 0.f, 0.f, 0.f);
-    if (L == 3)
-        for (int e = t; e < D * M; e += kThreads) W3s[(e / M) * (kMaxH2 + 1) + e % M] = ld_w(W3, wbf16, e);
+    // W3 (D * M <= 8 kThreads) and the biases into LDS, all loads in flight together
+    if (L == 3) {
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int e = t + i * kThreads;
+            if (e < D * M) W3s[(e / M) * (kMaxH2 + 1) + e % M] = ld_w(W3, wbf16, e);
+        }
+        if (t < D) b3s[t] = b3[t];
+    }
+    if (t < M) b2s[t] = b2[t];
+    if (sk_bk && t < H) b1s[t] = b1[t];
     const bool relu_a = (L == 3) || final_relu;
     for (int c0 = blockIdx.x * kTailRows; c0 < n_u; c0 += gridDim.x * kTailRows) {
         const int row = c0 + r32;
@@ -1007,74 +1020,89 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
             // only the first contributor can hold this tile as its second piece
             slot_a = (tile == (int)(P.it0(wa) / P.S)) ? 0 : 1;
         }
-        if (wb > wa) {
-            // tile cut by share boundaries: add the pieces in K order, one
-            // share at a time with all of this lane's 16 loads of a share in
-            // flight together (a tile spans at most three shares; more are
-            // looped)
+        const bool split = wb > wa;             // the same for the whole block (one column tile)
+        if (split) {
+            // tile cut by share boundaries: the two waves of this K half each
+            // add up half of its 32-k blocks, the pieces in K order with the
+            // loads of up to three shares in flight together (a tile spans at
+            // most three shares; more are looped), apply b1 and the
+            // activation, store H1 and pass the rows on through LDS
             const int id = uniq[rowc];
-            const bool ok = id >= 0 && (int64_t)id < n_rows;
             const int rl = rowc % Sk<float>::BM;
             const float *pr = pbuf + (size_t)rl * kSkBN + (cbase - cb * kSkBN) + 16 * h;
-#pragma unroll
-            for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-                for (int q = 0; q < 4; ++q) areg[kb][q] = make_float4(0.f, 0.f, 0.f, 0.f);
-            auto add_share = [&](int w, int sl) {
+            float4 v[3][KH][4];
+            auto load_share = [&](int w, int sl, float4 (&x)[KH][4]) {
                 const float *pw = pr + ((size_t)w * 2 + sl) * Sk<float>::TILE;
-                float4 v[KB][4];
 #pragma unroll
-                for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-                    for (int q = 0; q < 4; ++q)
-                        v[kb][q] = kb < nkb ? *(const float4 *)(pw + kb * 32 + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
-#pragma unroll
-                for (int kb = 0; kb < KB; ++kb)
+                for (int i = 0; i < KH; ++i)
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
-                        areg[kb][q].x += v[kb][q].x;
-                        areg[kb][q].y += v[kb][q].y;
-                        areg[kb][q].z += v[kb][q].z;
-                        areg[kb][q].w += v[kb][q].w;
+                        const int kb = nb * KH + i;
+                        x[i][q] = kb < nkb ? *(const float4 *)(pw + kb * 32 + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
                     }
             };
-            add_share(wa, slot_a);
-            if (wa + 1 <= wb) add_share(wa + 1, 0);
-            if (wa + 2 <= wb) add_share(wa + 2, 0);
-            for (int w = wa + 3; w <= wb; ++w) add_share(w, 0);
+            auto add = [&](float4 (&acc4)[KH][4], const float4 (&x)[KH][4]) {
 #pragma unroll
-            for (int kb = 0; kb < KB; ++kb)
+                for (int i = 0; i < KH; ++i)
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        acc4[i][q].x += x[i][q].x;
+                        acc4[i][q].y += x[i][q].y;
+                        acc4[i][q].z += x[i][q].z;
+                        acc4[i][q].w += x[i][q].w;
+                    }
+            };
+            load_share(wa, slot_a, v[0]);
+            if (wa + 1 <= wb) load_share(wa + 1, 0, v[1]);
+            if (wa + 2 <= wb) load_share(wa + 2, 0, v[2]);
+            float4 sum[KH][4];
+#pragma unroll
+            for (int i = 0; i < KH; ++i)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) sum[i][q] = make_float4(0.f, 0.f, 0.f, 0.f);
+            add(sum, v[0]);
+            if (wa + 1 <= wb) add(sum, v[1]);
+            if (wa + 2 <= wb) add(sum, v[2]);
+            for (int w = wa + 3; w <= wb; ++w) {
+                load_share(w, 0, v[0]);
+                add(sum, v[0]);
+            }
+            const bool ok = id >= 0 && (int64_t)id < n_rows;
+#pragma unroll
+            for (int i = 0; i < KH; ++i)
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
+                    const int kb = nb * KH + i;
+                    if (kb >= nkb) continue;
                     const int col = cbase + kb * 32 + 16 * h + 4 * q;
-                    float4 a = areg[kb][q];
-                    if (kb < nkb) {
-                        const float4 bb = *(const float4 *)&b1[col];
-                        a.x = ok ? a.x + bb.x : bb.x;
-                        a.y = ok ? a.y + bb.y : bb.y;
-                        a.z = ok ? a.z + bb.z : bb.z;
-                        a.w = ok ? a.w + bb.w : bb.w;
-                        // PReLU keeps Z1 in H1 (activated below); ReLU stores H1
-                        if (!PR) a = make_float4(fmaxf(a.x, 0.f), fmaxf(a.y, 0.f), fmaxf(a.z, 0.f), fmaxf(a.w, 0.f));
-                        if (nb == 0 && row < n_u) {
-                            *(float4 *)(hrow + kb * 32 + 4 * q) = a;
-                            if (H1b) {
-                                uint16_t *hb = H1b + (size_t)rowc * H + col;
-                                const uint32_t lo = ams_f32_to_bf16(a.x) | ((uint32_t)ams_f32_to_bf16(a.y) << 16);
-                                const uint32_t hi = ams_f32_to_bf16(a.z) | ((uint32_t)ams_f32_to_bf16(a.w) << 16);
-                                *(uint2 *)hb = make_uint2(lo, hi);
-                            }
+                    float4 a = sum[i][q];
+                    const float4 c = *(const float4 *)&b1s[col];
+                    a.x = ok ? a.x + c.x : c.x;
+                    a.y = ok ? a.y + c.y : c.y;
+                    a.z = ok ? a.z + c.z : c.z;
+                    a.w = ok ? a.w + c.w : c.w;
+                    // PReLU keeps Z1 in H1 (activated below); ReLU stores H1
+                    if (!PR) a = make_float4(fmaxf(a.x, 0.f), fmaxf(a.y, 0.f), fmaxf(a.z, 0.f), fmaxf(a.w, 0.f));
+                    if (row < n_u) {
+                        *(float4 *)(H1 + (size_t)rowc * H + col) = a;
+                        if (H1b) {
+                            uint16_t *hb = H1b + (size_t)rowc * H + col;
+                            const uint32_t lo = ams_f32_to_bf16(a.x) | ((uint32_t)ams_f32_to_bf16(a.y) << 16);
+                            const uint32_t hi = ams_f32_to_bf16(a.z) | ((uint32_t)ams_f32_to_bf16(a.w) << 16);
+                            *(uint2 *)hb = make_uint2(lo, hi);
                         }
                     }
-                    areg[kb][q] = a;
+                    *(float4 *)&H1s[r32][col] = a;
                 }
-        } else {
-#pragma unroll
-            for (int kb = 0; kb < KB; ++kb)
-#pragma unroll
-                for (int q = 0; q < 4; ++q)
-                    areg[kb][q] = kb < nkb ? *(const float4 *)(hrow + kb * 32 + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
         }
+        __syncthreads();                        // the pair's rows are in H1s
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                areg[kb][q] = kb >= nkb ? make_float4(0.f, 0.f, 0.f, 0.f)
+                              : split ? *(const float4 *)&H1s[r32][cbase + kb * 32 + 16 * h + 4 * q]
+                                      : *(const float4 *)(hrow + kb * 32 + 4 * q);
         if (PR) {
             // layer 1's PReLU on this lane's operands (Z1 -> H1), slope per column
 #pragma unroll
@@ -1108,7 +1136,7 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
         __syncthreads();
         for (int e = t; e < kTailRows * M; e += kThreads) {
             const int r = e / M, oo = e % M;
-            float z = Zp[0][r][oo] + Zp[1][r][oo] + b2[oo];
+            float z = Zp[0][r][oo] + Zp[1][r][oo] + b2s[oo];
             const float zpre = z;                // saved for layer 2's PReLU backward
             if (PR && L == 3) z = z > 0.f ? z : s2[oo] * z;
             else if (relu_a) z = fmaxf(z, 0.f);
@@ -1126,7 +1154,7 @@ __global__ __launch_bounds__(kThreads) void tail_fwd(float *__restrict__ H1, int
             for (int e = t; e < kTailRows * D; e += kThreads) {
                 const int r = e / D, d = e % D;
                 if (c0 + r >= n_u) continue;
-                float v = b3[d];
+                float v = b3s[d];
                 for (int oo = 0; oo < M; ++oo) v += W3s[d * (kMaxH2 + 1) + oo] * h2s[r][oo];
                 if (final_relu) v = fmaxf(v, 0.f);
                 E[(size_t)(c0 + r) * D + d] = v;
