@@ -203,20 +203,21 @@ def main():
     step.alloc_workspace(w.n_images)
     stream = torch.cuda.current_stream()
 
-    def one(b, ev=None):
+    def one(b, ev=None, st=None):
+        st = step if st is None else st
         if ev is not None:
             ev[0].record(stream)
-        step.dedup(b["ids"], w.n_images)
+        st.dedup(b["ids"], w.n_images)
         if ev is not None:
             ev[1].record(stream)
-        step.embed_fwd(T, Wd, bd)
+        st.embed_fwd(T, Wd, bd)
         if ev is not None:
             ev[2].record(stream)
-        step.pool_fwd(b["seg_off"], b["n_beh"])
-        step.pool_bwd(b["seg_off"], b["n_beh"], b["dU"], b["dA"])
+        st.pool_fwd(b["seg_off"], b["n_beh"])
+        st.pool_bwd(b["seg_off"], b["n_beh"], b["dU"], b["dA"])
         if ev is not None:
             ev[3].record(stream)
-        step.embed_bwd(T, Wd)
+        st.embed_bwd(T, Wd)
         if ev is not None:
             ev[4].record(stream)
 
@@ -259,6 +260,28 @@ def main():
     beh_total = sum(dev_batches[i]["n_beh"] for i in order)
     uniq_total = sum(n_uniq[i] for i in order)
     value = beh_total / (ms_total * 1e-3)
+    # float32 workloads: the same K steps in AMS_F32_X3 mode (float32 storage,
+    # the 4096-wide forward product on bf16 MFMA with an exact three-part
+    # split), reported beside
+    split3 = None
+    if w.dtype == "f32":
+        step3 = ams.Step(w.dims, "f32x3", mode, w.batch, n_beh_max)
+        step3.alloc_workspace(w.n_images)
+        for b in seq[:2]:
+            one(b, st=step3)
+        torch.cuda.synchronize()
+        t_start.record(stream)
+        for b in seq:
+            one(b, st=step3)
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        assert int(step3.dev_status.item()) == 0
+        ms3 = t_start.elapsed_time(t_end) / args.steps
+        split3 = {"value": beh_total / (ms3 * args.steps * 1e-3), "ms_per_step": ms3,
+                  "note": "the same steps with dtype f32x3: float32 operands, layer 1's forward product on "
+                          "bf16 MFMA with each operand split exactly into three bf16 parts (six part "
+                          "products kept, float32-rounding-sized error)"}
+        del step3
 
     # per-call durations: a second pass with events between the calls
     evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
@@ -344,6 +367,7 @@ def main():
         "samples_per_s": w.batch * args.steps / (ms_total * 1e-3),
         "pipelined": {"value": beh_total / (ms_step_pipe * args.steps * 1e-3), "ms_per_step": ms_step_pipe,
                       "note": "the same steps through StepPipeline (dedup of the next batch on a second stream)"},
+        "f32x3": split3,
         "cold": {"value": beh_total / (sum(cold_ms) * 1e-3), "ms_per_step": cold_step,
                  "note": "each step timed alone after a 512 MiB device write"},
         "per_call_ms": per,

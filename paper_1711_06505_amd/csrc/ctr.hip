@@ -27,9 +27,12 @@ constexpr int kCtrMaxLayers = 3, kCtrMaxFields = 8;
 
 // ------------------------------------------------------------ bag forward
 
-// One wave per sample: lane l adds the rows of behaviors l, l + 64, ...;
-// the lanes' partial rows are summed by a fixed butterfly, then the ad row.
-// An ID outside [0, n_rows) reads as a zero row (dedup reports it).
+// One wave per sample: lane l adds the rows of behaviors l, l + 64, ... in
+// that order; the lanes' partial rows are summed by a fixed butterfly, then
+// the ad row.  Behaviors go in rounds of U per lane (8 for rows up to 16
+// floats, else 4) with every ID load, then every row load, of a round in
+// flight together.  An ID outside [0, n_rows) reads as a zero row (dedup
+// reports it).
 template <int DM>
 __global__ __launch_bounds__(kThreads) void bag_fwd_k(int B, int D, const int32_t *__restrict__ seg_off,
                                                       int64_t n_beh, const int32_t *__restrict__ ids,
@@ -44,24 +47,42 @@ __global__ __launch_bounds__(kThreads) void bag_fwd_k(int B, int D, const int32_
 #pragma unroll
     for (int d = 0; d < DM; ++d) acc[d] = 0.f;
     const bool vec4 = (D & 3) == 0;
-    for (int j = j0 + lane; j < j1; j += AMS_WAVE) {
-        const int id = ids[j];
-        if (id < 0 || (int64_t)id >= n_rows) continue;
-        const float *r = table + (size_t)id * D;
-        if (vec4) {
+    constexpr int kBagU = DM <= 16 ? 8 : 4;
+    for (int jr = j0; jr < j1; jr += kBagU * AMS_WAVE) {
+        int id[kBagU];
 #pragma unroll
-            for (int d4 = 0; d4 < DM / 4; ++d4)
-                if (4 * d4 < D) {
-                    const float4 v = *(const float4 *)(r + 4 * d4);
-                    acc[4 * d4] += v.x;
-                    acc[4 * d4 + 1] += v.y;
-                    acc[4 * d4 + 2] += v.z;
-                    acc[4 * d4 + 3] += v.w;
+        for (int u = 0; u < kBagU; ++u) {
+            const int j = jr + u * AMS_WAVE + lane;
+            id[u] = j < j1 ? ids[j] : -1;
+        }
+        if (vec4) {
+            float4 v[kBagU][DM / 4];
+#pragma unroll
+            for (int u = 0; u < kBagU; ++u) {
+                const bool ok = id[u] >= 0 && (int64_t)id[u] < n_rows;
+                const float *r = table + (size_t)(ok ? id[u] : 0) * D;
+#pragma unroll
+                for (int d4 = 0; d4 < DM / 4; ++d4)
+                    v[u][d4] = (ok && 4 * d4 < D) ? *(const float4 *)(r + 4 * d4) : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+            for (int u = 0; u < kBagU; ++u)
+#pragma unroll
+                for (int d4 = 0; d4 < DM / 4; ++d4) {
+                    acc[4 * d4] += v[u][d4].x;
+                    acc[4 * d4 + 1] += v[u][d4].y;
+                    acc[4 * d4 + 2] += v[u][d4].z;
+                    acc[4 * d4 + 3] += v[u][d4].w;
                 }
         } else {
 #pragma unroll
-            for (int d = 0; d < DM; ++d)
-                if (d < D) acc[d] += r[d];
+            for (int u = 0; u < kBagU; ++u) {
+                if (id[u] < 0 || (int64_t)id[u] >= n_rows) continue;
+                const float *r = table + (size_t)id[u] * D;
+#pragma unroll
+                for (int d = 0; d < DM; ++d)
+                    if (d < D) acc[d] += r[d];
+            }
         }
     }
     float mine = 0.f;

@@ -41,6 +41,28 @@ def gpu_dedup(occ_dev, n_ids, n):
 
 # ------------------------------------------------------------------ bags
 
+@pytest.mark.parametrize("D", [5, 12, 20, 32])
+def test_bag_fwd_shapes_lengths_and_bad_ids(D):
+    """Row widths on both kernel instances (vector and scalar loads), empty
+    and single-behavior samples, a sample cut at the 64-lane and 512-ID round
+    boundaries and one past two rounds; IDs out of range read as zero rows."""
+    N = 1000
+    rng = np.random.default_rng(D)
+    lengths = [0, 1, 63, 64, 600, 1100, 5]
+    B = len(lengths)
+    seg = np.concatenate([[0], np.cumsum(lengths)]).astype(np.int64)
+    n_beh = int(seg[-1])
+    occ = rng.integers(0, N, size=n_beh + B).astype(np.int32)
+    occ[[3, 70, 800, n_beh + 2]] = [N, -1, N + 5, -7]
+    tab = rng.standard_normal((N, D)).astype(np.float32)
+    bag = torch.full((B, D), float("nan"), device="cuda")
+    ams.ams_bag_fwd(cuda_i32(seg), n_beh, cuda_i32(occ), torch.from_numpy(tab).cuda(), bag)
+    torch.cuda.synchronize()
+    padded = np.concatenate([tab, np.zeros((1, D), np.float32)])       # row N: the zero row
+    idx = np.where((occ >= 0) & (occ < N), occ, N)
+    assert_close(bag, oracle.bag_fwd(seg, idx, padded), F32, f"bag D={D}", rows=True)
+
+
 @pytest.mark.parametrize("name", ["tiny_joint", "mid_joint", "c4_joint"])
 def test_bag_fwd_and_bwd_match_oracle(name):
     w = mid_joint() if name == "mid_joint" else synth.get(name)
