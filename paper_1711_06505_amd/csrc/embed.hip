@@ -296,24 +296,23 @@ struct SkShape {
 };
 
 // 128-row tiles, 128-byte stage rows, 3 slots (48 KB each) for both types.
-// (256-row bf16 tiles with 64-byte stages and 4 slots, SkShape<256, 4, 64>,
-// cut the W1 stream per row in half and the layer-1 time by 7% on 163k
-// unique rows, but doubled the partial-tile bytes the tail kernel adds up,
-// which cost as much again.)
+// (256-row bf16 tiles with 64-byte stages and a 4-slot ring cut the W1
+// stream per row in half and the layer-1 time by 7% on 163k unique rows, but
+// doubled the partial-tile bytes the tail kernel adds up, which cost as much
+// again.)
 template <typename TT>
 struct Sk : SkShape<128, 3, 128> {};
 
 template <typename TT>
 constexpr int sk_bk() { return Sk<TT>::RB / (int)sizeof(TT); }   // K per stage
 
-// Chunk swizzle of a stage row: 128-byte rows as the ring of the
-// one-tile-per-block kernel; 64-byte rows: rows r and r + 4 (same banks)
-// take different chunks.
+// Chunk swizzle of a 128-byte stage row, as in the ring of the one-tile-per-
+// block kernel (bits 0-3 of the row).
 template <class K>
 __device__ __forceinline__ int sk_swz(int row)
 {
-    if constexpr (K::CPR == 8) return ring_swz(row);      // bits 0-3 of the row
-    else return (row >> 2) & 3;                           // bits 2-3 of the row
+    static_assert(K::CPR == 8, "stage rows of 8 chunks");
+    return ring_swz(row);
 }
 
 struct SkPlan {
@@ -467,8 +466,7 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
     constexpr int BK = sk_bk<TT>();
     __shared__ __attribute__((aligned(16))) float ring0[K::SLOT];
     __shared__ __attribute__((aligned(16))) float ring1[K::SLOT];
-    __shared__ __attribute__((aligned(16))) float ring2[K::R >= 3 ? K::SLOT : 4];
-    __shared__ __attribute__((aligned(16))) float ring3[K::R == 4 ? K::SLOT : 4];
+    __shared__ __attribute__((aligned(16))) float ring2[K::R == 3 ? K::SLOT : 4];
     __shared__ int rid[K::BM];
 
     const int n_u = min(*n_uniq_p, cap);
@@ -515,35 +513,7 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
 #pragma unroll
             for (int nb = 0; nb < kSkNB; ++nb) acc[mb][nb] = (v16f){};
         const int n = ke - ks;
-        if constexpr (K::R == 4) {
-            // 4 slots: at the top of stage s, stages s+1 and s+2 may still be
-            // in flight; after the barrier (everyone is done with the slot of
-            // s-1) stage s+3 is issued into it and stage s is computed.
-#define SK_STAGE4(cur, nxt, s)                                                     \
-    do {                                                                           \
-        __builtin_amdgcn_sched_barrier(0);                                         \
-        AMS_WAIT_VM_LDS(2 * K::PW);                                                \
-        __builtin_amdgcn_s_barrier();                                              \
-        __builtin_amdgcn_sched_barrier(0);                                         \
-        sk_issue<TT>(nxt, src, (int64_t)(ks + min((s) + 3, n - 1)) * K::RB, wave); \
-        __builtin_amdgcn_sched_barrier(0);                                         \
-        sk_compute<TT>(cur, acc, lane, wave);                                      \
-    } while (0)
-            sk_issue<TT>(ring0, src, (int64_t)ks * K::RB, wave);
-            sk_issue<TT>(ring1, src, (int64_t)(ks + min(1, n - 1)) * K::RB, wave);
-            sk_issue<TT>(ring2, src, (int64_t)(ks + min(2, n - 1)) * K::RB, wave);
-            int s = 0;
-            for (; s + 4 <= n; s += 4) {
-                SK_STAGE4(ring0, ring3, s);
-                SK_STAGE4(ring1, ring0, s + 1);
-                SK_STAGE4(ring2, ring1, s + 2);
-                SK_STAGE4(ring3, ring2, s + 3);
-            }
-            if (s < n) SK_STAGE4(ring0, ring3, s);
-            if (s + 1 < n) SK_STAGE4(ring1, ring0, s + 1);
-            if (s + 2 < n) SK_STAGE4(ring2, ring1, s + 2);
-#undef SK_STAGE4
-        } else if constexpr (K::R == 3) {
+        if constexpr (K::R == 3) {
 #define SK_STAGE(cur, nxt, s)                                                      \
     do {                                                                           \
         __builtin_amdgcn_sched_barrier(0);                                         \
@@ -1711,25 +1681,27 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
 }
 
 // Sum of the tail backward's block partials, written straight into dW2, db2,
-// dW3, db3, db1 and (PReLU) the slope gradients.  Thread (e, q) of a block sums partials g = q, q + 4, ...
-// in eight running chains (independent loads in flight); the chains, then the
-// four q, are added in a fixed order, so the result is deterministic.
-__global__ __launch_bounds__(256) void tail_reduce(const float *__restrict__ part, int G, int PS, int L,
-                                                   int H, int M, int D, float *__restrict__ dW2,
-                                                   float *__restrict__ db2, float *__restrict__ dW3,
-                                                   float *__restrict__ db3, float *__restrict__ db1,
-                                                   float *__restrict__ ds1, float *__restrict__ ds2)
+// dW3, db3, db1 and (PReLU) the slope gradients.  Thread (e, q) of a block
+// (64 elements x kRedQ groups) sums partials g = q, q + kRedQ, ... in eight
+// running chains (independent loads in flight); the chains, then the groups,
+// are added in a fixed order, so the result is deterministic.
+constexpr int kRedQ = 16;
+__global__ __launch_bounds__(64 * kRedQ) void tail_reduce(const float *__restrict__ part, int G, int PS, int L,
+                                                          int H, int M, int D, float *__restrict__ dW2,
+                                                          float *__restrict__ db2, float *__restrict__ dW3,
+                                                          float *__restrict__ db3, float *__restrict__ db1,
+                                                          float *__restrict__ ds1, float *__restrict__ ds2)
 {
-    __shared__ float sq[4][64];
+    __shared__ float sq[kRedQ][64];
     const int t = threadIdx.x, q = t >> 6;
     const int e = blockIdx.x * 64 + (t & 63);
     float c[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if (e < PS) {
         int k = 0;
-        for (; q + 4 * (k + 7) < G; k += 8)
+        for (; q + kRedQ * (k + 7) < G; k += 8)
 #pragma unroll
-            for (int r = 0; r < 8; ++r) c[r] += part[(size_t)(q + 4 * (k + r)) * PS + e];
-        for (int r = 0; r < 8 && q + 4 * (k + r) < G; ++r) c[r] += part[(size_t)(q + 4 * (k + r)) * PS + e];
+            for (int r = 0; r < 8; ++r) c[r] += part[(size_t)(q + kRedQ * (k + r)) * PS + e];
+        for (int r = 0; r < 8 && q + kRedQ * (k + r) < G; ++r) c[r] += part[(size_t)(q + kRedQ * (k + r)) * PS + e];
     }
     float tot = 0.f;
 #pragma unroll
@@ -1737,7 +1709,9 @@ __global__ __launch_bounds__(256) void tail_reduce(const float *__restrict__ par
     sq[q][t & 63] = tot;
     __syncthreads();
     if (q != 0 || e >= PS) return;
-    const float v = ((sq[0][t] + sq[1][t]) + sq[2][t]) + sq[3][t];
+    float v = sq[0][t];
+#pragma unroll
+    for (int j = 1; j < kRedQ; ++j) v += sq[j][t];
     const int Mo = (L == 3) ? M : D;
     const int n2 = Mo * H, n3 = (L == 3) ? D * M : 0, nb3 = (L == 3) ? D : 0;
     int x = e;
@@ -1775,8 +1749,6 @@ __global__ __launch_bounds__(kThreads) void partial_reduce(const float *__restri
     for (int r = 0; r < 8; ++r) tot += s[r];
     out[e] = tot;
 }
-
-// Scatter the reduced tail partials into the caller's gradient arrays.
 
 // ------------------------------------------------------------- dW1 split-K
 
@@ -2892,7 +2864,7 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
         TB_LAUNCH(2, float, float, false);
     }
 #undef TB_LAUNCH
-    AMS_LAUNCH("tail_reduce", st, tail_reduce<<<(PS + 63) / 64, 256, 0, st>>>(tail, TG, PS, L, H, M, D, dW2,
+    AMS_LAUNCH("tail_reduce", st, tail_reduce<<<(PS + 63) / 64, 64 * kRedQ, 0, st>>>(tail, TG, PS, L, H, M, D, dW2,
                                                                           db2, dW3, db3, db1, ds1, ds2));
 
     const int bm = (H % 128 == 0) ? 128 : 64;
@@ -2931,6 +2903,7 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
                                                                dw1p));
     }
     const size_t nw = (size_t)H * F;
+    // (four elements per thread as float4 measured twice as slow: 21 vs 10 us)
     AMS_LAUNCH("reduce_dw1", st, partial_reduce<<<(unsigned)((nw + kThreads - 1) / kThreads), kThreads, 0, st>>>(dw1p, p.kc, nw, dW1));
     return ams_launch_status();
 }
