@@ -43,7 +43,8 @@
  *             AMS_F32_X3: T and W float32 as AMS_F32.  The 4096-wide layer's
  *             forward product (dims[1] a multiple of 256) runs on bf16 MFMA:
  *             every float32 operand is split exactly into three bf16 parts
- *             h + m + l (round to nearest at each step) and six of the nine
+ *             h + m + l (round to nearest at each step; exact for
+ *             |x| >= 2^-100, where all parts are normal) and six of the nine
  *             part products (hh, hm, mh, hl, lh, mm) are accumulated in
  *             float32; the three left out stay below 2^-22 |x y| per
  *             product, about one float32 rounding.  Everything else as

@@ -571,7 +571,8 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
 // (AMS_F32_X3.)  A float32 x is the exact sum of three bf16 values h =
 // bf16(x), m = bf16(x - h), l = bf16(x - h - m), each rounded to nearest:
 // both residuals are exact in float32 (x and h are within a factor 2 of each
-// other), and at most 8 significant bits are left for l.  Of the nine part
+// other), and at most 8 significant bits are left for l (exact while l is a
+// normal number, |x| >= 2^-100).  Of the nine part
 // products of x y the six kept (hh, hm, mh, hl, lh, mm) leave out
 // |ml + lm + ll| < 2^-22 |x y| (|m| <= 2^-8 |x|, |l| <= 2^-16 |x|), and each
 // part product is exact in the float32 accumulator.  A 16-deep k step is six
