@@ -1202,16 +1202,35 @@ __global__ __launch_bounds__(kThreads) void tail_fwd_bf16(uint16_t *__restrict__
     const int h = lane >> 5, r32 = lane & 31;
     const int Mo = (L == 3) ? M : D;           // width of the second layer's output
     constexpr int cpr = H / 8;                 // 16-byte chunks per W2 row
-    for (int idx = t; idx < kMaxH2 * cpr; idx += kThreads) {
-        const int o = idx / cpr, c = idx % cpr;
-        const uint4 v = o < Mo ? *(const uint4 *)&W2[(size_t)o * H + c * 8] : make_uint4(0, 0, 0, 0);
-        *(uint4 *)&W2s[o * H + ((c ^ (o & 7)) << 3)] = v;
-    }
-    if (L == 3)
-        for (int e = t; e < 32 * kW3S; e += kThreads) {
-            const int d = e / kW3S, o = e % kW3S;
-            W3s[e] = (d < D && o < M) ? W3[d * M + o] : (uint16_t)0;
+    // W2 and W3 into LDS with every load of the block in flight together
+    static_assert(kMaxH2 * cpr % kThreads == 0, "W2 chunks per thread");
+    {
+        uint4 v[kMaxH2 * cpr / kThreads];
+#pragma unroll
+        for (int i = 0; i < kMaxH2 * cpr / kThreads; ++i) {
+            const int idx = t + i * kThreads, o = idx / cpr, c = idx % cpr;
+            v[i] = o < Mo ? *(const uint4 *)&W2[(size_t)o * H + c * 8] : make_uint4(0, 0, 0, 0);
         }
+#pragma unroll
+        for (int i = 0; i < kMaxH2 * cpr / kThreads; ++i) {
+            const int idx = t + i * kThreads, o = idx / cpr, c = idx % cpr;
+            *(uint4 *)&W2s[o * H + ((c ^ (o & 7)) << 3)] = v[i];
+        }
+    }
+    if (L == 3) {
+        constexpr int n3 = (32 * kW3S + kThreads - 1) / kThreads;
+        uint16_t v[n3];
+#pragma unroll
+        for (int i = 0; i < n3; ++i) {
+            const int e = t + i * kThreads, d = e / kW3S, o = e % kW3S;
+            v[i] = (e < 32 * kW3S && d < D && o < M) ? W3[d * M + o] : (uint16_t)0;
+        }
+#pragma unroll
+        for (int i = 0; i < n3; ++i) {
+            const int e = t + i * kThreads;
+            if (e < 32 * kW3S) W3s[e] = v[i];
+        }
+    }
     // this lane's outputs o = 32 ob + 8 q + 4 h + r and their biases
     float bias[2][16];
 #pragma unroll
@@ -1467,8 +1486,10 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
             W2s[e] = i < H ? x : 0.f;
         }
         const brsrc_t rW3 = make_buf(L == 3 ? W3 : W2, L == 3 ? (uint32_t)(D * M * sizeof(TW)) : 0u);
-        for (int e = threadIdx.x; e < 2 * SD * kMaxH2; e += kTbThreads) {
-            const int d = e / kMaxH2, o = e % kMaxH2;
+        static_assert(2 * SD * kMaxH2 % kTbThreads == 0, "W3 entries per thread");
+#pragma unroll
+        for (int i = 0; i < 2 * SD * kMaxH2 / kTbThreads; ++i) {
+            const int e = threadIdx.x + i * kTbThreads, d = e / kMaxH2, o = e % kMaxH2;
             const float x = buf_ld<TW>(rW3, (uint32_t)(d * M + min(o, M - 1)));
             W3s[e] = o < M ? x : 0.f;
         }
@@ -2328,9 +2349,25 @@ void tail_bwd_bf16(const uint16_t *__restrict__ H1b, const float *__restrict__ H
     if (blockIdx.x == 0)
         for (int i = t; i < zero_n; i += kThreads) zero_row[i] = 0.f;
     const int Mo = (L == 3) ? M : D;
-    for (int e = t; e < kMaxH2 * H; e += kThreads) {
-        const int o = e / H, i = e % H;
-        *(uint16_t *)(W2T + i * kW2S + o * 2) = o < Mo ? W2[(size_t)o * H + i] : (uint16_t)0;
+    // W2 transposed into LDS: 8 consecutive i of one row o per 16-byte load,
+    // every load of the block in flight together
+    static_assert(kMaxH2 * H / 8 % kThreads == 0, "W2 chunks per thread");
+    {
+        constexpr int NC = kMaxH2 * H / 8 / kThreads;
+        uint4 v[NC];
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const int q = t + c * kThreads, o = q / (H / 8), i0 = (q % (H / 8)) * 8;
+            v[c] = o < Mo ? *(const uint4 *)&W2[(size_t)o * H + i0] : make_uint4(0, 0, 0, 0);
+        }
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            const int q = t + c * kThreads, o = q / (H / 8), i0 = (q % (H / 8)) * 8;
+            const uint32_t w[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
+#pragma unroll
+            for (int j = 0; j < 8; ++j)
+                *(uint16_t *)(W2T + (i0 + j) * kW2S + o * 2) = (uint16_t)(w[j >> 1] >> (16 * (j & 1)));
+        }
     }
     const int po = t & 63, pg = t >> 6;        // phase-A role: output o, row group
     float w3c[DM];                             // W3[:, po] (3 layers)
