@@ -263,6 +263,25 @@ def main():
     # float32 workloads: the same K steps in AMS_F32_X3 mode (float32 storage,
     # the 4096-wide forward product on bf16 MFMA with an exact three-part
     # split), reported beside
+    # the workload's other pooling modes: the same steps with each, reported beside
+    other_modes = {}
+    for m in w.pools:
+        if m == mode:
+            continue
+        stm = ams.Step(w.dims, w.dtype, m, w.batch, n_beh_max)
+        stm.alloc_workspace(w.n_images)
+        for b in seq[:2]:
+            one(b, st=stm)
+        torch.cuda.synchronize()
+        t_start.record(stream)
+        for b in seq:
+            one(b, st=stm)
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        assert int(stm.dev_status.item()) == 0
+        msm = t_start.elapsed_time(t_end) / args.steps
+        other_modes[m] = {"value": beh_total / (msm * args.steps * 1e-3), "ms_per_step": msm}
+        del stm
     split3 = None
     if w.dtype == "f32":
         step3 = ams.Step(w.dims, "f32x3", mode, w.batch, n_beh_max)
@@ -368,6 +387,7 @@ def main():
         "pipelined": {"value": beh_total / (ms_step_pipe * args.steps * 1e-3), "ms_per_step": ms_step_pipe,
                       "note": "the same steps through StepPipeline (dedup of the next batch on a second stream)"},
         "f32x3": split3,
+        "other_pooling_modes": other_modes or None,
         "cold": {"value": beh_total / (sum(cold_ms) * 1e-3), "ms_per_step": cold_step,
                  "note": "each step timed alone after a 512 MiB device write"},
         "per_call_ms": per,

@@ -82,15 +82,39 @@ __global__ __launch_bounds__(kThreads) void pool_fwd_k(int B, int D, const int32
     const int ad_row = inv[n_beh + i];
     if (MODE != kPoolQuery && lane < D) A[(size_t)i * D + lane] = E[(size_t)ad_row * D + lane];
     float out[DM];
+    // sum and max: lane l takes behaviors l, l + 64, ... in that order, in
+    // rounds of PU per lane with the round's index loads, then its row
+    // loads, in flight together
+    constexpr int PU = DM <= 16 ? 4 : 2;
+    auto load_round = [&](int jr, float (&e)[PU][DM]) {
+        int r[PU];
+#pragma unroll
+        for (int q = 0; q < PU; ++q) {
+            const int j = jr + q * AMS_WAVE + lane;
+            r[q] = j < j1 ? inv[j] : -1;
+        }
+#pragma unroll
+        for (int q = 0; q < PU; ++q) {
+            if (r[q] >= 0) load_row<DM>(E, r[q], D, e[q]);
+            else {
+#pragma unroll
+                for (int d = 0; d < DM; ++d) e[q][d] = 0.f;
+            }
+        }
+    };
     if (MODE == AMS_POOL_SUM) {
         float acc[DM];
 #pragma unroll
         for (int d = 0; d < DM; ++d) acc[d] = 0.f;
-        for (int j = j0 + lane; j < j1; j += AMS_WAVE) {
-            float e[DM];
-            load_row<DM>(E, inv[j], D, e);
+        for (int jr = j0; jr < j1; jr += PU * AMS_WAVE) {
+            float e[PU][DM];
+            load_round(jr, e);
 #pragma unroll
-            for (int d = 0; d < DM; ++d) acc[d] += e[d];
+            for (int q = 0; q < PU; ++q)
+                if (jr + q * AMS_WAVE + lane < j1) {
+#pragma unroll
+                    for (int d = 0; d < DM; ++d) acc[d] += e[q][d];
+                }
         }
 #pragma unroll
         for (int d = 0; d < DM; ++d) out[d] = ams_wave_sum(acc[d]);
@@ -102,15 +126,20 @@ __global__ __launch_bounds__(kThreads) void pool_fwd_k(int B, int D, const int32
             best[d] = 0.f;
             bidx[d] = -1;
         }
-        for (int j = j0 + lane; j < j1; j += AMS_WAVE) {
-            float e[DM];
-            load_row<DM>(E, inv[j], D, e);
+        for (int jr = j0; jr < j1; jr += PU * AMS_WAVE) {
+            float e[PU][DM];
+            load_round(jr, e);
 #pragma unroll
-            for (int d = 0; d < DM; ++d)
-                if (bidx[d] < 0 || e[d] > best[d]) {
-                    best[d] = e[d];
-                    bidx[d] = j;
-                }
+            for (int q = 0; q < PU; ++q) {
+                const int j = jr + q * AMS_WAVE + lane;
+                if (j >= j1) continue;
+#pragma unroll
+                for (int d = 0; d < DM; ++d)
+                    if (bidx[d] < 0 || e[q][d] > best[d]) {
+                        best[d] = e[q][d];
+                        bidx[d] = j;
+                    }
+            }
         }
         // first maximum over the segment: larger value wins, ties -> lower j
 #pragma unroll
