@@ -984,10 +984,13 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         const int cb = cbase / kSkBN;
         int wa = 0, wb = -1, slot_a = 0;
         if (sk_bk) {
+            // the chunk's 32 rows lie in one row tile (BM is a multiple of
+            // 32): the plan is the same for the whole wave, worked out on the
+            // scalar unit
             const SkPlan P = sk_plan(n_u, H, F, G, sk_bk, Sk<float>::BM);
-            const int tile = (rowc / Sk<float>::BM) * P.n_cb + cb;
-            wa = P.owner((int64_t)tile * P.S);
-            wb = P.owner((int64_t)(tile + 1) * P.S - 1);
+            const int tile = __builtin_amdgcn_readfirstlane((c0 / Sk<float>::BM) * P.n_cb + cb);
+            wa = __builtin_amdgcn_readfirstlane(P.owner((int64_t)tile * P.S));
+            wb = __builtin_amdgcn_readfirstlane(P.owner((int64_t)(tile + 1) * P.S - 1));
             // only the first contributor can hold this tile as its second piece
             slot_a = (tile == (int)(P.it0(wa) / P.S)) ? 0 : 1;
         }
@@ -2812,8 +2815,12 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
     // K per stream-K stage, which fixes the plan the tail reads the partial
     // tiles by (the bf16 stream-K path returned above)
     const int skk = !sk ? 0 : x3 ? X3::BK : sk_bk<float>();
+    // at most the two blocks per CU that fit at once (LDS); the kernel loops
+    // over chunks, and blocks sized for cap but past n_u would each still
+    // cost a dispatch (with 1024 blocks for ~400 chunks the launch took
+    // 34 us while each wave lived 6 us)
     int tg = (cap + kTailRows - 1) / kTailRows;
-    if (tg > 1024) tg = 1024;
+    if (tg > 2 * sk_workers()) tg = 2 * sk_workers();
 #define TF_LAUNCH(LL, PRV)                                                                                 \
     AMS_LAUNCH("tail_fwd", st, (tail_fwd<LL, PRV><<<tg, kThreads, 0, st>>>(                                   \
                                    H1f, H, M, D, W2, b2, W3, b3, bf, mlp->final_relu, n_uniq, cap, H2_save, E, \
