@@ -147,23 +147,25 @@ __device__ __forceinline__ int pass_bits(const Plan &P, int pass)
 }
 
 // Global digit histograms (partials per prep block), range check, zeroing.
-__global__ __launch_bounds__(kThreads) void dd_prep(const uint32_t *__restrict__ keys, int n, Plan P,
-                                                    uint32_t n_ids, int32_t *__restrict__ hpart,
-                                                    int32_t *__restrict__ bad,
-                                                    uint32_t *__restrict__ words, int n_words)
+// 1024 threads per block: one LDS histogram per wave (a hot ID's digit then
+// contends within one wave only), 16 waves adding at once.
+constexpr int kPrepThreads = 1024;
+constexpr int kPrepWaves = kPrepThreads / AMS_WAVE;
+__global__ __launch_bounds__(kPrepThreads) void dd_prep(const uint32_t *__restrict__ keys, int n, Plan P,
+                                                        uint32_t n_ids, int32_t *__restrict__ hpart,
+                                                        int32_t *__restrict__ bad,
+                                                        uint32_t *__restrict__ words, int n_words)
 {
-    // one histogram per wave (a hot ID's digit then contends within one wave
-    // only); eight keys per thread are loaded before their counts are added
+    // eight keys per thread are loaded before their counts are added
     constexpr int U = 8;
-    __shared__ int h[kWaves][kMaxPasses][kRadix];
+    __shared__ int h[kPrepWaves][kMaxPasses][kRadix];
     const int t = threadIdx.x, wave = t / AMS_WAVE;
-    for (int w = 0; w < kWaves; ++w)
-        for (int p = 0; p < kMaxPasses; ++p) h[w][p][t] = 0;
-    for (int i = blockIdx.x * kThreads + t; i < n_words; i += gridDim.x * kThreads) words[i] = 0;
+    for (int i = t; i < kPrepWaves * kMaxPasses * kRadix; i += kPrepThreads) (&h[0][0][0])[i] = 0;
+    for (int i = blockIdx.x * kPrepThreads + t; i < n_words; i += gridDim.x * kPrepThreads) words[i] = 0;
     __syncthreads();
     bool out = false;
-    const int stride = gridDim.x * kThreads;
-    for (int i0 = blockIdx.x * kThreads + t; i0 < n; i0 += U * stride) {
+    const int stride = gridDim.x * kPrepThreads;
+    for (int i0 = blockIdx.x * kPrepThreads + t; i0 < n; i0 += U * stride) {
         uint32_t k[U];
 #pragma unroll
         for (int u = 0; u < U; ++u) {
@@ -181,11 +183,12 @@ __global__ __launch_bounds__(kThreads) void dd_prep(const uint32_t *__restrict__
         }
     }
     const int any_out = __syncthreads_or(out);
-    for (int p = 0; p < P.passes; ++p) {
-        int c = 0;
-        for (int w = 0; w < kWaves; ++w) c += h[w][p][t];
-        hpart[((size_t)blockIdx.x * kMaxPasses + p) * kRadix + t] = c;
-    }
+    if (t < kRadix)
+        for (int p = 0; p < P.passes; ++p) {
+            int c = 0;
+            for (int w = 0; w < kPrepWaves; ++w) c += h[w][p][t];
+            hpart[((size_t)blockIdx.x * kMaxPasses + p) * kRadix + t] = c;
+        }
     if (t == 0) bad[blockIdx.x] = any_out;
 }
 
@@ -426,7 +429,7 @@ extern "C" ams_status ams_dedup(const int32_t *ids, int64_t n_occ, int32_t n_ids
     uint32_t *words = (uint32_t *)(w + L.off_words);
     int32_t *err = (int32_t *)(words + L.n_words - 1);
 
-    AMS_LAUNCH("dd_prep", st, dd_prep<<<L.n_prep, kThreads, 0, st>>>((const uint32_t *)ids, n, L.P, (uint32_t)n_ids, hpart, bad, words,
+    AMS_LAUNCH("dd_prep", st, dd_prep<<<L.n_prep, kPrepThreads, 0, st>>>((const uint32_t *)ids, n, L.P, (uint32_t)n_ids, hpart, bad, words,
                                           L.n_words));
     const uint32_t *kin = (const uint32_t *)ids;
     const int32_t *vin = nullptr;
