@@ -299,12 +299,32 @@ __global__ __launch_bounds__(kThreads) void dd_unique(const uint32_t *__restrict
     __shared__ uint32_t tile_base;
     const int t = threadIdx.x, w = t / AMS_WAVE;
     const int i0 = blockIdx.x * kTile + t * kItems;
+    static_assert(kItems == 8, "two 16-byte loads per thread");
+    // a thread's 8 keys and values: two 16-byte loads each when all 8 are in
+    // range (i0 is a multiple of 8), else one by one
+    const bool full = i0 + kItems <= n;
+    uint32_t kk[kItems];
+    int32_t vv[kItems];
+    if (full) {
+        const uint4 a = *(const uint4 *)(k + i0), b = *(const uint4 *)(k + i0 + 4);
+        const int4 x = *(const int4 *)(v + i0), y = *(const int4 *)(v + i0 + 4);
+        kk[0] = a.x; kk[1] = a.y; kk[2] = a.z; kk[3] = a.w; kk[4] = b.x; kk[5] = b.y; kk[6] = b.z; kk[7] = b.w;
+        vv[0] = x.x; vv[1] = x.y; vv[2] = x.z; vv[3] = x.w; vv[4] = y.x; vv[5] = y.y; vv[6] = y.z; vv[7] = y.w;
+    } else {
+#pragma unroll
+        for (int q = 0; q < kItems; ++q) {
+            kk[q] = i0 + q < n ? k[i0 + q] : 0u;
+            vv[q] = i0 + q < n ? v[i0 + q] : 0;
+        }
+    }
+    const uint32_t kprev = (i0 > 0 && i0 < n) ? k[i0 - 1] : 0u;
     int flag[kItems];
     int c = 0;
 #pragma unroll
     for (int q = 0; q < kItems; ++q) {
         const int i = i0 + q;
-        flag[q] = (i < n && (i == 0 || k[i] != k[i - 1])) ? 1 : 0;
+        const uint32_t before = q == 0 ? kprev : kk[q - 1];
+        flag[q] = (i < n && (i == 0 || kk[q] != before)) ? 1 : 0;
         c += flag[q];
     }
     const int incl = ams_wave_incl_scan(c);
@@ -331,17 +351,23 @@ __global__ __launch_bounds__(kThreads) void dd_unique(const uint32_t *__restrict
     __syncthreads();
     int run = (int)tile_base + incl - c;      // heads strictly before position i0
     for (int x = 0; x < w; ++x) run += ws[x];
+    // (the caller's occ_perm may start anywhere: 16-byte stores only when aligned)
+    const bool vec_out = full && (((uintptr_t)occ_perm & 15) == 0);
+    if (vec_out) {
+        *(int4 *)(occ_perm + i0) = make_int4(vv[0], vv[1], vv[2], vv[3]);
+        *(int4 *)(occ_perm + i0 + 4) = make_int4(vv[4], vv[5], vv[6], vv[7]);
+    }
 #pragma unroll
     for (int q = 0; q < kItems; ++q) {
         const int i = i0 + q;
         if (i >= n) break;
         run += flag[q];
         const int rank = run - 1;
-        const int32_t occ = v[i];
-        occ_perm[i] = occ;
+        const int32_t occ = vv[q];
+        if (!vec_out) occ_perm[i] = occ;
         inv[occ] = rank;
         if (flag[q]) {
-            uniq[rank] = (int32_t)k[i];
+            uniq[rank] = (int32_t)kk[q];
             uniq_off[rank] = i;
         }
         if (i == n - 1) {
