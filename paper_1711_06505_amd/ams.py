@@ -146,6 +146,9 @@ def _stream(stream):
 
 
 def make_mlp(dims, dtype: str = "f32", final_relu: bool = False) -> ams_mlp:
+    """ams_mlp for layer widths `dims`; dtype "f32", "bf16" or "f32x3" (float32
+    storage, the first layer's forward product on bf16 MFMA with an exact
+    three-part split of each operand)."""
     m = ams_mlp()
     m.n_layers = len(dims) - 1
     for i, d in enumerate(dims):
