@@ -466,7 +466,7 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
     constexpr int BK = sk_bk<TT>();
     __shared__ __attribute__((aligned(16))) float ring0[K::SLOT];
     __shared__ __attribute__((aligned(16))) float ring1[K::SLOT];
-    __shared__ __attribute__((aligned(16))) float ring2[K::R == 3 ? K::SLOT : 4];
+    __shared__ __attribute__((aligned(16))) float ring2[K::SLOT];
     __shared__ int rid[K::BM];
 
     const int n_u = min(*n_uniq_p, cap);
@@ -513,7 +513,13 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
 #pragma unroll
             for (int nb = 0; nb < kSkNB; ++nb) acc[mb][nb] = (v16f){};
         const int n = ke - ks;
-        if constexpr (K::R == 3) {
+        // 3 slots: at the top of stage s, stages s and s+1 may be in flight;
+        // the wait leaves only s+1, the barrier (everyone done with the slot
+        // of s-1) lets stage s+2 be issued into that slot, and stage s is
+        // computed meanwhile.  Past the end the last stage is loaded again
+        // (same data, into a slot nobody reads).
+        static_assert(K::R == 3, "three ring slots");
+        {
 #define SK_STAGE(cur, nxt, s)                                                      \
     do {                                                                           \
         __builtin_amdgcn_sched_barrier(0);                                         \
@@ -535,28 +541,6 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
             if (s < n) SK_STAGE(ring0, ring2, s);
             if (s + 1 < n) SK_STAGE(ring1, ring0, s + 1);
 #undef SK_STAGE
-        } else {
-            // 2 slots: at the top of stage s only stage s is in flight; after the
-            // barrier (everyone is done with the other slot) stage s+1 is issued
-            // into it and stage s is computed meanwhile.
-#define SK_STAGE2(cur, nxt, s)                                                     \
-    do {                                                                           \
-        __builtin_amdgcn_sched_barrier(0);                                         \
-        AMS_WAIT_VM_LDS(0);                                                        \
-        __builtin_amdgcn_s_barrier();                                              \
-        __builtin_amdgcn_sched_barrier(0);                                         \
-        if ((s) + 1 < n) sk_issue<TT>(nxt, src, (int64_t)(ks + (s) + 1) * K::RB, wave); \
-        __builtin_amdgcn_sched_barrier(0);                                         \
-        sk_compute<TT>(cur, acc, lane, wave);                                      \
-    } while (0)
-            sk_issue<TT>(ring0, src, (int64_t)ks * K::RB, wave);
-            int s = 0;
-            for (; s + 2 <= n; s += 2) {
-                SK_STAGE2(ring0, ring1, s);
-                SK_STAGE2(ring1, ring0, s + 1);
-            }
-            if (s < n) SK_STAGE2(ring0, ring1, s);
-#undef SK_STAGE2
         }
         AMS_WAIT_VM(0);
 
