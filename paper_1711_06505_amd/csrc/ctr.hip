@@ -693,22 +693,54 @@ __global__ __launch_bounds__(kThreads) void ctr_reduce_k(const float *__restrict
 
 // ---------------------------------------------------------------- Adagrad
 
+// One thread per 4 elements of a touched row when D % 4 == 0 and the arrays
+// are 16-byte aligned (vec4), else per element; a grid-stride loop over the
+// n_u rows the device counted (the grid is sized for at most kAdaBlocks, not
+// for the host cap, whose blocks past n_u would each still be dispatched).
+constexpr int kAdaBlocks = 2048;
+__device__ __forceinline__ float ada_one(float p, float g, float &a, float lr, float eps)
+{
+    a = a + g * g;
+    return p - lr * g / (sqrtf(a) + eps);
+}
+
 __global__ __launch_bounds__(kThreads) void adagrad_k(int D, const int32_t *__restrict__ uniq,
                                                       const int32_t *__restrict__ n_uniq_p, int cap,
                                                       const float *__restrict__ grad, float *__restrict__ table,
-                                                      int64_t n_rows, float *__restrict__ accum, float lr, float eps)
+                                                      int64_t n_rows, float *__restrict__ accum, float lr, float eps,
+                                                      int vec4)
 {
     const int n_u = min(*n_uniq_p, cap);
-    const int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (e >= (int64_t)n_u * D) return;
-    const int u = (int)(e / D), d = (int)(e % D);
-    const int r = uniq[u];
-    if (r < 0 || (int64_t)r >= n_rows) return;
-    const float g = grad[e];
-    const size_t x = (size_t)r * D + d;
-    const float acc = accum[x] + g * g;
-    accum[x] = acc;
-    table[x] -= lr * g / (sqrtf(acc) + eps);
+    const int64_t stride = (int64_t)gridDim.x * kThreads;
+    if (vec4) {
+        const int D4 = D / 4;
+        const int64_t n4 = (int64_t)n_u * D4;
+        for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < n4; e += stride) {
+            const int u = (int)(e / D4), d = (int)(e % D4) * 4;
+            const int r = uniq[u];
+            if (r < 0 || (int64_t)r >= n_rows) continue;
+            const float4 g = *(const float4 *)(grad + (size_t)u * D + d);
+            const size_t x = (size_t)r * D + d;
+            float4 a = *(const float4 *)(accum + x), t = *(const float4 *)(table + x);
+            t.x = ada_one(t.x, g.x, a.x, lr, eps);
+            t.y = ada_one(t.y, g.y, a.y, lr, eps);
+            t.z = ada_one(t.z, g.z, a.z, lr, eps);
+            t.w = ada_one(t.w, g.w, a.w, lr, eps);
+            *(float4 *)(accum + x) = a;
+            *(float4 *)(table + x) = t;
+        }
+    } else {
+        const int64_t n = (int64_t)n_u * D;
+        for (int64_t e = (int64_t)blockIdx.x * kThreads + threadIdx.x; e < n; e += stride) {
+            const int u = (int)(e / D), d = (int)(e % D);
+            const int r = uniq[u];
+            if (r < 0 || (int64_t)r >= n_rows) continue;
+            const size_t x = (size_t)r * D + d;
+            float a = accum[x];
+            table[x] = ada_one(table[x], grad[e], a, lr, eps);
+            accum[x] = a;
+        }
+    }
 }
 
 // ------------------------------------------------------------------- Adam
@@ -998,9 +1030,11 @@ extern "C" ams_status ams_adagrad_rows(int32_t D, const int32_t *uniq, const int
     if (n_uniq_cap == 0) return AMS_OK;
     if (!uniq || !n_uniq || !grad || !table || !accum) return AMS_ERR_NULL;
     hipStream_t st = (hipStream_t)stream;
-    const int64_t n = (int64_t)n_uniq_cap * D;
-    AMS_LAUNCH("adagrad_rows", st, adagrad_k<<<(unsigned)((n + kThreads - 1) / kThreads), kThreads, 0, st>>>(
-                                       D, uniq, n_uniq, n_uniq_cap, grad, table, n_rows, accum, lr, eps));
+    const int vec4 = (D % 4 == 0) && ((((uintptr_t)grad) | ((uintptr_t)table) | ((uintptr_t)accum)) & 15) == 0;
+    const int64_t n = (int64_t)n_uniq_cap * (vec4 ? D / 4 : D);
+    const int64_t g = (n + kThreads - 1) / kThreads;
+    AMS_LAUNCH("adagrad_rows", st, adagrad_k<<<(unsigned)(g < kAdaBlocks ? g : kAdaBlocks), kThreads, 0, st>>>(
+                                       D, uniq, n_uniq, n_uniq_cap, grad, table, n_rows, accum, lr, eps, vec4));
     return ams_launch_status();
 }
 
