@@ -34,7 +34,11 @@
  *             ams_dedup (*n_uniq) and read there by later calls; they take a
  *             host upper bound `n_uniq_cap` (n_u <= n_uniq_cap <= n_occ) that
  *             sizes grids and buffers.  Work past n_u is skipped and outputs
- *             past n_u are left unspecified.
+ *             past n_u are left unspecified.  A bound below the real n_u
+ *             leaves the rows past it uncomputed and the occurrences that
+ *             refer to them dropped (read as zero rows): results are then
+ *             unspecified, but no call reads or writes outside the
+ *             buffers the bound sizes.
  * Layouts:    row-major.  Feature table T is [n_rows x dims[0]].  Weights
  *             W_l are [dims[l+1] x dims[l]] (out x in), biases float32
  *             [dims[l+1]].  E, U, A, dE, dU, dA have row stride D = dims[last]
@@ -227,7 +231,12 @@ ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n_rows,
  *                   occurrences j in [seg_off[i], seg_off[i+1]);
  *                   seg_off[0] = 0, seg_off[B] = n_beh, non-decreasing.
  * inv[n_beh+B]      from ams_dedup (behaviors then ads).
- * E [n_u x D]       embeddings from ams_embed_fwd.
+ * n_uniq_cap        rows of E (host).  An occurrence whose unique index is
+ *                   n_uniq_cap or more (only possible when the caller's
+ *                   capacity is below the real unique count) reads a zero
+ *                   row: results are then unspecified, but nothing outside
+ *                   E is read.
+ * E [n_uniq_cap x D] embeddings from ams_embed_fwd.
  * U [B x D]         out: pooled user vectors (empty segment -> 0).
  * A [B x D]         out: the ad image embedding of each sample, E[inv[n_beh+i]].
  * saved             out: MAX: int32 [B x D] index j of the first maximum
@@ -235,7 +244,7 @@ ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n_rows,
  *                   weights; SUM: unused (may be NULL). */
 ams_status ams_pool_fwd(int32_t mode, int32_t B, int32_t D,
                         const int32_t *seg_off, int64_t n_beh,
-                        const int32_t *inv, const float *E,
+                        const int32_t *inv, int32_t n_uniq_cap, const float *E,
                         float *U, float *A, void *saved, void *stream);
 
 /* ---------------------------------------------------------- pool bwd ----
@@ -246,6 +255,10 @@ ams_status ams_pool_fwd(int32_t mode, int32_t B, int32_t D,
  * dE [cap x D]      out: for each unique image, the sum over its occurrences
  *                   (in ascending occurrence order) of the gradient w.r.t.
  *                   that occurrence's embedding; fully overwritten for u < n_u.
+ *                   E and dE have n_uniq_cap rows: occurrences whose unique
+ *                   index is n_uniq_cap or more (a capacity below the real
+ *                   unique count) are dropped and read E as a zero row, so
+ *                   no access leaves the caller's buffers.
  * ws                at least ams_pool_workspace(mode, B, n_beh, D, cap) bytes. */
 size_t ams_pool_workspace(int32_t mode, int32_t B, int64_t n_beh, int32_t D,
                           int32_t n_uniq_cap);
@@ -267,8 +280,8 @@ ams_status ams_pool_bwd(int32_t mode, int32_t B, int32_t D,
  *
  * fwd:  Q [B x D] queries (device); U [B x D] out: u_i = sum_j w_j e_j with
  *       w = softmax_j(e_j . q_i) (max subtracted; an empty segment pools to
- *       0); w [n_beh] out: the attention weights.  Other arguments as in
- *       ams_pool_fwd.
+ *       0); w [n_beh] out: the attention weights.  Other arguments (E with
+ *       n_uniq_cap rows) as in ams_pool_fwd.
  * bwd:  with dU [B x D] the loss gradient of U, the gradient of behavior j is
  *       w_j dU_i + ds_j q_i, ds_j = w_j (dU_i . e_j - dU_i . u_i); dE[u]
  *       receives the sum over the behaviors of image u in ascending order
@@ -279,8 +292,8 @@ ams_status ams_pool_bwd(int32_t mode, int32_t B, int32_t D,
  *       ws: at least ams_pool_workspace(AMS_POOL_ATT, B, n_beh, D, cap) bytes.
  * Host errors as ams_pool_fwd / ams_pool_bwd. */
 ams_status ams_pool_query_fwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
-                              const int32_t *inv, const float *E, const float *Q,
-                              float *U, float *w, void *stream);
+                              const int32_t *inv, int32_t n_uniq_cap, const float *E,
+                              const float *Q, float *U, float *w, void *stream);
 ams_status ams_pool_query_bwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
                               const int32_t *inv, const int32_t *occ_perm,
                               const int32_t *uniq_off, const int32_t *n_uniq,
@@ -305,8 +318,8 @@ ams_status ams_pool_query_bwd(int32_t B, int32_t D, const int32_t *seg_off, int6
  *       ws: at least ams_pool_workspace(AMS_POOL_SUM, B, n_beh, D, cap).
  * Other arguments and host errors as ams_pool_fwd / ams_pool_bwd. */
 ams_status ams_pool_concat_fwd(int32_t B, int32_t D, int32_t Lc, const int32_t *seg_off,
-                               int64_t n_beh, const int32_t *inv, const float *E,
-                               float *U, float *A, void *stream);
+                               int64_t n_beh, const int32_t *inv, int32_t n_uniq_cap,
+                               const float *E, float *U, float *A, void *stream);
 ams_status ams_pool_concat_bwd(int32_t B, int32_t D, int32_t Lc, const int32_t *seg_off,
                                int64_t n_beh, const int32_t *inv, const int32_t *occ_perm,
                                const int32_t *uniq_off, const int32_t *n_uniq,

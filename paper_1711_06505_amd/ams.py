@@ -77,7 +77,7 @@ def load() -> ctypes.CDLL:
     lib.ams_embed_bwd.argtypes = [M, P, i64, P, P, i32, P, P, P, PP, P, P, P, P, P, P, P, P, P, P, PP, P, sz,
                                   P]
     lib.ams_pool_fwd.restype = ctypes.c_int
-    lib.ams_pool_fwd.argtypes = [i32, i32, i32, P, i64, P, P, P, P, P, P]
+    lib.ams_pool_fwd.argtypes = [i32, i32, i32, P, i64, P, i32, P, P, P, P, P]
     lib.ams_pool_workspace.restype = sz
     lib.ams_pool_workspace.argtypes = [i32, i32, i64, i32, i32]
     lib.ams_pool_bwd.restype = ctypes.c_int
@@ -102,11 +102,11 @@ def load() -> ctypes.CDLL:
     lib.ams_adagrad_rows.restype = ctypes.c_int
     lib.ams_adagrad_rows.argtypes = [i32, P, P, i32, P, P, i64, P, ctypes.c_float, ctypes.c_float, P]
     lib.ams_pool_query_fwd.restype = ctypes.c_int
-    lib.ams_pool_query_fwd.argtypes = [i32, i32, P, i64, P, P, P, P, P, P]
+    lib.ams_pool_query_fwd.argtypes = [i32, i32, P, i64, P, i32, P, P, P, P, P]
     lib.ams_pool_query_bwd.restype = ctypes.c_int
     lib.ams_pool_query_bwd.argtypes = [i32, i32, P, i64, P, P, P, P, i32, P, P, P, P, P, P, P, i32, P, sz, P]
     lib.ams_pool_concat_fwd.restype = ctypes.c_int
-    lib.ams_pool_concat_fwd.argtypes = [i32, i32, i32, P, i64, P, P, P, P, P]
+    lib.ams_pool_concat_fwd.argtypes = [i32, i32, i32, P, i64, P, i32, P, P, P, P]
     lib.ams_pool_concat_bwd.restype = ctypes.c_int
     lib.ams_pool_concat_bwd.argtypes = [i32, i32, i32, P, i64, P, P, P, P, i32, P, P, P, P, sz, P]
     f = ctypes.c_float
@@ -137,6 +137,13 @@ def _p(t):
     if t is None:
         return None
     return ctypes.c_void_p(t.data_ptr())
+
+
+def _rows_at_least(n: int, **tensors):
+    """Every named tensor must hold at least n rows (the capacity the call is told)."""
+    for name, t in tensors.items():
+        if t is not None and t.shape[0] < int(n):
+            raise ValueError(f"{name} has {t.shape[0]} rows, fewer than the capacity {int(n)}")
 
 
 def _stream(stream):
@@ -202,8 +209,8 @@ def ams_embed_bwd(mlp, T, uniq, n_uniq, n_uniq_cap, W, H1_save, H2_save, E_fwd, 
 def ams_pool_fwd(mode, seg_off, n_beh, inv, E, U, A, saved, stream=None):
     m = POOL[mode] if isinstance(mode, str) else int(mode)
     B = seg_off.numel() - 1
-    _check(load().ams_pool_fwd(m, B, U.shape[1], _p(seg_off), int(n_beh), _p(inv), _p(E), _p(U), _p(A),
-                               _p(saved), _stream(stream)), "ams_pool_fwd")
+    _check(load().ams_pool_fwd(m, B, U.shape[1], _p(seg_off), int(n_beh), _p(inv), E.shape[0], _p(E), _p(U),
+                               _p(A), _p(saved), _stream(stream)), "ams_pool_fwd")
 
 
 def ams_pool_workspace(mode, B: int, n_beh: int, D: int, n_uniq_cap: int) -> int:
@@ -215,6 +222,7 @@ def ams_pool_bwd(mode, seg_off, n_beh, inv, occ_perm, uniq_off, n_uniq, n_uniq_c
                  dU, dA, dE, ws, stream=None):
     m = POOL[mode] if isinstance(mode, str) else int(mode)
     B = seg_off.numel() - 1
+    _rows_at_least(n_uniq_cap, E=E, dE=dE)
     _check(load().ams_pool_bwd(m, B, U.shape[1], _p(seg_off), int(n_beh), _p(inv), _p(occ_perm),
                                _p(uniq_off), _p(n_uniq), int(n_uniq_cap), _p(E), _p(U), _p(A), _p(saved),
                                _p(dU), _p(dA), _p(dE), _p(ws),
@@ -241,13 +249,14 @@ def ams_timing_read(cap: int = 64) -> dict:
 
 def ams_pool_query_fwd(seg_off, n_beh: int, inv, E, Q, U, w, stream=None):
     B, D = Q.shape
-    _check(load().ams_pool_query_fwd(B, D, _p(seg_off), int(n_beh), _p(inv), _p(E), _p(Q), _p(U), _p(w),
-                                     _stream(stream)), "ams_pool_query_fwd")
+    _check(load().ams_pool_query_fwd(B, D, _p(seg_off), int(n_beh), _p(inv), E.shape[0], _p(E), _p(Q), _p(U),
+                                     _p(w), _stream(stream)), "ams_pool_query_fwd")
 
 
 def ams_pool_query_bwd(seg_off, n_beh: int, inv, occ_perm, uniq_off, n_uniq, n_uniq_cap: int, E, Q, U, w, dU, dQ,
                        dE, accumulate: bool, ws, stream=None):
     B, D = Q.shape
+    _rows_at_least(n_uniq_cap, E=E, dE=dE)
     _check(load().ams_pool_query_bwd(B, D, _p(seg_off), int(n_beh), _p(inv), _p(occ_perm), _p(uniq_off),
                                      _p(n_uniq), int(n_uniq_cap), _p(E), _p(Q), _p(U), _p(w), _p(dU), _p(dQ),
                                      _p(dE), int(bool(accumulate)), _p(ws), ws.numel() * ws.element_size(),
@@ -262,13 +271,14 @@ def ams_adam_update(param, grad, m, v, lr: float, t: int, b1: float = 0.9, b2: f
 
 def ams_pool_concat_fwd(Lc: int, seg_off, n_beh: int, inv, E, U, A, stream=None):
     B, D = seg_off.numel() - 1, E.shape[1]
-    _check(load().ams_pool_concat_fwd(B, D, int(Lc), _p(seg_off), int(n_beh), _p(inv), _p(E), _p(U), _p(A),
-                                      _stream(stream)), "ams_pool_concat_fwd")
+    _check(load().ams_pool_concat_fwd(B, D, int(Lc), _p(seg_off), int(n_beh), _p(inv), E.shape[0], _p(E), _p(U),
+                                      _p(A), _stream(stream)), "ams_pool_concat_fwd")
 
 
 def ams_pool_concat_bwd(Lc: int, seg_off, n_beh: int, inv, occ_perm, uniq_off, n_uniq, n_uniq_cap: int, dU, dA,
                         dE, ws, stream=None):
     B, D = seg_off.numel() - 1, dE.shape[1]
+    _rows_at_least(n_uniq_cap, dE=dE)
     _check(load().ams_pool_concat_bwd(B, D, int(Lc), _p(seg_off), int(n_beh), _p(inv), _p(occ_perm), _p(uniq_off),
                                       _p(n_uniq), int(n_uniq_cap), _p(dU), _p(dA), _p(dE), _p(ws),
                                       ws.numel() * ws.element_size(), _stream(stream)), "ams_pool_concat_bwd")
@@ -300,6 +310,7 @@ def ams_bag_workspace(B: int, n_beh: int, D: int, n_uniq_cap: int) -> int:
 def ams_bag_bwd(seg_off, n_beh: int, inv, occ_perm, uniq_off, n_uniq, n_uniq_cap: int, dbag, grad, ws,
                 stream=None):
     B, D = dbag.shape
+    _rows_at_least(n_uniq_cap, grad=grad)
     _check(load().ams_bag_bwd(B, D, _p(seg_off), int(n_beh), _p(inv), _p(occ_perm), _p(uniq_off), _p(n_uniq),
                               int(n_uniq_cap), _p(dbag), _p(grad), _p(ws), ws.numel() * ws.element_size(),
                               _stream(stream)), "ams_bag_bwd")
@@ -359,13 +370,17 @@ class Step:
 
     Buffers are sized for up to B samples and n_beh_max behaviors; `cap`
     (default B + n_beh_max) bounds the unique count used for grids, since n_u
-    is only known on the device.  With `prelu` (float32 models) the hidden
-    layers use PReLU: the slopes are passed to run / embed_fwd / embed_bwd
-    and their gradients land in `dslope`.
+    is only known on the device.  A cap below B + n_beh_max saves memory but
+    can be exceeded by a batch with more distinct images: the kernels then
+    stay inside the buffers and the results are unspecified, so such a Step
+    is only built with ``cap_checked=True``, by a caller that checks
+    `capacity_ok()` after its steps.  With `prelu` (float32 models) the
+    hidden layers use PReLU: the slopes are passed to run / embed_fwd /
+    embed_bwd and their gradients land in `dslope`.
     """
 
     def __init__(self, dims, dtype: str, mode: str, B: int, n_beh_max: int, final_relu: bool = False,
-                 device="cuda", cap: int | None = None, prelu: bool = False):
+                 device="cuda", cap: int | None = None, prelu: bool = False, cap_checked: bool = False):
         self.mlp = make_mlp(dims, dtype, final_relu)
         self.dims = tuple(dims)
         self.dtype = dtype
@@ -373,6 +388,9 @@ class Step:
         self.B, self.n_beh = int(B), int(n_beh_max)
         self.n_occ = self.n_beh + self.B
         self.cap = self.n_occ if cap is None else int(cap)
+        if self.cap < 0 or (self.cap < self.n_occ and not cap_checked):
+            raise ValueError(f"cap {self.cap} is below the {self.n_occ} occurrences a batch may hold: "
+                             "pass cap_checked=True and check capacity_ok() after the step")
         D, H = dims[-1], dims[1]
         dev = torch.device(device)
         i32, f32 = torch.int32, torch.float32
@@ -402,6 +420,10 @@ class Step:
         self.dslope = [torch.empty((o,), dtype=f32, device=dev) for o in dims[1:-1]] if prelu else None
         self.ws = None
         self.n_ids = None
+
+    def capacity_ok(self) -> bool:
+        """True when the last dedup's unique count fits the cap (synchronises)."""
+        return int(self.n_uniq.item()) <= self.cap
 
     def alloc_workspace(self, n_ids: int):
         """One workspace shared by the five calls (they run in order on one stream)."""

@@ -85,7 +85,7 @@ __device__ uint32_t lookback(uint32_t *words, int stride, int t, uint32_t count,
         }
         if (!ready) {                             // some tile of the batch has not published
             if (++spins < kSpinLimit) continue;
-            *err = 1;
+            __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             break;
         }
         spins = 0;
@@ -121,7 +121,7 @@ __device__ uint32_t lookback_wave(uint32_t *words, int t, uint32_t count, int32_
         const uint32_t w = j >= 0 ? ld_relaxed(&words[j]) : kPrefix;   // before tile 0: prefix 0
         if (ams_ballot((w & ~kValMask) == 0) != 0) {                   // not all published yet
             if (++spins < kSpinLimit) continue;
-            if (lane == 0) *err = 1;
+            if (lane == 0) __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
             break;
         }
         spins = 0;
@@ -287,6 +287,7 @@ __global__ __launch_bounds__(kThreads) void dd_pass(const uint32_t *__restrict__
 __global__ __launch_bounds__(kThreads) void dd_unique(const uint32_t *__restrict__ k,
                                                       const int32_t *__restrict__ v, int n,
                                                       uint32_t *__restrict__ words, int32_t *__restrict__ err,
+                                                      uint32_t *__restrict__ done,
                                                       const int32_t *__restrict__ bad, int n_prep,
                                                       int32_t *__restrict__ uniq, int32_t *__restrict__ inv,
                                                       int32_t *__restrict__ occ_perm,
@@ -297,6 +298,7 @@ __global__ __launch_bounds__(kThreads) void dd_unique(const uint32_t *__restrict
     constexpr int kItems = kTile / kThreads;  // 8 consecutive positions per thread
     __shared__ int ws[kWaves];
     __shared__ uint32_t tile_base;
+    __shared__ int last_tile;
     const int t = threadIdx.x, w = t / AMS_WAVE;
     const int i0 = blockIdx.x * kTile + t * kItems;
     static_assert(kItems == 8, "two 16-byte loads per thread");
@@ -334,21 +336,26 @@ __global__ __launch_bounds__(kThreads) void dd_unique(const uint32_t *__restrict
         int tot = 0;
         for (int x = 0; x < kWaves; ++x) tot += ws[x];
         const uint32_t b = lookback_wave(words, blockIdx.x, (uint32_t)tot, err);
-        if (t == 0) tile_base = b;
-    }
-    int any_bad = 0;
-    if (blockIdx.x == 0) {
-        int mine = 0;
-        for (int b = t; b < n_prep; b += kThreads) mine |= bad[b];
-        any_bad = __syncthreads_or(mine);
-    }
-    if (blockIdx.x == 0 && t == 0) {
-        // a look-back bound hit in an earlier pass is a runtime failure
-        *dev_status = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                          ? AMS_ERR_HIP
-                          : (any_bad ? AMS_ERR_ID_RANGE : AMS_OK);
+        if (t == 0) {
+            tile_base = b;
+            // the tile that finishes its look-back last writes the status: by
+            // then every tile's wait has ended or recorded its failure in
+            // *err (ordered before this count by release/acquire)
+            last_tile = __hip_atomic_fetch_add(done, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) ==
+                        gridDim.x - 1;
+        }
     }
     __syncthreads();
+    if (last_tile) {
+        int mine = 0;
+        for (int b = t; b < n_prep; b += kThreads) mine |= bad[b];
+        const int any_bad = __syncthreads_or(mine);
+        // a look-back bound hit in any pass is a runtime failure
+        if (t == 0)
+            *dev_status = __hip_atomic_load(err, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT)
+                              ? AMS_ERR_HIP
+                              : (any_bad ? AMS_ERR_ID_RANGE : AMS_OK);
+    }
     int run = (int)tile_base + incl - c;      // heads strictly before position i0
     for (int x = 0; x < w; ++x) run += ws[x];
     // (the caller's occ_perm may start anywhere: 16-byte stores only when aligned)
@@ -386,7 +393,7 @@ __global__ void dd_empty(int32_t *n_uniq, int32_t *dev_status, int32_t *uniq_off
     }
 }
 
-int id_bits(int32_t n_ids)
+constexpr int id_bits(int32_t n_ids)
 {
     int b = 1;
     while (b < 31 && (1ll << b) < (long long)n_ids) ++b;
@@ -399,7 +406,7 @@ struct Layout {
     size_t off_kb, off_va, off_vb, off_hpart, off_bad, off_words, total;
 };
 
-Layout layout(int64_t n_occ, int32_t n_ids)
+constexpr Layout layout(int64_t n_occ, int32_t n_ids)
 {
     Layout L{};
     L.P.bits = id_bits(n_ids);
@@ -407,8 +414,9 @@ Layout layout(int64_t n_occ, int32_t n_ids)
     L.P.width = (L.P.bits + L.P.passes - 1) / L.P.passes;
     L.P.ntiles = (int)((n_occ + kTile - 1) / kTile);
     L.n_prep = L.P.ntiles < kPrepBlocks ? (L.P.ntiles > 0 ? L.P.ntiles : 1) : kPrepBlocks;
-    L.n_words = L.P.passes * L.P.ntiles * kRadix + L.P.ntiles + 1;   // last word: look-back error flag
-    auto al = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    // the last two words: the look-back error flag and the count of unique-pass tiles done
+    L.n_words = L.P.passes * L.P.ntiles * kRadix + L.P.ntiles + 2;
+    auto al = [](size_t x) constexpr { return (x + 255) & ~(size_t)255; };
     const size_t nb = al((size_t)n_occ * 4);
     size_t o = nb;                           // keys ping (pong is the caller's ids on pass 0)
     L.off_kb = o; o += nb;
@@ -419,6 +427,45 @@ Layout layout(int64_t n_occ, int32_t n_ids)
     L.off_words = o; o += al((size_t)L.n_words * 4);
     L.total = o;
     return L;
+}
+
+// Enqueues the whole dedup with its workspace at `w` (layout L).
+ams_status dedup_enqueue(const int32_t *ids, int n, int32_t n_ids, int32_t *uniq, int32_t *inv,
+                         int32_t *occ_perm, int32_t *uniq_off, int32_t *n_uniq, int32_t *dev_status,
+                         char *w, const Layout &L, hipStream_t st)
+{
+    if (n == 0) {
+        AMS_LAUNCH("dd_empty", st, dd_empty<<<1, 64, 0, st>>>(n_uniq, dev_status, uniq_off));
+        return ams_launch_status();
+    }
+    uint32_t *ka = (uint32_t *)w;
+    uint32_t *kb = (uint32_t *)(w + L.off_kb);
+    int32_t *va = (int32_t *)(w + L.off_va);
+    int32_t *vb = (int32_t *)(w + L.off_vb);
+    int32_t *hpart = (int32_t *)(w + L.off_hpart);
+    int32_t *bad = (int32_t *)(w + L.off_bad);
+    uint32_t *words = (uint32_t *)(w + L.off_words);
+    int32_t *err = (int32_t *)(words + L.n_words - 2);
+    uint32_t *done = words + L.n_words - 1;
+
+    // dd_prep also zeroes every look-back word, the error flag and the tile count
+    AMS_LAUNCH("dd_prep", st, dd_prep<<<L.n_prep, kPrepThreads, 0, st>>>((const uint32_t *)ids, n, L.P, (uint32_t)n_ids, hpart, bad, words,
+                                          L.n_words));
+    const uint32_t *kin = (const uint32_t *)ids;
+    const int32_t *vin = nullptr;
+    uint32_t *bufk[2] = {ka, kb};
+    int32_t *bufv[2] = {va, vb};
+    for (int pass = 0; pass < L.P.passes; ++pass) {
+        uint32_t *kout = bufk[pass & 1];
+        int32_t *vout = bufv[pass & 1];
+        AMS_LAUNCH("dd_pass", st, dd_pass<<<L.P.ntiles, kThreads, 0, st>>>(kin, vin, kout, vout, n, L.P, pass, hpart, L.n_prep, words,
+                                                 err));
+        kin = kout;
+        vin = vout;
+    }
+    AMS_LAUNCH("dd_unique", st, dd_unique<<<L.P.ntiles, kThreads, 0, st>>>(kin, vin, n, words + (size_t)L.P.passes * L.P.ntiles * kRadix,
+                                              err, done, bad, L.n_prep, uniq, inv, occ_perm, uniq_off, n_uniq, dev_status));
+    return ams_launch_status();
 }
 
 }  // namespace
@@ -439,37 +486,6 @@ extern "C" ams_status ams_dedup(const int32_t *ids, int64_t n_occ, int32_t n_ids
     if (n_occ > 0 && (!ids || !uniq || !inv || !occ_perm || !ws)) return AMS_ERR_NULL;
     const Layout L = layout(n_occ, n_ids);
     if (n_occ > 0 && ws_bytes < L.total) return AMS_ERR_WORKSPACE;
-    hipStream_t st = (hipStream_t)stream;
-    const int n = (int)n_occ;
-    if (n == 0) {
-        AMS_LAUNCH("dd_empty", st, dd_empty<<<1, 64, 0, st>>>(n_uniq, dev_status, uniq_off));
-        return ams_launch_status();
-    }
-    char *w = (char *)ws;
-    uint32_t *ka = (uint32_t *)w;
-    uint32_t *kb = (uint32_t *)(w + L.off_kb);
-    int32_t *va = (int32_t *)(w + L.off_va);
-    int32_t *vb = (int32_t *)(w + L.off_vb);
-    int32_t *hpart = (int32_t *)(w + L.off_hpart);
-    int32_t *bad = (int32_t *)(w + L.off_bad);
-    uint32_t *words = (uint32_t *)(w + L.off_words);
-    int32_t *err = (int32_t *)(words + L.n_words - 1);
-
-    AMS_LAUNCH("dd_prep", st, dd_prep<<<L.n_prep, kPrepThreads, 0, st>>>((const uint32_t *)ids, n, L.P, (uint32_t)n_ids, hpart, bad, words,
-                                          L.n_words));
-    const uint32_t *kin = (const uint32_t *)ids;
-    const int32_t *vin = nullptr;
-    uint32_t *bufk[2] = {ka, kb};
-    int32_t *bufv[2] = {va, vb};
-    for (int pass = 0; pass < L.P.passes; ++pass) {
-        uint32_t *kout = bufk[pass & 1];
-        int32_t *vout = bufv[pass & 1];
-        AMS_LAUNCH("dd_pass", st, dd_pass<<<L.P.ntiles, kThreads, 0, st>>>(kin, vin, kout, vout, n, L.P, pass, hpart, L.n_prep, words,
-                                                 err));
-        kin = kout;
-        vin = vout;
-    }
-    AMS_LAUNCH("dd_unique", st, dd_unique<<<L.P.ntiles, kThreads, 0, st>>>(kin, vin, n, words + (size_t)L.P.passes * L.P.ntiles * kRadix,
-                                              err, bad, L.n_prep, uniq, inv, occ_perm, uniq_off, n_uniq, dev_status));
-    return ams_launch_status();
+    return dedup_enqueue(ids, (int)n_occ, n_ids, uniq, inv, occ_perm, uniq_off, n_uniq, dev_status, (char *)ws, L,
+                         (hipStream_t)stream);
 }

@@ -59,6 +59,19 @@ __device__ __forceinline__ void load_row(const float *__restrict__ E, int row, i
     }
 }
 
+// Row `row` of E when it is below the row count `cap`, else a zero row: a
+// caller whose capacity is below the real unique count gets unspecified
+// values, never an access past its buffers.
+template <int DM>
+__device__ __forceinline__ void load_row_cap(const float *__restrict__ E, int row, int cap, int D, float (&e)[DM])
+{
+    if ((unsigned)row < (unsigned)cap) load_row<DM>(E, row, D, e);
+    else {
+#pragma unroll
+        for (int d = 0; d < DM; ++d) e[d] = 0.f;
+    }
+}
+
 // Calls f with the register width DM (12, 16 or 32) that covers D.
 template <class F>
 void with_dm(int D, F f)
@@ -70,7 +83,7 @@ void with_dm(int D, F f)
 
 template <int MODE, int DM>
 __global__ __launch_bounds__(kThreads) void pool_fwd_k(int B, int D, const int32_t *__restrict__ seg_off,
-                                                       int64_t n_beh, const int32_t *__restrict__ inv,
+                                                       int64_t n_beh, const int32_t *__restrict__ inv, int cap,
                                                        const float *__restrict__ E, float *__restrict__ U,
                                                        float *__restrict__ A, void *__restrict__ saved,
                                                        const float *__restrict__ Q)
@@ -80,7 +93,8 @@ __global__ __launch_bounds__(kThreads) void pool_fwd_k(int B, int D, const int32
     if (i >= B) return;
     const int j0 = seg_off[i], j1 = seg_off[i + 1];
     const int ad_row = inv[n_beh + i];
-    if (MODE != kPoolQuery && lane < D) A[(size_t)i * D + lane] = E[(size_t)ad_row * D + lane];
+    if (MODE != kPoolQuery && lane < D)
+        A[(size_t)i * D + lane] = (unsigned)ad_row < (unsigned)cap ? E[(size_t)ad_row * D + lane] : 0.f;
     float out[DM];
     // sum and max: lane l takes behaviors l, l + 64, ... in that order, in
     // rounds of PU per lane with the round's index loads, then its row
@@ -92,6 +106,7 @@ __global__ __launch_bounds__(kThreads) void pool_fwd_k(int B, int D, const int32
         for (int q = 0; q < PU; ++q) {
             const int j = jr + q * AMS_WAVE + lane;
             r[q] = j < j1 ? inv[j] : -1;
+            if (r[q] >= cap) r[q] = -1;
         }
 #pragma unroll
         for (int q = 0; q < PU; ++q) {
@@ -166,7 +181,7 @@ __global__ __launch_bounds__(kThreads) void pool_fwd_k(int B, int D, const int32
         // The logits are kept in w and normalised in a second, cheap pass.
         float a[DM];
         if (MODE == kPoolQuery) load_row<DM>(Q, i, D, a);
-        else load_row<DM>(E, ad_row, D, a);
+        else load_row_cap<DM>(E, ad_row, cap, D, a);
         float *w = (float *)saved;
         float m = -INFINITY, den = 0.f, acc[DM];
 #pragma unroll
@@ -187,14 +202,14 @@ __global__ __launch_bounds__(kThreads) void pool_fwd_k(int B, int D, const int32
         for (; j + AMS_WAVE < j1; j += 2 * AMS_WAVE) {   // two rows in flight
             const int r0 = inv[j], r1 = inv[j + AMS_WAVE];
             float e0[DM], e1[DM];
-            load_row<DM>(E, r0, D, e0);
-            load_row<DM>(E, r1, D, e1);
+            load_row_cap<DM>(E, r0, cap, D, e0);
+            load_row_cap<DM>(E, r1, cap, D, e1);
             take(j, e0);
             take(j + AMS_WAVE, e1);
         }
         if (j < j1) {
             float e0[DM];
-            load_row<DM>(E, inv[j], D, e0);
+            load_row_cap<DM>(E, inv[j], cap, D, e0);
             take(j, e0);
         }
         const float M = ams_wave_max(m);
@@ -218,7 +233,7 @@ __global__ __launch_bounds__(kThreads) void pool_fwd_k(int B, int D, const int32
 // embedding rows come from L2.
 __global__ __launch_bounds__(kThreads) void pool_concat_fwd_k(int B, int D, int Lc,
                                                               const int32_t *__restrict__ seg_off, int64_t n_beh,
-                                                              const int32_t *__restrict__ inv,
+                                                              const int32_t *__restrict__ inv, int cap,
                                                               const float *__restrict__ E, float *__restrict__ U,
                                                               float *__restrict__ A)
 {
@@ -229,11 +244,13 @@ __global__ __launch_bounds__(kThreads) void pool_concat_fwd_k(int B, int D, int 
             const int r = (int)(e - (int64_t)i * row);
             const int p = r / D, d = r - p * D;
             const int j0 = seg_off[i], len = seg_off[i + 1] - j0;
-            U[e] = p < len ? E[(size_t)inv[j0 + p] * D + d] : 0.f;
+            const int row_u = p < len ? inv[j0 + p] : -1;
+            U[e] = (unsigned)row_u < (unsigned)cap ? E[(size_t)row_u * D + d] : 0.f;
         } else {
             const int64_t x = e - nU;
             const int i = (int)(x / D), d = (int)(x - (int64_t)i * D);
-            A[x] = E[(size_t)inv[n_beh + i] * D + d];
+            const int r = inv[n_beh + i];
+            A[x] = (unsigned)r < (unsigned)cap ? E[(size_t)r * D + d] : 0.f;
         }
     }
 }
@@ -242,7 +259,7 @@ __global__ __launch_bounds__(kThreads) void pool_concat_fwd_k(int B, int D, int 
 // c_i = g_i . u_i and da_i = sum_j ds_j e_j, ds_j = w_j (g_i . e_j - c_i).
 template <int MODE, int DM>
 __global__ __launch_bounds__(kThreads) void pool_bwd_sample(int B, int D, const int32_t *__restrict__ seg_off,
-                                                            const int32_t *__restrict__ inv,
+                                                            const int32_t *__restrict__ inv, int cap,
                                                             const float *__restrict__ E,
                                                             const float *__restrict__ U,
                                                             const float *__restrict__ wsaved,
@@ -278,14 +295,14 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_sample(int B, int D, const 
     for (; j + AMS_WAVE < j1; j += 2 * AMS_WAVE) {       // two rows in flight
         const int r0 = inv[j], r1 = inv[j + AMS_WAVE];
         float e0[DM], e1[DM];
-        load_row<DM>(E, r0, D, e0);
-        load_row<DM>(E, r1, D, e1);
+        load_row_cap<DM>(E, r0, cap, D, e0);
+        load_row_cap<DM>(E, r1, cap, D, e1);
         take(j, e0);
         take(j + AMS_WAVE, e1);
     }
     if (j < j1) {
         float e0[DM];
-        load_row<DM>(E, inv[j], D, e0);
+        load_row_cap<DM>(E, inv[j], cap, D, e0);
         take(j, e0);
     }
     float mine = 0.f;
@@ -335,7 +352,7 @@ __device__ __forceinline__ void seg_scan(int u, float (&v)[DM])
 
 // (2) segmented sums over chunks of 64 positions of the stable occurrence order.
 template <int MODE, int DM>
-__global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int64_t n_beh, int n_occ,
+__global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int64_t n_beh, int n_occ, int cap,
                                                          const int32_t *__restrict__ inv,
                                                          const int32_t *__restrict__ occ_perm,
                                                          const int32_t *__restrict__ uniq_off,
@@ -358,14 +375,18 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int64_t n_beh, i
     if (ch >= nch) return;
     const int c0 = ch * AMS_WAVE, c1 = c0 + AMS_WAVE;
     const int p = c0 + lane;
-    const bool valid = p < n_occ;
+    // an occurrence whose unique index is at or past the caller's capacity
+    // (possible only when the capacity is below the real unique count) is
+    // dropped: its row of dE does not exist
+    const int k = p < n_occ ? occ_perm[p] : 0;
+    const int uk = p < n_occ ? inv[k] : -1;
+    const bool valid = p < n_occ && uk < cap;
     int u = -1 - lane;       // distinct per invalid lane: never joins a run
     float v[DM];
 #pragma unroll
     for (int d = 0; d < DM; ++d) v[d] = 0.f;
     if (valid) {
-        const int k = occ_perm[p];
-        u = inv[k];
+        u = uk;
         if (k < n_beh) {
             const int i = samp[k];
             float g[DM];
@@ -492,15 +513,15 @@ PoolPlan plan_pool(int32_t B, int64_t n_beh, int32_t D)
 }
 
 template <int MODE, int DM>
-void launch_fwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32_t *inv, const float *E,
+void launch_fwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32_t *inv, int cap, const float *E,
                 float *U, float *A, void *saved, hipStream_t st, const float *Q = nullptr)
 {
-    AMS_LAUNCH("pool_fwd_k", st, pool_fwd_k<MODE, DM><<<(B + kWaves - 1) / kWaves, kThreads, 0, st>>>(B, D, seg_off, n_beh, inv, E, U, A,
-                                                                         saved, Q));
+    AMS_LAUNCH("pool_fwd_k", st, pool_fwd_k<MODE, DM><<<(B + kWaves - 1) / kWaves, kThreads, 0, st>>>(B, D, seg_off, n_beh, inv, cap,
+                                                                         E, U, A, saved, Q));
 }
 
 template <int MODE, int DM>
-void launch_bwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32_t *inv,
+void launch_bwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32_t *inv, int cap,
                 const int32_t *occ_perm, const int32_t *uniq_off, const float *E, const float *U,
                 const float *A, const void *saved, const float *dU, const float *dA, float *dE,
                 char *ws, const PoolPlan &p, hipStream_t st, float *dQ = nullptr, int accumulate = 0,
@@ -516,9 +537,9 @@ void launch_bwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32
     const int n_occ = (int)(n_beh + B);
     if (B > 0)
         AMS_LAUNCH("pool_bwd_sample", st, pool_bwd_sample<MODE, DM><<<(B + kWaves - 1) / kWaves, kThreads, 0, st>>>(
-            B, D, seg_off, inv, E, U, (const float *)saved, dU, samp, cvec, da));
+            B, D, seg_off, inv, cap, E, U, (const float *)saved, dU, samp, cvec, da));
     const int g = (p.nch + kWaves - 1) / kWaves;
-    AMS_LAUNCH("pool_bwd_seg", st, pool_bwd_seg<MODE, DM><<<g, kThreads, 0, st>>>(D, n_beh, n_occ, inv, occ_perm, uniq_off, E, A, saved, dU,
+    AMS_LAUNCH("pool_bwd_seg", st, pool_bwd_seg<MODE, DM><<<g, kThreads, 0, st>>>(D, n_beh, n_occ, cap, inv, occ_perm, uniq_off, E, A, saved, dU,
                                                    dA, samp, cvec, da, p.nch, dE, head, tail, cross, accumulate,
                                                    seg_off, Lc));
     AMS_LAUNCH("pool_bwd_fix", st, pool_bwd_fix<DM><<<g, kThreads, 0, st>>>(D, p.nch, uniq_off, cross, head, tail, dE,
@@ -536,11 +557,12 @@ ams_status check_common(int32_t mode, int32_t B, int32_t D, int64_t n_beh)
 }  // namespace
 
 extern "C" ams_status ams_pool_fwd(int32_t mode, int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
-                                   const int32_t *inv, const float *E, float *U, float *A, void *saved,
-                                   void *stream)
+                                   const int32_t *inv, int32_t n_uniq_cap, const float *E, float *U, float *A,
+                                   void *saved, void *stream)
 {
     ams_status s = check_common(mode, B, D, n_beh);
     if (s != AMS_OK) return s;
+    if (n_uniq_cap < 0) return AMS_ERR_SIZE;
     if (B == 0) return AMS_OK;
     if (!seg_off || !inv || !E || !U || !A) return AMS_ERR_NULL;
     if (mode != AMS_POOL_SUM && !saved) return AMS_ERR_NULL;
@@ -548,9 +570,9 @@ extern "C" ams_status ams_pool_fwd(int32_t mode, int32_t B, int32_t D, const int
     with_dm(D, [&](auto dm) {
         constexpr int DM = decltype(dm)::value;
         switch (mode) {
-        case AMS_POOL_SUM: launch_fwd<AMS_POOL_SUM, DM>(B, D, seg_off, n_beh, inv, E, U, A, saved, st); break;
-        case AMS_POOL_MAX: launch_fwd<AMS_POOL_MAX, DM>(B, D, seg_off, n_beh, inv, E, U, A, saved, st); break;
-        default: launch_fwd<AMS_POOL_ATT, DM>(B, D, seg_off, n_beh, inv, E, U, A, saved, st);
+        case AMS_POOL_SUM: launch_fwd<AMS_POOL_SUM, DM>(B, D, seg_off, n_beh, inv, n_uniq_cap, E, U, A, saved, st); break;
+        case AMS_POOL_MAX: launch_fwd<AMS_POOL_MAX, DM>(B, D, seg_off, n_beh, inv, n_uniq_cap, E, U, A, saved, st); break;
+        default: launch_fwd<AMS_POOL_ATT, DM>(B, D, seg_off, n_beh, inv, n_uniq_cap, E, U, A, saved, st);
         }
     });
     return ams_launch_status();
@@ -586,15 +608,15 @@ extern "C" ams_status ams_pool_bwd(int32_t mode, int32_t B, int32_t D, const int
         constexpr int DM = decltype(dm)::value;
         switch (mode) {
         case AMS_POOL_SUM:
-            launch_bwd<AMS_POOL_SUM, DM>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, A, saved, dU, dA, dE,
+            launch_bwd<AMS_POOL_SUM, DM>(B, D, seg_off, n_beh, inv, n_uniq_cap, occ_perm, uniq_off, E, U, A, saved, dU, dA, dE,
                                          w, p, st);
             break;
         case AMS_POOL_MAX:
-            launch_bwd<AMS_POOL_MAX, DM>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, A, saved, dU, dA, dE,
+            launch_bwd<AMS_POOL_MAX, DM>(B, D, seg_off, n_beh, inv, n_uniq_cap, occ_perm, uniq_off, E, U, A, saved, dU, dA, dE,
                                          w, p, st);
             break;
         default:
-            launch_bwd<AMS_POOL_ATT, DM>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, A, saved, dU, dA, dE,
+            launch_bwd<AMS_POOL_ATT, DM>(B, D, seg_off, n_beh, inv, n_uniq_cap, occ_perm, uniq_off, E, U, A, saved, dU, dA, dE,
                                          w, p, st);
         }
     });
@@ -602,16 +624,17 @@ extern "C" ams_status ams_pool_bwd(int32_t mode, int32_t B, int32_t D, const int
 }
 
 extern "C" ams_status ams_pool_query_fwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
-                                         const int32_t *inv, const float *E, const float *Q, float *U, float *w,
-                                         void *stream)
+                                         const int32_t *inv, int32_t n_uniq_cap, const float *E, const float *Q,
+                                         float *U, float *w, void *stream)
 {
     ams_status s = check_common(AMS_POOL_ATT, B, D, n_beh);
     if (s != AMS_OK) return s;
+    if (n_uniq_cap < 0) return AMS_ERR_SIZE;
     if (B == 0) return AMS_OK;
     if (!seg_off || !inv || !E || !Q || !U || !w) return AMS_ERR_NULL;
     hipStream_t st = (hipStream_t)stream;
     with_dm(D, [&](auto dm) {
-        launch_fwd<kPoolQuery, decltype(dm)::value>(B, D, seg_off, n_beh, inv, E, U, nullptr, w, st, Q);
+        launch_fwd<kPoolQuery, decltype(dm)::value>(B, D, seg_off, n_beh, inv, n_uniq_cap, E, U, nullptr, w, st, Q);
     });
     return ams_launch_status();
 }
@@ -635,18 +658,19 @@ extern "C" ams_status ams_pool_query_bwd(int32_t B, int32_t D, const int32_t *se
     hipStream_t st = (hipStream_t)stream;
     char *wsc = (char *)ws;
     with_dm(D, [&](auto dm) {
-        launch_bwd<kPoolQuery, decltype(dm)::value>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, E, U, Q, w, dU,
+        launch_bwd<kPoolQuery, decltype(dm)::value>(B, D, seg_off, n_beh, inv, n_uniq_cap, occ_perm, uniq_off, E, U, Q, w, dU,
                                                     nullptr, dE, wsc, p, st, dQ, accumulate != 0);
     });
     return ams_launch_status();
 }
 
 extern "C" ams_status ams_pool_concat_fwd(int32_t B, int32_t D, int32_t Lc, const int32_t *seg_off, int64_t n_beh,
-                                          const int32_t *inv, const float *E, float *U, float *A, void *stream)
+                                          const int32_t *inv, int32_t n_uniq_cap, const float *E, float *U, float *A,
+                                          void *stream)
 {
     ams_status s = check_common(AMS_POOL_SUM, B, D, n_beh);
     if (s != AMS_OK) return s;
-    if (Lc < 1 || (int64_t)Lc * D > INT32_MAX) return AMS_ERR_SIZE;
+    if (n_uniq_cap < 0 || Lc < 1 || (int64_t)Lc * D > INT32_MAX) return AMS_ERR_SIZE;
     if (B == 0) return AMS_OK;
     if (!seg_off || !inv || !E || !U || !A) return AMS_ERR_NULL;
     hipStream_t st = (hipStream_t)stream;
@@ -654,7 +678,7 @@ extern "C" ams_status ams_pool_concat_fwd(int32_t B, int32_t D, int32_t Lc, cons
     int64_t g = (n + kThreads - 1) / kThreads;
     if (g > 8192) g = 8192;
     AMS_LAUNCH("pool_concat_fwd", st, pool_concat_fwd_k<<<(unsigned)g, kThreads, 0, st>>>(B, D, Lc, seg_off, n_beh, inv,
-                                                                                          E, U, A));
+                                                                                          n_uniq_cap, E, U, A));
     return ams_launch_status();
 }
 
@@ -676,7 +700,7 @@ extern "C" ams_status ams_pool_concat_bwd(int32_t B, int32_t D, int32_t Lc, cons
     hipStream_t st = (hipStream_t)stream;
     char *w = (char *)ws;
     with_dm(D, [&](auto dm) {
-        launch_bwd<kPoolConcat, decltype(dm)::value>(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, nullptr, nullptr,
+        launch_bwd<kPoolConcat, decltype(dm)::value>(B, D, seg_off, n_beh, inv, n_uniq_cap, occ_perm, uniq_off, nullptr, nullptr,
                                                      nullptr, nullptr, dU, dA, dE, w, p, st, nullptr, 0, Lc);
     });
     return ams_launch_status();

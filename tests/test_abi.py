@@ -45,7 +45,8 @@ def test_every_declared_symbol_is_exported(lib):
 
 def test_status_strings(lib):
     for s in range(9):
-        assert lib.ams_status_str(s).decode()
+        assert lib.ams_status_str(s).decode() != "unknown status"
+    assert lib.ams_status_str(9).decode() == "unknown status"
     assert b"gfx950" in lib.ams_build_info()
 
 
@@ -129,7 +130,7 @@ def test_embed_host_errors(lib):
 
 
 def test_pool_host_errors(lib):
-    f = [2, 4, 12, FAKE, 40, FAKE, FAKE, FAKE, FAKE, FAKE, None]
+    f = [2, 4, 12, FAKE, 40, FAKE, 44, FAKE, FAKE, FAKE, FAKE, None]
     a = list(f); a[0] = 3
     assert lib.ams_pool_fwd(*a) == MODE
     a = list(f); a[2] = 0
@@ -138,7 +139,9 @@ def test_pool_host_errors(lib):
     assert lib.ams_pool_fwd(*a) == SIZE
     a = list(f); a[1] = -1
     assert lib.ams_pool_fwd(*a) == SIZE
-    a = list(f); a[9] = None                  # attention needs its weights buffer
+    a = list(f); a[6] = -1                    # capacity (rows of E)
+    assert lib.ams_pool_fwd(*a) == SIZE
+    a = list(f); a[10] = None                 # attention needs its weights buffer
     assert lib.ams_pool_fwd(*a) == NULL
     a = list(f); a[1] = 0                     # empty batch: nothing to do
     assert lib.ams_pool_fwd(*a) == OK
@@ -210,9 +213,11 @@ def test_joint_host_errors(lib):
 
 
 def test_query_pool_host_errors(lib):
-    f = [4, 12, FAKE, 40, FAKE, FAKE, None, FAKE, FAKE, None]
+    f = [4, 12, FAKE, 40, FAKE, 44, FAKE, None, FAKE, FAKE, None]
     assert lib.ams_pool_query_fwd(*f) == NULL                # Q
     a = list(f); a[1] = 33
+    assert lib.ams_pool_query_fwd(*a) == SIZE
+    a = list(f); a[5] = -1
     assert lib.ams_pool_query_fwd(*a) == SIZE
     a = list(f); a[0] = 0
     assert lib.ams_pool_query_fwd(*a) == OK
@@ -232,8 +237,10 @@ def test_adam_host_errors(lib):
 
 
 def test_concat_pool_host_errors(lib):
-    f = [4, 12, 5, FAKE, 40, FAKE, FAKE, FAKE, None, None]
+    f = [4, 12, 5, FAKE, 40, FAKE, 44, FAKE, FAKE, None, None]
     assert lib.ams_pool_concat_fwd(*f) == NULL                # A
+    a = list(f); a[6] = -1
+    assert lib.ams_pool_concat_fwd(*a) == SIZE
     a = list(f); a[2] = 0
     assert lib.ams_pool_concat_fwd(*a) == SIZE                # Lc
     a = list(f); a[1] = 33
@@ -271,3 +278,9 @@ def test_dssm_host_errors(lib):
     assert lib.ams_dssm_fwd_bwd(*a) == NULL
     a = list(args); a[21] = None                                    # dWa
     assert lib.ams_dssm_fwd_bwd(*a) == NULL
+
+
+def test_step_rejects_an_unchecked_capacity_below_the_occurrences():
+    # the check runs before any buffer is allocated
+    with pytest.raises(ValueError, match="cap_checked"):
+        ams.Step((256, 64, 16), "f32", "sum", 4, 10, device="cpu", cap=13)

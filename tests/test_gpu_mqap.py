@@ -58,21 +58,23 @@ def test_two_channel_pooling_matches_oracle(name):
     assert_close(U2, f2["U"], F32, "U (ID channel)", rows=True)
     assert_close(w2[:n_beh], f2["w"], F32, "w (ID channel)")
     cap = n_u + 33
+    E_cap = torch.zeros((cap, D), device="cuda")        # E and dE hold `cap` rows
+    E_cap[:n_u] = E_d
     ws = torch.empty(max(ams.ams_pool_workspace("att", B, n_beh, D, cap), 256), dtype=torch.uint8, device="cuda")
     dE = torch.full((cap, D), 7.0, device="cuda")
     dQ = torch.full((B, D), 7.0, device="cuda")
     # backward on the oracle's forward values (identical inputs for both sides)
     U1o, A1o, w1o = cuda(f1["U"].astype(np.float32)), cuda(f1["A"].astype(np.float32)), cuda(f1["w"].astype(np.float32))
     U2o, w2o = cuda(f2["U"].astype(np.float32)), cuda(f2["w"].astype(np.float32))
-    ams.ams_pool_query_bwd(seg_d, n_beh, inv_d, perm_d, off_d, nu_d, cap, E_d, Q_d, U2o, w2o, cuda(g2), dQ, dE,
+    ams.ams_pool_query_bwd(seg_d, n_beh, inv_d, perm_d, off_d, nu_d, cap, E_cap, Q_d, U2o, w2o, cuda(g2), dQ, dE,
                            False, ws)
     torch.cuda.synchronize()
     assert_close(dE[:n_u], b2["dE"], F32, "dE (ID channel alone)", rows=True)
     assert_close(dQ, b2["dQ"], F32, "dQ", rows=True)
     # both channels into one dE: image channel first, then the ID channel accumulated
-    ams.ams_pool_bwd("att", seg_d, n_beh, inv_d, perm_d, off_d, nu_d, cap, E_d, U1o, A1o, w1o, cuda(g1), cuda(gA),
+    ams.ams_pool_bwd("att", seg_d, n_beh, inv_d, perm_d, off_d, nu_d, cap, E_cap, U1o, A1o, w1o, cuda(g1), cuda(gA),
                      dE, ws)
-    ams.ams_pool_query_bwd(seg_d, n_beh, inv_d, perm_d, off_d, nu_d, cap, E_d, Q_d, U2o, w2o, cuda(g2), dQ, dE,
+    ams.ams_pool_query_bwd(seg_d, n_beh, inv_d, perm_d, off_d, nu_d, cap, E_cap, Q_d, U2o, w2o, cuda(g2), dQ, dE,
                            True, ws)
     torch.cuda.synchronize()
     assert_close(dE[:n_u], b1["dE"] + b2["dE"], F32, "dE (both channels)", rows=True)
