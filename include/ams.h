@@ -91,7 +91,8 @@ typedef enum {
     AMS_ERR_WORKSPACE = 5,  /* ws_bytes below the matching *_workspace() size */
     AMS_ERR_HIP = 6,        /* a HIP launch or runtime call failed */
     AMS_ERR_ID_RANGE = 7,   /* (device) an image ID is outside [0, n_ids) */
-    AMS_ERR_MODE = 8        /* unknown pooling mode */
+    AMS_ERR_MODE = 8,       /* unknown pooling mode */
+    AMS_ERR_CAPACITY = 9    /* beyond the fixed scratch of ams_dedup_noalloc */
 } ams_status;
 
 typedef enum { AMS_F32 = 0, AMS_BF16 = 1, AMS_F32_X3 = 2 } ams_dtype;
@@ -163,6 +164,29 @@ ams_status ams_dedup(const int32_t *ids, int64_t n_occ, int32_t n_ids,
                      int32_t *uniq, int32_t *inv, int32_t *occ_perm,
                      int32_t *uniq_off, int32_t *n_uniq, int32_t *dev_status,
                      void *ws, size_t ws_bytes, void *stream);
+
+/* ------------------------------------------- dedup without allocation ----
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): ams_dedup
+ * with the workspace replaced by a fixed scratch array that the library's
+ * code object holds on every GPU it runs on (about 19 MB each, kept until
+ * the process ends).  Arguments, outputs, determinism and device status as
+ * ams_dedup; the outputs are bit-identical to ams_dedup's.  The call itself
+ * allocates nothing (no hipMalloc, no allocating library routine); its first
+ * call on a device looks up that device's scratch address once.
+ *   n_occ <= AMS_DEDUP_NOALLOC_MAX_OCC (2^20), else AMS_ERR_CAPACITY before
+ *   anything is enqueued; any n_ids >= 1 (IDs of up to 31 bits).
+ * Every call on one GPU shares that GPU's scratch: calls that overlap on one
+ * GPU (different streams without ordering, or several host threads) race
+ * and give unspecified results.  Calls ordered on one stream are safe; each
+ * call clears the parts of the scratch that must start at zero itself.
+ * Host errors: SIZE, CAPACITY, NULL; AMS_ERR_HIP if the scratch address
+ * cannot be found or a launch fails. */
+#define AMS_DEDUP_NOALLOC_MAX_OCC (1 << 20)
+ams_status ams_dedup_noalloc(const int32_t *ids, int64_t n_occ, int32_t n_ids,
+                             int32_t *uniq, int32_t *inv, int32_t *occ_perm,
+                             int32_t *uniq_off, int32_t *n_uniq, int32_t *dev_status,
+                             void *stream);
 
 /* --------------------------------------------------------- embed fwd ----
  * SERVEREMBED (Algorithm 1): e = E(I) for every unique image.

@@ -19,8 +19,10 @@ AMS_F32, AMS_BF16, AMS_F32_X3 = 0, 1, 2
 AMS_POOL_SUM, AMS_POOL_MAX, AMS_POOL_ATT = 0, 1, 2
 POOL = {"sum": AMS_POOL_SUM, "max": AMS_POOL_MAX, "att": AMS_POOL_ATT}
 STATUS = {0: "AMS_OK", 1: "AMS_ERR_NULL", 2: "AMS_ERR_SIZE", 3: "AMS_ERR_DTYPE", 4: "AMS_ERR_DIMS",
-          5: "AMS_ERR_WORKSPACE", 6: "AMS_ERR_HIP", 7: "AMS_ERR_ID_RANGE", 8: "AMS_ERR_MODE"}
-EXPORTS = ["ams_status_str", "ams_build_info", "ams_dedup_workspace", "ams_dedup",
+          5: "AMS_ERR_WORKSPACE", 6: "AMS_ERR_HIP", 7: "AMS_ERR_ID_RANGE", 8: "AMS_ERR_MODE",
+          9: "AMS_ERR_CAPACITY"}
+DEDUP_NOALLOC_MAX_OCC = 1 << 20     # AMS_DEDUP_NOALLOC_MAX_OCC
+EXPORTS = ["ams_status_str", "ams_build_info", "ams_dedup_workspace", "ams_dedup", "ams_dedup_noalloc",
            "ams_embed_workspace", "ams_embed_fwd", "ams_embed_bwd", "ams_pool_fwd",
            "ams_pool_workspace", "ams_pool_bwd", "ams_timing_enable", "ams_timing_read",
            "ams_bag_fwd", "ams_bag_workspace", "ams_bag_bwd", "ams_ctr_workspace", "ams_ctr_fwd_bwd",
@@ -69,6 +71,8 @@ def load() -> ctypes.CDLL:
     lib.ams_dedup_workspace.argtypes = [i64, i32]
     lib.ams_dedup.restype = ctypes.c_int
     lib.ams_dedup.argtypes = [P, i64, i32, P, P, P, P, P, P, P, sz, P]
+    lib.ams_dedup_noalloc.restype = ctypes.c_int
+    lib.ams_dedup_noalloc.argtypes = [P, i64, i32, P, P, P, P, P, P, P]
     lib.ams_embed_workspace.restype = sz
     lib.ams_embed_workspace.argtypes = [M, i32]
     lib.ams_embed_fwd.restype = ctypes.c_int
@@ -176,6 +180,13 @@ def ams_dedup(ids, n_ids, uniq, inv, occ_perm, uniq_off, n_uniq, dev_status, ws,
                             _p(uniq_off), _p(n_uniq), _p(dev_status), _p(ws),
                             ws.numel() * ws.element_size() if ws is not None else 0,
                             _stream(stream)), "ams_dedup")
+
+
+def ams_dedup_noalloc(ids, n_ids, uniq, inv, occ_perm, uniq_off, n_uniq, dev_status, stream=None):
+    """ams_dedup on the library's fixed per-device scratch (no workspace, no
+    allocation); at most DEDUP_NOALLOC_MAX_OCC occurrences."""
+    _check(load().ams_dedup_noalloc(_p(ids), ids.numel(), int(n_ids), _p(uniq), _p(inv), _p(occ_perm),
+                                    _p(uniq_off), _p(n_uniq), _p(dev_status), _stream(stream)), "ams_dedup_noalloc")
 
 
 def ams_embed_workspace(mlp: ams_mlp, n_uniq_cap: int) -> int:

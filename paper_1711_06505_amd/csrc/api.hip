@@ -19,6 +19,7 @@ extern "C" const char *ams_status_str(ams_status s)
     case AMS_ERR_HIP: return "HIP launch or runtime error";
     case AMS_ERR_ID_RANGE: return "image ID out of range";
     case AMS_ERR_MODE: return "unknown pooling mode";
+    case AMS_ERR_CAPACITY: return "size beyond the fixed scratch of the no-allocation call";
     }
     return "unknown status";
 }

@@ -23,6 +23,9 @@
 // publish, and blocks are dispatched in index order, so every wait ends.
 #include "ams_device.h"
 
+#include <climits>
+#include <mutex>
+
 namespace {
 
 constexpr int kThreads = 256;                 // 4 waves
@@ -468,6 +471,35 @@ ams_status dedup_enqueue(const int32_t *ids, int n, int32_t n_ids, int32_t *uniq
     return ams_launch_status();
 }
 
+// ------------------------------------------------ no-allocation variant ----
+// Scratch of ams_dedup_noalloc: the workspace of the largest batch it takes
+// (kNoAllocMaxOcc occurrences, IDs of up to 31 bits: four radix passes),
+// 19.0 MB in every GPU's copy of the library's code object.  Host code never
+// passes `scratch` itself to a kernel (on the host it names a stand-in, not
+// device memory): the device address comes from hipGetSymbolAddress, looked
+// up once per device with that device current.
+constexpr int64_t kNoAllocMaxOcc = AMS_DEDUP_NOALLOC_MAX_OCC;
+constexpr size_t kScratchBytes = layout(kNoAllocMaxOcc, INT32_MAX).total;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void *g_scratch_ptr[kMaxDevices];
+
+// Device address of this device's scratch (nullptr on failure).
+void *scratch_on_current_device()
+{
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void *ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+        g_scratch_ptr[dev] = ptr;
+    }
+    return g_scratch_ptr[dev];
+}
+
 }  // namespace
 
 extern "C" size_t ams_dedup_workspace(int64_t n_occ, int32_t n_ids)
@@ -487,5 +519,21 @@ extern "C" ams_status ams_dedup(const int32_t *ids, int64_t n_occ, int32_t n_ids
     const Layout L = layout(n_occ, n_ids);
     if (n_occ > 0 && ws_bytes < L.total) return AMS_ERR_WORKSPACE;
     return dedup_enqueue(ids, (int)n_occ, n_ids, uniq, inv, occ_perm, uniq_off, n_uniq, dev_status, (char *)ws, L,
+                         (hipStream_t)stream);
+}
+
+extern "C" ams_status ams_dedup_noalloc(const int32_t *ids, int64_t n_occ, int32_t n_ids, int32_t *uniq,
+                                        int32_t *inv, int32_t *occ_perm, int32_t *uniq_off,
+                                        int32_t *n_uniq, int32_t *dev_status, void *stream)
+{
+    if (n_occ < 0 || n_ids < 1) return AMS_ERR_SIZE;
+    if (n_occ > kNoAllocMaxOcc) return AMS_ERR_CAPACITY;
+    if (!uniq_off || !n_uniq || !dev_status) return AMS_ERR_NULL;
+    if (n_occ > 0 && (!ids || !uniq || !inv || !occ_perm)) return AMS_ERR_NULL;
+    const Layout L = layout(n_occ, n_ids);
+    if (L.total > kScratchBytes) return AMS_ERR_CAPACITY;
+    char *w = (char *)scratch_on_current_device();
+    if (!w) return AMS_ERR_HIP;
+    return dedup_enqueue(ids, (int)n_occ, n_ids, uniq, inv, occ_perm, uniq_off, n_uniq, dev_status, w, L,
                          (hipStream_t)stream);
 }

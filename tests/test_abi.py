@@ -13,7 +13,7 @@ from paper_1711_06505_amd import ams
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "ams.h")
 
-OK, NULL, SIZE, DTYPE, DIMS, WS, HIP, IDR, MODE = range(9)
+OK, NULL, SIZE, DTYPE, DIMS, WS, HIP, IDR, MODE, CAPACITY = range(10)
 FAKE = ctypes.c_void_p(0x1000)      # never dereferenced: validation fails first
 
 
@@ -44,9 +44,9 @@ def test_every_declared_symbol_is_exported(lib):
 
 
 def test_status_strings(lib):
-    for s in range(9):
+    for s in range(10):
         assert lib.ams_status_str(s).decode() != "unknown status"
-    assert lib.ams_status_str(9).decode() == "unknown status"
+    assert lib.ams_status_str(10).decode() == "unknown status"
     assert b"gfx950" in lib.ams_build_info()
 
 
@@ -79,6 +79,23 @@ def test_dedup_host_errors(lib):
     assert lib.ams_dedup(*a) == NULL
     a = list(args); a[10] = 16
     assert lib.ams_dedup(*a) == WS
+
+
+def test_dedup_noalloc_host_errors(lib):
+    # every check here returns before the scratch is looked up or anything enqueued
+    args = [FAKE, 100, 10, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None]
+    a = list(args); a[1] = -1
+    assert lib.ams_dedup_noalloc(*a) == SIZE
+    a = list(args); a[2] = 0
+    assert lib.ams_dedup_noalloc(*a) == SIZE
+    a = list(args); a[1] = ams.DEDUP_NOALLOC_MAX_OCC + 1
+    assert lib.ams_dedup_noalloc(*a) == CAPACITY
+    a = list(args); a[0] = None
+    assert lib.ams_dedup_noalloc(*a) == NULL
+    a = list(args); a[8] = None               # dev_status
+    assert lib.ams_dedup_noalloc(*a) == NULL
+    hdr = open(HEADER).read()
+    assert f"#define AMS_DEDUP_NOALLOC_MAX_OCC (1 << {ams.DEDUP_NOALLOC_MAX_OCC.bit_length() - 1})" in hdr
 
 
 def _embed_args(m, slope=None):
