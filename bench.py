@@ -59,8 +59,8 @@ def flops_per_unique(dims):
 
 # Algorithmic work of the layer-1 GEMM kernels per unique image: 2*F*H flops
 # and one read of the image's F-wide feature row.
-GEMM_KERNELS = ("l1sk_f32", "l1sk_bf16", "l1sk_x3", "l1_fwd_f32", "l1_fwd_bf16", "dw1_part_f32", "dw1_part_bf16",
-                "dw1_part")
+GEMM_KERNELS = ("l1sk_f32", "l1sk_bf16", "l1rs_bf16", "l1sk_x3", "l1_fwd_f32", "l1_fwd_bf16", "dw1_part_f32",
+                "dw1_part_bf16", "dw1_part")
 
 
 def gemm_work_per_unique(dims, esz):
@@ -127,6 +127,74 @@ def cpu_baseline(w, batch, mode, min_runs=3, min_seconds=10.0, max_runs=30):
                       f"CPU: {cpu_model()}"}
 
 
+def bench_peaks(args):
+    """Achievable rates of this part: HBM copy and read, gathers of the
+    2M-image step's unique rows (8 KB bf16 rows) in the first-layer kernels'
+    visit orders, and MFMA loops on operands read from memory.  Each probe is
+    timed with events on the stream it is launched on, median of 5 runs."""
+    import numpy as np
+    import torch
+
+    from oracle import oracle
+    from paper_1711_06505_amd import ams, synth
+
+    st = torch.cuda.current_stream()
+
+    def timed(fn, reps=5):
+        fn()
+        out = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record(st)
+            fn()
+            b.record(st)
+            b.synchronize()
+            out.append(a.elapsed_time(b) * 1e-3)
+        return sorted(out)[len(out) // 2]
+
+    res = {"metric": "achievable peaks", "peak_hbm_bytes_per_s": PEAK_HBM, "peak_mfma_flops": PEAK_MFMA}
+    sink = torch.empty(4096 * 256, dtype=torch.int32, device="cuda")
+    nb = 1 << 30
+    src = torch.empty(nb // 4, dtype=torch.int32, device="cuda").fill_(7)
+    dst = torch.empty_like(src)
+    for blocks in (1024, 4096):
+        t = timed(lambda: ams.ams_peak_copy(src, dst, blocks))
+        res[f"copy_1GiB_blocks{blocks}"] = {"bytes_per_s": 2 * nb / t, "seconds": t}
+        t = timed(lambda: ams.ams_peak_read(src, blocks, sink))
+        res[f"read_1GiB_blocks{blocks}"] = {"bytes_per_s": nb / t, "seconds": t}
+    del src, dst
+    # the unique rows of the 4096-sample long-behavior batch, table of 2M x 4096 bf16
+    w = synth.get("c3_long")
+    batch = synth.make_batch(w)
+    uniq = oracle.dedup(synth.occurrences(batch), w.n_images)["uniq"]
+    rows = torch.from_numpy(np.ascontiguousarray(uniq, dtype=np.int32)).cuda()
+    T = torch.empty((w.n_images, w.in_dim), dtype=torch.bfloat16, device="cuda")
+    T.view(torch.int16).random_(-32768, 32767)
+    row_bytes = w.in_dim * 2
+    gather = {}
+    variants = [(128, 128, 256), (256, 128, 256), (128, 1024, 256), (32, row_bytes, 256)]
+    variants += [(tile, chunk, blocks) for blocks in (1024, 2048) for tile, chunk in
+                 ((128, 128), (128, 256), (128, 512), (64, 1024), (32, 2048), (16, row_bytes))]
+    variants += [(8, row_bytes, 4096)]
+    for tile, chunk, blocks in variants:
+        t = timed(lambda: ams.ams_peak_gather(T, rows, tile, chunk, blocks, sink))
+        gather[f"tile{tile}_chunk{chunk}_blocks{blocks}"] = {"bytes_per_s": rows.numel() * row_bytes / t,
+                                                             "seconds": t}
+    res["gather_c3_unique_rows"] = {"rows": int(rows.numel()), "row_bytes": row_bytes, "variants": gather}
+    del T
+    out = torch.empty(4096 * 256, device="cuda")
+    for dt, flops in (("bf16", 32768), ("f32", 4096)):
+        # random operands (the MFMA rate depends on the data through the clock)
+        ops_d = (torch.randn(524288 // 2, device="cuda").to(torch.bfloat16) if dt == "bf16"
+                 else torch.randn(524288 // 4, device="cuda"))
+        blocks, iters = 1024, (2000 if dt == "bf16" else 250)
+        t = timed(lambda: ams.ams_peak_mfma(dt, ops_d, iters, blocks, out))
+        total = blocks * 4 * iters * 16 * flops
+        res[f"mfma_{dt}_random_operands"] = {"flops_per_s": total / t, "seconds": t,
+                                             "frac_of_peak": total / t / PEAK_MFMA[dt]}
+    print(json.dumps(res))
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -142,6 +210,9 @@ def main():
     ap.add_argument("--ops", action="store_true",
                     help="instead of the step, time the widened operations one by one at their real shapes "
                          "(one JSON line each)")
+    ap.add_argument("--peaks", action="store_true",
+                    help="instead of the step, time the achievable-peak probes (HBM copy and read, gathers of "
+                         "the long-behavior step's unique rows by visit order, MFMA loops) and print one JSON line")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="instead of the step, run a plain device copy of this many MiB "
                          "(calibrates the FETCH_SIZE / WRITE_SIZE counters)")
@@ -171,6 +242,11 @@ def main():
         torch.cuda.set_device(0)
         ams.load()
         return bench_ops(args)
+
+    if args.peaks:
+        torch.cuda.set_device(0)
+        ams.load()
+        return bench_peaks(args)
 
     w = synth.get(args.workload)
     if args.dtype and args.dtype != w.dtype:

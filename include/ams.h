@@ -491,6 +491,37 @@ ams_status ams_adam_update(int64_t n, float *param, const float *grad, float *m,
                            float lr, float b1, float b2, float eps, int64_t t,
                            uint16_t *param_bf16, void *stream);
 
+/* ============================================================= probes ====
+ * Achievable-peak probes of the device (they compute nothing of the method):
+ * the rates the part delivers for plain HBM streams, for gathering table
+ * rows in the order the first-layer kernels visit them, and for MFMA on
+ * operands read from memory, to stand beside the kernels' rates and the
+ * vendor peaks.  Every pointer is a device pointer; `blocks` workgroups of
+ * 256 threads.  Host errors: SIZE, NULL (DTYPE for ams_peak_mfma).
+ *
+ * ams_peak_copy    dst = src, `bytes` (a multiple of 16), grid-stride.
+ * ams_peak_read    reads `bytes` of src; out[blocks * 256] receives one xor
+ *                  per thread.
+ * ams_peak_gather  reads rows[0..n) of the table T [n_table x row_bytes]:
+ *                  each block a contiguous range of the list, in tiles of
+ *                  `tile` rows, each tile in stages of `chunk` bytes per row
+ *                  (row_bytes a multiple of chunk, chunk a multiple of 16;
+ *                  chunk == row_bytes reads each row whole); a row index
+ *                  outside [0, n_table) reads row 0; out[blocks * 256] as
+ *                  ams_peak_read.
+ * ams_peak_mfma    dtype AMS_BF16 (v_mfma_f32_32x32x16_bf16, 32768 flops) or
+ *                  AMS_F32 (v_mfma_f32_32x32x2_f32, 4096 flops): every wave
+ *                  runs iters x 16 independent products on operands read from
+ *                  ops (524288 bytes); out[blocks * 256] one float per
+ *                  thread. */
+ams_status ams_peak_copy(const void *src, void *dst, int64_t bytes, int32_t blocks, void *stream);
+ams_status ams_peak_read(const void *src, int64_t bytes, int32_t blocks, uint32_t *out, void *stream);
+ams_status ams_peak_gather(const void *T, int64_t n_table, int32_t row_bytes, const int32_t *rows,
+                           int32_t n, int32_t tile, int32_t chunk, int32_t blocks, uint32_t *out,
+                           void *stream);
+ams_status ams_peak_mfma(int32_t dtype, const void *ops, int32_t iters, int32_t blocks, float *out,
+                         void *stream);
+
 #ifdef __cplusplus
 }
 #endif

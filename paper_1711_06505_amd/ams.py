@@ -28,7 +28,7 @@ EXPORTS = ["ams_status_str", "ams_build_info", "ams_dedup_workspace", "ams_dedup
            "ams_bag_fwd", "ams_bag_workspace", "ams_bag_bwd", "ams_ctr_workspace", "ams_ctr_fwd_bwd",
            "ams_adagrad_rows", "ams_pool_query_fwd", "ams_pool_query_bwd",
            "ams_adam_update", "ams_pool_concat_fwd", "ams_pool_concat_bwd", "ams_dssm_workspace",
-           "ams_dssm_fwd_bwd"]
+           "ams_dssm_fwd_bwd", "ams_peak_copy", "ams_peak_read", "ams_peak_gather", "ams_peak_mfma"]
 
 
 class AmsError(RuntimeError):
@@ -116,6 +116,11 @@ def load() -> ctypes.CDLL:
     f = ctypes.c_float
     lib.ams_adam_update.restype = ctypes.c_int
     lib.ams_adam_update.argtypes = [i64, P, P, P, P, f, f, f, f, i64, P, P]
+    for name, args in (("ams_peak_copy", [P, P, i64, i32, P]), ("ams_peak_read", [P, i64, i32, P, P]),
+                       ("ams_peak_gather", [P, i64, i32, P, i32, i32, i32, i32, P, P]),
+                       ("ams_peak_mfma", [i32, P, i32, i32, P, P])):
+        getattr(lib, name).restype = ctypes.c_int
+        getattr(lib, name).argtypes = args
     lib.ams_timing_enable.restype = ctypes.c_int
     lib.ams_timing_enable.argtypes = [ctypes.c_int]
     lib.ams_timing_read.restype = ctypes.c_int
@@ -372,6 +377,30 @@ def ams_adagrad_rows(uniq, n_uniq, n_uniq_cap: int, grad, table, accum, lr: floa
     _check(load().ams_adagrad_rows(table.shape[1], _p(uniq), _p(n_uniq), int(n_uniq_cap), _p(grad), _p(table),
                                    table.shape[0], _p(accum), float(lr), float(eps), _stream(stream)),
            "ams_adagrad_rows")
+
+
+# ---------------------------------------------------------------- probes
+
+def ams_peak_copy(src, dst, blocks: int, stream=None):
+    _check(load().ams_peak_copy(_p(src), _p(dst), src.numel() * src.element_size(), int(blocks), _stream(stream)),
+           "ams_peak_copy")
+
+
+def ams_peak_read(src, blocks: int, out, stream=None):
+    _check(load().ams_peak_read(_p(src), src.numel() * src.element_size(), int(blocks), _p(out), _stream(stream)),
+           "ams_peak_read")
+
+
+def ams_peak_gather(T, rows, tile: int, chunk: int, blocks: int, out, stream=None):
+    _check(load().ams_peak_gather(_p(T), T.shape[0], T.shape[1] * T.element_size(), _p(rows), rows.numel(),
+                                  int(tile), int(chunk), int(blocks), _p(out), _stream(stream)), "ams_peak_gather")
+
+
+def ams_peak_mfma(dtype: str, ops, iters: int, blocks: int, out, stream=None):
+    if ops.numel() * ops.element_size() < 524288:
+        raise ValueError("ams_peak_mfma reads 524288 bytes of operands")
+    _check(load().ams_peak_mfma({"f32": AMS_F32, "bf16": AMS_BF16}[dtype], _p(ops), int(iters), int(blocks), _p(out),
+                                _stream(stream)), "ams_peak_mfma")
 
 
 class Step:

@@ -12,7 +12,7 @@ import sys
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "libams.so")
-SOURCES = ["dedup.hip", "embed.hip", "pool.hip", "ctr.hip", "api.hip"]
+SOURCES = ["dedup.hip", "embed.hip", "pool.hip", "ctr.hip", "peaks.hip", "api.hip"]
 ARCH = "gfx950"
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")

@@ -551,6 +551,259 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
     }
 }
 
+// ------------------------------------------------ bf16 layer 1, row split
+// Z1 = T[uniq] W1^T for bf16 storage (H = 256, F = 4096) on large batches:
+// each of G persistent blocks (one per CU) takes a contiguous range of the
+// unique rows with the whole K, so no tile is cut (no partial tiles for the
+// tail to add), and all blocks sweep K in step, so each XCD's L2 serves a W1
+// slice to its 32 CUs at about the same time.  A block is 8 waves (two per
+// SIMD) working in tiles of 256 rows: a wave computes its 32 rows against all
+// 256 units (eight 32x32 accumulator blocks, 128 registers); a wave with no
+// rows left in the block's range skips its products.
+//
+// The gathered feature rows, the dominant HBM stream, go straight into
+// registers: a 64-k stage is 128 contiguous bytes of a row, lane (r, h) of a
+// wave holding bytes 64h .. 64h + 63 of row r (k = 32h .. 32h + 31 of the
+// stage, four 16-byte MFMA operands), PA = 3 stages ahead: 96 KB of rows in
+// flight per CU, what the registers left beside the accumulators allow.  The
+// stage's W1 slice (256 rows x 128 bytes, an L2 hit after the first CU of an
+// XCD) moves into a 4-slot LDS ring by direct DMA PW = 3 stages ahead; B
+// operands are 16-byte LDS reads of the same k.  Vector memory completes in
+// issue order, so rows cannot usefully run further ahead than W1, whose ring
+// the LDS bounds.  Every vector memory instruction of the stages (4 row loads
+// and 4 W1 DMAs per wave and stage, in that order) comes from inline
+// assembly, so the compiler adds no waits of its own: stage s waits with
+// s_waitcnt vmcnt(16), which completes everything up to its own W1 DMA
+// (issued PW stages earlier, its rows PA stages earlier).  Stages past the
+// last load the last one again (into registers and a slot nobody reads), so
+// every stage issues the same count.  The stage sequence is unrolled for the
+// whole row, so no register such a load writes is carried around a loop
+// (where the register allocator could copy it before it has landed);
+// tests/test_l1rs_asm.py checks the generated code for that.
+namespace rs {
+constexpr int BN_ = 256;
+constexpr int kThreads = 512;
+constexpr int kWaves = kThreads / AMS_WAVE;
+constexpr int kWavesPerSimd = kWaves / 4;
+constexpr int BM = 32 * kWaves;              // rows per tile
+constexpr int WROWS = BN_ / kWaves;          // W1 slot rows a wave moves per stage
+constexpr int BN = BN_;                      // hidden units (the whole width)
+constexpr int KS = 64;                       // k per stage: 128 bytes of a row
+constexpr int kF = 4096;                     // feature width (the stages are unrolled for it)
+constexpr int S = kF / KS;                   // stages per tile
+constexpr int PA = 3;                        // stages of rows in flight
+constexpr int PW = 3;                        // stages of W1 in flight
+constexpr int NA = PA + 1;                   // row register sets
+constexpr int R = PW + 1;                    // W1 ring slots
+constexpr int SLOT = BN * KS * 2;            // bytes per slot (32 KB)
+constexpr int DMA_PER_WAVE = SLOT / 1024 / kWaves;   // 1 KB per DMA instruction
+constexpr int VM_PER_STAGE = 4 + DMA_PER_WAVE;
+constexpr int WAIT = (PW - 1) * VM_PER_STAGE;        // ops a stage may leave in flight
+constexpr uint32_t W1_Q = 8 * kF * 2;        // bytes between a wave's DMA row groups (8 W1 rows)
+static_assert(PA >= PW, "rows are issued at least as far ahead as W1");
+static_assert(R * SLOT <= 160 * 1024, "the ring fits the LDS");
+static_assert((size_t)BN * kF * 2 < (1ull << 32), "W1 offsets fit 32 bits");
+}  // namespace rs
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// 16-byte global load into registers at p + OFF, invisible to the
+// compiler's wait bookkeeping (the stages wait for it explicitly).
+template <int OFF>
+__device__ __forceinline__ void rs_load16(u32x4 &v, const char *p)
+{
+    asm volatile("global_load_dwordx4 %0, %1, off offset:%2" : "=v"(v) : "v"(p), "n"(OFF) : "memory");
+}
+
+// DMA of 64 lanes x 16 bytes from base + voff into LDS at lds_addr (+16 per
+// lane).
+__device__ __forceinline__ void rs_dma16(const void *base, uint32_t voff, uint32_t lds_addr)
+{
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+                 :
+                 : "s"(lds_addr), "v"(voff), "s"(base)
+                 : "memory", "m0");
+}
+
+// 16-byte chunk swizzle of the W1 slot rows (128 bytes each).  The LDS
+// serves a 16-byte read for 16 lanes per cycle over 64 banks, so rows r and
+// r + 1 sit in different bank halves and the even (odd) rows of 16
+// consecutive ones must use 8 distinct chunk positions: chunk ^ (row / 2 % 8).
+// It depends on row bits 1-3 only, so the four DMA row groups of a lane
+// (rows 8 apart) differ in bit 3 and get different swizzles.
+__device__ __forceinline__ int rs_swz(int row) { return (row >> 1) & 7; }
+
+struct RsLane {
+    const char *a;         // this lane's feature row at the next row stage to issue (+ 64 h), or a dummy
+    const void *w1;        // W1 (uniform)
+    uint32_t w;            // byte offset in W1 of this lane's first DMA row at the next W1 stage
+    uint32_t dq[rs::DMA_PER_WAVE];   // per DMA group q: its row (8 q further) and chunk, relative to w
+    uint32_t lds_wave;     // byte address of this wave's DMA rows in slot 0
+};
+
+// Stage t's issue: rows of stage t + PA (into register set (t + PA) % NA)
+// and W1 of stage t + PW (into slot (t + PW) % R), or of the last stage past
+// the end; the running pointers advance only over real stages, and the
+// empty asm keeps the compiler from precomputing every stage's addresses.
+__device__ __forceinline__ void rs_issue(RsLane &L, int t, u32x4 (&A)[rs::NA][4])
+{
+    const int sa = t + rs::PA, sw = t + rs::PW;
+    if (sa >= 0) {
+        u32x4 *d = A[sa % rs::NA];
+        rs_load16<0>(d[0], L.a);
+        rs_load16<16>(d[1], L.a);
+        rs_load16<32>(d[2], L.a);
+        rs_load16<48>(d[3], L.a);
+        if (sa < rs::S - 1) {
+            L.a += 128;
+            asm volatile("" : "+v"(L.a));
+        }
+    }
+    if (sw >= 0) {
+#pragma unroll
+        for (int q = 0; q < rs::DMA_PER_WAVE; ++q)
+            rs_dma16(L.w1, L.w + L.dq[q], L.lds_wave + (sw % rs::R) * rs::SLOT + q * 1024);
+        if (sw < rs::S - 1) {
+            L.w += 128;
+            asm volatile("" : "+v"(L.w));
+        }
+    }
+}
+
+__device__ __forceinline__ void rs_compute(const char *slot, const u32x4 (&av)[4], v16f (&acc)[8],
+                                           const int (&boff)[4], bool live)
+{
+    if (!live) return;                        // (uniform per wave)
+    // 32 (k step j, unit block nb) products; the B operand of each is one
+    // 16-byte LDS read.  The reads are written first and the products after
+    // them; sched_group_barrier then interleaves them RA products apart.
+    constexpr int RA = rs::kWavesPerSimd == 1 ? 8 : 4;
+    u32x4 b[4][8];
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int nb = 0; nb < 8; ++nb) b[j][nb] = *(const u32x4 *)(slot + boff[j] + nb * 4096);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int nb = 0; nb < 8; ++nb)
+            acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av[j]),
+                                                               __builtin_bit_cast(bf16x8, b[j][nb]), acc[nb], 0, 0,
+                                                               0);
+    __builtin_amdgcn_sched_group_barrier(0x100, RA, 0);
+#pragma unroll
+    for (int g = 0; g < 32 / RA - 1; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x100, RA, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, RA, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, RA, 0);
+}
+
+// H1b / H1lo: the bf16 rounding of H1 = ReLU(Z1 + b1) and the bf16 rounding
+// of what it leaves out (the tail's fp32-level layer-2 operand).
+__global__ __launch_bounds__(rs::kThreads) __attribute__((amdgpu_waves_per_eu(rs::kWavesPerSimd, rs::kWavesPerSimd))) void l1rs_bf16(
+    const uint16_t *__restrict__ T, int64_t n_rows, const int32_t *__restrict__ uniq,
+    const int32_t *__restrict__ n_uniq_p, int cap, const uint16_t *__restrict__ W1, const float *__restrict__ b1,
+    int G, uint16_t *__restrict__ H1b, uint16_t *__restrict__ H1lo)
+{
+    using namespace rs;
+    __shared__ __attribute__((aligned(256))) char ring[R * SLOT];
+    const int n_u = min(*n_uniq_p, cap);
+    if (n_u <= 0) return;
+    const int r0 = (int)((int64_t)n_u * blockIdx.x / G), r1 = (int)((int64_t)n_u * (blockIdx.x + 1) / G);
+    if (r0 >= r1) return;
+    const int lane = ams_lane(), wave = threadIdx.x / AMS_WAVE, h = lane >> 5, r32 = lane & 31;
+    constexpr size_t row_bytes = (size_t)kF * 2;
+    RsLane L;
+    {
+        // DMA group q of this wave covers slot rows 64 wave + 8 q .. + 7; lane
+        // i writes row + i / 8, physical chunk i % 8, which holds W1 chunk
+        // (i % 8) ^ rs_swz(row)
+        const int row0 = WROWS * wave + (lane >> 3);
+        L.w1 = W1;
+        L.w = 0;
+#pragma unroll
+        for (int q = 0; q < DMA_PER_WAVE; ++q) {
+            const int row = row0 + 8 * q;
+            L.dq[q] = (uint32_t)(row * row_bytes + (((lane & 7) ^ rs_swz(row)) << 4));
+        }
+        L.lds_wave = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(ring + WROWS * wave * 128));
+    }
+    int boff[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) boff[j] = r32 * 128 + (((4 * h + j) ^ rs_swz(r32)) << 4);
+
+    for (int m0 = r0; m0 < r1; m0 += BM) {
+        const int row = m0 + 32 * wave + r32;
+        const int id = row < r1 ? uniq[row] : -1;
+        const bool ok = id >= 0 && (int64_t)id < n_rows;
+        // rows past the range or with an ID outside the table stream W1's
+        // first row instead (a valid address); their results are not stored
+        // or are replaced by the zero row's result, ReLU(b1)
+        L.a = (ok ? (const char *)T + (size_t)id * row_bytes : (const char *)W1) + 64 * h;
+        L.w = 0;
+        const uint64_t okmask = ams_ballot(ok);
+        const bool wave_live = m0 + 32 * wave < r1;
+        v16f acc[8];
+#pragma unroll
+        for (int nb = 0; nb < 8; ++nb) acc[nb] = (v16f){};
+        u32x4 A[NA][4];
+#pragma unroll
+        for (int t = -PA; t < 0; ++t) rs_issue(L, t, A);
+#pragma unroll
+        for (int s = 0; s < S; ++s) {
+            // this stage's W1 DMA (this wave's part) and rows have landed; the
+            // registers are inputs (not tied outputs), so the allocator has no
+            // reason to move them, and the scheduling barrier keeps their uses
+            // below
+            asm volatile("s_waitcnt vmcnt(%4) lgkmcnt(0)" ::"v"(A[s % NA][0]), "v"(A[s % NA][1]),
+                         "v"(A[s % NA][2]), "v"(A[s % NA][3]), "n"(WAIT));
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_barrier();             // ... every wave's DMA, and slot s - 1 is free
+            __builtin_amdgcn_sched_barrier(0);
+            rs_issue(L, s, A);
+            __builtin_amdgcn_sched_barrier(0);
+            const u32x4 av[4] = {A[s % NA][0], A[s % NA][1], A[s % NA][2], A[s % NA][3]};
+            rs_compute(ring + (s % R) * SLOT, av, acc, boff, wave_live);
+            __builtin_amdgcn_sched_barrier(0);        // the products stay ahead of the next wait
+        }
+        // every register the loads past the last stage may still write stays
+        // allocated until they have landed
+#pragma unroll
+        for (int u = 0; u < NA; ++u)
+            asm volatile("s_waitcnt vmcnt(0)" ::"v"(A[u][0]), "v"(A[u][1]), "v"(A[u][2]), "v"(A[u][3]) : "memory");
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_barrier();                 // the ring is free for the next tile
+        __builtin_amdgcn_sched_barrier(0);
+        if (!wave_live) continue;
+        float bias[8];
+#pragma unroll
+        for (int nb = 0; nb < 8; ++nb) bias[nb] = b1[nb * 32 + r32];
+        // this lane's accumulator rows are 4 h + 8 (j / 4) + j % 4 of the wave's 32
+        const int rbase = m0 + 32 * wave + 4 * h;
+        // opaque per-tile bases: keeps the compiler from hoisting (and
+        // spilling) the tile-invariant parts of 32 row addresses
+        uint16_t *hb = H1b + (size_t)rbase * BN + r32, *hl = H1lo + (size_t)rbase * BN + r32;
+        asm volatile("" : "+v"(hb), "+v"(hl));
+        const uint32_t okh = (uint32_t)(okmask >> (4 * h));      // bit dr: row 4 h + dr has a table row
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int dr = 8 * (j >> 2) + (j & 3);
+            if (rbase + dr >= r1) continue;
+            const bool rok = (okh >> dr) & 1u;
+            uint16_t *pb = hb + dr * BN;
+            uint16_t *pl = hl + dr * BN;
+#pragma unroll
+            for (int nb = 0; nb < 8; ++nb) {
+                const float z = fmaxf(rok ? acc[nb][j] + bias[nb] : bias[nb], 0.f);
+                const uint16_t hi = ams_f32_to_bf16(z);
+                pb[nb * 32] = hi;
+                pl[nb * 32] = ams_f32_to_bf16(z - ams_bf16_to_f32(hi));
+            }
+        }
+    }
+}
+
 // ------------------------------------------- float32 layer 1 on bf16 MFMA
 // (AMS_F32_X3.)  A float32 x is the exact sum of three bf16 values h =
 // bf16(x), m = bf16(x - h), l = bf16(x - h - m), each rounded to nearest:
@@ -1242,7 +1495,7 @@ __global__ __launch_bounds__(kThreads) void tail_fwd_bf16(uint16_t *__restrict__
         // the chunk lies in one stream-K row tile: finished in place or cut
         const int tile = c0 / K::BM;
         const int wa = P.owner((int64_t)tile * P.S), wb = P.owner((int64_t)(tile + 1) * P.S - 1);
-        const bool split = wb > wa;
+        const bool split = pbuf != nullptr && wb > wa;      // no pieces: every tile is whole
         const int slot_a = (tile == (int)(P.it0(wa) / P.S)) ? 0 : 1;   // first contributor's piece
         bool id_ok = true;
         if (split) {
@@ -2672,6 +2925,17 @@ int sk_workers()
 
 bool use_stream_k(const ams_mlp *m) { return m->dims[1] % kSkBN == 0; }
 
+// The row-split bf16 first layer (H = 256, F = 4096) once the capacity
+// holds at least two of its 256-row tiles per CU: it then gives every CU
+// whole tiles and its output needs no partial-tile pass.  Below that (the
+// 1024-sample batches, ~50 unique rows per CU) each CU would stream all of W1
+// for a few rows, and the stream-K kernel, which splits K instead, is faster.
+bool use_row_split(const ams_mlp *m, int32_t cap)
+{
+    return m->dtype == AMS_BF16 && m->dims[1] == rs::BN && m->dims[0] == rs::kF &&
+           (int64_t)cap >= 2 * (int64_t)rs::BM * sk_workers();
+}
+
 }  // namespace
 
 extern "C" size_t ams_embed_workspace(const ams_mlp *mlp, int32_t n_uniq_cap)
@@ -2759,6 +3023,10 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
         AMS_LAUNCH("l1sk_f32", st, l1sk<float><<<G, kSkThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap,
                                                                       (const float *)W1, b1, H, G, H1f, nullptr, nullptr, pbuf,
                                                                       (int)pr));
+    } else if (sk && use_row_split(mlp, cap)) {
+        AMS_LAUNCH("l1rs_bf16", st, l1rs_bf16<<<G, rs::kThreads, 0, st>>>((const uint16_t *)T, n_rows, uniq, n_uniq,
+                                                                        cap, (const uint16_t *)W1, b1, G, h1b, h1lo));
+        pbuf = nullptr;
     } else if (sk) {
         AMS_LAUNCH("l1sk_bf16", st, l1sk<uint16_t><<<G, kSkThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq, n_uniq,
                                                                            cap, (const uint16_t *)W1, b1, H, G, nullptr,

@@ -151,6 +151,34 @@ def test_embed_fwd_matches_oracle(wname):
     assert_close(g["E"], o["E"], 1e-4, "E (fp32-accumulation accuracy)")
 
 
+# From this capacity on, the bf16 first layer runs as the row-split kernel
+# (each CU a contiguous range of the unique rows); small batches with such a
+# capacity leave most CUs a few rows or none, with ragged last tiles.
+ROW_SPLIT_CAP = 2 * 256 * 256
+
+
+@pytest.mark.parametrize("case", ["few_rows", "mid", "c2", "bad_ids"])
+def test_embed_fwd_bf16_row_split_matches_oracle(case):
+    w = synth.get("c2_bf16") if case == "c2" else mid("bf16")
+    batch, dd, Ws, bs, T_u = embed_case(w)
+    rows = np.arange(dd["n_uniq"])
+    uniq = dd["uniq"].copy()
+    if case == "few_rows":                       # fewer rows than CUs
+        rows, uniq = rows[:100], uniq[:100]
+    T_rows = T_u[rows]
+    if case == "bad_ids":                        # out-of-range IDs read as zero rows
+        uniq[[3, 700, len(uniq) - 1]] = [w.n_images + 5, -3, w.n_images]
+        T_rows = T_rows.clone()
+        T_rows[[3, 700, len(uniq) - 1]] = 0
+    print(f"row-split embed fwd {case}: n_u={len(uniq)} cap={ROW_SPLIT_CAP + 13}", flush=True)
+    T_dev = synth.table_rows(w, np.arange(w.n_images), device="cuda")
+    g = gpu_embed_fwd(w, T_dev, uniq, Ws, bs, cap=ROW_SPLIT_CAP + 13)
+    o = oracle.mlp_fwd(T_rows, np.arange(len(uniq)), Ws, bs)
+    assert_close(g["E"], o["E"], 1e-4, "E")                      # fp32 accumulation
+    assert_close(g["H1"], np.maximum(o["Z"][0], 0), RTOL["bf16"], "H1 (bf16 copy)")
+    assert_close(g["H2"], np.maximum(o["Z"][1], 0), RTOL["bf16"], "H2")
+
+
 def test_embed_fwd_out_of_range_row_reads_zero():
     w = synth.get("tiny")
     Ws, bs = synth.make_weights(w)
