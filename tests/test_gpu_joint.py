@@ -270,6 +270,88 @@ def compare_image_chained(w, batch, Ws, T_u, g, o, dU, dA):
         assert_close(g["db"][l], bw["db"][l], rt, f"db{l + 1}", extra=eb[l])
 
 
+def oracle_chain_from(w, batch, jb, Ws, T_u, o, od_t, E, bags):
+    """The oracle's joint step downstream of the first-stage outputs: pooling
+    of E, the CTR model on [U, A, bags], the pooling and MLP backward, the ID
+    row gradients and their Adagrad step, all in float64 on the given E and
+    bags (the MLP backward on the oracle's own forward activations)."""
+    od = o["dedup"]
+    seg = batch["seg_off"]
+    pf = oracle.pool_fwd("att", seg, od["inv"], E)
+    X = np.concatenate([pf["U"], pf["A"]] + list(bags), axis=1)
+    c = oracle.ctr_fwd_bwd(X, jb["labels"], *synth.make_ctr_weights(w))
+    D = w.out_dim
+    dU, dA = c["dX"][:, :D], c["dX"][:, D:2 * D]
+    dbags = [c["dX"][:, 2 * D + 12 * t:2 * D + 12 * (t + 1)] for t in range(len(bags))]
+    pb = oracle.pool_bwd("att", seg, od["inv"], od["n_uniq"], E, pf, dU, dA)
+    bw = oracle.mlp_bwd(T_u, np.arange(od["n_uniq"], dtype=np.int32), Ws, o["fwd"], pb["dE"])
+    grads, new_rows, new_acc = [], [], []
+    for t in range(len(bags)):
+        g = oracle.merged_row_grad(seg, od_t[t]["inv"], od_t[t]["n_uniq"], dbags[t])
+        r, a = oracle.adagrad_rows(g, o["_rows0"][t], o["_acc0"][t], w.joint.lr, w.joint.eps)
+        grads.append(g)
+        new_rows.append(r)
+        new_acc.append(a)
+    return {"U": pf["U"], "A": pf["A"], "w": pf["w"], "ctr": c, "dU": dU, "dA": dA, "dbags": dbags,
+            "dE": pb["dE"], "dW": bw["dW"], "db": bw["db"], "row_grads": grads, "new_rows": new_rows,
+            "new_accum": new_acc}
+
+
+def compare_joint_end_to_end(w, batch, jb, Ws, T_u, g, js, o, od_t, tabs, accs):
+    """The whole joint step against the whole float64 oracle chain.  E and the
+    bags, the first stage, are held to rtol against the oracle's.  Every later
+    output X is held to rtol plus twice |X(E_gpu, bags_gpu) - X|, where
+    X(E_gpu, bags_gpu) is the oracle's own chain evaluated on the GPU's E and
+    bags: the tolerance follows the measured sensitivity of the computation to
+    its fp32 inputs (a decision of the CTR model's ReLU near its tie, or a
+    long segment's attention term, show up there) instead of assuming it.
+    ReLU decisions of the image model near a tie widen its weight gradients'
+    tolerance as in compare_step."""
+    from tests.parity import assert_close_sensitive, grad_flip_bounds, relu_flips
+    from tests.test_gpu_parity import TAU
+    rt = RTOL[w.dtype]
+    B, n_t = w.batch, len(tabs)
+    od = o["dedup"]
+    for k in ("uniq", "inv", "occ_perm", "uniq_off"):
+        np.testing.assert_array_equal(g[k], od[k], err_msg=k)
+    assert g["n_uniq"] == od["n_uniq"] and g["dev_status"] == 0
+    assert_close(g["E"], o["fwd"]["E"], rt, "E", rows=True)
+    bags_g = [f64(js.bags[t][:B]) for t in range(n_t)]
+    for t in range(n_t):
+        assert_close(bags_g[t], o["bags"][t], F32, f"bag {t}", rows=True)
+    p = oracle_chain_from(w, batch, jb, Ws, T_u, o, od_t, g["E"], bags_g)
+
+    def held(x, ref, pert, name, rtol=rt, extra=None, rows=False):
+        return assert_close_sensitive(x, ref, pert, rtol, name, extra=extra, rows=rows)
+
+    held(g["U"], o["pool"]["U"], p["U"], "U", rows=True)
+    held(g["A"], o["pool"]["A"], p["A"], "A", rows=True)
+    held(g["w"], o["pool"]["w"], p["w"], "attention weights")
+    c = o["ctr"]
+    assert abs(float(js.loss.item()) - c["loss"]) <= F32 * max(1.0, c["loss"]) + 2 * abs(p["ctr"]["loss"] - c["loss"])
+    held(js.prob[:B], c["prob"], p["ctr"]["prob"], "prob", rtol=F32)
+    for l in range(len(js.ctr_dW)):
+        held(js.ctr_dW[l], c["dW"][l], p["ctr"]["dW"][l], f"ctr dW{l + 1}", rtol=F32)
+        held(js.ctr_db[l], c["db"][l], p["ctr"]["db"][l], f"ctr db{l + 1}", rtol=F32)
+    held(js.dU[:B], o["dU"], p["dU"], "dU", rtol=F32, rows=True)
+    held(js.dA[:B], o["dA"], p["dA"], "dA", rtol=F32, rows=True)
+    for t in range(n_t):
+        n_u = od_t[t]["n_uniq"]
+        held(js.dbags[t][:B], o["dbags"][t], p["dbags"][t], f"dbag {t}", rtol=F32, rows=True)
+        held(js.row_grad[t][:n_u], o["row_grads"][t], p["row_grads"][t], f"row grad {t}", rtol=F32, rows=True)
+        u = torch.from_numpy(od_t[t]["uniq"]).long().cuda()
+        held(tabs[t][u], o["new_rows"][t], p["new_rows"][t], f"updated rows {t}", rtol=F32)
+        held(accs[t][u], o["new_accum"][t], p["new_accum"][t], f"accumulators {t}", rtol=F32)
+    held(g["dE"], o["pool_bwd"]["dE"], p["dE"], "dE", rows=True)
+    fo = o["fwd"]
+    flips1 = relu_flips(fo["Z"][0], g["H1"], TAU)
+    flips2 = relu_flips(fo["Z"][1], g["H2"], TAU) if w.n_layers == 3 else []
+    eW, eb = grad_flip_bounds(w.dims, Ws, T_u, fo, o["bwd"], flips1, flips2, None)
+    for l in range(w.n_layers):
+        held(g["dW"][l], o["bwd"]["dW"][l], p["dW"][l], f"dW{l + 1}", extra=eW[l])
+        held(g["db"][l], o["bwd"]["db"][l], p["db"][l], f"db{l + 1}", extra=eb[l])
+
+
 @pytest.mark.parametrize("name", ["tiny_joint", "mid_joint", "c4_joint"])
 def test_joint_step_end_to_end(name):
     from tests.test_gpu_parity import compare_step
@@ -280,6 +362,8 @@ def test_joint_step_end_to_end(name):
     # chain against the oracle at the small sizes, chained stage by stage at
     # the full size (see compare_image_chained)
     if name == "c4_joint":
+        # the whole chain end to end, then each stage on the GPU's own inputs
+        compare_joint_end_to_end(w, batch, jb, Ws, T_u, g, js, o, od_t, tabs, accs)
         compare_image_chained(w, batch, Ws, T_u, g, o, js.dU[:w.batch], js.dA[:w.batch])
     else:
         compare_step(w, "att", batch, Ws, T_u, g, o)
@@ -329,3 +413,41 @@ def test_joint_step_end_to_end(name):
     for l in range(len(js.ctr_dW)):
         assert_close(js.ctr_dW[l], c["dW"][l], F32, f"ctr dW{l + 1}")
         assert_close(js.ctr_db[l], c["db"][l], F32, f"ctr db{l + 1}")
+
+
+def test_joint_step_is_bitwise_deterministic():
+    """The joint step twice from the same state (ID tables and accumulators
+    restored), with the ID-table work on its side stream beside the image
+    path: every output, the updated rows and the accumulators bit for bit."""
+    w = mid_joint()
+    batch = synth.make_batch(w)
+    jb = synth.make_joint(w, batch)
+    Ws, bs = synth.make_weights(w)
+    cW, cb = synth.make_ctr_weights(w)
+    T = synth.table_full(w, device="cuda")
+    tabs0 = [synth.id_table_full(w, t, device="cuda") for t in range(len(w.joint.id_rows))]
+    rng = np.random.default_rng(17)
+    accs0 = [torch.from_numpy(rng.uniform(0.0, 0.1, size=tuple(x.shape)).astype(np.float32)).cuda() for x in tabs0]
+    n_beh = int(batch["seg_off"][-1])
+    occ = cuda_i32(synth.occurrences(batch))
+    id_occ = [cuda_i32(synth.joint_occurrences(jb, t)) for t in range(len(tabs0))]
+    outs = []
+    for _ in range(2):
+        js = ams.JointStep(w.dims, w.dtype, "att", w.batch, n_beh, w.joint.id_rows, w.joint.id_dim,
+                           synth.ctr_dims(w))
+        tabs, accs = [x.clone() for x in tabs0], [x.clone() for x in accs0]
+        js.run(occ, w.n_images, T, [x.cuda() for x in Ws], [x.cuda() for x in bs], cuda_i32(batch["seg_off"]),
+               id_occ, tabs, accs, cuda_i32(jb["labels"]), [x.cuda() for x in cW], [x.cuda() for x in cb],
+               w.joint.lr, w.joint.eps)
+        torch.cuda.synchronize()
+        g = gpu_outputs(js.img)
+        g.update({"loss": js.loss.cpu().numpy(), "dU": f64(js.dU), "dA": f64(js.dA),
+                  "tabs": [x.cpu().numpy() for x in tabs], "accs": [x.cpu().numpy() for x in accs],
+                  "ctr_dW": [f64(x) for x in js.ctr_dW], "dbags": [f64(x) for x in js.dbags]})
+        outs.append(g)
+    a, b = outs
+    for k in ("E", "U", "A", "dE", "loss", "dU", "dA"):
+        np.testing.assert_array_equal(a[k], b[k], err_msg=k)
+    for k in ("dW", "db", "tabs", "accs", "ctr_dW", "dbags"):
+        for x, y in zip(a[k], b[k]):
+            np.testing.assert_array_equal(x, y, err_msg=k)

@@ -405,6 +405,24 @@ def test_step_is_bitwise_deterministic():
         np.testing.assert_array_equal(outs[0]["db"][l], outs[1]["db"][l])
 
 
+@pytest.mark.parametrize("mode,cap", [("att", None), ("sum", None), ("att", ROW_SPLIT_CAP)])
+def test_bf16_step_is_bitwise_deterministic(mode, cap):
+    """The 1024-sample bf16 step twice, on fresh buffers: the stream-K first
+    layer (partial tiles added in K order), the split high/low tails and, with
+    a capacity past ROW_SPLIT_CAP, the row-split first layer."""
+    w = synth.get("c2_bf16")
+    batch = synth.make_batch(w)
+    Ws, bs = synth.make_weights(w)
+    T_dev = synth.table_full(w, device="cuda")
+    print(f"bf16 determinism {mode} cap={cap}", flush=True)
+    outs = [gpu_outputs(run_gpu_step(w, batch, T_dev, Ws, bs, mode, cap=cap)) for _ in range(2)]
+    for k in ("E", "H1", "H2", "U", "A", "dE"):
+        np.testing.assert_array_equal(outs[0][k], outs[1][k], err_msg=k)
+    for l in range(w.n_layers):
+        np.testing.assert_array_equal(outs[0]["dW"][l], outs[1]["dW"][l])
+        np.testing.assert_array_equal(outs[0]["db"][l], outs[1]["db"][l])
+
+
 def test_table_generator_is_device_independent():
     w = synth.get("c2_bf16")
     rows = np.array([0, 1, 77, 199_999, 123_456])
