@@ -18,7 +18,13 @@ Passes after the timed one (none of them enters `value`):
     largest total time, from its algorithmic flops and bytes per unique image;
   * cold: each step timed alone after a 512 MiB write that evicts the caches.
 The CPU baseline is the float64 oracle, timed on this host on one whole batch
-of the same workload, repeated for about ten seconds (median run).
+of the same workload, repeated for about ten seconds (median run), with the
+time of each of its phases and a one-thread run on the batch's first 64
+samples.  With the default workload (the 1024-sample float32 step, whose
+number is `value`) the line also carries, under "workloads", the same
+measurement of the bf16 workloads: the 1024-sample bf16 step (attentive
+pooling, sum and max beside) and the 4096-sample step over the 2M-image
+table, each with its own roofline entry.
 """
 from __future__ import annotations
 
@@ -36,6 +42,8 @@ sys.path.insert(0, ROOT)
 METRIC = "behavior images embedded+pooled/sec (fwd+bwd), % HBM peak and % MFMA peak"
 PEAK_HBM = 8.0e12
 PEAK_MFMA = {"f32": 157.3e12, "bf16": 2.5e15}
+DEFAULT_WORKLOAD = "c1_f32"
+OTHER_WORKLOADS = ("c2_bf16", "c3_long")
 
 
 def mfma_peak(kernel: str, dtype: str) -> float:
@@ -101,7 +109,40 @@ def cpu_model():
     return "unknown"
 
 
-def cpu_baseline(w, batch, mode, min_runs=3, min_seconds=10.0, max_runs=30):
+def oracle_phases(batch, n_ids, T_u, Ws, bs, mode):
+    """One oracle step, phase by phase (the oracle's own calls, in its order),
+    with the wall time of each phase."""
+    import numpy as np
+
+    from oracle import oracle
+    t = {}
+    t0 = time.perf_counter()
+    occ = np.concatenate([batch["beh_ids"], batch["ad_ids"]]).astype(np.int32)
+    dd = oracle.dedup(occ, n_ids)
+    t1 = time.perf_counter()
+    rows = np.arange(dd["n_uniq"], dtype=np.int32)
+    fw = oracle.mlp_fwd(T_u, rows, Ws, bs)
+    t2 = time.perf_counter()
+    pf = oracle.pool_fwd(mode, batch["seg_off"], dd["inv"], fw["E"])
+    t3 = time.perf_counter()
+    pb = oracle.pool_bwd(mode, batch["seg_off"], dd["inv"], dd["n_uniq"], fw["E"], pf, batch["g_u"], batch["g_a"])
+    t4 = time.perf_counter()
+    oracle.mlp_bwd(T_u, rows, Ws, fw, pb["dE"])
+    t5 = time.perf_counter()
+    t = {"dedup": t1 - t0, "mlp_fwd": t2 - t1, "pool_fwd": t3 - t2, "pool_bwd": t4 - t3, "mlp_bwd": t5 - t4}
+    return t5 - t0, t
+
+
+def sub_batch(batch, n_samples):
+    """The first n_samples samples of a batch (their behaviors, ads and
+    upstream gradients)."""
+    seg = batch["seg_off"][:n_samples + 1]
+    n_beh = int(seg[-1])
+    return {"seg_off": seg, "beh_ids": batch["beh_ids"][:n_beh], "ad_ids": batch["ad_ids"][:n_samples],
+            "g_u": batch["g_u"][:n_samples], "g_a": batch["g_a"][:n_samples]}
+
+
+def cpu_baseline(w, batch, mode, min_runs=3, min_seconds=10.0, max_runs=30, one_thread_samples=64):
     import numpy as np
 
     from oracle import oracle
@@ -111,20 +152,33 @@ def cpu_baseline(w, batch, mode, min_runs=3, min_seconds=10.0, max_runs=30):
     uniq = np.unique(occ)
     T_u = synth.table_rows(w, uniq)
     # repeated until about min_seconds of CPU work, then the median run
-    times = []
-    while len(times) < min_runs or (sum(times) < min_seconds and len(times) < max_runs):
-        t0 = time.perf_counter()
-        oracle.step(batch, w.n_images, T_u, Ws, bs, mode, table_is_compact=True)
-        times.append(time.perf_counter() - t0)
-    dt = sorted(times)[len(times) // 2]
-    runs = len(times)
+    runs = []
+    while len(runs) < min_runs or (sum(r[0] for r in runs) < min_seconds and len(runs) < max_runs):
+        runs.append(oracle_phases(batch, w.n_images, T_u, Ws, bs, mode))
+    runs.sort(key=lambda r: r[0])
+    dt, phases = runs[len(runs) // 2]
+    times = [r[0] for r in runs]
     n_beh = int(batch["seg_off"][-1])
-    return {"value": n_beh / dt, "unit": "behavior images/s", "cores": oracle.num_threads(),
+    threads = oracle.num_threads()
+    # one thread, on a bounded sample: the batch's first samples
+    sb = sub_batch(batch, one_thread_samples)
+    su = np.unique(synth.occurrences(sb))
+    oracle.set_threads(1)
+    try:
+        t1, ph1 = oracle_phases(sb, w.n_images, synth.table_rows(w, su), Ws, bs, mode)
+    finally:
+        oracle.set_threads(threads)
+    n_beh1 = int(sb["seg_off"][-1])
+    return {"value": n_beh / dt, "unit": "behavior images/s", "cores": threads,
             "kind": "oracle",
             "sample": f"one whole batch of the same workload ({w.batch} samples, {n_beh} behaviors, "
-                      f"{uniq.size} unique images), float64 C oracle with OpenMP, median of {runs} runs "
+                      f"{uniq.size} unique images), float64 C oracle with OpenMP, median of {len(runs)} runs "
                       f"(total {sum(times):.1f} s, min {min(times):.2f} s, max {max(times):.2f} s), "
-                      f"CPU: {cpu_model()}"}
+                      f"CPU: {cpu_model()}",
+            "phases_s": phases,
+            "one_thread": {"value": n_beh1 / t1, "unit": "behavior images/s", "cores": 1, "phases_s": ph1,
+                           "sample": f"the batch's first {one_thread_samples} samples ({n_beh1} behaviors, "
+                                     f"{su.size} unique images), one run"}}
 
 
 def bench_peaks(args):
@@ -200,13 +254,16 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default="c1_f32")
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--mode", default=None)
     ap.add_argument("--dtype", default=None, choices=("f32", "f32x3", "bf16"),
                     help="override the workload's storage/arithmetic mode (f32x3: float32 storage, "
                          "the 4096-wide forward product on bf16 MFMA with a three-part split)")
     ap.add_argument("--batches", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-other-workloads", action="store_true",
+                    help="with the default workload, leave out the bf16 legs (the 1024-sample step with each "
+                         "pooling mode, the 2M-image long-behavior step) added under 'workloads'")
     ap.add_argument("--ops", action="store_true",
                     help="instead of the step, time the widened operations one by one at their real shapes "
                          "(one JSON line each)")
@@ -258,6 +315,25 @@ def main():
     ams.load()
     if w.joint is not None:
         return bench_joint(w, mode, args)
+
+    out = bench_step(w, mode, args)
+    if args.workload == DEFAULT_WORKLOAD and not args.no_other_workloads:
+        # the bf16 workloads of the same metric, each a leg of its own
+        out["workloads"] = {}
+        for name in OTHER_WORKLOADS:
+            torch.cuda.empty_cache()
+            w2 = synth.get(name)
+            out["workloads"][name] = bench_step(w2, w2.pools[-1], args, light=True)
+    print(json.dumps(out))
+
+
+def bench_step(w, mode, args, light=False):
+    """Times the hot path of workload w (pooling `mode`) and returns its JSON
+    record.  light: the value, the other pooling modes, per-kernel times and
+    the roofline only (no pipelined, f32x3, cold, per-call or CPU legs)."""
+    import torch
+
+    from paper_1711_06505_amd import ams, synth
 
     # inputs, resident in HBM before timing starts
     T = synth.table_full(w, device="cuda")
@@ -321,17 +397,19 @@ def main():
     ms_step = ms_total / args.steps
     # the same K steps through StepPipeline (dedup of batch k + 1 on a second
     # stream beside batch k's pooling and backward), reported beside
-    pipe = ams.StepPipeline(step, w.n_images)
-    pipe.run(seq[:2], T, Wd, bd)
-    torch.cuda.synchronize()
-    t_start.record(stream)
-    last = pipe.run(seq, T, Wd, bd)
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    assert int(pipe.sets[last]["dev_status"].item()) == 0
-    ms_step_pipe = t_start.elapsed_time(t_end) / args.steps
-    for key in pipe._SET:
-        setattr(step, key, pipe.sets[0][key])
+    ms_step_pipe = None
+    if not light:
+        pipe = ams.StepPipeline(step, w.n_images)
+        pipe.run(seq[:2], T, Wd, bd)
+        torch.cuda.synchronize()
+        t_start.record(stream)
+        last = pipe.run(seq, T, Wd, bd)
+        t_end.record(stream)
+        torch.cuda.synchronize()
+        assert int(pipe.sets[last]["dev_status"].item()) == 0
+        ms_step_pipe = t_start.elapsed_time(t_end) / args.steps
+        for key in pipe._SET:
+            setattr(step, key, pipe.sets[0][key])
     order = [s % len(dev_batches) for s in range(args.steps)]
     beh_total = sum(dev_batches[i]["n_beh"] for i in order)
     uniq_total = sum(n_uniq[i] for i in order)
@@ -359,7 +437,7 @@ def main():
         other_modes[m] = {"value": beh_total / (msm * args.steps * 1e-3), "ms_per_step": msm}
         del stm
     split3 = None
-    if w.dtype == "f32":
+    if w.dtype == "f32" and not light:
         step3 = ams.Step(w.dims, "f32x3", mode, w.batch, n_beh_max)
         step3.alloc_workspace(w.n_images)
         for b in seq[:2]:
@@ -379,17 +457,19 @@ def main():
         del step3
 
     # per-call durations: a second pass with events between the calls
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
-    for s in range(args.steps):
-        one(dev_batches[s % len(dev_batches)], evs[s])
-    torch.cuda.synchronize()
-    per = {"dedup": 0.0, "embed_fwd": 0.0, "pool_fwd_bwd": 0.0, "embed_bwd": 0.0}
-    for e in evs:
-        per["dedup"] += e[0].elapsed_time(e[1])
-        per["embed_fwd"] += e[1].elapsed_time(e[2])
-        per["pool_fwd_bwd"] += e[2].elapsed_time(e[3])
-        per["embed_bwd"] += e[3].elapsed_time(e[4])
-    per = {k: v / args.steps for k, v in per.items()}
+    per = None
+    if not light:
+        evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
+        for s in range(args.steps):
+            one(dev_batches[s % len(dev_batches)], evs[s])
+        torch.cuda.synchronize()
+        per = {"dedup": 0.0, "embed_fwd": 0.0, "pool_fwd_bwd": 0.0, "embed_bwd": 0.0}
+        for e in evs:
+            per["dedup"] += e[0].elapsed_time(e[1])
+            per["embed_fwd"] += e[1].elapsed_time(e[2])
+            per["pool_fwd_bwd"] += e[2].elapsed_time(e[3])
+            per["embed_bwd"] += e[3].elapsed_time(e[4])
+        per = {k: v / args.steps for k, v in per.items()}
 
     # per-kernel durations: the library's event pairs on the launching stream
     ams.ams_timing_read()                      # drop anything recorded before
@@ -404,7 +484,7 @@ def main():
     # cold caches: each step timed alone after a 512 MiB write
     scratch = torch.empty(512 << 18, dtype=torch.float32, device="cuda")
     cold_ms = []
-    for s in range(args.steps):
+    for s in range(0 if light else args.steps):
         scratch.fill_(float(s))
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         e0.record(stream)
@@ -413,7 +493,10 @@ def main():
         torch.cuda.synchronize()
         cold_ms.append(e0.elapsed_time(e1))
     del scratch
-    cold_step = sum(cold_ms) / len(cold_ms)
+    cold = None
+    if cold_ms:
+        cold = {"value": beh_total / (sum(cold_ms) * 1e-3), "ms_per_step": sum(cold_ms) / len(cold_ms),
+                "note": "each step timed alone after a 512 MiB device write"}
 
     fwd_f, bwd_f = flops_per_unique(w.dims)
     u_mean = uniq_total / args.steps
@@ -460,20 +543,24 @@ def main():
         "step_hbm_frac": step_bytes / (ms_step * 1e-3) / PEAK_HBM,
         "unique_images_per_s": uniq_total / (ms_total * 1e-3),
         "samples_per_s": w.batch * args.steps / (ms_total * 1e-3),
-        "pipelined": {"value": beh_total / (ms_step_pipe * args.steps * 1e-3), "ms_per_step": ms_step_pipe,
-                      "note": "the same steps through StepPipeline (dedup of the next batch on a second stream)"},
+        "pipelined": None if ms_step_pipe is None else {
+            "value": beh_total / (ms_step_pipe * args.steps * 1e-3), "ms_per_step": ms_step_pipe,
+            "note": "the same steps through StepPipeline (dedup of the next batch on a second stream)"},
         "f32x3": split3,
         "other_pooling_modes": other_modes or None,
-        "cold": {"value": beh_total / (sum(cold_ms) * 1e-3), "ms_per_step": cold_step,
-                 "note": "each step timed alone after a 512 MiB device write"},
+        "cold": cold,
         "per_call_ms": per,
         "kernels": kernels,
         "roofline": roof,
         "cpu_baseline": None,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not light:
         out["cpu_baseline"] = cpu_baseline(w, host_batches[0], mode)
-    print(json.dumps(out))
+    if light:
+        for k in ("n_gpus", "steps", "warmup", "higher_is_better", "scaling", "vs_baseline", "data", "metric",
+                  "unit", "pipelined", "f32x3", "cold", "per_call_ms", "cpu_baseline"):
+            out.pop(k, None)
+    return out
 
 
 def bench_joint(w, mode, args):
