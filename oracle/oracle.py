@@ -18,7 +18,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "ams_oracle.c")
-_LIB_PATH = os.path.join(_HERE, "libams_oracle.so")
+# AMS_ORACLE_LIB selects another build of the same source (the test that
+# runs the oracle under AddressSanitizer/UBSan builds one with sanitize=True)
+_LIB_PATH = os.environ.get("AMS_ORACLE_LIB") or os.path.join(_HERE, "libams_oracle.so")
 
 POOL_SUM, POOL_MAX, POOL_ATT = 0, 1, 2
 POOL_MODES = {"sum": POOL_SUM, "max": POOL_MAX, "att": POOL_ATT}
@@ -27,16 +29,22 @@ F32, BF16 = 0, 1
 _lib = None
 
 
-def build(force: bool = True) -> str:
-    """Compile ams_oracle.c with gcc (plain -O2, IEEE semantics, OpenMP)."""
-    if not force and os.path.exists(_LIB_PATH) and os.path.getmtime(_LIB_PATH) >= os.path.getmtime(_SRC):
-        return _LIB_PATH
-    tmp = _LIB_PATH + ".tmp%d" % os.getpid()
+def build(force: bool = True, sanitize: bool = False, out: str | None = None) -> str:
+    """Compile ams_oracle.c with gcc (plain -O2, IEEE semantics, OpenMP).
+    sanitize: instrument with AddressSanitizer and UndefinedBehaviorSanitizer
+    (every finding fatal); out: where the library goes (default: the one
+    this module loads)."""
+    path = out or _LIB_PATH
+    if not force and os.path.exists(path) and os.path.getmtime(path) >= os.path.getmtime(_SRC):
+        return path
+    tmp = path + ".tmp%d" % os.getpid()
     cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-ffp-contract=off", "-fno-fast-math",
            "-Wall", "-Wextra", "-shared", "-fPIC", "-o", tmp, _SRC, "-lm"]
+    if sanitize:
+        cmd[1:1] = ["-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined", "-fno-sanitize-recover=all"]
     subprocess.run(cmd, check=True)
-    os.replace(tmp, _LIB_PATH)
-    return _LIB_PATH
+    os.replace(tmp, path)
+    return path
 
 
 def _load():
