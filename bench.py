@@ -267,6 +267,8 @@ def main():
     ap.add_argument("--ops", action="store_true",
                     help="instead of the step, time the widened operations one by one at their real shapes "
                          "(one JSON line each)")
+    ap.add_argument("--ops-scaled-only", action="store_true",
+                    help="with --ops, time only the aggregators at the 65,536-sample point (for counter runs)")
     ap.add_argument("--peaks", action="store_true",
                     help="instead of the step, time the achievable-peak probes (HBM copy and read, gathers of "
                          "the long-behavior step's unique rows by visit order, MFMA loops) and print one JSON line")
@@ -694,10 +696,11 @@ PEAK_F32_VALU = 157.3e12
 
 def bench_ops(args):
     """The operations beside the step, each timed alone at its real shape on
-    inputs resident in HBM: one channel of multiple-query attentive pooling
-    and the concatenate aggregator on the long-sequence batch, the Adam update
-    of the image model, the CTR model with PReLU and the pre-rank towers at
-    4096 samples.  Per op: ms per call over --steps calls (HIP events on the
+    inputs resident in HBM: the sum and attentive aggregators at 65,536
+    samples, one channel of multiple-query attentive pooling and the
+    concatenate aggregator on the long-sequence batch, the Adam update of the
+    image model, the CTR model with PReLU and the pre-rank towers at 4096
+    samples.  Per op: ms per call over --steps calls (HIP events on the
     launch stream) after --warmup calls, the library's per-kernel times, and
     a roofline entry: compulsory HBM bytes (every input read once, every
     output written once) against 8 TB/s, or for the small fp32 nets their
@@ -735,6 +738,45 @@ def bench_ops(args):
                           "roofline": {"bound": bound, "achieved": ach, "peak": pk, "unit": unit, "frac": ach / pk,
                                        "work_per_call": work, "unit_of_work": unit_note},
                           "kernels": kt}), flush=True)
+
+    # ---- the aggregators alone at a scale where bandwidth, not latency,
+    # bounds them: 65,536 samples with the long-sequence lengths (geometric,
+    # mean 200, capped at 500) and image IDs (Zipf 1.05 over 2M), ~12M
+    # behaviors; E random (the embedding model is not part of this leg).
+    # Algorithmic bytes per the step's units: forward 52 B per behavior (its
+    # index and its 48-byte row) + 96 B per sample (U and A), + 4 B per
+    # behavior for the attention weights; backward 60 B per occurrence
+    # (stable order, inverse index and its 48-byte gradient) + 48 B per
+    # unique image (dE), + 8 B per behavior for attention (weights, E row).
+    wsc = dataclasses.replace(synth.get("c3_long"), name="pool_scaled", index=31, batch=65_536, stream=-1)
+    hb = synth.make_batch(wsc)
+    occ = torch.from_numpy(synth.occurrences(hb)).cuda()
+    seg = torch.from_numpy(hb["seg_off"]).cuda()
+    B, n_beh, D = wsc.batch, int(hb["seg_off"][-1]), 12
+    gA_d = torch.from_numpy(hb["g_a"]).cuda()
+    gU_d = torch.from_numpy(hb["g_u"]).cuda()
+    for mode in ("sum", "att"):
+        # (at most n_images distinct images: that capacity always holds)
+        st = ams.Step((wsc.in_dim, 256, 64, D), "bf16", mode, B, n_beh, cap=wsc.n_images, cap_checked=True)
+        st.dedup(occ, wsc.n_images)
+        torch.cuda.synchronize()
+        assert int(st.dev_status.item()) == 0
+        n_u = int(st.n_uniq.item())
+        st.alloc_workspace(wsc.n_images)
+        g = torch.Generator(device="cuda").manual_seed(7)
+        st.E.copy_(torch.randn(st.E.shape, generator=g, device="cuda") * 0.5)
+        shape = f"B={B} (lengths geometric mean 200 cap 500), {n_beh} behaviors, {n_u} unique images, D={D}"
+        att = 1 if mode == "att" else 0
+        timed(f"pool_scaled_{mode}_fwd", lambda: st.pool_fwd(seg, n_beh), shape, "hbm",
+              n_beh * (52 + 4 * att) + B * 96, "52 B per behavior (+4 attention weight) + 96 B per sample")
+        st.pool_fwd(seg, n_beh)
+        timed(f"pool_scaled_{mode}_bwd", lambda: st.pool_bwd(seg, n_beh, gU_d, gA_d), shape, "hbm",
+              (n_beh + B) * 60 + n_u * 48 + n_beh * 8 * att,
+              "60 B per occurrence (+8 attention) + 48 B per unique image")
+        del st
+        torch.cuda.empty_cache()
+    if args.ops_scaled_only:
+        return
 
     # ---- pooling variants on the long-sequence batch
     w = synth.get("c3_long")

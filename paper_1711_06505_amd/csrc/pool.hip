@@ -255,16 +255,23 @@ __global__ __launch_bounds__(kThreads) void pool_concat_fwd_k(int B, int D, int 
     }
 }
 
-// (1) per sample: tag occurrences with their sample; attention terms
+// The record of occurrence k, written in occurrence order for the stable-order
+// pass to read with one access: its unique index, and its sample i for a
+// behavior or -1 - i for the ad of sample i; with attention also the
+// behavior's weight w_j and its score gradient ds_j (float bits).
+template <int MODE>
+constexpr bool wide_rec() { return MODE == AMS_POOL_ATT || MODE == kPoolQuery; }
+
+// (1) per sample: the records of its occurrences; attention terms
 // c_i = g_i . u_i and da_i = sum_j ds_j e_j, ds_j = w_j (g_i . e_j - c_i).
 template <int MODE, int DM>
 __global__ __launch_bounds__(kThreads) void pool_bwd_sample(int B, int D, const int32_t *__restrict__ seg_off,
-                                                            const int32_t *__restrict__ inv, int cap,
+                                                            int64_t n_beh, const int32_t *__restrict__ inv, int cap,
                                                             const float *__restrict__ E,
                                                             const float *__restrict__ U,
                                                             const float *__restrict__ wsaved,
                                                             const float *__restrict__ dU,
-                                                            int32_t *__restrict__ samp,
+                                                            void *__restrict__ rec,
                                                             float *__restrict__ cvec,
                                                             float *__restrict__ da)
 {
@@ -272,7 +279,21 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_sample(int B, int D, const 
     const int i = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
     if (i >= B) return;
     const int j0 = seg_off[i], j1 = seg_off[i + 1];
-    for (int j = j0 + lane; j < j1; j += AMS_WAVE) samp[j] = i;
+    if (lane == 0) {
+        const int k = (int)(n_beh + i);
+        if (wide_rec<MODE>()) ((int4 *)rec)[k] = make_int4(inv[k], -1 - i, 0, 0);
+        else ((int2 *)rec)[k] = make_int2(inv[k], -1 - i);
+    }
+    if (!wide_rec<MODE>()) {
+        int2 *r2 = (int2 *)rec;
+        int j = j0 + lane;
+        for (; j + AMS_WAVE < j1; j += 2 * AMS_WAVE) {
+            const int u0 = inv[j], u1 = inv[j + AMS_WAVE];
+            r2[j] = make_int2(u0, i);
+            r2[j + AMS_WAVE] = make_int2(u1, i);
+        }
+        if (j < j1) r2[j] = make_int2(inv[j], i);
+    }
     if (MODE != AMS_POOL_ATT && MODE != kPoolQuery) return;
     float g[DM], u[DM];
     load_row<DM>(dU, i, D, g);
@@ -283,11 +304,14 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_sample(int B, int D, const 
     float acc[DM];
 #pragma unroll
     for (int d = 0; d < DM; ++d) acc[d] = 0.f;
-    auto take = [&](int j, const float (&e)[DM]) {
+    int4 *r4 = (int4 *)rec;
+    auto take = [&](int j, int r, const float (&e)[DM]) {
         float dw = 0.f;
 #pragma unroll
         for (int d = 0; d < DM; ++d) dw += g[d] * e[d];
-        const float ds = wsaved[j] * (dw - c);
+        const float wj = wsaved[j];
+        const float ds = wj * (dw - c);
+        r4[j] = make_int4(r, i, __float_as_int(wj), __float_as_int(ds));
 #pragma unroll
         for (int d = 0; d < DM; ++d) acc[d] += ds * e[d];
     };
@@ -297,13 +321,14 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_sample(int B, int D, const 
         float e0[DM], e1[DM];
         load_row_cap<DM>(E, r0, cap, D, e0);
         load_row_cap<DM>(E, r1, cap, D, e1);
-        take(j, e0);
-        take(j + AMS_WAVE, e1);
+        take(j, r0, e0);
+        take(j + AMS_WAVE, r1, e1);
     }
     if (j < j1) {
+        const int r0 = inv[j];
         float e0[DM];
-        load_row_cap<DM>(E, inv[j], cap, D, e0);
-        take(j, e0);
+        load_row_cap<DM>(E, r0, cap, D, e0);
+        take(j, r0, e0);
     }
     float mine = 0.f;
 #pragma unroll
@@ -350,19 +375,24 @@ __device__ __forceinline__ void seg_scan(int u, float (&v)[DM])
     seg_step<0x143, 0xC, DM>(u, v);
 }
 
-// (2) segmented sums over chunks of 64 positions of the stable occurrence order.
+// (2) segmented sums over chunks of 64 positions of the stable occurrence
+// order.  A wave takes CPW consecutive chunks and issues each level of their
+// dependent loads for all of them before using any (the stable order; then
+// each position's unique index and sample; then the rows), so CPW chains of
+// random reads are in flight per lane instead of one; each chunk is then
+// scanned and written as one.
 template <int MODE, int DM>
-__global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int64_t n_beh, int n_occ, int cap,
-                                                         const int32_t *__restrict__ inv,
+constexpr int seg_cpw() { return DM > 16 || MODE == AMS_POOL_MAX ? 2 : 4; }
+
+template <int MODE, int DM>
+__global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int n_occ, int cap,
                                                          const int32_t *__restrict__ occ_perm,
                                                          const int32_t *__restrict__ uniq_off,
-                                                         const float *__restrict__ E,
                                                          const float *__restrict__ A,
                                                          const void *__restrict__ saved,
                                                          const float *__restrict__ dU,
                                                          const float *__restrict__ dA,
-                                                         const int32_t *__restrict__ samp,
-                                                         const float *__restrict__ cvec,
+                                                         const void *__restrict__ rec,
                                                          const float *__restrict__ da, int nch,
                                                          float *__restrict__ dE,
                                                          float *__restrict__ head_part,
@@ -370,112 +400,180 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int64_t n_beh, i
                                                          int32_t *__restrict__ cross, int accumulate,
                                                          const int32_t *__restrict__ seg_off, int Lc)
 {
+    constexpr int CPW = seg_cpw<MODE, DM>();
+    constexpr bool ATT = MODE == AMS_POOL_ATT || MODE == kPoolQuery;
     const int lane = ams_lane();
-    const int ch = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
-    if (ch >= nch) return;
-    const int c0 = ch * AMS_WAVE, c1 = c0 + AMS_WAVE;
-    const int p = c0 + lane;
-    // an occurrence whose unique index is at or past the caller's capacity
-    // (possible only when the capacity is below the real unique count) is
-    // dropped: its row of dE does not exist
-    const int k = p < n_occ ? occ_perm[p] : 0;
-    const int uk = p < n_occ ? inv[k] : -1;
-    const bool valid = p < n_occ && uk < cap;
-    int u = -1 - lane;       // distinct per invalid lane: never joins a run
-    float v[DM];
+    const int ch0 = (blockIdx.x * kWaves + threadIdx.x / AMS_WAVE) * CPW;
+    if (ch0 >= nch) return;
+    // level 1: the stable order
+    int k[CPW];
 #pragma unroll
-    for (int d = 0; d < DM; ++d) v[d] = 0.f;
-    if (valid) {
-        u = uk;
-        if (k < n_beh) {
-            const int i = samp[k];
-            float g[DM];
-            if (MODE != kPoolConcat) load_row<DM>(dU, i, D, g);
-            if (MODE == AMS_POOL_SUM) {
+    for (int c = 0; c < CPW; ++c) {
+        const int p = (ch0 + c) * AMS_WAVE + lane;
+        k[c] = p < n_occ ? occ_perm[p] : 0;
+    }
+    // level 2: the record of each position's occurrence (unique index, sample,
+    // attention weight).  An occurrence whose unique index is at or past the
+    // caller's capacity (possible only when the capacity is below the real
+    // unique count) is dropped: its row of dE does not exist.  si: the sample
+    // of a behavior, -1 - i for the ad of sample i, or INT_MIN (nothing)
+    int uk[CPW], si[CPW];
+    float wk[CPW], dsk[CPW];
 #pragma unroll
-                for (int d = 0; d < DM; ++d) v[d] = g[d];
-            } else if (MODE == kPoolConcat) {
-                const int pos = k - seg_off[i];
-                if (pos < Lc) load_row<DM>(dU + (size_t)i * Lc * D, pos, D, v);
+    for (int c = 0; c < CPW; ++c) {
+        const int p = (ch0 + c) * AMS_WAVE + lane;
+        uk[c] = -1;
+        si[c] = INT_MIN;
+        wk[c] = 0.f;
+        dsk[c] = 0.f;
+        if (p < n_occ) {
+            if constexpr (ATT) {
+                const int4 r = ((const int4 *)rec)[k[c]];
+                uk[c] = r.x;
+                si[c] = r.y;
+                wk[c] = __int_as_float(r.z);
+                dsk[c] = __int_as_float(r.w);
+            } else {
+                const int2 r = ((const int2 *)rec)[k[c]];
+                uk[c] = r.x;
+                si[c] = r.y;
+            }
+        }
+    }
+    // level 3: the rows each position's gradient is made of
+    float r[CPW][DM];            // dU of the behavior's sample (concat: its slice), or the ad's dA
+    float a[ATT ? CPW : 1][DM];  // attentive: the sample's query row, or the ad's attention term da
+    int am[MODE == AMS_POOL_MAX ? CPW : 1][DM];
+#pragma unroll
+    for (int c = 0; c < CPW; ++c) {
+        const bool valid = si[c] != INT_MIN && uk[c] < cap;
+        const bool beh = valid && si[c] >= 0;
+        const bool ad = valid && si[c] < 0 && MODE != kPoolQuery;
+        const int i = beh ? si[c] : (ad ? -1 - si[c] : 0);
+#pragma unroll
+        for (int d = 0; d < DM; ++d) r[c][d] = 0.f;
+        if (beh && MODE != kPoolConcat) load_row<DM>(dU, i, D, r[c]);
+        if (beh && MODE == kPoolConcat) {
+            const int pos = k[c] - seg_off[i];
+            if (pos < Lc) load_row<DM>(dU + (size_t)i * Lc * D, pos, D, r[c]);
+        }
+        if (ad && dA) load_row<DM>(dA, i, D, r[c]);
+        if constexpr (MODE == AMS_POOL_MAX) {
+            const int32_t *amr = (const int32_t *)saved + (size_t)i * D;
+#pragma unroll
+            for (int d = 0; d < DM; ++d) am[c][d] = (beh && d < D) ? amr[d] : -1;
+        }
+        if constexpr (ATT) {
+#pragma unroll
+            for (int d = 0; d < DM; ++d) a[c][d] = 0.f;
+            if (beh) load_row<DM>(A, i, D, a[c]);
+            if (ad && MODE == AMS_POOL_ATT) load_row<DM>(da, i, D, a[c]);
+        }
+    }
+    // each chunk: its positions' gradients, summed per run of one image
+#pragma unroll
+    for (int c = 0; c < CPW; ++c) {
+        const int ch = ch0 + c;
+        if (ch >= nch) break;
+        const int c0 = ch * AMS_WAVE, c1 = c0 + AMS_WAVE;
+        const bool valid = si[c] != INT_MIN && uk[c] < cap;
+        const bool beh = valid && si[c] >= 0;
+        int u = valid ? uk[c] : -1 - lane;       // distinct per invalid lane: never joins a run
+        float v[DM];
+#pragma unroll
+        for (int d = 0; d < DM; ++d) v[d] = 0.f;
+        if (beh) {
+            if (MODE == AMS_POOL_SUM || MODE == kPoolConcat) {
+#pragma unroll
+                for (int d = 0; d < DM; ++d) v[d] = r[c][d];
             } else if (MODE == AMS_POOL_MAX) {
-                const int32_t *am = (const int32_t *)saved + (size_t)i * D;
 #pragma unroll
-                for (int d = 0; d < DM; ++d) v[d] = (d < D && am[d] == k) ? g[d] : 0.f;
-            } else {   // attentive; A holds the query rows in the query mode
-                const float wk = ((const float *)saved)[k];
-                float e[DM], a[DM];
-                load_row<DM>(E, u, D, e);
-                load_row<DM>(A, i, D, a);
-                float dw = 0.f;
+                for (int d = 0; d < DM; ++d) v[d] = am[MODE == AMS_POOL_MAX ? c : 0][d] == k[c] ? r[c][d] : 0.f;
+            } else {   // attentive: w_j g_i + ds_j a_i; A holds the query rows in the query mode
 #pragma unroll
-                for (int d = 0; d < DM; ++d) dw += g[d] * e[d];
-                const float ds = wk * (dw - cvec[i]);
-#pragma unroll
-                for (int d = 0; d < DM; ++d) v[d] = wk * g[d] + ds * a[d];
+                for (int d = 0; d < DM; ++d) v[d] = wk[c] * r[c][d] + dsk[c] * a[ATT ? c : 0][d];
             }
-        } else if (MODE != kPoolQuery) {
-            const int i = (int)(k - n_beh);
-            if (dA) load_row<DM>(dA, i, D, v);
+        } else if (valid && MODE != kPoolQuery) {   // an ad: dA (+ the attention term)
+#pragma unroll
+            for (int d = 0; d < DM; ++d) v[d] = r[c][d];
             if (MODE == AMS_POOL_ATT) {
-                float t[DM];
-                load_row<DM>(da, i, D, t);
 #pragma unroll
-                for (int d = 0; d < DM; ++d) v[d] += t[d];
+                for (int d = 0; d < DM; ++d) v[d] += a[ATT ? c : 0][d];
             }
         }
-    }
-    seg_scan<DM>(u, v);
-    const int nu_next = __shfl_down(u, 1, AMS_WAVE);
-    const bool run_end = valid && (lane == AMS_WAVE - 1 || nu_next != u);
-    int cross_u = -1;
-    if (run_end) {
-        const int s = uniq_off[u], e = uniq_off[u + 1];
-        float *dst;
-        if (s < c0) {
-            dst = head_part + (size_t)ch * D;          // run began in an earlier chunk
-        } else if (e > c1) {
-            dst = tail_part + (size_t)ch * D;          // run starts here, continues later
-            cross_u = u;
-        } else {
-            dst = dE + (size_t)u * D;                   // whole run inside this chunk
-            if (accumulate) {
+        seg_scan<DM>(u, v);
+        const int nu_next = __shfl_down(u, 1, AMS_WAVE);
+        const bool run_end = valid && (lane == AMS_WAVE - 1 || nu_next != u);
+        int cross_u = -1;
+        if (run_end) {
+            const int s0 = uniq_off[u], e0 = uniq_off[u + 1];
+            float *dst;
+            if (s0 < c0) {
+                dst = head_part + (size_t)ch * D;          // run began in an earlier chunk
+            } else if (e0 > c1) {
+                dst = tail_part + (size_t)ch * D;          // run starts here, continues later
+                cross_u = u;
+            } else {
+                dst = dE + (size_t)u * D;                   // whole run inside this chunk
+                if (accumulate) {
 #pragma unroll
-                for (int d = 0; d < DM; ++d)
-                    if (d < D) v[d] += dst[d];
+                    for (int d = 0; d < DM; ++d)
+                        if (d < D) v[d] += dst[d];
+                }
             }
-        }
 #pragma unroll
-        for (int d = 0; d < DM; ++d)
-            if (d < D) dst[d] = v[d];
+            for (int d = 0; d < DM; ++d)
+                if (d < D) dst[d] = v[d];
+        }
+        // only lane 63 can end a run that continues past the chunk
+        const int cu = __shfl(cross_u, AMS_WAVE - 1, AMS_WAVE);
+        if (lane == 0) cross[ch] = cu;
     }
-    // only lane 63 can end a run that continues past the chunk
-    const int cu = __shfl(cross_u, AMS_WAVE - 1, AMS_WAVE);
-    if (lane == 0) cross[ch] = cu;
 }
 
-// (3) a run that starts in chunk ch and crosses chunk edges: tail part of ch,
-// then the head parts of the following chunks up to the run's last chunk.
+// A row of D floats read as DM/4 16-byte loads with no condition: D == DM
+// and 16-byte aligned rows (the fast path of the fix-up below).
 template <int DM>
-__global__ __launch_bounds__(kThreads) void pool_bwd_fix(int D, int nch, const int32_t *__restrict__ uniq_off,
-                                                         const int32_t *__restrict__ cross,
-                                                         const float *__restrict__ head_part,
-                                                         const float *__restrict__ tail_part,
-                                                         float *__restrict__ dE, int accumulate)
+__device__ __forceinline__ void load_row_full(const float *__restrict__ p, float (&e)[DM])
 {
+#pragma unroll
+    for (int d4 = 0; d4 < DM / 4; ++d4) {
+        const float4 v = *(const float4 *)(p + 4 * d4);
+        e[4 * d4] = v.x;
+        e[4 * d4 + 1] = v.y;
+        e[4 * d4 + 2] = v.z;
+        e[4 * d4 + 3] = v.w;
+    }
+}
+
+// Chunks per block of the head-part block sums.
+constexpr int kFixBlock = 512;
+
+// Sum of a wave's items: lane l adds items l, l + 64, ... in ascending order,
+// U rows in flight (the last group clamps its index and drops the extra
+// rows); then a butterfly over the lanes.  Lane d < D returns coordinate d.
+template <int DM, class Row>
+__device__ __forceinline__ float sum_items(int n_items, int D, bool full, Row row)
+{
+    constexpr int U = DM > 16 ? 4 : 8;
     const int lane = ams_lane();
-    const int ch = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
-    if (ch >= nch) return;
-    const int u = cross[ch];
-    if (u < 0) return;
-    const int last = (uniq_off[u + 1] - 1) / AMS_WAVE;
     float acc[DM];
 #pragma unroll
     for (int d = 0; d < DM; ++d) acc[d] = 0.f;
-    for (int c = ch + 1 + lane; c <= last; c += AMS_WAVE) {
-        float h[DM];
-        load_row<DM>(head_part, c, D, h);
+    for (int t0 = lane; t0 < n_items; t0 += U * AMS_WAVE) {
+        float h[U][DM];
 #pragma unroll
-        for (int d = 0; d < DM; ++d) acc[d] += h[d];
+        for (int q = 0; q < U; ++q) {
+            const float *rp = row(min(t0 + q * AMS_WAVE, n_items - 1));
+            if (full) load_row_full<DM>(rp, h[q]);
+            else load_row<DM>(rp, 0, D, h[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < U; ++q) {
+            const bool take = t0 + q * AMS_WAVE < n_items;
+#pragma unroll
+            for (int d = 0; d < DM; ++d) acc[d] += take ? h[q][d] : 0.f;
+        }
     }
     float mine = 0.f;
 #pragma unroll
@@ -483,31 +581,127 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_fix(int D, int nch, const i
         const float s = ams_wave_sum(acc[d]);
         if (lane == d) mine = s;
     }
-    if (lane < D) {
-        const float r = tail_part[(size_t)ch * D + lane] + mine;
-        dE[(size_t)u * D + lane] = accumulate ? dE[(size_t)u * D + lane] + r : r;
+    return mine;
+}
+
+// (3a) block sums of the head parts: bsum[b] = sum of the head parts of
+// chunks b*kFixBlock .. (b+1)*kFixBlock - 1.  Only blocks that lie inside
+// one run's head chunks are ever used, where every one of those head parts
+// was written.
+template <int DM>
+__global__ __launch_bounds__(kThreads) void pool_bwd_bsum(int D, int nch, bool full,
+                                                          const float *__restrict__ head_part,
+                                                          float *__restrict__ bsum)
+{
+    const int b = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
+    if (b >= nch / kFixBlock) return;                     // whole blocks only
+    const float *base = head_part + (size_t)b * kFixBlock * D;
+    const float s = sum_items<DM>(kFixBlock, D, full, [&](int t) { return base + (size_t)t * D; });
+    if (ams_lane() < D) bsum[(size_t)b * D + ams_lane()] = s;
+}
+
+// Head chunks a lane adds by itself in the fix-up.
+template <int DM>
+constexpr int fix_short() { return DM > 16 ? 2 : 4; }
+
+// (3b) a run that starts in chunk ch and crosses chunk edges: tail part of
+// ch, then the head parts of chunks ch + 1 .. last (the run's last chunk).
+// A wave looks at 64 consecutive chunks, one per lane.  A run with at most
+// fix_short head chunks is summed by its lane in order (tail, then heads).
+// Longer ones are taken by the whole wave, one after another, summing items
+// lane-strided: the head parts before the first whole block of kFixBlock
+// chunks inside the range, the block sums, the head parts after the last
+// one; so a hot image's run (thousands of chunks) costs the wave at most
+// 2 kFixBlock head parts and one block sum per block.
+template <int DM>
+__global__ __launch_bounds__(kThreads) void pool_bwd_fix(int D, int nch, bool full,
+                                                         const int32_t *__restrict__ uniq_off,
+                                                         const int32_t *__restrict__ cross,
+                                                         const float *__restrict__ head_part,
+                                                         const float *__restrict__ tail_part,
+                                                         const float *__restrict__ bsum,
+                                                         float *__restrict__ dE, int accumulate)
+{
+    constexpr int NS = fix_short<DM>();
+    const int lane = ams_lane();
+    const int ch0 = (blockIdx.x * kWaves + threadIdx.x / AMS_WAVE) * AMS_WAVE;
+    if (ch0 >= nch) return;
+    const int ch = ch0 + lane;
+    const int u = ch < nch ? cross[ch] : -1;
+    const int last = u >= 0 ? (uniq_off[u + 1] - 1) / AMS_WAVE : ch;
+    const int n = last - ch;                              // head chunks of the run
+    auto row = [&](const float *base, int r, float (&e)[DM]) {
+        if (full) load_row_full<DM>(base + (size_t)r * D, e);
+        else load_row<DM>(base, r, D, e);
+    };
+    if (u >= 0 && n <= NS) {
+        float t[DM], h[NS][DM];
+        row(tail_part, ch, t);
+#pragma unroll
+        for (int q = 0; q < NS; ++q) row(head_part, min(ch + 1 + q, last), h[q]);
+#pragma unroll
+        for (int q = 0; q < NS; ++q)
+#pragma unroll
+            for (int d = 0; d < DM; ++d) t[d] += q < n ? h[q][d] : 0.f;
+        float *dst = dE + (size_t)u * D;
+        if (accumulate) {
+            float o[DM];
+            load_row<DM>(dE, u, D, o);          // dE: the caller's buffer, any alignment
+#pragma unroll
+            for (int d = 0; d < DM; ++d) t[d] = o[d] + t[d];
+        }
+#pragma unroll
+        for (int d = 0; d < DM; ++d)
+            if (d < D) dst[d] = t[d];
+    }
+    uint64_t todo = __ballot(u >= 0 && n > NS);
+    while (todo) {
+        const int b = __builtin_ctzll(todo);
+        todo &= todo - 1;
+        const int cb = ch0 + b;
+        const int ub = __shfl(u, b, AMS_WAVE), lb = __shfl(last, b, AMS_WAVE);
+        const int first = cb + 1;
+        const int jb = (first + kFixBlock - 1) / kFixBlock, je = (lb + 1) / kFixBlock;
+        int n1 = lb - cb, n2 = 0, n3 = 0;
+        if (jb < je) {
+            n1 = jb * kFixBlock - first;
+            n2 = je - jb;
+            n3 = lb + 1 - je * kFixBlock;
+        }
+        const float s = sum_items<DM>(n1 + n2 + n3, D, full, [&](int t) {
+            if (t < n1) return head_part + (size_t)(first + t) * D;
+            if (t < n1 + n2) return bsum + (size_t)(jb + t - n1) * D;
+            return head_part + ((size_t)je * kFixBlock + (t - n1 - n2)) * D;
+        });
+        if (lane < D) {
+            const float r = tail_part[(size_t)cb * D + lane] + s;
+            dE[(size_t)ub * D + lane] = accumulate ? dE[(size_t)ub * D + lane] + r : r;
+        }
     }
 }
 
 size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 struct PoolPlan {
-    size_t off_samp, off_c, off_da, off_head, off_tail, off_cross, total;
+    size_t off_rec, off_c, off_da, off_head, off_tail, off_cross, off_bsum, total;
     int nch;
 };
 
-PoolPlan plan_pool(int32_t B, int64_t n_beh, int32_t D)
+// Workspace of the backward; the records are 16 bytes with attention
+// (ams_pool_workspace's AMS_POOL_ATT also covers the query mode), 8 without.
+PoolPlan plan_pool(bool wide, int32_t B, int64_t n_beh, int32_t D)
 {
     PoolPlan p{};
     const int64_t n_occ = n_beh + B;
     p.nch = (int)((n_occ + AMS_WAVE - 1) / AMS_WAVE);
     size_t o = 0;
-    p.off_samp = o; o += al256((size_t)n_beh * 4);
+    p.off_rec = o; o += al256((size_t)n_occ * (wide ? 16 : 8));
     p.off_c = o; o += al256((size_t)B * 4);
     p.off_da = o; o += al256((size_t)B * D * 4);
     p.off_head = o; o += al256((size_t)p.nch * D * 4);
     p.off_tail = o; o += al256((size_t)p.nch * D * 4);
     p.off_cross = o; o += al256((size_t)p.nch * 4);
+    p.off_bsum = o; o += al256((size_t)(p.nch / kFixBlock) * D * 4);
     p.total = o;
     return p;
 }
@@ -527,23 +721,32 @@ void launch_bwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32
                 char *ws, const PoolPlan &p, hipStream_t st, float *dQ = nullptr, int accumulate = 0,
                 int Lc = 0)
 {
-    int32_t *samp = (int32_t *)(ws + p.off_samp);
+    void *rec = ws + p.off_rec;
     float *cvec = (float *)(ws + p.off_c);
     // the attention term of each sample: the query's gradient in the query mode
     float *da = MODE == kPoolQuery ? dQ : (float *)(ws + p.off_da);
     float *head = (float *)(ws + p.off_head);
     float *tail = (float *)(ws + p.off_tail);
     int32_t *cross = (int32_t *)(ws + p.off_cross);
+    float *bsum = (float *)(ws + p.off_bsum);
     const int n_occ = (int)(n_beh + B);
+    // head and tail rows start at 256-byte boundaries, so rows of D == DM
+    // floats (D a multiple of 4) are 16-byte aligned
+    const bool full = D == DM;
     if (B > 0)
         AMS_LAUNCH("pool_bwd_sample", st, pool_bwd_sample<MODE, DM><<<(B + kWaves - 1) / kWaves, kThreads, 0, st>>>(
-            B, D, seg_off, inv, cap, E, U, (const float *)saved, dU, samp, cvec, da));
-    const int g = (p.nch + kWaves - 1) / kWaves;
-    AMS_LAUNCH("pool_bwd_seg", st, pool_bwd_seg<MODE, DM><<<g, kThreads, 0, st>>>(D, n_beh, n_occ, cap, inv, occ_perm, uniq_off, E, A, saved, dU,
-                                                   dA, samp, cvec, da, p.nch, dE, head, tail, cross, accumulate,
-                                                   seg_off, Lc));
-    AMS_LAUNCH("pool_bwd_fix", st, pool_bwd_fix<DM><<<g, kThreads, 0, st>>>(D, p.nch, uniq_off, cross, head, tail, dE,
-                                                                          accumulate));
+            B, D, seg_off, n_beh, inv, cap, E, U, (const float *)saved, dU, rec, cvec, da));
+    const int gs = (p.nch + kWaves * seg_cpw<MODE, DM>() - 1) / (kWaves * seg_cpw<MODE, DM>());
+    AMS_LAUNCH("pool_bwd_seg", st, pool_bwd_seg<MODE, DM><<<gs, kThreads, 0, st>>>(D, n_occ, cap, occ_perm, uniq_off, A,
+                                                   saved, dU, dA, rec, da, p.nch, dE, head, tail, cross,
+                                                   accumulate, seg_off, Lc));
+    const int nblk = p.nch / kFixBlock;
+    if (nblk > 0)
+        AMS_LAUNCH("pool_bwd_bsum", st, pool_bwd_bsum<DM><<<(nblk + kWaves - 1) / kWaves, kThreads, 0, st>>>(
+            D, p.nch, full, head, bsum));
+    const int gf = (p.nch + kWaves * AMS_WAVE - 1) / (kWaves * AMS_WAVE);
+    AMS_LAUNCH("pool_bwd_fix", st, pool_bwd_fix<DM><<<gf, kThreads, 0, st>>>(D, p.nch, full, uniq_off, cross, head, tail,
+                                                                          bsum, dE, accumulate));
 }
 
 ams_status check_common(int32_t mode, int32_t B, int32_t D, int64_t n_beh)
@@ -582,7 +785,7 @@ extern "C" size_t ams_pool_workspace(int32_t mode, int32_t B, int64_t n_beh, int
 {
     (void)n_uniq_cap;
     if (check_common(mode, B, D, n_beh) != AMS_OK) return 0;
-    return plan_pool(B, n_beh, D).total;
+    return plan_pool(mode == AMS_POOL_ATT, B, n_beh, D).total;
 }
 
 extern "C" ams_status ams_pool_bwd(int32_t mode, int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
@@ -600,7 +803,7 @@ extern "C" ams_status ams_pool_bwd(int32_t mode, int32_t B, int32_t D, const int
     if (!seg_off || !inv || !occ_perm || !uniq_off || !E || !dE) return AMS_ERR_NULL;
     if (B > 0 && (!U || !A || !dU)) return AMS_ERR_NULL;
     if (mode != AMS_POOL_SUM && B > 0 && !saved) return AMS_ERR_NULL;
-    const PoolPlan p = plan_pool(B, n_beh, D);
+    const PoolPlan p = plan_pool(mode == AMS_POOL_ATT, B, n_beh, D);
     if (!ws || ws_bytes < p.total) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     char *w = (char *)ws;
@@ -653,7 +856,7 @@ extern "C" ams_status ams_pool_query_bwd(int32_t B, int32_t D, const int32_t *se
     if (n_occ == 0) return AMS_OK;
     if (!seg_off || !inv || !occ_perm || !uniq_off || !E || !dE) return AMS_ERR_NULL;
     if (B > 0 && (!Q || !U || !w || !dU || !dQ)) return AMS_ERR_NULL;
-    const PoolPlan p = plan_pool(B, n_beh, D);
+    const PoolPlan p = plan_pool(true, B, n_beh, D);
     if (!ws || ws_bytes < p.total) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     char *wsc = (char *)ws;
@@ -695,7 +898,7 @@ extern "C" ams_status ams_pool_concat_bwd(int32_t B, int32_t D, int32_t Lc, cons
     if (n_occ == 0) return AMS_OK;
     if (!seg_off || !inv || !occ_perm || !uniq_off || !dE) return AMS_ERR_NULL;
     if (B > 0 && !dU) return AMS_ERR_NULL;
-    const PoolPlan p = plan_pool(B, n_beh, D);
+    const PoolPlan p = plan_pool(false, B, n_beh, D);
     if (!ws || ws_bytes < p.total) return AMS_ERR_WORKSPACE;
     hipStream_t st = (hipStream_t)stream;
     char *w = (char *)ws;

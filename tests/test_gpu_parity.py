@@ -254,6 +254,26 @@ def test_pool_fwd_bwd_match_oracle(mode, wname):
     assert_close(dE, pb["dE"], 1e-4, "dE")
 
 
+@pytest.mark.parametrize("mode", ["sum", "max", "att"])
+def test_pool_long_runs_match_oracle(mode):
+    """The long-sequence batch (754k behaviors): its hottest image's run of
+    the stable order spans over a thousand 64-position chunks, so the
+    backward's fix-up adds whole blocks of 512 chunks as block sums.  E is
+    seeded random (the embedding model is not under test here)."""
+    w = synth.get("c3_long")
+    batch = synth.make_batch(w)
+    dd = oracle.dedup(synth.occurrences(batch), w.n_images)
+    runs = np.diff(dd["uniq_off"])
+    assert runs.max() > 2 * 512 * 64                  # a run covering a whole block of chunks
+    E32 = (np.random.default_rng(11).standard_normal((dd["n_uniq"], w.out_dim)) * 0.5).astype(np.float32)
+    print(f"pool long runs {mode}: n_u={dd['n_uniq']} longest run={runs.max()}", flush=True)
+    pf = oracle.pool_fwd(mode, batch["seg_off"], dd["inv"], E32)
+    pb = oracle.pool_bwd(mode, batch["seg_off"], dd["inv"], dd["n_uniq"], E32, pf, batch["g_u"], batch["g_a"])
+    fwd, dE = gpu_pool(mode, batch, dd, E32, pf_orc=pf)
+    assert_close(fwd["U"], pf["U"], 1e-4, "U")
+    assert_close(dE, pb["dE"], 1e-4, "dE")
+
+
 @pytest.mark.parametrize("wname", ["tiny", "c1_f32", "c3_long"])
 def test_pool_bwd_sum_unit_gradient_is_exact_multiplicity(wname):
     w = synth.get(wname)
