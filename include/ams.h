@@ -202,7 +202,9 @@ ams_status ams_dedup_noalloc(const int32_t *ids, int64_t n_occ, int32_t n_ids,
  *                   and for 3 layers slope[1] [dims[2]], float32, none NULL):
  *                   PReLU, z for z > 0 and slope[c] z otherwise, a learnable
  *                   slope per channel (the activation of section 7.2).
- *                   AMS_F32 only (DTYPE in AMS_BF16 mode).
+ *                   AMS_F32 and AMS_F32_X3; AMS_BF16 with dims[1] = 256 and,
+ *                   for 3 layers, dims[2] a multiple of 4 with dims[2]*D <=
+ *                   1024 (the bf16 tails): other bf16 shapes return DTYPE.
  * H1_save           out, optional: first hidden layer [cap x dims[1]] (bf16 in
  *                   AMS_BF16 mode, float32 otherwise): post-ReLU, or with
  *                   PReLU the pre-activation Z1 (bias included).  Needed by

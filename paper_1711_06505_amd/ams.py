@@ -199,7 +199,7 @@ def ams_embed_workspace(mlp: ams_mlp, n_uniq_cap: int) -> int:
 
 
 def ams_embed_fwd(mlp, T, uniq, n_uniq, n_uniq_cap, W, b, H1_save, H2_save, E, ws, stream=None, slopes=None):
-    """slopes: None (ReLU) or the PReLU slopes of every hidden layer (float32 mode)."""
+    """slopes: None (ReLU) or the PReLU slopes of every hidden layer."""
     W3 = W[2] if len(W) > 2 else None
     b3 = b[2] if len(b) > 2 else None
     _check(load().ams_embed_fwd(ctypes.byref(mlp), _p(T), T.shape[0], _p(uniq), _p(n_uniq),
@@ -414,9 +414,10 @@ class Step:
     can be exceeded by a batch with more distinct images: the kernels then
     stay inside the buffers and the results are unspecified, so such a Step
     is only built with ``cap_checked=True``, by a caller that checks
-    `capacity_ok()` after its steps.  With `prelu` (float32 models) the
-    hidden layers use PReLU: the slopes are passed to run / embed_fwd /
-    embed_bwd and their gradients land in `dslope`.
+    `capacity_ok()` after its steps.  With `prelu` the hidden layers use
+    PReLU (float32 models, and bf16 ones whose first hidden layer is 256
+    wide): the slopes are passed to run / embed_fwd / embed_bwd and their
+    gradients land in `dslope`.
     """
 
     def __init__(self, dims, dtype: str, mode: str, B: int, n_beh_max: int, final_relu: bool = False,

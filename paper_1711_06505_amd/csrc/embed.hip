@@ -699,12 +699,13 @@ __device__ __forceinline__ void rs_compute(const char *slot, const u32x4 (&av)[4
     __builtin_amdgcn_sched_group_barrier(0x008, RA, 0);
 }
 
-// H1b / H1lo: the bf16 rounding of H1 = ReLU(Z1 + b1) and the bf16 rounding
-// of what it leaves out (the tail's fp32-level layer-2 operand).
+// H1b / H1lo: the bf16 rounding of H1 = ReLU(Z1 + b1) (keep_z: of Z1 + b1,
+// the pre-activation PReLU keeps) and the bf16 rounding of what it leaves
+// out (the tail's fp32-level layer-2 operand).
 __global__ __launch_bounds__(rs::kThreads) __attribute__((amdgpu_waves_per_eu(rs::kWavesPerSimd, rs::kWavesPerSimd))) void l1rs_bf16(
     const uint16_t *__restrict__ T, int64_t n_rows, const int32_t *__restrict__ uniq,
     const int32_t *__restrict__ n_uniq_p, int cap, const uint16_t *__restrict__ W1, const float *__restrict__ b1,
-    int G, uint16_t *__restrict__ H1b, uint16_t *__restrict__ H1lo)
+    int G, uint16_t *__restrict__ H1b, uint16_t *__restrict__ H1lo, int keep_z)
 {
     using namespace rs;
     __shared__ __attribute__((aligned(256))) char ring[R * SLOT];
@@ -795,7 +796,8 @@ __global__ __launch_bounds__(rs::kThreads) __attribute__((amdgpu_waves_per_eu(rs
             uint16_t *pl = hl + dr * BN;
 #pragma unroll
             for (int nb = 0; nb < 8; ++nb) {
-                const float z = fmaxf(rok ? acc[nb][j] + bias[nb] : bias[nb], 0.f);
+                const float z0 = rok ? acc[nb][j] + bias[nb] : bias[nb];
+                const float z = keep_z ? z0 : fmaxf(z0, 0.f);
                 const uint16_t hi = ams_f32_to_bf16(z);
                 pb[nb * 32] = hi;
                 pl[nb * 32] = ams_f32_to_bf16(z - ams_bf16_to_f32(hi));
@@ -1406,6 +1408,19 @@ __device__ __forceinline__ uint32_t pack_bf16(float a, float b)
     return (uint32_t)ams_f32_to_bf16(a) | ((uint32_t)ams_f32_to_bf16(b) << 16);
 }
 
+// The eight fp32 values hi + lo of a pair of bf16x8 operands.
+__device__ __forceinline__ void join8(uint4 hi, uint4 lo, float (&x)[8])
+{
+    const uint32_t h[4] = {hi.x, hi.y, hi.z, hi.w}, l[4] = {lo.x, lo.y, lo.z, lo.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        const uint32_t hw = h[e >> 1], lw = l[e >> 1];
+        const float a = __uint_as_float((e & 1) ? (hw & 0xffff0000u) : (hw << 16));
+        const float b = __uint_as_float((e & 1) ? (lw & 0xffff0000u) : (lw << 16));
+        x[e] = a + b;
+    }
+}
+
 // hi/lo split of 8 fp32 values into two bf16x8 operands
 __device__ __forceinline__ void split8(const float (&x)[8], uint4 &hi, uint4 &lo)
 {
@@ -1421,8 +1436,12 @@ __device__ __forceinline__ void split8(const float (&x)[8], uint4 &hi, uint4 &lo
     lo = make_uint4(pack_bf16(r[0], r[1]), pack_bf16(r[2], r[3]), pack_bf16(r[4], r[5]), pack_bf16(r[6], r[7]));
 }
 
-template <int L>
-__global__ __launch_bounds__(kThreads) void tail_fwd_bf16(uint16_t *__restrict__ H1b,
+// PR: PReLU between the layers with per-channel slopes s1 [H] and s2 [M]
+// (3 layers).  H1b / H1lo then hold Z1 (split tiles: stored here) and the
+// layer-2 operand is the fp32 activation re-split into hi / lo; H2_save holds
+// Z2 and the layer-3 operand is its activation.
+template <int L, bool PR>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void tail_fwd_bf16(uint16_t *__restrict__ H1b,
                                                           const uint16_t *__restrict__ H1lo,
                                                           const float *__restrict__ pbuf, int F, int G,
                                                           const float *__restrict__ b1,
@@ -1432,12 +1451,14 @@ __global__ __launch_bounds__(kThreads) void tail_fwd_bf16(uint16_t *__restrict__
                                                           const uint16_t *__restrict__ W3,
                                                           const float *__restrict__ b3, int final_relu,
                                                           const int32_t *__restrict__ n_uniq_p, int cap,
-                                                          float *__restrict__ H2_save, float *__restrict__ E)
+                                                          float *__restrict__ H2_save, float *__restrict__ E,
+                                                          const float *__restrict__ s1, const float *__restrict__ s2)
 {
     constexpr int H = kMaxH1;
     constexpr int KS = H / 16;                 // k steps
     __shared__ __attribute__((aligned(16))) uint16_t W2s[kMaxH2 * kMaxH1];
     __shared__ __attribute__((aligned(16))) uint16_t W3s[32 * kW3S];
+    __shared__ __attribute__((aligned(16))) float S1s[PR ? H : 4];      // layer 1's slopes
     const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
     const int h = lane >> 5, r32 = lane & 31;
     const int Mo = (L == 3) ? M : D;           // width of the second layer's output
@@ -1471,20 +1492,24 @@ __global__ __launch_bounds__(kThreads) void tail_fwd_bf16(uint16_t *__restrict__
             if (e < 32 * kW3S) W3s[e] = v[i];
         }
     }
-    // this lane's outputs o = 32 ob + 8 q + 4 h + r and their biases
-    float bias[2][16];
+    if (PR)
+        for (int i = t; i < H; i += kThreads) S1s[i] = s1[i];
+    // this lane's outputs o = 32 ob + 8 q + 4 h + r, their biases and (PReLU,
+    // 3 layers) slopes
+    float bias[2][16], sl2[2][16];
 #pragma unroll
     for (int ob = 0; ob < 2; ++ob)
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             const int o = 32 * ob + acc_row(j, lane);
             bias[ob][j] = o < Mo ? b2[o] : 0.f;
+            sl2[ob][j] = (PR && L == 3 && o < M) ? s2[o] : 0.f;
         }
     __syncthreads();
 
     const int n_u = min(*n_uniq_p, cap);
     if (n_u <= 0) return;
-    const bool relu2 = (L == 3) || final_relu;
+    const bool relu2 = (L == 3 && !PR) || (L == 2 && final_relu);
     using K = Sk<uint16_t>;
     const SkPlan P = sk_plan(n_u, H, F, G, sk_bk<uint16_t>(), K::BM);
     for (int c0 = (blockIdx.x * (kThreads / AMS_WAVE) + wave) * 32; c0 < n_u;
@@ -1533,7 +1558,10 @@ __global__ __launch_bounds__(kThreads) void tail_fwd_bf16(uint16_t *__restrict__
                     const float4 c0v = *(const float4 *)&b1[k0], c1v = *(const float4 *)&b1[k0 + 4];
                     const float bb[8] = {c0v.x, c0v.y, c0v.z, c0v.w, c1v.x, c1v.y, c1v.z, c1v.w};
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) x[e] = fmaxf(id_ok ? x[e] + bb[e] : bb[e], 0.f);
+                    for (int e = 0; e < 8; ++e) {
+                        x[e] = id_ok ? x[e] + bb[e] : bb[e];
+                        if (!PR) x[e] = fmaxf(x[e], 0.f);
+                    }
                     split8(x, bh[s4], bl[s4]);
                     if (live) *(uint4 *)(H1b + (size_t)row * H + k0) = bh[s4];
                 }
@@ -1542,6 +1570,19 @@ __global__ __launch_bounds__(kThreads) void tail_fwd_bf16(uint16_t *__restrict__
                 for (int s4 = 0; s4 < KS / 4; ++s4) {
                     bh[s4] = *(const uint4 *)(H1b + roff + 16 * (qt * (KS / 4) + s4));
                     bl[s4] = *(const uint4 *)(H1lo + roff + 16 * (qt * (KS / 4) + s4));
+                }
+            }
+            if (PR) {   // the operand: PReLU(Z1) in fp32, split again
+#pragma unroll
+                for (int s4 = 0; s4 < KS / 4; ++s4) {
+                    const int k0 = 16 * (qt * (KS / 4) + s4) + 8 * h;
+                    float x[8];
+                    join8(bh[s4], bl[s4], x);
+                    const float4 a0 = *(const float4 *)&S1s[k0], a1 = *(const float4 *)&S1s[k0 + 4];
+                    const float a[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) x[e] = x[e] > 0.f ? x[e] : a[e] * x[e];
+                    split8(x, bh[s4], bl[s4]);
                 }
             }
 #pragma unroll
@@ -1593,6 +1634,13 @@ __global__ __launch_bounds__(kThreads) void tail_fwd_bf16(uint16_t *__restrict__
                     for (int e = 0; e < 4; ++e) {
                         x[e] = z[ob][8 * p + e];           // o = 32 ob + 16 p + 4 h + e
                         x[4 + e] = z[ob][8 * p + 4 + e];   // o = 32 ob + 16 p + 8 + 4 h + e
+                    }
+                    if (PR) {                              // Z2 -> H2
+#pragma unroll
+                        for (int e = 0; e < 4; ++e) {
+                            x[e] = x[e] > 0.f ? x[e] : sl2[ob][8 * p + e] * x[e];
+                            x[4 + e] = x[4 + e] > 0.f ? x[4 + e] : sl2[ob][8 * p + 4 + e] * x[4 + e];
+                        }
                     }
                     uint4 hi, lo;
                     split8(x, hi, lo);
@@ -2566,14 +2614,19 @@ __device__ __forceinline__ float bf16_elem(uint2 v, int r)
 }
 
 // DM: upper bound of D (16 or 32), the length of the per-thread dzl rows.
-template <int L, int DM>
+// PR: PReLU with slopes s1 [H], s2 [M] (3 layers): H1b holds Z1 and H2s Z2;
+// the masks become 1 / slope, the dW2 and dW3 operands are the activations
+// (dW2's re-rounded to bf16 from Z1's bf16), and the slope gradients
+// sum dH * min(Z, 0) go to the two partial slots after db1.
+template <int L, int DM, bool PR>
 __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2)))
 void tail_bwd_bf16(const uint16_t *__restrict__ H1b, const float *__restrict__ H2s,
                    const float *__restrict__ Efwd, const float *__restrict__ dE,
                    const uint16_t *__restrict__ W2, const uint16_t *__restrict__ W3, int M, int D,
                    int final_relu, const int32_t *__restrict__ n_uniq_p, int cap,
                    uint16_t *__restrict__ dZ1, float *__restrict__ part, int PS,
-                   float *__restrict__ zero_row, int zero_n)
+                   float *__restrict__ zero_row, int zero_n,
+                   const float *__restrict__ s1, const float *__restrict__ s2)
 {
     constexpr int H = kMaxH1;
     __shared__ __attribute__((aligned(16))) char H1t[32 * kH1S];      // H1, then dZ1, of the chunk
@@ -2610,6 +2663,10 @@ void tail_bwd_bf16(const uint16_t *__restrict__ H1b, const float *__restrict__ H
         }
     }
     const int po = t & 63, pg = t >> 6;        // phase-A role: output o, row group
+    const float sl2 = (PR && L == 3 && po < M) ? s2[po] : 0.f;
+    float sl1[2];                              // slopes of phase B's columns 64 wave + 32 ib + r32
+#pragma unroll
+    for (int ib = 0; ib < 2; ++ib) sl1[ib] = PR ? s1[64 * wave + 32 * ib + r32] : 0.f;
     float w3c[DM];                             // W3[:, po] (3 layers)
 #pragma unroll
     for (int d = 0; d < DM; ++d) w3c[d] = (L == 3 && d < D && po < M) ? ams_bf16_to_f32(W3[d * M + po]) : 0.f;
@@ -2619,8 +2676,8 @@ void tail_bwd_bf16(const uint16_t *__restrict__ H1b, const float *__restrict__ H
     const int r1 = (int)((int64_t)(blockIdx.x + 1) * n_u / gridDim.x);
 
     v16f dw2[2][2] = {{(v16f){}, (v16f){}}, {(v16f){}, (v16f){}}};   // [o block][i block]
-    float db1a[2] = {0.f, 0.f};
-    float db2p = 0.f, db3p = 0.f;
+    float db1a[2] = {0.f, 0.f}, ds1a[2] = {0.f, 0.f};
+    float db2p = 0.f, db3p = 0.f, ds2p = 0.f;
     float dw3a[DM];
 #pragma unroll
     for (int d = 0; d < DM; ++d) dw3a[d] = 0.f;
@@ -2707,10 +2764,17 @@ void tail_bwd_bf16(const uint16_t *__restrict__ H1b, const float *__restrict__ H
                 float a = 0.f;
 #pragma unroll
                 for (int d = 0; d < DM; ++d) a = fmaf(zl[d], w3c[d], a);
-                const float h2 = H2t[rr * kMaxH2 + po];
-                dz2 = h2 > 0.f ? a : 0.f;
+                const float h2 = H2t[rr * kMaxH2 + po];      // PReLU: Z2
+                float act = h2;
+                if (PR) {
+                    dz2 = h2 > 0.f ? a : sl2 * a;
+                    ds2p += h2 > 0.f ? 0.f : a * h2;
+                    act = h2 > 0.f ? h2 : sl2 * h2;
+                } else {
+                    dz2 = h2 > 0.f ? a : 0.f;
+                }
 #pragma unroll
-                for (int d = 0; d < DM; ++d) dw3a[d] = fmaf(zl[d], h2, dw3a[d]);
+                for (int d = 0; d < DM; ++d) dw3a[d] = fmaf(zl[d], act, dw3a[d]);
             } else {
                 dz2 = 0.f;
 #pragma unroll
@@ -2748,17 +2812,29 @@ void tail_bwd_bf16(const uint16_t *__restrict__ H1b, const float *__restrict__ H
 #pragma unroll
             for (int ib = 0; ib < 2; ++ib) {
                 const int icol = i0 + 32 * ib + r32;
-                float cs = 0.f;
+                float cs = 0.f, css = 0.f;
 #pragma unroll
-                for (int q = 0; q < 4; ++q)
+                for (int q = 0; q < 4; ++q) {
+                    float av[4];               // PReLU: the activation, dW2's operand
 #pragma unroll
                     for (int r = 0; r < 4; ++r) {
-                        const float dz = bf16_elem(hv[ib][q], r) > 0.f ? acc[ib][4 * q + r] : 0.f;
+                        const float z1 = bf16_elem(hv[ib][q], r), g = acc[ib][4 * q + r];
+                        float dz;
+                        if (PR) {
+                            dz = z1 > 0.f ? g : sl1[ib] * g;
+                            css += z1 > 0.f ? 0.f : g * z1;
+                            av[r] = z1 > 0.f ? z1 : sl1[ib] * z1;
+                        } else {
+                            dz = z1 > 0.f ? g : 0.f;
+                        }
                         cs += dz;
                         // this wave's own columns of the H1 tile now hold dZ1
                         *(uint16_t *)(H1t + (8 * q + 4 * h + r) * kH1S + icol * 2) = ams_f32_to_bf16(dz);
                     }
+                    if (PR) hv[ib][q] = make_uint2(pack_bf16(av[0], av[1]), pack_bf16(av[2], av[3]));
+                }
                 db1a[ib] += cs + __shfl_xor(cs, 32, AMS_WAVE);
+                if (PR) ds1a[ib] += css + __shfl_xor(css, 32, AMS_WAVE);
             }
 #pragma unroll
             for (int s = 0; s < 2; ++s) {
@@ -2831,6 +2907,20 @@ void tail_bwd_bf16(const uint16_t *__restrict__ H1b, const float *__restrict__ H
     if (h == 0) {
         p[i0 + r32] = db1a[0];
         p[i0 + 32 + r32] = db1a[1];
+    }
+    if (PR) {   // slope gradients: [H], then [M] from the four row groups in a fixed order
+        p += H;
+        if (h == 0) {
+            p[i0 + r32] = ds1a[0];
+            p[i0 + 32 + r32] = ds1a[1];
+        }
+        p += H;
+        if (L == 3) {
+            __syncthreads();
+            H2t[t] = ds2p;
+            __syncthreads();
+            if (t < M) p[t] = ((H2t[t] + H2t[64 + t]) + H2t[128 + t]) + H2t[192 + t];
+        }
     }
 }
 
@@ -2953,12 +3043,13 @@ extern "C" size_t ams_embed_workspace(const ams_mlp *mlp, int32_t n_uniq_cap)
 }
 
 // PReLU slopes of the hidden layers: NULL (ReLU), or one array per hidden
-// layer, float32 path only.
+// layer.  float32 paths, and bf16 where the bf16 tails run both directions
+// (first layer 256 wide: stream-K or row-split).
 ams_status prelu_slopes(const ams_mlp *mlp, const float *const *slope, const float **s1, const float **s2)
 {
     *s1 = *s2 = nullptr;
     if (!slope) return AMS_OK;
-    if (mlp->dtype == AMS_BF16) return AMS_ERR_DTYPE;
+    if (mlp->dtype == AMS_BF16 && !(use_stream_k(mlp) && use_tail_bf16(mlp))) return AMS_ERR_DTYPE;
     for (int l = 0; l < mlp->n_layers - 1; ++l)
         if (!slope[l]) return AMS_ERR_NULL;
     *s1 = slope[0];
@@ -3025,12 +3116,13 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
                                                                       (int)pr));
     } else if (sk && use_row_split(mlp, cap)) {
         AMS_LAUNCH("l1rs_bf16", st, l1rs_bf16<<<G, rs::kThreads, 0, st>>>((const uint16_t *)T, n_rows, uniq, n_uniq,
-                                                                        cap, (const uint16_t *)W1, b1, G, h1b, h1lo));
+                                                                        cap, (const uint16_t *)W1, b1, G, h1b, h1lo,
+                                                                        (int)pr));
         pbuf = nullptr;
     } else if (sk) {
         AMS_LAUNCH("l1sk_bf16", st, l1sk<uint16_t><<<G, kSkThreads, 0, st>>>((const uint16_t *)T, n_rows, F, uniq, n_uniq,
                                                                            cap, (const uint16_t *)W1, b1, H, G, nullptr,
-                                                                           h1b, h1lo, pbuf, 0));
+                                                                           h1b, h1lo, pbuf, (int)pr));
     } else if (!bf) {
         if (NT == 128)
             AMS_LAUNCH("l1_fwd_f32", st, l1_fwd_f32<128><<<grid, kThreads, 0, st>>>((const float *)T, n_rows, F, uniq, n_uniq, cap, n_mt,
@@ -3053,15 +3145,16 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
         // way); two resident blocks per CU stage W2 once and loop over chunks
         int tg = (cap + 4 * 32 - 1) / (4 * 32);
         if (tg > 2 * G) tg = 2 * G;
-        if (L == 3)
-            AMS_LAUNCH("tail_fwd_bf16", st, tail_fwd_bf16<3><<<tg, kThreads, 0, st>>>(
-                                                h1b, h1lo, pbuf, F, G, b1, uniq, n_rows, M, D, (const uint16_t *)W2,
-                                                b2, (const uint16_t *)W3, b3, mlp->final_relu, n_uniq, cap, H2_save,
-                                                E));
-        else
-            AMS_LAUNCH("tail_fwd_bf16", st, tail_fwd_bf16<2><<<tg, kThreads, 0, st>>>(
-                                                h1b, h1lo, pbuf, F, G, b1, uniq, n_rows, M, D, (const uint16_t *)W2,
-                                                b2, nullptr, nullptr, mlp->final_relu, n_uniq, cap, H2_save, E));
+#define TFB_LAUNCH(LL, PRV)                                                                                \
+    AMS_LAUNCH("tail_fwd_bf16", st, (tail_fwd_bf16<LL, PRV><<<tg, kThreads, 0, st>>>(                        \
+                                        h1b, h1lo, pbuf, F, G, b1, uniq, n_rows, M, D, (const uint16_t *)W2, \
+                                        b2, LL == 3 ? (const uint16_t *)W3 : nullptr, LL == 3 ? b3 : nullptr, \
+                                        mlp->final_relu, n_uniq, cap, H2_save, E, s1, s2)))
+        if (L == 3 && pr) TFB_LAUNCH(3, true);
+        else if (L == 3) TFB_LAUNCH(3, false);
+        else if (pr) TFB_LAUNCH(2, true);
+        else TFB_LAUNCH(2, false);
+#undef TFB_LAUNCH
         return ams_launch_status();
     }
     // K per stream-K stage, which fixes the plan the tail reads the partial
@@ -3137,15 +3230,22 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
                                    F > H ? F : H, s1, s2)))
     const int TG = tail_blocks(mlp);
     if (use_tail_bf16(mlp)) {
-#define TBF_LAUNCH(LL, DM)                                                                              \
-    AMS_LAUNCH("tail_bwd_bf16", st, (tail_bwd_bf16<LL, DM><<<TG, kThreads, 0, st>>>(                     \
+#define TBF_LAUNCH(LL, DM, PRV)                                                                         \
+    AMS_LAUNCH("tail_bwd_bf16", st, (tail_bwd_bf16<LL, DM, PRV><<<TG, kThreads, 0, st>>>(                \
                                         (const uint16_t *)H1_save, H2_save, E_fwd, dE, (const uint16_t *)W2, \
                                         (const uint16_t *)W3, M, D, mlp->final_relu, n_uniq, cap,          \
-                                        (uint16_t *)dz1, tail, PS, zero, F > H ? F : H)))
-        if (L == 3 && D <= 16) TBF_LAUNCH(3, 16);
-        else if (L == 3) TBF_LAUNCH(3, 32);
-        else if (D <= 16) TBF_LAUNCH(2, 16);
-        else TBF_LAUNCH(2, 32);
+                                        (uint16_t *)dz1, tail, PS, zero, F > H ? F : H, s1, s2)))
+        if (pr) {
+            if (L == 3 && D <= 16) TBF_LAUNCH(3, 16, true);
+            else if (L == 3) TBF_LAUNCH(3, 32, true);
+            else if (D <= 16) TBF_LAUNCH(2, 16, true);
+            else TBF_LAUNCH(2, 32, true);
+        } else {
+            if (L == 3 && D <= 16) TBF_LAUNCH(3, 16, false);
+            else if (L == 3) TBF_LAUNCH(3, 32, false);
+            else if (D <= 16) TBF_LAUNCH(2, 16, false);
+            else TBF_LAUNCH(2, 32, false);
+        }
 #undef TBF_LAUNCH
     } else if (L == 3 && bf) {
         TB_LAUNCH(3, uint16_t, uint16_t, false);

@@ -384,7 +384,7 @@ __device__ __forceinline__ void seg_scan(int u, float (&v)[DM])
 template <int MODE, int DM>
 constexpr int seg_cpw() { return DM > 16 || MODE == AMS_POOL_MAX ? 2 : 4; }
 
-template <int MODE, int DM>
+template <int MODE, int DM, int CPW>
 __global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int n_occ, int cap,
                                                          const int32_t *__restrict__ occ_perm,
                                                          const int32_t *__restrict__ uniq_off,
@@ -400,7 +400,6 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_seg(int D, int n_occ, int c
                                                          int32_t *__restrict__ cross, int accumulate,
                                                          const int32_t *__restrict__ seg_off, int Lc)
 {
-    constexpr int CPW = seg_cpw<MODE, DM>();
     constexpr bool ATT = MODE == AMS_POOL_ATT || MODE == kPoolQuery;
     const int lane = ams_lane();
     const int ch0 = (blockIdx.x * kWaves + threadIdx.x / AMS_WAVE) * CPW;
@@ -560,6 +559,16 @@ __device__ __forceinline__ float sum_items(int n_items, int D, bool full, Row ro
     float acc[DM];
 #pragma unroll
     for (int d = 0; d < DM; ++d) acc[d] = 0.f;
+    if (n_items <= AMS_WAVE) {                  // one item per lane at most: one load each
+        const float *rp = row(min(lane, n_items - 1));
+        if (full) load_row_full<DM>(rp, acc);
+        else load_row<DM>(rp, 0, D, acc);
+        if (lane >= n_items) {
+#pragma unroll
+            for (int d = 0; d < DM; ++d) acc[d] = 0.f;
+        }
+        n_items = 0;                            // (the loop below does nothing)
+    }
     for (int t0 = lane; t0 < n_items; t0 += U * AMS_WAVE) {
         float h[U][DM];
 #pragma unroll
@@ -604,15 +613,87 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_bsum(int D, int nch, bool f
 template <int DM>
 constexpr int fix_short() { return DM > 16 ? 2 : 4; }
 
-// (3b) a run that starts in chunk ch and crosses chunk edges: tail part of
-// ch, then the head parts of chunks ch + 1 .. last (the run's last chunk).
-// A wave looks at 64 consecutive chunks, one per lane.  A run with at most
-// fix_short head chunks is summed by its lane in order (tail, then heads).
-// Longer ones are taken by the whole wave, one after another, summing items
-// lane-strided: the head parts before the first whole block of kFixBlock
-// chunks inside the range, the block sums, the head parts after the last
-// one; so a hot image's run (thousands of chunks) costs the wave at most
-// 2 kFixBlock head parts and one block sum per block.
+// Below this many 64-position chunks the backward runs one chunk per wave
+// (stable-order pass and fix-up): the grid is then small enough that more
+// waves, not longer ones, keep the part busy.
+constexpr int kSmallChunks = 16384;
+
+// (3b) the fix-up of a run that starts in chunk ch and crosses chunk edges:
+// tail part of ch plus the sum of the head parts of chunks ch + 1 .. last
+// (the run's last chunk).  A wave sums items lane-strided, then by the
+// butterfly of ams_wave_sum: the head parts before the first whole block of
+// kFixBlock chunks inside the range, the block sums, the head parts after
+// the last one (a hot image's run of thousands of chunks costs at most
+// 2 kFixBlock head parts and one block sum per block).  In the large-grid
+// kernel a run of at most fix_short head chunks is summed by one lane in the
+// butterfly's association, (h0 + h2) + (h1 + h3), so which kernel or path
+// takes a run changes nothing in its sum.
+template <int DM>
+__device__ __forceinline__ void fix_one_lane(int D, bool full, int ch, int u, int last,
+                                             const float *__restrict__ head_part,
+                                             const float *__restrict__ tail_part, float *__restrict__ dE,
+                                             int accumulate)
+{
+    constexpr int NS = fix_short<DM>();
+    auto row = [&](const float *base, int r, float (&e)[DM]) {
+        if (full) load_row_full<DM>(base + (size_t)r * D, e);
+        else load_row<DM>(base, r, D, e);
+    };
+    static_assert(NS == 2 || NS == 4, "the butterfly's association below");
+    const int n = last - ch;
+    float t[DM], h[NS][DM];
+    row(tail_part, ch, t);
+#pragma unroll
+    for (int q = 0; q < NS; ++q) row(head_part, min(ch + 1 + q, last), h[q]);
+#pragma unroll
+    for (int q = 0; q < NS; ++q)
+#pragma unroll
+        for (int d = 0; d < DM; ++d) h[q][d] = q < n ? h[q][d] : 0.f;
+#pragma unroll
+    for (int d = 0; d < DM; ++d) {
+        const float sh = NS == 4 ? (h[0][d] + h[NS / 2][d]) + (h[1][d] + h[NS - 1][d]) : h[0][d] + h[1][d];
+        t[d] = t[d] + sh;
+    }
+    float *dst = dE + (size_t)u * D;
+    if (accumulate) {
+        float o[DM];
+        load_row<DM>(dE, u, D, o);              // dE: the caller's buffer, any alignment
+#pragma unroll
+        for (int d = 0; d < DM; ++d) t[d] = o[d] + t[d];
+    }
+#pragma unroll
+    for (int d = 0; d < DM; ++d)
+        if (d < D) dst[d] = t[d];
+}
+
+template <int DM>
+__device__ __forceinline__ void fix_one_wave(int D, bool full, int cb, int ub, int lb,
+                                             const float *__restrict__ head_part,
+                                             const float *__restrict__ tail_part,
+                                             const float *__restrict__ bsum, float *__restrict__ dE,
+                                             int accumulate)
+{
+    const int first = cb + 1;
+    const int jb = (first + kFixBlock - 1) / kFixBlock, je = (lb + 1) / kFixBlock;
+    int n1 = lb - cb, n2 = 0, n3 = 0;
+    if (jb < je) {
+        n1 = jb * kFixBlock - first;
+        n2 = je - jb;
+        n3 = lb + 1 - je * kFixBlock;
+    }
+    const float s = sum_items<DM>(n1 + n2 + n3, D, full, [&](int t) {
+        if (t < n1) return head_part + (size_t)(first + t) * D;
+        if (t < n1 + n2) return bsum + (size_t)(jb + t - n1) * D;
+        return head_part + ((size_t)je * kFixBlock + (t - n1 - n2)) * D;
+    });
+    const int lane = ams_lane();
+    if (lane < D) {
+        const float r = tail_part[(size_t)cb * D + lane] + s;
+        dE[(size_t)ub * D + lane] = accumulate ? dE[(size_t)ub * D + lane] + r : r;
+    }
+}
+
+// One wave per chunk (small grids).
 template <int DM>
 __global__ __launch_bounds__(kThreads) void pool_bwd_fix(int D, int nch, bool full,
                                                          const int32_t *__restrict__ uniq_off,
@@ -622,62 +703,51 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_fix(int D, int nch, bool fu
                                                          const float *__restrict__ bsum,
                                                          float *__restrict__ dE, int accumulate)
 {
-    constexpr int NS = fix_short<DM>();
-    const int lane = ams_lane();
-    const int ch0 = (blockIdx.x * kWaves + threadIdx.x / AMS_WAVE) * AMS_WAVE;
-    if (ch0 >= nch) return;
-    const int ch = ch0 + lane;
+    const int ch = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
+    if (ch >= nch) return;
+    const int u = cross[ch];
+    if (u < 0) return;
+    const int last = (uniq_off[u + 1] - 1) / AMS_WAVE;
+    fix_one_wave<DM>(D, full, ch, u, last, head_part, tail_part, bsum, dE, accumulate);
+}
+
+// 64 chunks per wave, one per lane (large grids): short runs by their lanes;
+// the block's long runs gathered in LDS and shared out over its waves.
+template <int DM>
+__global__ __launch_bounds__(kThreads) void pool_bwd_fix64(int D, int nch, bool full,
+                                                           const int32_t *__restrict__ uniq_off,
+                                                           const int32_t *__restrict__ cross,
+                                                           const float *__restrict__ head_part,
+                                                           const float *__restrict__ tail_part,
+                                                           const float *__restrict__ bsum,
+                                                           float *__restrict__ dE, int accumulate)
+{
+    __shared__ int lr_ch[kWaves * AMS_WAVE], lr_u[kWaves * AMS_WAVE], lr_last[kWaves * AMS_WAVE];
+    __shared__ int lr_cnt[kWaves];
+    const int lane = ams_lane(), wave = threadIdx.x / AMS_WAVE;
+    const int ch = (blockIdx.x * kWaves + wave) * AMS_WAVE + lane;
     const int u = ch < nch ? cross[ch] : -1;
     const int last = u >= 0 ? (uniq_off[u + 1] - 1) / AMS_WAVE : ch;
-    const int n = last - ch;                              // head chunks of the run
-    auto row = [&](const float *base, int r, float (&e)[DM]) {
-        if (full) load_row_full<DM>(base + (size_t)r * D, e);
-        else load_row<DM>(base, r, D, e);
-    };
-    if (u >= 0 && n <= NS) {
-        float t[DM], h[NS][DM];
-        row(tail_part, ch, t);
+    const bool is_long = u >= 0 && last - ch > fix_short<DM>();
+    if (u >= 0 && !is_long) fix_one_lane<DM>(D, full, ch, u, last, head_part, tail_part, dE, accumulate);
+    const uint64_t todo = __ballot(is_long);
+    if (lane == 0) lr_cnt[wave] = __popcll(todo);
+    __syncthreads();
+    int off = 0, tot = 0;
 #pragma unroll
-        for (int q = 0; q < NS; ++q) row(head_part, min(ch + 1 + q, last), h[q]);
-#pragma unroll
-        for (int q = 0; q < NS; ++q)
-#pragma unroll
-            for (int d = 0; d < DM; ++d) t[d] += q < n ? h[q][d] : 0.f;
-        float *dst = dE + (size_t)u * D;
-        if (accumulate) {
-            float o[DM];
-            load_row<DM>(dE, u, D, o);          // dE: the caller's buffer, any alignment
-#pragma unroll
-            for (int d = 0; d < DM; ++d) t[d] = o[d] + t[d];
-        }
-#pragma unroll
-        for (int d = 0; d < DM; ++d)
-            if (d < D) dst[d] = t[d];
+    for (int w = 0; w < kWaves; ++w) {
+        off += w < wave ? lr_cnt[w] : 0;
+        tot += lr_cnt[w];
     }
-    uint64_t todo = __ballot(u >= 0 && n > NS);
-    while (todo) {
-        const int b = __builtin_ctzll(todo);
-        todo &= todo - 1;
-        const int cb = ch0 + b;
-        const int ub = __shfl(u, b, AMS_WAVE), lb = __shfl(last, b, AMS_WAVE);
-        const int first = cb + 1;
-        const int jb = (first + kFixBlock - 1) / kFixBlock, je = (lb + 1) / kFixBlock;
-        int n1 = lb - cb, n2 = 0, n3 = 0;
-        if (jb < je) {
-            n1 = jb * kFixBlock - first;
-            n2 = je - jb;
-            n3 = lb + 1 - je * kFixBlock;
-        }
-        const float s = sum_items<DM>(n1 + n2 + n3, D, full, [&](int t) {
-            if (t < n1) return head_part + (size_t)(first + t) * D;
-            if (t < n1 + n2) return bsum + (size_t)(jb + t - n1) * D;
-            return head_part + ((size_t)je * kFixBlock + (t - n1 - n2)) * D;
-        });
-        if (lane < D) {
-            const float r = tail_part[(size_t)cb * D + lane] + s;
-            dE[(size_t)ub * D + lane] = accumulate ? dE[(size_t)ub * D + lane] + r : r;
-        }
+    if (is_long) {
+        const int i = off + __popcll(todo & ((1ull << lane) - 1));
+        lr_ch[i] = ch;
+        lr_u[i] = u;
+        lr_last[i] = last;
     }
+    __syncthreads();
+    for (int i = wave; i < tot; i += kWaves)
+        fix_one_wave<DM>(D, full, lr_ch[i], lr_u[i], lr_last[i], head_part, tail_part, bsum, dE, accumulate);
 }
 
 size_t al256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -736,17 +806,28 @@ void launch_bwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32
     if (B > 0)
         AMS_LAUNCH("pool_bwd_sample", st, pool_bwd_sample<MODE, DM><<<(B + kWaves - 1) / kWaves, kThreads, 0, st>>>(
             B, D, seg_off, n_beh, inv, cap, E, U, (const float *)saved, dU, rec, cvec, da));
-    const int gs = (p.nch + kWaves * seg_cpw<MODE, DM>() - 1) / (kWaves * seg_cpw<MODE, DM>());
-    AMS_LAUNCH("pool_bwd_seg", st, pool_bwd_seg<MODE, DM><<<gs, kThreads, 0, st>>>(D, n_occ, cap, occ_perm, uniq_off, A,
-                                                   saved, dU, dA, rec, da, p.nch, dE, head, tail, cross,
-                                                   accumulate, seg_off, Lc));
+    const bool small = p.nch < kSmallChunks;
+#define SEG_LAUNCH(CPWV)                                                                                     \
+    AMS_LAUNCH("pool_bwd_seg", st, (pool_bwd_seg<MODE, DM, CPWV><<<(p.nch + kWaves * CPWV - 1) / (kWaves * CPWV), \
+                                                                  kThreads, 0, st>>>(                        \
+                                       D, n_occ, cap, occ_perm, uniq_off, A, saved, dU, dA, rec, da, p.nch, dE, \
+                                       head, tail, cross, accumulate, seg_off, Lc)))
+    if (small) SEG_LAUNCH(1);
+    else SEG_LAUNCH((seg_cpw<MODE, DM>()));
+#undef SEG_LAUNCH
+    // a whole block of chunks inside one run's head chunks starts at block 1
+    // or later (the run starts in an earlier chunk), so it needs 2 blocks
     const int nblk = p.nch / kFixBlock;
-    if (nblk > 0)
+    if (p.nch >= 2 * kFixBlock)
         AMS_LAUNCH("pool_bwd_bsum", st, pool_bwd_bsum<DM><<<(nblk + kWaves - 1) / kWaves, kThreads, 0, st>>>(
             D, p.nch, full, head, bsum));
-    const int gf = (p.nch + kWaves * AMS_WAVE - 1) / (kWaves * AMS_WAVE);
-    AMS_LAUNCH("pool_bwd_fix", st, pool_bwd_fix<DM><<<gf, kThreads, 0, st>>>(D, p.nch, full, uniq_off, cross, head, tail,
-                                                                          bsum, dE, accumulate));
+    if (small)
+        AMS_LAUNCH("pool_bwd_fix", st, pool_bwd_fix<DM><<<(p.nch + kWaves - 1) / kWaves, kThreads, 0, st>>>(
+            D, p.nch, full, uniq_off, cross, head, tail, bsum, dE, accumulate));
+    else
+        AMS_LAUNCH("pool_bwd_fix", st, pool_bwd_fix64<DM><<<(p.nch + kWaves * AMS_WAVE - 1) / (kWaves * AMS_WAVE),
+                                                           kThreads, 0, st>>>(D, p.nch, full, uniq_off, cross, head,
+                                                                              tail, bsum, dE, accumulate));
 }
 
 ams_status check_common(int32_t mode, int32_t B, int32_t D, int64_t n_beh)

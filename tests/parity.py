@@ -175,3 +175,13 @@ def grad_flip_bounds(dims, Ws, Xrows, orc_fwd, orc_bwd, flips1, flips2, dE_delta
     # a layer-1 flip changes only its own row of dW1 / db1 (covered above);
     # grow by a factor 2 for rounding in the perturbed terms themselves
     return [2 * e for e in extra_W], [2 * e for e in extra_b]
+
+
+def large_grid_workload():
+    """The long-sequence shapes at 6144 samples: 1.12M occurrences, 17.5k
+    chunks of 64 positions, the hottest image's run 1.6k chunks long.  Past
+    16,384 chunks the pooling backward switches to its large-grid kernels
+    (several chunks per wave in the stable-order pass, 64 chunks per wave in
+    the fix-up), which smaller batches never reach."""
+    import dataclasses
+    return dataclasses.replace(synth.get("c3_long"), name="long_6144", index=33, batch=6144, stream=-1)

@@ -123,12 +123,16 @@ def test_embed_host_errors(lib):
     # fp32 without H1_save keeps H1 in the workspace, which is then required
     a = _embed_args(m); a[13] = None; a[16] = None; a[17] = 0
     assert lib.ams_embed_fwd(*a) == WS
-    # PReLU: float32 only, and every hidden layer needs its slopes
+    # PReLU: float32, or bf16 with the 256-wide first layer of the bf16 tails;
+    # every hidden layer needs its slopes
     P = ctypes.c_void_p
     two = (P * 2)(0x1000, 0x1000)
     half = (P * 2)(0x1000, None)
-    mb = ams.make_mlp((4096, 256, 64, 12), "bf16")
+    mb = ams.make_mlp((4096, 128, 64, 12), "bf16")
     assert lib.ams_embed_fwd(*_embed_args(mb, two)) == DTYPE
+    mb256 = ams.make_mlp((4096, 256, 64, 12), "bf16")
+    a = _embed_args(mb256, two); a[5] = 0
+    assert lib.ams_embed_fwd(*a) == OK
     assert lib.ams_embed_fwd(*_embed_args(m, half)) == NULL
     a = _embed_args(m, two); a[5] = 0
     assert lib.ams_embed_fwd(*a) == OK

@@ -3,14 +3,15 @@ against the float64 oracle: U and A are copies and must be bit-exact; dE is
 a sum per unique image (1e-4 relative).  Batch shapes: the tiny one, the
 1024-sample one and the long-sequence one (lengths up to 500 against Lc = 64,
 so most lists are truncated, and hot images whose runs cross many 64-position
-chunks), plus Lc larger than every list (pure padding)."""
+chunks), the same shapes at 6144 samples (the backward's large-grid
+kernels), plus Lc larger than every list (pure padding)."""
 import numpy as np
 import pytest
 import torch
 
 from oracle import oracle
 from paper_1711_06505_amd import ams, synth
-from tests.parity import RTOL, assert_close
+from tests.parity import RTOL, assert_close, large_grid_workload
 
 pytestmark = pytest.mark.gpu
 F32 = RTOL["f32"]
@@ -21,9 +22,10 @@ def cuda(x, dtype=None):
     return (t.to(dtype) if dtype is not None else t).cuda()
 
 
-@pytest.mark.parametrize("name,Lc", [("tiny", 3), ("tiny", 40), ("c1_f32", 20), ("c3_long", 64)])
+@pytest.mark.parametrize("name,Lc", [("tiny", 3), ("tiny", 40), ("c1_f32", 20), ("c3_long", 64),
+                                     ("large_grid", 16)])
 def test_concat_pooling_matches_oracle(name, Lc):
-    w = synth.get(name)
+    w = large_grid_workload() if name == "large_grid" else synth.get(name)
     batch = synth.make_batch(w)
     occ = synth.occurrences(batch)
     dd = oracle.dedup(occ, w.n_images)

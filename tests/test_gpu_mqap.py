@@ -4,14 +4,15 @@ and backward, and the two channels of one step merged into one dE (the image
 channel's ams_pool_bwd, then the ID channel with accumulate = 1).  Per call:
 both sides get the same dedup, embeddings and queries (float32 values), at the
 tiny, the 1024-sample and the long-sequence batch shapes (hot images whose
-runs cross many 64-position chunks)."""
+runs cross many 64-position chunks), and the long-sequence shapes at 6144
+samples, where the backward takes its large-grid kernels."""
 import numpy as np
 import pytest
 import torch
 
 from oracle import oracle
 from paper_1711_06505_amd import ams, synth
-from tests.parity import RTOL, assert_close, f64
+from tests.parity import RTOL, assert_close, f64, large_grid_workload
 
 pytestmark = pytest.mark.gpu
 F32 = RTOL["f32"]
@@ -22,9 +23,9 @@ def cuda(x, dtype=None):
     return (t.to(dtype) if dtype is not None else t).cuda()
 
 
-@pytest.mark.parametrize("name", ["tiny", "c1_f32", "c3_long"])
+@pytest.mark.parametrize("name", ["tiny", "c1_f32", "c3_long", "large_grid"])
 def test_two_channel_pooling_matches_oracle(name):
-    w = synth.get(name)
+    w = large_grid_workload() if name == "large_grid" else synth.get(name)
     batch = synth.make_batch(w)
     occ = synth.occurrences(batch)
     dd = oracle.dedup(occ, w.n_images)

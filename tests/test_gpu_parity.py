@@ -17,7 +17,7 @@ import torch
 from oracle import oracle
 from paper_1711_06505_amd import ams, synth
 from tests.parity import (RTOL, assert_close, device_batch, f64, gpu_outputs, grad_flip_bounds,
-                          max_flips, relu_flips, run_gpu_step)
+                          large_grid_workload, max_flips, relu_flips, run_gpu_step)
 
 pytestmark = pytest.mark.gpu
 
@@ -254,19 +254,21 @@ def test_pool_fwd_bwd_match_oracle(mode, wname):
     assert_close(dE, pb["dE"], 1e-4, "dE")
 
 
+@pytest.mark.parametrize("size", ["c3_long", "large_grid"])
 @pytest.mark.parametrize("mode", ["sum", "max", "att"])
-def test_pool_long_runs_match_oracle(mode):
-    """The long-sequence batch (754k behaviors): its hottest image's run of
-    the stable order spans over a thousand 64-position chunks, so the
-    backward's fix-up adds whole blocks of 512 chunks as block sums.  E is
-    seeded random (the embedding model is not under test here)."""
-    w = synth.get("c3_long")
+def test_pool_long_runs_match_oracle(mode, size):
+    """The long-sequence batch (754k behaviors) and the same shapes at 6144
+    samples (1.12M occurrences, past the large-grid switch): the hottest
+    image's run of the stable order spans over a thousand 64-position
+    chunks, so the backward's fix-up adds whole blocks of 512 chunks as block
+    sums.  E is seeded random (the embedding model is not under test here)."""
+    w = synth.get("c3_long") if size == "c3_long" else large_grid_workload()
     batch = synth.make_batch(w)
     dd = oracle.dedup(synth.occurrences(batch), w.n_images)
     runs = np.diff(dd["uniq_off"])
     assert runs.max() > 2 * 512 * 64                  # a run covering a whole block of chunks
     E32 = (np.random.default_rng(11).standard_normal((dd["n_uniq"], w.out_dim)) * 0.5).astype(np.float32)
-    print(f"pool long runs {mode}: n_u={dd['n_uniq']} longest run={runs.max()}", flush=True)
+    print(f"pool long runs {mode} {size}: n_u={dd['n_uniq']} longest run={runs.max()}", flush=True)
     pf = oracle.pool_fwd(mode, batch["seg_off"], dd["inv"], E32)
     pb = oracle.pool_bwd(mode, batch["seg_off"], dd["inv"], dd["n_uniq"], E32, pf, batch["g_u"], batch["g_a"])
     fwd, dE = gpu_pool(mode, batch, dd, E32, pf_orc=pf)
