@@ -595,8 +595,9 @@ def bench_joint(w, mode, args):
             "n_beh": int(hb["seg_off"][-1]),
         })
     n_beh_max = max(b["n_beh"] for b in dev_batches)
+    tq = w.joint.query_table if w.joint.query_table >= 0 else None
     js = ams.JointStep(w.dims, w.dtype, mode, w.batch, n_beh_max, w.joint.id_rows, w.joint.id_dim,
-                       synth.ctr_dims(w))
+                       synth.ctr_dims(w), query_table=tq)
     js.alloc_workspace(w.n_images)
     stream = torch.cuda.current_stream()
 
@@ -672,7 +673,9 @@ def bench_joint(w, mode, args):
         "scaling": "weak", "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": f"{w.name}: B={w.batch}, lengths {w.lengths}, image ids {w.ids} over "
                                f"{w.n_images} images, table {w.n_images}x{w.in_dim} {w.dtype}, MLP "
-                               f"{'-'.join(map(str, w.dims))}, pooling {mode}; ID tables "
+                               f"{'-'.join(map(str, w.dims))}, pooling {mode}"
+                               f"{'' if tq is None else f' + a query channel on ID table {tq} (MultiQueryAttentivePooling)'}"
+                               f"; ID tables "
                                f"{'/'.join(str(n) for n in w.joint.id_rows)} x {w.joint.id_dim} fp32 "
                                f"Zipf({w.joint.id_zipf}); CTR MLP {'-'.join(map(str, synth.ctr_dims(w)))} fp32, "
                                f"softmax cross-entropy; sparse Adagrad lr {w.joint.lr}; fwd+bwd+update",

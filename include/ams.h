@@ -382,12 +382,17 @@ ams_status ams_bag_fwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_b
  * and fully written for u < n_u.  This is the SUM aggregator's backward with
  * dbag as the upstream gradient of behaviors and ads (ams_pool_bwd, SUM):
  * deterministic, no atomics, hot IDs split at fixed boundaries.
+ * dad: NULL, or [B x D] a second gradient of each sample's ad row (device),
+ * for a table whose ad row also serves elsewhere, as the query of the ID
+ * channel of MultiQueryAttentivePooling (section 5.2: dQ from
+ * ams_pool_query_bwd): the ad occurrence of sample i then contributes
+ * dbag[i] + dad[i].
  * ws: at least ams_bag_workspace(B, n_beh, D, n_uniq_cap) bytes. */
 size_t ams_bag_workspace(int32_t B, int64_t n_beh, int32_t D, int32_t n_uniq_cap);
 ams_status ams_bag_bwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,
                        const int32_t *inv, const int32_t *occ_perm, const int32_t *uniq_off,
                        const int32_t *n_uniq, int32_t n_uniq_cap, const float *dbag,
-                       float *grad, void *ws, size_t ws_bytes, void *stream);
+                       const float *dad, float *grad, void *ws, size_t ws_bytes, void *stream);
 
 /* ------------------------------------------------------------- CTR -----
  * The CTR MLP (the basic net's MLP, section 3.2): dims[0] inputs (the

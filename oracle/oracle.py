@@ -348,19 +348,23 @@ def adagrad_rows(grad, rows, accum, lr: float, eps: float):
     return r, a
 
 
-def merged_row_grad(seg_off, inv, n_uniq: int, dbag) -> np.ndarray:
+def merged_row_grad(seg_off, inv, n_uniq: int, dbag, dad=None) -> np.ndarray:
     """Gradient of every touched row: the sum over its occurrences (ascending)
     of the bag gradient of the sample each belongs to (the SUM aggregator's
-    backward with the bag gradient as upstream for behaviors and ad alike)."""
+    backward with the bag gradient as upstream for behaviors and ad alike).
+    dad: a second gradient of each sample's ad row (the ad's ID embedding
+    also being the query of an attentive channel, section 5.2), added to
+    what the ad occurrence carries."""
     dbag = _f64(dbag)
     D = dbag.shape[1]
     B = dbag.shape[0]
+    g_ad = dbag if dad is None else dbag + _f64(dad)
     fwd = {"U": np.zeros((B, D)), "A": np.zeros((B, D)), "w": np.zeros(1), "argmax": np.full((B, D), -1, np.int32)}
-    return pool_bwd("sum", seg_off, inv, n_uniq, np.zeros((max(n_uniq, 1), D)), fwd, dbag, dbag)["dE"]
+    return pool_bwd("sum", seg_off, inv, n_uniq, np.zeros((max(n_uniq, 1), D)), fwd, dbag, g_ad)["dE"]
 
 
 def joint_step(batch: dict, jb: dict, spec, n_ids: int, T, Ws, bs, id_rows, ctr_Ws, ctr_bs, accum,
-               mode: str = "att", table_is_compact: bool = True) -> dict:
+               mode: str = "att", table_is_compact: bool = True, query_table=None) -> dict:
     """One joint training step (Algorithm 1: worker iteration, server embed and
     update) in float64.
 
@@ -370,9 +374,16 @@ def joint_step(batch: dict, jb: dict, spec, n_ids: int, T, Ws, bs, id_rows, ctr_
     id_rows[t]:  rows of ID table t for its unique IDs (ascending), float32
     accum[t]:    their Adagrad accumulators
     spec:        the workload's JointSpec (lr, eps)
+    query_table: None, or the ID table t_q whose ad row is the query of a
+                 second attentive channel (MultiQueryAttentivePooling, section
+                 5.2): Q_i = the ad's row of t_q, U2 = pool_query_fwd(E, Q),
+                 the CTR input [U, U2, A, bags...]; the backward adds the ID
+                 channel's dE to the image channel's and the query gradient
+                 dQ_i to the ad occurrence's row gradient in table t_q.
     Returns the image-step pieces (dedup, fwd, pool, pool_bwd, bwd), the ID
     dedups, bags, the CTR forward/backward, the merged row gradients and the
-    Adagrad results (new rows and accumulators, float64).
+    Adagrad results (new rows and accumulators, float64); with a query table
+    also Q, the query channel's forward and backward and dU2.
     """
     occ = np.concatenate([_i32(batch["beh_ids"]), _i32(batch["ad_ids"])])
     dd = dedup(occ, n_ids)
@@ -385,28 +396,48 @@ def joint_step(batch: dict, jb: dict, spec, n_ids: int, T, Ws, bs, id_rows, ctr_
         o_t = np.concatenate([_i32(jb["beh_ids"][t]), _i32(jb["ad_ids"][t])])
         idd.append(dedup(o_t, spec.id_rows[t]))
         bags.append(bag_fwd(batch["seg_off"], idd[t]["inv"], id_rows[t]))
-    X = np.concatenate([pf["U"], pf["A"]] + bags, axis=1)
-    cf = ctr_fwd_bwd(X, jb["labels"], ctr_Ws, ctr_bs)
     D = pf["U"].shape[1]
-    dU, dA = cf["dX"][:, :D], cf["dX"][:, D:2 * D]
+    mq = query_table is not None
+    users = [pf["U"]]
+    if mq:
+        n_beh = int(batch["seg_off"][-1])
+        Q = _f64(id_rows[query_table])[idd[query_table]["inv"][n_beh:]]      # each sample's ad row
+        pq = pool_query_fwd(batch["seg_off"], dd["inv"], fw["E"], Q)
+        users.append(pq["U"])
+    X = np.concatenate(users + [pf["A"]] + bags, axis=1)
+    cf = ctr_fwd_bwd(X, jb["labels"], ctr_Ws, ctr_bs)
+    dU = cf["dX"][:, :D]
+    o = D
+    if mq:
+        dU2 = cf["dX"][:, o:o + D]
+        o += D
+    dA = cf["dX"][:, o:o + D]
+    o += D
     dbags = []
-    o = 2 * D
     for t in range(n_t):
         w_t = bags[t].shape[1]
         dbags.append(cf["dX"][:, o:o + w_t])
         o += w_t
     pb = pool_bwd(mode, batch["seg_off"], dd["inv"], dd["n_uniq"], fw["E"], pf, dU, dA)
-    bw = mlp_bwd(T, rows, Ws, fw, pb["dE"])
+    dE = pb["dE"]
+    if mq:
+        qb = pool_query_bwd(batch["seg_off"], dd["inv"], dd["n_uniq"], fw["E"], Q, pq, dU2)
+        dE = dE + qb["dE"]
+    bw = mlp_bwd(T, rows, Ws, fw, dE)
     grads, new_rows, new_acc = [], [], []
     for t in range(n_t):
-        g = merged_row_grad(batch["seg_off"], idd[t]["inv"], idd[t]["n_uniq"], dbags[t])
+        dad = qb["dQ"] if mq and t == query_table else None
+        g = merged_row_grad(batch["seg_off"], idd[t]["inv"], idd[t]["n_uniq"], dbags[t], dad)
         grads.append(g)
         r, a = adagrad_rows(g, id_rows[t], accum[t], spec.lr, spec.eps)
         new_rows.append(r)
         new_acc.append(a)
-    return {"dedup": dd, "fwd": fw, "pool": pf, "pool_bwd": pb, "bwd": bw, "id_dedup": idd, "bags": bags,
-            "X": X, "ctr": cf, "dU": dU, "dA": dA, "dbags": dbags, "row_grads": grads,
-            "new_rows": new_rows, "new_accum": new_acc}
+    out = {"dedup": dd, "fwd": fw, "pool": pf, "pool_bwd": pb, "bwd": bw, "id_dedup": idd, "bags": bags,
+           "X": X, "ctr": cf, "dU": dU, "dA": dA, "dbags": dbags, "dE": dE, "row_grads": grads,
+           "new_rows": new_rows, "new_accum": new_acc}
+    if mq:
+        out.update({"Q": Q, "query": pq, "query_bwd": qb, "dU2": dU2})
+    return out
 
 
 # ------------------------------------------------- multiple-query attention

@@ -92,7 +92,7 @@ def load() -> ctypes.CDLL:
     lib.ams_bag_workspace.restype = sz
     lib.ams_bag_workspace.argtypes = [i32, i64, i32, i32]
     lib.ams_bag_bwd.restype = ctypes.c_int
-    lib.ams_bag_bwd.argtypes = [i32, i32, P, i64, P, P, P, P, i32, P, P, P, sz, P]
+    lib.ams_bag_bwd.argtypes = [i32, i32, P, i64, P, P, P, P, i32, P, P, P, P, sz, P]
     lib.ams_ctr_workspace.restype = sz
     lib.ams_ctr_workspace.argtypes = [C, i32]
     lib.ams_ctr_fwd_bwd.restype = ctypes.c_int
@@ -324,12 +324,15 @@ def ams_bag_workspace(B: int, n_beh: int, D: int, n_uniq_cap: int) -> int:
 
 
 def ams_bag_bwd(seg_off, n_beh: int, inv, occ_perm, uniq_off, n_uniq, n_uniq_cap: int, dbag, grad, ws,
-                stream=None):
+                stream=None, dad=None):
+    """dad: None, or a second gradient [B x D] of each sample's ad row."""
     B, D = dbag.shape
     _rows_at_least(n_uniq_cap, grad=grad)
+    if dad is not None and tuple(dad.shape) != (B, D):
+        raise ValueError("dad must be [B x D] like dbag")
     _check(load().ams_bag_bwd(B, D, _p(seg_off), int(n_beh), _p(inv), _p(occ_perm), _p(uniq_off), _p(n_uniq),
-                              int(n_uniq_cap), _p(dbag), _p(grad), _p(ws), ws.numel() * ws.element_size(),
-                              _stream(stream)), "ams_bag_bwd")
+                              int(n_uniq_cap), _p(dbag), _p(dad), _p(grad), _p(ws),
+                              ws.numel() * ws.element_size(), _stream(stream)), "ams_bag_bwd")
 
 
 def ams_ctr_workspace(net: ams_ctr, B: int) -> int:
@@ -586,6 +589,14 @@ class JointStep:
       image pool + embed backward     ams_pool_bwd(dU, dA), ams_embed_bwd
       ID rows: merged grad, Adagrad   ams_bag_bwd, ams_adagrad_rows x tables (side stream)
 
+    With ``query_table`` t_q (MultiQueryAttentivePooling, section 5.2) the
+    image embeddings are pooled by a second attentive channel whose query is
+    each sample's ad row of ID table t_q (gathered by ams_bag_fwd over the ad
+    IDs alone): ams_pool_query_fwd gives U2, the CTR fields are
+    [U, U2, A, bags...], ams_pool_query_bwd adds that channel's dE to the image
+    channel's and yields dQ, which table t_q's ams_bag_bwd adds to the ad
+    occurrences' row gradients before its Adagrad step.
+
     With ``overlap`` (the default) the ID-table work runs on a second stream
     of default priority, forked from the caller's stream at the start and
     joined before the CTR call and at the end, so it hides behind the image
@@ -596,7 +607,13 @@ class JointStep:
     """
 
     def __init__(self, dims, dtype: str, mode: str, B: int, n_beh_max: int, id_rows, id_dim: int, ctr_dims,
-                 device="cuda", overlap: bool = True):
+                 device="cuda", overlap: bool = True, query_table: int | None = None):
+        if query_table is not None:
+            if mode != "att":
+                raise ValueError("the query channel pairs with attentive pooling of the image channel")
+            if not 0 <= int(query_table) < len(id_rows) or int(id_dim) != dims[-1]:
+                raise ValueError("query_table must name an ID table whose rows are as wide as the embeddings")
+        self.query_table = None if query_table is None else int(query_table)
         self.img = Step(dims, dtype, mode, B, n_beh_max, device=device)
         self.B, self.n_beh = int(B), int(n_beh_max)
         self.n_occ = self.B + self.n_beh
@@ -625,6 +642,13 @@ class JointStep:
         self.prob = torch.empty((Bm, self.ctr_dims[-1]), dtype=f32, device=dev)
         self.ctr_dW = [torch.empty((o, i), dtype=f32, device=dev) for i, o in zip(ctr_dims[:-1], ctr_dims[1:])]
         self.ctr_db = [torch.empty((o,), dtype=f32, device=dev) for o in ctr_dims[1:]]
+        if self.query_table is not None:
+            self.Q = torch.empty((Bm, D), dtype=f32, device=dev)
+            self.U2 = torch.empty((Bm, D), dtype=f32, device=dev)
+            self.w2 = torch.empty((max(self.n_beh, 1),), dtype=f32, device=dev)
+            self.dU2 = torch.empty((Bm, D), dtype=f32, device=dev)
+            self.dQ = torch.empty((Bm, D), dtype=f32, device=dev)
+            self.no_beh = torch.zeros(Bm + 1, dtype=i32, device=dev)      # offsets of bags holding the ad alone
         self.ws = None
         self.ws_id = None
         self.side = torch.cuda.Stream(device=dev) if overlap else None
@@ -661,29 +685,48 @@ class JointStep:
             side.wait_stream(main)                  # the caller's inputs are ready
             for x in [seg_off, labels] + list(id_ids) + list(id_tables) + list(accum):
                 x.record_stream(side)
-        # ID tables: dedup (needed from bag_bwd on) and bags, beside the image forward
+        tq = self.query_table
+        # ID tables: dedup (needed from bag_bwd on) and bags, beside the image forward;
+        # with a query table also each sample's ad row of it (a bag of the ad alone)
         for t in range(len(self.id_rows)):
             ams_dedup(id_ids[t], self.id_rows[t], self.t_uniq[t], self.t_inv[t], self.t_perm[t], self.t_off[t],
                       self.t_nu[t], self.t_status[t], self.ws_id, side)
             ams_bag_fwd(seg_off, n_beh, id_ids[t], id_tables[t], self.bags[t], side)
+            if t == tq:
+                ams_bag_fwd(self.no_beh[:B + 1], 0, id_ids[t][n_beh:], id_tables[t], self.Q[:B], side)
         st.dedup(ids, n_ids, main)
         st.embed_fwd(T, W, b, main)
         st.pool_fwd(seg_off, n_beh, main)
         if side is not main:
-            main.wait_stream(side)                  # bags ready
-        fields = [st.U[:B], st.A[:B]] + [x[:B] for x in self.bags]
-        dfields = [self.dU[:B], self.dA[:B]] + [x[:B] for x in self.dbags]
+            main.wait_stream(side)                  # bags (and the queries) ready
+        users, dusers = [st.U[:B]], [self.dU[:B]]
+        if tq is not None:
+            ams_pool_query_fwd(seg_off, n_beh, st.inv, st.E, self.Q[:B], self.U2[:B], self.w2, main)
+            users.append(self.U2[:B])
+            dusers.append(self.dU2[:B])
+        fields = users + [st.A[:B]] + [x[:B] for x in self.bags]
+        dfields = dusers + [self.dA[:B]] + [x[:B] for x in self.dbags]
         ams_ctr_fwd_bwd(self.ctr, fields, labels, ctr_W, ctr_b, self.loss, self.prob, self.ctr_dW, self.ctr_db,
                         dfields, self.ws, main)
         if side is not main:
             side.wait_stream(main)                  # bag gradients ready
-        # ID rows: merged gradients and Adagrad, beside the image backward
-        for t in range(len(self.id_rows)):
+        # ID rows: merged gradients and Adagrad, beside the image backward (the
+        # query table after the query channel's backward has produced dQ)
+        def id_update(t, dad=None):
             ams_bag_bwd(seg_off, n_beh, self.t_inv[t], self.t_perm[t], self.t_off[t], self.t_nu[t], self.n_occ,
-                        self.dbags[t][:B], self.row_grad[t], self.ws_id, side)
+                        self.dbags[t][:B], self.row_grad[t], self.ws_id, side, dad=dad)
             ams_adagrad_rows(self.t_uniq[t], self.t_nu[t], self.n_occ, self.row_grad[t], id_tables[t], accum[t],
                              lr, eps, side)
+        for t in range(len(self.id_rows)):
+            if t != tq:
+                id_update(t)
         st.pool_bwd(seg_off, n_beh, self.dU, self.dA, main)
+        if tq is not None:
+            ams_pool_query_bwd(seg_off, n_beh, st.inv, st.occ_perm, st.uniq_off, st.n_uniq, st.cap, st.E,
+                               self.Q[:B], self.U2[:B], self.w2, self.dU2[:B], self.dQ[:B], st.dE, True, st.ws, main)
+            if side is not main:
+                side.wait_stream(main)              # dQ ready
+            id_update(tq, self.dQ[:B])
         st.embed_bwd(T, W, main)
         if side is not main:
             main.wait_stream(side)                  # the whole step is ordered before later work on main

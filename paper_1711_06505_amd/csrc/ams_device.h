@@ -85,3 +85,10 @@ __device__ __forceinline__ uint16_t ams_f32_to_bf16(float f)
     u += 0x7fffu + ((u >> 16) & 1u);
     return (uint16_t)(u >> 16);
 }
+
+// The SUM aggregator's backward (ams_pool_bwd, AMS_POOL_SUM) with a second
+// upstream gradient of the ads: the ad of sample i contributes dA[i] + dA2[i]
+// (dA or dA2 NULL: nothing from it).  Shared by the ID-bag backward.
+ams_status pool_bwd_sum_ads(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh, const int32_t *inv,
+                            const int32_t *occ_perm, const int32_t *uniq_off, int32_t n_uniq_cap, const float *dU,
+                            const float *dA, const float *dA2, float *dE, void *ws, size_t ws_bytes, void *stream);

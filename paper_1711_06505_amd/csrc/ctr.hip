@@ -918,14 +918,15 @@ extern "C" size_t ams_bag_workspace(int32_t B, int64_t n_beh, int32_t D, int32_t
 
 extern "C" ams_status ams_bag_bwd(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh, const int32_t *inv,
                                   const int32_t *occ_perm, const int32_t *uniq_off, const int32_t *n_uniq,
-                                  int32_t n_uniq_cap, const float *dbag, float *grad, void *ws, size_t ws_bytes,
-                                  void *stream)
+                                  int32_t n_uniq_cap, const float *dbag, const float *dad, float *grad, void *ws,
+                                  size_t ws_bytes, void *stream)
 {
+    (void)n_uniq;
     if (B > 0 && !dbag) return AMS_ERR_NULL;
     // the SUM aggregator's backward with the bag gradient as the upstream
-    // gradient of behaviors and ads alike (it reads neither E, U nor A)
-    return ams_pool_bwd(AMS_POOL_SUM, B, D, seg_off, n_beh, inv, occ_perm, uniq_off, n_uniq, n_uniq_cap,
-                        grad, dbag, dbag, nullptr, dbag, dbag, grad, ws, ws_bytes, stream);
+    // gradient of behaviors and ads alike, the ads also taking dad
+    return pool_bwd_sum_ads(B, D, seg_off, n_beh, inv, occ_perm, uniq_off, n_uniq_cap, dbag, dbag, dad, grad, ws,
+                            ws_bytes, stream);
 }
 
 extern "C" size_t ams_ctr_workspace(const ams_ctr *net, int32_t B)

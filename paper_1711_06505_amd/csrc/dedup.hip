@@ -17,7 +17,10 @@
 //                  earlier tiles comes from decoupled look-back over the
 //                  per-tile digit counts they publish; then a stable scatter;
 //   dd_unique      head flags of the sorted keys, rank by the same look-back,
-//                  and the outputs.
+//                  and the outputs;
+//   dd_status      one block: the device status from the passes' error flag
+//                  and the range check (after the last tile, by the kernel
+//                  boundary, at no cost to the tiles).
 // Tiles, waves, rows and lanes are visited in index order, so the sort is
 // stable and every output bit-exact.  A tile only waits for earlier tiles to
 // publish, and blocks are dispatched in index order, so every wait ends.
@@ -290,18 +293,14 @@ __global__ __launch_bounds__(kThreads) void dd_pass(const uint32_t *__restrict__
 __global__ __launch_bounds__(kThreads) void dd_unique(const uint32_t *__restrict__ k,
                                                       const int32_t *__restrict__ v, int n,
                                                       uint32_t *__restrict__ words, int32_t *__restrict__ err,
-                                                      uint32_t *__restrict__ done,
-                                                      const int32_t *__restrict__ bad, int n_prep,
                                                       int32_t *__restrict__ uniq, int32_t *__restrict__ inv,
                                                       int32_t *__restrict__ occ_perm,
                                                       int32_t *__restrict__ uniq_off,
-                                                      int32_t *__restrict__ n_uniq,
-                                                      int32_t *__restrict__ dev_status)
+                                                      int32_t *__restrict__ n_uniq)
 {
     constexpr int kItems = kTile / kThreads;  // 8 consecutive positions per thread
     __shared__ int ws[kWaves];
     __shared__ uint32_t tile_base;
-    __shared__ int last_tile;
     const int t = threadIdx.x, w = t / AMS_WAVE;
     const int i0 = blockIdx.x * kTile + t * kItems;
     static_assert(kItems == 8, "two 16-byte loads per thread");
@@ -339,26 +338,9 @@ __global__ __launch_bounds__(kThreads) void dd_unique(const uint32_t *__restrict
         int tot = 0;
         for (int x = 0; x < kWaves; ++x) tot += ws[x];
         const uint32_t b = lookback_wave(words, blockIdx.x, (uint32_t)tot, err);
-        if (t == 0) {
-            tile_base = b;
-            // the tile that finishes its look-back last writes the status: by
-            // then every tile's wait has ended or recorded its failure in
-            // *err (ordered before this count by release/acquire)
-            last_tile = __hip_atomic_fetch_add(done, 1u, __ATOMIC_ACQ_REL, __HIP_MEMORY_SCOPE_AGENT) ==
-                        gridDim.x - 1;
-        }
+        if (t == 0) tile_base = b;
     }
     __syncthreads();
-    if (last_tile) {
-        int mine = 0;
-        for (int b = t; b < n_prep; b += kThreads) mine |= bad[b];
-        const int any_bad = __syncthreads_or(mine);
-        // a look-back bound hit in any pass is a runtime failure
-        if (t == 0)
-            *dev_status = __hip_atomic_load(err, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT)
-                              ? AMS_ERR_HIP
-                              : (any_bad ? AMS_ERR_ID_RANGE : AMS_OK);
-    }
     int run = (int)tile_base + incl - c;      // heads strictly before position i0
     for (int x = 0; x < w; ++x) run += ws[x];
     // (the caller's occ_perm may start anywhere: 16-byte stores only when aligned)
@@ -385,6 +367,23 @@ __global__ __launch_bounds__(kThreads) void dd_unique(const uint32_t *__restrict
             *n_uniq = rank + 1;
         }
     }
+}
+
+// The device status, one block after the unique pass (the kernel boundary
+// orders every tile's writes of the error flag before this read): a
+// look-back bound hit in any pass is a runtime failure, else an ID out of
+// range is reported, else OK.
+__global__ __launch_bounds__(kThreads) void dd_status(const int32_t *__restrict__ err,
+                                                      const int32_t *__restrict__ bad, int n_prep,
+                                                      int32_t *__restrict__ dev_status)
+{
+    int mine = 0;
+    for (int b = threadIdx.x; b < n_prep; b += kThreads) mine |= bad[b];
+    const int any_bad = __syncthreads_or(mine);
+    if (threadIdx.x == 0)
+        *dev_status = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                          ? AMS_ERR_HIP
+                          : (any_bad ? AMS_ERR_ID_RANGE : AMS_OK);
 }
 
 __global__ void dd_empty(int32_t *n_uniq, int32_t *dev_status, int32_t *uniq_off)
@@ -417,8 +416,8 @@ constexpr Layout layout(int64_t n_occ, int32_t n_ids)
     L.P.width = (L.P.bits + L.P.passes - 1) / L.P.passes;
     L.P.ntiles = (int)((n_occ + kTile - 1) / kTile);
     L.n_prep = L.P.ntiles < kPrepBlocks ? (L.P.ntiles > 0 ? L.P.ntiles : 1) : kPrepBlocks;
-    // the last two words: the look-back error flag and the count of unique-pass tiles done
-    L.n_words = L.P.passes * L.P.ntiles * kRadix + L.P.ntiles + 2;
+    // the last word: the look-back error flag
+    L.n_words = L.P.passes * L.P.ntiles * kRadix + L.P.ntiles + 1;
     auto al = [](size_t x) constexpr { return (x + 255) & ~(size_t)255; };
     const size_t nb = al((size_t)n_occ * 4);
     size_t o = nb;                           // keys ping (pong is the caller's ids on pass 0)
@@ -448,10 +447,9 @@ ams_status dedup_enqueue(const int32_t *ids, int n, int32_t n_ids, int32_t *uniq
     int32_t *hpart = (int32_t *)(w + L.off_hpart);
     int32_t *bad = (int32_t *)(w + L.off_bad);
     uint32_t *words = (uint32_t *)(w + L.off_words);
-    int32_t *err = (int32_t *)(words + L.n_words - 2);
-    uint32_t *done = words + L.n_words - 1;
+    int32_t *err = (int32_t *)(words + L.n_words - 1);
 
-    // dd_prep also zeroes every look-back word, the error flag and the tile count
+    // dd_prep also zeroes every look-back word and the error flag
     AMS_LAUNCH("dd_prep", st, dd_prep<<<L.n_prep, kPrepThreads, 0, st>>>((const uint32_t *)ids, n, L.P, (uint32_t)n_ids, hpart, bad, words,
                                           L.n_words));
     const uint32_t *kin = (const uint32_t *)ids;
@@ -467,7 +465,8 @@ ams_status dedup_enqueue(const int32_t *ids, int n, int32_t n_ids, int32_t *uniq
         vin = vout;
     }
     AMS_LAUNCH("dd_unique", st, dd_unique<<<L.P.ntiles, kThreads, 0, st>>>(kin, vin, n, words + (size_t)L.P.passes * L.P.ntiles * kRadix,
-                                              err, done, bad, L.n_prep, uniq, inv, occ_perm, uniq_off, n_uniq, dev_status));
+                                              err, uniq, inv, occ_perm, uniq_off, n_uniq));
+    AMS_LAUNCH("dd_status", st, dd_status<<<1, kThreads, 0, st>>>(err, bad, L.n_prep, dev_status));
     return ams_launch_status();
 }
 

@@ -264,6 +264,8 @@ constexpr bool wide_rec() { return MODE == AMS_POOL_ATT || MODE == kPoolQuery; }
 
 // (1) per sample: the records of its occurrences; attention terms
 // c_i = g_i . u_i and da_i = sum_j ds_j e_j, ds_j = w_j (g_i . e_j - c_i).
+// Sum mode with a second upstream gradient of the ads (dA2): da_i = dA_i +
+// dA2_i, the ad rows' gradient the stable-order pass then reads.
 template <int MODE, int DM>
 __global__ __launch_bounds__(kThreads) void pool_bwd_sample(int B, int D, const int32_t *__restrict__ seg_off,
                                                             int64_t n_beh, const int32_t *__restrict__ inv, int cap,
@@ -273,11 +275,15 @@ __global__ __launch_bounds__(kThreads) void pool_bwd_sample(int B, int D, const 
                                                             const float *__restrict__ dU,
                                                             void *__restrict__ rec,
                                                             float *__restrict__ cvec,
-                                                            float *__restrict__ da)
+                                                            float *__restrict__ da,
+                                                            const float *__restrict__ dA,
+                                                            const float *__restrict__ dA2)
 {
     const int lane = ams_lane();
     const int i = blockIdx.x * kWaves + threadIdx.x / AMS_WAVE;
     if (i >= B) return;
+    if (MODE == AMS_POOL_SUM && dA2 && lane < D)
+        da[(size_t)i * D + lane] = (dA ? dA[(size_t)i * D + lane] : 0.f) + dA2[(size_t)i * D + lane];
     const int j0 = seg_off[i], j1 = seg_off[i + 1];
     if (lane == 0) {
         const int k = (int)(n_beh + i);
@@ -789,7 +795,7 @@ void launch_bwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32
                 const int32_t *occ_perm, const int32_t *uniq_off, const float *E, const float *U,
                 const float *A, const void *saved, const float *dU, const float *dA, float *dE,
                 char *ws, const PoolPlan &p, hipStream_t st, float *dQ = nullptr, int accumulate = 0,
-                int Lc = 0)
+                int Lc = 0, const float *dA2 = nullptr)
 {
     void *rec = ws + p.off_rec;
     float *cvec = (float *)(ws + p.off_c);
@@ -805,7 +811,9 @@ void launch_bwd(int B, int D, const int32_t *seg_off, int64_t n_beh, const int32
     const bool full = D == DM;
     if (B > 0)
         AMS_LAUNCH("pool_bwd_sample", st, pool_bwd_sample<MODE, DM><<<(B + kWaves - 1) / kWaves, kThreads, 0, st>>>(
-            B, D, seg_off, n_beh, inv, cap, E, U, (const float *)saved, dU, rec, cvec, da));
+            B, D, seg_off, n_beh, inv, cap, E, U, (const float *)saved, dU, rec, cvec, da, dA, dA2));
+    // sum mode with a second ad gradient: the ads read the folded rows
+    if (MODE == AMS_POOL_SUM && dA2) dA = da;
     const bool small = p.nch < kSmallChunks;
 #define SEG_LAUNCH(CPWV)                                                                                     \
     AMS_LAUNCH("pool_bwd_seg", st, (pool_bwd_seg<MODE, DM, CPWV><<<(p.nch + kWaves * CPWV - 1) / (kWaves * CPWV), \
@@ -867,6 +875,27 @@ extern "C" size_t ams_pool_workspace(int32_t mode, int32_t B, int64_t n_beh, int
     (void)n_uniq_cap;
     if (check_common(mode, B, D, n_beh) != AMS_OK) return 0;
     return plan_pool(mode == AMS_POOL_ATT, B, n_beh, D).total;
+}
+
+ams_status pool_bwd_sum_ads(int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh, const int32_t *inv,
+                            const int32_t *occ_perm, const int32_t *uniq_off, int32_t n_uniq_cap, const float *dU,
+                            const float *dA, const float *dA2, float *dE, void *ws, size_t ws_bytes, void *stream)
+{
+    ams_status s = check_common(AMS_POOL_SUM, B, D, n_beh);
+    if (s != AMS_OK) return s;
+    if (n_uniq_cap < 0) return AMS_ERR_SIZE;
+    if (n_beh + B == 0) return AMS_OK;
+    if (!seg_off || !inv || !occ_perm || !uniq_off || !dE) return AMS_ERR_NULL;
+    if (B > 0 && !dU) return AMS_ERR_NULL;
+    const PoolPlan p = plan_pool(false, B, n_beh, D);
+    if (!ws || ws_bytes < p.total) return AMS_ERR_WORKSPACE;
+    hipStream_t st = (hipStream_t)stream;
+    with_dm(D, [&](auto dm) {
+        launch_bwd<AMS_POOL_SUM, decltype(dm)::value>(B, D, seg_off, n_beh, inv, n_uniq_cap, occ_perm, uniq_off,
+                                                      nullptr, nullptr, nullptr, nullptr, dU, dA, dE, (char *)ws, p,
+                                                      st, nullptr, 0, 0, dA2);
+    });
+    return ams_launch_status();
 }
 
 extern "C" ams_status ams_pool_bwd(int32_t mode, int32_t B, int32_t D, const int32_t *seg_off, int64_t n_beh,

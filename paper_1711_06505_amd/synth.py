@@ -50,6 +50,11 @@ class JointSpec:
     n_classes:  softmax classes (2: click / no click)
     label_p:    probability of a click label
     lr, eps, acc0: sparse Adagrad on the touched ID rows
+    query_table: -1, or the ID table whose ad row (the ad's category, say)
+                is the query of a second attentive channel
+                (MultiQueryAttentivePooling, section 5.2); its id_dim must be
+                the image embedding's width, and the CTR input grows by one
+                pooled vector
     """
     id_rows: tuple
     id_dim: int
@@ -60,6 +65,7 @@ class JointSpec:
     lr: float = 0.01
     eps: float = 1e-8
     acc0: float = 0.0
+    query_table: int = -1
 
 
 @dataclasses.dataclass(frozen=True)
@@ -140,6 +146,20 @@ WORKLOADS = {
     "tiny_joint": Workload("tiny_joint", 5, 64, ("fixed", 8), 512, ("uniform",),
                            (256, 64, 16), "f32", "normal", ("att",), stream=0,
                            joint=JointSpec((1000, 100, 10), 12, 1.05, (32, 16), 2, 0.3)),
+    # MultiQueryAttentivePooling (section 5.2): the joint step with a second
+    # attentive channel whose query is the ad's row of the 10k-row ID table
+    # (a category-sized table); the two pooled vectors (24-D) feed the CTR
+    # MLP, 72-200-80-2.  Same data as c4_joint.
+    "c4_mqap": Workload("c4_mqap", 6, 4096, ("geometric", 200, 500), 2_000_000,
+                        ("zipf", 1.05), (4096, 256, 64, 12), "bf16",
+                        "relu_normal", ("att",), stream=3,
+                        joint=JointSpec((10_000_000, 1_000_000, 10_000), 12, 1.05, (200, 80), 2, 0.05,
+                                        query_table=2)),
+    # Small MultiQueryAttentivePooling step for tests: the tiny batch with a
+    # 12-wide embedding (the query's width), the 10-row table as the query.
+    "tiny_mqap": Workload("tiny_mqap", 7, 64, ("fixed", 8), 512, ("uniform",),
+                          (256, 64, 12), "f32", "normal", ("att",), stream=0,
+                          joint=JointSpec((1000, 100, 10), 12, 1.05, (32, 16), 2, 0.3, query_table=2)),
 }
 _BY_INDEX = {w.index: w for w in WORKLOADS.values()}
 
@@ -333,11 +353,13 @@ def table_full(w, device="cpu", seed: int = 0, chunk_rows: int = 16384) -> torch
 # ---- joint step: ID features, labels, CTR weights ----------------------------
 
 def ctr_dims(w) -> tuple:
-    """Layer widths of the CTR MLP: [pooled user image vector, ad image
-    embedding, one bag per ID table] -> hidden -> classes (60-200-80-2)."""
+    """Layer widths of the CTR MLP: [pooled user image vector (two with a
+    query table), ad image embedding, one bag per ID table] -> hidden ->
+    classes (60-200-80-2; 72-200-80-2 with the query channel)."""
     w = get(w)
     j = w.joint
-    return (2 * w.out_dim + len(j.id_rows) * j.id_dim,) + tuple(j.ctr_hidden) + (j.n_classes,)
+    n_img = 3 if j.query_table >= 0 else 2
+    return (n_img * w.out_dim + len(j.id_rows) * j.id_dim,) + tuple(j.ctr_hidden) + (j.n_classes,)
 
 
 _PERM_CACHE: dict = {}

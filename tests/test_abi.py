@@ -195,11 +195,15 @@ def test_joint_host_errors(lib):
     assert lib.ams_bag_fwd(0, 12, None, 0, None, None, 100, None, None) == OK
     # bag backward = the SUM aggregator's backward: its checks apply
     assert lib.ams_bag_workspace(4, 40, 12, 44) == lib.ams_pool_workspace(0, 4, 40, 12, 44) > 0
-    bb = [4, 12, FAKE, 40, FAKE, FAKE, FAKE, FAKE, 44, FAKE, FAKE, FAKE, 16, None]
+    bb = [4, 12, FAKE, 40, FAKE, FAKE, FAKE, FAKE, 44, FAKE, None, FAKE, FAKE, 16, None]
     assert lib.ams_bag_bwd(*bb) == WS
+    a = list(bb); a[10] = FAKE                # with the ads' second gradient
+    assert lib.ams_bag_bwd(*a) == WS
     a = list(bb); a[9] = None                 # dbag
     assert lib.ams_bag_bwd(*a) == NULL
     a = list(bb); a[5] = None                 # occ_perm
+    assert lib.ams_bag_bwd(*a) == NULL
+    a = list(bb); a[11] = None                # grad
     assert lib.ams_bag_bwd(*a) == NULL
     # CTR
     net = ams.make_ctr((60, 200, 80, 2))

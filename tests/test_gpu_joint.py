@@ -22,10 +22,12 @@ def cuda_i32(x):
     return torch.from_numpy(np.ascontiguousarray(x, dtype=np.int32)).cuda()
 
 
-def mid_joint(B=96):
+def mid_joint(B=96, query_table=-1):
     base = synth.get("c4_joint")
-    return dataclasses.replace(base, name="mid_joint", index=21, batch=B, n_images=20_000, stream=-1,
-                               joint=dataclasses.replace(base.joint, id_rows=(200_000, 20_000, 500)))
+    return dataclasses.replace(base, name="mid_joint" if query_table < 0 else "mid_mqap", index=21, batch=B,
+                               n_images=20_000, stream=-1,
+                               joint=dataclasses.replace(base.joint, id_rows=(200_000, 20_000, 500),
+                                                         query_table=query_table))
 
 
 def gpu_dedup(occ_dev, n_ids, n):
@@ -218,7 +220,9 @@ def run_joint(w, mode="att"):
     rng = np.random.default_rng(17)
     accs = [torch.from_numpy(rng.uniform(0.0, 0.1, size=tuple(x.shape)).astype(np.float32)).cuda() for x in tabs]
     n_beh = int(batch["seg_off"][-1])
-    js = ams.JointStep(w.dims, w.dtype, mode, w.batch, n_beh, w.joint.id_rows, w.joint.id_dim, synth.ctr_dims(w))
+    tq = w.joint.query_table if w.joint.query_table >= 0 else None
+    js = ams.JointStep(w.dims, w.dtype, mode, w.batch, n_beh, w.joint.id_rows, w.joint.id_dim, synth.ctr_dims(w),
+                       query_table=tq)
     occ = cuda_i32(synth.occurrences(batch))
     id_occ = [cuda_i32(synth.joint_occurrences(jb, t)) for t in range(len(tabs))]
     # the oracle's inputs: rows of the batch's unique IDs before the update
@@ -232,7 +236,8 @@ def run_joint(w, mode="att"):
     g = gpu_outputs(js.img)
     T_u = synth.table_rows(w, g["uniq"], device="cuda").cpu()
     del T
-    o = oracle.joint_step(batch, jb, w.joint, w.n_images, T_u, Ws, bs, rows0, cW, cb, acc0, mode=mode)
+    o = oracle.joint_step(batch, jb, w.joint, w.n_images, T_u, Ws, bs, rows0, cW, cb, acc0, mode=mode,
+                          query_table=tq)
     o["_rows0"], o["_acc0"] = rows0, acc0
     return batch, jb, Ws, T_u, js, g, o, tabs, accs, od_t
 
@@ -272,29 +277,44 @@ def compare_image_chained(w, batch, Ws, T_u, g, o, dU, dA):
 
 def oracle_chain_from(w, batch, jb, Ws, T_u, o, od_t, E, bags):
     """The oracle's joint step downstream of the first-stage outputs: pooling
-    of E, the CTR model on [U, A, bags], the pooling and MLP backward, the ID
-    row gradients and their Adagrad step, all in float64 on the given E and
-    bags (the MLP backward on the oracle's own forward activations)."""
+    of E (and, with a query table, the query channel with the oracle's
+    queries), the CTR model on [U, (U2,) A, bags], the pooling and MLP
+    backward, the ID row gradients and their Adagrad step, all in float64 on
+    the given E and bags (the MLP backward on the oracle's own forward
+    activations)."""
     od = o["dedup"]
     seg = batch["seg_off"]
+    mq = "Q" in o
     pf = oracle.pool_fwd("att", seg, od["inv"], E)
-    X = np.concatenate([pf["U"], pf["A"]] + list(bags), axis=1)
+    users = [pf["U"]]
+    if mq:
+        pq = oracle.pool_query_fwd(seg, od["inv"], E, o["Q"])
+        users.append(pq["U"])
+    X = np.concatenate(users + [pf["A"]] + list(bags), axis=1)
     c = oracle.ctr_fwd_bwd(X, jb["labels"], *synth.make_ctr_weights(w))
     D = w.out_dim
-    dU, dA = c["dX"][:, :D], c["dX"][:, D:2 * D]
-    dbags = [c["dX"][:, 2 * D + 12 * t:2 * D + 12 * (t + 1)] for t in range(len(bags))]
+    k = 2 if mq else 1
+    dU, dA = c["dX"][:, :D], c["dX"][:, k * D:(k + 1) * D]
+    dbags = [c["dX"][:, (k + 1) * D + 12 * t:(k + 1) * D + 12 * (t + 1)] for t in range(len(bags))]
     pb = oracle.pool_bwd("att", seg, od["inv"], od["n_uniq"], E, pf, dU, dA)
-    bw = oracle.mlp_bwd(T_u, np.arange(od["n_uniq"], dtype=np.int32), Ws, o["fwd"], pb["dE"])
+    dE = pb["dE"]
+    extra = {}
+    if mq:
+        qb = oracle.pool_query_bwd(seg, od["inv"], od["n_uniq"], E, o["Q"], pq, c["dX"][:, D:2 * D])
+        dE = dE + qb["dE"]
+        extra = {"U2": pq["U"], "w2": pq["w"], "dU2": c["dX"][:, D:2 * D], "dQ": qb["dQ"]}
+    bw = oracle.mlp_bwd(T_u, np.arange(od["n_uniq"], dtype=np.int32), Ws, o["fwd"], dE)
     grads, new_rows, new_acc = [], [], []
     for t in range(len(bags)):
-        g = oracle.merged_row_grad(seg, od_t[t]["inv"], od_t[t]["n_uniq"], dbags[t])
+        dad = extra["dQ"] if mq and t == w.joint.query_table else None
+        g = oracle.merged_row_grad(seg, od_t[t]["inv"], od_t[t]["n_uniq"], dbags[t], dad)
         r, a = oracle.adagrad_rows(g, o["_rows0"][t], o["_acc0"][t], w.joint.lr, w.joint.eps)
         grads.append(g)
         new_rows.append(r)
         new_acc.append(a)
     return {"U": pf["U"], "A": pf["A"], "w": pf["w"], "ctr": c, "dU": dU, "dA": dA, "dbags": dbags,
-            "dE": pb["dE"], "dW": bw["dW"], "db": bw["db"], "row_grads": grads, "new_rows": new_rows,
-            "new_accum": new_acc}
+            "dE": dE, "dW": bw["dW"], "db": bw["db"], "row_grads": grads, "new_rows": new_rows,
+            "new_accum": new_acc, **extra}
 
 
 def compare_joint_end_to_end(w, batch, jb, Ws, T_u, g, js, o, od_t, tabs, accs):
@@ -335,6 +355,12 @@ def compare_joint_end_to_end(w, batch, jb, Ws, T_u, g, js, o, od_t, tabs, accs):
         held(js.ctr_db[l], c["db"][l], p["ctr"]["db"][l], f"ctr db{l + 1}", rtol=F32)
     held(js.dU[:B], o["dU"], p["dU"], "dU", rtol=F32, rows=True)
     held(js.dA[:B], o["dA"], p["dA"], "dA", rtol=F32, rows=True)
+    if "Q" in o:
+        np.testing.assert_array_equal(f64(js.Q[:B]), o["Q"])        # a copy of table rows
+        held(js.U2[:B], o["query"]["U"], p["U2"], "U2", rows=True)
+        held(js.w2[:g["w"].size], o["query"]["w"], p["w2"], "query weights")
+        held(js.dU2[:B], o["dU2"], p["dU2"], "dU2", rtol=F32, rows=True)
+        held(js.dQ[:B], o["query_bwd"]["dQ"], p["dQ"], "dQ", rtol=F32, rows=True)
     for t in range(n_t):
         n_u = od_t[t]["n_uniq"]
         held(js.dbags[t][:B], o["dbags"][t], p["dbags"][t], f"dbag {t}", rtol=F32, rows=True)
@@ -342,7 +368,7 @@ def compare_joint_end_to_end(w, batch, jb, Ws, T_u, g, js, o, od_t, tabs, accs):
         u = torch.from_numpy(od_t[t]["uniq"]).long().cuda()
         held(tabs[t][u], o["new_rows"][t], p["new_rows"][t], f"updated rows {t}", rtol=F32)
         held(accs[t][u], o["new_accum"][t], p["new_accum"][t], f"accumulators {t}", rtol=F32)
-    held(g["dE"], o["pool_bwd"]["dE"], p["dE"], "dE", rows=True)
+    held(g["dE"], o["dE"], p["dE"], "dE", rows=True)
     fo = o["fwd"]
     flips1 = relu_flips(fo["Z"][0], g["H1"], TAU)
     flips2 = relu_flips(fo["Z"][1], g["H2"], TAU) if w.n_layers == 3 else []
@@ -415,11 +441,58 @@ def test_joint_step_end_to_end(name):
         assert_close(js.ctr_db[l], c["db"][l], F32, f"ctr db{l + 1}")
 
 
-def test_joint_step_is_bitwise_deterministic():
+@pytest.mark.parametrize("name", ["tiny_mqap", "mid_mqap", "c4_mqap"])
+def test_mqap_joint_step_end_to_end(name):
+    """MultiQueryAttentivePooling in the joint step (section 5.2): a second
+    attentive channel with each ad's row of the category-sized ID table as its
+    query, both pooled vectors into the CTR model (24-D), dE of both channels
+    into the image model's backward and the query gradient into that table's
+    rows before their Adagrad step.  The whole chain against the oracle at the
+    small sizes; at full size (c4_mqap, 4096 samples) end to end with the
+    sensitivity-bounded tolerance of the plain joint step."""
+    from tests.test_gpu_parity import compare_step
+    w = mid_joint(query_table=2) if name == "mid_mqap" else synth.get(name)
+    print(f"mqap joint step {name}", flush=True)
+    batch, jb, Ws, T_u, js, g, o, tabs, accs, od_t = run_joint(w)
+    B, n_t = w.batch, len(tabs)
+    assert js.query_table == 2 and synth.ctr_dims(w)[0] == 3 * w.out_dim + 12 * n_t
+    if name == "c4_mqap":
+        compare_joint_end_to_end(w, batch, jb, Ws, T_u, g, js, o, od_t, tabs, accs)
+        return
+    compare_step(w, "att", batch, Ws, T_u, g, o)
+    n_beh = int(batch["seg_off"][-1])
+    np.testing.assert_array_equal(f64(js.Q[:B]), o["Q"])            # a copy of table rows
+    assert_close(js.U2[:B], o["query"]["U"], F32, "U2", rows=True)
+    assert_close(js.w2[:n_beh], o["query"]["w"], F32, "query weights")
+    c = o["ctr"]
+    assert abs(float(js.loss.item()) - c["loss"]) <= F32 * max(1.0, c["loss"])
+    assert_close(js.prob[:B], c["prob"], F32, "prob")
+    assert_close(js.dU[:B], o["dU"], F32, "dU", rows=True)
+    assert_close(js.dU2[:B], o["dU2"], F32, "dU2", rows=True)
+    assert_close(js.dA[:B], o["dA"], F32, "dA", rows=True)
+    assert_close(js.dQ[:B], o["query_bwd"]["dQ"], F32, "dQ", rows=True)
+    for l in range(len(js.ctr_dW)):
+        assert_close(js.ctr_dW[l], c["dW"][l], F32, f"ctr dW{l + 1}")
+        assert_close(js.ctr_db[l], c["db"][l], F32, f"ctr db{l + 1}")
+    for t in range(n_t):
+        n_u = od_t[t]["n_uniq"]
+        assert int(js.t_status[t].item()) == 0 and int(js.t_nu[t].item()) == n_u
+        assert_close(js.bags[t][:B], o["bags"][t], F32, f"bag {t}", rows=True)
+        assert_close(js.dbags[t][:B], o["dbags"][t], F32, f"dbag {t}", rows=True)
+        assert_close(js.row_grad[t][:n_u], o["row_grads"][t], F32, f"row grad {t}", rows=True)
+        u = torch.from_numpy(od_t[t]["uniq"]).long().cuda()
+        assert_close(tabs[t][u], o["new_rows"][t], F32, f"updated rows {t}")
+        assert_close(accs[t][u], o["new_accum"][t], F32, f"accumulators {t}")
+
+
+@pytest.mark.parametrize("query", [False, True])
+def test_joint_step_is_bitwise_deterministic(query):
     """The joint step twice from the same state (ID tables and accumulators
     restored), with the ID-table work on its side stream beside the image
-    path: every output, the updated rows and the accumulators bit for bit."""
-    w = mid_joint()
+    path: every output, the updated rows and the accumulators bit for bit;
+    also with the query channel (the query table's update then waits for dQ)."""
+    w = mid_joint(query_table=2 if query else -1)
+    tq = 2 if query else None
     batch = synth.make_batch(w)
     jb = synth.make_joint(w, batch)
     Ws, bs = synth.make_weights(w)
@@ -434,7 +507,7 @@ def test_joint_step_is_bitwise_deterministic():
     outs = []
     for _ in range(2):
         js = ams.JointStep(w.dims, w.dtype, "att", w.batch, n_beh, w.joint.id_rows, w.joint.id_dim,
-                           synth.ctr_dims(w))
+                           synth.ctr_dims(w), query_table=tq)
         tabs, accs = [x.clone() for x in tabs0], [x.clone() for x in accs0]
         js.run(occ, w.n_images, T, [x.cuda() for x in Ws], [x.cuda() for x in bs], cuda_i32(batch["seg_off"]),
                id_occ, tabs, accs, cuda_i32(jb["labels"]), [x.cuda() for x in cW], [x.cuda() for x in cb],
@@ -444,9 +517,11 @@ def test_joint_step_is_bitwise_deterministic():
         g.update({"loss": js.loss.cpu().numpy(), "dU": f64(js.dU), "dA": f64(js.dA),
                   "tabs": [x.cpu().numpy() for x in tabs], "accs": [x.cpu().numpy() for x in accs],
                   "ctr_dW": [f64(x) for x in js.ctr_dW], "dbags": [f64(x) for x in js.dbags]})
+        if query:
+            g.update({"U2": f64(js.U2), "dQ": f64(js.dQ)})
         outs.append(g)
     a, b = outs
-    for k in ("E", "U", "A", "dE", "loss", "dU", "dA"):
+    for k in ("E", "U", "A", "dE", "loss", "dU", "dA") + (("U2", "dQ") if query else ()):
         np.testing.assert_array_equal(a[k], b[k], err_msg=k)
     for k in ("dW", "db", "tabs", "accs", "ctr_dW", "dbags"):
         for x, y in zip(a[k], b[k]):

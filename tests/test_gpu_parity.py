@@ -361,7 +361,8 @@ def compare_step(w, mode, batch, Ws, T_u, g, o):
                 for j in (g["argmax"][i, d], pf["argmax"][i, d]):
                     dE_delta[od["inv"][j], d] += abs(batch["g_u"][i, d])
     extra_dE = np.abs(dE_delta) if dE_delta is not None else None
-    assert_close(g["dE"], pb["dE"], rt, "dE", extra=extra_dE, rows=True)
+    # (a joint step with a query channel adds that channel's dE: o["dE"])
+    assert_close(g["dE"], o.get("dE", pb["dE"]), rt, "dE", extra=extra_dE, rows=True)
     flips1 = relu_flips(fo["Z"][0], g["H1"], TAU)
     flips2 = relu_flips(fo["Z"][1], g["H2"], TAU) if w.n_layers == 3 else []
     eW, eb = grad_flip_bounds(w.dims, Ws, T_u, fo, bo, flips1, flips2, dE_delta)

@@ -20,7 +20,8 @@ def rel_err(x, r):
     return float(np.abs(x - r).max() / max(np.abs(r).max(), 1e-300))
 
 
-def joint_case(seed=5, B=10, n_img=30, n_rows=(50, 7), dims=(32, 16, 8), hidden=(12, 6), mode_lens=None):
+def joint_case(seed=5, B=10, n_img=30, n_rows=(50, 7), dims=(32, 16, 8), hidden=(12, 6), mode_lens=None,
+               query_table=None):
     rng = np.random.default_rng(seed)
     lens = rng.integers(1, 7, size=B) if mode_lens is None else np.asarray(mode_lens)
     seg = np.zeros(B + 1, np.int32)
@@ -41,7 +42,7 @@ def joint_case(seed=5, B=10, n_img=30, n_rows=(50, 7), dims=(32, 16, 8), hidden=
         Ws.append(torch.from_numpy(rng.uniform(-lim, lim, (fo, fi)).astype(np.float32)))
         bs.append(torch.from_numpy(rng.uniform(-0.1, 0.1, fo).astype(np.float32)))
     tabs = [rng.standard_normal((N, 12)).astype(np.float32) * 0.3 for N in n_rows]
-    cd = (2 * dims[-1] + 12 * len(n_rows),) + tuple(hidden) + (2,)
+    cd = ((2 if query_table is None else 3) * dims[-1] + 12 * len(n_rows),) + tuple(hidden) + (2,)
     cW, cb = [], []
     for fi, fo in zip(cd[:-1], cd[1:]):
         lim = math.sqrt(6.0 / (fi + fo))
@@ -51,14 +52,14 @@ def joint_case(seed=5, B=10, n_img=30, n_rows=(50, 7), dims=(32, 16, 8), hidden=
     return batch, jb, T, Ws, bs, tabs, cW, cb, spec
 
 
-def oracle_joint(batch, jb, T, Ws, bs, tabs, cW, cb, spec, accum=None, mode="att"):
+def oracle_joint(batch, jb, T, Ws, bs, tabs, cW, cb, spec, accum=None, mode="att", query_table=None):
     rows, acc = [], []
     for t, tab in enumerate(tabs):
         u = oracle.dedup(np.concatenate([jb["beh_ids"][t], jb["ad_ids"][t]]), tab.shape[0])["uniq"]
         rows.append(tab[u])
         acc.append(np.zeros((u.size, 12)) if accum is None else accum[t][u])
     return oracle.joint_step(batch, jb, spec, T.shape[0], T, Ws, bs, rows, cW, cb, acc, mode=mode,
-                             table_is_compact=False)
+                             table_is_compact=False, query_table=query_table)
 
 
 # ------------------------------------------------------------------ bags
@@ -273,6 +274,64 @@ def test_joint_step_row_gradients_by_finite_differences():
             assert abs(fd - g) <= 1e-5 * max(1.0, abs(g)), (t, ui, d, fd, g)
 
 
+def test_joint_mqap_matches_torch_autograd():
+    """MultiQueryAttentivePooling (section 5.2): the second attentive channel
+    takes each ad's row of ID table 1 as its query; loss, CTR input and its
+    gradient, every ID table's row gradients (the query table's including the
+    query gradient of the ad rows) and the image model's gradients against
+    torch autograd over the whole chain.  Image embeddings are 12 wide, the
+    query's width."""
+    batch, jb, T, Ws, bs, tabs, cW, cb, spec = joint_case(seed=21, dims=(32, 16, 12), query_table=1)
+    o = oracle_joint(batch, jb, T, Ws, bs, tabs, cW, cb, spec, query_table=1)
+    r = joint_autograd(batch, jb, T, Ws, bs, tabs, cW, cb, query_table=1)
+    assert o["X"].shape[1] == 3 * 12 + 2 * 12
+    assert abs(o["ctr"]["loss"] - r["loss"]) < 1e-13
+    assert rel_err(o["X"], r["X"]) < 1e-13
+    assert rel_err(o["ctr"]["dX"], r["dX"]) < 1e-12
+    for t in range(2):
+        u = o["id_dedup"][t]["uniq"]
+        assert rel_err(o["row_grads"][t], r["id_grad"][t][u]) < 1e-12
+    for l in range(2):
+        assert rel_err(o["bwd"]["dW"][l], r["dW"][l]) < 1e-11
+        assert rel_err(o["bwd"]["db"][l], r["db"][l]) < 1e-11
+    # the query gradient is really there: without it table 1's ad rows differ
+    plain = oracle.merged_row_grad(batch["seg_off"], o["id_dedup"][1]["inv"], o["id_dedup"][1]["n_uniq"],
+                                   o["dbags"][1])
+    assert rel_err(plain, o["row_grads"][1]) > 1e-3
+
+
+def test_joint_mqap_query_rows_by_finite_differences():
+    """dLoss/dtable_q[r][d] by central differences of the oracle's forward
+    (the row enters a bag and, for the samples whose ad it is, the query of
+    the ID channel) equals the merged row gradient of the query table."""
+    batch, jb, T, Ws, bs, tabs, cW, cb, spec = joint_case(seed=22, B=9, dims=(32, 16, 12), query_table=1)
+    o = oracle_joint(batch, jb, T, Ws, bs, tabs, cW, cb, spec, query_table=1)
+    X0, E = o["X"], o["fwd"]["E"]
+    D = 12
+    inv_img = o["dedup"]["inv"]
+    occ = np.concatenate([jb["beh_ids"][1], jb["ad_ids"][1]])
+
+    def loss_with(r, d, delta):
+        tab = tabs[1].astype(np.float64).copy()
+        tab[r, d] += delta
+        X = X0.copy()
+        Q = tab[jb["ad_ids"][1]]
+        X[:, D:2 * D] = oracle.pool_query_fwd(batch["seg_off"], inv_img, E, Q)["U"]
+        X[:, 3 * D + 12:3 * D + 24] = oracle.bag_fwd(batch["seg_off"], occ, tab)
+        return oracle.ctr_fwd_bwd(X, jb["labels"], cW, cb)["loss"]
+
+    u_all = o["id_dedup"][1]["uniq"]
+    ads = set(jb["ad_ids"][1].tolist())
+    picks = [k for k, r in enumerate(u_all) if r in ads][:3] + [k for k, r in enumerate(u_all) if r not in ads][:1]
+    assert len(picks) == 4
+    for ui in picks:
+        for d in (0, 5, 11):
+            h = 2.0 ** -10
+            fd = (loss_with(u_all[ui], d, h) - loss_with(u_all[ui], d, -h)) / (2 * h)
+            g = o["row_grads"][1][ui, d]
+            assert abs(fd - g) <= 1e-5 * max(1.0, abs(g)), (ui, d, fd, g)
+
+
 def test_joint_step_adagrad_applies_to_touched_rows_only():
     batch, jb, T, Ws, bs, tabs, cW, cb, spec = joint_case(seed=12)
     rng = np.random.default_rng(3)
@@ -288,11 +347,14 @@ def test_joint_step_adagrad_applies_to_touched_rows_only():
 
 
 def test_joint_workloads_are_well_formed():
-    for name in ("tiny_joint",):
+    for name in ("tiny_joint", "tiny_mqap"):
         w = synth.get(name)
         b = synth.make_batch(w)
         jb = synth.make_joint(w, b)
-        assert synth.ctr_dims(w)[0] == 2 * w.out_dim + 12 * len(w.joint.id_rows)
+        n_img = 3 if w.joint.query_table >= 0 else 2
+        assert synth.ctr_dims(w)[0] == n_img * w.out_dim + 12 * len(w.joint.id_rows)
+        if w.joint.query_table >= 0:
+            assert w.joint.id_dim == w.out_dim            # the query meets the image embeddings
         for t, N in enumerate(w.joint.id_rows):
             occ = synth.joint_occurrences(jb, t)
             assert occ.size == int(b["seg_off"][-1]) + w.batch

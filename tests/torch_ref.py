@@ -66,13 +66,16 @@ def step_autograd(batch, T, Ws, bs, mode: str, final_relu: bool = False):
     }
 
 
-def joint_autograd(batch, jb, T, Ws, bs, id_tables, ctr_Ws, ctr_bs, mode: str = "att"):
+def joint_autograd(batch, jb, T, Ws, bs, id_tables, ctr_Ws, ctr_bs, mode: str = "att", query_table=None):
     """The joint step in float64 autograd, every occurrence embedded on its own.
 
     Image path as step_autograd (no dedup); each ID table is bag-summed over a
     sample's behaviors and its ad with torch's embedding_bag; the CTR MLP (ReLU
     between layers) runs on [U, A, bag_0, bag_1, ...] and the loss is torch's
-    mean softmax cross-entropy.  T and id_tables are whole tables.  Returns the
+    mean softmax cross-entropy.  With query_table t_q, a second attentive
+    channel takes the ad's row of ID table t_q as its query (U2_i =
+    softmax(e_j . Q_i) weighted sum of the behaviors' e_j) and the CTR input
+    is [U, U2, A, bags...].  T and id_tables are whole tables.  Returns the
     loss, U, A, the bags, X, the gradient of X, the image-model and CTR
     gradients, and the dense gradient of every ID table.
     """
@@ -115,7 +118,12 @@ def joint_autograd(batch, jb, T, Ws, bs, id_tables, ctr_Ws, ctr_bs, mode: str = 
             flat.append(int(at[i]))
         bags.append(torch.nn.functional.embedding_bag(torch.as_tensor(flat), tab, torch.as_tensor(offs),
                                                       mode="sum"))
-    X = torch.cat([U, A] + bags, dim=1)
+    users = [U]
+    if query_table is not None:
+        Q = tabs[query_table][torch.as_tensor(np.asarray(jb["ad_ids"][query_table], np.int64))]
+        users.append(torch.stack([torch.softmax(E_occ[seg[i]:seg[i + 1]] @ Q[i], dim=0) @ E_occ[seg[i]:seg[i + 1]]
+                                  for i in range(B)]))
+    X = torch.cat(users + [A] + bags, dim=1)
     X.retain_grad()
     cW = [_f64(w).requires_grad_() for w in ctr_Ws]
     cb = [_f64(x).requires_grad_() for x in ctr_bs]
