@@ -46,42 +46,55 @@ __global__ __launch_bounds__(kThreads) void bag_fwd_k(int B, int D, const int32_
     float acc[DM];
 #pragma unroll
     for (int d = 0; d < DM; ++d) acc[d] = 0.f;
-    const bool vec4 = (D & 3) == 0;
+    const bool vec4 = (D & 3) == 0 && ((uintptr_t)table & 15) == 0;
     constexpr int kBagU = DM <= 16 ? 8 : 4;
-    for (int jr = j0; jr < j1; jr += kBagU * AMS_WAVE) {
-        int id[kBagU];
-#pragma unroll
-        for (int u = 0; u < kBagU; ++u) {
-            const int j = jr + u * AMS_WAVE + lane;
-            id[u] = j < j1 ? ids[j] : -1;
-        }
-        if (vec4) {
-            float4 v[kBagU][DM / 4];
+    // every load of a round unconditional (a position past the sample reads
+    // its last ID, an ID outside the table reads row 0), masked once all are
+    // in flight; no table rows at all: nothing to read
+    if (n_rows > 0) {
+        for (int jr = j0; jr < j1; jr += kBagU * AMS_WAVE) {
+            int id[kBagU];
 #pragma unroll
             for (int u = 0; u < kBagU; ++u) {
-                const bool ok = id[u] >= 0 && (int64_t)id[u] < n_rows;
-                const float *r = table + (size_t)(ok ? id[u] : 0) * D;
-#pragma unroll
-                for (int d4 = 0; d4 < DM / 4; ++d4)
-                    v[u][d4] = (ok && 4 * d4 < D) ? *(const float4 *)(r + 4 * d4) : make_float4(0.f, 0.f, 0.f, 0.f);
+                const int j = jr + u * AMS_WAVE + lane;
+                id[u] = ids[j < j1 ? j : j1 - 1];
             }
-#pragma unroll
-            for (int u = 0; u < kBagU; ++u)
-#pragma unroll
-                for (int d4 = 0; d4 < DM / 4; ++d4) {
-                    acc[4 * d4] += v[u][d4].x;
-                    acc[4 * d4 + 1] += v[u][d4].y;
-                    acc[4 * d4 + 2] += v[u][d4].z;
-                    acc[4 * d4 + 3] += v[u][d4].w;
-                }
-        } else {
+            bool ok[kBagU];
 #pragma unroll
             for (int u = 0; u < kBagU; ++u) {
-                if (id[u] < 0 || (int64_t)id[u] >= n_rows) continue;
-                const float *r = table + (size_t)id[u] * D;
+                const int j = jr + u * AMS_WAVE + lane;
+                ok[u] = j < j1 && id[u] >= 0 && (int64_t)id[u] < n_rows;
+            }
+            if (vec4) {
+                float4 v[kBagU][DM / 4];
 #pragma unroll
-                for (int d = 0; d < DM; ++d)
-                    if (d < D) acc[d] += r[d];
+                for (int u = 0; u < kBagU; ++u) {
+                    const float *r = table + (size_t)(ok[u] ? id[u] : 0) * D;
+#pragma unroll
+                    for (int d4 = 0; d4 < DM / 4; ++d4) v[u][d4] = *(const float4 *)(r + (4 * d4 < D ? 4 * d4 : 0));
+                }
+#pragma unroll
+                for (int u = 0; u < kBagU; ++u)
+#pragma unroll
+                    for (int d4 = 0; d4 < DM / 4; ++d4) {
+                        const bool take = ok[u] && 4 * d4 < D;
+                        acc[4 * d4] += take ? v[u][d4].x : 0.f;
+                        acc[4 * d4 + 1] += take ? v[u][d4].y : 0.f;
+                        acc[4 * d4 + 2] += take ? v[u][d4].z : 0.f;
+                        acc[4 * d4 + 3] += take ? v[u][d4].w : 0.f;
+                    }
+            } else {
+                float v[kBagU][DM];
+#pragma unroll
+                for (int u = 0; u < kBagU; ++u) {
+                    const float *r = table + (size_t)(ok[u] ? id[u] : 0) * D;
+#pragma unroll
+                    for (int d = 0; d < DM; ++d) v[u][d] = r[d < D ? d : 0];
+                }
+#pragma unroll
+                for (int u = 0; u < kBagU; ++u)
+#pragma unroll
+                    for (int d = 0; d < DM; ++d) acc[d] += (ok[u] && d < D) ? v[u][d] : 0.f;
             }
         }
     }

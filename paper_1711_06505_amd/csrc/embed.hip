@@ -1193,25 +1193,69 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     const int o = nb * 32 + r32;              // this lane's B row (output column)
     const int n_u = min(*n_uniq_p, cap);
     if (blockIdx.x * kTailRows >= n_u) return;    // the grid is sized by cap: no chunk for this block
+    // this lane's W2 operands and W3 (D * M <= 8 kThreads): every load
+    // unconditional (an index outside the weights reads element 0 and is
+    // dropped) and inside one branch on the storage type, so they are all in
+    // flight together instead of one wait each
     float4 breg[KB][4];
+    float w3v[8];
+    auto w2_at = [&](int kb, int q) { return (size_t)o * H + kh * khalf + kb * 32 + 16 * h + 4 * q; };
+    if (wbf16) {
+        uint2 r2[KB][4];
+        uint16_t r3[8];
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb)
+        for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-            breg[kb][q] = (kb < nkb && o < M)
-                              ? ld4_any(W2, wbf16, (size_t)o * H + kh * khalf + kb * 32 + 16 * h + 4 * q)
-                              : make_float4(0.f, 0.f, 0.f, 0.f);
-    // W3 (D * M <= 8 kThreads) and the biases into LDS, all loads in flight together
+            for (int q = 0; q < 4; ++q)
+                r2[kb][q] = *(const uint2 *)((const uint16_t *)W2 + ((kb < nkb && o < M) ? w2_at(kb, q) : 0));
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int e = t + i * kThreads;
+            r3[i] = L == 3 ? ((const uint16_t *)W3)[e < D * M ? e : 0] : (uint16_t)0;
+        }
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const uint2 v = r2[kb][q];
+                breg[kb][q] = (kb < nkb && o < M)
+                                  ? make_float4(__uint_as_float(v.x << 16), __uint_as_float(v.x & 0xffff0000u),
+                                                __uint_as_float(v.y << 16), __uint_as_float(v.y & 0xffff0000u))
+                                  : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) w3v[i] = ams_bf16_to_f32(r3[i]);
+    } else {
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                breg[kb][q] = *(const float4 *)((const float *)W2 + ((kb < nkb && o < M) ? w2_at(kb, q) : 0));
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int e = t + i * kThreads;
+            w3v[i] = L == 3 ? ((const float *)W3)[e < D * M ? e : 0] : 0.f;
+        }
+#pragma unroll
+        for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+                if (!(kb < nkb && o < M)) breg[kb][q] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    // W3 and the biases into LDS (the bias loads unconditional, in flight together)
+    const float b3v = L == 3 ? b3[t < D ? t : 0] : 0.f;
+    const float b2v = b2[t < M ? t : 0];
+    const float b1v = sk_bk ? b1[t < H ? t : 0] : 0.f;
     if (L == 3) {
 #pragma unroll
         for (int i = 0; i < 8; ++i) {
             const int e = t + i * kThreads;
-            if (e < D * M) W3s[(e / M) * (kMaxH2 + 1) + e % M] = ld_w(W3, wbf16, e);
+            if (e < D * M) W3s[(e / M) * (kMaxH2 + 1) + e % M] = w3v[i];
         }
-        if (t < D) b3s[t] = b3[t];
+        if (t < D) b3s[t] = b3v;
     }
-    if (t < M) b2s[t] = b2[t];
-    if (sk_bk && t < H) b1s[t] = b1[t];
+    if (t < M) b2s[t] = b2v;
+    if (sk_bk && t < H) b1s[t] = b1v;
     const bool relu_a = (L == 3) || final_relu;
     for (int c0 = blockIdx.x * kTailRows; c0 < n_u; c0 += gridDim.x * kTailRows) {
         const int row = c0 + r32;
@@ -1244,6 +1288,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
             const int rl = rowc % Sk<float>::BM;
             const float *pr = pbuf + (size_t)rl * kSkBN + (cbase - cb * kSkBN) + 16 * h;
             float4 v[3][KH][4];
+            // (a 32-k block past the half reloads block 0: every load of a
+            // share is issued unconditionally; such blocks are never used)
             auto load_share = [&](int w, int sl, float4 (&x)[KH][4]) {
                 const float *pw = pr + ((size_t)w * 2 + sl) * Sk<float>::TILE;
 #pragma unroll
@@ -1251,7 +1297,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll
                     for (int q = 0; q < 4; ++q) {
                         const int kb = nb * KH + i;
-                        x[i][q] = kb < nkb ? *(const float4 *)(pw + kb * 32 + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+                        x[i][q] = *(const float4 *)(pw + (kb < nkb ? kb * 32 : 0) + 4 * q);
                     }
             };
             auto add = [&](float4 (&acc4)[KH][4], const float4 (&x)[KH][4]) {
@@ -1309,13 +1355,27 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
                 }
         }
         __syncthreads();                        // the pair's rows are in H1s
+        if (split) {
 #pragma unroll
-        for (int kb = 0; kb < KB; ++kb)
+            for (int kb = 0; kb < KB; ++kb)
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-                areg[kb][q] = kb >= nkb ? make_float4(0.f, 0.f, 0.f, 0.f)
-                              : split ? *(const float4 *)&H1s[r32][cbase + kb * 32 + 16 * h + 4 * q]
-                                      : *(const float4 *)(hrow + kb * 32 + 4 * q);
+                for (int q = 0; q < 4; ++q)
+                    areg[kb][q] = kb >= nkb ? make_float4(0.f, 0.f, 0.f, 0.f)
+                                            : *(const float4 *)&H1s[r32][cbase + kb * 32 + 16 * h + 4 * q];
+        } else {
+            // every row load issued before any is used (a block past the
+            // half reloads block 0 and is zeroed)
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    areg[kb][q] = *(const float4 *)(hrow + (kb < nkb ? kb * 32 : 0) + 4 * q);
+#pragma unroll
+            for (int kb = 0; kb < KB; ++kb)
+#pragma unroll
+                for (int q = 0; q < 4; ++q)
+                    if (kb >= nkb) areg[kb][q] = make_float4(0.f, 0.f, 0.f, 0.f);
+        }
         if (PR) {
             // layer 1's PReLU on this lane's operands (Z1 -> H1), slope per column
 #pragma unroll
@@ -1459,9 +1519,15 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     __shared__ __attribute__((aligned(16))) uint16_t W2s[kMaxH2 * kMaxH1];
     __shared__ __attribute__((aligned(16))) uint16_t W3s[32 * kW3S];
     __shared__ __attribute__((aligned(16))) float S1s[PR ? H : 4];      // layer 1's slopes
+    __shared__ float S2s[PR ? kMaxH2 : 1];                               // layer 2's slopes (3 layers)
+    __shared__ __attribute__((aligned(16))) float B1s[kMaxH1];           // b1, for the split tiles
     const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
     const int h = lane >> 5, r32 = lane & 31;
     const int Mo = (L == 3) ? M : D;           // width of the second layer's output
+    // the grid is sized by the capacity: a block with no 32-row chunk below
+    // n_u leaves before staging the weights
+    const int n_u = min(*n_uniq_p, cap);
+    if ((int64_t)blockIdx.x * (kThreads / AMS_WAVE) * 32 >= n_u) return;
     constexpr int cpr = H / 8;                 // 16-byte chunks per W2 row
     // W2 and W3 into LDS with every load of the block in flight together
     static_assert(kMaxH2 * cpr % kThreads == 0, "W2 chunks per thread");
@@ -1479,12 +1545,16 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         }
     }
     if (L == 3) {
+        // every load unconditional (an index past W3 reads element 0 and is
+        // dropped), so they are all in flight together
         constexpr int n3 = (32 * kW3S + kThreads - 1) / kThreads;
         uint16_t v[n3];
 #pragma unroll
         for (int i = 0; i < n3; ++i) {
             const int e = t + i * kThreads, d = e / kW3S, o = e % kW3S;
-            v[i] = (e < 32 * kW3S && d < D && o < M) ? W3[d * M + o] : (uint16_t)0;
+            const bool ok = e < 32 * kW3S && d < D && o < M;
+            const uint16_t x = W3[ok ? d * M + o : 0];
+            v[i] = ok ? x : (uint16_t)0;
         }
 #pragma unroll
         for (int i = 0; i < n3; ++i) {
@@ -1492,23 +1562,25 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
             if (e < 32 * kW3S) W3s[e] = v[i];
         }
     }
-    if (PR)
+    if (pbuf)
+        for (int i = t; i < H; i += kThreads) B1s[i] = b1[i];
+    if (PR) {
         for (int i = t; i < H; i += kThreads) S1s[i] = s1[i];
-    // this lane's outputs o = 32 ob + 8 q + 4 h + r, their biases and (PReLU,
-    // 3 layers) slopes
-    float bias[2][16], sl2[2][16];
+        if (L == 3)
+            for (int i = t; i < kMaxH2; i += kThreads) S2s[i] = i < M ? s2[i] : 0.f;
+    }
+    // this lane's outputs o = 32 ob + 8 q + 4 h + r and their biases
+    float bias[2][16];
 #pragma unroll
     for (int ob = 0; ob < 2; ++ob)
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
             const int o = 32 * ob + acc_row(j, lane);
-            bias[ob][j] = o < Mo ? b2[o] : 0.f;
-            sl2[ob][j] = (PR && L == 3 && o < M) ? s2[o] : 0.f;
+            const float bv = b2[o < Mo ? o : 0];           // unconditional loads, all in flight
+            bias[ob][j] = o < Mo ? bv : 0.f;
         }
     __syncthreads();
 
-    const int n_u = min(*n_uniq_p, cap);
-    if (n_u <= 0) return;
     const bool relu2 = (L == 3 && !PR) || (L == 2 && final_relu);
     using K = Sk<uint16_t>;
     const SkPlan P = sk_plan(n_u, H, F, G, sk_bk<uint16_t>(), K::BM);
@@ -1534,17 +1606,32 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
         for (int qt = 0; qt < 4; ++qt) {
             uint4 bh[KS / 4], bl[KS / 4];
             if (split) {
+                // the quarter's pieces of the first three shares, every load
+                // issued before any is used (a share past wb reloads the
+                // first one and is not added); later shares, rare, one by one
+                const bool has1 = wa + 1 <= wb, has2 = wa + 2 <= wb;
+                const float *pw0 = pbuf + ((size_t)wa * 2 + slot_a) * K::TILE + rl * kSkBN;
+                const float *pw1 = has1 ? pbuf + ((size_t)(wa + 1) * 2) * K::TILE + rl * kSkBN : pw0;
+                const float *pw2 = has2 ? pbuf + ((size_t)(wa + 2) * 2) * K::TILE + rl * kSkBN : pw0;
+                float4 pv[3][KS / 4][2];
+#pragma unroll
+                for (int s4 = 0; s4 < KS / 4; ++s4) {
+                    const int k0 = 16 * (qt * (KS / 4) + s4) + 8 * h;
+                    pv[0][s4][0] = *(const float4 *)(pw0 + k0);
+                    pv[0][s4][1] = *(const float4 *)(pw0 + k0 + 4);
+                    pv[1][s4][0] = *(const float4 *)(pw1 + k0);
+                    pv[1][s4][1] = *(const float4 *)(pw1 + k0 + 4);
+                    pv[2][s4][0] = *(const float4 *)(pw2 + k0);
+                    pv[2][s4][1] = *(const float4 *)(pw2 + k0 + 4);
+                }
 #pragma unroll
                 for (int s4 = 0; s4 < KS / 4; ++s4) {
                     const int k0 = 16 * (qt * (KS / 4) + s4) + 8 * h;
                     float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
                     for (int pi = 0; pi < 3; ++pi) {
-                        const int w = wa + pi;
-                        if (w <= wb) {
-                            const float *pc = pbuf + ((size_t)w * 2 + (pi == 0 ? slot_a : 0)) * K::TILE +
-                                              rl * kSkBN + k0;
-                            const float4 v0 = *(const float4 *)pc, v1 = *(const float4 *)(pc + 4);
+                        if (pi == 0 || (pi == 1 ? has1 : has2)) {
+                            const float4 v0 = pv[pi][s4][0], v1 = pv[pi][s4][1];
                             x[0] += v0.x; x[1] += v0.y; x[2] += v0.z; x[3] += v0.w;
                             x[4] += v1.x; x[5] += v1.y; x[6] += v1.z; x[7] += v1.w;
                         }
@@ -1555,7 +1642,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
                         x[0] += v0.x; x[1] += v0.y; x[2] += v0.z; x[3] += v0.w;
                         x[4] += v1.x; x[5] += v1.y; x[6] += v1.z; x[7] += v1.w;
                     }
-                    const float4 c0v = *(const float4 *)&b1[k0], c1v = *(const float4 *)&b1[k0 + 4];
+                    const float4 c0v = *(const float4 *)&B1s[k0], c1v = *(const float4 *)&B1s[k0 + 4];
                     const float bb[8] = {c0v.x, c0v.y, c0v.z, c0v.w, c1v.x, c1v.y, c1v.z, c1v.w};
 #pragma unroll
                     for (int e = 0; e < 8; ++e) {
@@ -1636,10 +1723,11 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
                         x[4 + e] = z[ob][8 * p + 4 + e];   // o = 32 ob + 16 p + 8 + 4 h + e
                     }
                     if (PR) {                              // Z2 -> H2
+                        const int ob0 = 32 * ob + 16 * p + 4 * h;
 #pragma unroll
                         for (int e = 0; e < 4; ++e) {
-                            x[e] = x[e] > 0.f ? x[e] : sl2[ob][8 * p + e] * x[e];
-                            x[4 + e] = x[4 + e] > 0.f ? x[4 + e] : sl2[ob][8 * p + 4 + e] * x[4 + e];
+                            x[e] = x[e] > 0.f ? x[e] : S2s[ob0 + e] * x[e];
+                            x[4 + e] = x[4 + e] > 0.f ? x[4 + e] : S2s[ob0 + 8 + e] * x[4 + e];
                         }
                     }
                     uint4 hi, lo;
@@ -2668,8 +2756,16 @@ void tail_bwd_bf16(const uint16_t *__restrict__ H1b, const float *__restrict__ H
 #pragma unroll
     for (int ib = 0; ib < 2; ++ib) sl1[ib] = PR ? s1[64 * wave + 32 * ib + r32] : 0.f;
     float w3c[DM];                             // W3[:, po] (3 layers)
+    if (L == 3) {
+        uint16_t wv[DM];                       // unconditional loads (index 0 past W3), all in flight
 #pragma unroll
-    for (int d = 0; d < DM; ++d) w3c[d] = (L == 3 && d < D && po < M) ? ams_bf16_to_f32(W3[d * M + po]) : 0.f;
+        for (int d = 0; d < DM; ++d) wv[d] = W3[(d < D && po < M) ? d * M + po : 0];
+#pragma unroll
+        for (int d = 0; d < DM; ++d) w3c[d] = (d < D && po < M) ? ams_bf16_to_f32(wv[d]) : 0.f;
+    } else {
+#pragma unroll
+        for (int d = 0; d < DM; ++d) w3c[d] = 0.f;
+    }
 
     const int n_u = min(*n_uniq_p, cap);
     const int r0 = (int)((int64_t)blockIdx.x * n_u / gridDim.x);
@@ -2699,15 +2795,20 @@ void tail_bwd_bf16(const uint16_t *__restrict__ H1b, const float *__restrict__ H
                                                   : make_float4(0.f, 0.f, 0.f, 0.f);
             }
         }
+        // dE (and the forward's E for a final ReLU): unconditional loads,
+        // index 0 of the chunk past its rows, all in flight
+        float ev[4];
 #pragma unroll
         for (int m = 0; m < 4; ++m) {
             const int idx = t + kThreads * m;
-            float g = 0.f;
-            if (idx < nr * D) {
-                g = dE[(size_t)c0 * D + idx];
-                if (final_relu && !(Efwd[(size_t)c0 * D + idx] > 0.f)) g = 0.f;
-            }
-            pdz[m] = g;
+            const size_t at = (size_t)c0 * D + (idx < nr * D ? idx : 0);
+            pdz[m] = dE[at];
+            ev[m] = final_relu ? Efwd[at] : 1.f;
+        }
+#pragma unroll
+        for (int m = 0; m < 4; ++m) {
+            const int idx = t + kThreads * m;
+            pdz[m] = (idx < nr * D && ev[m] > 0.f) ? pdz[m] : 0.f;
         }
     };
 
