@@ -30,6 +30,17 @@ namespace {
 
 constexpr int kThreads = 256;
 constexpr int kTailBlocks = 256;      // fixed row partition of the tail backward
+
+// The tail backward's blocks: with n_u unique images, blocks [0, tail_active)
+// each take an equal share of at least kTailMinRows rows and write a partial
+// slot; the rest of the grid leaves at once, and the reduction of the slots
+// reads only the active ones (a small batch then moves far fewer partials).
+constexpr int kTailMinRows = 64;
+__host__ __device__ constexpr int tail_active(int n_u, int G)
+{
+    const int g = (n_u + kTailMinRows - 1) / kTailMinRows;
+    return g < 1 ? 1 : (g > G ? G : g);
+}
 constexpr int kMaxH1 = 256;
 constexpr int kMaxH2 = 64;
 constexpr int kMaxD = 32;
@@ -1838,6 +1849,9 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
                                                         int PS, float *__restrict__ zero_row, int zero_n,
                                                         const float *__restrict__ s1, const float *__restrict__ s2)
 {
+    const int n_u = min(*n_uniq_p, cap);
+    const int n_act = tail_active(n_u, (int)gridDim.x);
+    if ((int)blockIdx.x >= n_act) return;          // (block 0 is always active)
     // the zero row that dW1's padding rows stream (read by the next launch)
     if (blockIdx.x == 0)
         for (int i = threadIdx.x; i < zero_n; i += kTbThreads) zero_row[i] = 0.f;
@@ -1872,9 +1886,8 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
     }
     __syncthreads();
 
-    const int n_u = min(*n_uniq_p, cap);
-    const int r0 = (int)((int64_t)blockIdx.x * n_u / gridDim.x);
-    const int r1 = (int)((int64_t)(blockIdx.x + 1) * n_u / gridDim.x);
+    const int r0 = (int)((int64_t)blockIdx.x * n_u / n_act);
+    const int r1 = (int)((int64_t)(blockIdx.x + 1) * n_u / n_act);
 
     v16f dw2[2][2] = {{(v16f){}, (v16f){}}, {(v16f){}, (v16f){}}};   // [o block][i block]
     v16f dw3 = (v16f){};                     // wave ob < 2: lanes <-> o, rows d
@@ -2084,12 +2097,15 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
 // running chains (independent loads in flight); the chains, then the groups,
 // are added in a fixed order, so the result is deterministic.
 constexpr int kRedQ = 16;
-__global__ __launch_bounds__(64 * kRedQ) void tail_reduce(const float *__restrict__ part, int G, int PS, int L,
+__global__ __launch_bounds__(64 * kRedQ) void tail_reduce(const float *__restrict__ part, int G_grid, int PS, int L,
                                                           int H, int M, int D, float *__restrict__ dW2,
                                                           float *__restrict__ db2, float *__restrict__ dW3,
                                                           float *__restrict__ db3, float *__restrict__ db1,
-                                                          float *__restrict__ ds1, float *__restrict__ ds2)
+                                                          float *__restrict__ ds1, float *__restrict__ ds2,
+                                                          const int32_t *__restrict__ n_uniq_p, int cap)
 {
+    // the slots the tail backward's active blocks wrote
+    const int G = tail_active(min(*n_uniq_p, cap), G_grid);
     __shared__ float sq[kRedQ][64];
     const int t = threadIdx.x, q = t >> 6;
     const int e = blockIdx.x * 64 + (t & 63);
@@ -2716,6 +2732,9 @@ void tail_bwd_bf16(const uint16_t *__restrict__ H1b, const float *__restrict__ H
                    float *__restrict__ zero_row, int zero_n,
                    const float *__restrict__ s1, const float *__restrict__ s2)
 {
+    const int n_u = min(*n_uniq_p, cap);
+    const int n_act = tail_active(n_u, (int)gridDim.x);
+    if ((int)blockIdx.x >= n_act) return;          // (block 0 is always active)
     constexpr int H = kMaxH1;
     __shared__ __attribute__((aligned(16))) char H1t[32 * kH1S];      // H1, then dZ1, of the chunk
     __shared__ __attribute__((aligned(16))) char Z2t[32 * kZ2S];      // dZ2, high bf16 part
@@ -2767,9 +2786,8 @@ void tail_bwd_bf16(const uint16_t *__restrict__ H1b, const float *__restrict__ H
         for (int d = 0; d < DM; ++d) w3c[d] = 0.f;
     }
 
-    const int n_u = min(*n_uniq_p, cap);
-    const int r0 = (int)((int64_t)blockIdx.x * n_u / gridDim.x);
-    const int r1 = (int)((int64_t)(blockIdx.x + 1) * n_u / gridDim.x);
+    const int r0 = (int)((int64_t)blockIdx.x * n_u / n_act);
+    const int r1 = (int)((int64_t)(blockIdx.x + 1) * n_u / n_act);
 
     v16f dw2[2][2] = {{(v16f){}, (v16f){}}, {(v16f){}, (v16f){}}};   // [o block][i block]
     float db1a[2] = {0.f, 0.f}, ds1a[2] = {0.f, 0.f};
@@ -3363,7 +3381,8 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
     }
 #undef TB_LAUNCH
     AMS_LAUNCH("tail_reduce", st, tail_reduce<<<(PS + 63) / 64, 64 * kRedQ, 0, st>>>(tail, TG, PS, L, H, M, D, dW2,
-                                                                          db2, dW3, db3, db1, ds1, ds2));
+                                                                          db2, dW3, db3, db1, ds1, ds2, n_uniq,
+                                                                          cap));
 
     const int bm = (H % 128 == 0) ? 128 : 64;
     const int nmt = H / bm, outer = (F / 64) * p.kc;
