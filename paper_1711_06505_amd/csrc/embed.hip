@@ -568,66 +568,77 @@ __global__ __launch_bounds__(kSkThreads) void l1sk(const TT *__restrict__ T, int
 // unique rows with the whole K, so no tile is cut (no partial tiles for the
 // tail to add), and all blocks sweep K in step, so each XCD's L2 serves a W1
 // slice to its 32 CUs at about the same time.  A block is 8 waves (two per
-// SIMD) working in tiles of 256 rows: a wave computes its 32 rows against all
-// 256 units (eight 32x32 accumulator blocks, 128 registers); a wave with no
-// rows left in the block's range skips its products.
+// SIMD) working in tiles of 256 rows; wave (wm, wn) computes rows
+// 128 wm .. + 127 against units 64 wn .. + 63 (eight 32x32 accumulator
+// blocks, 128 registers).
 //
-// The gathered feature rows, the dominant HBM stream, go straight into
-// registers: a 64-k stage is 128 contiguous bytes of a row, lane (r, h) of a
-// wave holding bytes 64h .. 64h + 63 of row r (k = 32h .. 32h + 31 of the
-// stage, four 16-byte MFMA operands), PA = 3 stages ahead: 96 KB of rows in
-// flight per CU, what the registers left beside the accumulators allow.  The
-// stage's W1 slice (256 rows x 128 bytes, an L2 hit after the first CU of an
-// XCD) moves into a 4-slot LDS ring by direct DMA PW = 3 stages ahead; B
-// operands are 16-byte LDS reads of the same k.  Vector memory completes in
-// issue order, so rows cannot usefully run further ahead than W1, whose ring
-// the LDS bounds.  Every vector memory instruction of the stages (4 row loads
-// and 4 W1 DMAs per wave and stage, in that order) comes from inline
-// assembly, so the compiler adds no waits of its own: stage s waits with
-// s_waitcnt vmcnt(16), which completes everything up to its own W1 DMA
-// (issued PW stages earlier, its rows PA stages earlier).  Stages past the
-// last load the last one again (into registers and a slot nobody reads), so
-// every stage issues the same count.  The stage sequence is unrolled for the
-// whole row, so no register such a load writes is carried around a loop
-// (where the register allocator could copy it before it has landed);
-// tests/test_l1rs_asm.py checks the generated code for that.
+// The gathered feature rows are the dominant HBM stream.  They move by
+// direct DMA (global_load_lds_dwordx4) into a 3-slot LDS ring, 2 stages
+// ahead, one 64-k stage being 128 contiguous bytes of each of the tile's 256
+// rows: every DMA instruction reads 8 whole 128-byte lines (8 rows), the
+// access pattern that reads a scattered row set fastest (a lane-per-row
+// pattern, 16 bytes of 32 rows per instruction, reached about 80 % of it),
+// and carries the non-temporal hint so the streamed rows do not push W1 out
+// of L2.  The stage's W1 slice (256 rows x 128 bytes) moves into a 2-slot
+// ring the same way, 1 stage ahead.  Both operands are then 16-byte LDS
+// reads (slot rows swizzled by 16-byte chunk, chunk ^ ((row >> 1) & 7), so a
+// quarter-wave's reads of 16 rows hit distinct banks; the DMA lanes read the
+// permuted chunks from global memory, within the same line).
+//
+// One stage sequence runs across all tiles of the block: the rows of the
+// next tile's first two stages are in flight while the last stages of a
+// tile and its epilogue run, and the next tile's IDs are loaded at the
+// tile's first stage.  Every vector memory instruction of the stages (4 W1
+// DMAs and 4 row DMAs per wave and stage, the 4 ID loads at a tile's first
+// stage) comes from inline assembly, so the compiler adds no waits of its
+// own: stage g waits with s_waitcnt vmcnt(4) (vmcnt(8) right after the ID
+// loads), which completes everything up to its own W1 DMA (issued one stage
+// earlier, after its rows).  Stages past the block's last tile issue the
+// same DMAs from a zero row, so every stage issues the same count.
+//
+// DMA geometry: instruction q (0..3) of wave w fills the 8 slot rows
+// 32 w + 8 q .. + 7, lane i row 32 w + 8 q + i / 8, 16-byte chunk i % 8;
+// for feature rows, slot row 32 w + 8 q + a holds the tile's row
+// 32 w + 4 a + q, so a lane's four rows are consecutive entries of uniq.
 namespace rs {
-constexpr int BN_ = 256;
 constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / AMS_WAVE;
 constexpr int kWavesPerSimd = kWaves / 4;
-constexpr int BM = 32 * kWaves;              // rows per tile
-constexpr int WROWS = BN_ / kWaves;          // W1 slot rows a wave moves per stage
-constexpr int BN = BN_;                      // hidden units (the whole width)
+constexpr int BM = 256;                      // rows per tile
+constexpr int BN = 256;                      // hidden units (the whole width)
 constexpr int KS = 64;                       // k per stage: 128 bytes of a row
 constexpr int kF = 4096;                     // feature width (the stages are unrolled for it)
 constexpr int S = kF / KS;                   // stages per tile
-constexpr int PA = 3;                        // stages of rows in flight
-constexpr int PW = 3;                        // stages of W1 in flight
-constexpr int NA = PA + 1;                   // row register sets
-constexpr int R = PW + 1;                    // W1 ring slots
-constexpr int SLOT = BN * KS * 2;            // bytes per slot (32 KB)
-constexpr int DMA_PER_WAVE = SLOT / 1024 / kWaves;   // 1 KB per DMA instruction
-constexpr int VM_PER_STAGE = 4 + DMA_PER_WAVE;
-constexpr int WAIT = (PW - 1) * VM_PER_STAGE;        // ops a stage may leave in flight
-constexpr uint32_t W1_Q = 8 * kF * 2;        // bytes between a wave's DMA row groups (8 W1 rows)
-static_assert(PA >= PW, "rows are issued at least as far ahead as W1");
-static_assert(R * SLOT <= 160 * 1024, "the ring fits the LDS");
-static_assert((size_t)BN * kF * 2 < (1ull << 32), "W1 offsets fit 32 bits");
+constexpr int NX = 3;                        // feature-row slots (rows issued 2 stages ahead)
+constexpr int NW = 2;                        // W1 slots (1 stage ahead)
+constexpr int SLOT = BM * KS * 2;            // bytes per slot (32 KB, also BN * KS * 2)
+constexpr int DMA = 4;                       // DMA instructions per wave and slot (8 slot rows each)
+constexpr int WAIT = 4;                      // ops a stage may leave in flight (the next stage's rows)
+constexpr int WAIT_AFTER_IDS = 8;            // ... and the 4 ID loads issued one stage earlier
+static_assert(BM == BN && (NX + NW) * SLOT <= 160 * 1024, "the rings fit the LDS");
+static_assert(DMA * 1024 * kWaves == SLOT && kWaves == 8, "four slot-row groups of 8 per wave; 2 x 4 waves");
+static_assert(WAIT == DMA && WAIT_AFTER_IDS == DMA + 4, "wait counts follow the issue order");
+static_assert(S > 3, "the next tile's first two stages are issued from the last two");
 }  // namespace rs
+
+// A zero feature row: rows past the block's range, rows whose ID is outside
+// the table and the stages past the last tile read it (their products are
+// then exactly 0, and Z1 = b1 for a bad ID).
+__device__ __attribute__((aligned(256))) uint16_t rs_zero_row[rs::kF];
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-// 16-byte global load into registers at p + OFF, invisible to the
-// compiler's wait bookkeeping (the stages wait for it explicitly).
-template <int OFF>
-__device__ __forceinline__ void rs_load16(u32x4 &v, const char *p)
+// DMA of 64 lanes x 16 bytes from per-lane addresses, non-temporal, into
+// LDS at lds_addr + 16 lane.
+__device__ __forceinline__ void rs_dma_row(const char *src, uint32_t lds_addr)
 {
-    asm volatile("global_load_dwordx4 %0, %1, off offset:%2" : "=v"(v) : "v"(p), "n"(OFF) : "memory");
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off nt"
+                 :
+                 : "s"(lds_addr), "v"(src)
+                 : "memory", "m0");
 }
 
-// DMA of 64 lanes x 16 bytes from base + voff into LDS at lds_addr (+16 per
-// lane).
+// DMA of 64 lanes x 16 bytes from base + voff into LDS at lds_addr + 16 lane.
 __device__ __forceinline__ void rs_dma16(const void *base, uint32_t voff, uint32_t lds_addr)
 {
     asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
@@ -636,78 +647,48 @@ __device__ __forceinline__ void rs_dma16(const void *base, uint32_t voff, uint32
                  : "memory", "m0");
 }
 
-// 16-byte chunk swizzle of the W1 slot rows (128 bytes each).  The LDS
-// serves a 16-byte read for 16 lanes per cycle over 64 banks, so rows r and
-// r + 1 sit in different bank halves and the even (odd) rows of 16
-// consecutive ones must use 8 distinct chunk positions: chunk ^ (row / 2 % 8).
-// It depends on row bits 1-3 only, so the four DMA row groups of a lane
-// (rows 8 apart) differ in bit 3 and get different swizzles.
-__device__ __forceinline__ int rs_swz(int row) { return (row >> 1) & 7; }
-
-struct RsLane {
-    const char *a;         // this lane's feature row at the next row stage to issue (+ 64 h), or a dummy
-    const void *w1;        // W1 (uniform)
-    uint32_t w;            // byte offset in W1 of this lane's first DMA row at the next W1 stage
-    uint32_t dq[rs::DMA_PER_WAVE];   // per DMA group q: its row (8 q further) and chunk, relative to w
-    uint32_t lds_wave;     // byte address of this wave's DMA rows in slot 0
-};
-
-// Stage t's issue: rows of stage t + PA (into register set (t + PA) % NA)
-// and W1 of stage t + PW (into slot (t + PW) % R), or of the last stage past
-// the end; the running pointers advance only over real stages, and the
-// empty asm keeps the compiler from precomputing every stage's addresses.
-__device__ __forceinline__ void rs_issue(RsLane &L, int t, u32x4 (&A)[rs::NA][4])
+// 4-byte load whose completion the stages count themselves.
+__device__ __forceinline__ void rs_ld_id(int &v, const int32_t *p)
 {
-    const int sa = t + rs::PA, sw = t + rs::PW;
-    if (sa >= 0) {
-        u32x4 *d = A[sa % rs::NA];
-        rs_load16<0>(d[0], L.a);
-        rs_load16<16>(d[1], L.a);
-        rs_load16<32>(d[2], L.a);
-        rs_load16<48>(d[3], L.a);
-        if (sa < rs::S - 1) {
-            L.a += 128;
-            asm volatile("" : "+v"(L.a));
-        }
-    }
-    if (sw >= 0) {
-#pragma unroll
-        for (int q = 0; q < rs::DMA_PER_WAVE; ++q)
-            rs_dma16(L.w1, L.w + L.dq[q], L.lds_wave + (sw % rs::R) * rs::SLOT + q * 1024);
-        if (sw < rs::S - 1) {
-            L.w += 128;
-            asm volatile("" : "+v"(L.w));
-        }
-    }
+    asm volatile("global_load_dword %0, %1, off" : "=v"(v) : "v"(p) : "memory");
 }
 
-__device__ __forceinline__ void rs_compute(const char *slot, const u32x4 (&av)[4], v16f (&acc)[8],
-                                           const int (&boff)[4], bool live)
+// 16-byte chunk swizzle of the 128-byte slot rows.  The LDS serves a
+// 16-byte read for 16 lanes per cycle over 64 banks, so rows r and r + 1 sit
+// in different bank halves and the even (odd) rows of 16 consecutive ones
+// must use 8 distinct chunk positions: chunk ^ (row / 2 % 8).
+__device__ __forceinline__ int rs_swz(int row) { return (row >> 1) & 7; }
+
+// One stage's products from X slot xs and W1 slot ws: 4 k steps of 16, each
+// 4 (row blocks) x 2 (unit blocks) MFMAs; the k step's 6 operand reads are
+// issued while the previous step's products run.
+__device__ __forceinline__ void rs_compute(const char *xs, const char *ws, const int (&ao)[4], const int (&bo)[4],
+                                           v16f (&acc)[8])
 {
-    if (!live) return;                        // (uniform per wave)
-    // 32 (k step j, unit block nb) products; the B operand of each is one
-    // 16-byte LDS read.  The reads are written first and the products after
-    // them; sched_group_barrier then interleaves them RA products apart.
-    constexpr int RA = rs::kWavesPerSimd == 1 ? 8 : 4;
-    u32x4 b[4][8];
+    u32x4 a[4][4], b[4][2];
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
+    for (int j = 0; j < 4; ++j) {
 #pragma unroll
-        for (int nb = 0; nb < 8; ++nb) b[j][nb] = *(const u32x4 *)(slot + boff[j] + nb * 4096);
+        for (int rb = 0; rb < 4; ++rb) a[j][rb] = *(const u32x4 *)(xs + ao[j] + rb * 4096);
 #pragma unroll
-    for (int j = 0; j < 4; ++j)
-#pragma unroll
-        for (int nb = 0; nb < 8; ++nb)
-            acc[nb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, av[j]),
-                                                               __builtin_bit_cast(bf16x8, b[j][nb]), acc[nb], 0, 0,
-                                                               0);
-    __builtin_amdgcn_sched_group_barrier(0x100, RA, 0);
-#pragma unroll
-    for (int g = 0; g < 32 / RA - 1; ++g) {
-        __builtin_amdgcn_sched_group_barrier(0x100, RA, 0);
-        __builtin_amdgcn_sched_group_barrier(0x008, RA, 0);
+        for (int cb = 0; cb < 2; ++cb) b[j][cb] = *(const u32x4 *)(ws + bo[j] + cb * 4096);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, RA, 0);
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+#pragma unroll
+        for (int rb = 0; rb < 4; ++rb)
+#pragma unroll
+            for (int cb = 0; cb < 2; ++cb)
+                acc[rb * 2 + cb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(
+                    __builtin_bit_cast(bf16x8, a[j][rb]), __builtin_bit_cast(bf16x8, b[j][cb]), acc[rb * 2 + cb], 0, 0,
+                    0);
+    __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
 }
 
 // H1b / H1lo: the bf16 rounding of H1 = ReLU(Z1 + b1) (keep_z: of Z1 + b1,
@@ -719,102 +700,154 @@ __global__ __launch_bounds__(rs::kThreads) __attribute__((amdgpu_waves_per_eu(rs
     int G, uint16_t *__restrict__ H1b, uint16_t *__restrict__ H1lo, int keep_z)
 {
     using namespace rs;
-    __shared__ __attribute__((aligned(256))) char ring[R * SLOT];
+    __shared__ __attribute__((aligned(1024))) char ring[(NX + NW) * SLOT];
     const int n_u = min(*n_uniq_p, cap);
     if (n_u <= 0) return;
     const int r0 = (int)((int64_t)n_u * blockIdx.x / G), r1 = (int)((int64_t)n_u * (blockIdx.x + 1) / G);
     if (r0 >= r1) return;
-    const int lane = ams_lane(), wave = threadIdx.x / AMS_WAVE, h = lane >> 5, r32 = lane & 31;
+    const int n_tiles = (r1 - r0 + BM - 1) / BM;
+    const int lane = ams_lane(), h = lane >> 5, r32 = lane & 31;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / AMS_WAVE);
+    const int wm = wave >> 2, wn = wave & 3;
     constexpr size_t row_bytes = (size_t)kF * 2;
-    RsLane L;
-    {
-        // DMA group q of this wave covers slot rows 64 wave + 8 q .. + 7; lane
-        // i writes row + i / 8, physical chunk i % 8, which holds W1 chunk
-        // (i % 8) ^ rs_swz(row)
-        const int row0 = WROWS * wave + (lane >> 3);
-        L.w1 = W1;
-        L.w = 0;
-#pragma unroll
-        for (int q = 0; q < DMA_PER_WAVE; ++q) {
-            const int row = row0 + 8 * q;
-            L.dq[q] = (uint32_t)(row * row_bytes + (((lane & 7) ^ rs_swz(row)) << 4));
-        }
-        L.lds_wave = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)(ring + WROWS * wave * 128));
-    }
-    int boff[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) boff[j] = r32 * 128 + (((4 * h + j) ^ rs_swz(r32)) << 4);
+    const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)ring);
+    const uint32_t lds_x = lds0 + 4 * wave * 1024, lds_w = lds0 + NX * SLOT + 4 * wave * 1024;
 
-    for (int m0 = r0; m0 < r1; m0 += BM) {
-        const int row = m0 + 32 * wave + r32;
-        const int id = row < r1 ? uniq[row] : -1;
-        const bool ok = id >= 0 && (int64_t)id < n_rows;
-        // rows past the range or with an ID outside the table stream W1's
-        // first row instead (a valid address); their results are not stored
-        // or are replaced by the zero row's result, ReLU(b1)
-        L.a = (ok ? (const char *)T + (size_t)id * row_bytes : (const char *)W1) + 64 * h;
-        L.w = 0;
-        const uint64_t okmask = ams_ballot(ok);
-        const bool wave_live = m0 + 32 * wave < r1;
+    // this lane's DMA rows: slot row 32 wave + 8 q + lane / 8, chunk lane % 8
+    // holding source chunk (lane % 8) ^ rs_swz(slot row)
+    int co[DMA];
+    uint32_t wdq[DMA];
+#pragma unroll
+    for (int q = 0; q < DMA; ++q) {
+        const int srow = 32 * wave + 8 * q + (lane >> 3);
+        co[q] = ((lane & 7) ^ rs_swz(srow)) << 4;
+        wdq[q] = (uint32_t)(srow * row_bytes) + co[q];
+    }
+    // the tile rows of this lane's DMAs: 32 wave + 4 (lane / 8) + q
+    const int lrow = 32 * wave + 4 * (lane >> 3);
+    auto row_src = [&](int id, int r, int q) -> const char * {
+        const bool ok = r < r1 && id >= 0 && (int64_t)id < n_rows;
+        return (ok ? (const char *)T + (size_t)id * row_bytes : (const char *)rs_zero_row) + co[q];
+    };
+    // operand read offsets: A slot row 128 wm + 32 rb + r32, B slot row
+    // 64 wn + 32 cb + r32, k step j taking chunk 2 j + h (k = 16 j + 8 h ..)
+    int ao[4], bo[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+        const int c = ((2 * j + h) ^ rs_swz(r32)) << 4;
+        ao[j] = (128 * wm + r32) * 128 + c;
+        bo[j] = (64 * wn + r32) * 128 + c;
+    }
+    // prologue: the biases and tile 0's IDs (waited for here, before any
+    // DMA is in flight), then X(0), W(0), X(1)
+    float bias[2];
+#pragma unroll
+    for (int cb = 0; cb < 2; ++cb) bias[cb] = b1[64 * wn + 32 * cb + r32];
+    const char *xp[DMA];
+#pragma unroll
+    for (int q = 0; q < DMA; ++q) {
+        const int r = r0 + lrow + q;
+        xp[q] = row_src(uniq[min(r, r1 - 1)], r, q);
+    }
+    asm volatile("" ::"v"(bias[0]), "v"(bias[1]), "v"(xp[0]), "v"(xp[1]), "v"(xp[2]), "v"(xp[3]));
+    const char *wb = (const char *)W1;
+    uint32_t xs_d = 0;                       // X slot the next row DMA fills (bytes from the ring)
+#pragma unroll
+    for (int q = 0; q < DMA; ++q) {
+        rs_dma_row(xp[q], lds_x + q * 1024);
+        xp[q] += 128;
+        asm volatile("" : "+v"(xp[q]));
+    }
+#pragma unroll
+    for (int q = 0; q < DMA; ++q) rs_dma16(wb, wdq[q], lds_w + q * 1024);
+    wb += 128;
+#pragma unroll
+    for (int q = 0; q < DMA; ++q) {
+        rs_dma_row(xp[q], lds_x + SLOT + q * 1024);
+        xp[q] += 128;
+        asm volatile("" : "+v"(xp[q]));
+    }
+    xs_d = 2 * SLOT;
+    uint32_t xs_c = 0;                       // X slot the next stage computes from
+    int idn[DMA];
+
+    for (int m = 0; m < n_tiles; ++m) {
+        const int m0 = r0 + m * BM;
+        const bool live = m0 + 128 * wm < r1;     // (uniform per wave)
         v16f acc[8];
 #pragma unroll
-        for (int nb = 0; nb < 8; ++nb) acc[nb] = (v16f){};
-        u32x4 A[NA][4];
+        for (int x = 0; x < 8; ++x) acc[x] = (v16f){};
 #pragma unroll
-        for (int t = -PA; t < 0; ++t) rs_issue(L, t, A);
+        for (int k = 0; k < S; ++k) {
+            // this stage's rows and W1 slice have landed (all waves: the
+            // barrier), and every wave is done with the slots refilled below
+            if (k == 1)
+                asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(WAIT_AFTER_IDS) : "memory");
+            else
+                asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(WAIT) : "memory");
+            __builtin_amdgcn_sched_barrier(0);
+            if (k == 2) {
+                // the ID loads of stage 0 have landed: until here their
+                // registers stay reserved whatever uses the values later
 #pragma unroll
-        for (int s = 0; s < S; ++s) {
-            // this stage's W1 DMA (this wave's part) and rows have landed; the
-            // registers are inputs (not tied outputs), so the allocator has no
-            // reason to move them, and the scheduling barrier keeps their uses
-            // below
-            asm volatile("s_waitcnt vmcnt(%4) lgkmcnt(0)" ::"v"(A[s % NA][0]), "v"(A[s % NA][1]),
-                         "v"(A[s % NA][2]), "v"(A[s % NA][3]), "n"(WAIT));
+                for (int q = 0; q < DMA; ++q) asm volatile("" : "+v"(idn[q]));
+            }
+            __builtin_amdgcn_s_barrier();
             __builtin_amdgcn_sched_barrier(0);
-            __builtin_amdgcn_s_barrier();             // ... every wave's DMA, and slot s - 1 is free
+            // W1 of the next stage (k + 1, the next tile's 0 after 63)
+#pragma unroll
+            for (int q = 0; q < DMA; ++q) rs_dma16(wb, wdq[q], lds_w + ((k + 1) & 1) * SLOT + q * 1024);
+            wb = (k == S - 2) ? (const char *)W1 : wb + 128;
+            asm volatile("" : "+s"(wb));
+            // rows of stage k + 2 (the next tile's first two from k = S - 2)
+            if (k == S - 2) {
+#pragma unroll
+                for (int q = 0; q < DMA; ++q) xp[q] = row_src(idn[q], m0 + BM + lrow + q, q);
+            }
+#pragma unroll
+            for (int q = 0; q < DMA; ++q) {
+                rs_dma_row(xp[q], lds_x + xs_d + q * 1024);
+                xp[q] += 128;
+                asm volatile("" : "+v"(xp[q]));
+            }
+            xs_d = xs_d == (NX - 1) * SLOT ? 0 : xs_d + SLOT;
+            if (k == 0) {
+                // the next tile's IDs (rows past the range are clamped, then zero rows)
+#pragma unroll
+                for (int q = 0; q < DMA; ++q) rs_ld_id(idn[q], uniq + min(m0 + BM + lrow + q, r1 - 1));
+            }
             __builtin_amdgcn_sched_barrier(0);
-            rs_issue(L, s, A);
-            __builtin_amdgcn_sched_barrier(0);
-            const u32x4 av[4] = {A[s % NA][0], A[s % NA][1], A[s % NA][2], A[s % NA][3]};
-            rs_compute(ring + (s % R) * SLOT, av, acc, boff, wave_live);
+            if (live) rs_compute(ring + xs_c, ring + NX * SLOT + (k & 1) * SLOT, ao, bo, acc);
+            xs_c = xs_c == (NX - 1) * SLOT ? 0 : xs_c + SLOT;
             __builtin_amdgcn_sched_barrier(0);        // the products stay ahead of the next wait
         }
-        // every register the loads past the last stage may still write stays
-        // allocated until they have landed
-#pragma unroll
-        for (int u = 0; u < NA; ++u)
-            asm volatile("s_waitcnt vmcnt(0)" ::"v"(A[u][0]), "v"(A[u][1]), "v"(A[u][2]), "v"(A[u][3]) : "memory");
-        __builtin_amdgcn_sched_barrier(0);
-        __builtin_amdgcn_s_barrier();                 // the ring is free for the next tile
-        __builtin_amdgcn_sched_barrier(0);
-        if (!wave_live) continue;
-        float bias[8];
-#pragma unroll
-        for (int nb = 0; nb < 8; ++nb) bias[nb] = b1[nb * 32 + r32];
-        // this lane's accumulator rows are 4 h + 8 (j / 4) + j % 4 of the wave's 32
-        const int rbase = m0 + 32 * wave + 4 * h;
-        // opaque per-tile bases: keeps the compiler from hoisting (and
-        // spilling) the tile-invariant parts of 32 row addresses
-        uint16_t *hb = H1b + (size_t)rbase * BN + r32, *hl = H1lo + (size_t)rbase * BN + r32;
+        if (!live) continue;
+        // accumulator element j of block (rb, cb): slot row 128 wm + 32 rb +
+        // 8 (j / 4) + 4 h + j % 4, i.e. tile row 32 (4 wm + rb) + 16 h + 4 (j % 4) + j / 4;
+        // unit 64 wn + 32 cb + r32
+        const int rbase = m0 + 128 * wm + 16 * h;
+        typedef __attribute__((address_space(1))) uint16_t gu16;
+        gu16 *hb = (gu16 *)(H1b + (size_t)rbase * BN + 64 * wn + r32);
+        gu16 *hl = (gu16 *)(H1lo + (size_t)rbase * BN + 64 * wn + r32);
         asm volatile("" : "+v"(hb), "+v"(hl));
-        const uint32_t okh = (uint32_t)(okmask >> (4 * h));      // bit dr: row 4 h + dr has a table row
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-            const int dr = 8 * (j >> 2) + (j & 3);
-            if (rbase + dr >= r1) continue;
-            const bool rok = (okh >> dr) & 1u;
-            uint16_t *pb = hb + dr * BN;
-            uint16_t *pl = hl + dr * BN;
+        for (int rb = 0; rb < 4; ++rb)
 #pragma unroll
-            for (int nb = 0; nb < 8; ++nb) {
-                const float z0 = rok ? acc[nb][j] + bias[nb] : bias[nb];
-                const float z = keep_z ? z0 : fmaxf(z0, 0.f);
-                const uint16_t hi = ams_f32_to_bf16(z);
-                pb[nb * 32] = hi;
-                pl[nb * 32] = ams_f32_to_bf16(z - ams_bf16_to_f32(hi));
+            for (int j = 0; j < 16; ++j) {
+                const int dr = 32 * rb + 4 * (j & 3) + (j >> 2);
+                if (rbase + dr >= r1) continue;
+#pragma unroll
+                for (int cb = 0; cb < 2; ++cb) {
+                    const float z0 = acc[rb * 2 + cb][j] + bias[cb];
+                    const float z = keep_z ? z0 : fmaxf(z0, 0.f);
+                    const uint16_t hi = ams_f32_to_bf16(z);
+                    hb[dr * BN + 32 * cb] = hi;
+                    hl[dr * BN + 32 * cb] = ams_f32_to_bf16(z - ams_bf16_to_f32(hi));
+                }
             }
-        }
     }
+    // the DMAs issued past the last stage land before the block leaves
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
 // ------------------------------------------- float32 layer 1 on bf16 MFMA

@@ -1,15 +1,15 @@
-"""The bf16 row-split first layer issues its stage loads from inline assembly
-and waits for them with explicit s_waitcnt counts, so the compiler does not
-know that those registers are still being written.  This test compiles
-embed.hip for gfx950 and checks, on the generated assembly, what that design
-relies on:
+"""The bf16 row-split first layer issues its stage memory operations (W1 and
+feature-row DMAs into LDS, the next tile's ID loads) from inline assembly and
+waits for them with explicit s_waitcnt counts, so the compiler does not know
+that the ID registers are still being written.  This test compiles embed.hip
+for gfx950 and checks, on the generated assembly, what that design relies on:
 
   * no instruction reads or writes a register that an inline-assembly load
     has not finished writing (simulating the in-order vector-memory queue in
     program order, and the loop bodies a second time for their back edges);
   * no spill (scratch) access and no other vector-memory wait inside the
     stage code, where it would not be counted;
-  * one explicit wait per stage.
+  * one explicit wait per stage, with the counts the issue order needs.
 """
 import os
 import re
@@ -108,15 +108,20 @@ def test_no_register_is_touched_before_its_load_lands(kernel_asm):
 
 def test_stage_code_has_no_spills_and_only_the_explicit_waits(kernel_asm):
     body, in_asm = parse(kernel_asm)
-    loads = [i for i, l in enumerate(body) if l.startswith("global_load_dwordx4") and in_asm[i]]
-    first, last = loads[0], loads[-1]
+    dmas = [i for i, l in enumerate(body) if l.startswith("global_load_lds_dwordx4") and in_asm[i]]
+    first, last = dmas[0], dmas[-1]
     region = body[first:last + 1]
     assert not [l for l in region if l.startswith("scratch_")]
     waits = [l for l in region if re.match(r"s_waitcnt\s+.*vmcnt", l)]
-    stages, pa, pw = rs_constant("kF") // rs_constant("KS"), rs_constant("PA"), rs_constant("PW")
-    waves = rs_constant("kThreads") // 64
-    wait = (pw - 1) * (4 + 32 // waves)        # 4 row loads and the wave's share of 32 W1 DMAs per stage
-    assert waits and set(waits) == {waits[0]} and f"vmcnt({wait})" in waits[0], set(waits)
-    # four row loads per stage: the prologue's PA stages and one issued by each stage
-    assert len(loads) == 4 * (pa + stages)
-    assert len(waits) == stages
+    stages = rs_constant("kF") // rs_constant("KS")
+    dma, wait, wait_ids = rs_constant("DMA"), rs_constant("WAIT"), rs_constant("WAIT_AFTER_IDS")
+    plain = [w for w in waits if f"vmcnt({wait})" in w]
+    after_ids = [w for w in waits if f"vmcnt({wait_ids})" in w]
+    # every stage waits once: the stage after the ID loads with the larger count
+    assert len(plain) == stages - 1 and len(after_ids) == 1 and len(waits) == stages, set(waits)
+    assert all("lgkmcnt(0)" in w for w in waits)
+    # the prologue's three slots (rows, W1, rows) and two slots per stage
+    assert len(dmas) == 3 * dma + 2 * dma * stages
+    # the next tile's four ID loads, once per tile, from inline assembly
+    ids = [i for i in range(first, last + 1) if body[i].startswith("global_load_dword ") and in_asm[i]]
+    assert len(ids) == 4
