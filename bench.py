@@ -68,7 +68,7 @@ def flops_per_unique(dims):
 # Algorithmic work of the layer-1 GEMM kernels per unique image: 2*F*H flops
 # and one read of the image's F-wide feature row.
 GEMM_KERNELS = ("l1sk_f32", "l1sk_bf16", "l1rs_bf16", "l1sk_x3", "l1_fwd_f32", "l1_fwd_bf16", "dw1_part_f32",
-                "dw1_part_bf16", "dw1_part")
+                "dw1_part_bf16", "dw1_rs_bf16", "dw1_part")
 
 
 def gemm_work_per_unique(dims, esz):

@@ -2498,9 +2498,9 @@ __global__ __launch_bounds__(kDwThreads) void dw1_part_f32(const float *__restri
 // ring like the fp32 kernel.  16-byte chunks are stored at chunk ^ 4 (row & 3):
 // the 4 rows x 64 bytes that a half-wave's transpose reads touch then fall
 // in distinct banks.  Waves are 4 (h) x 2 (f), 64 x 64 each.
-// BN = 128: 64 unique images per stage (48 KB slots); BN = 256 (for large
-// unique counts): 32 per stage (32 KB slots), each feature row gathered in
-// 512-byte pieces, half the dZ1 re-reads of BN = 128.
+// BN = 128 (64 unique images per stage, 48 KB slots) serves the smaller
+// unique counts; from kDwTrWideCap slots on, 256-column tiles run as
+// dw1_rs_bf16 (below), which keeps the same operand layout.
 template <int BN_>
 struct DwTrT {
     static constexpr int BM = 256, BN = BN_, BK = BN_ == 256 ? 32 : 64, WAVES = 8;
@@ -2699,6 +2699,194 @@ __global__ __launch_bounds__(DwTrT<BN>::WAVES * AMS_WAVE) void dw1_part_bf16(
             for (int j = 0; j < 16; ++j) {
                 const int row = wm * 64 + mb * 32 + acc_row(j, lane);
                 out[(size_t)row * F + col] = acc[mb * R::NB + nb][j];
+            }
+        }
+}
+
+// ---- bf16 dW1 for large unique counts ----
+// Partial dW1 of chunk c (of KC) over feature columns n0 .. n0 + 255, the
+// same contraction and operand layout as dw1_part_bf16, with 256-column tiles (a block owns all 256
+// hidden rows x 256 feature columns of one chunk of the unique images; 8
+// waves in 4 (m) x 2 (n), each 64 x 128) with the first layer's row-split
+// pipeline: a stage is 64 unique images (2048 MFMA cycles per SIMD, so the
+// fixed cost of a stage is paid half as often), the dZ1 rows of a stage
+// (64 x 512 bytes, an L2 hit for all but the first of the chunk's 16 column
+// blocks, which run on one XCD) move by DMA into a 2-slot LDS ring one stage
+// ahead, and the stage's pieces of the gathered feature rows (64 x 512
+// bytes, the HBM stream) by non-temporal DMA into a 3-slot ring two stages
+// ahead; every DMA instruction reads two whole 512-byte row pieces.  The
+// IDs of a stage's rows are uniform per wave (its 8 rows) and come by
+// scalar loads one stage before their DMA is issued, so the vector memory
+// queue holds only DMAs and each stage waits with s_waitcnt vmcnt(4): the
+// next stage's feature rows may stay in flight.  Slot rows are 512 bytes,
+// swizzled by 16-byte chunk as dwtr_swz (for the transposed operand reads);
+// stages past the chunk DMA the zero row.
+namespace dwr {
+constexpr int kThreads = 512;
+constexpr int kWaves = kThreads / AMS_WAVE;
+constexpr int BM = 256, BN = 256, BK = 64;    // hidden rows, feature columns, images per stage
+constexpr int KK = BK / 16;                   // MFMA k steps per stage
+constexpr int NB = BN / 64;                   // 32-column blocks per wave (a wave spans BN / 2 columns)
+constexpr int NA = 2, NX = 3;                 // dZ1 slots (1 stage ahead), feature-row slots (2 ahead)
+constexpr int SLOT = BK * 512;                // 32 KB: 64 rows of 512 bytes (both operands)
+constexpr int DMA = 4;                        // DMA instructions per wave and slot (2 rows each)
+constexpr int WAIT = 4;                       // ops a stage may leave in flight (the next stage's rows)
+static_assert(BM * 2 == 512 && BN * 2 == 512, "both operands have 512-byte slot rows");
+static_assert((NA + NX) * SLOT <= 160 * 1024, "the rings fit the LDS");
+static_assert(DMA * 1024 * kWaves == SLOT && kWaves == 8, "8 slot rows per wave, 2 per DMA instruction");
+static_assert(WAIT == DMA, "wait count follows the issue order");
+}  // namespace dwr
+
+__device__ __forceinline__ void dwr_dma(const char *src, uint32_t lds_addr)
+{
+    asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off"
+                 :
+                 : "s"(lds_addr), "v"(src)
+                 : "memory", "m0");
+}
+
+// One stage's products: A = dZ1 slot [image][hidden], B = feature slot
+// [image][column]; both operands by transposed 8-byte reads (dwtr_compute's
+// lane mapping), the next k step's reads issued while this one's products run.
+__device__ __forceinline__ void dwr_compute(const char *A, const char *B, v16f (&acc)[2 * dwr::NB], int lane,
+                                            int wave)
+{
+    using namespace dwr;
+    const int g = lane >> 4, i = lane & 15;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int r_in = 8 * (g >> 1) + (i >> 2);
+    const int c_in = 16 * (g & 1) + 4 * (i & 3);
+    uint4 a[KK][2], b[KK][NB];
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+        const int r0 = 16 * kk + r_in;
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb) {
+            const int col = wm * 64 + mb * 32 + c_in;
+            const uint2 lo = ds_read_tr16(A + dwtr_off(r0, col, 512));
+            const uint2 hi = ds_read_tr16(A + dwtr_off(r0 + 4, col, 512));
+            a[kk][mb] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        }
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            const int col = wn * (BN / 2) + nb * 32 + c_in;
+            const uint2 lo = ds_read_tr16(B + dwtr_off(r0, col, 512));
+            const uint2 hi = ds_read_tr16(B + dwtr_off(r0 + 4, col, 512));
+            b[kk][nb] = make_uint4(lo.x, lo.y, hi.x, hi.y);
+        }
+    }
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk)
+#pragma unroll
+        for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb) acc[mb * NB + nb] = mfma_bf16(a[kk][mb], b[kk][nb], acc[mb * NB + nb]);
+    __builtin_amdgcn_sched_group_barrier(0x100, 4 + 2 * NB, 0);
+#pragma unroll
+    for (int kk = 0; kk < KK; ++kk) {
+        if (kk < KK - 1) __builtin_amdgcn_sched_group_barrier(0x100, 4 + 2 * NB, 0);
+        __builtin_amdgcn_sched_group_barrier(0x008, 2 * NB, 0);
+    }
+}
+
+__global__ __launch_bounds__(dwr::kThreads) __attribute__((amdgpu_waves_per_eu(2, 2))) void dw1_rs_bf16(
+    const uint16_t *__restrict__ T, int64_t n_rows, int F, const int32_t *__restrict__ uniq,
+    const int32_t *__restrict__ n_uniq_p, int cap, const uint16_t *__restrict__ dZ1, int KC,
+    float *__restrict__ part)
+{
+    using namespace dwr;
+    __shared__ __attribute__((aligned(1024))) char ring[(NA + NX) * SLOT];
+    const int nnt = F / BN;
+    // the column tiles of one chunk go to one XCD: they share its dZ1 rows
+    int c, nt;
+    if (!xcd_tile(blockIdx.x, KC, nnt, c, nt)) return;
+    const int n_u = min(*n_uniq_p, cap);
+    const int u0 = (int)((int64_t)c * n_u / KC), u1 = (int)((int64_t)(c + 1) * n_u / KC);
+    const int n0 = nt * BN;
+    const int lane = ams_lane();
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / AMS_WAVE);
+
+    v16f acc[2 * NB];
+#pragma unroll
+    for (int x = 0; x < 2 * NB; ++x) acc[x] = (v16f){};
+    const int S = (u1 - u0 + BK - 1) / BK;
+    if (S > 0) {
+        const uint32_t lds0 = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)ring);
+        const uint32_t lds_a = lds0 + 4 * wave * 1024, lds_x = lds0 + NA * SLOT + 4 * wave * 1024;
+        // DMA instruction q of this wave: slot rows 8 wave + 2 q + lane / 32,
+        // chunk lane % 32 holding source chunk (lane % 32) ^ dwtr_swz(row)
+        const int half = lane >> 5;
+        int co[DMA];
+#pragma unroll
+        for (int q = 0; q < DMA; ++q) co[q] = ((lane & 31) ^ dwtr_swz(8 * wave + 2 * q + half)) << 4;
+        const char *zero = (const char *)rs_zero_row;
+        asm volatile("" : "+s"(zero));             // once, not per DMA
+        auto a_src = [&](int s, int q) -> const char * {
+            const int u = u0 + s * BK + 8 * wave + 2 * q + half;
+            return (u < u1 ? (const char *)(dZ1 + (size_t)u * BM) : zero) + co[q];
+        };
+        // the IDs of stage s's rows 8 wave .. + 7 (uniform per wave)
+        auto load_ids = [&](int s, int (&id)[8]) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                const int u = u0 + s * BK + 8 * wave + e;
+                const int v = uniq[min(u, u1 - 1)];
+                id[e] = u < u1 ? v : -1;
+            }
+        };
+        auto x_src = [&](const int (&id)[8], int q) -> const char * {
+            // lane half 0 takes row 2 q, half 1 row 2 q + 1 (a select, not an
+            // indexed read, which would put the IDs in scratch memory)
+            const int v = id[2 * q] + ((id[2 * q + 1] - id[2 * q]) & -half);
+            const bool ok = v >= 0 && (int64_t)v < n_rows;
+            const char *row = (const char *)(T + (size_t)(ok ? v : 0) * F + n0);
+            return (ok ? row : zero) + co[q];
+        };
+        // prologue: X(0), dZ1(0), X(1), in the order a stage issues them
+        int id[8];
+        load_ids(0, id);
+#pragma unroll
+        for (int q = 0; q < DMA; ++q) rs_dma_row(x_src(id, q), lds_x + q * 1024);
+#pragma unroll
+        for (int q = 0; q < DMA; ++q) dwr_dma(a_src(0, q), lds_a + q * 1024);
+        load_ids(1, id);
+#pragma unroll
+        for (int q = 0; q < DMA; ++q) rs_dma_row(x_src(id, q), lds_x + SLOT + q * 1024);
+        load_ids(2, id);
+        uint32_t xs_d = 2 * SLOT, xs_c = 0;       // feature slot to fill next, to compute from next
+        for (int s = 0; s < S; ++s) {
+            // stage s's dZ1 and feature rows have landed (all waves: the
+            // barrier), and every wave is done with the slots refilled below
+            asm volatile("s_waitcnt vmcnt(%0) lgkmcnt(0)" ::"n"(WAIT) : "memory");
+            __builtin_amdgcn_sched_barrier(0);
+            __builtin_amdgcn_s_barrier();
+            __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+            for (int q = 0; q < DMA; ++q) dwr_dma(a_src(s + 1, q), lds_a + ((s + 1) & 1) * SLOT + q * 1024);
+#pragma unroll
+            for (int q = 0; q < DMA; ++q) rs_dma_row(x_src(id, q), lds_x + xs_d + q * 1024);
+            xs_d = xs_d == (NX - 1) * SLOT ? 0 : xs_d + SLOT;
+            __builtin_amdgcn_sched_barrier(0);
+            dwr_compute(ring + (s & 1) * SLOT, ring + NA * SLOT + xs_c, acc, lane, wave);
+            xs_c = xs_c == (NX - 1) * SLOT ? 0 : xs_c + SLOT;
+            __builtin_amdgcn_sched_barrier(0);
+            load_ids(s + 3, id);                   // for the feature rows the next stage issues
+        }
+        // the DMAs issued past the last stage land before the block leaves
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    }
+
+    float *out = part + (size_t)c * BM * F;
+    const int wm = wave >> 1, wn = wave & 1;
+#pragma unroll
+    for (int mb = 0; mb < 2; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) {
+            const int col = n0 + wn * (BN / 2) + nb * 32 + (lane & 31);
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const int row = wm * 64 + mb * 32 + acc_row(j, lane);
+                out[(size_t)row * F + col] = acc[mb * NB + nb][j];
             }
         }
 }
@@ -3427,10 +3615,10 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
     } else if (use_dw_tr(mlp)) {
         const int bn = dwtr_bn(F, cap);
         const int gtr = ((p.kc + 7) / 8) * 8 * (F / bn);
-        if (bn == 256)
-            AMS_LAUNCH("dw1_part_bf16", st, dw1_part_bf16<256><<<gtr, DwTrT<256>::WAVES * AMS_WAVE, 0, st>>>(
-                                                (const uint16_t *)T, n_rows, F, uniq, n_uniq, cap, (const uint16_t *)dz1,
-                                                p.kc, zero, dw1p));
+        if (bn == 256)          // (use_dw_tr: H = 256)
+            AMS_LAUNCH("dw1_rs_bf16", st, dw1_rs_bf16<<<gtr, dwr::kThreads, 0, st>>>(
+                                              (const uint16_t *)T, n_rows, F, uniq, n_uniq, cap, (const uint16_t *)dz1,
+                                              p.kc, dw1p));
         else
             AMS_LAUNCH("dw1_part_bf16", st, dw1_part_bf16<128><<<gtr, DwTr::WAVES * AMS_WAVE, 0, st>>>(
                                                 (const uint16_t *)T, n_rows, F, uniq, n_uniq, cap, (const uint16_t *)dz1,

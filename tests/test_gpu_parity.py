@@ -290,19 +290,17 @@ def test_pool_bwd_sum_unit_gradient_is_exact_multiplicity(wname):
 
 # ------------------------------------------------------------ embed bwd
 
-@pytest.mark.parametrize("wname", ["tiny", "mid_f32", "mid_bf16"])
-def test_embed_bwd_matches_oracle(wname):
-    w = synth.get("tiny") if wname == "tiny" else mid(wname[4:])
-    batch, dd, Ws, bs, T_u = embed_case(w)
-    n_u = dd["n_uniq"]
-    print(f"embed bwd {wname}: n_u={n_u}", flush=True)
-    fo = oracle.mlp_fwd(T_u, np.arange(n_u), Ws, bs)
+def run_embed_bwd(w, uniq_np, T_rows, Ws, bs, cap):
+    """ams_embed_bwd on the saved activations of the oracle's forward over
+    T_rows (the feature rows of uniq_np, zero rows for IDs outside the
+    table) against the oracle's backward, at capacity cap."""
+    n_u = len(uniq_np)
+    fo = oracle.mlp_fwd(T_rows, np.arange(n_u), Ws, bs)
     rng = np.random.default_rng(5)
     dE32 = rng.standard_normal((n_u, w.out_dim)).astype(np.float32)
-    bo = oracle.mlp_bwd(T_u, np.arange(n_u), Ws, fo, dE32)
+    bo = oracle.mlp_bwd(T_rows, np.arange(n_u), Ws, fo, dE32)
     T_dev = synth.table_rows(w, np.arange(w.n_images), device="cuda")
     mlp = ams.make_mlp(w.dims, w.dtype)
-    cap = n_u + 40
     h1dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
     H1 = torch.zeros((cap, w.dims[1]), dtype=h1dt, device="cuda")
     H1[:n_u] = torch.from_numpy(np.maximum(fo["Z"][0], 0)).to(h1dt).cuda()
@@ -313,7 +311,7 @@ def test_embed_bwd_matches_oracle(wname):
     dE = torch.zeros((cap, w.out_dim), device="cuda")
     dE[:n_u] = torch.from_numpy(dE32).cuda()
     uniq = torch.zeros(cap, dtype=torch.int32, device="cuda")
-    uniq[:n_u] = cuda_i32(dd["uniq"])
+    uniq[:n_u] = cuda_i32(uniq_np)
     nu = torch.tensor([n_u], dtype=torch.int32, device="cuda")
     dW = [torch.full((o, i), float("nan"), device="cuda") for i, o in zip(w.dims[:-1], w.dims[1:])]
     db = [torch.full((o,), float("nan"), device="cuda") for o in w.dims[1:]]
@@ -324,6 +322,34 @@ def test_embed_bwd_matches_oracle(wname):
     for l in range(w.n_layers):
         assert_close(dW[l], bo["dW"][l], rt, f"dW{l + 1}")
         assert_close(db[l], bo["db"][l], rt, f"db{l + 1}")
+
+
+@pytest.mark.parametrize("wname", ["tiny", "mid_f32", "mid_bf16"])
+def test_embed_bwd_matches_oracle(wname):
+    w = synth.get("tiny") if wname == "tiny" else mid(wname[4:])
+    batch, dd, Ws, bs, T_u = embed_case(w)
+    print(f"embed bwd {wname}: n_u={dd['n_uniq']}", flush=True)
+    run_embed_bwd(w, dd["uniq"], T_u, Ws, bs, dd["n_uniq"] + 40)
+
+
+@pytest.mark.parametrize("case", ["mid", "few_rows", "bad_ids"])
+def test_embed_bwd_bf16_wide_capacity_matches_oracle(case):
+    """From a capacity of 2 x 256 x 256 unique slots the bf16 dW1 takes each
+    chunk of the unique images in stages of 64 with the feature rows DMA'd
+    two stages ahead; mid-size and tiny batches at that capacity give chunks
+    of a few stages, a single ragged stage or none."""
+    w = mid("bf16")
+    batch, dd, Ws, bs, T_u = embed_case(w)
+    uniq, T_rows = dd["uniq"].copy(), T_u
+    if case == "few_rows":
+        uniq, T_rows = uniq[:100], T_u[:100]
+    if case == "bad_ids":                        # out-of-range IDs read as zero rows
+        bad = [3, 700, len(uniq) - 1]
+        uniq[bad] = [w.n_images + 5, -3, w.n_images]
+        T_rows = T_rows.clone()
+        T_rows[bad] = 0
+    print(f"embed bwd wide {case}: n_u={len(uniq)} cap={ROW_SPLIT_CAP + 13}", flush=True)
+    run_embed_bwd(w, uniq, T_rows, Ws, bs, ROW_SPLIT_CAP + 13)
 
 
 # ---------------------------------------------------------- whole step
