@@ -225,17 +225,22 @@ def bench_peaks(args):
     T = torch.empty((w.n_images, w.in_dim), dtype=torch.bfloat16, device="cuda")
     T.view(torch.int16).random_(-32768, 32767)
     row_bytes = w.in_dim * 2
+    W = torch.empty(256 * w.in_dim, dtype=torch.bfloat16, device="cuda").normal_()
+    patterns = {0: "registers, 16-byte pieces of 32 rows per load (MFMA operand layout)",
+                1: "registers, whole 128-byte lines (8 rows per load)",
+                2: "registers, whole lines, non-temporal",
+                3: "LDS DMA ring, whole lines, non-temporal",
+                4: "LDS DMA ring, whole lines, non-temporal, plus a 32 KB weight slice per stage from L2"}
     gather = {}
-    variants = [(128, 128, 256), (256, 128, 256), (128, 1024, 256), (32, row_bytes, 256)]
-    variants += [(tile, chunk, blocks) for blocks in (1024, 2048) for tile, chunk in
-                 ((128, 128), (128, 256), (128, 512), (64, 1024), (32, 2048), (16, row_bytes))]
-    variants += [(8, row_bytes, 4096)]
-    for tile, chunk, blocks in variants:
-        t = timed(lambda: ams.ams_peak_gather(T, rows, tile, chunk, blocks, sink))
-        gather[f"tile{tile}_chunk{chunk}_blocks{blocks}"] = {"bytes_per_s": rows.numel() * row_bytes / t,
-                                                             "seconds": t}
-    res["gather_c3_unique_rows"] = {"rows": int(rows.numel()), "row_bytes": row_bytes, "variants": gather}
-    del T
+    for pat, what in patterns.items():
+        for blocks in (256, 512):
+            t = timed(lambda: ams.ams_peak_gather(T, rows, pat, blocks, sink, W=W))
+            gather[f"pattern{pat}_blocks{blocks}"] = {"what": what, "bytes_per_s": rows.numel() * row_bytes / t,
+                                                      "seconds": t}
+    res["gather_c3_unique_rows"] = {"rows": int(rows.numel()), "row_bytes": row_bytes, "variants": gather,
+                                    "note": "512-thread blocks, each a contiguous range of the ascending unique-row list "
+                                            "in 256-row tiles, 64 stages of 128 bytes per row, 3 stages in flight"}
+    del T, W
     out = torch.empty(4096 * 256, device="cuda")
     for dt, flops in (("bf16", 32768), ("f32", 4096)):
         # random operands (the MFMA rate depends on the data through the clock)

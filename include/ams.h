@@ -509,13 +509,21 @@ ams_status ams_adam_update(int64_t n, float *param, const float *grad, float *m,
  * ams_peak_copy    dst = src, `bytes` (a multiple of 16), grid-stride.
  * ams_peak_read    reads `bytes` of src; out[blocks * 256] receives one xor
  *                  per thread.
- * ams_peak_gather  reads rows[0..n) of the table T [n_table x row_bytes]:
- *                  each block a contiguous range of the list, in tiles of
- *                  `tile` rows, each tile in stages of `chunk` bytes per row
- *                  (row_bytes a multiple of chunk, chunk a multiple of 16;
- *                  chunk == row_bytes reads each row whole); a row index
- *                  outside [0, n_table) reads row 0; out[blocks * 256] as
- *                  ams_peak_read.
+ * ams_peak_gather  reads rows[0..n) of the table T [n_table x 8192 bytes]
+ *                  (row_bytes must be 8192, else SIZE) the way the bf16
+ *                  first layer visits them: 512-thread blocks, each a
+ *                  contiguous range of the list in tiles of 256 rows, a tile
+ *                  in 64 stages of 128 bytes per row, 3 stages ahead.
+ *                  pattern 0: register loads, each lane 16-byte pieces of
+ *                  its own row (every load touches 32 rows: the MFMA operand
+ *                  layout); 1: register loads of whole 128-byte lines (8 rows
+ *                  per load); 2: as 1, non-temporal; 3: whole-line
+ *                  non-temporal DMA into a 3-slot LDS ring, 2 stages ahead,
+ *                  one barrier per stage; 4: as 3 plus a 32 KB slice of W
+ *                  (2 MB: 256 rows of 8192 bytes, needed only here) per stage
+ *                  into a 2-slot ring.  Other patterns: MODE.  A row index
+ *                  outside [0, n_table) reads row 0; out[blocks * 512]
+ *                  receives one xor per thread.
  * ams_peak_mfma    dtype AMS_BF16 (v_mfma_f32_32x32x16_bf16, 32768 flops) or
  *                  AMS_F32 (v_mfma_f32_32x32x2_f32, 4096 flops): every wave
  *                  runs iters x 16 independent products on operands read from
@@ -524,7 +532,7 @@ ams_status ams_adam_update(int64_t n, float *param, const float *grad, float *m,
 ams_status ams_peak_copy(const void *src, void *dst, int64_t bytes, int32_t blocks, void *stream);
 ams_status ams_peak_read(const void *src, int64_t bytes, int32_t blocks, uint32_t *out, void *stream);
 ams_status ams_peak_gather(const void *T, int64_t n_table, int32_t row_bytes, const int32_t *rows,
-                           int32_t n, int32_t tile, int32_t chunk, int32_t blocks, uint32_t *out,
+                           int32_t n, int32_t pattern, const void *W, int32_t blocks, uint32_t *out,
                            void *stream);
 ams_status ams_peak_mfma(int32_t dtype, const void *ops, int32_t iters, int32_t blocks, float *out,
                          void *stream);

@@ -117,7 +117,7 @@ def load() -> ctypes.CDLL:
     lib.ams_adam_update.restype = ctypes.c_int
     lib.ams_adam_update.argtypes = [i64, P, P, P, P, f, f, f, f, i64, P, P]
     for name, args in (("ams_peak_copy", [P, P, i64, i32, P]), ("ams_peak_read", [P, i64, i32, P, P]),
-                       ("ams_peak_gather", [P, i64, i32, P, i32, i32, i32, i32, P, P]),
+                       ("ams_peak_gather", [P, i64, i32, P, i32, i32, P, i32, P, P]),
                        ("ams_peak_mfma", [i32, P, i32, i32, P, P])):
         getattr(lib, name).restype = ctypes.c_int
         getattr(lib, name).argtypes = args
@@ -394,9 +394,12 @@ def ams_peak_read(src, blocks: int, out, stream=None):
            "ams_peak_read")
 
 
-def ams_peak_gather(T, rows, tile: int, chunk: int, blocks: int, out, stream=None):
+def ams_peak_gather(T, rows, pattern: int, blocks: int, out, W=None, stream=None):
+    """Gather probe over T's rows (8192 bytes each); pattern 0-4 as in ams.h
+    (4 also streams slices of W, 2 MB)."""
     _check(load().ams_peak_gather(_p(T), T.shape[0], T.shape[1] * T.element_size(), _p(rows), rows.numel(),
-                                  int(tile), int(chunk), int(blocks), _p(out), _stream(stream)), "ams_peak_gather")
+                                  int(pattern), _p(W) if W is not None else None, int(blocks), _p(out),
+                                  _stream(stream)), "ams_peak_gather")
 
 
 def ams_peak_mfma(dtype: str, ops, iters: int, blocks: int, out, stream=None):

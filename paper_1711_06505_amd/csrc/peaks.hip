@@ -41,45 +41,160 @@ __global__ __launch_bounds__(kThreads) void peak_read_k(const uint4 *__restrict_
     out[(int64_t)blockIdx.x * kThreads + threadIdx.x] = x;
 }
 
-// Gather of table rows rows[0..n) (row_bytes each) in the first layer's
-// order: each block takes a contiguous range of the list in tiles of `tile`
-// rows and visits a tile in stages of `chunk` bytes per row (stage s reads
-// bytes s*chunk .. of every row of the tile), `chunk` contiguous bytes per
-// row and stage, 16 bytes per thread and load, eight loads per thread in
-// flight.  chunk == row_bytes visits each row whole.  A row index outside
-// [0, n_table) is read as row 0.
-__global__ __launch_bounds__(kThreads) void peak_gather_k(const uint4 *__restrict__ T, int64_t n_table,
-                                                          int row_bytes, const int32_t *__restrict__ rows, int n,
-                                                          int tile, int chunk, uint32_t *__restrict__ out)
+// Gathers of 8192-byte table rows rows[0..n) the way the bf16 first layer
+// meets them: 512-thread blocks, each a contiguous range of the list in
+// tiles of 256 rows, a tile in 64 stages of 128 bytes per row (32 KB per
+// stage), loads 3 stages ahead, one xor per thread kept so no load is
+// dropped.  A row index outside [0, n_table) reads row 0.
+namespace pg {
+constexpr int kBlk = 512, kRowBytes = 8192, kStage = 128, kStages = kRowBytes / kStage, kTileRows = 256;
+constexpr int kAhead = 3;
+}
+
+// Register loads (compiler-visible, so its own waits are exact), 4 per lane
+// and stage.  ORD 0: lane (r, h) of a wave takes 16-byte pieces 4 h .. 4 h + 3
+// of its row r (the MFMA operand layout: every load touches 32 rows);
+// ORD 1: load i of a wave covers 8 whole 128-byte lines (8 rows).  NT: the
+// non-temporal hint.  The empty asm per stage takes the stage's values after
+// the loads of the stages ahead are issued.
+template <int ORD, int NT>
+__global__ __launch_bounds__(pg::kBlk) void peak_gather_reg_k(const char *__restrict__ T, int64_t n_table,
+                                                                  const int32_t *__restrict__ rows, int n,
+                                                                  uint32_t *__restrict__ out)
 {
+    using namespace pg;
+    const int lane = ams_lane(), wave = threadIdx.x / AMS_WAVE;
     const int r0 = (int)((int64_t)n * blockIdx.x / gridDim.x), r1 = (int)((int64_t)n * (blockIdx.x + 1) / gridDim.x);
-    const int per_row = chunk / 16;                 // 16-byte pieces of a row per stage
-    const int stages = row_bytes / chunk;
-    const int64_t row_u4 = row_bytes / 16;
-    uint32_t x = 0;
-    for (int m0 = r0; m0 < r1; m0 += tile) {
-        const int nr = min(tile, r1 - m0);
-        const int pieces = nr * per_row;            // 16-byte loads of one stage
-        for (int s = 0; s < stages; ++s) {
-            for (int p0 = threadIdx.x; p0 < pieces; p0 += 8 * kThreads) {
-                uint4 v[8];
+    uint4 x = make_uint4(0, 0, 0, 0);
+    for (int m0 = r0; m0 < r1; m0 += kTileRows) {
+        const char *p[4];
 #pragma unroll
-                for (int u = 0; u < 8; ++u) {
-                    const int p = p0 + u * kThreads;
-                    if (p < pieces) {
-                        int r = rows[m0 + p / per_row];
-                        if (r < 0 || r >= n_table) r = 0;
-                        v[u] = T[(int64_t)r * row_u4 + (int64_t)s * per_row + p % per_row];
-                    } else {
-                        v[u] = make_uint4(0, 0, 0, 0);
-                    }
-                }
+        for (int i = 0; i < 4; ++i) {
+            const int row = ORD == 0 ? (lane & 31) : 8 * i + (lane >> 3);
+            const int off = ORD == 0 ? 16 * (4 * (lane >> 5) + i) : 16 * (lane & 7);
+            const int r = m0 + 32 * wave + row;
+            int id = rows[r < r1 ? r : r0];
+            if (id < 0 || (int64_t)id >= n_table) id = 0;
+            p[i] = T + (size_t)id * kRowBytes + off;
+        }
+        typedef unsigned int u4 __attribute__((ext_vector_type(4)));
+        u4 v[kAhead + 1][4];
+        auto ld = [&](int st, u4 (&d)[4]) {
 #pragma unroll
-                for (int u = 0; u < 8; ++u) x ^= v[u].x ^ v[u].y ^ v[u].z ^ v[u].w;
+            for (int i = 0; i < 4; ++i) {
+                const u4 *q = (const u4 *)(p[i] + st * kStage);
+                d[i] = NT ? __builtin_nontemporal_load(q) : *q;
+            }
+        };
+#pragma unroll
+        for (int st = 0; st < kAhead; ++st) ld(st, v[st]);
+#pragma unroll
+        for (int st = 0; st < kStages; ++st) {
+            if (st + kAhead < kStages) ld(st + kAhead, v[(st + kAhead) % (kAhead + 1)]);
+            u4 (&c)[4] = v[st % (kAhead + 1)];
+            asm volatile("" : "+v"(c[0]), "+v"(c[1]), "+v"(c[2]), "+v"(c[3]));
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                x.x ^= c[i].x;
+                x.y ^= c[i].y;
+                x.z ^= c[i].z;
+                x.w ^= c[i].w;
             }
         }
     }
-    out[(int64_t)blockIdx.x * kThreads + threadIdx.x] = x;
+    out[(size_t)blockIdx.x * kBlk + threadIdx.x] = x.x ^ x.y ^ x.z ^ x.w;
+}
+
+// 16-byte DMA of every lane into LDS at lds + 16 lane (no register is written).
+template <int NT>
+__device__ __forceinline__ void pg_dma(const char *src, uint32_t lds)
+{
+    if (NT)
+        asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off nt" ::"s"(lds), "v"(src)
+                     : "memory", "m0");
+    else
+        asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, off" ::"s"(lds), "v"(src)
+                     : "memory", "m0");
+}
+
+// Whole-line DMA into a 3-slot LDS ring (non-temporal, 2 stages ahead), one
+// barrier per stage.  WSTREAM: each stage also DMAs a 32 KB slice of W (256
+// rows of 8192 bytes, an L2-resident 2 MB array) into a 2-slot ring, one
+// stage ahead, as the first layer moves its weight slices.
+template <int WSTREAM>
+__global__ __launch_bounds__(pg::kBlk) void peak_gather_dma_k(const char *__restrict__ T, int64_t n_table,
+                                                                  const int32_t *__restrict__ rows, int n,
+                                                                  const char *__restrict__ W,
+                                                                  uint32_t *__restrict__ out)
+{
+    using namespace pg;
+    constexpr int SLOT = kTileRows * kStage;                   // 32 KB
+    __shared__ __attribute__((aligned(1024))) char ring[(3 + 2 * WSTREAM) * SLOT];
+    const int lane = ams_lane(), wave = __builtin_amdgcn_readfirstlane(threadIdx.x / AMS_WAVE);
+    const int r0 = (int)((int64_t)n * blockIdx.x / gridDim.x), r1 = (int)((int64_t)n * (blockIdx.x + 1) / gridDim.x);
+    const uint32_t xb = __builtin_amdgcn_readfirstlane((uint32_t)(uintptr_t)ring) + 4 * wave * 1024;
+    const uint32_t wb = xb + 3 * SLOT;
+    uint32_t x = 0;
+    for (int m0 = r0; m0 < r1; m0 += kTileRows) {
+        // DMA q of this wave: 8 rows (32 wave + 8 q ..), whole lines
+        const char *p[4], *w[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const int r = m0 + 32 * wave + 8 * q + (lane >> 3);
+            int id = rows[r < r1 ? r : r0];
+            if (id < 0 || (int64_t)id >= n_table) id = 0;
+            p[q] = T + (size_t)id * kRowBytes + 16 * (lane & 7);
+            w[q] = WSTREAM ? W + (size_t)(32 * wave + 8 * q + (lane >> 3)) * kRowBytes + 16 * (lane & 7) : nullptr;
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        // prologue: rows of stages 0, 1; W of stage 0 between them (the order
+        // a stage issues: W of the next stage, then rows two ahead).  The
+        // pointers advance by one stage per issue (opaque to the compiler, so
+        // it does not precompute every stage's addresses)
+        auto adv = [](const char *&q, int by) {
+            q += by;
+            asm volatile("" : "+v"(q));
+        };
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            pg_dma<1>(p[q], xb + q * 1024);
+            adv(p[q], kStage);
+        }
+        if (WSTREAM) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                pg_dma<0>(w[q], wb + q * 1024);
+                adv(w[q], kStage);
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            pg_dma<1>(p[q], xb + SLOT + q * 1024);
+            adv(p[q], kStage);
+        }
+#pragma unroll
+        for (int st = 0; st < kStages; ++st) {
+            // this stage's rows (and W) landed: only the next stage's rows may be in flight
+            asm volatile("s_waitcnt vmcnt(4) lgkmcnt(0)" ::: "memory");
+            __builtin_amdgcn_s_barrier();
+            if (WSTREAM) {                          // W of stage st + 1 (the last one again past the end)
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    pg_dma<0>(w[q], wb + ((st + 1) & 1) * SLOT + q * 1024);
+                    if (st + 2 < kStages) adv(w[q], kStage);
+                }
+            }
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {           // rows of stage st + 2 (the last one again past the end)
+                pg_dma<1>(p[q], xb + ((st + 2) % 3) * SLOT + q * 1024);
+                if (st + 3 < kStages) adv(p[q], kStage);
+            }
+            x ^= *(const uint32_t *)(ring + (st % 3) * SLOT + threadIdx.x * 16);
+        }
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __builtin_amdgcn_s_barrier();
+    }
+    out[(size_t)blockIdx.x * kBlk + threadIdx.x] = x;
 }
 
 // MFMA rate on operands read from memory: each wave reads its own 16-byte
@@ -147,16 +262,22 @@ extern "C" ams_status ams_peak_read(const void *src, int64_t bytes, int32_t bloc
 }
 
 extern "C" ams_status ams_peak_gather(const void *T, int64_t n_table, int32_t row_bytes, const int32_t *rows,
-                                      int32_t n, int32_t tile, int32_t chunk, int32_t blocks, uint32_t *out,
+                                      int32_t n, int32_t pattern, const void *W, int32_t blocks, uint32_t *out,
                                       void *stream)
 {
-    if (n_table < 1 || n < 0 || tile < 1 || blocks < 1 || chunk < 16 || chunk % 16 || row_bytes % chunk)
-        return AMS_ERR_SIZE;
+    if (n_table < 1 || n < 0 || blocks < 1 || row_bytes != pg::kRowBytes) return AMS_ERR_SIZE;
+    if (pattern < 0 || pattern > 4) return AMS_ERR_MODE;
     if (n == 0) return AMS_OK;
-    if (!T || !rows || !out) return AMS_ERR_NULL;
+    if (!T || !rows || !out || (pattern == 4 && !W)) return AMS_ERR_NULL;
     hipStream_t st = (hipStream_t)stream;
-    AMS_LAUNCH("peak_gather", st, peak_gather_k<<<blocks, kThreads, 0, st>>>((const uint4 *)T, n_table, row_bytes,
-                                                                               rows, n, tile, chunk, out));
+    const char *t = (const char *)T;
+    switch (pattern) {
+    case 0: AMS_LAUNCH("peak_gather", st, peak_gather_reg_k<0, 0><<<blocks, pg::kBlk, 0, st>>>(t, n_table, rows, n, out)); break;
+    case 1: AMS_LAUNCH("peak_gather", st, peak_gather_reg_k<1, 0><<<blocks, pg::kBlk, 0, st>>>(t, n_table, rows, n, out)); break;
+    case 2: AMS_LAUNCH("peak_gather", st, peak_gather_reg_k<1, 1><<<blocks, pg::kBlk, 0, st>>>(t, n_table, rows, n, out)); break;
+    case 3: AMS_LAUNCH("peak_gather", st, peak_gather_dma_k<0><<<blocks, pg::kBlk, 0, st>>>(t, n_table, rows, n, nullptr, out)); break;
+    default: AMS_LAUNCH("peak_gather", st, peak_gather_dma_k<1><<<blocks, pg::kBlk, 0, st>>>(t, n_table, rows, n, (const char *)W, out)); break;
+    }
     return ams_launch_status();
 }
 
