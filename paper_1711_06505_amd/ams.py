@@ -600,11 +600,12 @@ class JointStep:
     channel's and yields dQ, which table t_q's ams_bag_bwd adds to the ad
     occurrences' row gradients before its Adagrad step.
 
-    With ``overlap`` (the default) the ID-table work runs on a second stream
-    of default priority, forked from the caller's stream at the start and
-    joined before the CTR call and at the end, so it hides behind the image
-    path; each stream has its own workspace.  Without it, every call is on
-    the caller's stream in the order above.  The ID tables and their Adagrad
+    With ``overlap`` (the default) each ID table's work runs on a stream of
+    its own (default priority), forked from the caller's stream at the start
+    and joined before the CTR call and at the end, so the tables' dedups, bags
+    and row updates (latency-bound kernels) overlap one another and the image
+    path's own small kernels; each stream has its own workspace.  Without it,
+    every call is on the caller's stream in the order above.  The ID tables and their Adagrad
     accumulators are caller tensors updated in place; everything else is held
     here.
     """
@@ -654,7 +655,7 @@ class JointStep:
             self.no_beh = torch.zeros(Bm + 1, dtype=i32, device=dev)      # offsets of bags holding the ad alone
         self.ws = None
         self.ws_id = None
-        self.side = torch.cuda.Stream(device=dev) if overlap else None
+        self.sides = [torch.cuda.Stream(device=dev) for _ in range(T)] if overlap else None
 
     def alloc_workspace(self, n_ids: int):
         id_need = max(ams_dedup_workspace(self.n_occ, max(self.id_rows)),
@@ -662,13 +663,13 @@ class JointStep:
         img_need = max(ams_dedup_workspace(self.n_occ, n_ids), ams_embed_workspace(self.img.mlp, self.img.cap),
                        ams_pool_workspace(self.img.mode, self.B, self.n_beh, self.img.dims[-1], self.img.cap),
                        ams_ctr_workspace(self.ctr, max(self.B, 1)), 256)
-        if self.side is None:
+        if self.sides is None:
             img_need = max(img_need, id_need)
         self.img.ws = torch.empty(img_need, dtype=torch.uint8, device=self.loss.device)
         self.img.n_ids = int(n_ids)
         self.ws = self.img.ws
-        self.ws_id = (torch.empty(id_need, dtype=torch.uint8, device=self.loss.device) if self.side is not None
-                      else self.ws)
+        self.ws_id = ([torch.empty(id_need, dtype=torch.uint8, device=self.loss.device) for _ in self.sides]
+                      if self.sides is not None else [self.ws] * len(self.id_rows))
 
     def run(self, ids, n_ids, T, W, b, seg_off, id_ids, id_tables, accum, labels, ctr_W, ctr_b, lr: float,
             eps: float, stream=None):
@@ -682,26 +683,33 @@ class JointStep:
             self.alloc_workspace(n_ids)
         st = self.img
         main = stream if stream is not None else torch.cuda.current_stream()
-        side = self.side if self.side is not None else main
+        nt = len(self.id_rows)
+        sides = self.sides if self.sides is not None else [main] * nt
+        forked = self.sides is not None
         B = seg_off.numel() - 1
-        if side is not main:
-            side.wait_stream(main)                  # the caller's inputs are ready
-            for x in [seg_off, labels] + list(id_ids) + list(id_tables) + list(accum):
-                x.record_stream(side)
+        if forked:
+            for t, sd in enumerate(sides):
+                sd.wait_stream(main)                # the caller's inputs are ready
+                for x in (seg_off, labels, id_ids[t], id_tables[t], accum[t]):
+                    x.record_stream(sd)
         tq = self.query_table
-        # ID tables: dedup (needed from bag_bwd on) and bags, beside the image forward;
-        # with a query table also each sample's ad row of it (a bag of the ad alone)
-        for t in range(len(self.id_rows)):
+        # ID tables, beside the image forward: dedup (needed from bag_bwd on) and
+        # bags; with a query table also each sample's ad row of it (a bag of the
+        # ad alone).  (Issuing the bags first and letting the CTR call wait for
+        # them alone moves the dedups into the image backward, where they meet
+        # the dW1 product that fills every CU: slower.)
+        for t in range(nt):
             ams_dedup(id_ids[t], self.id_rows[t], self.t_uniq[t], self.t_inv[t], self.t_perm[t], self.t_off[t],
-                      self.t_nu[t], self.t_status[t], self.ws_id, side)
-            ams_bag_fwd(seg_off, n_beh, id_ids[t], id_tables[t], self.bags[t], side)
+                      self.t_nu[t], self.t_status[t], self.ws_id[t], sides[t])
+            ams_bag_fwd(seg_off, n_beh, id_ids[t], id_tables[t], self.bags[t], sides[t])
             if t == tq:
-                ams_bag_fwd(self.no_beh[:B + 1], 0, id_ids[t][n_beh:], id_tables[t], self.Q[:B], side)
+                ams_bag_fwd(self.no_beh[:B + 1], 0, id_ids[t][n_beh:], id_tables[t], self.Q[:B], sides[t])
         st.dedup(ids, n_ids, main)
         st.embed_fwd(T, W, b, main)
         st.pool_fwd(seg_off, n_beh, main)
-        if side is not main:
-            main.wait_stream(side)                  # bags (and the queries) ready
+        if forked:
+            for sd in sides:
+                main.wait_stream(sd)                # bags (and the queries) ready
         users, dusers = [st.U[:B]], [self.dU[:B]]
         if tq is not None:
             ams_pool_query_fwd(seg_off, n_beh, st.inv, st.E, self.Q[:B], self.U2[:B], self.w2, main)
@@ -711,25 +719,27 @@ class JointStep:
         dfields = dusers + [self.dA[:B]] + [x[:B] for x in self.dbags]
         ams_ctr_fwd_bwd(self.ctr, fields, labels, ctr_W, ctr_b, self.loss, self.prob, self.ctr_dW, self.ctr_db,
                         dfields, self.ws, main)
-        if side is not main:
-            side.wait_stream(main)                  # bag gradients ready
+        if forked:
+            for sd in sides:
+                sd.wait_stream(main)                # bag gradients ready
         # ID rows: merged gradients and Adagrad, beside the image backward (the
         # query table after the query channel's backward has produced dQ)
         def id_update(t, dad=None):
             ams_bag_bwd(seg_off, n_beh, self.t_inv[t], self.t_perm[t], self.t_off[t], self.t_nu[t], self.n_occ,
-                        self.dbags[t][:B], self.row_grad[t], self.ws_id, side, dad=dad)
+                        self.dbags[t][:B], self.row_grad[t], self.ws_id[t], sides[t], dad=dad)
             ams_adagrad_rows(self.t_uniq[t], self.t_nu[t], self.n_occ, self.row_grad[t], id_tables[t], accum[t],
-                             lr, eps, side)
-        for t in range(len(self.id_rows)):
+                             lr, eps, sides[t])
+        for t in range(nt):
             if t != tq:
                 id_update(t)
         st.pool_bwd(seg_off, n_beh, self.dU, self.dA, main)
         if tq is not None:
             ams_pool_query_bwd(seg_off, n_beh, st.inv, st.occ_perm, st.uniq_off, st.n_uniq, st.cap, st.E,
                                self.Q[:B], self.U2[:B], self.w2, self.dU2[:B], self.dQ[:B], st.dE, True, st.ws, main)
-            if side is not main:
-                side.wait_stream(main)              # dQ ready
+            if forked:
+                sides[tq].wait_stream(main)         # dQ ready
             id_update(tq, self.dQ[:B])
         st.embed_bwd(T, W, main)
-        if side is not main:
-            main.wait_stream(side)                  # the whole step is ordered before later work on main
+        if forked:
+            for sd in sides:
+                main.wait_stream(sd)                # the whole step is ordered before later work on main
