@@ -43,6 +43,8 @@ METRIC = "behavior images embedded+pooled/sec (fwd+bwd), % HBM peak and % MFMA p
 PEAK_HBM = 8.0e12
 PEAK_MFMA = {"f32": 157.3e12, "bf16": 2.5e15}
 DEFAULT_WORKLOAD = "c1_f32"
+# joint workloads whose image path is another workload's (for its counter record)
+JOINT_IMAGE_PATH = {"c4_joint": "c3_long", "c4_mqap": "c3_long"}
 OTHER_WORKLOADS = ("c2_bf16", "c3_long")
 
 
@@ -659,10 +661,15 @@ def bench_joint(w, mode, args):
             ach, pk, unit, alg = u_mean * fl_u / t_launch / 1e12, peak / 1e12, "TFLOP/s", u_mean * fl_u
         else:
             ach, pk, unit, alg = u_mean * by_u / t_launch / 1e9, PEAK_HBM / 1e9, "GB/s", u_mean * by_u
+        # the joint workloads' image path is the long-sequence step's (same
+        # batch, table, weights and kernels): its counter record applies
+        rec = JOINT_IMAGE_PATH.get(w.name, w.name)
         roof = {"kernel": dom, "bound": bound, "achieved": ach, "peak": pk, "unit": unit, "frac": ach / pk,
-                "traffic": traffic_from_profile(w.name, dom, u_mean), "algorithmic_per_launch": alg,
+                "traffic": traffic_from_profile(rec, dom, u_mean), "algorithmic_per_launch": alg,
                 "avg_launch_ms": t_launch * 1e3,
                 "unit_of_work": f"{fl_u} flop and {by_u} B per unique image, {u_mean:.0f} unique per launch"}
+        if rec != w.name:
+            roof["traffic_record"] = f"profiles/traffic_{rec}.json (the same image-path kernels)"
     else:
         roof = {"kernel": dom, "bound": None, "achieved": None, "peak": None, "unit": None, "frac": None,
                 "traffic": None, "avg_launch_ms": t_launch * 1e3}

@@ -488,8 +488,8 @@ def test_mqap_joint_step_end_to_end(name):
 @pytest.mark.parametrize("query", [False, True])
 def test_joint_step_is_bitwise_deterministic(query):
     """The joint step twice from the same state (ID tables and accumulators
-    restored), with the ID-table work on its side stream beside the image
-    path: every output, the updated rows and the accumulators bit for bit;
+    restored), with each ID table's work on a side stream of its own beside
+    the image path: every output, the updated rows and the accumulators bit for bit;
     also with the query channel (the query table's update then waits for dQ)."""
     w = mid_joint(query_table=2 if query else -1)
     tq = 2 if query else None
