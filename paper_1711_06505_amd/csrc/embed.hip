@@ -2130,18 +2130,19 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
 // running chains (independent loads in flight); the chains, then the groups,
 // are added in a fixed order, so the result is deterministic.
 constexpr int kRedQ = 16;
-__global__ __launch_bounds__(64 * kRedQ) void tail_reduce(const float *__restrict__ part, int G_grid, int PS, int L,
-                                                          int H, int M, int D, float *__restrict__ dW2,
-                                                          float *__restrict__ db2, float *__restrict__ dW3,
-                                                          float *__restrict__ db3, float *__restrict__ db1,
-                                                          float *__restrict__ ds1, float *__restrict__ ds2,
-                                                          const int32_t *__restrict__ n_uniq_p, int cap)
+constexpr int kRedThreads = 64 * kRedQ;
+__device__ __forceinline__ void tail_reduce_block(int blk, const float *__restrict__ part, int G_grid, int PS, int L,
+                                                  int H, int M, int D, float *__restrict__ dW2,
+                                                  float *__restrict__ db2, float *__restrict__ dW3,
+                                                  float *__restrict__ db3, float *__restrict__ db1,
+                                                  float *__restrict__ ds1, float *__restrict__ ds2,
+                                                  const int32_t *__restrict__ n_uniq_p, int cap)
 {
     // the slots the tail backward's active blocks wrote
     const int G = tail_active(min(*n_uniq_p, cap), G_grid);
     __shared__ float sq[kRedQ][64];
     const int t = threadIdx.x, q = t >> 6;
-    const int e = blockIdx.x * 64 + (t & 63);
+    const int e = blk * 64 + (t & 63);
     float c[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     if (e < PS) {
         int k = 0;
@@ -2180,10 +2181,9 @@ __global__ __launch_bounds__(64 * kRedQ) void tail_reduce(const float *__restric
 // out[e] = sum of part[g * PS + e] over g = 0..G-1, in a fixed association:
 // eight running sums over g = 8i + r, added r = 0..7 at the end (the eight
 // independent load chains keep the reads in flight).
-__global__ __launch_bounds__(kThreads) void partial_reduce(const float *__restrict__ part, int G,
-                                                           size_t PS, float *__restrict__ out)
+__device__ __forceinline__ void partial_reduce_elem(size_t e, const float *__restrict__ part, int G, size_t PS,
+                                                    float *__restrict__ out)
 {
-    const size_t e = (size_t)blockIdx.x * kThreads + threadIdx.x;
     if (e >= PS) return;
     float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
     int g = 0;
@@ -2195,6 +2195,27 @@ __global__ __launch_bounds__(kThreads) void partial_reduce(const float *__restri
 #pragma unroll
     for (int r = 0; r < 8; ++r) tot += s[r];
     out[e] = tot;
+}
+
+// The backward's two fixed-order sums in one launch (they read what the tail
+// backward and the dW1 product wrote, both earlier on the stream): blocks
+// [0, n_dw) add the dW1 partials, kRedThreads elements each; the blocks after
+// them add the tail's block partials into dW2, db2, dW3, db3, db1 and the
+// slope gradients, 64 elements each.  Every sum keeps its association.
+__global__ __launch_bounds__(kRedThreads) void bwd_reduce(const float *__restrict__ dw1p, int kc, size_t nw,
+                                                         float *__restrict__ dW1, int n_dw,
+                                                         const float *__restrict__ tail, int G_grid, int PS, int L,
+                                                         int H, int M, int D, float *__restrict__ dW2,
+                                                         float *__restrict__ db2, float *__restrict__ dW3,
+                                                         float *__restrict__ db3, float *__restrict__ db1,
+                                                         float *__restrict__ ds1, float *__restrict__ ds2,
+                                                         const int32_t *__restrict__ n_uniq_p, int cap)
+{
+    if ((int)blockIdx.x < n_dw)
+        partial_reduce_elem((size_t)blockIdx.x * kRedThreads + threadIdx.x, dw1p, kc, nw, dW1);
+    else
+        tail_reduce_block((int)blockIdx.x - n_dw, tail, G_grid, PS, L, H, M, D, dW2, db2, dW3, db3, db1, ds1, ds2,
+                          n_uniq_p, cap);
 }
 
 // ------------------------------------------------------------- dW1 split-K
@@ -3601,9 +3622,6 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
         TB_LAUNCH(2, float, float, false);
     }
 #undef TB_LAUNCH
-    AMS_LAUNCH("tail_reduce", st, tail_reduce<<<(PS + 63) / 64, 64 * kRedQ, 0, st>>>(tail, TG, PS, L, H, M, D, dW2,
-                                                                          db2, dW3, db3, db1, ds1, ds2, n_uniq,
-                                                                          cap));
 
     const int bm = (H % 128 == 0) ? 128 : 64;
     const int nmt = H / bm, outer = (F / 64) * p.kc;
@@ -3640,8 +3658,12 @@ extern "C" ams_status ams_embed_bwd(const ams_mlp *mlp, const void *T, int64_t n
                                                                n_uniq, cap, (const uint16_t *)dz1, H, p.kc,
                                                                dw1p));
     }
+    // the dW1 partials and the tail's partials summed by one launch (four
+    // dW1 elements per thread as float4 measured twice as slow: 21 vs 10 us)
     const size_t nw = (size_t)H * F;
-    // (four elements per thread as float4 measured twice as slow: 21 vs 10 us)
-    AMS_LAUNCH("reduce_dw1", st, partial_reduce<<<(unsigned)((nw + kThreads - 1) / kThreads), kThreads, 0, st>>>(dw1p, p.kc, nw, dW1));
+    const int n_dw = (int)((nw + kRedThreads - 1) / kRedThreads);
+    AMS_LAUNCH("bwd_reduce", st, bwd_reduce<<<n_dw + (PS + 63) / 64, kRedThreads, 0, st>>>(
+                                     dw1p, p.kc, nw, dW1, n_dw, tail, TG, PS, L, H, M, D, dW2, db2, dW3, db3, db1, ds1,
+                                     ds2, n_uniq, cap));
     return ams_launch_status();
 }
