@@ -17,10 +17,10 @@
 //                  earlier tiles comes from decoupled look-back over the
 //                  per-tile digit counts they publish; then a stable scatter;
 //   dd_unique      head flags of the sorted keys, rank by the same look-back,
-//                  and the outputs;
-//   dd_status      one block: the device status from the passes' error flag
-//                  and the range check (after the last tile, by the kernel
-//                  boundary, at no cost to the tiles).
+//                  and the outputs; the tile that completes a count of
+//                  finished tiles writes the device status (the passes' error
+//                  flag, the unique pass's own look-back bound hits carried in
+//                  the count, and the range check).
 // Tiles, waves, rows and lanes are visited in index order, so the sort is
 // stable and every output bit-exact.  A tile only waits for earlier tiles to
 // publish, and blocks are dispatched in index order, so every wait ends.
@@ -112,7 +112,7 @@ __device__ uint32_t lookback(uint32_t *words, int stride, int t, uint32_t count,
 // The same look-back walked by one whole wave: lane i reads the word of tile
 // (hi - i), so 64 earlier tiles cost one round trip.  The lowest lane holding
 // an inclusive prefix is the nearest one; the sum runs up to it.
-__device__ uint32_t lookback_wave(uint32_t *words, int t, uint32_t count, int32_t *err)
+__device__ uint32_t lookback_wave(uint32_t *words, int t, uint32_t count, bool &hit)
 {
     const int lane = ams_lane();
     if (t == 0) {
@@ -127,7 +127,7 @@ __device__ uint32_t lookback_wave(uint32_t *words, int t, uint32_t count, int32_
         const uint32_t w = j >= 0 ? ld_relaxed(&words[j]) : kPrefix;   // before tile 0: prefix 0
         if (ams_ballot((w & ~kValMask) == 0) != 0) {                   // not all published yet
             if (++spins < kSpinLimit) continue;
-            if (lane == 0) __hip_atomic_store(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            hit = true;
             break;
         }
         spins = 0;
@@ -263,12 +263,14 @@ __global__ __launch_bounds__(kThreads) void dd_pass(const uint32_t *__restrict__
     }
     __syncthreads();
     // this tile's count of digit t, and its position among earlier tiles
+    // (2^width look-back words per tile; digits past this pass's bits are
+    // empty everywhere)
+    const int R = 1 << P.width;
     int tile_cnt = 0;
     for (int w = 0; w < kWaves; ++w) tile_cnt += cnt[w][t];
     uint32_t before = 0;
     if (t < (1 << bits))
-        before = lookback(words + ((size_t)pass * P.ntiles) * kRadix + t, kRadix, blockIdx.x,
-                          (uint32_t)tile_cnt, err);
+        before = lookback(words + ((size_t)pass * P.ntiles) * R + t, R, blockIdx.x, (uint32_t)tile_cnt, err);
     // wave offsets inside the tile
     int run = gbase + (int)before;
     for (int w = 0; w < kWaves; ++w) {
@@ -289,14 +291,23 @@ __global__ __launch_bounds__(kThreads) void dd_pass(const uint32_t *__restrict__
     }
 }
 
-// Unique set, CSR offsets, stable occurrence order, inverse index, count.
+// Unique set, CSR offsets, stable occurrence order, inverse index, count,
+// and the device status: each tile adds 1 + (hit << 32) to *done (one
+// relaxed 64-bit add: tiles finished in the low word, look-back bound hits of
+// this pass in the high word); the tile whose add completes the count reads
+// the passes' error flag and the range check (earlier launches, ordered by
+// the kernel boundaries) and writes the status.  Only the count itself is
+// communicated between tiles, so no ordering beyond the add's atomicity is
+// needed.
 __global__ __launch_bounds__(kThreads) void dd_unique(const uint32_t *__restrict__ k,
                                                       const int32_t *__restrict__ v, int n,
-                                                      uint32_t *__restrict__ words, int32_t *__restrict__ err,
+                                                      uint32_t *__restrict__ words, const int32_t *__restrict__ err,
+                                                      unsigned long long *__restrict__ done,
+                                                      const int32_t *__restrict__ bad, int n_prep,
                                                       int32_t *__restrict__ uniq, int32_t *__restrict__ inv,
                                                       int32_t *__restrict__ occ_perm,
                                                       int32_t *__restrict__ uniq_off,
-                                                      int32_t *__restrict__ n_uniq)
+                                                      int32_t *__restrict__ n_uniq, int32_t *__restrict__ dev_status)
 {
     constexpr int kItems = kTile / kThreads;  // 8 consecutive positions per thread
     __shared__ int ws[kWaves];
@@ -334,10 +345,11 @@ __global__ __launch_bounds__(kThreads) void dd_unique(const uint32_t *__restrict
     const int incl = ams_wave_incl_scan(c);
     if (ams_lane() == AMS_WAVE - 1) ws[w] = incl;
     __syncthreads();
+    bool hit = false;                          // (wave 0: this tile's look-back bound)
     if (w == 0) {
         int tot = 0;
         for (int x = 0; x < kWaves; ++x) tot += ws[x];
-        const uint32_t b = lookback_wave(words, blockIdx.x, (uint32_t)tot, err);
+        const uint32_t b = lookback_wave(words, blockIdx.x, (uint32_t)tot, hit);
         if (t == 0) tile_base = b;
     }
     __syncthreads();
@@ -367,23 +379,17 @@ __global__ __launch_bounds__(kThreads) void dd_unique(const uint32_t *__restrict
             *n_uniq = rank + 1;
         }
     }
-}
-
-// The device status, one block after the unique pass (the kernel boundary
-// orders every tile's writes of the error flag before this read): a
-// look-back bound hit in any pass is a runtime failure, else an ID out of
-// range is reported, else OK.
-__global__ __launch_bounds__(kThreads) void dd_status(const int32_t *__restrict__ err,
-                                                      const int32_t *__restrict__ bad, int n_prep,
-                                                      int32_t *__restrict__ dev_status)
-{
-    int mine = 0;
-    for (int b = threadIdx.x; b < n_prep; b += kThreads) mine |= bad[b];
-    const int any_bad = __syncthreads_or(mine);
-    if (threadIdx.x == 0)
-        *dev_status = __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
-                          ? AMS_ERR_HIP
-                          : (any_bad ? AMS_ERR_ID_RANGE : AMS_OK);
+    if (t == 0) {
+        const unsigned long long old = __hip_atomic_fetch_add(done, 1ull + ((unsigned long long)hit << 32),
+                                                              __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if ((uint32_t)old == gridDim.x - 1) {
+            const bool lb = (old >> 32) != 0 || hit ||
+                            __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0;
+            int any_bad = 0;
+            for (int b = 0; b < n_prep; ++b) any_bad |= bad[b];
+            *dev_status = lb ? AMS_ERR_HIP : (any_bad ? AMS_ERR_ID_RANGE : AMS_OK);
+        }
+    }
 }
 
 __global__ void dd_empty(int32_t *n_uniq, int32_t *dev_status, int32_t *uniq_off)
@@ -404,7 +410,7 @@ constexpr int id_bits(int32_t n_ids)
 
 struct Layout {
     Plan P;
-    int n_prep, n_words;
+    int n_prep, n_words, i_err, i_done;
     size_t off_kb, off_va, off_vb, off_hpart, off_bad, off_words, total;
 };
 
@@ -416,8 +422,13 @@ constexpr Layout layout(int64_t n_occ, int32_t n_ids)
     L.P.width = (L.P.bits + L.P.passes - 1) / L.P.passes;
     L.P.ntiles = (int)((n_occ + kTile - 1) / kTile);
     L.n_prep = L.P.ntiles < kPrepBlocks ? (L.P.ntiles > 0 ? L.P.ntiles : 1) : kPrepBlocks;
-    // the last word: the look-back error flag
-    L.n_words = L.P.passes * L.P.ntiles * kRadix + L.P.ntiles + 1;
+    // look-back words (1 << width per tile and pass, then one per tile for
+    // the unique pass), the passes' error flag, and the unique pass's 64-bit
+    // completion count at an even word (the region is 256-byte aligned)
+    const int n_lb = L.P.passes * L.P.ntiles * (1 << L.P.width) + L.P.ntiles;
+    L.i_err = n_lb;
+    L.i_done = (n_lb + 2) & ~1;
+    L.n_words = L.i_done + 2;
     auto al = [](size_t x) constexpr { return (x + 255) & ~(size_t)255; };
     const size_t nb = al((size_t)n_occ * 4);
     size_t o = nb;                           // keys ping (pong is the caller's ids on pass 0)
@@ -447,9 +458,10 @@ ams_status dedup_enqueue(const int32_t *ids, int n, int32_t n_ids, int32_t *uniq
     int32_t *hpart = (int32_t *)(w + L.off_hpart);
     int32_t *bad = (int32_t *)(w + L.off_bad);
     uint32_t *words = (uint32_t *)(w + L.off_words);
-    int32_t *err = (int32_t *)(words + L.n_words - 1);
+    int32_t *err = (int32_t *)(words + L.i_err);
+    unsigned long long *done = (unsigned long long *)(words + L.i_done);
 
-    // dd_prep also zeroes every look-back word and the error flag
+    // dd_prep also zeroes every look-back word, the error flag and the count
     AMS_LAUNCH("dd_prep", st, dd_prep<<<L.n_prep, kPrepThreads, 0, st>>>((const uint32_t *)ids, n, L.P, (uint32_t)n_ids, hpart, bad, words,
                                           L.n_words));
     const uint32_t *kin = (const uint32_t *)ids;
@@ -464,9 +476,9 @@ ams_status dedup_enqueue(const int32_t *ids, int n, int32_t n_ids, int32_t *uniq
         kin = kout;
         vin = vout;
     }
-    AMS_LAUNCH("dd_unique", st, dd_unique<<<L.P.ntiles, kThreads, 0, st>>>(kin, vin, n, words + (size_t)L.P.passes * L.P.ntiles * kRadix,
-                                              err, uniq, inv, occ_perm, uniq_off, n_uniq));
-    AMS_LAUNCH("dd_status", st, dd_status<<<1, kThreads, 0, st>>>(err, bad, L.n_prep, dev_status));
+    AMS_LAUNCH("dd_unique", st, dd_unique<<<L.P.ntiles, kThreads, 0, st>>>(
+                                    kin, vin, n, words + (size_t)L.P.passes * L.P.ntiles * (1 << L.P.width), err, done,
+                                    bad, L.n_prep, uniq, inv, occ_perm, uniq_off, n_uniq, dev_status));
     return ams_launch_status();
 }
 

@@ -79,11 +79,13 @@ def test_dedup_bit_exact_on_workloads(name):
     (0, 10, "rand"), (1, 10, "rand"), (1, 1, "rand"), (5000, 1, "rand"), (2047, 300, "rand"),
     (2048, 300, "rand"), (2049, 300, "rand"), (4097, 2 ** 21, "rand"), (10000, 7, "desc"),
     (65537, 2 ** 31 - 1, "rand"), (3000, 2 ** 21, "top"), (40000, 200_000, "same"),
-    # around the switch to 8192-key tiles (2^19 occurrences): the last small-tile
-    # size, exactly 64 large tiles, a ragged last large tile, all keys equal,
-    # descending keys, four radix passes
+    # larger batches: 2^19 - 1 and 2^19 occurrences, a ragged last tile, all
+    # keys equal, descending keys over 24 bits (three passes of 8)
     (2 ** 19 - 1, 2 ** 21, "rand"), (2 ** 19, 2 ** 31 - 1, "rand"), (2 ** 19 + 8193, 300, "rand"),
     (600_000, 200_000, "same"), (2 ** 20, 2 ** 24, "desc"),
+    # pass widths: 9 bits in two passes of 5, 18 bits in three of 6, 19 bits
+    # in three of 7, 27 bits in four of 7
+    (5000, 512, "rand"), (70_000, 2 ** 18, "rand"), (9000, 2 ** 18 + 1, "rand"), (100_000, 2 ** 27, "rand"),
 ])
 def test_dedup_edges(n, n_ids, kind):
     rng = np.random.default_rng(n + n_ids)
