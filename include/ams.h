@@ -154,7 +154,9 @@ ams_status ams_timing_read(ams_kernel_time *out, int cap, int *n_out);
  *                   occ_perm[uniq_off[u] .. uniq_off[u+1]); uniq_off[n_u] = n_occ.
  * n_uniq[1]         out: n_u.
  * dev_status[1]     out: AMS_OK, or AMS_ERR_ID_RANGE if some ID is out of range.
- * ws, ws_bytes      workspace of at least ams_dedup_workspace(n_occ, n_ids) bytes.
+ * ws, ws_bytes      workspace of at least ams_dedup_workspace(n_occ, n_ids) bytes;
+ *                   that size also serves every smaller n_occ and n_ids (one
+ *                   workspace for several ID tables).
  * n_occ == 0 is valid (n_u = 0).  Host errors: NULL, SIZE (n_occ < 0,
  * n_occ > 2^30 - 1, n_ids < 1), WORKSPACE.  Outputs are bit-exact: they are
  * the unique canonical answer.  *dev_status = AMS_ERR_HIP reports an internal

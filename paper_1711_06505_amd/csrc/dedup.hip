@@ -442,6 +442,21 @@ constexpr Layout layout(int64_t n_occ, int32_t n_ids)
     return L;
 }
 
+// Workspace that serves every ID range up to n_ids (and, the layout growing
+// with n_occ, every smaller batch): the look-back words grow with the digit
+// width, which is not monotonic in n_ids (100 IDs: one 7-bit pass; 1000: two
+// of 5), so the largest layout over the bit counts up to n_ids's.
+constexpr size_t workspace_bound(int64_t n_occ, int32_t n_ids)
+{
+    size_t t = 0;
+    const int B = id_bits(n_ids);
+    for (int b = 1; b <= B; ++b) {
+        const size_t x = layout(n_occ, b == B ? n_ids : (int32_t)(1u << b)).total;
+        t = x > t ? x : t;
+    }
+    return t;
+}
+
 // Enqueues the whole dedup with its workspace at `w` (layout L).
 ams_status dedup_enqueue(const int32_t *ids, int n, int32_t n_ids, int32_t *uniq, int32_t *inv,
                          int32_t *occ_perm, int32_t *uniq_off, int32_t *n_uniq, int32_t *dev_status,
@@ -490,7 +505,7 @@ ams_status dedup_enqueue(const int32_t *ids, int n, int32_t n_ids, int32_t *uniq
 // device memory): the device address comes from hipGetSymbolAddress, looked
 // up once per device with that device current.
 constexpr int64_t kNoAllocMaxOcc = AMS_DEDUP_NOALLOC_MAX_OCC;
-constexpr size_t kScratchBytes = layout(kNoAllocMaxOcc, INT32_MAX).total;
+constexpr size_t kScratchBytes = workspace_bound(kNoAllocMaxOcc, INT32_MAX);
 static __device__ __align__(256) unsigned char scratch[kScratchBytes];
 
 constexpr int kMaxDevices = 64;
@@ -516,7 +531,7 @@ void *scratch_on_current_device()
 extern "C" size_t ams_dedup_workspace(int64_t n_occ, int32_t n_ids)
 {
     if (n_occ < 0 || n_ids < 1) return 0;
-    return layout(n_occ, n_ids).total;
+    return workspace_bound(n_occ, n_ids);
 }
 
 extern "C" ams_status ams_dedup(const int32_t *ids, int64_t n_occ, int32_t n_ids, int32_t *uniq,

@@ -1849,6 +1849,25 @@ __device__ __forceinline__ float buf_ld(brsrc_t r, uint32_t elem)
         return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(r, elem * 4, 0, 0));
 }
 
+typedef unsigned int v2u32 __attribute__((ext_vector_type(2)));
+typedef unsigned int v4u32 __attribute__((ext_vector_type(4)));
+
+// Four consecutive elements from elem (a multiple of 4): one 16-byte (fp32)
+// or 8-byte (bf16) buffer load, 0 past the descriptor's size.
+template <typename T>
+__device__ __forceinline__ float4 buf_ld4(brsrc_t r, uint32_t elem)
+{
+    if constexpr (sizeof(T) == 2) {
+        const v2u32 v = __builtin_amdgcn_raw_buffer_load_b64(r, elem * 2, 0, 0);
+        return make_float4(__uint_as_float(v[0] << 16), __uint_as_float(v[0] & 0xffff0000u),
+                           __uint_as_float(v[1] << 16), __uint_as_float(v[1] & 0xffff0000u));
+    } else {
+        const v4u32 v = __builtin_amdgcn_raw_buffer_load_b128(r, elem * 4, 0, 0);
+        return make_float4(__uint_as_float(v[0]), __uint_as_float(v[1]), __uint_as_float(v[2]),
+                           __uint_as_float(v[3]));
+    }
+}
+
 // Buffer store: dropped by the hardware past the descriptor's size.
 template <typename T>
 __device__ __forceinline__ void buf_st(brsrc_t r, uint32_t elem, float v)
@@ -1895,18 +1914,26 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
 
     // W2 (fp32, zero-padded to 64 x 256) and W3 (2 SD x 64) in LDS: operands of
     // dH1 and dZ2, re-read per chunk (registers hold the chunk's data)
-    __shared__ float W2s[kMaxH2 * kMaxH1];
+    __shared__ __attribute__((aligned(16))) float W2s[kMaxH2 * kMaxH1];
     __shared__ float W3s[2 * SD * kMaxH2];
     __shared__ float S2s[PR ? kMaxH2 : 1];     // layer 2's PReLU slopes (3 layers)
     if (PR && L == 3)
         for (int o = threadIdx.x; o < kMaxH2; o += kTbThreads) S2s[o] = o < M ? s2[o] : 0.f;
     {
+        // four consecutive i per load (H is a multiple of 64), all 16 loads
+        // of a thread in flight together
         const brsrc_t rW2 = make_buf(W2, (uint32_t)(Mo * H * sizeof(TW)));   // rows o >= Mo read 0
-#pragma unroll 8
-        for (int e = threadIdx.x; e < kMaxH2 * kMaxH1; e += kTbThreads) {
-            const int o = e / kMaxH1, i = e % kMaxH1;
-            const float x = buf_ld<TW>(rW2, (uint32_t)(o * H + min(i, H - 1)));
-            W2s[e] = i < H ? x : 0.f;
+        constexpr int N4 = kMaxH2 * kMaxH1 / 4 / kTbThreads;
+        float4 v[N4];
+#pragma unroll
+        for (int k = 0; k < N4; ++k) {
+            const int e = 4 * ((int)threadIdx.x + k * kTbThreads), o = e / kMaxH1, i = e % kMaxH1;
+            v[k] = buf_ld4<TW>(rW2, (uint32_t)(o * H + min(i, H - 4)));
+        }
+#pragma unroll
+        for (int k = 0; k < N4; ++k) {
+            const int e = 4 * ((int)threadIdx.x + k * kTbThreads), i = e % kMaxH1;
+            *(float4 *)&W2s[e] = i < H ? v[k] : make_float4(0.f, 0.f, 0.f, 0.f);
         }
         const brsrc_t rW3 = make_buf(L == 3 ? W3 : W2, L == 3 ? (uint32_t)(D * M * sizeof(TW)) : 0u);
         static_assert(2 * SD * kMaxH2 % kTbThreads == 0, "W3 entries per thread");

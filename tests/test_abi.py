@@ -53,6 +53,19 @@ def test_status_strings(lib):
 def test_workspace_sizes(lib):
     assert lib.ams_dedup_workspace(-1, 10) == 0
     assert lib.ams_dedup_workspace(57_000, 200_000) >= 4 * 57_000 * 4
+
+
+def test_dedup_workspace_serves_smaller_calls(lib):
+    # one workspace sized for the largest ID table serves the smaller ones
+    # (the look-back words grow with the digit width, which is not monotonic
+    # in the ID range: 100 IDs sort in one 7-bit pass, 1000 in two of 5)
+    ks = list(range(1, 300)) + [2 ** b + o for b in range(9, 31) for o in (-1, 0, 1)] + [2 ** 31 - 1]
+    for n in (1, 100, 2047, 2048, 2049, 57_000, 750_000):
+        ws = [lib.ams_dedup_workspace(n, k) for k in ks]
+        assert all(b >= a for a, b in zip(ws, ws[1:])), n
+    for k in (7, 100, 1000, 200_000, 2 ** 31 - 1):
+        ws = [lib.ams_dedup_workspace(n, k) for n in range(0, 20_000, 97)]
+        assert all(b >= a for a, b in zip(ws, ws[1:])), k
     m = ams.make_mlp((4096, 256, 64, 12), "f32")
     assert lib.ams_embed_workspace(ctypes.byref(m), 57_000) >= 57_000 * 256 * 4
     bad = ams.make_mlp((4000, 256, 64, 12), "f32")
