@@ -1480,21 +1480,19 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     }
 }
 
-// ---- bf16 forward tail (stream-K layer 1, H = 256) ----
+// ---- bf16 forward tail (H = 256) ----
 //
-// tail_fwd_bf16: the small layers after the bf16 stream-K first layer, for
-// 32-row chunks (one chunk per wave at a time, no block-level sync in the
-// loop).  Every product runs on v_mfma_f32_32x32x16_bf16 with its fp32
+// tail_fwd_bf16: the small layers after the bf16 row-split first layer
+// (whole rows stored as an H1b / H1lo pair), for 32-row chunks (one chunk per
+// wave at a time, no block-level sync in the loop); tail_fwd_bf16_q below
+// serves the stream-K layer.  Every product runs on v_mfma_f32_32x32x16_bf16 with its fp32
 // activation split into a high and a low bf16 part (x = hi + lo to 2^-18
 // relative); the weights are exact in bf16 and each part's products are exact
 // in fp32, so the results carry fp32 accumulation of fp32-level operands.
 //
 // Layer 2: Z2^T = W2 H1^T.  First operand a W2 row (16 bytes of 8
-// consecutive k, LDS), second the chunk's H1 row: for a tile finished in place
-// by one stream-K worker the (H1b, H1lo) pair it stored; for a tile cut
-// between workers the workers' fp32 partial tiles added in K order, b1 and
-// ReLU applied (ReLU(b1) for an ID outside the table), split, and H1b stored
-// for the backward.  K step s covers k = 16 s .. +15, lane half h supplying
+// consecutive k, LDS), second the chunk's H1 row, the (H1b, H1lo) pair the
+// first layer stored.  K step s covers k = 16 s .. +15, lane half h supplying
 // k = 16 s + 8 h + e.  The accumulator holds Z2[row = lane % 32][o = 32 ob +
 // acc_row(j, lane)]: each lane owns one image row and 32 of its outputs.
 // H2 = ReLU(Z2 + b2) is stored as float4 runs of 4 outputs.
@@ -1545,11 +1543,8 @@ __device__ __forceinline__ void split8(const float (&x)[8], uint4 &hi, uint4 &lo
 // layer-2 operand is the fp32 activation re-split into hi / lo; H2_save holds
 // Z2 and the layer-3 operand is its activation.
 template <int L, bool PR>
-__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void tail_fwd_bf16(uint16_t *__restrict__ H1b,
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void tail_fwd_bf16(const uint16_t *__restrict__ H1b,
                                                           const uint16_t *__restrict__ H1lo,
-                                                          const float *__restrict__ pbuf, int F, int G,
-                                                          const float *__restrict__ b1,
-                                                          const int32_t *__restrict__ uniq, int64_t n_rows,
                                                           int M, int D, const uint16_t *__restrict__ W2,
                                                           const float *__restrict__ b2,
                                                           const uint16_t *__restrict__ W3,
@@ -1564,7 +1559,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     __shared__ __attribute__((aligned(16))) uint16_t W3s[32 * kW3S];
     __shared__ __attribute__((aligned(16))) float S1s[PR ? H : 4];      // layer 1's slopes
     __shared__ float S2s[PR ? kMaxH2 : 1];                               // layer 2's slopes (3 layers)
-    __shared__ __attribute__((aligned(16))) float B1s[kMaxH1];           // b1, for the split tiles
     const int t = threadIdx.x, lane = ams_lane(), wave = t / AMS_WAVE;
     const int h = lane >> 5, r32 = lane & 31;
     const int Mo = (L == 3) ? M : D;           // width of the second layer's output
@@ -1606,8 +1600,6 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
             if (e < 32 * kW3S) W3s[e] = v[i];
         }
     }
-    if (pbuf)
-        for (int i = t; i < H; i += kThreads) B1s[i] = b1[i];
     if (PR) {
         for (int i = t; i < H; i += kThreads) S1s[i] = s1[i];
         if (L == 3)
@@ -1626,94 +1618,44 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
     __syncthreads();
 
     const bool relu2 = (L == 3 && !PR) || (L == 2 && final_relu);
-    using K = Sk<uint16_t>;
-    const SkPlan P = sk_plan(n_u, H, F, G, sk_bk<uint16_t>(), K::BM);
     for (int c0 = (blockIdx.x * (kThreads / AMS_WAVE) + wave) * 32; c0 < n_u;
          c0 += gridDim.x * (kThreads / AMS_WAVE) * 32) {
         const int row = c0 + r32;
         const bool live = row < n_u;
         const int rowc = min(row, n_u - 1);
-        // the chunk lies in one stream-K row tile: finished in place or cut
-        const int tile = c0 / K::BM;
-        const int wa = P.owner((int64_t)tile * P.S), wb = P.owner((int64_t)(tile + 1) * P.S - 1);
-        const bool split = pbuf != nullptr && wb > wa;      // no pieces: every tile is whole
-        const int slot_a = (tile == (int)(P.it0(wa) / P.S)) ? 0 : 1;   // first contributor's piece
-        bool id_ok = true;
-        if (split) {
-            const int id = uniq[rowc];
-            id_ok = id >= 0 && (int64_t)id < n_rows;
-        }
-        const int rl = rowc % K::BM;
         const size_t roff = (size_t)rowc * H + 8 * h;
+        // quarters of 64 k, double-buffered: quarter qt + 1's loads are
+        // issued before quarter qt's products (the scheduling barriers keep
+        // later quarters' loads from being hoisted, which runs out of
+        // registers)
         v16f acc[2] = {(v16f){}, (v16f){}};
+        uint4 bh[2][KS / 4], bl[2][KS / 4];
+        auto load_q = [&](int qt, uint4 (&hb)[KS / 4], uint4 (&lb)[KS / 4]) {
+#pragma unroll
+            for (int s4 = 0; s4 < KS / 4; ++s4) {
+                hb[s4] = *(const uint4 *)(H1b + roff + 16 * (qt * (KS / 4) + s4));
+                lb[s4] = *(const uint4 *)(H1lo + roff + 16 * (qt * (KS / 4) + s4));
+            }
+        };
+        load_q(0, bh[0], bl[0]);
 #pragma unroll
         for (int qt = 0; qt < 4; ++qt) {
-            uint4 bh[KS / 4], bl[KS / 4];
-            if (split) {
-                // the quarter's pieces of the first three shares, every load
-                // issued before any is used (a share past wb reloads the
-                // first one and is not added); later shares, rare, one by one
-                const bool has1 = wa + 1 <= wb, has2 = wa + 2 <= wb;
-                const float *pw0 = pbuf + ((size_t)wa * 2 + slot_a) * K::TILE + rl * kSkBN;
-                const float *pw1 = has1 ? pbuf + ((size_t)(wa + 1) * 2) * K::TILE + rl * kSkBN : pw0;
-                const float *pw2 = has2 ? pbuf + ((size_t)(wa + 2) * 2) * K::TILE + rl * kSkBN : pw0;
-                float4 pv[3][KS / 4][2];
-#pragma unroll
-                for (int s4 = 0; s4 < KS / 4; ++s4) {
-                    const int k0 = 16 * (qt * (KS / 4) + s4) + 8 * h;
-                    pv[0][s4][0] = *(const float4 *)(pw0 + k0);
-                    pv[0][s4][1] = *(const float4 *)(pw0 + k0 + 4);
-                    pv[1][s4][0] = *(const float4 *)(pw1 + k0);
-                    pv[1][s4][1] = *(const float4 *)(pw1 + k0 + 4);
-                    pv[2][s4][0] = *(const float4 *)(pw2 + k0);
-                    pv[2][s4][1] = *(const float4 *)(pw2 + k0 + 4);
-                }
-#pragma unroll
-                for (int s4 = 0; s4 < KS / 4; ++s4) {
-                    const int k0 = 16 * (qt * (KS / 4) + s4) + 8 * h;
-                    float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-                    for (int pi = 0; pi < 3; ++pi) {
-                        if (pi == 0 || (pi == 1 ? has1 : has2)) {
-                            const float4 v0 = pv[pi][s4][0], v1 = pv[pi][s4][1];
-                            x[0] += v0.x; x[1] += v0.y; x[2] += v0.z; x[3] += v0.w;
-                            x[4] += v1.x; x[5] += v1.y; x[6] += v1.z; x[7] += v1.w;
-                        }
-                    }
-                    for (int w = wa + 3; w <= wb; ++w) {     // (a tile spans at most 3 shares)
-                        const float *pc = pbuf + ((size_t)w * 2) * K::TILE + rl * kSkBN + k0;
-                        const float4 v0 = *(const float4 *)pc, v1 = *(const float4 *)(pc + 4);
-                        x[0] += v0.x; x[1] += v0.y; x[2] += v0.z; x[3] += v0.w;
-                        x[4] += v1.x; x[5] += v1.y; x[6] += v1.z; x[7] += v1.w;
-                    }
-                    const float4 c0v = *(const float4 *)&B1s[k0], c1v = *(const float4 *)&B1s[k0 + 4];
-                    const float bb[8] = {c0v.x, c0v.y, c0v.z, c0v.w, c1v.x, c1v.y, c1v.z, c1v.w};
-#pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        x[e] = id_ok ? x[e] + bb[e] : bb[e];
-                        if (!PR) x[e] = fmaxf(x[e], 0.f);
-                    }
-                    split8(x, bh[s4], bl[s4]);
-                    if (live) *(uint4 *)(H1b + (size_t)row * H + k0) = bh[s4];
-                }
-            } else {
-#pragma unroll
-                for (int s4 = 0; s4 < KS / 4; ++s4) {
-                    bh[s4] = *(const uint4 *)(H1b + roff + 16 * (qt * (KS / 4) + s4));
-                    bl[s4] = *(const uint4 *)(H1lo + roff + 16 * (qt * (KS / 4) + s4));
-                }
-            }
+            __builtin_amdgcn_sched_barrier(0);
+            if (qt < 3) load_q(qt + 1, bh[(qt + 1) & 1], bl[(qt + 1) & 1]);
+            __builtin_amdgcn_sched_barrier(0);
+            uint4 (&ch)[KS / 4] = bh[qt & 1];
+            uint4 (&cl)[KS / 4] = bl[qt & 1];
             if (PR) {   // the operand: PReLU(Z1) in fp32, split again
 #pragma unroll
                 for (int s4 = 0; s4 < KS / 4; ++s4) {
                     const int k0 = 16 * (qt * (KS / 4) + s4) + 8 * h;
                     float x[8];
-                    join8(bh[s4], bl[s4], x);
+                    join8(ch[s4], cl[s4], x);
                     const float4 a0 = *(const float4 *)&S1s[k0], a1 = *(const float4 *)&S1s[k0 + 4];
                     const float a[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
 #pragma unroll
                     for (int e = 0; e < 8; ++e) x[e] = x[e] > 0.f ? x[e] : a[e] * x[e];
-                    split8(x, bh[s4], bl[s4]);
+                    split8(x, ch[s4], cl[s4]);
                 }
             }
 #pragma unroll
@@ -1723,8 +1665,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
                 for (int ob = 0; ob < 2; ++ob) {
                     const int o = 32 * ob + r32;
                     const uint4 av = *(const uint4 *)&W2s[o * H + (((2 * ss + h) ^ (o & 7)) << 3)];
-                    acc[ob] = mfma_bf16(av, bh[s4], acc[ob]);
-                    acc[ob] = mfma_bf16(av, bl[s4], acc[ob]);
+                    acc[ob] = mfma_bf16(av, ch[s4], acc[ob]);
+                    acc[ob] = mfma_bf16(av, cl[s4], acc[ob]);
                 }
             }
         }
@@ -1794,6 +1736,261 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
                 }
             }
         }
+    }
+}
+
+// The rest of a chunk after layer 2's products (acc[ob][j]: row lane % 32,
+// output 32 ob + acc_row(j, lane)): Z2 + b2 and its activation, stored to
+// H2_save (3 layers; Z2 itself with PReLU) or E (2 layers), then for 3
+// layers E = H2 W3^T + b3 on MFMA with W3 rows in LDS (kW3S bf16 apart) and
+// H2 split into hi and lo parts straight from the registers.
+template <int L, bool PR>
+__device__ __forceinline__ void tfb_finish(const v16f (&acc)[2], const float (&bias)[2][16], bool relu2,
+                                           const uint16_t *W3s, const float *S2s, const float *__restrict__ b3,
+                                           int final_relu, int M, int D, int row, bool live,
+                                           float *__restrict__ H2_save, float *__restrict__ E, int lane)
+{
+    const int h = lane >> 5, r32 = lane & 31;
+    float z[2][16];
+#pragma unroll
+    for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const float v = acc[ob][j] + bias[ob][j];
+            z[ob][j] = relu2 ? fmaxf(v, 0.f) : v;
+        }
+    float *out2 = (L == 3) ? H2_save : E;  // where the second layer's output goes
+    const int w2 = (L == 3) ? M : D;
+    if (live && out2) {
+#pragma unroll
+        for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                const int o = 32 * ob + 8 * q + 4 * h;
+                float *dst = out2 + (size_t)row * w2 + o;
+                if ((w2 & 3) == 0 && o + 3 < w2) {
+                    *(float4 *)dst = make_float4(z[ob][4 * q], z[ob][4 * q + 1], z[ob][4 * q + 2], z[ob][4 * q + 3]);
+                } else {
+#pragma unroll
+                    for (int r = 0; r < 4; ++r)
+                        if (o + r < w2) dst[r] = z[ob][4 * q + r];
+                }
+            }
+    }
+    if constexpr (L == 3) {
+        v16f a3 = (v16f){};
+#pragma unroll
+        for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+            for (int p = 0; p < 2; ++p) {
+                float x[8];
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    x[e] = z[ob][8 * p + e];           // o = 32 ob + 16 p + 4 h + e
+                    x[4 + e] = z[ob][8 * p + 4 + e];   // o = 32 ob + 16 p + 8 + 4 h + e
+                }
+                if (PR) {                              // Z2 -> H2
+                    const int ob0 = 32 * ob + 16 * p + 4 * h;
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        x[e] = x[e] > 0.f ? x[e] : S2s[ob0 + e] * x[e];
+                        x[4 + e] = x[4 + e] > 0.f ? x[4 + e] : S2s[ob0 + 8 + e] * x[4 + e];
+                    }
+                }
+                uint4 hi, lo;
+                split8(x, hi, lo);
+                const uint16_t *wr = &W3s[r32 * kW3S + 32 * ob + 16 * p + 4 * h];
+                const uint2 w0 = *(const uint2 *)wr, w1 = *(const uint2 *)(wr + 8);
+                const uint4 wv = make_uint4(w0.x, w0.y, w1.x, w1.y);
+                a3 = mfma_bf16(wv, hi, a3);
+                a3 = mfma_bf16(wv, lo, a3);
+            }
+        if (live) {
+#pragma unroll
+            for (int j = 0; j < 16; ++j) {
+                const int d = acc_row(j, lane);
+                if (d < D) {
+                    float v = a3[j] + b3[d];
+                    if (final_relu) v = fmaxf(v, 0.f);
+                    E[(size_t)row * D + d] = v;
+                }
+            }
+        }
+    }
+}
+
+// tail_fwd_bf16_q: the same small layers after the stream-K first layer, for
+// the stream-K path's batches (below the row-split size): one block per
+// 32-row chunk (blocks loop over chunks), wave q taking layer 2's
+// contraction over k = 64 q .. + 63.  A wave's W2 operands come straight
+// from global memory (rows o = 32 ob + lane % 32), the chunk's H1 quarter
+// from the stream-K pieces (added in K order, b1 and the activation applied,
+// H1b stored, as in tail_fwd_bf16) or from the finished rows; every load of
+// a wave is issued before the first is used, so a chunk costs one memory
+// round trip where one wave walking all four quarters costs four.  The four
+// quarters' products (the same MFMA sequence per quarter as tail_fwd_bf16)
+// are added in q order through LDS, and wave 0 finishes the chunk.
+template <int L, bool PR>
+__global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) void tail_fwd_bf16_q(
+    uint16_t *__restrict__ H1b, const uint16_t *__restrict__ H1lo, const float *__restrict__ pbuf, int F, int G,
+    const float *__restrict__ b1, const int32_t *__restrict__ uniq, int64_t n_rows, int M, int D,
+    const uint16_t *__restrict__ W2, const float *__restrict__ b2, const uint16_t *__restrict__ W3,
+    const float *__restrict__ b3, int final_relu, const int32_t *__restrict__ n_uniq_p, int cap,
+    float *__restrict__ H2_save, float *__restrict__ E, const float *__restrict__ s1, const float *__restrict__ s2)
+{
+    constexpr int H = kMaxH1;
+    static_assert(kThreads == 4 * AMS_WAVE, "one wave per K quarter");
+    __shared__ __attribute__((aligned(16))) float Zq[4][2][16][AMS_WAVE];   // quarter partials, lane-major
+    __shared__ __attribute__((aligned(16))) uint16_t W3s[32 * kW3S];
+    __shared__ __attribute__((aligned(16))) float B1s[kMaxH1];
+    __shared__ __attribute__((aligned(16))) float S1s[PR ? kMaxH1 : 4];
+    __shared__ float S2s[PR ? kMaxH2 : 1];
+    const int t = threadIdx.x, lane = ams_lane(), q = t / AMS_WAVE;
+    const int h = lane >> 5, r32 = lane & 31;
+    const int Mo = (L == 3) ? M : D;
+    const int n_u = min(*n_uniq_p, cap);
+    if (blockIdx.x * 32 >= n_u) return;
+    // this wave's W2 operands (rows past Mo read row 0 and are zeroed), all
+    // in flight together, then W3, b1 and the slopes into LDS
+    uint4 aw[4][2];
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+        for (int ob = 0; ob < 2; ++ob) {
+            const int o = 32 * ob + r32;
+            aw[s4][ob] = *(const uint4 *)&W2[(size_t)(o < Mo ? o : 0) * H + 64 * q + 16 * s4 + 8 * h];
+        }
+#pragma unroll
+    for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+        for (int ob = 0; ob < 2; ++ob)
+            if (32 * ob + r32 >= Mo) aw[s4][ob] = make_uint4(0, 0, 0, 0);
+    if (L == 3)
+        for (int e = t; e < 32 * kW3S; e += kThreads) {
+            const int d = e / kW3S, o = e % kW3S;
+            W3s[e] = (d < D && o < M) ? W3[d * M + o] : (uint16_t)0;
+        }
+    for (int i = t; i < H; i += kThreads) B1s[i] = b1[i];
+    if (PR) {
+        for (int i = t; i < H; i += kThreads) S1s[i] = s1[i];
+        if (L == 3)
+            for (int i = t; i < kMaxH2; i += kThreads) S2s[i] = i < M ? s2[i] : 0.f;
+    }
+    // wave 0's layer-2 biases (output 32 ob + acc_row(j, lane))
+    float bias[2][16];
+#pragma unroll
+    for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+            const int o = 32 * ob + acc_row(j, lane);
+            const float bv = b2[o < Mo ? o : 0];
+            bias[ob][j] = o < Mo ? bv : 0.f;
+        }
+    __syncthreads();
+
+    const bool relu2 = (L == 3 && !PR) || (L == 2 && final_relu);
+    using K = Sk<uint16_t>;
+    const SkPlan P = sk_plan(n_u, H, F, G, sk_bk<uint16_t>(), K::BM);
+    for (int c0 = blockIdx.x * 32; c0 < n_u; c0 += gridDim.x * 32) {
+        const int row = c0 + r32;
+        const bool live = row < n_u;
+        const int rowc = min(row, n_u - 1);
+        const int tile = c0 / K::BM;
+        const int wa = P.owner((int64_t)tile * P.S), wb = P.owner((int64_t)(tile + 1) * P.S - 1);
+        const bool split = wb > wa;
+        const int slot_a = (tile == (int)(P.it0(wa) / P.S)) ? 0 : 1;   // first contributor's piece
+        uint4 bh[4], bl[4];
+        if (split) {
+            const int id = uniq[rowc];
+            const bool id_ok = id >= 0 && (int64_t)id < n_rows;
+            const int rl = rowc % K::BM;
+            const bool has1 = wa + 1 <= wb, has2 = wa + 2 <= wb;
+            const float *pw0 = pbuf + ((size_t)wa * 2 + slot_a) * K::TILE + rl * kSkBN;
+            const float *pw1 = has1 ? pbuf + ((size_t)(wa + 1) * 2) * K::TILE + rl * kSkBN : pw0;
+            const float *pw2 = has2 ? pbuf + ((size_t)(wa + 2) * 2) * K::TILE + rl * kSkBN : pw0;
+            float4 pv[3][4][2];
+#pragma unroll
+            for (int s4 = 0; s4 < 4; ++s4) {
+                const int k0 = 64 * q + 16 * s4 + 8 * h;
+                pv[0][s4][0] = *(const float4 *)(pw0 + k0);
+                pv[0][s4][1] = *(const float4 *)(pw0 + k0 + 4);
+                pv[1][s4][0] = *(const float4 *)(pw1 + k0);
+                pv[1][s4][1] = *(const float4 *)(pw1 + k0 + 4);
+                pv[2][s4][0] = *(const float4 *)(pw2 + k0);
+                pv[2][s4][1] = *(const float4 *)(pw2 + k0 + 4);
+            }
+#pragma unroll
+            for (int s4 = 0; s4 < 4; ++s4) {
+                const int k0 = 64 * q + 16 * s4 + 8 * h;
+                float x[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+                for (int pi = 0; pi < 3; ++pi) {
+                    if (pi == 0 || (pi == 1 ? has1 : has2)) {
+                        const float4 v0 = pv[pi][s4][0], v1 = pv[pi][s4][1];
+                        x[0] += v0.x; x[1] += v0.y; x[2] += v0.z; x[3] += v0.w;
+                        x[4] += v1.x; x[5] += v1.y; x[6] += v1.z; x[7] += v1.w;
+                    }
+                }
+                for (int w = wa + 3; w <= wb; ++w) {     // (a tile spans at most 3 shares)
+                    const float *pc = pbuf + ((size_t)w * 2) * K::TILE + rl * kSkBN + k0;
+                    const float4 v0 = *(const float4 *)pc, v1 = *(const float4 *)(pc + 4);
+                    x[0] += v0.x; x[1] += v0.y; x[2] += v0.z; x[3] += v0.w;
+                    x[4] += v1.x; x[5] += v1.y; x[6] += v1.z; x[7] += v1.w;
+                }
+                const float4 c0v = *(const float4 *)&B1s[k0], c1v = *(const float4 *)&B1s[k0 + 4];
+                const float bb[8] = {c0v.x, c0v.y, c0v.z, c0v.w, c1v.x, c1v.y, c1v.z, c1v.w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    x[e] = id_ok ? x[e] + bb[e] : bb[e];
+                    if (!PR) x[e] = fmaxf(x[e], 0.f);
+                }
+                split8(x, bh[s4], bl[s4]);
+                if (live) *(uint4 *)(H1b + (size_t)row * H + k0) = bh[s4];
+            }
+        } else {
+            const size_t roff = (size_t)rowc * H + 64 * q + 8 * h;
+#pragma unroll
+            for (int s4 = 0; s4 < 4; ++s4) {
+                bh[s4] = *(const uint4 *)(H1b + roff + 16 * s4);
+                bl[s4] = *(const uint4 *)(H1lo + roff + 16 * s4);
+            }
+        }
+        if (PR) {   // the operand: PReLU(Z1) in fp32, split again
+#pragma unroll
+            for (int s4 = 0; s4 < 4; ++s4) {
+                const int k0 = 64 * q + 16 * s4 + 8 * h;
+                float x[8];
+                join8(bh[s4], bl[s4], x);
+                const float4 a0 = *(const float4 *)&S1s[k0], a1 = *(const float4 *)&S1s[k0 + 4];
+                const float a[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+#pragma unroll
+                for (int e = 0; e < 8; ++e) x[e] = x[e] > 0.f ? x[e] : a[e] * x[e];
+                split8(x, bh[s4], bl[s4]);
+            }
+        }
+        v16f acc[2] = {(v16f){}, (v16f){}};
+#pragma unroll
+        for (int s4 = 0; s4 < 4; ++s4)
+#pragma unroll
+            for (int ob = 0; ob < 2; ++ob) {
+                acc[ob] = mfma_bf16(aw[s4][ob], bh[s4], acc[ob]);
+                acc[ob] = mfma_bf16(aw[s4][ob], bl[s4], acc[ob]);
+            }
+#pragma unroll
+        for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+            for (int j = 0; j < 16; ++j) Zq[q][ob][j][lane] = acc[ob][j];
+        __syncthreads();
+        if (q == 0) {
+            v16f z[2];
+#pragma unroll
+            for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+                for (int j = 0; j < 16; ++j)
+                    z[ob][j] = ((Zq[0][ob][j][lane] + Zq[1][ob][j][lane]) + Zq[2][ob][j][lane]) + Zq[3][ob][j][lane];
+            tfb_finish<L, PR>(z, bias, relu2, W3s, S2s, b3, final_relu, M, D, row, live, H2_save, E, lane);
+        }
+        __syncthreads();                        // Zq is free for the next chunk
     }
 }
 
@@ -3528,14 +3725,31 @@ extern "C" ams_status ams_embed_fwd(const ams_mlp *mlp, const void *T, int64_t n
                                                        cap, n_mt, (const uint16_t *)W1, b1, H, H1f,
                                                        (uint16_t *)H1_save));
     }
+    if (sk && bf && pbuf) {
+        // after the stream-K layer: a block per 32-row chunk, a wave per K
+        // quarter (split tiles finished on the way), two blocks per CU
+        int tg = (cap + 31) / 32;
+        if (tg > 2 * G) tg = 2 * G;
+#define TFQ_LAUNCH(LL, PRV)                                                                                \
+    AMS_LAUNCH("tail_fwd_bf16", st, (tail_fwd_bf16_q<LL, PRV><<<tg, kThreads, 0, st>>>(                      \
+                                        h1b, h1lo, pbuf, F, G, b1, uniq, n_rows, M, D, (const uint16_t *)W2, \
+                                        b2, LL == 3 ? (const uint16_t *)W3 : nullptr, LL == 3 ? b3 : nullptr, \
+                                        mlp->final_relu, n_uniq, cap, H2_save, E, s1, s2)))
+        if (L == 3 && pr) TFQ_LAUNCH(3, true);
+        else if (L == 3) TFQ_LAUNCH(3, false);
+        else if (pr) TFQ_LAUNCH(2, true);
+        else TFQ_LAUNCH(2, false);
+#undef TFQ_LAUNCH
+        return ams_launch_status();
+    }
     if (sk && bf) {
-        // the small layers on bf16 MFMA (split tiles of layer 1 finished on the
-        // way); two resident blocks per CU stage W2 once and loop over chunks
+        // after the row-split layer (whole tiles): two resident blocks per CU
+        // stage W2 once and loop over chunks, a wave per chunk
         int tg = (cap + 4 * 32 - 1) / (4 * 32);
         if (tg > 2 * G) tg = 2 * G;
 #define TFB_LAUNCH(LL, PRV)                                                                                \
     AMS_LAUNCH("tail_fwd_bf16", st, (tail_fwd_bf16<LL, PRV><<<tg, kThreads, 0, st>>>(                        \
-                                        h1b, h1lo, pbuf, F, G, b1, uniq, n_rows, M, D, (const uint16_t *)W2, \
+                                        h1b, h1lo, M, D, (const uint16_t *)W2,                               \
                                         b2, LL == 3 ? (const uint16_t *)W3 : nullptr, LL == 3 ? b3 : nullptr, \
                                         mlp->final_relu, n_uniq, cap, H2_save, E, s1, s2)))
         if (L == 3 && pr) TFB_LAUNCH(3, true);
