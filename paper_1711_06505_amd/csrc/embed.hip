@@ -3215,24 +3215,31 @@ void tail_bwd_bf16(const uint16_t *__restrict__ H1b, const float *__restrict__ H
     if (blockIdx.x == 0)
         for (int i = t; i < zero_n; i += kThreads) zero_row[i] = 0.f;
     const int Mo = (L == 3) ? M : D;
-    // W2 transposed into LDS: 8 consecutive i of one row o per 16-byte load,
-    // every load of the block in flight together
-    static_assert(kMaxH2 * H / 8 % kThreads == 0, "W2 chunks per thread");
+    // W2 transposed into LDS: thread t takes the 8 x 8 tile of rows
+    // o0 = 8 (t / 32) .. + 7 and columns i0 = 8 (t % 32) .. + 7 (eight 16-byte
+    // loads, a row's 512 bytes read by 32 consecutive threads, all in flight
+    // together), transposes it in registers and writes 8 rows of W2^T, 16
+    // bytes each
+    static_assert(kMaxH2 * H == 64 * kThreads, "one 8 x 8 tile per thread");
     {
-        constexpr int NC = kMaxH2 * H / 8 / kThreads;
-        uint4 v[NC];
+        const int o0 = 8 * (t / (H / 8)), i0 = 8 * (t % (H / 8));
+        uint4 v[8];
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            const int q = t + c * kThreads, o = q / (H / 8), i0 = (q % (H / 8)) * 8;
-            v[c] = o < Mo ? *(const uint4 *)&W2[(size_t)o * H + i0] : make_uint4(0, 0, 0, 0);
-        }
+        for (int a = 0; a < 8; ++a)
+            v[a] = o0 + a < Mo ? *(const uint4 *)&W2[(size_t)(o0 + a) * H + i0] : make_uint4(0, 0, 0, 0);
 #pragma unroll
-        for (int c = 0; c < NC; ++c) {
-            const int q = t + c * kThreads, o = q / (H / 8), i0 = (q % (H / 8)) * 8;
-            const uint32_t w[4] = {v[c].x, v[c].y, v[c].z, v[c].w};
+        for (int j = 0; j < 8; ++j) {
+            uint32_t w[4];
 #pragma unroll
-            for (int j = 0; j < 8; ++j)
-                *(uint16_t *)(W2T + (i0 + j) * kW2S + o * 2) = (uint16_t)(w[j >> 1] >> (16 * (j & 1)));
+            for (int k = 0; k < 4; ++k) {
+                const uint4 r0 = v[2 * k], r1 = v[2 * k + 1];
+                const uint32_t a0 = (j >> 1) == 0 ? r0.x : (j >> 1) == 1 ? r0.y : (j >> 1) == 2 ? r0.z : r0.w;
+                const uint32_t a1 = (j >> 1) == 0 ? r1.x : (j >> 1) == 1 ? r1.y : (j >> 1) == 2 ? r1.z : r1.w;
+                const uint32_t lo = (j & 1) ? (a0 >> 16) : (a0 & 0xffffu);
+                const uint32_t hi = (j & 1) ? (a1 & 0xffff0000u) : (a1 << 16);
+                w[k] = lo | hi;
+            }
+            *(uint4 *)(W2T + (i0 + j) * kW2S + o0 * 2) = make_uint4(w[0], w[1], w[2], w[3]);
         }
     }
     const int po = t & 63, pg = t >> 6;        // phase-A role: output o, row group
