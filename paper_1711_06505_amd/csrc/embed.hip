@@ -2166,6 +2166,24 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
         const brsrc_t rH2 = make_buf(L == 3 ? H2s + (size_t)c0 * M : dE, L == 3 ? nr * M * 4 : 0);
         const brsrc_t rH1 = make_buf(H1s + (size_t)c0 * H, nr * H * (uint32_t)sizeof(TH));
         const brsrc_t rZ1 = make_buf(dZ1 + (size_t)c0 * H, nr * H * (uint32_t)sizeof(TH));
+        // phase 2's operands loaded with phase 1's (one memory round trip per
+        // chunk; one wave per SIMD leaves the registers for it)
+        float dA3[16];                          // dzl[row][d = r32] (dW3's operand, db3)
+#pragma unroll
+        for (int jj = 0; jj < 16; ++jj) dA3[jj] = tb_dzl(rdE, rE, final_relu, acc_row(jj, lane), r32, D);
+        float h2Av[2][16];                      // H2 (or dzl) [row][o = r32 + 32 ob]
+#pragma unroll
+        for (int ob = 0; ob < 2; ++ob)
+#pragma unroll
+            for (int jj = 0; jj < 16; ++jj) {
+                const int rr = acc_row(jj, lane), o = r32 + 32 * ob;
+                if (L == 3) {
+                    const float x = buf_ld<float>(rH2, (uint32_t)(rr * M + o));
+                    h2Av[ob][jj] = o < M ? x : 0.f;
+                } else {
+                    h2Av[ob][jj] = tb_dzl(rdE, rE, final_relu, rr, o, D);
+                }
+            }
         // ==== phase 1: dZ2 with lanes <-> rows, dH1, dZ1 (one o block at a time)
         float dzB[SD];                         // dzl[r32][2 s + h]
 #pragma unroll
@@ -2238,9 +2256,6 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
         __builtin_amdgcn_sched_barrier(0);
 
         // ==== phase 2: dZ2 with lanes <-> o; dW2, db2, dW3, db3 (one o block at a time)
-        float dA3[16];                          // dzl[row][d = r32] (dW3's operand, db3)
-#pragma unroll
-        for (int jj = 0; jj < 16; ++jj) dA3[jj] = tb_dzl(rdE, rE, final_relu, acc_row(jj, lane), r32, D);
         {
             float c3 = 0.f;
 #pragma unroll
@@ -2251,15 +2266,7 @@ __global__ __launch_bounds__(kTbThreads) void tail_bwd(const TH *__restrict__ H1
         for (int ob = 0; ob < 2; ++ob) {
             float h2A[16], dz2A[16];
 #pragma unroll
-            for (int jj = 0; jj < 16; ++jj) {
-                const int rr = acc_row(jj, lane), o = r32 + 32 * ob;
-                if (L == 3) {
-                    const float x = buf_ld<float>(rH2, (uint32_t)(rr * M + o));
-                    h2A[jj] = o < M ? x : 0.f;
-                } else {
-                    h2A[jj] = tb_dzl(rdE, rE, final_relu, rr, o, D);
-                }
-            }
+            for (int jj = 0; jj < 16; ++jj) h2A[jj] = h2Av[ob][jj];
             if constexpr (L == 3) {
                 v16f aA = (v16f){};
 #pragma unroll
