@@ -317,13 +317,18 @@ struct Sk : SkShape<128, 3, 128> {};
 template <typename TT>
 constexpr int sk_bk() { return Sk<TT>::RB / (int)sizeof(TT); }   // K per stage
 
-// Chunk swizzle of a 128-byte stage row, as in the ring of the one-tile-per-
-// block kernel (bits 0-3 of the row).
+// Chunk swizzle of a 128-byte stage row: chunk ^ (row / 2 % 8).  The LDS
+// serves a 16-byte read for 16 lanes per cycle over 64 banks; rows r and
+// r + 1 fall in different bank halves, so the even (odd) rows of 16
+// consecutive ones need 8 distinct chunk positions (the one-tile-per-block
+// ring's swizzle, bits 0-2 of the row, gives 4: counters showed 2-way
+// conflicts).  A lane's rows differ by multiples of 32, which leave it
+// unchanged.
 template <class K>
 __device__ __forceinline__ int sk_swz(int row)
 {
     static_assert(K::CPR == 8, "stage rows of 8 chunks");
-    return ring_swz(row);
+    return (row >> 1) & 7;
 }
 
 struct SkPlan {
