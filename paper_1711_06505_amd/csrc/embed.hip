@@ -906,7 +906,8 @@ __global__ __launch_bounds__(kThreads) void split3_k(const float *__restrict__ W
 
 // Stream-K layer 1 with the split: the tiles, shares and partial tiles of
 // l1sk<float> (128 x 256 tiles, 32 k per stage).  A stage slot holds the
-// 128 feature rows (float32, 128 bytes each, chunks swizzled by ring_swz)
+// 128 feature rows (float32, 128 bytes each, chunk c at c ^ (row / 2 % 8),
+// as in l1sk)
 // and the three bf16 planes of the tile's 256 W1 rows (64 bytes each,
 // chunk c at c ^ ((row >> 2) & 3)); 64 KB per slot, two slots.  Every wave
 // issues 2 DMA instructions of feature rows and 6 of planes per stage (the
@@ -932,7 +933,7 @@ __device__ __forceinline__ void x3_compute(const float *slot, v16f (&acc)[1][kSk
     const int h = lane >> 5, r32 = lane & 31, wm = wave >> 1, wn = wave & 1;
     // rows read are r32 plus multiples of 32: one swizzle per lane
     const float *pa = slot + (wm * 32 + r32) * 32;
-    const int swa = ring_swz(r32);
+    const int swa = (r32 >> 1) & 7;
     const float *pb = slot + X3::A_FL + (wn * (kSkBN / 2) + r32) * 16;
     const int swb = (r32 >> 2) & 3;
 #pragma unroll
@@ -1009,7 +1010,7 @@ __global__ __launch_bounds__(kSkThreads) void l1sk_x3(const float *__restrict__ 
             if (q < 2) {                        // feature rows 8 ja .. 8 ja + 7
                 const int ja = 2 * wave + q;
                 const int row = 8 * ja + (lane >> 3);
-                const int chunk = (lane & 7) ^ ring_swz(row);
+                const int chunk = (lane & 7) ^ ((row >> 1) & 7);
                 const int id = rid[row];
                 src[q] = (id >= 0 ? (const char *)(T + (size_t)id * F) : (const char *)W1) + chunk * 16;
             } else {                            // plane jb / 16, W1 rows 16 (jb % 16) .. + 15
@@ -3173,10 +3174,12 @@ __global__ __launch_bounds__(dwr::kThreads) __attribute__((amdgpu_waves_per_eu(2
 // The next chunk's H1, H2 and dE are loaded into registers while the current
 // one is computed.  Block partials have the layout of tail_bwd's
 // ([dW2][db2][dW3][db3][db1]) and go through the same fixed-order reduction.
-// Tiles are padded by 16 bytes per row so that the 16-byte and transposed
-// reads of a half-wave spread over the banks.
+// Tile rows are padded so that a half-wave's reads spread over the banks:
+// the dZ2 and W2^T tiles by 16 bytes (16-byte reads of 16 rows), the H1 tile
+// by 32 (a transposed read takes 32 bytes of 4 consecutive rows, which then
+// start 8 banks apart).
 constexpr int kTbfBlocks = 512;
-constexpr int kH1S = kMaxH1 * 2 + 16;       // bytes per H1 tile row
+constexpr int kH1S = kMaxH1 * 2 + 32;       // bytes per H1 tile row
 constexpr int kZ2S = kMaxH2 * 2 + 16;       // bytes per dZ2 tile row
 constexpr int kW2S = kMaxH2 * 2 + 16;       // bytes per W2^T tile row
 
@@ -3228,13 +3231,15 @@ void tail_bwd_bf16(const uint16_t *__restrict__ H1b, const float *__restrict__ H
         for (int i = t; i < zero_n; i += kThreads) zero_row[i] = 0.f;
     const int Mo = (L == 3) ? M : D;
     // W2 transposed into LDS: thread t takes the 8 x 8 tile of rows
-    // o0 = 8 (t / 32) .. + 7 and columns i0 = 8 (t % 32) .. + 7 (eight 16-byte
-    // loads, a row's 512 bytes read by 32 consecutive threads, all in flight
-    // together), transposes it in registers and writes 8 rows of W2^T, 16
-    // bytes each
-    static_assert(kMaxH2 * H == 64 * kThreads, "one 8 x 8 tile per thread");
+    // o0 = 8 (t % 8) .. + 7 and columns i0 = 8 (t / 8) .. + 7 (eight 16-byte
+    // loads, all in flight together), transposes it in registers and writes
+    // 8 rows of W2^T, 16 bytes each: the 8 threads of a column block fill
+    // 128 contiguous bytes of a W2^T row, the next 8 the row 8 further on
+    // (kW2S apart: the other bank half), so 16 lanes' writes meet no bank
+    // twice
+    static_assert(kMaxH2 * H == 64 * kThreads && kMaxH2 == 64, "one 8 x 8 tile per thread");
     {
-        const int o0 = 8 * (t / (H / 8)), i0 = 8 * (t % (H / 8));
+        const int o0 = 8 * (t % 8), i0 = 8 * (t / 8);
         uint4 v[8];
 #pragma unroll
         for (int a = 0; a < 8; ++a)
