@@ -30,6 +30,16 @@ def mid(dtype="f32", B=96, n_images=20_000, index=11):
                                pools=("sum", "max", "att"), stream=-1)
 
 
+def mid_l2():
+    """The mid bf16 batch through a two-layer MLP 4096-256-12 (the
+    two-layer instances of the bf16 tails)."""
+    return dataclasses.replace(mid("bf16"), name="mid_bf16_l2", dims=(4096, 256, 12))
+
+
+def named(wname):
+    return synth.get("tiny") if wname == "tiny" else mid_l2() if wname == "mid_bf16_l2" else mid(wname[4:])
+
+
 def cuda_i32(x):
     return torch.from_numpy(np.ascontiguousarray(x, dtype=np.int32)).cuda()
 
@@ -141,9 +151,9 @@ def gpu_embed_fwd(w, T_dev, uniq, Ws, bs, cap=None):
     return {"E": f64(E[:n_u]), "H1": f64(H1[:n_u]), "H2": f64(H2[:n_u]) if H2 is not None else None}
 
 
-@pytest.mark.parametrize("wname", ["tiny", "mid_f32", "mid_bf16"])
+@pytest.mark.parametrize("wname", ["tiny", "mid_f32", "mid_bf16", "mid_bf16_l2"])
 def test_embed_fwd_matches_oracle(wname):
-    w = synth.get("tiny") if wname == "tiny" else mid(wname[4:])
+    w = named(wname)
     batch, dd, Ws, bs, T_u = embed_case(w)
     print(f"embed fwd {wname}: n_u={dd['n_uniq']}", flush=True)
     T_dev = synth.table_rows(w, np.arange(w.n_images), device="cuda")
@@ -331,9 +341,9 @@ def run_embed_bwd(w, uniq_np, T_rows, Ws, bs, cap):
         assert_close(db[l], bo["db"][l], rt, f"db{l + 1}")
 
 
-@pytest.mark.parametrize("wname", ["tiny", "mid_f32", "mid_bf16"])
+@pytest.mark.parametrize("wname", ["tiny", "mid_f32", "mid_bf16", "mid_bf16_l2"])
 def test_embed_bwd_matches_oracle(wname):
-    w = synth.get("tiny") if wname == "tiny" else mid(wname[4:])
+    w = named(wname)
     batch, dd, Ws, bs, T_u = embed_case(w)
     print(f"embed bwd {wname}: n_u={dd['n_uniq']}", flush=True)
     run_embed_bwd(w, dd["uniq"], T_u, Ws, bs, dd["n_uniq"] + 40)
