@@ -1231,7 +1231,9 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 {
     constexpr int KB = kMaxH1 / 2 / 32;       // 32-k blocks in a K half (at most 4)
     constexpr int KH = KB / 2;                // ... added up by each wave of a K half's pair
-    __shared__ float Zp[2][kTailRows][kMaxH2 + 1];
+    // (rows 72 floats apart: the two lane halves' rows, 4 apart, then fall
+    // in opposite bank halves when a wave stores its accumulator)
+    __shared__ float Zp[2][kTailRows][kMaxH2 + 8];
     __shared__ float W3s[kMaxD * (kMaxH2 + 1)];
     __shared__ float h2s[kTailRows][kMaxH2 + 1];
     __shared__ __attribute__((aligned(16))) float H1s[kTailRows][kMaxH1 + 4];   // finished rows of a cut tile
@@ -1507,8 +1509,8 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 // H2 goes into the MFMA straight from the registers; W3 rows sit in LDS padded
 // to 68 bf16 (conflict-free 8-byte reads).  E = Z3 + b3 (ReLU if final).
 // W2 sits in LDS [64 o][256 k] bf16, rows past the layer width zero, 16-byte
-// chunks stored at chunk ^ (o & 7) so a half-wave's 32 rows spread over all
-// banks.
+// chunks stored at chunk ^ (o & 15): the rows are 512 bytes (all starting at
+// bank 0), so 16 lanes' rows need 16 distinct chunk positions.
 constexpr int kW3S = kMaxH2 + 4;               // bf16 per W3 row in LDS
 
 __device__ __forceinline__ uint32_t pack_bf16(float a, float b)
@@ -1585,7 +1587,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll
         for (int i = 0; i < kMaxH2 * cpr / kThreads; ++i) {
             const int idx = t + i * kThreads, o = idx / cpr, c = idx % cpr;
-            *(uint4 *)&W2s[o * H + ((c ^ (o & 7)) << 3)] = v[i];
+            *(uint4 *)&W2s[o * H + ((c ^ (o & 15)) << 3)] = v[i];
         }
     }
     if (L == 3) {
@@ -1670,7 +1672,7 @@ __global__ __launch_bounds__(kThreads) __attribute__((amdgpu_waves_per_eu(2))) v
 #pragma unroll
                 for (int ob = 0; ob < 2; ++ob) {
                     const int o = 32 * ob + r32;
-                    const uint4 av = *(const uint4 *)&W2s[o * H + (((2 * ss + h) ^ (o & 7)) << 3)];
+                    const uint4 av = *(const uint4 *)&W2s[o * H + (((2 * ss + h) ^ (o & 15)) << 3)];
                     acc[ob] = mfma_bf16(av, ch[s4], acc[ob]);
                     acc[ob] = mfma_bf16(av, cl[s4], acc[ob]);
                 }
