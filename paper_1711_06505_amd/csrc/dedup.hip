@@ -76,8 +76,11 @@ __device__ uint32_t lookback(uint32_t *words, int stride, int t, uint32_t count,
         return 0;
     }
     st_relaxed(&words[(size_t)t * stride], kAgg | count);
-    // walk back in batches of independent reads (one round trip each)
-    constexpr int kBatch = 32;
+    // walk back in batches of independent reads (one round trip each); the
+    // nearest inclusive prefix is usually a few tiles back, so a batch of 16
+    // (measured against 8, 32, 64 and 128: 20.3 against 21.5, 22.6, 32.7 and
+    // 42.9 us per pass on 750k keys) keeps the reads that are not needed few
+    constexpr int kBatch = 16;
     uint32_t excl = 0;
     int spins = 0;
     for (int hi = t - 1; hi >= 0;) {
